@@ -1,0 +1,22 @@
+"""SpecQuant hot path on MI355X (gfx950): a C-ABI HIP library and its binding.
+
+SpecQuant (arXiv 2609.21704) drafts tokens with quantized copies (INT4, FP8)
+of one FP16 parent, verifies the drafted block with the parent and accepts or
+corrects the drafted tokens.  The data-parallel steps of a round run in the
+HIP kernels of ``libspecquant.so``; this package only marshals arguments.
+"""
+from ._lib import (  # noqa: F401
+    EXPORTED,
+    LIB_PATH,
+    SQ_F16,
+    SQ_F32,
+    SpecQuantError,
+    load,
+    sq_abi_version,
+    sq_qgemv_w4a16,
+    sq_qgemv_w8a16,
+    sq_quantize_fp8_e4m3,
+    sq_quantize_int4_g128,
+    sq_spec_accept,
+    sq_verify_gemm_f16,
+)

@@ -1,0 +1,232 @@
+"""ctypes binding of libspecquant.so: argument marshalling only.
+
+Each function has the name of the C entry point it calls (see
+include/specquant.h).  Tensors supply device memory and the current torch
+stream supplies the HIP stream; every computation runs in the library's HIP
+kernels.  There is no fallback: if the library is not built, or a tensor is not
+on the GPU, the call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libspecquant.so")
+
+SQ_F16, SQ_F32 = 0, 1
+_STATUS = {0: "SQ_OK", 1: "SQ_ERR_NULL", 2: "SQ_ERR_SHAPE", 3: "SQ_ERR_ALIGN", 4: "SQ_ERR_ALIAS",
+           5: "SQ_ERR_VALUE", 6: "SQ_ERR_DEVICE"}
+
+_lib = None
+_lock = threading.Lock()
+
+
+class SpecQuantError(RuntimeError):
+    def __init__(self, status: int, fn: str):
+        self.status = status
+        super().__init__(f"{fn} failed: {_STATUS.get(status, status)}")
+
+
+def load() -> ctypes.CDLL:
+    """Load the built library (raises if it has not been built)."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "(the SpecQuant path has no non-HIP fallback)")
+        lib = ctypes.CDLL(LIB_PATH)
+        P, I64, I32, F = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float
+        S = ctypes.c_int
+        sigs = {
+            "sq_abi_version": ([], I32),
+            "sq_status_str": ([S], ctypes.c_char_p),
+            "sq_quantize_int4_g128": ([P, I64, I64, P, P, P, P, P], S),
+            "sq_quantize_fp8_e4m3": ([P, I64, I64, P, P, P, P], S),
+            "sq_qgemv_w4a16": ([P, I64, I64, P, P, P, I64, P, S, P], S),
+            "sq_qgemv_w8a16": ([P, I64, I64, P, P, I64, P, S, P], S),
+            "sq_verify_gemm_f16": ([P, I64, I64, P, I64, P, S, P], S),
+            "sq_spec_accept": ([P, P, P, P, I32, I32, I32, F, P, P, P, P, P], S),
+        }
+        for name, (args, res) in sigs.items():
+            fn = getattr(lib, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = lib
+        return lib
+
+
+EXPORTED = ("sq_abi_version", "sq_status_str", "sq_quantize_int4_g128", "sq_quantize_fp8_e4m3",
+            "sq_qgemv_w4a16", "sq_qgemv_w8a16", "sq_verify_gemm_f16", "sq_spec_accept")
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(dev: torch.device):
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+def _dev(*ts):
+    dev = None
+    for t in ts:
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError("SpecQuant calls take GPU tensors only")
+        if not t.is_contiguous():
+            raise ValueError("SpecQuant calls take contiguous tensors only")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError("all tensors of a call must be on one device")
+    return dev
+
+
+def _check(status: int, fn: str):
+    if status != 0:
+        raise SpecQuantError(status, fn)
+
+
+def _dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.float16:
+        return SQ_F16
+    if dt == torch.float32:
+        return SQ_F32
+    raise ValueError("output dtype must be torch.float16 or torch.float32")
+
+
+def _expect(t, dtype, shape, name):
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def sq_abi_version() -> int:
+    return int(load().sq_abi_version())
+
+
+def sq_quantize_int4_g128(w16: torch.Tensor, codes=None, scales=None, zeros=None, nonfinite_flag=None):
+    """FP16 parent [n][k] -> (codes u8 [n][k/2], scales f16 [n][k/128], zeros f16 [n][k/128])."""
+    n, k = w16.shape
+    if w16.dtype != torch.float16:
+        raise TypeError("w16 must be float16")
+    dev = w16.device
+    codes = torch.empty((n, k // 2), dtype=torch.uint8, device=dev) if codes is None else codes
+    scales = torch.empty((n, k // 128), dtype=torch.float16, device=dev) if scales is None else scales
+    zeros = torch.empty((n, k // 128), dtype=torch.float16, device=dev) if zeros is None else zeros
+    _dev(w16, codes, scales, zeros, nonfinite_flag)
+    _expect(codes, torch.uint8, (n, k // 2), "codes")
+    _expect(scales, torch.float16, (n, k // 128), "scales")
+    _expect(zeros, torch.float16, (n, k // 128), "zeros")
+    _check(load().sq_quantize_int4_g128(_ptr(w16), n, k, _ptr(codes), _ptr(scales), _ptr(zeros),
+                                        _ptr(nonfinite_flag), _stream(dev)), "sq_quantize_int4_g128")
+    return codes, scales, zeros
+
+
+def sq_quantize_fp8_e4m3(w16: torch.Tensor, codes=None, scales=None, nonfinite_flag=None):
+    """FP16 parent [n][k] -> (codes u8 [n][k] OCP E4M3, scales f32 [n])."""
+    n, k = w16.shape
+    if w16.dtype != torch.float16:
+        raise TypeError("w16 must be float16")
+    dev = w16.device
+    codes = torch.empty((n, k), dtype=torch.uint8, device=dev) if codes is None else codes
+    scales = torch.empty((n,), dtype=torch.float32, device=dev) if scales is None else scales
+    _dev(w16, codes, scales, nonfinite_flag)
+    _expect(codes, torch.uint8, (n, k), "codes")
+    _expect(scales, torch.float32, (n,), "scales")
+    _check(load().sq_quantize_fp8_e4m3(_ptr(w16), n, k, _ptr(codes), _ptr(scales), _ptr(nonfinite_flag),
+                                       _stream(dev)), "sq_quantize_fp8_e4m3")
+    return codes, scales
+
+
+def sq_qgemv_w4a16(x, codes, scales, zeros, y=None, y_dtype=torch.float32):
+    """y[m][n] = x . W4'^T with W4' the INT4 g128 dequantized weights."""
+    m, k = x.shape
+    n = codes.shape[0]
+    if x.dtype != torch.float16:
+        raise TypeError("x must be float16")
+    y = torch.empty((m, n), dtype=y_dtype, device=x.device) if y is None else y
+    _dev(x, codes, scales, zeros, y)
+    _expect(codes, torch.uint8, (n, k // 2), "codes")
+    _expect(scales, torch.float16, (n, k // 128), "scales")
+    _expect(zeros, torch.float16, (n, k // 128), "zeros")
+    if y.numel() != m * n:
+        raise ValueError("y must hold m * n elements")
+    _check(load().sq_qgemv_w4a16(_ptr(x), m, k, _ptr(codes), _ptr(scales), _ptr(zeros), n, _ptr(y),
+                                 _dtype_code(y.dtype), _stream(x.device)), "sq_qgemv_w4a16")
+    return y
+
+
+def sq_qgemv_w8a16(x, codes, scales, y=None, y_dtype=torch.float32):
+    """y[m][n] = x . W8'^T with W8' the FP8 E4M3 dequantized weights."""
+    m, k = x.shape
+    n = codes.shape[0]
+    if x.dtype != torch.float16:
+        raise TypeError("x must be float16")
+    y = torch.empty((m, n), dtype=y_dtype, device=x.device) if y is None else y
+    _dev(x, codes, scales, y)
+    _expect(codes, torch.uint8, (n, k), "codes")
+    _expect(scales, torch.float32, (n,), "scales")
+    if y.numel() != m * n:
+        raise ValueError("y must hold m * n elements")
+    _check(load().sq_qgemv_w8a16(_ptr(x), m, k, _ptr(codes), _ptr(scales), n, _ptr(y), _dtype_code(y.dtype),
+                                 _stream(x.device)), "sq_qgemv_w8a16")
+    return y
+
+
+def sq_verify_gemm_f16(x, w16, y=None, y_dtype=torch.float32):
+    """y[m][n] = x . W16^T (parent verification pass)."""
+    m, k = x.shape
+    n = w16.shape[0]
+    if x.dtype != torch.float16 or w16.dtype != torch.float16:
+        raise TypeError("x and w16 must be float16")
+    y = torch.empty((m, n), dtype=y_dtype, device=x.device) if y is None else y
+    _dev(x, w16, y)
+    _expect(w16, torch.float16, (n, k), "w16")
+    if y.numel() != m * n:
+        raise ValueError("y must hold m * n elements")
+    _check(load().sq_verify_gemm_f16(_ptr(x), m, k, _ptr(w16), n, _ptr(y), _dtype_code(y.dtype),
+                                     _stream(x.device)), "sq_verify_gemm_f16")
+    return y
+
+
+def sq_spec_accept(draft_logits, target_logits, draft_tokens, u24, temperature: float = 1.0,
+                   n_accepted=None, next_token=None, q_out=None, p_out=None):
+    """Speculative accept / resample.
+
+    draft_logits [kd][b][v] f32 (None when kd == 0), target_logits [b][kd+1][v] f32,
+    draft_tokens [b][kd] int32, u24 [b][kd+1] int32 holding uint32 bit patterns
+    (low 24 bits used).  Returns (n_accepted [b] int32, next_token [b] int32).
+    """
+    b, kd1, v = target_logits.shape
+    kd = kd1 - 1
+    dev = target_logits.device
+    n_accepted = torch.empty((b,), dtype=torch.int32, device=dev) if n_accepted is None else n_accepted
+    next_token = torch.empty((b,), dtype=torch.int32, device=dev) if next_token is None else next_token
+    _dev(draft_logits, target_logits, draft_tokens, u24, n_accepted, next_token, q_out, p_out)
+    if target_logits.dtype != torch.float32 or (draft_logits is not None and draft_logits.dtype != torch.float32):
+        raise TypeError("logits must be float32")
+    if draft_logits is not None and draft_logits.numel() != kd * b * v:
+        raise ValueError("draft_logits must be [kd][b][v]")
+    if draft_tokens is not None and (draft_tokens.dtype != torch.int32 or draft_tokens.numel() != b * kd):
+        raise ValueError("draft_tokens must be int32 [b][kd]")
+    if u24 is not None and (u24.dtype != torch.int32 or u24.numel() != b * (kd + 1)):
+        raise ValueError("u24 must be int32 [b][kd+1]")
+    _expect(n_accepted, torch.int32, (b,), "n_accepted")
+    _expect(next_token, torch.int32, (b,), "next_token")
+    if q_out is not None:
+        _expect(q_out, torch.float32, (kd, b, v), "q_out")
+    if p_out is not None:
+        _expect(p_out, torch.float32, (b, kd + 1, v), "p_out")
+    _check(load().sq_spec_accept(_ptr(draft_logits), _ptr(target_logits), _ptr(draft_tokens), _ptr(u24), b, kd, v,
+                                 float(temperature), _ptr(n_accepted), _ptr(next_token), _ptr(q_out), _ptr(p_out),
+                                 _stream(dev)), "sq_spec_accept")
+    return n_accepted, next_token

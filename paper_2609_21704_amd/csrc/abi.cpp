@@ -1,0 +1,210 @@
+// C ABI of the SpecQuant hot path: host-side argument validation, the
+// library-owned device workspace, and dispatch to the HIP kernels.
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <mutex>
+
+#include "sq_internal.hpp"
+#include "specquant.h"
+
+namespace sq {
+namespace {
+
+constexpr int kMaxDevices = 64;
+
+struct Workspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+
+std::mutex g_ws_mutex;
+Workspace g_ws[kMaxDevices];
+
+}  // namespace
+
+void* workspace(size_t bytes) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_ws_mutex);
+  Workspace& ws = g_ws[dev];
+  if (ws.bytes >= bytes && ws.ptr) return ws.ptr;
+  size_t want = bytes > 2 * ws.bytes ? bytes : 2 * ws.bytes;
+  const size_t grain = size_t(2) << 20;
+  want = (want + grain - 1) / grain * grain;
+  if (ws.ptr) {
+    // kernels enqueued earlier may still read the old buffer
+    if (hipDeviceSynchronize() != hipSuccess) return nullptr;
+    (void)hipFree(ws.ptr);
+    ws.ptr = nullptr;
+    ws.bytes = 0;
+  }
+  void* p = nullptr;
+  if (hipMalloc(&p, want) != hipSuccess) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  ws.ptr = p;
+  ws.bytes = want;
+  return p;
+}
+
+}  // namespace sq
+
+namespace {
+
+inline bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Byte ranges [a, a + na) and [b, b + nb) intersect.
+inline bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  const uintptr_t pa = reinterpret_cast<uintptr_t>(a), pb = reinterpret_cast<uintptr_t>(b);
+  return pa < pb + nb && pb < pa + na;
+}
+
+struct Range {
+  const void* p;
+  size_t n;
+};
+
+// Every output range against every input range and every other output range.
+template <size_t NO, size_t NI>
+bool any_alias(const Range (&outs)[NO], const Range (&ins)[NI]) {
+  for (size_t i = 0; i < NO; ++i) {
+    for (size_t j = 0; j < NI; ++j)
+      if (overlap(outs[i].p, outs[i].n, ins[j].p, ins[j].n)) return true;
+    for (size_t j = i + 1; j < NO; ++j)
+      if (overlap(outs[i].p, outs[i].n, outs[j].p, outs[j].n)) return true;
+  }
+  return false;
+}
+
+inline sq_status device_status(hipError_t e) { return e == hipSuccess ? SQ_OK : SQ_ERR_DEVICE; }
+
+constexpr int64_t kMaxK = int64_t(1) << 20;
+constexpr int64_t kMaxN = 0x7FFFFFFF;
+
+}  // namespace
+
+extern "C" {
+
+int32_t sq_abi_version(void) { return SQ_ABI_VERSION; }
+
+const char* sq_status_str(sq_status s) {
+  switch (s) {
+    case SQ_OK: return "SQ_OK";
+    case SQ_ERR_NULL: return "SQ_ERR_NULL: a required pointer is NULL";
+    case SQ_ERR_SHAPE: return "SQ_ERR_SHAPE: a size is outside the supported range";
+    case SQ_ERR_ALIGN: return "SQ_ERR_ALIGN: a pointer is misaligned";
+    case SQ_ERR_ALIAS: return "SQ_ERR_ALIAS: an output overlaps an input or another output";
+    case SQ_ERR_VALUE: return "SQ_ERR_VALUE: a scalar argument is invalid";
+    case SQ_ERR_DEVICE: return "SQ_ERR_DEVICE: the HIP runtime reported an error";
+  }
+  return "unknown sq_status";
+}
+
+sq_status sq_quantize_int4_g128(const uint16_t* w16, int64_t n, int64_t k, uint8_t* codes, uint16_t* scales,
+                                uint16_t* zeros, int32_t* nonfinite_flag, hipStream_t stream) {
+  if (!w16 || !codes || !scales || !zeros) return SQ_ERR_NULL;
+  if (n < 1 || n > kMaxN || k < 128 || k > kMaxK || k % 128 != 0) return SQ_ERR_SHAPE;
+  if (!aligned(w16, 16) || !aligned(codes, 16) || !aligned(scales, 2) || !aligned(zeros, 2) ||
+      !aligned(nonfinite_flag, 4))
+    return SQ_ERR_ALIGN;
+  const size_t nk = (size_t)n * (size_t)k, ng = nk / 128;
+  const Range outs[] = {{codes, nk / 2}, {scales, ng * 2}, {zeros, ng * 2}, {nonfinite_flag, 4}};
+  const Range ins[] = {{w16, nk * 2}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_quantize_int4(w16, n, k, codes, scales, zeros, nonfinite_flag, stream));
+}
+
+sq_status sq_quantize_fp8_e4m3(const uint16_t* w16, int64_t n, int64_t k, uint8_t* codes, float* scales,
+                               int32_t* nonfinite_flag, hipStream_t stream) {
+  if (!w16 || !codes || !scales) return SQ_ERR_NULL;
+  if (n < 1 || n > kMaxN || k < 16 || k > kMaxK || k % 16 != 0) return SQ_ERR_SHAPE;
+  if (!aligned(w16, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(nonfinite_flag, 4))
+    return SQ_ERR_ALIGN;
+  const size_t nk = (size_t)n * (size_t)k;
+  const Range outs[] = {{codes, nk}, {scales, (size_t)n * 4}, {nonfinite_flag, 4}};
+  const Range ins[] = {{w16, nk * 2}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_quantize_fp8(w16, n, k, codes, scales, nonfinite_flag, stream));
+}
+
+sq_status sq_qgemv_w4a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t* codes, const uint16_t* scales,
+                         const uint16_t* zeros, int64_t n, void* y, sq_dtype y_dtype, hipStream_t stream) {
+  if (!x || !codes || !scales || !zeros || !y) return SQ_ERR_NULL;
+  if (m < 1 || m > 8 || n < 1 || n > kMaxN || k < 128 || k > kMaxK || k % 128 != 0) return SQ_ERR_SHAPE;
+  if (y_dtype != SQ_F16 && y_dtype != SQ_F32) return SQ_ERR_VALUE;
+  const size_t ysz = y_dtype == SQ_F16 ? 2 : 4;
+  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 2) || !aligned(zeros, 2) || !aligned(y, ysz))
+    return SQ_ERR_ALIGN;
+  const size_t nk = (size_t)n * (size_t)k;
+  const Range outs[] = {{y, (size_t)m * n * ysz}};
+  const Range ins[] = {{x, (size_t)m * k * 2}, {codes, nk / 2}, {scales, nk / 64}, {zeros, nk / 64}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_gemv_w4(x, (int)m, k, codes, scales, zeros, n, y, y_dtype == SQ_F16, stream));
+}
+
+sq_status sq_qgemv_w8a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t* codes, const float* scales,
+                         int64_t n, void* y, sq_dtype y_dtype, hipStream_t stream) {
+  if (!x || !codes || !scales || !y) return SQ_ERR_NULL;
+  if (m < 1 || m > 8 || n < 1 || n > kMaxN || k < 16 || k > kMaxK || k % 16 != 0) return SQ_ERR_SHAPE;
+  if (y_dtype != SQ_F16 && y_dtype != SQ_F32) return SQ_ERR_VALUE;
+  const size_t ysz = y_dtype == SQ_F16 ? 2 : 4;
+  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(y, ysz)) return SQ_ERR_ALIGN;
+  const size_t nk = (size_t)n * (size_t)k;
+  const Range outs[] = {{y, (size_t)m * n * ysz}};
+  const Range ins[] = {{x, (size_t)m * k * 2}, {codes, nk}, {scales, (size_t)n * 4}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_gemv_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream));
+}
+
+sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint16_t* w16, int64_t n, void* y,
+                             sq_dtype y_dtype, hipStream_t stream) {
+  if (!x || !w16 || !y) return SQ_ERR_NULL;
+  if (m < 1 || m > 64 || n < 1 || n > kMaxN || k < 8 || k > kMaxK || k % 8 != 0) return SQ_ERR_SHAPE;
+  if (y_dtype != SQ_F16 && y_dtype != SQ_F32) return SQ_ERR_VALUE;
+  const size_t ysz = y_dtype == SQ_F16 ? 2 : 4;
+  if (!aligned(x, 16) || !aligned(w16, 16) || !aligned(y, ysz)) return SQ_ERR_ALIGN;
+  const Range outs[] = {{y, (size_t)m * n * ysz}};
+  const Range ins[] = {{x, (size_t)m * k * 2}, {w16, (size_t)n * k * 2}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_gemm_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream));
+}
+
+sq_status sq_spec_accept(const float* draft_logits, const float* target_logits, const int32_t* draft_tokens,
+                         const uint32_t* u24, int32_t b, int32_t kd, int32_t v, float temperature,
+                         int32_t* n_accepted, int32_t* next_token, float* q_out, float* p_out, hipStream_t stream) {
+  if (!target_logits || !n_accepted || !next_token) return SQ_ERR_NULL;
+  if (kd > 0 && (!draft_logits || !draft_tokens)) return SQ_ERR_NULL;
+  if (b < 1 || b > (1 << 24) || kd < 0 || kd > 64 || v < 1 || v > (1 << 26)) return SQ_ERR_SHAPE;
+  const int64_t nchunk = (v + 4095) / 4096;
+  if ((int64_t)b * (2 * kd + 1) * nchunk > (int64_t(1) << 24)) return SQ_ERR_SHAPE;
+  if (!isfinite(temperature) || temperature < 0.0f) return SQ_ERR_VALUE;
+  if (temperature == 0.0f && (q_out || p_out)) return SQ_ERR_VALUE;
+  if (temperature > 0.0f && !u24) return SQ_ERR_NULL;
+  if (!aligned(draft_logits, 4) || !aligned(target_logits, 4) || !aligned(draft_tokens, 4) || !aligned(u24, 4) ||
+      !aligned(n_accepted, 4) || !aligned(next_token, 4) || !aligned(q_out, 4) || !aligned(p_out, 4))
+    return SQ_ERR_ALIGN;
+  const size_t bk = (size_t)b * kd, bv = (size_t)b * v;
+  const Range outs[] = {{n_accepted, (size_t)b * 4},
+                        {next_token, (size_t)b * 4},
+                        {q_out, (size_t)kd * bv * 4},
+                        {p_out, (size_t)(kd + 1) * bv * 4}};
+  const Range ins[] = {{draft_logits, (size_t)kd * bv * 4},
+                       {target_logits, (size_t)(kd + 1) * bv * 4},
+                       {draft_tokens, bk * 4},
+                       {u24, (size_t)b * (kd + 1) * 4}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_spec_accept(draft_logits, target_logits, draft_tokens, u24, b, kd, v, temperature,
+                                              n_accepted, next_token, q_out, p_out, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,448 @@
+// LM-head softmax and speculative acceptance or correction (SpecQuant
+// SS III-D.4 and the guess-set rule of SS III-A), stochastic (T > 0) and
+// greedy (T = 0).
+//
+// Every vocabulary row is cut into chunks of kChunk logits so that a round's
+// b * (2kd + 1) rows spread over the whole chip:
+//   1. stats:    per (row, chunk) the max of z = l / T and sum exp(z - max),
+//                fp64 (online-softmax partials, merged later in chunk order);
+//   2. decide:   per (sequence, chunk) merge the row partials, take the kd
+//                accept decisions u * q(x) < p(x) in fp64 (one thread each),
+//                find the first rejection n, and sum the chunk's share of the
+//                draw weights R = rint(r * 2^60) in int64 (exact, so the total
+//                does not depend on the summation order);
+//   3. draw:     per sequence, locate the chunk holding t = floor(u Z / 2^24)
+//                from the chunk totals, then scan that chunk.
+// Greedy uses per-chunk (max, first index) pairs and one decision pass.
+#include <math.h>
+
+#include "sq_device.hpp"
+#include "sq_internal.hpp"
+
+#pragma clang fp contract(off)
+
+namespace sq {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kChunk = 4096;
+constexpr int kPer = kChunk / kThreads;  // logits per thread and chunk
+
+struct SeqInfo {
+  int n;
+  int pad;
+  double lp, sp, lq, sq;  // merged (max, sum) of the draw rows p_n and q_n
+};
+
+struct ArgMax {
+  float v;
+  int i;
+};
+
+__device__ __forceinline__ double zval(float l, float t) { return t == 1.0f ? (double)l : (double)l / (double)t; }
+
+__device__ __forceinline__ int64_t grid_weight(double r) { return llrint(ldexp(r, 60)); }
+
+// Deterministic block reductions over 256 threads (4 wavefronts).
+__device__ double block_max(double v, double* sh) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+  __syncthreads();
+  v = fmax(fmax(sh[0], sh[1]), fmax(sh[2], sh[3]));
+  __syncthreads();
+  return v;
+}
+
+__device__ double block_sum(double v, double* sh) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+  __syncthreads();
+  v = (sh[0] + sh[1]) + (sh[2] + sh[3]);
+  __syncthreads();
+  return v;
+}
+
+__device__ int64_t block_sum_i64(int64_t v, int64_t* sh) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+  __syncthreads();
+  v = (sh[0] + sh[1]) + (sh[2] + sh[3]);
+  __syncthreads();
+  return v;
+}
+
+// Row r of the combined row space: target rows first ([b][kd+1] order), then
+// draft rows ([kd][b] order); both arrays are contiguous in that order.
+__device__ __forceinline__ const float* row_ptr(const float* draft, const float* target, int64_t rows_t, int64_t r,
+                                                int v) {
+  return r < rows_t ? target + r * v : draft + (r - rows_t) * v;
+}
+
+__device__ __forceinline__ void merge_stats(const double2* st, int nchunk, double& L, double& S) {
+  double mx = -INFINITY;
+  for (int c = 0; c < nchunk; ++c) mx = fmax(mx, st[c].x);
+  double s = 0.0;
+  for (int c = 0; c < nchunk; ++c) s += st[c].y * exp(st[c].x - mx);
+  L = mx;
+  S = s;
+}
+
+// 1. per (row, chunk): (max z, sum exp(z - max z)).  blockIdx.x = row * nchunk + chunk.
+__global__ __launch_bounds__(kThreads) void stats_kernel(const float* __restrict__ draft,
+                                                         const float* __restrict__ target, int64_t rows_t, int v,
+                                                         float temp, int nchunk, double2* __restrict__ stats) {
+  __shared__ double sh[4];
+  const int64_t row = blockIdx.x / nchunk;
+  const int c = blockIdx.x % nchunk;
+  const float* l = row_ptr(draft, target, rows_t, row, v);
+  const int beg = c * kChunk;
+  double z[kPer];
+  double mx = -INFINITY;
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) {
+    const int j = beg + e * kThreads + threadIdx.x;
+    z[e] = j < v ? zval(l[j], temp) : -INFINITY;
+    mx = fmax(mx, z[e]);
+  }
+  mx = block_max(mx, sh);
+  double s = 0.0;
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) {
+    const int j = beg + e * kThreads + threadIdx.x;
+    if (j < v) s += exp(z[e] - mx);
+  }
+  s = block_sum(s, sh);
+  if (threadIdx.x == 0) stats[row * nchunk + c] = make_double2(mx, s);
+}
+
+// Optional copies of the distributions: p or q = exp(z - L) / S as fp32.
+__global__ __launch_bounds__(kThreads) void probs_kernel(const float* __restrict__ draft,
+                                                         const float* __restrict__ target, int64_t rows_t, int v,
+                                                         float temp, int nchunk, const double2* __restrict__ stats,
+                                                         float* __restrict__ q_out, float* __restrict__ p_out) {
+  __shared__ double sL, sS;
+  const int64_t row = blockIdx.x / nchunk;
+  const int c = blockIdx.x % nchunk;
+  float* out = row < rows_t ? (p_out ? p_out + row * v : nullptr) : (q_out ? q_out + (row - rows_t) * v : nullptr);
+  if (!out) return;  // uniform across the block
+  if (threadIdx.x == 0) merge_stats(stats + row * nchunk, nchunk, sL, sS);
+  __syncthreads();
+  const double L = sL, S = sS;
+  const float* l = row_ptr(draft, target, rows_t, row, v);
+  for (int e = 0; e < kPer; ++e) {
+    const int j = c * kChunk + e * kThreads + threadIdx.x;
+    if (j < v) out[j] = (float)(exp(zval(l[j], temp) - L) / S);
+  }
+}
+
+// 2. per (sequence, chunk): decisions, first rejection, chunk share of the draw weights.
+// zs[(s * nchunk + c) * 2 + 0] = sum of R over the chunk for the draw row
+// (residual max(0, p_n - q_n) when n < kd, else p_kd); [.. + 1] = sum of R for
+// p_n (the fallback when the residual mass is zero).  blockIdx.x = s * nchunk + c.
+__global__ __launch_bounds__(kThreads) void decide_kernel(const float* __restrict__ draft,
+                                                          const float* __restrict__ target,
+                                                          const int32_t* __restrict__ tokens,
+                                                          const uint32_t* __restrict__ u24, int b, int kd, int v,
+                                                          float temp, int nchunk, const double2* __restrict__ stats,
+                                                          int64_t* __restrict__ zs, SeqInfo* __restrict__ info) {
+  __shared__ double sL[129], sS[129];
+  __shared__ int sAcc[64];
+  __shared__ int sN;
+  __shared__ int64_t shi[4];
+  const int s = blockIdx.x / nchunk;
+  const int c = blockIdx.x % nchunk;
+  const int64_t rows_t = (int64_t)b * (kd + 1);
+  for (int rr = threadIdx.x; rr < 2 * kd + 1; rr += kThreads) {
+    const int64_t row = rr <= kd ? (int64_t)s * (kd + 1) + rr : rows_t + (int64_t)(rr - kd - 1) * b + s;
+    merge_stats(stats + row * nchunk, nchunk, sL[rr], sS[rr]);
+  }
+  __syncthreads();
+  if (threadIdx.x < kd) {
+    const int i = threadIdx.x;
+    const int32_t xt = tokens[(int64_t)s * kd + i];
+    int acc = 0;
+    if (xt >= 0 && xt < v) {
+      const double p = exp(zval(target[((int64_t)s * (kd + 1) + i) * v + xt], temp) - sL[i]) / sS[i];
+      const double q = exp(zval(draft[((int64_t)i * b + s) * v + xt], temp) - sL[kd + 1 + i]) / sS[kd + 1 + i];
+      const double u = ldexp((double)(u24[(int64_t)s * (kd + 1) + i] & 0xFFFFFFu), -24);
+      acc = (u * q < p) ? 1 : 0;
+    }
+    sAcc[i] = acc;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int n = kd;
+    for (int i = 0; i < kd; ++i)
+      if (!sAcc[i]) {
+        n = i;
+        break;
+      }
+    sN = n;
+  }
+  __syncthreads();
+  const int n = sN;
+  const float* lp = target + ((int64_t)s * (kd + 1) + n) * v;
+  const double Lp = sL[n], Sp = sS[n];
+  const bool resid = n < kd;
+  const float* lq = resid ? draft + ((int64_t)n * b + s) * v : nullptr;
+  const double Lq = resid ? sL[kd + 1 + n] : 0.0, Sq = resid ? sS[kd + 1 + n] : 1.0;
+  int64_t z0 = 0, z1 = 0;
+  for (int e = 0; e < kPer; ++e) {
+    const int j = c * kChunk + e * kThreads + threadIdx.x;
+    if (j >= v) break;
+    const double p = exp(zval(lp[j], temp) - Lp) / Sp;
+    if (resid) {
+      const double q = exp(zval(lq[j], temp) - Lq) / Sq;
+      const double r = p - q;
+      z0 += grid_weight(r > 0.0 ? r : 0.0);
+      z1 += grid_weight(p);
+    } else {
+      z0 += grid_weight(p);
+    }
+  }
+  z0 = block_sum_i64(z0, shi);
+  z1 = block_sum_i64(z1, shi);
+  if (threadIdx.x == 0) {
+    zs[((int64_t)s * nchunk + c) * 2 + 0] = z0;
+    zs[((int64_t)s * nchunk + c) * 2 + 1] = z1;
+    if (c == 0) {
+      SeqInfo si;
+      si.n = n;
+      si.pad = 0;
+      si.lp = Lp;
+      si.sp = Sp;
+      si.lq = Lq;
+      si.sq = Sq;
+      info[s] = si;
+    }
+  }
+}
+
+// 3. per sequence: the draw.  The chunk is scanned with 16 consecutive logits
+// per thread so that a block-wide exclusive scan of the thread sums orders them.
+__global__ __launch_bounds__(kThreads) void draw_kernel(const float* __restrict__ draft,
+                                                        const float* __restrict__ target,
+                                                        const uint32_t* __restrict__ u24, int b, int kd, int v,
+                                                        float temp, int nchunk, const int64_t* __restrict__ zs,
+                                                        const SeqInfo* __restrict__ info,
+                                                        int32_t* __restrict__ n_accepted,
+                                                        int32_t* __restrict__ next_token) {
+  __shared__ int64_t sOff;
+  __shared__ int sChunk, sWhich;
+  __shared__ int64_t sPre[kThreads];
+  const int s = blockIdx.x;
+  const SeqInfo si = info[s];
+  const int n = si.n;
+  if (threadIdx.x == 0) {
+    const int64_t* z = zs + (int64_t)s * nchunk * 2;
+    int which = 0;
+    int64_t Z = 0;
+    for (int c = 0; c < nchunk; ++c) Z += z[2 * c];
+    if (Z == 0 && n < kd) {
+      which = 1;
+      for (int c = 0; c < nchunk; ++c) Z += z[2 * c + 1];
+    }
+    int chunk = -1;
+    int64_t off = 0;
+    if (Z > 0) {
+      const uint64_t u = u24[(int64_t)s * (kd + 1) + kd] & 0xFFFFFFu;
+      const uint64_t lo = u * (uint64_t)Z;
+      const uint64_t hi = __umul64hi(u, (uint64_t)Z);
+      const int64_t t = (int64_t)((hi << 40) | (lo >> 24));  // floor(u * Z / 2^24) < Z
+      int64_t run = 0;
+      chunk = nchunk - 1;
+      for (int c = 0; c < nchunk; ++c) {
+        const int64_t zc = z[2 * c + which];
+        if (run + zc > t) {
+          chunk = c;
+          break;
+        }
+        run += zc;
+      }
+      off = t - run;
+    }
+    sChunk = chunk;
+    sWhich = which;
+    sOff = off;
+  }
+  __syncthreads();
+  const int chunk = sChunk;
+  if (chunk < 0) {  // no mass on the fixed-point grid
+    if (threadIdx.x == 0) {
+      n_accepted[s] = n;
+      next_token[s] = -1;
+    }
+    return;
+  }
+  const bool resid = n < kd && sWhich == 0;
+  const float* lp = target + ((int64_t)s * (kd + 1) + n) * v;
+  const float* lq = resid ? draft + ((int64_t)n * b + s) * v : nullptr;
+  int64_t R[kPer];
+  int64_t local = 0;
+  const int beg = chunk * kChunk + threadIdx.x * kPer;
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) {
+    const int j = beg + e;
+    int64_t w = 0;
+    if (j < v) {
+      const double p = exp(zval(lp[j], temp) - si.lp) / si.sp;
+      if (resid) {
+        const double q = exp(zval(lq[j], temp) - si.lq) / si.sq;
+        const double r = p - q;
+        w = grid_weight(r > 0.0 ? r : 0.0);
+      } else {
+        w = grid_weight(p);
+      }
+    }
+    R[e] = w;
+    local += w;
+  }
+  sPre[threadIdx.x] = local;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t run = 0;
+    for (int i = 0; i < kThreads; ++i) {
+      const int64_t t = sPre[i];
+      sPre[i] = run;
+      run += t;
+    }
+  }
+  __syncthreads();
+  const int64_t pre = sPre[threadIdx.x];
+  const int64_t off = sOff;
+  if (local > 0 && pre <= off && off < pre + local) {
+    int64_t run = pre;
+    int tok = beg;
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) {
+      run += R[e];
+      if (run > off) {
+        tok = beg + e;
+        break;
+      }
+    }
+    next_token[s] = tok;
+    n_accepted[s] = n;
+  }
+}
+
+// Greedy: per (target row, chunk) the max logit and its smallest index.
+__global__ __launch_bounds__(kThreads) void argmax_kernel(const float* __restrict__ target, int v, int nchunk,
+                                                          ArgMax* __restrict__ out) {
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const int64_t row = blockIdx.x / nchunk;
+  const int c = blockIdx.x % nchunk;
+  const float* l = target + row * v;
+  float best = -INFINITY;
+  int bi = 0x7FFFFFFF;
+  for (int e = 0; e < kPer; ++e) {
+    const int j = c * kChunk + e * kThreads + threadIdx.x;
+    if (j < v) {
+      const float x = l[j];
+      if (x > best || (x == best && j < bi)) {
+        best = x;
+        bi = j;
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float ov = __shfl_xor(best, off, 64);
+    const int oi = __shfl_xor(bi, off, 64);
+    if (ov > best || (ov == best && oi < bi)) {
+      best = ov;
+      bi = oi;
+    }
+  }
+  if ((threadIdx.x & 63) == 0) {
+    sv[threadIdx.x >> 6] = best;
+    si[threadIdx.x >> 6] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 4; ++w)
+      if (sv[w] > best || (sv[w] == best && si[w] < bi)) {
+        best = sv[w];
+        bi = si[w];
+      }
+    ArgMax a;
+    a.v = best;
+    a.i = bi;
+    out[row * nchunk + c] = a;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void greedy_kernel(const int32_t* __restrict__ tokens, int kd, int v,
+                                                          int nchunk, const ArgMax* __restrict__ am,
+                                                          int32_t* __restrict__ n_accepted,
+                                                          int32_t* __restrict__ next_token) {
+  __shared__ int sArg[65];
+  const int s = blockIdx.x;
+  for (int i = threadIdx.x; i <= kd; i += kThreads) {
+    const ArgMax* a = am + ((int64_t)s * (kd + 1) + i) * nchunk;
+    float best = a[0].v;
+    int bi = a[0].i;
+    for (int c = 1; c < nchunk; ++c)
+      if (a[c].v > best) {  // chunks ascend, so ties keep the earlier index
+        best = a[c].v;
+        bi = a[c].i;
+      }
+    sArg[i] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int n = kd;
+    for (int i = 0; i < kd; ++i) {
+      const int32_t xt = tokens[(int64_t)s * kd + i];
+      if (xt < 0 || xt >= v || xt != sArg[i]) {
+        n = i;
+        break;
+      }
+    }
+    n_accepted[s] = n;
+    next_token[s] = sArg[n];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_spec_accept(const float* draft, const float* target, const int32_t* tokens, const uint32_t* u24,
+                              int b, int kd, int v, float temperature, int32_t* n_accepted, int32_t* next_token,
+                              float* q_out, float* p_out, hipStream_t stream) {
+  const int nchunk = (v + kChunk - 1) / kChunk;
+  const int64_t rows_t = (int64_t)b * (kd + 1);
+  if (temperature == 0.0f) {
+    ArgMax* am = static_cast<ArgMax*>(workspace((size_t)rows_t * nchunk * sizeof(ArgMax)));
+    if (!am) return hipErrorOutOfMemory;
+    hipLaunchKernelGGL(argmax_kernel, dim3((unsigned)(rows_t * nchunk)), dim3(kThreads), 0, stream, target, v, nchunk,
+                       am);
+    hipLaunchKernelGGL(greedy_kernel, dim3((unsigned)b), dim3(kThreads), 0, stream, tokens, kd, v, nchunk, am,
+                       n_accepted, next_token);
+    return hipGetLastError();
+  }
+  const int64_t rows = rows_t + (int64_t)b * kd;
+  const size_t st_bytes = ((size_t)rows * nchunk * sizeof(double2) + 255) / 256 * 256;
+  const size_t zs_bytes = ((size_t)b * nchunk * 2 * sizeof(int64_t) + 255) / 256 * 256;
+  const size_t in_bytes = (size_t)b * sizeof(SeqInfo);
+  char* ws = static_cast<char*>(workspace(st_bytes + zs_bytes + in_bytes));
+  if (!ws) return hipErrorOutOfMemory;
+  double2* stats = reinterpret_cast<double2*>(ws);
+  int64_t* zs = reinterpret_cast<int64_t*>(ws + st_bytes);
+  SeqInfo* info = reinterpret_cast<SeqInfo*>(ws + st_bytes + zs_bytes);
+  hipLaunchKernelGGL(stats_kernel, dim3((unsigned)(rows * nchunk)), dim3(kThreads), 0, stream, draft, target, rows_t, v,
+                     temperature, nchunk, stats);
+  if (p_out || q_out)
+    hipLaunchKernelGGL(probs_kernel, dim3((unsigned)(rows * nchunk)), dim3(kThreads), 0, stream, draft, target, rows_t,
+                       v, temperature, nchunk, stats, q_out, p_out);
+  hipLaunchKernelGGL(decide_kernel, dim3((unsigned)((int64_t)b * nchunk)), dim3(kThreads), 0, stream, draft, target,
+                     tokens, u24, b, kd, v, temperature, nchunk, stats, zs, info);
+  hipLaunchKernelGGL(draw_kernel, dim3((unsigned)b), dim3(kThreads), 0, stream, draft, target, u24, b, kd, v,
+                     temperature, nchunk, zs, info, n_accepted, next_token);
+  return hipGetLastError();
+}
+
+}  // namespace sq

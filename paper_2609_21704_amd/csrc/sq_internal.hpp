@@ -1,0 +1,35 @@
+// Host-side launchers of the SpecQuant kernels; argument validation happens
+// in the C-ABI layer before any of these is called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sq {
+
+// Library-owned device workspace of at least `bytes` bytes on the current
+// device (grown on demand, never shrunk).  Returns nullptr on failure.
+void* workspace(size_t bytes);
+
+hipError_t launch_quantize_int4(const uint16_t* w, int64_t n, int64_t k, uint8_t* codes, uint16_t* scales,
+                                uint16_t* zeros, int32_t* flag, hipStream_t stream);
+hipError_t launch_quantize_fp8(const uint16_t* w, int64_t n, int64_t k, uint8_t* codes, float* scales,
+                               int32_t* flag, hipStream_t stream);
+
+hipError_t launch_gemv_w4(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const uint16_t* scales,
+                          const uint16_t* zeros, int64_t n, void* y, bool f16_out, hipStream_t stream);
+hipError_t launch_gemv_w8(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const float* scales,
+                          int64_t n, void* y, bool f16_out, hipStream_t stream);
+hipError_t launch_gemm_f16(const uint16_t* x, int m, int64_t k, const uint16_t* w, int64_t n, void* y,
+                           bool f16_out, hipStream_t stream);
+
+// Sum of S split-K partials [S][mn] fp32 into y[mn] (fixed order s = 0..S-1).
+hipError_t launch_splitk_reduce(const float* partial, int splits, int64_t mn, void* y, bool f16_out,
+                                hipStream_t stream);
+
+hipError_t launch_spec_accept(const float* draft, const float* target, const int32_t* tokens, const uint32_t* u24,
+                              int b, int kd, int v, float temperature, int32_t* n_accepted, int32_t* next_token,
+                              float* q_out, float* p_out, hipStream_t stream);
+
+}  // namespace sq

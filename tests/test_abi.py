@@ -1,0 +1,101 @@
+"""CPU-only checks of the C ABI: the built library loads, exports every symbol
+the header declares, and rejects invalid arguments on the host before any HIP
+call (fake, never dereferenced device addresses are passed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_21704_amd as sq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "specquant.h")
+
+OK, NULL, SHAPE, ALIGN, ALIAS, VALUE = 0, 1, 2, 3, 4, 5
+A = 0x7F0000000000          # 16-byte aligned fake addresses, far apart
+B = A + (1 << 32)
+C = A + (2 << 32)
+D = A + (3 << 32)
+E = A + (4 << 32)
+F32, F16 = 1, 0
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:sq_status|const char\*|int32_t)\s+(sq_\w+)\s*\(", text, re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = sq.load()
+    names = declared_symbols()
+    assert set(names) == {"sq_abi_version", "sq_status_str", "sq_quantize_int4_g128", "sq_quantize_fp8_e4m3",
+                          "sq_qgemv_w4a16", "sq_qgemv_w8a16", "sq_verify_gemm_f16", "sq_spec_accept"}
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sq.sq_abi_version() == 1
+    for s in range(7):
+        assert lib.sq_status_str(s).startswith(b"SQ_")
+
+
+def test_quantize_validation():
+    lib = sq.load()
+    q4, q8 = lib.sq_quantize_int4_g128, lib.sq_quantize_fp8_e4m3
+    assert q4(None, 4, 128, B, C, D, None, None) == NULL
+    assert q4(A, 4, 100, B, C, D, None, None) == SHAPE
+    assert q4(A, 0, 128, B, C, D, None, None) == SHAPE
+    assert q4(A, 4, 1 << 21, B, C, D, None, None) == SHAPE
+    assert q4(A + 2, 4, 128, B, C, D, None, None) == ALIGN
+    assert q4(A, 4, 128, B + 8, C, D, None, None) == ALIGN
+    assert q4(A, 4, 128, A + 16, C, D, None, None) == ALIAS       # codes inside w16
+    assert q4(A, 4, 128, B, C, C + 2, None, None) == ALIAS        # zeros overlap scales
+    assert q8(A, 4, 24, B, C, None, None) == SHAPE
+    assert q8(A, 4, 32, B, C + 2, None, None) == ALIGN
+    assert q8(A, 4, 32, B, A + 8, None, None) == ALIAS
+
+
+def test_gemv_gemm_validation():
+    lib = sq.load()
+    w4, w8, gm = lib.sq_qgemv_w4a16, lib.sq_qgemv_w8a16, lib.sq_verify_gemm_f16
+    assert w4(A, 1, 256, B, C, D, 10, None, F32, None) == NULL
+    assert w4(A, 9, 256, B, C, D, 10, E, F32, None) == SHAPE
+    assert w4(A, 0, 256, B, C, D, 10, E, F32, None) == SHAPE
+    assert w4(A, 1, 200, B, C, D, 10, E, F32, None) == SHAPE
+    assert w4(A, 1, 256, B, C, D, 0, E, F32, None) == SHAPE
+    assert w4(A, 1, 256, B, C, D, 10, E, 7, None) == VALUE
+    assert w4(A + 8, 1, 256, B, C, D, 10, E, F32, None) == ALIGN
+    assert w4(A, 1, 256, B, C, D, 10, E + 2, F32, None) == ALIGN
+    assert w4(A, 1, 256, B, C, D, 10, A + 64, F32, None) == ALIAS   # y overlaps x
+    assert w8(A, 1, 24, B, C, 10, E, F32, None) == SHAPE
+    assert w8(A, 1, 32, B, C + 2, 10, E, F32, None) == ALIGN
+    assert w8(A, 2, 32, B, C, 10, C + 4, F16, None) == ALIAS        # y overlaps scales
+    assert gm(A, 65, 64, B, 10, E, F32, None) == SHAPE
+    assert gm(A, 5, 12, B, 10, E, F32, None) == SHAPE
+    assert gm(A, 5, 64, B + 2, 10, E, F32, None) == ALIGN
+    assert gm(A, 5, 64, B, 10, B + 100, F32, None) == ALIAS
+
+
+def test_accept_validation():
+    lib = sq.load()
+    acc = lib.sq_spec_accept
+    # (draft, target, tokens, u24, b, kd, v, T, n_acc, next, q_out, p_out, stream)
+    assert acc(A, None, C, D, 1, 4, 100, 1.0, E, E + 64, None, None, None) == NULL
+    assert acc(None, B, C, D, 1, 4, 100, 1.0, E, E + 64, None, None, None) == NULL
+    assert acc(A, B, C, None, 1, 4, 100, 1.0, E, E + 64, None, None, None) == NULL
+    assert acc(A, B, C, D, 0, 4, 100, 1.0, E, E + 64, None, None, None) == SHAPE
+    assert acc(A, B, C, D, 1, 65, 100, 1.0, E, E + 64, None, None, None) == SHAPE
+    assert acc(A, B, C, D, 1, -1, 100, 1.0, E, E + 64, None, None, None) == SHAPE
+    assert acc(A, B, C, D, 1, 4, 0, 1.0, E, E + 64, None, None, None) == SHAPE
+    assert acc(A, B, C, D, 1 << 20, 8, 151936, 1.0, E, E + (1 << 22), None, None, None) == SHAPE
+    assert acc(A, B, C, D, 1, 4, 100, -1.0, E, E + 64, None, None, None) == VALUE
+    assert acc(A, B, C, D, 1, 4, 100, float("nan"), E, E + 64, None, None, None) == VALUE
+    assert acc(A, B, C, D, 1, 4, 100, 0.0, E, E + 64, E + 128, None, None) == VALUE
+    assert acc(A, B, C, D, 1, 4, 100, 1.0, E + 2, E + 64, None, None, None) == ALIGN
+    assert acc(A, B, C, D, 1, 4, 100, 1.0, E, E, None, None, None) == ALIAS
+    assert acc(A, B, C, D, 1, 4, 100, 1.0, E, E + 64, None, B + 40, None) == ALIAS
+
+
+def test_binding_fails_loudly_without_gpu_tensors():
+    torch = pytest.importorskip("torch")
+    with pytest.raises(ValueError):
+        sq.sq_quantize_int4_g128(torch.zeros((4, 128), dtype=torch.float16))

@@ -1,0 +1,313 @@
+"""GPU parity: every HIP entry point against the CPU oracle on the same seeded
+inputs, element by element.  Quantized codes, scales and accept decisions are
+compared bit for bit; GEMV/GEMM outputs within max |y - y_ref| / sum |x w'|
+<= 2e-3; softmax probabilities within 1e-5 absolute.  Shapes span several
+tiles with ragged tails and include the degenerate cases."""
+import numpy as np
+import pytest
+import torch
+from scipy import special, stats
+
+import oracle
+import paper_2609_21704_amd as sq
+from paper_2609_21704_amd import synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+GEMV_TOL = 2e-3
+PROB_TOL = 1e-5
+
+
+def bits16(t: torch.Tensor) -> np.ndarray:
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def special_rows(w: torch.Tensor) -> torch.Tensor:
+    """Overwrite the first rows with degenerate patterns (needs n >= 6)."""
+    w = w.clone()
+    n, k = w.shape
+    if n >= 6:
+        w[0] = 0.0                                             # all-zero row / groups
+        w[1] = 0.0
+        w[1, k // 3] = 1.0                                     # one-hot
+        w[2] = torch.linspace(-1e-6, 1e-6, k).to(torch.float16)  # fp16 subnormals
+        w[3] = -w[3].abs()                                     # all negative
+        w[3, 0] = -0.0
+        w[4] = w[4].abs()                                      # all positive
+        w[5, : min(k, 64)] = 65504.0                           # fp16 extremes
+        w[5, min(k, 64) // 2: min(k, 64)] = -65504.0
+    return w
+
+
+# ----------------------------------------------------------- quantizers ----
+INT4_SHAPES = [(1, 128), (37, 384), (896, 896), (128, 896), (4864, 896), (896, 4864), (129, 3584)]
+
+
+@pytest.mark.parametrize("n,k", INT4_SHAPES)
+def test_quantize_int4_bit_exact(n, k):
+    w = special_rows(synth.normal_f16((n, k), 0.02, synth.stream_seed(0, n, k)))
+    codes, scales, zeros = sq.sq_quantize_int4_g128(w.to(DEV))
+    c_ref, s_ref, z_ref = oracle.quantize_int4_g128(bits16(w))
+    assert np.array_equal(codes.cpu().numpy(), c_ref)
+    assert np.array_equal(bits16(scales), s_ref)
+    assert np.array_equal(bits16(zeros), z_ref)
+
+
+def test_quantize_int4_nonfinite_flag():
+    w = synth.normal_f16((4, 256), 0.02, 5)
+    w[2, 200] = float("nan")
+    flag = torch.zeros(1, dtype=torch.int32, device=DEV)
+    codes, scales, zeros = sq.sq_quantize_int4_g128(w.to(DEV), nonfinite_flag=flag)
+    assert int(flag.item()) == 1
+    assert bits16(scales)[2, 1] == 0x7E00 and np.all(codes.cpu().numpy()[2, 64:] == 0)
+    ok = torch.zeros(1, dtype=torch.int32, device=DEV)
+    sq.sq_quantize_int4_g128(synth.normal_f16((4, 256), 0.02, 6).to(DEV), nonfinite_flag=ok)
+    assert int(ok.item()) == 0
+
+
+FP8_SHAPES = [(1, 16), (37, 400), (896, 896), (128, 896), (4864, 896), (896, 4864), (5, 18944)]
+
+
+@pytest.mark.parametrize("n,k", FP8_SHAPES)
+def test_quantize_fp8_bit_exact(n, k):
+    w = special_rows(synth.normal_f16((n, k), 0.02, synth.stream_seed(1, n, k)))
+    codes, scales = sq.sq_quantize_fp8_e4m3(w.to(DEV))
+    c_ref, s_ref = oracle.quantize_fp8_e4m3(bits16(w))
+    assert np.array_equal(codes.cpu().numpy(), c_ref)
+    assert np.array_equal(scales.cpu().numpy().view(np.uint32), s_ref.view(np.uint32))
+
+
+def test_quantize_fp8_nonfinite_flag():
+    w = synth.normal_f16((3, 64), 0.02, 7)
+    w[1, 5] = float("inf")
+    flag = torch.zeros(1, dtype=torch.int32, device=DEV)
+    codes, scales = sq.sq_quantize_fp8_e4m3(w.to(DEV), nonfinite_flag=flag)
+    assert int(flag.item()) == 1
+    assert np.isnan(scales.cpu().numpy()[1]) and np.all(codes.cpu().numpy()[1] == 0)
+
+
+# ----------------------------------------------------------------- GEMV ----
+GEMV_SHAPES = [(1, 128), (37, 384), (896, 896), (4864, 896), (896, 4864), (257, 3584), (130, 18944)]
+
+
+def _gemv_inputs(m, n, k, seed):
+    w = synth.normal_f16((n, k), 0.02, synth.stream_seed(seed, 1, n, k))
+    x = synth.normal_f16((m, k), 1.0, synth.stream_seed(seed, 2, m, k))
+    return w, x
+
+
+@pytest.mark.parametrize("n,k", GEMV_SHAPES)
+@pytest.mark.parametrize("m", [1, 2, 3, 4, 5, 8])
+def test_qgemv_w4a16_parity(m, n, k):
+    w, x = _gemv_inputs(m, n, k, 10)
+    wd, xd = w.to(DEV), x.to(DEV)
+    codes, scales, zeros = sq.sq_quantize_int4_g128(wd)
+    c_ref, s_ref, z_ref = oracle.quantize_int4_g128(bits16(w))
+    y_ref, d_ref = oracle.qgemv_w4a16(bits16(x), c_ref, s_ref, z_ref)
+    for dt in (torch.float32, torch.float16):
+        y = sq.sq_qgemv_w4a16(xd, codes, scales, zeros, y_dtype=dt)
+        err = oracle.normalised_error(y.float().cpu().numpy(), y_ref, d_ref)
+        assert err <= GEMV_TOL, (dt, err)
+
+
+@pytest.mark.parametrize("n,k", [(1, 16), (37, 400), (896, 896), (4864, 896), (896, 4864), (257, 3584),
+                                 (130, 18944)])
+@pytest.mark.parametrize("m", [1, 2, 4, 5, 8])
+def test_qgemv_w8a16_parity(m, n, k):
+    w, x = _gemv_inputs(m, n, k, 11)
+    wd, xd = w.to(DEV), x.to(DEV)
+    codes, scales = sq.sq_quantize_fp8_e4m3(wd)
+    c_ref, s_ref = oracle.quantize_fp8_e4m3(bits16(w))
+    y_ref, d_ref = oracle.qgemv_w8a16(bits16(x), c_ref, s_ref)
+    for dt in (torch.float32, torch.float16):
+        y = sq.sq_qgemv_w8a16(xd, codes, scales, y_dtype=dt)
+        err = oracle.normalised_error(y.float().cpu().numpy(), y_ref, d_ref)
+        assert err <= GEMV_TOL, (dt, err)
+
+
+def test_qgemv_w8a16_every_code_decodes_exactly():
+    """Row c holds code c at column 0 (NaN codes replaced by 0); x = e_0."""
+    n, k = 256, 32
+    codes = np.zeros((n, k), np.uint8)
+    codes[:, 0] = np.arange(256)
+    codes[0x7F, 0] = codes[0xFF, 0] = 0
+    scales = np.ones(n, np.float32)
+    x = np.zeros((1, k), np.float16)
+    x[0, 0] = 1.0
+    y = sq.sq_qgemv_w8a16(torch.from_numpy(x).to(DEV), torch.from_numpy(codes).to(DEV),
+                          torch.from_numpy(scales).to(DEV)).cpu().numpy()[0]
+    y_ref, _ = oracle.qgemv_w8a16(x, codes, scales)
+    assert np.array_equal(y.astype(np.float64), y_ref[0])
+
+
+def test_qgemv_w4a16_closed_forms():
+    k = 512
+    x = synth.normal_f16((3, k), 1.0, 3)
+    # identity: one-hot groups give 1.00067138671875 * x
+    eye = torch.eye(k, dtype=torch.float16)
+    codes, scales, zeros = sq.sq_quantize_int4_g128(eye.to(DEV))
+    y = sq.sq_qgemv_w4a16(x.to(DEV), codes, scales, zeros).cpu().double().numpy()
+    ref = 1.00067138671875 * x.double().numpy()
+    d = np.abs(ref)
+    assert np.max(np.abs(y - ref) / np.maximum(d, 1e-30)) <= GEMV_TOL
+    # all-zero weights give exact zeros
+    zc, zs, zz = sq.sq_quantize_int4_g128(torch.zeros((9, k), dtype=torch.float16, device=DEV))
+    assert torch.count_nonzero(sq.sq_qgemv_w4a16(x.to(DEV), zc, zs, zz)).item() == 0
+
+
+# ------------------------------------------------------------ verify GEMM ----
+GEMM_SHAPES = [(1, 8), (37, 136), (896, 896), (4864, 896), (896, 4864), (100, 3584), (33, 18944)]
+
+
+@pytest.mark.parametrize("n,k", GEMM_SHAPES)
+@pytest.mark.parametrize("m", [1, 5, 7, 16, 17, 36, 48, 64])
+def test_verify_gemm_f16_parity(m, n, k):
+    w, x = _gemv_inputs(m, n, k, 12)
+    y_ref, d_ref = oracle.gemm_f16(bits16(x), bits16(w))
+    for dt in (torch.float32, torch.float16):
+        y = sq.sq_verify_gemm_f16(x.to(DEV), w.to(DEV), y_dtype=dt)
+        err = oracle.normalised_error(y.float().cpu().numpy(), y_ref, d_ref)
+        assert err <= GEMV_TOL, (dt, err)
+
+
+@pytest.mark.parametrize("m", [1, 5, 36])
+def test_verify_gemm_identity_is_exact(m):
+    k = 384
+    x = synth.normal_f16((m, k), 1.0, 4)
+    y = sq.sq_verify_gemm_f16(x.to(DEV), torch.eye(k, dtype=torch.float16, device=DEV))
+    assert torch.equal(y.cpu(), x.float())
+
+
+# --------------------------------------------------------------- accept ----
+def _accept_case(b, kd, v, seed, temp, token_mode="sampled", sd=2.0, noise=0.5):
+    """draft ~ N(0, sd), target = draft + N(0, noise) (bonus row fresh); tokens drawn from q."""
+    draft = synth.normal_f32((kd, b, v), sd, synth.stream_seed(seed, 1))
+    target = torch.empty((b, kd + 1, v), dtype=torch.float32)
+    eps = synth.normal_f32((b, kd + 1, v), noise, synth.stream_seed(seed, 2))
+    target[:, :kd] = draft.permute(1, 0, 2) + eps[:, :kd]
+    target[:, kd] = synth.normal_f32((b, v), sd, synth.stream_seed(seed, 3))
+    u24 = synth.uniform_u24((b, kd + 1), synth.stream_seed(seed, 4))
+    if kd == 0:
+        tok = torch.zeros((b, 0), dtype=torch.int32)
+    elif token_mode == "sampled" and temp > 0:
+        q = oracle.softmax(draft.reshape(kd * b, v).numpy(), float(np.float32(temp))).reshape(kd, b, v)
+        r = np.random.default_rng(seed).random((kd, b))
+        tok = np.minimum((r[..., None] >= np.cumsum(q, axis=2)).sum(axis=2), v - 1).T.astype(np.int32)
+        tok = torch.from_numpy(np.ascontiguousarray(tok))
+    else:
+        tok = synth.tokens((b, kd), v, synth.stream_seed(seed, 5))
+    return draft, target, tok, u24
+
+
+def _run_accept(draft, target, tok, u24, temp, want_pq=False):
+    b, kd1, v = target.shape
+    kd = kd1 - 1
+    q_out = torch.empty((kd, b, v), dtype=torch.float32, device=DEV) if want_pq and kd > 0 else None
+    p_out = torch.empty((b, kd1, v), dtype=torch.float32, device=DEV) if want_pq else None
+    n, t = sq.sq_spec_accept(draft.to(DEV) if kd > 0 else None, target.to(DEV), tok.to(DEV) if kd > 0 else None,
+                             u24.to(DEV), temp, q_out=q_out, p_out=p_out)
+    return n.cpu().numpy(), t.cpu().numpy(), q_out, p_out
+
+
+ACCEPT_CASES = [
+    (1, 4, 4096, 1.0), (1, 4, 151936, 1.0), (4, 8, 151936, 1.0), (3, 0, 1000, 1.0), (7, 3, 8, 0.7),
+    (2, 64, 300, 1.0), (64, 2, 5000, 1.3), (16, 6, 152064, 1.0), (5, 1, 4097, 0.5),
+]
+
+
+@pytest.mark.parametrize("b,kd,v,temp", ACCEPT_CASES)
+@pytest.mark.parametrize("token_mode", ["sampled", "uniform"])
+def test_spec_accept_parity(b, kd, v, temp, token_mode):
+    temp = float(np.float32(temp))
+    draft, target, tok, u24 = _accept_case(b, kd, v, 100 + b + kd, temp, token_mode)
+    n, t, _, _ = _run_accept(draft, target, tok, u24, temp)
+    n_ref, t_ref, _, _ = oracle.spec_accept(draft.numpy(), target.numpy(), tok.numpy(),
+                                            u24.numpy().view(np.uint32), temp)
+    assert np.array_equal(n, n_ref)
+    assert np.array_equal(t, t_ref)
+
+
+@pytest.mark.parametrize("b,kd,v,temp", [(1, 4, 4096, 1.0), (4, 8, 151936, 1.0), (3, 0, 1000, 0.8)])
+def test_spec_accept_probabilities(b, kd, v, temp):
+    temp = float(np.float32(temp))
+    draft, target, tok, u24 = _accept_case(b, kd, v, 7, temp)
+    n, t, q_out, p_out = _run_accept(draft, target, tok, u24, temp, want_pq=True)
+    n_ref, t_ref, q_ref, p_ref = oracle.spec_accept(draft.numpy(), target.numpy(), tok.numpy(),
+                                                    u24.numpy().view(np.uint32), temp, want_pq=True)
+    assert np.max(np.abs(p_out.cpu().numpy() - p_ref)) <= PROB_TOL
+    if kd > 0:
+        assert np.max(np.abs(q_out.cpu().numpy() - q_ref)) <= PROB_TOL
+    assert np.array_equal(n, n_ref) and np.array_equal(t, t_ref)
+
+
+@pytest.mark.parametrize("b,kd,v", [(5, 4, 4096), (3, 0, 100), (200, 3, 50), (2, 8, 151936)])
+def test_spec_accept_greedy(b, kd, v):
+    draft, target, tok, u24 = _accept_case(b, kd, v, 9, 0.0, "uniform")
+    target[0, 0] = 1.0                               # ties -> smallest index
+    am = target.argmax(dim=2).to(torch.int32)
+    if kd > 0:
+        tok = am[:, :kd].clone()
+        tok[1 % b, kd // 2] = (tok[1 % b, kd // 2] + 1) % v
+    n, t, _, _ = _run_accept(draft, target, tok, u24, 0.0)
+    n_ref, t_ref, _, _ = oracle.spec_accept(draft.numpy(), target.numpy(), tok.numpy(), None, 0.0)
+    assert np.array_equal(n, n_ref) and np.array_equal(t, t_ref)
+
+
+def test_spec_accept_edge_tokens_and_equal_distributions():
+    b, kd, v = 6, 4, 333
+    draft, target, tok, u24 = _accept_case(b, kd, v, 21, 1.0, "uniform")
+    tok[0, 0] = -1
+    tok[1, 2] = v
+    tok[2, 1] = 1 << 30
+    target[3, :kd] = draft[:, 3]                     # p = q for sequence 3: all accepted
+    u24[4] = (1 << 24) - 1
+    u24[5] = 0
+    n, t, _, _ = _run_accept(draft, target, tok, u24, 1.0)
+    n_ref, t_ref, _, _ = oracle.spec_accept(draft.numpy(), target.numpy(), tok.numpy(),
+                                            u24.numpy().view(np.uint32), 1.0)
+    assert np.array_equal(n, n_ref) and np.array_equal(t, t_ref)
+    assert n[0] == 0 and n[3] == kd
+
+
+def test_spec_accept_chi_square_on_gpu():
+    """10^6 sequences at V = 8, kd = 4: acceptance law and per-position token law."""
+    rng = np.random.default_rng(3)
+    b, kd, v = 1_000_000, 4, 8
+    dl = rng.normal(0, 1.2, (kd, v)).astype(np.float32)
+    tl = np.concatenate([dl + rng.normal(0, 0.8, (kd, v)).astype(np.float32),
+                         rng.normal(0, 1, (1, v)).astype(np.float32)])
+    q = special.softmax(dl.astype(np.float64), axis=1)
+    p = special.softmax(tl.astype(np.float64), axis=1)
+    x = np.minimum((rng.random((b, kd))[..., None] >= np.cumsum(q, axis=1)[None]).sum(axis=2), v - 1).astype(np.int32)
+    u24 = rng.integers(0, 1 << 24, (b, kd + 1)).astype(np.int32)
+    draft = torch.from_numpy(np.ascontiguousarray(np.broadcast_to(dl[:, None, :], (kd, b, v))))
+    target = torch.from_numpy(np.ascontiguousarray(np.broadcast_to(tl[None], (b, kd + 1, v))))
+    n, nxt, _, _ = _run_accept(draft, target, torch.from_numpy(x), torch.from_numpy(u24), 1.0)
+    crit = lambda dof: stats.chi2.ppf(1 - 1e-3, dof)
+    beta = np.minimum(p[:kd], q).sum(axis=1)
+    law = np.array([np.prod(beta[:i]) * (1 - beta[i]) for i in range(kd)] + [np.prod(beta)])
+    obs = np.bincount(n, minlength=kd + 1)
+    assert np.sum((obs - b * law) ** 2 / (b * law)) < crit(kd)
+    for i in range(kd + 1):
+        reached = n >= i
+        tok = np.where(n[reached] > i, x[reached, min(i, kd - 1)], nxt[reached])
+        cnt = np.bincount(tok, minlength=v)
+        exp = reached.sum() * p[i]
+        assert np.sum((cnt - exp) ** 2 / exp) < crit(v - 1), i
+
+
+# ---------------------------------------------------------- determinism ----
+def test_repeat_runs_are_bitwise_identical():
+    w, x = _gemv_inputs(5, 4864, 896, 13)
+    wd, xd = w.to(DEV), x.to(DEV)
+    c4 = sq.sq_quantize_int4_g128(wd)
+    c8 = sq.sq_quantize_fp8_e4m3(wd)
+    outs = []
+    for _ in range(2):
+        outs.append((sq.sq_qgemv_w4a16(xd[:1], *c4), sq.sq_qgemv_w8a16(xd[:4], *c8), sq.sq_verify_gemm_f16(xd, wd)))
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+    draft, target, tok, u24 = _accept_case(4, 8, 151936, 5, 1.0)
+    r1 = _run_accept(draft, target, tok, u24, 1.0)
+    r2 = _run_accept(draft, target, tok, u24, 1.0)
+    assert np.array_equal(r1[0], r2[0]) and np.array_equal(r1[1], r2[1])
