@@ -10,13 +10,15 @@
 //
 // INT4 (W4A16).  A 16-byte load holds 32 consecutive 4-bit codes of one row,
 // i.e. a quarter of one 128-element group.  Each 32-bit word (codes of k..k+7)
-// is turned into four half2 values without any conversion instruction: a
-// nibble masked into the low mantissa bits of a binary16 constant c gives the
-// exact value c + q (c = 1024, 64, 4, 64 for the four nibble pairs (0,4),
-// (1,5), (2,6), (3,7)).  v_dot2_f32_f16 accumulates sum (c + q) * x in fp32;
-// the per-chunk constants Xc = sum c * x and Xs = sum x are precomputed at
-// staging time, so a chunk contributes s * (A - Xc - z * Xs) with the group
-// scale s and zero z.  That is 1.125 VALU operations per weight at m = 1.
+// is turned into four half2 values without a conversion instruction: a nibble
+// masked into mantissa bits 0-3 (or 4-7) of the binary16 constant 1024 (or
+// 64) is the exact value 1024 + q (or 64 + q); one shift by 8 serves the
+// upper nibble pairs.  Subtracting the packed constant c + z in fp16 is exact
+// and leaves q - z in [-15, 15], so v_dot2_f32_f16 forms exact products
+// (q - z) * x and the fp32 accumulation error is bounded by sum |(q - z) x|;
+// the group scale multiplies the chunk sum once.  Per word: one shift, four
+// and-or, four packed subtracts, four dot2 -- 1.6 VALU operations per weight
+// at m = 1.
 //
 // FP8 (W8A16).  A 16-byte load holds 16 E4M3 codes; v_cvt_scalef32_pk_f16_fp8
 // converts two codes to two exact binary16 values, v_dot2_f32_f16 accumulates,
@@ -35,31 +37,20 @@ constexpr size_t kLdsBudget = 64 * 1024;    // bytes of LDS one workgroup may us
 // ----------------------------------------------------------------- INT4 ----
 // LDS layout for a K slice of nchunk 32-element chunks (consecutive chunks,
 // which consecutive lanes read, are consecutive 16-byte cells):
-//   xs  [M][4 words][nchunk][8 halves]  halves of word w in the order
-//        x[8w+0], x[8w+4], x[8w+1], x[8w+5], x[8w+2], x[8w+6], x[8w+3], x[8w+7]
-//   xcs [M][nchunk] float2 = (Xc, Xs) for the chunk
+//   xs [M][4 words][nchunk][8 halves], halves of word w in the order
+//      x[8w+0], x[8w+4], x[8w+1], x[8w+5], x[8w+2], x[8w+6], x[8w+3], x[8w+7]
+// matching the nibble pairs (0,4), (1,5), (2,6), (3,7) of a code word.
 template <int M>
 __device__ __forceinline__ void stage_x_w4(const uint16_t* __restrict__ x, int64_t k, int64_t k0, int nchunk,
-                                           half_t* xs, float2* xcs) {
-  for (int idx = threadIdx.x; idx < nchunk * M; idx += kThreads) {
-    const int c = idx / M, m = idx % M;
-    const uint16_t* src = x + (int64_t)m * k + k0 + 32 * c;
-    float xsum = 0.f, xc = 0.f;
+                                           half_t* xs) {
+  for (int idx = threadIdx.x; idx < nchunk * M * 4; idx += kThreads) {
+    const int c = idx / (M * 4), rem = idx % (M * 4), m = rem >> 2, wd = rem & 3;
+    const u32x4 raw = *reinterpret_cast<const u32x4*>(x + (int64_t)m * k + k0 + 32 * c + 8 * wd);
+    half_t e[8];
 #pragma unroll
-    for (int wd = 0; wd < 4; ++wd) {
-      const u32x4 raw = *reinterpret_cast<const u32x4*>(src + 8 * wd);
-      half_t e[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) e[i] = __builtin_bit_cast(half_t, (uint16_t)(raw[i >> 1] >> (16 * (i & 1))));
-      half8_t p = {e[0], e[4], e[1], e[5], e[2], e[6], e[3], e[7]};
-      *reinterpret_cast<half8_t*>(xs + (((size_t)m * 4 + wd) * nchunk + c) * 8) = p;
-      float f[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) f[i] = (float)e[i];
-      xsum += ((f[0] + f[4]) + (f[1] + f[5])) + ((f[2] + f[6]) + (f[3] + f[7]));
-      xc += 1024.f * (f[0] + f[4]) + 64.f * ((f[1] + f[5]) + (f[3] + f[7])) + 4.f * (f[2] + f[6]);
-    }
-    xcs[(size_t)m * nchunk + c] = make_float2(xc, xsum);
+    for (int i = 0; i < 8; ++i) e[i] = __builtin_bit_cast(half_t, (uint16_t)(raw[i >> 1] >> (16 * (i & 1))));
+    const half8_t p = {e[0], e[4], e[1], e[5], e[2], e[6], e[3], e[7]};
+    *reinterpret_cast<half8_t*>(xs + (((size_t)m * 4 + wd) * nchunk + c) * 8) = p;
   }
 }
 
@@ -75,8 +66,7 @@ __global__ __launch_bounds__(kThreads) void gemv_w4_kernel(const uint16_t* __res
   const int64_t kl = (k - k0) < kslice ? (k - k0) : kslice;
   const int nchunk = (int)(kl / 32);
   half_t* xs = reinterpret_cast<half_t*>(smem);
-  float2* xcs = reinterpret_cast<float2*>(smem + (size_t)nchunk * M * 64);
-  stage_x_w4<M>(x, k, k0, nchunk, xs, xcs);
+  stage_x_w4<M>(x, k, k0, nchunk, xs);
   __syncthreads();
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -94,13 +84,35 @@ __global__ __launch_bounds__(kThreads) void gemv_w4_kernel(const uint16_t* __res
       const int64_t kc = k0 + 32 * (int64_t)c;
       const int64_t g = kc >> 7;
       u32x4 wq[kRows];
-      float s[kRows], z[kRows];
+      uint32_t zb[kRows];
+      float s[kRows];
 #pragma unroll
       for (int r = 0; r < kRows; ++r) {
         const int64_t row = (r0 + r) < n ? (r0 + r) : (n - 1);
         wq[r] = *reinterpret_cast<const u32x4*>(codes + row * (k >> 1) + (kc >> 1));
         s[r] = f16_bits_to_f32(scales[row * groups + g]);
-        z[r] = f16_bits_to_f32(zeros[row * groups + g]);
+        zb[r] = zeros[row * groups + g];
+      }
+      // (q - z) as exact half2 values for the 4 words of each row.  The masks
+      // and magic constants live in VGPRs so that each mask-and-insert is a
+      // single v_and_or_b32 (a VOP3 encoding cannot carry two literals).
+      uint32_t mlo = 0x000F000Fu, mhi = 0x00F000F0u, k1024 = 0x64006400u, k64 = 0x54005400u;
+      asm("" : "+v"(mlo), "+v"(mhi), "+v"(k1024), "+v"(k64));
+      half2_t dq[kRows][16];
+#pragma unroll
+      for (int r = 0; r < kRows; ++r) {
+        const half2_t z2 = __builtin_bit_cast(half2_t, zb[r] | (zb[r] << 16));
+        const half2_t c1024 = z2 + half2_t{(half_t)1024.0f, (half_t)1024.0f};
+        const half2_t c64 = z2 + half2_t{(half_t)64.0f, (half_t)64.0f};
+#pragma unroll
+        for (int wd = 0; wd < 4; ++wd) {
+          const uint32_t q = wq[r][wd];
+          const uint32_t q8 = q >> 8;
+          dq[r][4 * wd + 0] = __builtin_bit_cast(half2_t, (q & mlo) | k1024) - c1024;   // q0, q4
+          dq[r][4 * wd + 1] = __builtin_bit_cast(half2_t, (q & mhi) | k64) - c64;       // q1, q5
+          dq[r][4 * wd + 2] = __builtin_bit_cast(half2_t, (q8 & mlo) | k1024) - c1024;  // q2, q6
+          dq[r][4 * wd + 3] = __builtin_bit_cast(half2_t, (q8 & mhi) | k64) - c64;      // q3, q7
+        }
       }
 #pragma unroll
       for (int m = 0; m < M; ++m) {
@@ -111,23 +123,12 @@ __global__ __launch_bounds__(kThreads) void gemv_w4_kernel(const uint16_t* __res
 #pragma unroll
           for (int i = 0; i < 4; ++i) xv[4 * wd + i] = xp[i];
         }
-        const float2 cs = xcs[(size_t)m * nchunk + c];
 #pragma unroll
         for (int r = 0; r < kRows; ++r) {
           float a = 0.f;
 #pragma unroll
-          for (int wd = 0; wd < 4; ++wd) {
-            const uint32_t q = wq[r][wd];
-            const uint32_t t0 = (q & 0x000F000Fu) | 0x64006400u;          // 1024 + q0, 1024 + q4
-            const uint32_t t1 = (q & 0x00F000F0u) | 0x54005400u;          //   64 + q1,   64 + q5
-            const uint32_t t2 = (q & 0x0F000F00u) | 0x44004400u;          //    4 + q2,    4 + q6
-            const uint32_t t3 = ((q >> 8) & 0x00F000F0u) | 0x54005400u;   //   64 + q3,   64 + q7
-            a = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, t0), xv[4 * wd + 0], a, false);
-            a = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, t1), xv[4 * wd + 1], a, false);
-            a = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, t2), xv[4 * wd + 2], a, false);
-            a = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, t3), xv[4 * wd + 3], a, false);
-          }
-          acc[r][m] += s[r] * ((a - cs.x) - z[r] * cs.y);
+          for (int i = 0; i < 16; ++i) a = __builtin_amdgcn_fdot2(dq[r][i], xv[i], a, false);
+          acc[r][m] += s[r] * a;
         }
       }
     }
@@ -271,8 +272,8 @@ Plan make_plan(int64_t n, int64_t k, int64_t kgrain, size_t lds_per_grain, int64
 template <int M>
 hipError_t gemv_w4_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint16_t* scales,
                      const uint16_t* zeros, int64_t n, void* y, bool f16_out, hipStream_t stream) {
-  // per 128 k: 4 chunks x M x (64 B of permuted x + 8 B of (Xc, Xs))
-  const size_t lds_per_grain = (size_t)4 * M * 72;
+  // per 128 k: 4 chunks x M x 64 B of permuted x
+  const size_t lds_per_grain = (size_t)4 * M * 64;
   const Plan p = make_plan(n, k, 128, lds_per_grain, 512);
   float* partial = nullptr;
   if (p.splits > 1) {

@@ -75,7 +75,7 @@ __global__ __launch_bounds__(256) void quantize_int4_kernel(const uint16_t* __re
   } else {
     const double s16 = f16_ceil((hi - lo) / 15.0);
     double z = rint(-lo / s16);
-    z = z < 0.0 ? 0.0 : (z > 15.0 ? 15.0 : z);
+    z = z > 0.0 ? (z > 15.0 ? 15.0 : z) : 0.0;  // also maps -0.0 (lo == 0) to +0.0
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       double c = rint(v[i] / s16) + z;
