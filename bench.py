@@ -1,0 +1,299 @@
+#!/usr/bin/env python3
+"""SpecQuant round benchmark on one MI355X.
+
+A step is one speculative round of the hot path (SpecQuant SS III-D) on a
+synthetic Qwen2.5-shaped stack: k draft passes with the quantized draft copy
+(dequant GEMVs, then a draft-token draw each), one verify pass with the FP16
+parent (MFMA GEMMs at m = batch * (k + 1)), and the accept / resample step.
+Rounds are replayed from a captured HIP graph; the timed region is K rounds
+with the inputs resident in HBM.
+
+Prints one JSON line: tokens/s (emitted tokens = accepted drafts + 1 per
+sequence and round), the draft GEMV's achieved HBM bandwidth against the
+MI355X peak, and the CPU oracle timed on this host as a baseline.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
+METRIC = "draft+verify tokens/s at Qwen2.5-7B shape (k=4); INT4/FP8 GEMV HBM TB/s vs peak"
+GEMV_SRC = os.path.join(ROOT, "paper_2609_21704_amd", "csrc", "gemv.hip")
+
+
+def gemv_bytes(variant: str, m: int, n: int, k: int, out_bytes: int) -> float:
+    """Algorithmic bytes of one draft GEMV launch: weights + activations + outputs."""
+    w = n * k * 17 / 32 if variant == "int4" else n * k + 4 * n
+    return w + 2 * m * k + m * n * out_bytes
+
+
+def measure_gemv(rnd, steps: int):
+    """Per-launch durations of the draft GEMVs, timed with HIP events on the
+    launching stream.  A verify pass runs first so that the launches and
+    events are already queued when the GPU reaches them."""
+    import torch
+
+    cfg, st = rnd.cfg, rnd.stack
+    shapes = {}
+    for l, name, n, k in st.mats:
+        if name != "lm_head":
+            shapes[(l, name)] = (n, k, 2)
+        else:
+            shapes[(cfg.layers, name)] = (n, k, 4)
+    order = []
+    for l in range(st.layers):
+        for name, _, _ in cfg.layer_matrices():
+            order.append((l, name))
+    if cfg.lm_head:
+        order.append((cfg.layers, "lm_head"))
+    tot_bytes, tot_s, launches = 0.0, 0.0, 0
+    for i in range(steps):
+        events = []
+
+        def hook(start, events=events):
+            e = torch.cuda.Event(enable_timing=True)
+            e.record()
+            events.append(e)
+
+        rnd.verify()
+        rnd.draft_step(i % cfg.k, on_gemv=hook)
+        torch.cuda.synchronize()
+        for j, key in enumerate(order):
+            n, k, ob = shapes[key]
+            dt = events[2 * j].elapsed_time(events[2 * j + 1]) * 1e-3
+            tot_s += dt
+            tot_bytes += gemv_bytes(st.variant, cfg.draft_m, n, k, ob)
+            launches += 1
+    return tot_bytes, tot_s, launches
+
+
+def traffic_from_profile(variant: str):
+    """HBM bytes per draft-GEMV launch from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"gemv_{variant}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    sha = hashlib.sha256(open(GEMV_SRC, "rb").read()).hexdigest()
+    vals = {}
+    for line in open(path):
+        if "=" in line and not line.startswith("#"):
+            key, val = line.split("=", 1)
+            vals[key.strip()] = val.strip()
+    if vals.get("gemv_source_sha256") != sha:
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(rnd, tokens_per_round: float):
+    """The fp64 CPU oracle on this host: layers 0 and L-1 plus the LM head, one
+    full round of their work (k draft GEMVs, draws, verify GEMMs, accept),
+    extrapolated to the whole stack."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    cfg, st, b = rnd.cfg, rnd.stack, rnd.buf
+    T = rnd.temperature
+
+    def bits(t):
+        return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+    layers = sorted({0, st.layers - 1})
+    w16 = {}
+    packs = {}
+    for l in layers:
+        for name, _, _ in cfg.layer_matrices():
+            w16[(l, name)] = bits(st.w16[(l, name)])
+    if cfg.lm_head:
+        w16[(cfg.layers, "lm_head")] = bits(st.w16[(cfg.layers, "lm_head")])
+    for key, w in w16.items():  # the oracle's own draft copy (not timed)
+        packs[key] = oracle.quantize_int4_g128(w) if st.variant == "int4" else oracle.quantize_fp8_e4m3(w)
+    xd = {key: bits(t) for key, t in b.xd.items() if key[2] == "lm_head" or key[1] in layers}
+    xv = {key: bits(t) for key, t in b.xv.items() if key[1] == "lm_head" or key[0] in layers}
+
+    def gemv(key, x):
+        p = packs[key]
+        return oracle.qgemv_w4a16(x, *p)[0] if st.variant == "int4" else oracle.qgemv_w8a16(x, *p)[0]
+
+    eps = b.eps.cpu().numpy()
+    u_d = b.u_draft.cpu().numpy().view(np.uint32)
+    u_a = b.u_accept.cpu().numpy().view(np.uint32)
+    t_layer_draft = t_lm_draft = t_sample = t_layer_verify = t_lm_verify = t_accept = 0.0
+    B, k, V = cfg.batch, cfg.k, cfg.vocab
+    draft_logits = np.zeros((k, B, V), np.float32) if cfg.lm_head else b.draft_logits.cpu().numpy()
+    tokens = np.zeros((k, B), np.int32)
+    for i in range(k):
+        for l in layers:
+            t0 = time.perf_counter()
+            for name, _, _ in cfg.layer_matrices():
+                gemv((l, name), xd[(i, l, name)])
+            t_layer_draft += (time.perf_counter() - t0) / len(layers)
+        if cfg.lm_head:
+            t0 = time.perf_counter()
+            draft_logits[i] = gemv((cfg.layers, "lm_head"), xd[(i, st.layers, "lm_head")]).astype(np.float32)
+            t_lm_draft += time.perf_counter() - t0
+        t0 = time.perf_counter()
+        _, nxt, _, _ = oracle.spec_accept(None, draft_logits[i].reshape(B, 1, V), None,
+                                          u_d[i].reshape(B, 1), T)
+        t_sample += time.perf_counter() - t0
+        tokens[i] = nxt
+    for l in layers:
+        t0 = time.perf_counter()
+        for name, _, _ in cfg.layer_matrices():
+            oracle.gemm_f16(xv[(l, name)], w16[(l, name)])
+        t_layer_verify += (time.perf_counter() - t0) / len(layers)
+    target = np.zeros((B, k + 1, V), np.float32)
+    if cfg.lm_head:
+        t0 = time.perf_counter()
+        y = oracle.gemm_f16(xv[(st.layers, "lm_head")], w16[(cfg.layers, "lm_head")])[0]
+        t_lm_verify = time.perf_counter() - t0
+        target[:, k] = y.reshape(B, k + 1, V)[:, k]
+    target[:, :k] = draft_logits.transpose(1, 0, 2) + eps
+    t0 = time.perf_counter()
+    oracle.spec_accept(draft_logits, target, tokens, u_a, T)
+    t_accept = time.perf_counter() - t0
+    round_s = (k * (cfg.layers * t_layer_draft + t_lm_draft + t_sample)
+               + cfg.layers * t_layer_verify + t_lm_verify + t_accept)
+    measured = (k * (len(layers) * t_layer_draft + t_lm_draft + t_sample)
+                + len(layers) * t_layer_verify + t_lm_verify + t_accept)
+    return {
+        "value": round(tokens_per_round * cfg.batch / round_s, 4),
+        "unit": "tokens/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": (f"layers {layers} of {cfg.layers} (4 projections each) and the LM head: one round of their "
+                   f"draft GEMVs, draws, verify GEMMs and the accept step, timed in {measured:.1f} s and "
+                   f"extrapolated to {cfg.layers} layers ({round_s:.1f} s per round)"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20, help="timed rounds")
+    ap.add_argument("--warmup", type=int, default=3, help="untimed rounds")
+    ap.add_argument("--config", type=int, default=2, help="workload index (2 = Qwen2.5-7B-shaped, INT4, k=4)")
+    ap.add_argument("--temperature", type=float, default=1.0)
+    ap.add_argument("--gemv-steps", type=int, default=2, help="draft passes timed per launch for the roofline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-only", action="store_true",
+                    help="run warmup rounds and one eager draft pass, print nothing (for rocprofv3 counters)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: every box here has a single MI355X, and the SpecQuant hot path "
+              f"is built and timed on one GPU (requested --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_21704_amd.configs import CONFIGS
+    from paper_2609_21704_amd.rounds import Round, Stack, round_uniforms
+
+    cfg = CONFIGS[args.config]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stack = Stack(cfg, dev)
+    rnd = Round(stack, temperature=args.temperature)
+    total = args.warmup + args.steps
+    ud, ua = round_uniforms(cfg, total, dev)
+    n_hist = torch.zeros((total, cfg.batch), dtype=torch.int32, device=dev)
+    rnd.set_uniforms(ud[0], ua[0])
+    rnd.capture()  # one eager round first (library workspace), then the graph
+
+    def one(r):
+        rnd.set_uniforms(ud[r], ua[r])
+        rnd.replay()
+        n_hist[r].copy_(rnd.buf.n_accepted)
+
+    for r in range(args.warmup):
+        one(r)
+    torch.cuda.synchronize()
+    if args.profile_only:
+        rnd.draft_step(0)
+        torch.cuda.synchronize()
+        return
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for r in range(args.warmup, total):
+        one(r)
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    elapsed = e0.elapsed_time(e1) * 1e-3
+    n_acc = n_hist[args.warmup:].cpu().numpy().astype(np.int64)
+    tokens = int((n_acc + 1).sum())
+    tokens_per_round = tokens / (args.steps * cfg.batch)
+
+    gbytes, gsec, glaunch = measure_gemv(rnd, args.gemv_steps)
+    achieved = gbytes / gsec / 1e9
+    traffic = traffic_from_profile(stack.variant)
+
+    out = {
+        "metric": METRIC,
+        "value": round(tokens / elapsed, 3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic (seeded random weights and activations; no trained weights or datasets)",
+        "config": {
+            "workload": cfg.describe(),
+            "draft_variant": stack.variant,
+            "k": cfg.k,
+            "batch": cfg.batch,
+            "draft_m": cfg.draft_m,
+            "verify_m": cfg.verify_m,
+            "vocab": cfg.vocab,
+            "temperature": args.temperature,
+            "graph": True,
+        },
+        "rounds_per_s": round(args.steps / elapsed, 3),
+        "tokens_per_round": round(tokens_per_round, 4),
+        "acceptance_rate": round(float(n_acc.sum()) / (args.steps * cfg.batch * cfg.k), 4),
+        "round_bytes": cfg.round_bytes(),
+        "stack_gbs": round(cfg.round_bytes() * args.steps / elapsed / 1e9, 1),
+        "wall_s": round(wall, 4),
+        "roofline": {
+            "kernel": f"draft GEMV ({'W4A16' if stack.variant == 'int4' else 'W8A16'}, m={cfg.draft_m})",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "launches_timed": glaunch,
+            "avg_launch_us": round(gsec / glaunch * 1e6, 3),
+            "algorithmic_bytes_per_launch": round(gbytes / glaunch, 1),
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(rnd, tokens_per_round)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -136,10 +136,11 @@ sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint
  * draft_logits  [kd][b][v] f32 (position-major: one draft step for all b;
  *               may be NULL when kd == 0)
  * target_logits [b][kd+1][v] f32 (sequence-major: the parent's verify rows)
- * draft_tokens  [b][kd] int32 (NULL allowed when kd == 0)
+ * draft_tokens  [kd][b] int32 (position-major like draft_logits; NULL allowed
+ *               when kd == 0)
  * u24           [b][kd+1] uint32
  * n_accepted [b] int32 out; next_token [b] int32 out.  The emitted tokens of
- *   sequence s are draft_tokens[s][0 .. n_accepted[s]) then next_token[s].
+ *   sequence s are draft_tokens[0 .. n_accepted[s])[s] then next_token[s].
  * q_out [kd][b][v] f32, p_out [b][kd+1][v] f32: optional (nullable) copies of
  *   the distributions, T > 0 only.
  * Limits: 1 <= b <= 2^24, 0 <= kd <= 64, 1 <= v <= 2^26,

@@ -213,7 +213,7 @@ def spec_accept(draft_logits, target_logits, draft_tokens, u24, temperature: flo
     """Speculative accept / resample.
 
     draft_logits [kd][b][v] f32, target_logits [b][kd+1][v] f32,
-    draft_tokens [b][kd] i32, u24 [b][kd+1] u32 (low 24 bits used).
+    draft_tokens [kd][b] i32, u24 [b][kd+1] u32 (low 24 bits used).
     Returns (n_accepted [b], next_token [b], q [kd][b][v] | None, p [b][kd+1][v] | None).
     """
     target_logits = np.ascontiguousarray(target_logits, np.float32)
@@ -221,7 +221,7 @@ def spec_accept(draft_logits, target_logits, draft_tokens, u24, temperature: flo
     kd = kd1 - 1
     if kd > 0:
         draft_logits = np.ascontiguousarray(draft_logits, np.float32).reshape(kd, b, v)
-        draft_tokens = np.ascontiguousarray(draft_tokens, np.int32).reshape(b, kd)
+        draft_tokens = np.ascontiguousarray(draft_tokens, np.int32).reshape(kd, b)
     else:
         draft_logits = None
         draft_tokens = None

@@ -385,7 +385,8 @@ static int64_t draw_fixed_point(const double* r, int64_t v, uint32_t u24) {
 /* Speculative acceptance for b sequences with kd drafted tokens each.
  *   draft_logits  [kd][b][v]    (position-major: one draft step for all b)
  *   target_logits [b][kd+1][v]  (sequence-major: the parent's verify rows)
- *   draft_tokens  [b][kd], u24 [b][kd+1] (low 24 bits used; u = u24 / 2^24)
+ *   draft_tokens  [kd][b] (position-major), u24 [b][kd+1] (low 24 bits used;
+ *   u = u24 / 2^24)
  * T > 0: accept position i iff u_i * q_i(x_i) < p_i(x_i); n = first rejection
  * (kd if none); at a rejection draw from max(0, p_n - q_n) renormalised (p_n
  * if that mass rounds to zero), otherwise draw the bonus token from p_kd; the
@@ -410,7 +411,7 @@ int sqo_spec_accept(const float* draft_logits, const float* target_logits, const
     if (temperature == 0.0) {
       int32_t n = kd;
       for (int32_t i = 0; i < kd; ++i) {
-        int32_t x = draft_tokens[(int64_t)s * kd + i];
+        int32_t x = draft_tokens[(int64_t)i * b + s];
         if (x < 0 || x >= v || (int64_t)x != argmax_row(tgt + (int64_t)i * v, v)) {
           n = i;
           break;
@@ -427,7 +428,7 @@ int sqo_spec_accept(const float* draft_logits, const float* target_logits, const
       softmax_row(draft_logits + ((int64_t)i * b + s) * v, v, temperature, q + (int64_t)i * v);
     int32_t n = kd;
     for (int32_t i = 0; i < kd; ++i) {
-      int32_t x = draft_tokens[(int64_t)s * kd + i];
+      int32_t x = draft_tokens[(int64_t)i * b + s];
       double u = ldexp((double)(u24[(int64_t)s * (kd + 1) + i] & 0xFFFFFFu), -24);
       int accept = 0;
       if (x >= 0 && x < v) accept = (u * q[(int64_t)i * v + x] < p[(int64_t)i * v + x]);

@@ -203,7 +203,7 @@ def sq_spec_accept(draft_logits, target_logits, draft_tokens, u24, temperature: 
     """Speculative accept / resample.
 
     draft_logits [kd][b][v] f32 (None when kd == 0), target_logits [b][kd+1][v] f32,
-    draft_tokens [b][kd] int32, u24 [b][kd+1] int32 holding uint32 bit patterns
+    draft_tokens [kd][b] int32, u24 [b][kd+1] int32 holding uint32 bit patterns
     (low 24 bits used).  Returns (n_accepted [b] int32, next_token [b] int32).
     """
     b, kd1, v = target_logits.shape
@@ -217,7 +217,7 @@ def sq_spec_accept(draft_logits, target_logits, draft_tokens, u24, temperature: 
     if draft_logits is not None and draft_logits.numel() != kd * b * v:
         raise ValueError("draft_logits must be [kd][b][v]")
     if draft_tokens is not None and (draft_tokens.dtype != torch.int32 or draft_tokens.numel() != b * kd):
-        raise ValueError("draft_tokens must be int32 [b][kd]")
+        raise ValueError("draft_tokens must be int32 [kd][b]")
     if u24 is not None and (u24.dtype != torch.int32 or u24.numel() != b * (kd + 1)):
         raise ValueError("u24 must be int32 [b][kd+1]")
     _expect(n_accepted, torch.int32, (b,), "n_accepted")

@@ -4,7 +4,9 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <map>
 #include <mutex>
+#include <tuple>
 
 #include "sq_internal.hpp"
 #include "specquant.h"
@@ -21,8 +23,37 @@ struct Workspace {
 
 std::mutex g_ws_mutex;
 Workspace g_ws[kMaxDevices];
+int g_cus[kMaxDevices];
 
 }  // namespace
+
+int resident_blocks(const void* kernel, int threads, size_t lds) {
+  static std::mutex mu;
+  static std::map<std::tuple<const void*, int, size_t>, int> cache;
+  const auto key = std::make_tuple(kernel, threads, lds);
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  int blocks = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, kernel, threads, lds) != hipSuccess || blocks < 1) {
+    (void)hipGetLastError();
+    blocks = 1;
+  }
+  cache[key] = blocks;
+  return blocks;
+}
+
+int cu_count() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+  std::lock_guard<std::mutex> lock(g_ws_mutex);
+  if (g_cus[dev] <= 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
+    g_cus[dev] = cus;
+  }
+  return g_cus[dev];
+}
 
 void* workspace(size_t bytes) {
   int dev = -1;

@@ -162,7 +162,7 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(const float* __restric
   __syncthreads();
   if (threadIdx.x < kd) {
     const int i = threadIdx.x;
-    const int32_t xt = tokens[(int64_t)s * kd + i];
+    const int32_t xt = tokens[(int64_t)i * b + s];
     int acc = 0;
     if (xt >= 0 && xt < v) {
       const double p = exp(zval(target[((int64_t)s * (kd + 1) + i) * v + xt], temp) - sL[i]) / sS[i];
@@ -376,7 +376,7 @@ __global__ __launch_bounds__(kThreads) void argmax_kernel(const float* __restric
   }
 }
 
-__global__ __launch_bounds__(kThreads) void greedy_kernel(const int32_t* __restrict__ tokens, int kd, int v,
+__global__ __launch_bounds__(kThreads) void greedy_kernel(const int32_t* __restrict__ tokens, int b, int kd, int v,
                                                           int nchunk, const ArgMax* __restrict__ am,
                                                           int32_t* __restrict__ n_accepted,
                                                           int32_t* __restrict__ next_token) {
@@ -397,7 +397,7 @@ __global__ __launch_bounds__(kThreads) void greedy_kernel(const int32_t* __restr
   if (threadIdx.x == 0) {
     int n = kd;
     for (int i = 0; i < kd; ++i) {
-      const int32_t xt = tokens[(int64_t)s * kd + i];
+      const int32_t xt = tokens[(int64_t)i * b + s];
       if (xt < 0 || xt >= v || xt != sArg[i]) {
         n = i;
         break;
@@ -420,7 +420,7 @@ hipError_t launch_spec_accept(const float* draft, const float* target, const int
     if (!am) return hipErrorOutOfMemory;
     hipLaunchKernelGGL(argmax_kernel, dim3((unsigned)(rows_t * nchunk)), dim3(kThreads), 0, stream, target, v, nchunk,
                        am);
-    hipLaunchKernelGGL(greedy_kernel, dim3((unsigned)b), dim3(kThreads), 0, stream, tokens, kd, v, nchunk, am,
+    hipLaunchKernelGGL(greedy_kernel, dim3((unsigned)b), dim3(kThreads), 0, stream, tokens, b, kd, v, nchunk, am,
                        n_accepted, next_token);
     return hipGetLastError();
   }

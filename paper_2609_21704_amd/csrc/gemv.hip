@@ -2,228 +2,378 @@
 // produces the speculative tokens; every draft step streams the whole
 // quantized stack once at m = 1 .. 8 activation rows).
 //
-// The kernels are HBM-bound: each weight byte is read exactly once, with
-// 16-byte loads that are contiguous across the lanes of a wavefront.  The
-// activations of the workgroup's K range are staged once in LDS; each lane
-// reads its x chunk from LDS once per chunk position and reuses it for the
-// four rows its wavefront streams together.
+// The kernels are HBM-bound: each weight byte is read once, with 16-byte
+// loads, 32 contiguous bytes per lane per row.  A task is a block of four
+// rows; one step of a task is 64 lanes x 32 bytes of each of its rows.  The
+// grid is persistent: a workgroup stages the activations of its K range in
+// LDS once and walks tasks; its NW wavefronts (NW = min(4, steps per task))
+// split each task's steps, fetching their next step while computing the
+// current one, so every CU keeps ~16 wavefronts x 16 KB of codes in flight.
+// Row sums are reduced across a wavefront with DPP and across the
+// workgroup's wavefronts through LDS, in a fixed order.
 //
-// INT4 (W4A16).  A 16-byte load holds 32 consecutive 4-bit codes of one row,
-// i.e. a quarter of one 128-element group.  Each 32-bit word (codes of k..k+7)
-// is turned into four half2 values without a conversion instruction: a nibble
+// INT4 (W4A16).  A lane's 32 bytes are 64 consecutive 4-bit codes of one row,
+// i.e. half of one 128-element group.  Each 32-bit word (codes of k..k+7) is
+// turned into four half2 values without a conversion instruction: a nibble
 // masked into mantissa bits 0-3 (or 4-7) of the binary16 constant 1024 (or
-// 64) is the exact value 1024 + q (or 64 + q); one shift by 8 serves the
-// upper nibble pairs.  Subtracting the packed constant c + z in fp16 is exact
-// and leaves q - z in [-15, 15], so v_dot2_f32_f16 forms exact products
+// 64) is the exact value 1024 + q (or 64 + q); one shift by 8 serves the upper
+// nibble pairs.  Subtracting the packed constant c + z in fp16 is exact and
+// leaves q - z in [-15, 15], so v_dot2_f32_f16 forms exact products
 // (q - z) * x and the fp32 accumulation error is bounded by sum |(q - z) x|;
-// the group scale multiplies the chunk sum once.  Per word: one shift, four
-// and-or, four packed subtracts, four dot2 -- 1.6 VALU operations per weight
-// at m = 1.
+// the group scale multiplies the half-group sum once.  Per word: one shift,
+// four and-or, four packed subtracts, four dot2 -- 1.6 VALU operations per
+// weight at m = 1.
 //
-// FP8 (W8A16).  A 16-byte load holds 16 E4M3 codes; v_cvt_scalef32_pk_f16_fp8
-// converts two codes to two exact binary16 values, v_dot2_f32_f16 accumulates,
-// and the per-row fp32 scale is applied once after the reduction.
+// FP8 (W8A16).  A lane's 32 bytes are 32 E4M3 codes; v_cvt_scalef32_pk_f16_fp8
+// converts two codes to two exact binary16 values, v_dot2_f32_f16
+// accumulates, and the per-row fp32 scale is applied once after the reduction.
 #include "sq_device.hpp"
 #include "sq_internal.hpp"
 
 namespace sq {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / kWave;
-constexpr int kRows = 4;                    // rows streamed together by one wavefront
-constexpr size_t kLdsBudget = 64 * 1024;    // bytes of LDS one workgroup may use
+// rows of a task: four for m <= 2; two for larger m, where the activation
+// fragments need the registers
+constexpr int rows_for(int m) { return m <= 2 ? 4 : 2; }
+constexpr int kLaneBytes = 32;              // code bytes per lane per row and step
+constexpr size_t kLdsBudget = 64 * 1024;    // activation bytes one workgroup may stage
+#ifndef SQ_GEMV_WAVES_PER_CU
+#define SQ_GEMV_WAVES_PER_CU 16             // resident wavefronts per CU in the persistent grid
+#endif
 
-// ----------------------------------------------------------------- INT4 ----
-// LDS layout for a K slice of nchunk 32-element chunks (consecutive chunks,
-// which consecutive lanes read, are consecutive 16-byte cells):
-//   xs [M][4 words][nchunk][8 halves], halves of word w in the order
-//      x[8w+0], x[8w+4], x[8w+1], x[8w+5], x[8w+2], x[8w+6], x[8w+3], x[8w+7]
-// matching the nibble pairs (0,4), (1,5), (2,6), (3,7) of a code word.
-template <int M>
-__device__ __forceinline__ void stage_x_w4(const uint16_t* __restrict__ x, int64_t k, int64_t k0, int nchunk,
-                                           half_t* xs) {
-  for (int idx = threadIdx.x; idx < nchunk * M * 4; idx += kThreads) {
-    const int c = idx / (M * 4), rem = idx % (M * 4), m = rem >> 2, wd = rem & 3;
-    const u32x4 raw = *reinterpret_cast<const u32x4*>(x + (int64_t)m * k + k0 + 32 * c + 8 * wd);
-    half_t e[8];
+template <int Ctrl>
+__device__ __forceinline__ float dpp_add(float v) {
+  return v + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), Ctrl, 0xF, 0xF,
+                                                                   false));
+}
+
+// Sums of V = 4T values across the 64 lanes of a wavefront, transposed: the
+// lane halves are folded with v_permlane32_swap, the row pairs with
+// v_permlane16_swap, and the 16-lane rows with DPP, 2.5 operations per value.
+// Afterwards every lane of row j of w[t] holds the total of value
+// 4t + (0, 2, 1, 3)[j].
+template <int T>
+__device__ __forceinline__ void wave_sums(const float (&v)[4 * T], float (&w)[T]) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) e[i] = __builtin_bit_cast(half_t, (uint16_t)(raw[i >> 1] >> (16 * (i & 1))));
-    const half8_t p = {e[0], e[4], e[1], e[5], e[2], e[6], e[3], e[7]};
-    *reinterpret_cast<half8_t*>(xs + (((size_t)m * 4 + wd) * nchunk + c) * 8) = p;
+  for (int t = 0; t < T; ++t) {
+    float u[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const auto p = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(int, v[4 * t + 2 * h]),
+                                                      __builtin_bit_cast(int, v[4 * t + 2 * h + 1]), false, false);
+      const int p0 = p[0], p1 = p[1];  // bit-cast scalar copies: vector element lvalues are misread
+      u[h] = __builtin_bit_cast(float, p0) + __builtin_bit_cast(float, p1);
+    }
+    const auto q = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(int, u[0]), __builtin_bit_cast(int, u[1]),
+                                                    false, false);
+    const int q0 = q[0], q1 = q[1];
+    float x = __builtin_bit_cast(float, q0) + __builtin_bit_cast(float, q1);
+    x = dpp_add<0xB1>(x);   // quad_perm [1,0,3,2]
+    x = dpp_add<0x4E>(x);   // quad_perm [2,3,0,1]
+    x = dpp_add<0x141>(x);  // row_half_mirror
+    x = dpp_add<0x140>(x);  // row_mirror: every lane holds its row's total
+    w[t] = x;
   }
 }
 
-template <int M, bool F16Out>
-__global__ __launch_bounds__(kThreads) void gemv_w4_kernel(const uint16_t* __restrict__ x, int64_t k, int64_t kslice,
-                                                           const uint8_t* __restrict__ codes,
-                                                           const uint16_t* __restrict__ scales,
-                                                           const uint16_t* __restrict__ zeros, int64_t n,
-                                                           void* __restrict__ y, float* __restrict__ partial) {
+template <int R>
+struct Frag {
+  u32x4 c[R][2];
+  uint32_t s[R];  // INT4 group scale bits
+  uint32_t z[R];  // INT4 group zero bits
+};
+
+// Where a task's rows start.  The last task may hold fewer than R rows:
+// its extra rows read row n - 1 again and are never stored.
+struct TaskPtr {
+  const uint8_t* codes;   // row0's codes at the slice start
+  const uint16_t* scales; // row0's group scales at the slice start (INT4)
+  const uint16_t* zeros;
+  int last;               // index of the task's last real row (0 .. R-1)
+};
+
+template <bool W8, int R>
+__device__ __forceinline__ TaskPtr task_ptr(const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
+                                            const uint16_t* __restrict__ zeros, int64_t n, int64_t k, int64_t k0,
+                                            int64_t task) {
+  TaskPtr t;
+  const int64_t row0 = task * R;
+  const int64_t left = n - 1 - row0;
+  t.last = left < R - 1 ? (int)left : R - 1;
+  t.codes = codes + row0 * (W8 ? k : (k >> 1)) + (W8 ? k0 : (k0 >> 1));
+  t.scales = W8 ? nullptr : scales + row0 * (k >> 7) + (k0 >> 7);
+  t.zeros = W8 ? nullptr : zeros + row0 * (k >> 7) + (k0 >> 7);
+  return t;
+}
+
+// Codes of a task's rows for the lane's chunk of step `it`.  The loads are
+// unconditional: a lane past the end of the slice reads the slice's last chunk
+// again (its contribution is dropped in the compute), and an FP8 slice that
+// ends on half a chunk (k % 32 == 16) reads its first 16 bytes twice; the
+// copy meets zero activations in LDS.
+template <bool W8, int R>
+__device__ __forceinline__ Frag<R> load_frag(const TaskPtr& t, int row_bytes, int groups, int64_t kl, int nchunk,
+                                             int it, int lane) {
+  Frag<R> f;
+  int chunk = it * kWave + lane;
+  chunk = chunk < nchunk ? chunk : nchunk - 1;
+  const bool hi = W8 ? (chunk * 32 + 16 < kl) : true;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int rr = r < t.last ? r : t.last;
+    const u32x4* p = reinterpret_cast<const u32x4*>(t.codes + rr * row_bytes + chunk * kLaneBytes);
+    f.c[r][0] = p[0];
+    f.c[r][1] = p[hi ? 1 : 0];
+    if constexpr (!W8) {
+      const int gi = rr * groups + (chunk >> 1);
+      f.s[r] = t.scales[gi];
+      f.z[r] = t.zeros[gi];
+    } else {
+      f.s[r] = 0u;
+      f.z[r] = 0u;
+    }
+  }
+  return f;
+}
+
+// INT4 LDS layout for a K slice of nchunk 64-element chunks (lane-consecutive
+// chunks are consecutive 16-byte cells): xs [M][8 words][nchunk][8 halves],
+// halves of word w in the order x[8w+0], x[8w+4], x[8w+1], x[8w+5], x[8w+2],
+// x[8w+6], x[8w+3], x[8w+7] -- the nibble pairs of a code word.
+// FP8 layout: xs [M][4 cells][nchunk][8 halves] in natural order.
+template <int M, bool W8, int NThreads>
+__device__ __forceinline__ void stage_x(const uint16_t* __restrict__ x, int64_t k, int64_t k0, int64_t kl, int nchunk,
+                                        half_t* xs) {
+  constexpr int kCells = W8 ? 4 : 8;  // 16-byte cells of x per chunk and row
+  for (int idx = threadIdx.x; idx < nchunk * M * kCells; idx += NThreads) {
+    const int c = idx / (M * kCells), rem = idx % (M * kCells), m = rem / kCells, w = rem % kCells;
+    const int64_t kk = (int64_t)c * (W8 ? 32 : 64) + 8 * w;
+    const u32x4 raw = kk < kl ? *reinterpret_cast<const u32x4*>(x + (int64_t)m * k + k0 + kk) : u32x4{0u, 0u, 0u, 0u};
+    u32x4 out = raw;
+    if constexpr (!W8) {
+      // halves (x0,x1),(x2,x3),(x4,x5),(x6,x7) -> (x0,x4),(x1,x5),(x2,x6),(x3,x7)
+      out[0] = __builtin_amdgcn_perm(raw[2], raw[0], 0x05040100u);
+      out[1] = __builtin_amdgcn_perm(raw[2], raw[0], 0x07060302u);
+      out[2] = __builtin_amdgcn_perm(raw[3], raw[1], 0x05040100u);
+      out[3] = __builtin_amdgcn_perm(raw[3], raw[1], 0x07060302u);
+    }
+    *reinterpret_cast<u32x4*>(xs + (((size_t)m * kCells + w) * nchunk + c) * 8) = out;
+  }
+}
+
+template <int M, bool W8, int NW>
+__global__ __launch_bounds__(NW * 64) void gemv_kernel(const uint16_t* __restrict__ x, int64_t k, int64_t kslice,
+                                                       const uint8_t* __restrict__ codes,
+                                                       const uint16_t* __restrict__ scales16,
+                                                       const uint16_t* __restrict__ zeros16,
+                                                       const float* __restrict__ scales32, int64_t n,
+                                                       void* __restrict__ y, int f16_out,
+                                                       float* __restrict__ partial) {
   extern __shared__ __align__(16) char smem[];
+  constexpr int kCells = W8 ? 4 : 8;
+  constexpr int R = rows_for(M);
+  constexpr int kChunkK = W8 ? 32 : 64;  // weights per 32-byte lane chunk
   const int split = blockIdx.y;
   const int64_t k0 = (int64_t)split * kslice;
   const int64_t kl = (k - k0) < kslice ? (k - k0) : kslice;
-  const int nchunk = (int)(kl / 32);
-  half_t* xs = reinterpret_cast<half_t*>(smem);
-  stage_x_w4<M>(x, k, k0, nchunk, xs);
-  __syncthreads();
-
+  const int nchunk = (int)((kl + kChunkK - 1) / kChunkK);
+  const int nit = (nchunk + kWave - 1) / kWave;  // >= NW by the host's choice of NW
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t groups = k / 128;
-  const int64_t nquads = (n + kRows - 1) / kRows;
-  for (int64_t quad = (int64_t)blockIdx.x * kWaves + wave; quad < nquads; quad += (int64_t)gridDim.x * kWaves) {
-    const int64_t r0 = quad * kRows;
-    float acc[kRows][M];
-#pragma unroll
-    for (int r = 0; r < kRows; ++r)
-#pragma unroll
-      for (int m = 0; m < M; ++m) acc[r][m] = 0.f;
+  const int64_t ntask = (n + R - 1) / R;
+  int64_t task = blockIdx.x;
+  int it = wave;
+  half_t* xs = reinterpret_cast<half_t*>(smem);
+  float* red = reinterpret_cast<float*>(smem + (size_t)M * kCells * nchunk * 16);  // [NW][R][M]
 
-    for (int c = lane; c < nchunk; c += kWave) {
-      const int64_t kc = k0 + 32 * (int64_t)c;
-      const int64_t g = kc >> 7;
-      u32x4 wq[kRows];
-      uint32_t zb[kRows];
-      float s[kRows];
+  const int row_bytes = (int)(W8 ? k : (k >> 1));
+  const int groups = (int)(k >> 7);
+
+  // the first fragment is in flight while the activations are staged
+  Frag<R> fa, fb;
+  TaskPtr tp = task_ptr<W8, R>(codes, scales16, zeros16, n, k, k0, task < ntask ? task : ntask - 1);
+  fa = load_frag<W8, R>(tp, row_bytes, groups, kl, nchunk, it, lane);
+  stage_x<M, W8, NW * 64>(x, k, k0, kl, nchunk, xs);
+  __syncthreads();
+  if (task >= ntask) return;  // uniform across the workgroup
+
+  // masks and magic numbers in VGPRs, so each mask-and-insert is one v_and_or_b32
+  uint32_t mlo = 0x000F000Fu, mhi = 0x00F000F0u, k1024 = 0x64006400u, k64 = 0x54005400u;
+  asm("" : "+v"(mlo), "+v"(mhi), "+v"(k1024), "+v"(k64));
+
+  float acc[R][M];
 #pragma unroll
-      for (int r = 0; r < kRows; ++r) {
-        const int64_t row = (r0 + r) < n ? (r0 + r) : (n - 1);
-        wq[r] = *reinterpret_cast<const u32x4*>(codes + row * (k >> 1) + (kc >> 1));
-        s[r] = f16_bits_to_f32(scales[row * groups + g]);
-        zb[r] = zeros[row * groups + g];
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int m = 0; m < M; ++m) acc[r][m] = 0.f;
+
+  // One step (task, it): fetch this wavefront's next step into `nxt`, then
+  // consume `cur`; after the task's last step the row sums are finished.
+  // Returns false when the workgroup has no tasks left.
+  auto step = [&](const Frag<R>& cur, Frag<R>& nxt) -> bool {
+    int64_t task_n = task;
+    int it_n = it + NW;
+    if (it_n >= nit) {
+      it_n = wave;
+      task_n = task + gridDim.x;
+    }
+    const TaskPtr tp_n = task_n == task ? tp : task_ptr<W8, R>(codes, scales16, zeros16, n, k, k0,
+                                                             task_n < ntask ? task_n : ntask - 1);
+    nxt = load_frag<W8, R>(tp_n, row_bytes, groups, kl, nchunk, it_n, lane);
+
+    const int chunk = it * kWave + lane;
+    const bool ok = chunk < nchunk;
+    const int cc = ok ? chunk : nchunk - 1;
+    float a[R][M];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int m = 0; m < M; ++m) a[r][m] = 0.f;
+
+    if constexpr (!W8) {
+      half2_t c1024[R], c64[R];
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const uint32_t zb = cur.z[r];
+        const half2_t z2 = __builtin_bit_cast(half2_t, zb | (zb << 16));
+        c1024[r] = z2 + half2_t{(half_t)1024.0f, (half_t)1024.0f};
+        c64[r] = z2 + half2_t{(half_t)64.0f, (half_t)64.0f};
       }
-      // (q - z) as exact half2 values for the 4 words of each row.  The masks
-      // and magic constants live in VGPRs so that each mask-and-insert is a
-      // single v_and_or_b32 (a VOP3 encoding cannot carry two literals).
-      uint32_t mlo = 0x000F000Fu, mhi = 0x00F000F0u, k1024 = 0x64006400u, k64 = 0x54005400u;
-      asm("" : "+v"(mlo), "+v"(mhi), "+v"(k1024), "+v"(k64));
-      half2_t dq[kRows][16];
 #pragma unroll
-      for (int r = 0; r < kRows; ++r) {
-        const half2_t z2 = __builtin_bit_cast(half2_t, zb[r] | (zb[r] << 16));
-        const half2_t c1024 = z2 + half2_t{(half_t)1024.0f, (half_t)1024.0f};
-        const half2_t c64 = z2 + half2_t{(half_t)64.0f, (half_t)64.0f};
+      for (int w = 0; w < 8; ++w) {
+        half2_t xw[M][4];
 #pragma unroll
-        for (int wd = 0; wd < 4; ++wd) {
-          const uint32_t q = wq[r][wd];
+        for (int m = 0; m < M; ++m) {
+          const u32x4 v = *reinterpret_cast<const u32x4*>(xs + (((size_t)m * kCells + w) * nchunk + cc) * 8);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const uint32_t e = v[i];  // bit-cast a scalar copy: the element lvalue itself is misread
+            xw[m][i] = __builtin_bit_cast(half2_t, e);
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          const uint32_t q = cur.c[r][w >> 2][w & 3];
           const uint32_t q8 = q >> 8;
-          dq[r][4 * wd + 0] = __builtin_bit_cast(half2_t, (q & mlo) | k1024) - c1024;   // q0, q4
-          dq[r][4 * wd + 1] = __builtin_bit_cast(half2_t, (q & mhi) | k64) - c64;       // q1, q5
-          dq[r][4 * wd + 2] = __builtin_bit_cast(half2_t, (q8 & mlo) | k1024) - c1024;  // q2, q6
-          dq[r][4 * wd + 3] = __builtin_bit_cast(half2_t, (q8 & mhi) | k64) - c64;      // q3, q7
+          const half2_t d0 = __builtin_bit_cast(half2_t, (q & mlo) | k1024) - c1024[r];   // q0 - z, q4 - z
+          const half2_t d1 = __builtin_bit_cast(half2_t, (q & mhi) | k64) - c64[r];       // q1 - z, q5 - z
+          const half2_t d2 = __builtin_bit_cast(half2_t, (q8 & mlo) | k1024) - c1024[r];  // q2 - z, q6 - z
+          const half2_t d3 = __builtin_bit_cast(half2_t, (q8 & mhi) | k64) - c64[r];      // q3 - z, q7 - z
+#pragma unroll
+          for (int m = 0; m < M; ++m) {
+            float t = a[r][m];
+            t = __builtin_amdgcn_fdot2(d0, xw[m][0], t, false);
+            t = __builtin_amdgcn_fdot2(d1, xw[m][1], t, false);
+            t = __builtin_amdgcn_fdot2(d2, xw[m][2], t, false);
+            t = __builtin_amdgcn_fdot2(d3, xw[m][3], t, false);
+            a[r][m] = t;
+          }
         }
       }
 #pragma unroll
-      for (int m = 0; m < M; ++m) {
-        half2_t xv[16];
+      for (int r = 0; r < R; ++r) {
+        const float s = ok ? f16_bits_to_f32((uint16_t)cur.s[r]) : 0.f;  // a lane past the end adds 0
 #pragma unroll
-        for (int wd = 0; wd < 4; ++wd) {
-          const half2_t* xp = reinterpret_cast<const half2_t*>(xs + (((size_t)m * 4 + wd) * nchunk + c) * 8);
+        for (int m = 0; m < M; ++m) acc[r][m] += s * a[r][m];
+      }
+    } else {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) xv[4 * wd + i] = xp[i];
+      for (int cell = 0; cell < 4; ++cell) {
+        half2_t xw[M][4];
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+          const u32x4 v = *reinterpret_cast<const u32x4*>(xs + (((size_t)m * kCells + cell) * nchunk + cc) * 8);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const uint32_t e = v[i];  // bit-cast a scalar copy: the element lvalue itself is misread
+            xw[m][i] = __builtin_bit_cast(half2_t, e);
+          }
         }
 #pragma unroll
-        for (int r = 0; r < kRows; ++r) {
-          float a = 0.f;
+        for (int r = 0; r < R; ++r) {
+          const uint32_t q0 = cur.c[r][cell >> 1][2 * (cell & 1)];
+          const uint32_t q1 = cur.c[r][cell >> 1][2 * (cell & 1) + 1];
+          const half2_t w0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(q0, 1.0f, false);
+          const half2_t w1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(q0, 1.0f, true);
+          const half2_t w2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(q1, 1.0f, false);
+          const half2_t w3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(q1, 1.0f, true);
 #pragma unroll
-          for (int i = 0; i < 16; ++i) a = __builtin_amdgcn_fdot2(dq[r][i], xv[i], a, false);
-          acc[r][m] += s[r] * a;
+          for (int m = 0; m < M; ++m) {
+            float t = a[r][m];
+            t = __builtin_amdgcn_fdot2(w0, xw[m][0], t, false);
+            t = __builtin_amdgcn_fdot2(w1, xw[m][1], t, false);
+            t = __builtin_amdgcn_fdot2(w2, xw[m][2], t, false);
+            t = __builtin_amdgcn_fdot2(w3, xw[m][3], t, false);
+            a[r][m] = t;
+          }
         }
       }
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int m = 0; m < M; ++m) acc[r][m] += ok ? a[r][m] : 0.f;
     }
-#pragma unroll
-    for (int r = 0; r < kRows; ++r) {
-#pragma unroll
-      for (int m = 0; m < M; ++m) {
-        const float v = wave_sum(acc[r][m]);
-        if (lane == 0 && r0 + r < n) {
-          if (partial)
-            partial[((int64_t)split * M + m) * n + r0 + r] = v;
-          else
-            store_out<F16Out>(y, (int64_t)m * n + r0 + r, v);
-        }
-      }
-    }
-  }
-}
 
-// ------------------------------------------------------------------ FP8 ----
-// LDS layout: xs [M][2 halves of the chunk][nchunk][8 halves], natural order.
-template <int M, bool F16Out>
-__global__ __launch_bounds__(kThreads) void gemv_w8_kernel(const uint16_t* __restrict__ x, int64_t k, int64_t kslice,
-                                                           const uint8_t* __restrict__ codes,
-                                                           const float* __restrict__ scales, int64_t n,
-                                                           void* __restrict__ y, float* __restrict__ partial) {
-  extern __shared__ __align__(16) char smem[];
-  const int split = blockIdx.y;
-  const int64_t k0 = (int64_t)split * kslice;
-  const int64_t kl = (k - k0) < kslice ? (k - k0) : kslice;
-  const int nchunk = (int)(kl / 16);
-  half_t* xs = reinterpret_cast<half_t*>(smem);
-  for (int idx = threadIdx.x; idx < nchunk * M * 2; idx += kThreads) {
-    const int c = idx / (2 * M), rem = idx % (2 * M), m = rem >> 1, h = rem & 1;
-    *reinterpret_cast<u32x4*>(xs + (((size_t)m * 2 + h) * nchunk + c) * 8) =
-        *reinterpret_cast<const u32x4*>(x + (int64_t)m * k + k0 + 16 * c + 8 * h);
-  }
-  __syncthreads();
-
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t nquads = (n + kRows - 1) / kRows;
-  for (int64_t quad = (int64_t)blockIdx.x * kWaves + wave; quad < nquads; quad += (int64_t)gridDim.x * kWaves) {
-    const int64_t r0 = quad * kRows;
-    float acc[kRows][M];
+    if (task_n != task) {  // this wavefront's last step of the task
+      constexpr int T = (R * M + 3) / 4;
+      float v[4 * T];
 #pragma unroll
-    for (int r = 0; r < kRows; ++r)
+      for (int i = 0; i < 4 * T; ++i) v[i] = i < R * M ? acc[i / M][i % M] : 0.f;
 #pragma unroll
-      for (int m = 0; m < M; ++m) acc[r][m] = 0.f;
-
-    for (int c = lane; c < nchunk; c += kWave) {
-      const int64_t kc = k0 + 16 * (int64_t)c;
-      half2_t wv[kRows][8];
+      for (int r = 0; r < R; ++r)
 #pragma unroll
-      for (int r = 0; r < kRows; ++r) {
-        const int64_t row = (r0 + r) < n ? (r0 + r) : (n - 1);
-        const u32x4 q = *reinterpret_cast<const u32x4*>(codes + row * k + kc);
+        for (int m = 0; m < M; ++m) acc[r][m] = 0.f;
+      float w[T];
+      wave_sums<T>(v, w);
+      // lane 16 j holds value 4 t + (0, 2, 1, 3)[j] in w[t]
+      const int rowsel = lane >> 4;
+      const int which = rowsel == 0 ? 0 : (rowsel == 1 ? 2 : (rowsel == 2 ? 1 : 3));
+      const bool lead = (lane & 15) == 0;
+      auto emit = [&](int idx, float val) {
+        const int r = idx / M, m = idx % M;
+        const int64_t row = task * R + r;
+        if (row >= n) return;
+        if constexpr (W8) val *= scales32[row];
+        if (partial)
+          partial[((int64_t)split * M + m) * n + row] = val;
+        else if (f16_out)
+          reinterpret_cast<uint16_t*>(y)[(int64_t)m * n + row] = f32_to_f16_bits(val);
+        else
+          reinterpret_cast<float*>(y)[(int64_t)m * n + row] = val;
+      };
+      if constexpr (NW == 1) {
+        if (lead) {
 #pragma unroll
-        for (int wd = 0; wd < 4; ++wd) {
-          wv[r][2 * wd + 0] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(q[wd], 1.0f, false);
-          wv[r][2 * wd + 1] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(q[wd], 1.0f, true);
+          for (int t = 0; t < T; ++t) {
+            const int idx = 4 * t + which;
+            if (idx < R * M) emit(idx, w[t]);
+          }
         }
-      }
+      } else {
+        if (lead) {
 #pragma unroll
-      for (int m = 0; m < M; ++m) {
-        half2_t xv[8];
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const half2_t* xp = reinterpret_cast<const half2_t*>(xs + (((size_t)m * 2 + h) * nchunk + c) * 8);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) xv[4 * h + i] = xp[i];
+          for (int t = 0; t < T; ++t) {
+            const int idx = 4 * t + which;
+            if (idx < R * M) red[wave * R * M + idx] = w[t];
+          }
         }
+        __syncthreads();
+        if (threadIdx.x < R * M) {
+          float out = red[threadIdx.x];
 #pragma unroll
-        for (int r = 0; r < kRows; ++r) {
-          float a = acc[r][m];
-#pragma unroll
-          for (int i = 0; i < 8; ++i) a = __builtin_amdgcn_fdot2(wv[r][i], xv[i], a, false);
-          acc[r][m] = a;
+          for (int wv = 1; wv < NW; ++wv) out += red[wv * R * M + threadIdx.x];
+          emit(threadIdx.x, out);
         }
+        __syncthreads();
       }
     }
-#pragma unroll
-    for (int r = 0; r < kRows; ++r) {
-      const int64_t row = (r0 + r) < n ? (r0 + r) : (n - 1);
-      const float sc = scales[row];
-#pragma unroll
-      for (int m = 0; m < M; ++m) {
-        const float v = wave_sum(acc[r][m]);
-        if (lane == 0 && r0 + r < n) {
-          if (partial)
-            partial[((int64_t)split * M + m) * n + r0 + r] = v * sc;
-          else
-            store_out<F16Out>(y, (int64_t)m * n + r0 + r, v * sc);
-        }
-      }
-    }
+    task = task_n;
+    it = it_n;
+    tp = tp_n;
+    return task < ntask;
+  };
+
+  while (step(fa, fb) && step(fb, fa)) {
   }
 }
 
@@ -237,82 +387,86 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   }
 }
 
-// ------------------------------------------------------------ launching ----
-struct Plan {
-  int splits;
-  int64_t kslice;
-  unsigned grid_x;
-  size_t lds;
-};
+template <int M, bool W8, int NW>
+hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits, const uint8_t* codes,
+                       const uint16_t* scales16, const uint16_t* zeros16, const float* scales32, int64_t n, void* y,
+                       bool f16_out, float* partial, hipStream_t stream) {
+  constexpr int64_t chunk_k = W8 ? 32 : 64;
+  const int64_t kfirst = kslice < k ? kslice : k;
+  const int64_t nchunk = (kfirst + chunk_k - 1) / chunk_k;
+  constexpr int R = rows_for(M);
+  const size_t lds = (size_t)M * 2 * (size_t)(nchunk * chunk_k) + (NW > 1 ? (size_t)NW * R * M * 4 : 0);
+  const int64_t ntask = (n + R - 1) / R;
+  int64_t per_cu = SQ_GEMV_WAVES_PER_CU / NW;
+  const int64_t resident = resident_blocks(reinterpret_cast<const void*>(&gemv_kernel<M, W8, NW>), NW * 64, lds);
+  if (resident < per_cu) per_cu = resident;
+  const int64_t cap = (int64_t)cu_count() * per_cu;
+  const dim3 grid((unsigned)(ntask < cap ? ntask : cap), (unsigned)splits);
+  hipLaunchKernelGGL((gemv_kernel<M, W8, NW>), grid, dim3(NW * 64), lds, stream, x, k, kslice, codes, scales16,
+                     zeros16, scales32, n, y, (int)f16_out, partial);
+  return hipGetLastError();
+}
 
-// Split K when the activations of a full row do not fit the LDS budget, or
-// when there are too few row quads to give every CU work.
-Plan make_plan(int64_t n, int64_t k, int64_t kgrain, size_t lds_per_grain, int64_t target_blocks) {
-  Plan p;
-  const int64_t kmax = (int64_t)(kLdsBudget / lds_per_grain) * kgrain;
-  const int64_t nquads = (n + kRows - 1) / kRows;
-  const int64_t blocks_x = (nquads + kWaves - 1) / kWaves;
-  const int64_t splits_min = (k + kmax - 1) / kmax;
-  int64_t splits = splits_min;
-  if (blocks_x * splits < target_blocks) {
-    const int64_t want = (target_blocks + blocks_x - 1) / blocks_x;
-    const int64_t most = k / (4 * kgrain) > 1 ? k / (4 * kgrain) : 1;  // keep >= 4 grains per split
-    const int64_t extra = want < most ? want : most;
-    splits = extra > splits_min ? extra : splits_min;
-  }
+template <int M, bool W8>
+hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint16_t* scales16,
+                  const uint16_t* zeros16, const float* scales32, int64_t n, void* y, bool f16_out,
+                  hipStream_t stream) {
+  // the activations of a K slice sit in LDS (M * 2 bytes per k); slices are
+  // whole 128-element groups
+  const int64_t grain = 128;
+  int64_t kmax = (int64_t)(kLdsBudget / ((size_t)M * 2)) / grain * grain;
+#ifdef SQ_GEMV_KSLICE_MAX
+  if (kmax > SQ_GEMV_KSLICE_MAX) kmax = SQ_GEMV_KSLICE_MAX;
+#endif
+  const int splits = (int)((k + kmax - 1) / kmax);
   int64_t kslice = (k + splits - 1) / splits;
-  kslice = (kslice + kgrain - 1) / kgrain * kgrain;
-  p.splits = (int)((k + kslice - 1) / kslice);
-  p.kslice = kslice;
-  p.grid_x = (unsigned)(blocks_x < 65535 ? blocks_x : 65535);
-  p.lds = (size_t)(kslice / kgrain) * lds_per_grain;
-  return p;
-}
-
-template <int M>
-hipError_t gemv_w4_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint16_t* scales,
-                     const uint16_t* zeros, int64_t n, void* y, bool f16_out, hipStream_t stream) {
-  // per 128 k: 4 chunks x M x 64 B of permuted x
-  const size_t lds_per_grain = (size_t)4 * M * 64;
-  const Plan p = make_plan(n, k, 128, lds_per_grain, 512);
+  kslice = (kslice + grain - 1) / grain * grain;
   float* partial = nullptr;
-  if (p.splits > 1) {
-    partial = static_cast<float*>(workspace((size_t)p.splits * M * n * sizeof(float)));
+  if (splits > 1) {
+    partial = static_cast<float*>(workspace((size_t)splits * M * n * sizeof(float)));
     if (!partial) return hipErrorOutOfMemory;
   }
-  const dim3 grid(p.grid_x, p.splits);
-  if (f16_out)
-    hipLaunchKernelGGL((gemv_w4_kernel<M, true>), grid, dim3(kThreads), p.lds, stream, x, k, p.kslice, codes, scales,
-                       zeros, n, y, partial);
+  // wavefronts per workgroup: one per step of a task, at most four
+  const int64_t chunk_k = W8 ? 32 : 64;
+  const int64_t kfirst = kslice < k ? kslice : k;
+  const int64_t nit = ((kfirst + chunk_k - 1) / chunk_k + kWave - 1) / kWave;
+  // the last slice may be shorter: NW must not exceed its step count either
+  const int64_t klast = k - (int64_t)(splits - 1) * kslice;
+  const int64_t nit_last = ((klast + chunk_k - 1) / chunk_k + kWave - 1) / kWave;
+  const int64_t steps = nit < nit_last ? nit : nit_last;
+  // one wavefront per task when tasks outnumber the resident wavefronts;
+  // otherwise the workgroup's wavefronts split a task's steps
+  const int64_t ntask = (n + rows_for(M) - 1) / rows_for(M);
+  const bool many = ntask >= (int64_t)cu_count() * SQ_GEMV_WAVES_PER_CU;
+  hipError_t err;
+  if (!many && steps >= 4)
+    err = gemv_launch<M, W8, 4>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y, f16_out, partial,
+                                stream);
+  else if (!many && steps >= 2)
+    err = gemv_launch<M, W8, 2>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y, f16_out, partial,
+                                stream);
   else
-    hipLaunchKernelGGL((gemv_w4_kernel<M, false>), grid, dim3(kThreads), p.lds, stream, x, k, p.kslice, codes,
-                       scales, zeros, n, y, partial);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess || p.splits == 1) return err;
-  return launch_splitk_reduce(partial, p.splits, (int64_t)M * n, y, f16_out, stream);
+    err = gemv_launch<M, W8, 1>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y, f16_out, partial,
+                                stream);
+  if (err != hipSuccess || splits == 1) return err;
+  return launch_splitk_reduce(partial, splits, (int64_t)M * n, y, f16_out, stream);
 }
 
-template <int M>
-hipError_t gemv_w8_m(const uint16_t* x, int64_t k, const uint8_t* codes, const float* scales, int64_t n, void* y,
-                     bool f16_out, hipStream_t stream) {
-  // per 16 k: one chunk x M x 32 B of x
-  const size_t lds_per_grain = (size_t)M * 32;
-  const Plan p = make_plan(n, k, 16, lds_per_grain, 512);
-  float* partial = nullptr;
-  if (p.splits > 1) {
-    partial = static_cast<float*>(workspace((size_t)p.splits * M * n * sizeof(float)));
-    if (!partial) return hipErrorOutOfMemory;
+template <bool W8>
+hipError_t gemv_dispatch(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const uint16_t* scales16,
+                         const uint16_t* zeros16, const float* scales32, int64_t n, void* y, bool f16_out,
+                         hipStream_t stream) {
+  switch (m) {
+    case 1: return gemv_m<1, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
+    case 2: return gemv_m<2, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
+    case 3: return gemv_m<3, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
+    case 4: return gemv_m<4, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
+    case 5: return gemv_m<5, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
+    case 6: return gemv_m<6, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
+    case 7: return gemv_m<7, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
+    case 8: return gemv_m<8, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
+    default: return hipErrorInvalidValue;
   }
-  const dim3 grid(p.grid_x, p.splits);
-  if (f16_out)
-    hipLaunchKernelGGL((gemv_w8_kernel<M, true>), grid, dim3(kThreads), p.lds, stream, x, k, p.kslice, codes, scales,
-                       n, y, partial);
-  else
-    hipLaunchKernelGGL((gemv_w8_kernel<M, false>), grid, dim3(kThreads), p.lds, stream, x, k, p.kslice, codes,
-                       scales, n, y, partial);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess || p.splits == 1) return err;
-  return launch_splitk_reduce(partial, p.splits, (int64_t)M * n, y, f16_out, stream);
 }
 
 }  // namespace
@@ -332,32 +486,12 @@ hipError_t launch_splitk_reduce(const float* partial, int splits, int64_t mn, vo
 
 hipError_t launch_gemv_w4(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const uint16_t* scales,
                           const uint16_t* zeros, int64_t n, void* y, bool f16_out, hipStream_t stream) {
-  switch (m) {
-    case 1: return gemv_w4_m<1>(x, k, codes, scales, zeros, n, y, f16_out, stream);
-    case 2: return gemv_w4_m<2>(x, k, codes, scales, zeros, n, y, f16_out, stream);
-    case 3: return gemv_w4_m<3>(x, k, codes, scales, zeros, n, y, f16_out, stream);
-    case 4: return gemv_w4_m<4>(x, k, codes, scales, zeros, n, y, f16_out, stream);
-    case 5: return gemv_w4_m<5>(x, k, codes, scales, zeros, n, y, f16_out, stream);
-    case 6: return gemv_w4_m<6>(x, k, codes, scales, zeros, n, y, f16_out, stream);
-    case 7: return gemv_w4_m<7>(x, k, codes, scales, zeros, n, y, f16_out, stream);
-    case 8: return gemv_w4_m<8>(x, k, codes, scales, zeros, n, y, f16_out, stream);
-    default: return hipErrorInvalidValue;
-  }
+  return gemv_dispatch<false>(x, m, k, codes, scales, zeros, nullptr, n, y, f16_out, stream);
 }
 
 hipError_t launch_gemv_w8(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const float* scales, int64_t n,
                           void* y, bool f16_out, hipStream_t stream) {
-  switch (m) {
-    case 1: return gemv_w8_m<1>(x, k, codes, scales, n, y, f16_out, stream);
-    case 2: return gemv_w8_m<2>(x, k, codes, scales, n, y, f16_out, stream);
-    case 3: return gemv_w8_m<3>(x, k, codes, scales, n, y, f16_out, stream);
-    case 4: return gemv_w8_m<4>(x, k, codes, scales, n, y, f16_out, stream);
-    case 5: return gemv_w8_m<5>(x, k, codes, scales, n, y, f16_out, stream);
-    case 6: return gemv_w8_m<6>(x, k, codes, scales, n, y, f16_out, stream);
-    case 7: return gemv_w8_m<7>(x, k, codes, scales, n, y, f16_out, stream);
-    case 8: return gemv_w8_m<8>(x, k, codes, scales, n, y, f16_out, stream);
-    default: return hipErrorInvalidValue;
-  }
+  return gemv_dispatch<true>(x, m, k, codes, nullptr, nullptr, scales, n, y, f16_out, stream);
 }
 
 }  // namespace sq

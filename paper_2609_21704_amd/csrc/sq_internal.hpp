@@ -12,6 +12,13 @@ namespace sq {
 // device (grown on demand, never shrunk).  Returns nullptr on failure.
 void* workspace(size_t bytes);
 
+// Compute units of the current device (cached per device).
+int cu_count();
+
+// Resident workgroups per CU of `kernel` with `threads` threads and `lds`
+// bytes of dynamic LDS (cached; at least 1).
+int resident_blocks(const void* kernel, int threads, size_t lds);
+
 hipError_t launch_quantize_int4(const uint16_t* w, int64_t n, int64_t k, uint8_t* codes, uint16_t* scales,
                                 uint16_t* zeros, int32_t* flag, hipStream_t stream);
 hipError_t launch_quantize_fp8(const uint16_t* w, int64_t n, int64_t k, uint8_t* codes, float* scales,

@@ -180,7 +180,7 @@ def test_verify_gemm_identity_is_exact(m):
 
 # --------------------------------------------------------------- accept ----
 def _accept_case(b, kd, v, seed, temp, token_mode="sampled", sd=2.0, noise=0.5):
-    """draft ~ N(0, sd), target = draft + N(0, noise) (bonus row fresh); tokens drawn from q."""
+    """draft ~ N(0, sd), target = draft + N(0, noise) (bonus row fresh); tokens [kd][b] drawn from q."""
     draft = synth.normal_f32((kd, b, v), sd, synth.stream_seed(seed, 1))
     target = torch.empty((b, kd + 1, v), dtype=torch.float32)
     eps = synth.normal_f32((b, kd + 1, v), noise, synth.stream_seed(seed, 2))
@@ -188,14 +188,14 @@ def _accept_case(b, kd, v, seed, temp, token_mode="sampled", sd=2.0, noise=0.5):
     target[:, kd] = synth.normal_f32((b, v), sd, synth.stream_seed(seed, 3))
     u24 = synth.uniform_u24((b, kd + 1), synth.stream_seed(seed, 4))
     if kd == 0:
-        tok = torch.zeros((b, 0), dtype=torch.int32)
+        tok = torch.zeros((0, b), dtype=torch.int32)
     elif token_mode == "sampled" and temp > 0:
         q = oracle.softmax(draft.reshape(kd * b, v).numpy(), float(np.float32(temp))).reshape(kd, b, v)
         r = np.random.default_rng(seed).random((kd, b))
-        tok = np.minimum((r[..., None] >= np.cumsum(q, axis=2)).sum(axis=2), v - 1).T.astype(np.int32)
+        tok = np.minimum((r[..., None] >= np.cumsum(q, axis=2)).sum(axis=2), v - 1).astype(np.int32)  # [kd][b]
         tok = torch.from_numpy(np.ascontiguousarray(tok))
     else:
-        tok = synth.tokens((b, kd), v, synth.stream_seed(seed, 5))
+        tok = synth.tokens((kd, b), v, synth.stream_seed(seed, 5))
     return draft, target, tok, u24
 
 
@@ -246,8 +246,8 @@ def test_spec_accept_greedy(b, kd, v):
     target[0, 0] = 1.0                               # ties -> smallest index
     am = target.argmax(dim=2).to(torch.int32)
     if kd > 0:
-        tok = am[:, :kd].clone()
-        tok[1 % b, kd // 2] = (tok[1 % b, kd // 2] + 1) % v
+        tok = am[:, :kd].t().contiguous()
+        tok[kd // 2, 1 % b] = (tok[kd // 2, 1 % b] + 1) % v
     n, t, _, _ = _run_accept(draft, target, tok, u24, 0.0)
     n_ref, t_ref, _, _ = oracle.spec_accept(draft.numpy(), target.numpy(), tok.numpy(), None, 0.0)
     assert np.array_equal(n, n_ref) and np.array_equal(t, t_ref)
@@ -256,9 +256,9 @@ def test_spec_accept_greedy(b, kd, v):
 def test_spec_accept_edge_tokens_and_equal_distributions():
     b, kd, v = 6, 4, 333
     draft, target, tok, u24 = _accept_case(b, kd, v, 21, 1.0, "uniform")
-    tok[0, 0] = -1
-    tok[1, 2] = v
-    tok[2, 1] = 1 << 30
+    tok[0, 0] = -1          # [position][sequence]
+    tok[2, 1] = v
+    tok[1, 2] = 1 << 30
     target[3, :kd] = draft[:, 3]                     # p = q for sequence 3: all accepted
     u24[4] = (1 << 24) - 1
     u24[5] = 0
@@ -282,7 +282,7 @@ def test_spec_accept_chi_square_on_gpu():
     u24 = rng.integers(0, 1 << 24, (b, kd + 1)).astype(np.int32)
     draft = torch.from_numpy(np.ascontiguousarray(np.broadcast_to(dl[:, None, :], (kd, b, v))))
     target = torch.from_numpy(np.ascontiguousarray(np.broadcast_to(tl[None], (b, kd + 1, v))))
-    n, nxt, _, _ = _run_accept(draft, target, torch.from_numpy(x), torch.from_numpy(u24), 1.0)
+    n, nxt, _, _ = _run_accept(draft, target, torch.from_numpy(np.ascontiguousarray(x.T)), torch.from_numpy(u24), 1.0)
     crit = lambda dof: stats.chi2.ppf(1 - 1e-3, dof)
     beta = np.minimum(p[:kd], q).sum(axis=1)
     law = np.array([np.prod(beta[:i]) * (1 - beta[i]) for i in range(kd)] + [np.prod(beta)])

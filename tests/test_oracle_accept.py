@@ -109,7 +109,7 @@ def test_chi_square_kd4_positions_and_acceptance_law():
     u24 = rng.integers(0, U, (b, kd + 1), dtype=np.uint32)
     draft = np.broadcast_to(dl[:, None, :], (kd, b, v))
     target = np.broadcast_to(tl[None, :, :], (b, kd + 1, v))
-    n, nxt, _, _ = oracle.spec_accept(draft, target, x, u24, 1.0)
+    n, nxt, _, _ = oracle.spec_accept(draft, target, np.ascontiguousarray(x.T), u24, 1.0)
     crit = lambda dof: stats.chi2.ppf(1 - 1e-3, dof)
     # acceptance law: P(n = i) = prod_{j<i} beta_j (1 - beta_i), P(n = kd) = prod beta
     beta = np.minimum(p[:kd], q).sum(axis=1)
@@ -130,7 +130,7 @@ def test_equal_distributions_accept_everything():
     l = RNG.normal(0, 2, (kd + 1, v)).astype(np.float32)
     draft = np.broadcast_to(l[:kd, None, :], (kd, b, v))
     target = np.broadcast_to(l[None], (b, kd + 1, v))
-    x = RNG.integers(0, v, (b, kd)).astype(np.int32)
+    x = RNG.integers(0, v, (kd, b)).astype(np.int32)
     u24 = np.full((b, kd + 1), U - 1, np.uint32)
     n, nxt, _, _ = oracle.spec_accept(draft, target, x, u24, 1.0)
     assert np.all(n == kd)
@@ -163,7 +163,7 @@ def test_greedy_rule_matches_argmax():
         if cut[s] < kd:
             x[s, cut[s]] = (am[s, cut[s]] + 1) % v
     draft = RNG.normal(0, 1, (kd, b, v)).astype(np.float32)
-    n, nxt, _, _ = oracle.spec_accept(draft, tl, x, None, 0.0)
+    n, nxt, _, _ = oracle.spec_accept(draft, tl, np.ascontiguousarray(x.T), None, 0.0)
     exp_n = np.array([next((i for i in range(kd) if x[s, i] != am[s, i]), kd) for s in range(b)])
     assert np.array_equal(n, exp_n)
     assert np.array_equal(nxt, am[np.arange(b), exp_n])
@@ -183,7 +183,7 @@ def test_one_hot_stochastic_reduces_to_greedy():
             tl[s, i, pt[s, i]] = big
         for i in range(kd):
             dl[i, s, qt[s, i]] = big
-    x = qt.astype(np.int32)
+    x = np.ascontiguousarray(qt.T).astype(np.int32)
     u24 = RNG.integers(0, U, (b, kd + 1), dtype=np.uint32)
     n1, t1, _, _ = oracle.spec_accept(dl, tl, x, u24, 1.0)
     n0, t0, _, _ = oracle.spec_accept(dl, tl, x, None, 0.0)
@@ -206,7 +206,7 @@ def test_pq_outputs_and_errors():
     b, kd, v = 3, 2, 40
     dl = RNG.normal(0, 1, (kd, b, v)).astype(np.float32)
     tl = RNG.normal(0, 1, (b, kd + 1, v)).astype(np.float32)
-    x = RNG.integers(0, v, (b, kd)).astype(np.int32)
+    x = RNG.integers(0, v, (kd, b)).astype(np.int32)
     u24 = RNG.integers(0, U, (b, kd + 1), dtype=np.uint32)
     n, t, q, p = oracle.spec_accept(dl, tl, x, u24, 0.9, want_pq=True)
     assert np.max(np.abs(q - special.softmax(dl.astype(np.float64) / 0.9, axis=2))) < 1e-15
