@@ -30,6 +30,7 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
 METRIC = "draft+verify tokens/s at Qwen2.5-7B shape (k=4); INT4/FP8 GEMV HBM TB/s vs peak"
 GEMV_SRC = os.path.join(ROOT, "paper_2609_21704_amd", "csrc", "gemv.hip")
+COPY_BYTES = 1 << 30   # the plain copy that calibrates the HBM byte counters
 
 
 def gemv_bytes(variant: str, m: int, n: int, k: int, out_bytes: int) -> float:
@@ -39,42 +40,49 @@ def gemv_bytes(variant: str, m: int, n: int, k: int, out_bytes: int) -> float:
 
 
 def measure_gemv(rnd, steps: int):
-    """Per-launch durations of the draft GEMVs, timed with HIP events on the
-    launching stream.  A verify pass runs first so that the launches and
-    events are already queued when the GPU reaches them."""
+    """Average duration of a draft-GEMV launch: HIP events on the launching
+    stream bracket the back-to-back GEMV launches of a whole draft pass (every
+    layer's projections and the LM head), and the interval is divided by the
+    launch count.  A spin kernel of about 40 ms runs first, so that every
+    launch of the pass is queued before the GPU reaches it and no host-side
+    launch latency lands inside the interval."""
     import torch
 
+    # cycles of torch's spin kernel per millisecond on this device
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    torch.cuda._sleep(1 << 22)
+    e1.record()
+    torch.cuda.synchronize()
+    cycles_per_ms = (1 << 22) / max(e0.elapsed_time(e1), 1e-3)
+
     cfg, st = rnd.cfg, rnd.stack
-    shapes = {}
+    pass_bytes = 0.0
+    n_launch = 0
     for l, name, n, k in st.mats:
-        if name != "lm_head":
-            shapes[(l, name)] = (n, k, 2)
-        else:
-            shapes[(cfg.layers, name)] = (n, k, 4)
-    order = []
-    for l in range(st.layers):
-        for name, _, _ in cfg.layer_matrices():
-            order.append((l, name))
-    if cfg.lm_head:
-        order.append((cfg.layers, "lm_head"))
+        out_bytes = 4 if name == "lm_head" else 2
+        pass_bytes += gemv_bytes(st.variant, cfg.draft_m, n, k, out_bytes)
+        n_launch += 1
     tot_bytes, tot_s, launches = 0.0, 0.0, 0
     for i in range(steps):
-        events = []
+        marks, calls = [], [0]
 
-        def hook(start, events=events):
-            e = torch.cuda.Event(enable_timing=True)
-            e.record()
-            events.append(e)
+        def hook(start, marks=marks, calls=calls):
+            j = calls[0]
+            calls[0] += 1
+            if j == 0 or j == 2 * n_launch - 1:  # before the first launch, after the last
+                e = torch.cuda.Event(enable_timing=True)
+                e.record()
+                marks.append(e)
 
-        rnd.verify()
+        torch.cuda._sleep(int(40 * cycles_per_ms))
         rnd.draft_step(i % cfg.k, on_gemv=hook)
         torch.cuda.synchronize()
-        for j, key in enumerate(order):
-            n, k, ob = shapes[key]
-            dt = events[2 * j].elapsed_time(events[2 * j + 1]) * 1e-3
-            tot_s += dt
-            tot_bytes += gemv_bytes(st.variant, cfg.draft_m, n, k, ob)
-            launches += 1
+        assert calls[0] == 2 * n_launch and len(marks) == 2
+        tot_s += marks[0].elapsed_time(marks[1]) * 1e-3
+        tot_bytes += pass_bytes
+        launches += n_launch
     return tot_bytes, tot_s, launches
 
 
@@ -167,9 +175,10 @@ def cpu_baseline(rnd, tokens_per_round: float):
     t0 = time.perf_counter()
     oracle.spec_accept(draft_logits, target, tokens, u_a, T)
     t_accept = time.perf_counter() - t0
-    round_s = (k * (cfg.layers * t_layer_draft + t_lm_draft + t_sample)
+    # the draft terms already sum over the k draft steps
+    round_s = (cfg.layers * t_layer_draft + t_lm_draft + t_sample
                + cfg.layers * t_layer_verify + t_lm_verify + t_accept)
-    measured = (k * (len(layers) * t_layer_draft + t_lm_draft + t_sample)
+    measured = (len(layers) * t_layer_draft + t_lm_draft + t_sample
                 + len(layers) * t_layer_verify + t_lm_verify + t_accept)
     return {
         "value": round(tokens_per_round * cfg.batch / round_s, 4),
@@ -192,7 +201,8 @@ def main():
     ap.add_argument("--gemv-steps", type=int, default=2, help="draft passes timed per launch for the roofline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-only", action="store_true",
-                    help="run warmup rounds and one eager draft pass, print nothing (for rocprofv3 counters)")
+                    help="for rocprofv3 counter runs: one eager round, then a plain copy of COPY_BYTES bytes "
+                         "(the counter calibration); prints nothing")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -211,6 +221,16 @@ def main():
     torch.cuda.set_device(dev)
     stack = Stack(cfg, dev)
     rnd = Round(stack, temperature=args.temperature)
+    if args.profile_only:
+        ud, ua = round_uniforms(cfg, 1, dev)
+        rnd.set_uniforms(ud[0], ua[0])
+        rnd.run()
+        src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.bitwise_not(src, out=dst)  # reads and writes each byte once: the last dispatch of the run
+        torch.cuda.synchronize()
+        return
     total = args.warmup + args.steps
     ud, ua = round_uniforms(cfg, total, dev)
     n_hist = torch.zeros((total, cfg.batch), dtype=torch.int32, device=dev)
@@ -225,10 +245,6 @@ def main():
     for r in range(args.warmup):
         one(r)
     torch.cuda.synchronize()
-    if args.profile_only:
-        rnd.draft_step(0)
-        torch.cuda.synchronize()
-        return
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()

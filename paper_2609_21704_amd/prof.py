@@ -1,0 +1,134 @@
+"""Summaries of rocprofv3 output for the SpecQuant kernels.
+
+    python -m paper_2609_21704_amd.prof stats <rocprofv3 output dir> [--match SUBSTR]
+        per-kernel dispatch count and duration (avg / min / max), kernels grouped
+        by name and grid size
+    python -m paper_2609_21704_amd.prof traffic <FETCH_SIZE dir> <WRITE_SIZE dir> --copy-bytes N
+        HBM bytes per draft-GEMV dispatch from the FETCH_SIZE / WRITE_SIZE
+        counters, each divided by what the same counter reads, per byte, for the
+        plain copy pass over N bytes (read once, written once) that the profiled
+        command dispatches last
+
+The inputs are the rocpd SQLite databases rocprofv3 writes (*.db).
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import glob
+import hashlib
+import os
+import re
+import sqlite3
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+GEMV_SRC = os.path.join(ROOT, "paper_2609_21704_amd", "csrc", "gemv.hip")
+
+
+def _dbs(path):
+    return sorted(glob.glob(os.path.join(path, "**", "*.db"), recursive=True))
+
+
+def short_name(name: str) -> str:
+    name = name.replace("(anonymous namespace)::", "")
+    if name.startswith("void "):
+        name = name[5:]
+    depth = 0
+    for i, ch in enumerate(name):  # cut the argument list (the first '(' outside template brackets)
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            return name[:i].strip()
+    return name.strip()
+
+
+def kernel_rows(path):
+    for db in _dbs(path):
+        con = sqlite3.connect(db)
+        for row in con.execute("select name, grid_x, grid_y, workgroup_x, duration from kernels order by start"):
+            yield row
+
+
+def stats(path, match=None):
+    groups = collections.OrderedDict()
+    for name, gx, gy, wx, dur in kernel_rows(path):
+        sn = short_name(name)
+        if match and match not in sn:
+            continue
+        key = (sn, gx // max(wx, 1), gy, wx)
+        groups.setdefault(key, []).append(dur)
+    lines = [f"{'kernel':58s} {'grid':>12s} {'wg':>4s} {'calls':>7s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s}"]
+    by_name = collections.OrderedDict()
+    for (sn, gx, gy, wx), d in groups.items():
+        lines.append(f"{sn[:58]:58s} {f'{gx}x{gy}':>12s} {wx:>4d} {len(d):>7d} {sum(d) / len(d) / 1e3:>9.2f} "
+                     f"{min(d) / 1e3:>9.2f} {max(d) / 1e3:>9.2f}")
+        by_name.setdefault(sn, []).extend(d)
+    if match and by_name:
+        alld = [x for d in by_name.values() for x in d]
+        lines.append(f"all kernels matching '{match}': calls {len(alld)}, avg_us {sum(alld) / len(alld) / 1e3:.2f}")
+    lines.append("")
+    lines.append(f"{'kernel (all grids)':58s} {'calls':>7s} {'avg_us':>9s} {'total_ms':>10s}")
+    for sn, d in by_name.items():
+        lines.append(f"{sn[:58]:58s} {len(d):>7d} {sum(d) / len(d) / 1e3:>9.2f} {sum(d) / 1e6:>10.3f}")
+    return "\n".join(lines)
+
+
+def counter_values(path, counter):
+    """(dispatch_id, short kernel name, value) of every dispatch, in dispatch order."""
+    rows = []
+    for db in _dbs(path):
+        con = sqlite3.connect(db)
+        for d, k, c, v in con.execute("select dispatch_id, kernel_name, counter_name, value from counters_collection"):
+            if c == counter:
+                rows.append((d, short_name(k), v))
+    rows.sort()
+    return rows
+
+
+def traffic(fetch_dir, write_dir, copy_bytes):
+    fetch = counter_values(fetch_dir, "FETCH_SIZE")
+    write = counter_values(write_dir, "WRITE_SIZE")
+    copy_key = fetch[-1][1]
+    f_scale = fetch[-1][2] * 1024.0 / copy_bytes   # counters are in KiB
+    w_scale = write[-1][2] * 1024.0 / copy_bytes
+    f_g = [v * 1024.0 for _, k, v in fetch if k.startswith("sq::gemv_kernel")]
+    w_g = [v * 1024.0 for _, k, v in write if k.startswith("sq::gemv_kernel")]
+    f_mean = sum(f_g) / len(f_g) / f_scale
+    w_mean = sum(w_g) / len(w_g) / w_scale if w_g else 0.0
+    sha = hashlib.sha256(open(GEMV_SRC, "rb").read()).hexdigest()
+    return "\n".join([
+        f"copy_kernel = {copy_key}",
+        f"copy_bytes = {copy_bytes}",
+        f"fetch_counter_bytes_per_copied_byte = {f_scale:.6f}",
+        f"write_counter_bytes_per_copied_byte = {w_scale:.6f}",
+        f"gemv_dispatches = {len(f_g)}",
+        f"fetch_bytes_per_launch_raw = {sum(f_g) / len(f_g):.1f}",
+        f"write_bytes_per_launch_raw = {sum(w_g) / max(len(w_g), 1):.1f}",
+        f"hbm_read_bytes_per_launch = {f_mean:.1f}",
+        f"hbm_write_bytes_per_launch = {w_mean:.1f}",
+        f"hbm_bytes_per_launch = {f_mean + w_mean:.1f}",
+        f"gemv_source_sha256 = {sha}",
+    ])
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    a = sub.add_parser("stats")
+    a.add_argument("path")
+    a.add_argument("--match")
+    b = sub.add_parser("traffic")
+    b.add_argument("fetch_dir")
+    b.add_argument("write_dir")
+    b.add_argument("--copy-bytes", type=int, required=True)
+    args = ap.parse_args()
+    if args.cmd == "stats":
+        print(stats(args.path, args.match))
+    else:
+        print(traffic(args.fetch_dir, args.write_dir, args.copy_bytes))
+
+
+if __name__ == "__main__":
+    main()
