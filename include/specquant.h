@@ -143,8 +143,8 @@ sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint
  *   sequence s are draft_tokens[0 .. n_accepted[s])[s] then next_token[s].
  * q_out [kd][b][v] f32, p_out [b][kd+1][v] f32: optional (nullable) copies of
  *   the distributions, T > 0 only.
- * Limits: 1 <= b <= 2^24, 0 <= kd <= 64, 1 <= v <= 2^26,
- *   b * (2 kd + 1) * ceil(v / 4096) <= 2^24; T finite and >= 0. */
+ * Limits: 1 <= b < 2^24, 0 <= kd <= 64, 1 <= v <= 2^26,
+ *   b * (2 kd + 1) * ceil(v / 4096) < 2^24; T finite and >= 0. */
 sq_status sq_spec_accept(const float* draft_logits, const float* target_logits,
                          const int32_t* draft_tokens, const uint32_t* u24, int32_t b, int32_t kd,
                          int32_t v, float temperature, int32_t* n_accepted, int32_t* next_token,

@@ -214,9 +214,10 @@ sq_status sq_spec_accept(const float* draft_logits, const float* target_logits, 
                          int32_t* n_accepted, int32_t* next_token, float* q_out, float* p_out, hipStream_t stream) {
   if (!target_logits || !n_accepted || !next_token) return SQ_ERR_NULL;
   if (kd > 0 && (!draft_logits || !draft_tokens)) return SQ_ERR_NULL;
-  if (b < 1 || b > (1 << 24) || kd < 0 || kd > 64 || v < 1 || v > (1 << 26)) return SQ_ERR_SHAPE;
+  if (b < 1 || b >= (1 << 24) || kd < 0 || kd > 64 || v < 1 || v > (1 << 26)) return SQ_ERR_SHAPE;
   const int64_t nchunk = (v + 4095) / 4096;
-  if ((int64_t)b * (2 * kd + 1) * nchunk > (int64_t(1) << 24)) return SQ_ERR_SHAPE;
+  // every kernel grid stays below 2^24 workgroups of 256 threads (2^32 work-items)
+  if ((int64_t)b * (2 * kd + 1) * nchunk >= (int64_t(1) << 24)) return SQ_ERR_SHAPE;
   if (!isfinite(temperature) || temperature < 0.0f) return SQ_ERR_VALUE;
   if (temperature == 0.0f && (q_out || p_out)) return SQ_ERR_VALUE;
   if (temperature > 0.0f && !u24) return SQ_ERR_NULL;

@@ -28,15 +28,11 @@ __device__ __forceinline__ double f16_ceil(double s) {
   return ldexp(ceil(ldexp(s, -sp)), sp);
 }
 
-// INT4 g128: 16 threads per group of 128 elements, 8 elements (16 B) each.
-// Groups are contiguous in memory because k % 128 == 0, so group gi starts at
-// element 128 * gi and its 64 code bytes at byte 64 * gi.
-__global__ __launch_bounds__(256) void quantize_int4_kernel(const uint16_t* __restrict__ w, int64_t ngroups,
-                                                            uint8_t* __restrict__ codes,
-                                                            uint16_t* __restrict__ scales,
-                                                            uint16_t* __restrict__ zeros, int32_t* flag) {
-  const int64_t gi = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
-  const int sub = threadIdx.x & 15;
+// One group's quantization, by its 16 consecutive lanes (sub = 0 .. 15).
+__device__ __forceinline__ void quantize_int4_group(const uint16_t* __restrict__ w, int64_t ngroups, int64_t gi,
+                                                    int sub, uint8_t* __restrict__ codes,
+                                                    uint16_t* __restrict__ scales, uint16_t* __restrict__ zeros,
+                                                    int32_t* flag) {
   const bool active = gi < ngroups;
   u32x4 raw = {0u, 0u, 0u, 0u};
   if (active) raw = *reinterpret_cast<const u32x4*>(w + gi * 128 + sub * 8);
@@ -61,7 +57,7 @@ __global__ __launch_bounds__(256) void quantize_int4_kernel(const uint16_t* __re
     hi = ohi > hi ? ohi : hi;
     bad |= __shfl_xor((int)bad, off, 16) != 0;
   }
-  if (!active) return;
+  if (!active) return;  // whole 16-lane groups only: no shuffle follows
 
   uint32_t packed = 0;
   uint16_t sbits, zbits;
@@ -91,6 +87,18 @@ __global__ __launch_bounds__(256) void quantize_int4_kernel(const uint16_t* __re
     scales[gi] = sbits;
     zeros[gi] = zbits;
   }
+}
+
+// INT4 g128: 16 threads per group of 128 elements, 8 elements (16 B) each;
+// a workgroup handles 16 consecutive groups per pass of its grid-stride loop.
+// Groups are contiguous in memory because k % 128 == 0, so group gi starts at
+// element 128 * gi and its 64 code bytes at byte 64 * gi.
+__global__ __launch_bounds__(256) void quantize_int4_kernel(const uint16_t* __restrict__ w, int64_t ngroups,
+                                                            uint8_t* __restrict__ codes,
+                                                            uint16_t* __restrict__ scales,
+                                                            uint16_t* __restrict__ zeros, int32_t* flag) {
+  for (int64_t gbase = (int64_t)blockIdx.x * 16; gbase < ngroups; gbase += (int64_t)gridDim.x * 16)
+    quantize_int4_group(w, ngroups, gbase + (threadIdx.x >> 4), threadIdx.x & 15, codes, scales, zeros, flag);
 }
 
 // OCP E4M3 encode of a finite double: round to nearest, ties to even,
@@ -183,9 +191,8 @@ __global__ __launch_bounds__(256) void quantize_fp8_kernel(const uint16_t* __res
 hipError_t launch_quantize_int4(const uint16_t* w, int64_t n, int64_t k, uint8_t* codes, uint16_t* scales,
                                 uint16_t* zeros, int32_t* flag, hipStream_t stream) {
   const int64_t ngroups = n * (k / 128);
-  const int64_t threads = ngroups * 16;
-  const int64_t blocks = (threads + 255) / 256;
-  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  const int64_t need = (ngroups + 15) / 16;
+  const int64_t blocks = need < 65536 * 16 ? need : 65536 * 16;
   hipLaunchKernelGGL(quantize_int4_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, w, ngroups, codes, scales,
                      zeros, flag);
   return hipGetLastError();

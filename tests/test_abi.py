@@ -87,6 +87,9 @@ def test_accept_validation():
     assert acc(A, B, C, D, 1, -1, 100, 1.0, E, E + 64, None, None, None) == SHAPE
     assert acc(A, B, C, D, 1, 4, 0, 1.0, E, E + 64, None, None, None) == SHAPE
     assert acc(A, B, C, D, 1 << 20, 8, 151936, 1.0, E, E + (1 << 22), None, None, None) == SHAPE
+    assert acc(None, B, None, D, 1 << 24, 0, 1, 1.0, E, E + (1 << 26), None, None, None) == SHAPE
+    assert acc(None, B, None, D, 1 << 23, 0, 4097, 1.0, E, E + (1 << 25), None, None, None) == SHAPE
+    assert acc(A, B, C, D, 1, 1, (1 << 26) + 1, 1.0, E, E + 64, None, None, None) == SHAPE
     assert acc(A, B, C, D, 1, 4, 100, -1.0, E, E + 64, None, None, None) == VALUE
     assert acc(A, B, C, D, 1, 4, 100, float("nan"), E, E + 64, None, None, None) == VALUE
     assert acc(A, B, C, D, 1, 4, 100, 0.0, E, E + 64, E + 128, None, None) == VALUE

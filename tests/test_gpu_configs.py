@@ -1,0 +1,148 @@
+"""GPU parity at the five workloads' full shapes, through the resident stack and
+round driver that the benchmark times, against the CPU oracle.
+
+Workload 0 (one Qwen2.5-0.5B-shaped layer) is checked in full.  Workloads 1-4
+build layer 0 and the LM head at full size; every matrix's quantized codes are
+checked bit for bit on 64 seeded rows plus the first and last row, and the
+draft GEMV and verify GEMM outputs at those rows within the normalised-error
+bound.  One whole round then runs through the driver, and its draft draws and
+accept step are checked bit for bit against the oracle on the round's own
+logits and uniforms."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_21704_amd as sq
+from paper_2609_21704_amd import synth
+from paper_2609_21704_amd.configs import CONFIGS
+from paper_2609_21704_amd.rounds import Round, Stack, round_uniforms
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+GEMV_TOL = 2e-3
+
+
+def bits16(t: torch.Tensor) -> np.ndarray:
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def sample_rows(n: int, seed: int, count: int = 64) -> np.ndarray:
+    g = torch.Generator().manual_seed(seed)
+    rows = torch.randperm(n, generator=g)[:count].numpy()
+    return np.unique(np.concatenate([rows, [0, n - 1]]))
+
+
+def check_matrix(stack: Stack, key, rows, seed: int):
+    """Quantized rows bit for bit, then the draft GEMV (m = B) and the verify
+    GEMM (m = B(k+1)) at those rows, with the output types the driver uses."""
+    cfg = stack.cfg
+    w16 = stack.w16[key]
+    n, k = w16.shape
+    idx = torch.from_numpy(rows).to(DEV)
+    w_rows = bits16(w16.index_select(0, idx))
+    pack = stack.draft[key]
+    if stack.variant == "int4":
+        c_ref, s_ref, z_ref = oracle.quantize_int4_g128(w_rows)
+        assert np.array_equal(pack[0].index_select(0, idx).cpu().numpy(), c_ref), key
+        assert np.array_equal(bits16(pack[1].index_select(0, idx)), s_ref), key
+        assert np.array_equal(bits16(pack[2].index_select(0, idx)), z_ref), key
+    else:
+        c_ref, s_ref = oracle.quantize_fp8_e4m3(w_rows)
+        assert np.array_equal(pack[0].index_select(0, idx).cpu().numpy(), c_ref), key
+        assert np.array_equal(pack[1].index_select(0, idx).cpu().numpy().view(np.uint32), s_ref.view(np.uint32)), key
+
+    y_dtype = torch.float32 if key[1] == "lm_head" else torch.float16
+    xd = synth.normal_f16((cfg.draft_m, k), 1.0, synth.stream_seed(seed, 1), DEV)
+    y = torch.empty((cfg.draft_m, n), dtype=y_dtype, device=DEV)
+    stack.draft_gemv(key, xd, y)
+    if stack.variant == "int4":
+        y_ref, d_ref = oracle.qgemv_w4a16(bits16(xd), c_ref, s_ref, z_ref)
+    else:
+        y_ref, d_ref = oracle.qgemv_w8a16(bits16(xd), c_ref, s_ref)
+    err = oracle.normalised_error(y.index_select(1, idx).float().cpu().numpy(), y_ref, d_ref)
+    assert err <= GEMV_TOL, (key, "draft", err)
+
+    xv = synth.normal_f16((cfg.verify_m, k), 1.0, synth.stream_seed(seed, 2), DEV)
+    yv = torch.empty((cfg.verify_m, n), dtype=y_dtype, device=DEV)
+    stack.verify_gemm(key, xv, yv)
+    yv_ref, dv_ref = oracle.gemm_f16(bits16(xv), w_rows)
+    err = oracle.normalised_error(yv.index_select(1, idx).float().cpu().numpy(), yv_ref, dv_ref)
+    assert err <= GEMV_TOL, (key, "verify", err)
+
+
+def check_round(rnd: Round, round_index: int):
+    """Run one round and check its draws and accept step against the oracle."""
+    cfg = rnd.cfg
+    B, k, V = cfg.batch, cfg.k, cfg.vocab
+    T = rnd.temperature
+    ud, ua = round_uniforms(cfg, round_index + 1, DEV)
+    rnd.set_uniforms(ud[round_index], ua[round_index])
+    rnd.run()
+    torch.cuda.synchronize()
+    b = rnd.buf
+    draft = b.draft_logits.cpu().numpy()
+    target = b.target_logits.cpu().numpy()
+    tokens = b.draft_tokens.cpu().numpy()
+    u_d = b.u_draft.cpu().numpy().view(np.uint32)
+    u_a = b.u_accept.cpu().numpy().view(np.uint32)
+    for i in range(k):  # draft draw i: a plain sampler over draft row i
+        _, nxt, _, _ = oracle.spec_accept(None, draft[i].reshape(B, 1, V), None, u_d[i].reshape(B, 1), T)
+        assert np.array_equal(nxt, tokens[i]), ("draft draw", i)
+    n_ref, t_ref, _, _ = oracle.spec_accept(draft, target, tokens, u_a if T > 0 else None, T)
+    assert np.array_equal(b.n_accepted.cpu().numpy(), n_ref)
+    assert np.array_equal(b.next_token.cpu().numpy(), t_ref)
+    return n_ref
+
+
+@pytest.mark.parametrize("variant", ["int4", "fp8"])
+def test_workload0_full(variant):
+    cfg = CONFIGS[0]
+    stack = Stack(cfg, DEV, variant=variant)
+    for key in stack.w16:
+        n = stack.w16[key].shape[0]
+        check_matrix(stack, key, np.arange(n), seed=cfg.seed * 100 + len(key[1]))
+    rnd = Round(stack, temperature=1.0)
+    for r in range(3):
+        check_round(rnd, r)
+    greedy = Round(stack, temperature=0.0)
+    check_round(greedy, 0)
+
+
+WORKLOADS = [(1, "int4"), (1, "fp8"), (2, "int4"), (3, "fp8"), (4, "int4")]
+
+
+@pytest.mark.parametrize("index,variant", WORKLOADS)
+def test_workload_full_shapes_sampled(index, variant):
+    cfg = CONFIGS[index]
+    stack = Stack(cfg, DEV, variant=variant, layers=1)
+    for j, key in enumerate(sorted(stack.w16)):
+        n = stack.w16[key].shape[0]
+        check_matrix(stack, key, sample_rows(n, cfg.seed * 1000 + j), seed=cfg.seed * 100 + j)
+    rnd = Round(stack, temperature=1.0)
+    check_round(rnd, 0)
+    check_round(rnd, 1)
+    del rnd, stack
+    torch.cuda.empty_cache()
+
+
+def test_round_graph_replays_match_eager():
+    """One round captured as a HIP graph: each replay (fresh uniforms, eager
+    work and synchronisations in between) gives the eager round's bits."""
+    cfg = CONFIGS[0]
+    stack = Stack(cfg, DEV)
+    rnd = Round(stack, temperature=1.0)
+    rnd.capture()
+    ud, ua = round_uniforms(cfg, 4, DEV)
+    for r in range(4):
+        rnd.set_uniforms(ud[r], ua[r])
+        rnd.replay()
+        torch.cuda.synchronize()
+        b = rnd.buf
+        got = [t.clone() for t in (b.draft_logits, b.target_logits, b.draft_tokens, b.n_accepted, b.next_token)]
+        rnd.set_uniforms(ud[r], ua[r])
+        rnd.run()
+        torch.cuda.synchronize()
+        ref = (b.draft_logits, b.target_logits, b.draft_tokens, b.n_accepted, b.next_token)
+        for g, e in zip(got, ref):
+            assert torch.equal(g, e), r
