@@ -11,6 +11,11 @@
 #include "sq_internal.hpp"
 #include "specquant.h"
 
+// Large matrices stream through the matrix-core kernel; small ones (where
+// the launch and its ramp dominate) and m > 16 use the vector-ALU GEMV and the
+// tile-per-workgroup GEMM, which measured faster there.
+constexpr int64_t kLinearMinBytes = int64_t(64) << 20;
+
 namespace sq {
 namespace {
 
@@ -23,6 +28,7 @@ struct Workspace {
 
 std::mutex g_ws_mutex;
 Workspace g_ws[kMaxDevices];
+Workspace g_cnt[kMaxDevices];
 int g_cus[kMaxDevices];
 
 }  // namespace
@@ -79,6 +85,37 @@ void* workspace(size_t bytes) {
   ws.ptr = p;
   ws.bytes = want;
   return p;
+}
+
+int32_t* zeroed_counters(size_t count) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  const size_t bytes = count * sizeof(int32_t);
+  std::lock_guard<std::mutex> lock(g_ws_mutex);
+  Workspace& c = g_cnt[dev];
+  if (c.bytes >= bytes && c.ptr) return static_cast<int32_t*>(c.ptr);
+  size_t want = bytes > 2 * c.bytes ? bytes : 2 * c.bytes;
+  const size_t grain = size_t(64) << 10;
+  want = (want + grain - 1) / grain * grain;
+  if (c.ptr) {
+    if (hipDeviceSynchronize() != hipSuccess) return nullptr;
+    (void)hipFree(c.ptr);
+    c.ptr = nullptr;
+    c.bytes = 0;
+  }
+  void* p = nullptr;
+  if (hipMalloc(&p, want) != hipSuccess) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  if (hipMemset(p, 0, want) != hipSuccess) {
+    (void)hipGetLastError();
+    (void)hipFree(p);
+    return nullptr;
+  }
+  c.ptr = p;
+  c.bytes = want;
+  return static_cast<int32_t*>(p);
 }
 
 }  // namespace sq
@@ -192,7 +229,9 @@ sq_status sq_qgemv_w8a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t*
   const Range ins[] = {{x, (size_t)m * k * 2}, {codes, nk}, {scales, (size_t)n * 4}};
   if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
   (void)hipGetLastError();
-  return device_status(sq::launch_gemv_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream));
+  return device_status(n * k >= kLinearMinBytes
+                           ? sq::launch_linear_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream)
+                           : sq::launch_gemv_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream));
 }
 
 sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint16_t* w16, int64_t n, void* y,
@@ -206,7 +245,9 @@ sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint
   const Range ins[] = {{x, (size_t)m * k * 2}, {w16, (size_t)n * k * 2}};
   if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
   (void)hipGetLastError();
-  return device_status(sq::launch_gemm_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream));
+  return device_status(m <= 16 && n * k * 2 >= kLinearMinBytes
+                           ? sq::launch_linear_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream)
+                           : sq::launch_gemm_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream));
 }
 
 sq_status sq_spec_accept(const float* draft_logits, const float* target_logits, const int32_t* draft_tokens,

@@ -12,6 +12,12 @@ namespace sq {
 // device (grown on demand, never shrunk).  Returns nullptr on failure.
 void* workspace(size_t bytes);
 
+// At least `count` int32 counters on the current device that are zero
+// between launches: zeroed when allocated (grown on demand, never shrunk);
+// every kernel that counts on them returns them to zero before it ends.
+// Returns nullptr on failure.
+int32_t* zeroed_counters(size_t count);
+
 // Compute units of the current device (cached per device).
 int cu_count();
 
@@ -30,6 +36,15 @@ hipError_t launch_gemv_w8(const uint16_t* x, int m, int64_t k, const uint8_t* co
                           int64_t n, void* y, bool f16_out, hipStream_t stream);
 hipError_t launch_gemm_f16(const uint16_t* x, int m, int64_t k, const uint16_t* w, int64_t n, void* y,
                            bool f16_out, hipStream_t stream);
+
+// The matrix-core streaming kernels (one implementation for the three weight
+// kinds; m <= 8 for INT4 / FP8, m <= 64 for FP16).
+hipError_t launch_linear_w4(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const uint16_t* scales,
+                            const uint16_t* zeros, int64_t n, void* y, bool f16_out, hipStream_t stream);
+hipError_t launch_linear_w8(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const float* scales,
+                            int64_t n, void* y, bool f16_out, hipStream_t stream);
+hipError_t launch_linear_f16(const uint16_t* x, int m, int64_t k, const uint16_t* w, int64_t n, void* y,
+                             bool f16_out, hipStream_t stream);
 
 // Sum of S split-K partials [S][mn] fp32 into y[mn] (fixed order s = 0..S-1).
 hipError_t launch_splitk_reduce(const float* partial, int splits, int64_t mn, void* y, bool f16_out,

@@ -87,7 +87,10 @@ def test_quantize_fp8_nonfinite_flag():
 
 
 # ----------------------------------------------------------------- GEMV ----
-GEMV_SHAPES = [(1, 128), (37, 384), (896, 896), (4864, 896), (896, 4864), (257, 3584), (130, 18944)]
+# (3, 8192) and (2, 16384): a few rows with long rows, so tasks span several
+# wavefronts of one workgroup with idle wavefronts between them
+GEMV_SHAPES = [(1, 128), (37, 384), (896, 896), (4864, 896), (896, 4864), (257, 3584), (130, 18944), (3, 8192),
+               (2, 16384)]
 
 
 def _gemv_inputs(m, n, k, seed):
@@ -111,7 +114,7 @@ def test_qgemv_w4a16_parity(m, n, k):
 
 
 @pytest.mark.parametrize("n,k", [(1, 16), (37, 400), (896, 896), (4864, 896), (896, 4864), (257, 3584),
-                                 (130, 18944)])
+                                 (130, 18944), (3, 8192), (5, 4096)])
 @pytest.mark.parametrize("m", [1, 2, 4, 5, 8])
 def test_qgemv_w8a16_parity(m, n, k):
     w, x = _gemv_inputs(m, n, k, 11)
@@ -311,3 +314,41 @@ def test_repeat_runs_are_bitwise_identical():
     r1 = _run_accept(draft, target, tok, u24, 1.0)
     r2 = _run_accept(draft, target, tok, u24, 1.0)
     assert np.array_equal(r1[0], r2[0]) and np.array_equal(r1[1], r2[1])
+
+
+# ------------------------------------------- large matrices (matrix cores) ----
+# Matrices of 64 MB and more stream through the matrix-core kernel: ragged
+# row counts and k (partial 16-byte slabs), and k long enough that the
+# activations are cut into slices summed by a second kernel.
+LARGE_GEMM = [(1, 16384, 4096), (5, 16384, 4096), (16, 16384, 4096), (5, 16381, 4104), (7, 16381, 4104),
+              (16, 2048, 32768)]
+
+
+@pytest.mark.parametrize("m,n,k", LARGE_GEMM)
+def test_verify_gemm_f16_large_parity(m, n, k):
+    w, x = _gemv_inputs(m, n, k, 14)
+    y_ref, d_ref = oracle.gemm_f16(bits16(x), bits16(w))
+    wd, xd = w.to(DEV), x.to(DEV)
+    for dt in (torch.float32, torch.float16):
+        y = sq.sq_verify_gemm_f16(xd, wd, y_dtype=dt)
+        err = oracle.normalised_error(y.float().cpu().numpy(), y_ref, d_ref)
+        assert err <= GEMV_TOL, (dt, err)
+    assert torch.equal(sq.sq_verify_gemm_f16(xd, wd), sq.sq_verify_gemm_f16(xd, wd))
+
+
+LARGE_W8 = [(1, 16384, 4096), (4, 16384, 4096), (8, 16384, 4096), (4, 16381, 4112), (8, 4096, 16384)]
+
+
+@pytest.mark.parametrize("m,n,k", LARGE_W8)
+def test_qgemv_w8a16_large_parity(m, n, k):
+    w, x = _gemv_inputs(m, n, k, 15)
+    wd, xd = w.to(DEV), x.to(DEV)
+    codes, scales = sq.sq_quantize_fp8_e4m3(wd)
+    c_ref, s_ref = oracle.quantize_fp8_e4m3(bits16(w))
+    assert np.array_equal(codes.cpu().numpy(), c_ref)
+    y_ref, d_ref = oracle.qgemv_w8a16(bits16(x), c_ref, s_ref)
+    for dt in (torch.float32, torch.float16):
+        y = sq.sq_qgemv_w8a16(xd, codes, scales, y_dtype=dt)
+        err = oracle.normalised_error(y.float().cpu().numpy(), y_ref, d_ref)
+        assert err <= GEMV_TOL, (dt, err)
+    assert torch.equal(sq.sq_qgemv_w8a16(xd, codes, scales), sq.sq_qgemv_w8a16(xd, codes, scales))
