@@ -4,13 +4,16 @@
 //
 // The kernels are HBM-bound: each weight byte is read once, with 16-byte
 // loads, 32 contiguous bytes per lane per row.  A task is a block of four
-// rows; one step of a task is 64 lanes x 32 bytes of each of its rows.  The
-// grid is persistent: a workgroup stages the activations of its K range in
-// LDS once and walks tasks; its NW wavefronts (NW = min(4, steps per task))
-// split each task's steps, fetching their next step while computing the
-// current one, so every CU keeps ~16 wavefronts x 16 KB of codes in flight.
-// Row sums are reduced across a wavefront with DPP and across the
-// workgroup's wavefronts through LDS, in a fixed order.
+// rows; one step of a task is 64 lanes x 32 bytes of each of its rows.  A
+// team of NW wavefronts (NW = min(4, steps per task)) works on one task at a
+// time, its wavefronts splitting the task's steps; a workgroup holds T teams
+// and stages the activations of its K range in LDS once for all of them.  The
+// grid is persistent, about 16 wavefronts per CU: teams walk tasks with a
+// stride of the total team count, fetching their next step while computing
+// the current one.  Row sums are reduced across a wavefront with DPP and across
+// a team's wavefronts through LDS, in a fixed order; teams of several
+// wavefronts advance through their tasks in step with the workgroup's
+// barriers (a team without a task left runs an unstored copy of its last).
 //
 // INT4 (W4A16).  A lane's 32 bytes are 64 consecutive 4-bit codes of one row,
 // i.e. half of one 128-element group.  Each 32-bit word (codes of k..k+7) is
@@ -33,13 +36,16 @@
 namespace sq {
 namespace {
 
-// rows of a task: four for m <= 2; two for larger m, where the activation
-// fragments need the registers
-constexpr int rows_for(int m) { return m <= 2 ? 4 : 2; }
+// rows of a task: four for m <= 2, two for m <= 4, one above, where the
+// activation fragments need the registers
+constexpr int rows_for(int m) { return m <= 2 ? 4 : (m <= 4 ? 2 : 1); }
 constexpr int kLaneBytes = 32;              // code bytes per lane per row and step
 constexpr size_t kLdsBudget = 64 * 1024;    // activation bytes one workgroup may stage
 #ifndef SQ_GEMV_WAVES_PER_CU
 #define SQ_GEMV_WAVES_PER_CU 16             // resident wavefronts per CU in the persistent grid
+#endif
+#ifndef SQ_GEMV_TEAMS_MAX
+#define SQ_GEMV_TEAMS_MAX 4                 // teams per workgroup, at most (2 for 4-wavefront teams; measured)
 #endif
 
 template <int Ctrl>
@@ -142,28 +148,59 @@ __device__ __forceinline__ Frag<R> load_frag(const TaskPtr& t, int row_bytes, in
 // halves of word w in the order x[8w+0], x[8w+4], x[8w+1], x[8w+5], x[8w+2],
 // x[8w+6], x[8w+3], x[8w+7] -- the nibble pairs of a code word.
 // FP8 layout: xs [M][4 cells][nchunk][8 halves] in natural order.
-template <int M, bool W8, int NThreads>
-__device__ __forceinline__ void stage_x(const uint16_t* __restrict__ x, int64_t k, int64_t k0, int64_t kl, int nchunk,
-                                        half_t* xs) {
-  constexpr int kCells = W8 ? 4 : 8;  // 16-byte cells of x per chunk and row
-  for (int idx = threadIdx.x; idx < nchunk * M * kCells; idx += NThreads) {
-    const int c = idx / (M * kCells), rem = idx % (M * kCells), m = rem / kCells, w = rem % kCells;
-    const int64_t kk = (int64_t)c * (W8 ? 32 : 64) + 8 * w;
-    const u32x4 raw = kk < kl ? *reinterpret_cast<const u32x4*>(x + (int64_t)m * k + k0 + kk) : u32x4{0u, 0u, 0u, 0u};
-    u32x4 out = raw;
-    if constexpr (!W8) {
-      // halves (x0,x1),(x2,x3),(x4,x5),(x6,x7) -> (x0,x4),(x1,x5),(x2,x6),(x3,x7)
-      out[0] = __builtin_amdgcn_perm(raw[2], raw[0], 0x05040100u);
-      out[1] = __builtin_amdgcn_perm(raw[2], raw[0], 0x07060302u);
-      out[2] = __builtin_amdgcn_perm(raw[3], raw[1], 0x05040100u);
-      out[3] = __builtin_amdgcn_perm(raw[3], raw[1], 0x07060302u);
-    }
-    *reinterpret_cast<u32x4*>(xs + (((size_t)m * kCells + w) * nchunk + c) * 8) = out;
+template <int M, bool W8>
+__device__ __forceinline__ u32x4 x_cell(const uint16_t* __restrict__ x, int64_t k, int64_t k0, int64_t kl, int c,
+                                        int m, int w) {
+  const int64_t kk = (int64_t)c * (W8 ? 32 : 64) + 8 * w;
+  const u32x4 raw = kk < kl ? *reinterpret_cast<const u32x4*>(x + (int64_t)m * k + k0 + kk) : u32x4{0u, 0u, 0u, 0u};
+  u32x4 out = raw;
+  if constexpr (!W8) {
+    // halves (x0,x1),(x2,x3),(x4,x5),(x6,x7) -> (x0,x4),(x1,x5),(x2,x6),(x3,x7)
+    out[0] = __builtin_amdgcn_perm(raw[2], raw[0], 0x05040100u);
+    out[1] = __builtin_amdgcn_perm(raw[2], raw[0], 0x07060302u);
+    out[2] = __builtin_amdgcn_perm(raw[3], raw[1], 0x05040100u);
+    out[3] = __builtin_amdgcn_perm(raw[3], raw[1], 0x07060302u);
   }
+  return out;
 }
 
+// Activations staged in LDS by the whole workgroup.  The loads of the first
+// batch (B cells per thread, all of x for up to B * blockDim.x cells) are
+// issued before the weight prefetch, so that they do not queue behind it in
+// HBM; their stores follow once the weight loads are in flight.
+template <int M, bool W8>
+struct XStage {
+  static constexpr int kCells = W8 ? 4 : 8;  // 16-byte cells of x per chunk and row
+  static constexpr int B = M <= 4 ? 8 : 2;   // fewer held cells where the activation fragments need registers
+  u32x4 v[B];
+
+  __device__ __forceinline__ void load(const uint16_t* __restrict__ x, int64_t k, int64_t k0, int64_t kl, int nchunk,
+                                       int base) {
+    const int total = nchunk * M * kCells, nthreads = (int)blockDim.x;
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+      int idx = base + i * nthreads + (int)threadIdx.x;
+      idx = idx < total ? idx : total - 1;
+      const int c = idx / (M * kCells), rem = idx % (M * kCells);
+      v[i] = x_cell<M, W8>(x, k, k0, kl, c, rem / kCells, rem % kCells);
+    }
+  }
+
+  __device__ __forceinline__ void store(int nchunk, int base, half_t* xs) const {
+    const int total = nchunk * M * kCells, nthreads = (int)blockDim.x;
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+      const int idx = base + i * nthreads + (int)threadIdx.x;
+      if (idx < total) {
+        const int c = idx / (M * kCells), rem = idx % (M * kCells), m = rem / kCells, w = rem % kCells;
+        *reinterpret_cast<u32x4*>(xs + (((size_t)m * kCells + w) * nchunk + c) * 8) = v[i];
+      }
+    }
+  }
+};
+
 template <int M, bool W8, int NW>
-__global__ __launch_bounds__(NW * 64) void gemv_kernel(const uint16_t* __restrict__ x, int64_t k, int64_t kslice,
+__global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__ x, int64_t k, int64_t kslice,
                                                        const uint8_t* __restrict__ codes,
                                                        const uint16_t* __restrict__ scales16,
                                                        const uint16_t* __restrict__ zeros16,
@@ -179,23 +216,39 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(const uint16_t* __restric
   const int64_t kl = (k - k0) < kslice ? (k - k0) : kslice;
   const int nchunk = (int)((kl + kChunkK - 1) / kChunkK);
   const int nit = (nchunk + kWave - 1) / kWave;  // >= NW by the host's choice of NW
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int team = wave / NW, wt = wave % NW;         // team in the workgroup, wavefront in the team
+  const int nteam = (int)(blockDim.x >> 6) / NW;      // teams per workgroup
+  const int64_t tstride = (int64_t)gridDim.x * nteam;  // teams in the grid: the task stride
   const int64_t ntask = (n + R - 1) / R;
-  int64_t task = blockIdx.x;
-  int it = wave;
+  // multi-wavefront teams meet at barriers, so every team of the grid runs
+  // the same number of tasks (ntask_pad / tstride); single-wavefront teams
+  // stop at ntask
+  const int64_t ntask_pad = NW > 1 ? (ntask + tstride - 1) / tstride * tstride : ntask;
+  int64_t task = (int64_t)blockIdx.x * nteam + team;
+  int it = wt;
   half_t* xs = reinterpret_cast<half_t*>(smem);
-  float* red = reinterpret_cast<float*>(smem + (size_t)M * kCells * nchunk * 16);  // [NW][R][M]
+  float* red = reinterpret_cast<float*>(smem + (size_t)M * kCells * nchunk * 16);  // [teams][NW][R][M]
 
   const int row_bytes = (int)(W8 ? k : (k >> 1));
   const int groups = (int)(k >> 7);
 
-  // the first fragment is in flight while the activations are staged
+  // activations first, then the first fragment, so that x is not queued
+  // behind the weight stream
+  XStage<M, W8> xst;
+  xst.load(x, k, k0, kl, nchunk, 0);
   Frag<R> fa, fb;
   TaskPtr tp = task_ptr<W8, R>(codes, scales16, zeros16, n, k, k0, task < ntask ? task : ntask - 1);
   fa = load_frag<W8, R>(tp, row_bytes, groups, kl, nchunk, it, lane);
-  stage_x<M, W8, NW * 64>(x, k, k0, kl, nchunk, xs);
+  xst.store(nchunk, 0, xs);
+  const int xtotal = nchunk * M * kCells, xbatch = XStage<M, W8>::B * (int)blockDim.x;
+  for (int base = xbatch; base < xtotal; base += xbatch) {  // activations beyond the first batch
+    xst.load(x, k, k0, kl, nchunk, base);
+    xst.store(nchunk, base, xs);
+  }
   __syncthreads();
-  if (task >= ntask) return;  // uniform across the workgroup
+  if (task >= ntask_pad) return;  // uniform across the wavefront; never for a multi-wavefront team
 
   // masks and magic numbers in VGPRs, so each mask-and-insert is one v_and_or_b32
   uint32_t mlo = 0x000F000Fu, mhi = 0x00F000F0u, k1024 = 0x64006400u, k64 = 0x54005400u;
@@ -214,8 +267,8 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(const uint16_t* __restric
     int64_t task_n = task;
     int it_n = it + NW;
     if (it_n >= nit) {
-      it_n = wave;
-      task_n = task + gridDim.x;
+      it_n = wt;
+      task_n = task + tstride;
     }
     const TaskPtr tp_n = task_n == task ? tp : task_ptr<W8, R>(codes, scales16, zeros16, n, k, k0,
                                                              task_n < ntask ? task_n : ntask - 1);
@@ -332,7 +385,7 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(const uint16_t* __restric
       auto emit = [&](int idx, float val) {
         const int r = idx / M, m = idx % M;
         const int64_t row = task * R + r;
-        if (row >= n) return;
+        if (row >= n) return;  // also every row of a padding task (task >= ntask)
         if constexpr (W8) val *= scales32[row];
         if (partial)
           partial[((int64_t)split * M + m) * n + row] = val;
@@ -358,11 +411,11 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(const uint16_t* __restric
           }
         }
         __syncthreads();
-        if (threadIdx.x < R * M) {
-          float out = red[threadIdx.x];
+        if (wt == 0 && lane < R * M) {
+          float out = red[(team * NW) * R * M + lane];
 #pragma unroll
-          for (int wv = 1; wv < NW; ++wv) out += red[wv * R * M + threadIdx.x];
-          emit(threadIdx.x, out);
+          for (int wv = 1; wv < NW; ++wv) out += red[(team * NW + wv) * R * M + lane];
+          emit(lane, out);
         }
         __syncthreads();
       }
@@ -370,7 +423,7 @@ __global__ __launch_bounds__(NW * 64) void gemv_kernel(const uint16_t* __restric
     task = task_n;
     it = it_n;
     tp = tp_n;
-    return task < ntask;
+    return task < ntask_pad;
   };
 
   while (step(fa, fb) && step(fb, fa)) {
@@ -395,15 +448,23 @@ hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits,
   const int64_t kfirst = kslice < k ? kslice : k;
   const int64_t nchunk = (kfirst + chunk_k - 1) / chunk_k;
   constexpr int R = rows_for(M);
-  const size_t lds = (size_t)M * 2 * (size_t)(nchunk * chunk_k) + (NW > 1 ? (size_t)NW * R * M * 4 : 0);
   const int64_t ntask = (n + R - 1) / R;
-  int64_t per_cu = SQ_GEMV_WAVES_PER_CU / NW;
-  const int64_t resident = resident_blocks(reinterpret_cast<const void*>(&gemv_kernel<M, W8, NW>), NW * 64, lds);
-  if (resident < per_cu) per_cu = resident;
-  const int64_t cap = (int64_t)cu_count() * per_cu;
-  const dim3 grid((unsigned)(ntask < cap ? ntask : cap), (unsigned)splits);
-  hipLaunchKernelGGL((gemv_kernel<M, W8, NW>), grid, dim3(NW * 64), lds, stream, x, k, kslice, codes, scales16,
-                     zeros16, scales32, n, y, (int)f16_out, partial);
+  const int64_t cus = cu_count();
+  // teams: as many as the CUs hold (SQ_GEMV_WAVES_PER_CU wavefronts each) or
+  // as there are tasks; teams per workgroup: enough to cover the CUs once
+  const int64_t per_cu = SQ_GEMV_WAVES_PER_CU / NW > 0 ? SQ_GEMV_WAVES_PER_CU / NW : 1;
+  int64_t teams = ntask < cus * per_cu / splits ? ntask : cus * per_cu / splits;
+  if (teams < 1) teams = 1;
+  int64_t T = (teams + cus / splits - 1) / (cus / splits > 0 ? cus / splits : 1);
+  if (T > per_cu) T = per_cu;
+  const int64_t tmax = NW >= 4 ? (SQ_GEMV_TEAMS_MAX + 1) / 2 : SQ_GEMV_TEAMS_MAX;
+  if (T > tmax) T = tmax;
+  if (T < 1) T = 1;
+  const int64_t blocks = (teams + T - 1) / T;
+  const size_t lds = (size_t)M * 2 * (size_t)(nchunk * chunk_k) + (NW > 1 ? (size_t)T * NW * R * M * 4 : 0);
+  const dim3 grid((unsigned)blocks, (unsigned)splits);
+  hipLaunchKernelGGL((gemv_kernel<M, W8, NW>), grid, dim3((unsigned)(T * NW * 64)), lds, stream, x, k, kslice, codes,
+                     scales16, zeros16, scales32, n, y, (int)f16_out, partial);
   return hipGetLastError();
 }
 

@@ -144,21 +144,27 @@ __device__ __forceinline__ u32x4 x_cell(const uint16_t* __restrict__ x, int64_t 
 
 // Activations of a K slice in LDS: row m at cells [m * stride, + kl_cells);
 // a cell holds 8 consecutive k (INT4: in the order 0,4,1,5,2,6,3,7 -- the
-// nibble pairs of a code word); k past the slice is zero.  Each thread issues
-// its loads in batches of eight before storing, so the L2 round trips overlap.
+// nibble pairs of a code word); k past the slice is zero.  The loads of a
+// batch (eight cells per thread) are issued before the weight prefetch, so
+// that they do not queue behind it in HBM; the stores follow.
 template <int KIND>
-__device__ __forceinline__ void stage_x(const uint16_t* __restrict__ x, int M, int64_t k, const Geo& g, int kl_cells,
-                                        half_t* xs, int nthreads) {
-  constexpr int B = 8;
-  const int total = M * kl_cells;
-  for (int base = 0; base < total; base += B * nthreads) {
-    u32x4 v[B];
+struct XStage {
+  static constexpr int B = 8;
+  u32x4 v[B];
+
+  __device__ __forceinline__ void load(const uint16_t* __restrict__ x, int M, int64_t k, const Geo& g, int kl_cells,
+                                       int base) {
+    const int total = M * kl_cells, nthreads = (int)blockDim.x;
 #pragma unroll
     for (int i = 0; i < B; ++i) {
-      const int idx = base + i * nthreads + (int)threadIdx.x;
-      const int ic = idx < total ? idx : total - 1;
-      v[i] = x_cell<KIND>(x, k, g, ic / kl_cells, ic % kl_cells);
+      int idx = base + i * nthreads + (int)threadIdx.x;
+      idx = idx < total ? idx : total - 1;
+      v[i] = x_cell<KIND>(x, k, g, idx / kl_cells, idx % kl_cells);
     }
+  }
+
+  __device__ __forceinline__ void store(int M, const Geo& g, int kl_cells, int base, half_t* xs) const {
+    const int total = M * kl_cells, nthreads = (int)blockDim.x;
 #pragma unroll
     for (int i = 0; i < B; ++i) {
       const int idx = base + i * nthreads + (int)threadIdx.x;
@@ -166,7 +172,7 @@ __device__ __forceinline__ void stage_x(const uint16_t* __restrict__ x, int M, i
         *reinterpret_cast<u32x4*>(xs + ((size_t)(idx / kl_cells) * g.xs_stride + idx % kl_cells) * 8) = v[i];
     }
   }
-}
+};
 
 __device__ __forceinline__ int64_t part_begin(int64_t i, int64_t total, int64_t parts) { return i * total / parts; }
 __device__ __forceinline__ int64_t part_owner(int64_t j, int64_t total, int64_t parts) {
@@ -215,10 +221,18 @@ void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t ksl
   const int64_t t_first = f_beg / g.S;
   const int col = lane & 15, q = lane >> 4;
 
-  // the first unit is in flight while the activations are staged
+  // activations first, then the first unit, so that x is not queued behind
+  // the weight stream
+  XStage<KIND> xst;
+  xst.load(x, M, k, g, kl_cells, 0);
   Unit<KIND> fa, fb;
   if (f_beg < f_end) fa = load_unit<KIND>(w, scales16, zeros16, g, t_first, (int)(f_beg - t_first * g.S), lane);
-  stage_x<KIND>(x, M, k, g, kl_cells, xs, NW * 64);
+  xst.store(M, g, kl_cells, 0, xs);
+  const int xbatch = XStage<KIND>::B * (int)blockDim.x;
+  for (int base = xbatch; base < M * kl_cells; base += xbatch) {  // activations beyond the first batch
+    xst.load(x, M, k, g, kl_cells, base);
+    xst.store(M, g, kl_cells, base, xs);
+  }
   __syncthreads();
 
   // a valid activation row for the padding rows of the A tiles (their outputs are dropped)
