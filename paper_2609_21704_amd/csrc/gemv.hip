@@ -36,9 +36,11 @@
 namespace sq {
 namespace {
 
-// rows of a task: four for m <= 2, two for m <= 4, one above, where the
-// activation fragments need the registers
-constexpr int rows_for(int m) { return m <= 2 ? 4 : (m <= 4 ? 2 : 1); }
+// rows of a task, at most: four for m <= 2, two for m <= 4, one above, where
+// the activation fragments need the registers.  A launch takes fewer when the
+// matrix is too short to give every wavefront several tasks (measured: one row
+// for the 7B q|k|v / o / down shapes, two for gate|up, four for the LM head).
+constexpr int max_rows_for(int m) { return m <= 2 ? 4 : (m <= 4 ? 2 : 1); }
 constexpr int kLaneBytes = 32;              // code bytes per lane per row and step
 constexpr size_t kLdsBudget = 64 * 1024;    // activation bytes one workgroup may stage
 #ifndef SQ_GEMV_WAVES_PER_CU
@@ -82,6 +84,11 @@ __device__ __forceinline__ void wave_sums(const float (&v)[4 * T], float (&w)[T]
     w[t] = x;
   }
 }
+
+template <int V>
+struct IntC {
+  static constexpr int value = V;
+};
 
 template <int R>
 struct Frag {
@@ -199,7 +206,7 @@ struct XStage {
   }
 };
 
-template <int M, bool W8, int NW>
+template <int M, bool W8, int R, int NW>
 __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__ x, int64_t k, int64_t kslice,
                                                        const uint8_t* __restrict__ codes,
                                                        const uint16_t* __restrict__ scales16,
@@ -209,7 +216,6 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
                                                        float* __restrict__ partial) {
   extern __shared__ __align__(16) char smem[];
   constexpr int kCells = W8 ? 4 : 8;
-  constexpr int R = rows_for(M);
   constexpr int kChunkK = W8 ? 32 : 64;  // weights per 32-byte lane chunk
   const int split = blockIdx.y;
   const int64_t k0 = (int64_t)split * kslice;
@@ -440,14 +446,13 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   }
 }
 
-template <int M, bool W8, int NW>
+template <int M, bool W8, int R, int NW>
 hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits, const uint8_t* codes,
                        const uint16_t* scales16, const uint16_t* zeros16, const float* scales32, int64_t n, void* y,
                        bool f16_out, float* partial, hipStream_t stream) {
   constexpr int64_t chunk_k = W8 ? 32 : 64;
   const int64_t kfirst = kslice < k ? kslice : k;
   const int64_t nchunk = (kfirst + chunk_k - 1) / chunk_k;
-  constexpr int R = rows_for(M);
   const int64_t ntask = (n + R - 1) / R;
   const int64_t cus = cu_count();
   // teams: as many as the CUs hold (SQ_GEMV_WAVES_PER_CU wavefronts each) or
@@ -463,7 +468,7 @@ hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits,
   const int64_t blocks = (teams + T - 1) / T;
   const size_t lds = (size_t)M * 2 * (size_t)(nchunk * chunk_k) + (NW > 1 ? (size_t)T * NW * R * M * 4 : 0);
   const dim3 grid((unsigned)blocks, (unsigned)splits);
-  hipLaunchKernelGGL((gemv_kernel<M, W8, NW>), grid, dim3((unsigned)(T * NW * 64)), lds, stream, x, k, kslice, codes,
+  hipLaunchKernelGGL((gemv_kernel<M, W8, R, NW>), grid, dim3((unsigned)(T * NW * 64)), lds, stream, x, k, kslice, codes,
                      scales16, zeros16, scales32, n, y, (int)f16_out, partial);
   return hipGetLastError();
 }
@@ -495,20 +500,40 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
   const int64_t klast = k - (int64_t)(splits - 1) * kslice;
   const int64_t nit_last = ((klast + chunk_k - 1) / chunk_k + kWave - 1) / kWave;
   const int64_t steps = nit < nit_last ? nit : nit_last;
+  // rows per task: the most that still give each resident wavefront at least
+  // two tasks (four rows: eight), one row otherwise
+  const int64_t waves = (int64_t)cu_count() * SQ_GEMV_WAVES_PER_CU;
+  constexpr int RMAX = max_rows_for(M);
+  int rows = 1;
+  if (RMAX >= 4 && (n + 3) / 4 >= 8 * waves)
+    rows = 4;
+  else if (RMAX >= 2 && (n + 1) / 2 >= 2 * waves)
+    rows = 2;
   // one wavefront per task when tasks outnumber the resident wavefronts;
   // otherwise the workgroup's wavefronts split a task's steps
-  const int64_t ntask = (n + rows_for(M) - 1) / rows_for(M);
-  const bool many = ntask >= (int64_t)cu_count() * SQ_GEMV_WAVES_PER_CU;
-  hipError_t err;
-  if (!many && steps >= 4)
-    err = gemv_launch<M, W8, 4>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y, f16_out, partial,
-                                stream);
-  else if (!many && steps >= 2)
-    err = gemv_launch<M, W8, 2>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y, f16_out, partial,
-                                stream);
-  else
-    err = gemv_launch<M, W8, 1>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y, f16_out, partial,
-                                stream);
+  const int64_t ntask = (n + rows - 1) / rows;
+  const int nw = ntask >= waves ? 1 : (steps >= 4 ? 4 : (steps >= 2 ? 2 : 1));
+  hipError_t err = hipErrorInvalidValue;
+  auto go = [&](auto r_tag, auto nw_tag) {
+    constexpr int RR = decltype(r_tag)::value, NN = decltype(nw_tag)::value;
+    err = gemv_launch<M, W8, RR, NN>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y, f16_out, partial,
+                                     stream);
+  };
+  auto with_nw = [&](auto r_tag) {
+    if (nw == 4)
+      go(r_tag, IntC<4>{});
+    else if (nw == 2)
+      go(r_tag, IntC<2>{});
+    else
+      go(r_tag, IntC<1>{});
+  };
+  if constexpr (RMAX >= 4) {
+    if (rows == 4) with_nw(IntC<4>{});
+  }
+  if constexpr (RMAX >= 2) {
+    if (rows == 2) with_nw(IntC<2>{});
+  }
+  if (rows == 1) with_nw(IntC<1>{});
   if (err != hipSuccess || splits == 1) return err;
   return launch_splitk_reduce(partial, splits, (int64_t)M * n, y, f16_out, stream);
 }
