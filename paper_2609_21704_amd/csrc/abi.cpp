@@ -12,9 +12,12 @@
 #include "specquant.h"
 
 // Large matrices stream through the matrix-core kernel; small ones (where
-// the launch and its ramp dominate) and m > 16 use the vector-ALU GEMV and the
-// tile-per-workgroup GEMM, which measured faster there.
-constexpr int64_t kLinearMinBytes = int64_t(64) << 20;
+// its fixed cost of staging activations and combining chunks, about 4 us more
+// than the others', dominates) and m > 16 use the vector-ALU GEMV and the
+// tile-per-workgroup GEMM, which measured faster there.  Thresholds in weight
+// bytes.
+constexpr int64_t kLinearMinBytesF16 = int64_t(32) << 20;
+constexpr int64_t kLinearMinBytesW8 = int64_t(64) << 20;
 
 namespace sq {
 namespace {
@@ -229,7 +232,7 @@ sq_status sq_qgemv_w8a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t*
   const Range ins[] = {{x, (size_t)m * k * 2}, {codes, nk}, {scales, (size_t)n * 4}};
   if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
   (void)hipGetLastError();
-  return device_status(n * k >= kLinearMinBytes
+  return device_status(n * k >= kLinearMinBytesW8
                            ? sq::launch_linear_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream)
                            : sq::launch_gemv_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream));
 }
@@ -245,7 +248,7 @@ sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint
   const Range ins[] = {{x, (size_t)m * k * 2}, {w16, (size_t)n * k * 2}};
   if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
   (void)hipGetLastError();
-  return device_status(m <= 16 && n * k * 2 >= kLinearMinBytes
+  return device_status(m <= 16 && n * k * 2 >= kLinearMinBytesF16
                            ? sq::launch_linear_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream)
                            : sq::launch_gemm_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream));
 }

@@ -1,7 +1,7 @@
 // Weight-streaming linear layers on the matrix cores: the draft projections
 // with the INT4 or FP8 parent (SpecQuant SS III-D.2) and the verification
 // pass with the FP16 parent (SS III-D.3),
-//   y[m][n] = sum_c x[m][c] * W'[n][c],   1 <= m <= 64,
+//   y[m][n] = sum_c x[m][c] * W'[n][c],   1 <= m <= 16,
 // with W' the dequantized weight (INT4: (q - z) * s per 128-element group;
 // FP8: decode(c) * s per row; FP16: W itself).
 //
@@ -10,8 +10,8 @@
 // j-th quarter of each 16-byte-per-lane slab, which is the B operand layout of
 // v_mfma_f32_16x16x32_f16 (lane l: B[8 j .. 8 j + 8)[l % 16]).  The
 // activations are the A operand, read from LDS in the same k order, and the
-// output tile D[m][n] accumulates in fp32 on the matrix cores; m is padded to
-// 16-row tiles (MT of them).
+// output tile D[m][n] accumulates in fp32 on the matrix cores; the m rows
+// are padded to one 16-row tile.
 //   INT4: a 16-byte slab is one 128-element group of 16 rows (quarter j holds
 //     codes 32 j .. 32 j + 32); each 32-bit code word becomes 8 halves without
 //     a conversion instruction (a nibble masked into the mantissa of the
@@ -24,19 +24,23 @@
 //   FP16: the weights are the B operand as loaded.
 //
 // Work split: a unit is one tile x kU slabs along k (4 KB); a task is a tile's
-// units.  The units are split into equal contiguous ranges, one per
-// workgroup, and each workgroup's range into equal contiguous ranges, one per
-// wavefront (stream-K); a wavefront fetches its next unit while it computes
-// the current one.  A task split between wavefronts is summed in wavefront
-// order after the workgroup's barrier (the pieces go through a global scratch
-// buffer, so that LDS holds only activations).  Every workgroup owns at least
-// one task's units, so a task spans at most two workgroups: their two
-// partial sums meet in a 64-bit slot by atomic exchange (the value travels
-// inside the atomic, so no fence is needed); the second to arrive adds
-// lower + upper in that order, stores the result and empties the slot for the
-// next launch.  Results do not depend on timing.  The activations of a K
+// units, cut into chunks of a fixed number of units.  The chunks are split
+// into equal contiguous ranges, one per workgroup.  Inside a workgroup the
+// wavefronts take chunks from a counter in LDS, so that wavefronts the memory
+// system serves faster take more (their progress differs by tens of percent
+// when the shares are fixed); a wavefront fetches its next unit while it
+// computes the current one, and stores each chunk's partial sum in that
+// chunk's LDS slot.  After the workgroup's barrier each task's chunks are
+// added in chunk order, so results do not depend on which wavefront ran
+// which chunk.  Every workgroup owns at least one task's chunks, so a task
+// spans at most two workgroups: their two partial sums meet in a 64-bit slot
+// by atomic exchange (the value travels inside the atomic, so no fence is
+// needed); the second to arrive adds lower + upper in that order, stores the
+// result and empties the slot for the next launch.  The activations of a K
 // slice are staged in LDS once per workgroup; when they do not fit, K is cut
-// into slices whose partial outputs a second kernel adds in slice order.
+// into slices.  Two slices meet per output value in a 64-bit slot the same
+// way (slice 0's partial is the left operand); the partial outputs of more
+// slices are added in slice order by a second kernel.
 #include "sq_device.hpp"
 #include "sq_internal.hpp"
 
@@ -55,10 +59,6 @@ constexpr int words_per_slab() { return KIND == kW4 ? 4 : (KIND == kW8 ? 2 : 1);
 template <int KIND>
 constexpr int weight_bits() { return KIND == kW4 ? 4 : (KIND == kW8 ? 8 : 16); }
 
-template <bool B>
-struct BoolC {
-  static constexpr bool value = B;
-};
 
 template <int KIND>
 struct Unit {
@@ -123,71 +123,101 @@ __device__ __forceinline__ void quarters(uint32_t v, uint32_t (&out)[4]) {
   out[3] = o[1];
 }
 
-// Activations of a K slice in LDS: row m at cells [m * stride, + kl_pad / 8);
-// a cell holds 8 consecutive k (INT4: in the order 0,4,1,5,2,6,3,7 -- the
-// nibble pairs of a code word); k past the slice is zero.
-template <int KIND>
-__device__ __forceinline__ u32x4 x_cell(const uint16_t* __restrict__ x, int64_t k, const Geo& g, int m, int c) {
-  const int64_t kk = (int64_t)c * 8;
-  const u32x4 raw = kk < g.kl ? *reinterpret_cast<const u32x4*>(x + (int64_t)m * k + g.k0 + kk)
-                              : u32x4{0u, 0u, 0u, 0u};
-  u32x4 out = raw;
-  if constexpr (KIND == kW4) {
-    // halves (x0,x1),(x2,x3),(x4,x5),(x6,x7) -> (x0,x4),(x1,x5),(x2,x6),(x3,x7)
-    out[0] = __builtin_amdgcn_perm(raw[2], raw[0], 0x05040100u);
-    out[1] = __builtin_amdgcn_perm(raw[2], raw[0], 0x07060302u);
-    out[2] = __builtin_amdgcn_perm(raw[3], raw[1], 0x05040100u);
-    out[3] = __builtin_amdgcn_perm(raw[3], raw[1], 0x07060302u);
+// floor(a / b) for 0 <= a < 2^52 and 1 <= b < 2^52.  The correctly rounded
+// double quotient is within one of it, and one step corrects that; integer
+// division would expand to a long software sequence.
+__device__ __forceinline__ int64_t div_floor(int64_t a, int64_t b) {
+  int64_t q = (int64_t)((double)a / (double)b);
+  if (q * b > a)
+    --q;
+  else if ((q + 1) * b <= a)
+    ++q;
+  return q;
+}
+
+// q = a / b, r = a % b for 0 <= a < 2^24 and 16 <= b, with rb = 1 / b: the
+// float estimate is off by at most one.
+__device__ __forceinline__ void divmod_cells(int a, int b, float rb, int& q, int& r) {
+  q = (int)((float)a * rb);
+  r = a - q * b;
+  if (r < 0) {
+    --q;
+    r += b;
+  } else if (r >= b) {
+    ++q;
+    r -= b;
   }
-  return out;
 }
 
 // Activations of a K slice in LDS: row m at cells [m * stride, + kl_cells);
 // a cell holds 8 consecutive k (INT4: in the order 0,4,1,5,2,6,3,7 -- the
-// nibble pairs of a code word); k past the slice is zero.  The loads of a
-// batch (eight cells per thread) are issued before the weight prefetch, so
-// that they do not queue behind it in HBM; the stores follow.
+// nibble pairs of a code word); k past the slice is zero.  A thread's cells
+// are the flat indices base + i * blockDim.x + threadIdx.x over [M][kl_cells];
+// their (row, cell) pairs advance by a fixed step, without a division per
+// cell.  The loads of a batch (eight cells per thread) are unconditional (a
+// cell past the end reads the last cell, a k past the slice reads the last
+// k of the slice; neither is used) and are issued before the weight prefetch,
+// so that they do not queue behind it in HBM; the stores follow.
 template <int KIND>
 struct XStage {
   static constexpr int B = 8;
   u32x4 v[B];
+  int row[B], cell[B];
 
   __device__ __forceinline__ void load(const uint16_t* __restrict__ x, int M, int64_t k, const Geo& g, int kl_cells,
                                        int base) {
     const int total = M * kl_cells, nthreads = (int)blockDim.x;
+    const float rb = 1.0f / (float)kl_cells;
+    int m, c, dm, dc;
+    divmod_cells(base + (int)threadIdx.x, kl_cells, rb, m, c);
+    divmod_cells(nthreads, kl_cells, rb, dm, dc);
 #pragma unroll
     for (int i = 0; i < B; ++i) {
-      int idx = base + i * nthreads + (int)threadIdx.x;
-      idx = idx < total ? idx : total - 1;
-      v[i] = x_cell<KIND>(x, k, g, idx / kl_cells, idx % kl_cells);
+      const bool in = base + i * nthreads + (int)threadIdx.x < total;
+      row[i] = in ? m : -1;
+      cell[i] = c;
+      const int64_t kk = (int64_t)c * 8;
+      const int64_t kc = kk < g.kl ? kk : g.kl - 8;
+      const int mr = in ? m : M - 1;
+      v[i] = *reinterpret_cast<const u32x4*>(x + (int64_t)mr * k + g.k0 + kc);
+      c += dc;
+      m += dm;
+      if (c >= kl_cells) {
+        c -= kl_cells;
+        ++m;
+      }
     }
   }
 
-  __device__ __forceinline__ void store(int M, const Geo& g, int kl_cells, int base, half_t* xs) const {
-    const int total = M * kl_cells, nthreads = (int)blockDim.x;
+  __device__ __forceinline__ void store(const Geo& g, half_t* xs) const {
 #pragma unroll
     for (int i = 0; i < B; ++i) {
-      const int idx = base + i * nthreads + (int)threadIdx.x;
-      if (idx < total)
-        *reinterpret_cast<u32x4*>(xs + ((size_t)(idx / kl_cells) * g.xs_stride + idx % kl_cells) * 8) = v[i];
+      if (row[i] < 0) continue;
+      const u32x4 raw = (int64_t)cell[i] * 8 < g.kl ? v[i] : u32x4{0u, 0u, 0u, 0u};
+      u32x4 out = raw;
+      if constexpr (KIND == kW4) {
+        // halves (x0,x1),(x2,x3),(x4,x5),(x6,x7) -> (x0,x4),(x1,x5),(x2,x6),(x3,x7)
+        out[0] = __builtin_amdgcn_perm(raw[2], raw[0], 0x05040100u);
+        out[1] = __builtin_amdgcn_perm(raw[2], raw[0], 0x07060302u);
+        out[2] = __builtin_amdgcn_perm(raw[3], raw[1], 0x05040100u);
+        out[3] = __builtin_amdgcn_perm(raw[3], raw[1], 0x07060302u);
+      }
+      *reinterpret_cast<u32x4*>(xs + ((size_t)row[i] * g.xs_stride + cell[i]) * 8) = out;
     }
   }
 };
 
-__device__ __forceinline__ int64_t part_begin(int64_t i, int64_t total, int64_t parts) { return i * total / parts; }
-__device__ __forceinline__ int64_t part_owner(int64_t j, int64_t total, int64_t parts) {
-  return ((j + 1) * parts - 1) / total;
-}
-
 __device__ __forceinline__ half8_t as_h8(u32x4 v) { return __builtin_bit_cast(half8_t, v); }
 
-template <int KIND, int MT, int NW>
+template <int KIND, int NW>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4)))
 void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t kslice, const uint8_t* __restrict__ w,
                    const uint16_t* __restrict__ scales16, const uint16_t* __restrict__ zeros16,
                    const float* __restrict__ scales32, int64_t n, void* __restrict__ y, int f16_out,
-                   float* __restrict__ split_out, int64_t nwg_max, float* pieces, unsigned long long* xchg) {
+                   float* __restrict__ split_out, int64_t nwg_max, int chunk_units, unsigned long long* xchg,
+                   unsigned long long* slice_xchg) {
   extern __shared__ __align__(16) char smem[];
+  __shared__ int next_chunk;
   constexpr int KS = k_per_slab<KIND>();
   constexpr int UK = kU * KS;  // k per unit
   const int split = blockIdx.y;
@@ -202,98 +232,82 @@ void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t ksl
   g.row_bytes = (k * weight_bits<KIND>()) >> 3;
   g.groups = (int)(k >> 7);
   const int64_t ntask = (n + 15) / 16;
-  const int64_t F = ntask * g.S;
-  int64_t nwg = F / g.S;
-  nwg = nwg < 1 ? 1 : (nwg > nwg_max ? nwg_max : nwg);
+  const int C = chunk_units < g.S ? chunk_units : g.S;
+  const int J = (g.S + C - 1) / C;  // chunks per task: units [j C, min(j C + C, S))
+  const int64_t FC = ntask * J;
+  const int64_t nwg = ntask < nwg_max ? ntask : nwg_max;  // every workgroup owns at least one task's chunks
   const int64_t wg = blockIdx.x;
   if (wg >= nwg) return;  // uniform across the workgroup
-  const int64_t u0 = part_begin(wg, F, nwg), u1 = part_begin(wg + 1, F, nwg), U = u1 - u0;
 
   half_t* xs = reinterpret_cast<half_t*>(smem);
-  // this workgroup's pieces [NW][2][M][16]: after the activations in LDS when
-  // m <= 16, else in the global scratch buffer
-  float* pl = MT == 1 ? reinterpret_cast<float*>(smem + ((size_t)M * g.xs_stride * 16 + 15) / 16 * 16)
-                      : pieces + ((size_t)split * nwg_max + wg) * NW * 2 * M * 16;
+  // the chunks' partial sums [nch][M][16], after the activations in LDS
+  float* pl = reinterpret_cast<float*>(smem + ((size_t)M * g.xs_stride * 16 + 15) / 16 * 16);
 
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int64_t f_beg = u0 + part_begin(wv, U, NW), f_end = u0 + part_begin(wv + 1, U, NW);
-  const int64_t t_first = f_beg / g.S;
   const int col = lane & 15, q = lane >> 4;
 
-  // activations first, then the first unit, so that x is not queued behind
-  // the weight stream
+  // activations first, then the first unit of this wavefront's first chunk
+  // (chunk wv; the others come from the counter), so that x is not queued
+  // behind the weight stream
+  if (threadIdx.x == 0) next_chunk = NW;
   XStage<KIND> xst;
   xst.load(x, M, k, g, kl_cells, 0);
+  // equal contiguous chunk ranges: workgroup wg owns chunks [c0, c1)
+  const int64_t c0 = div_floor(wg * FC, nwg), c1 = div_floor((wg + 1) * FC, nwg);
+  const int nch = (int)(c1 - c0);
+  // local chunk cl: task t, units [b, b_end) of it
+  auto chunk_at = [&](int cl, int64_t& t, int& b, int& b_end) {
+    const int64_t c = c0 + cl;
+    t = div_floor(c, J);
+    b = (int)(c - t * J) * C;
+    b_end = b + C < g.S ? b + C : g.S;
+  };
+  int cl = wv;
+  int64_t t = 0;
+  int b = 0, b_end = 0;
   Unit<KIND> fa, fb;
-  if (f_beg < f_end) fa = load_unit<KIND>(w, scales16, zeros16, g, t_first, (int)(f_beg - t_first * g.S), lane);
-  xst.store(M, g, kl_cells, 0, xs);
+  if (cl < nch) {
+    chunk_at(cl, t, b, b_end);
+    fa = load_unit<KIND>(w, scales16, zeros16, g, t, b, lane);
+  }
+  xst.store(g, xs);
   const int xbatch = XStage<KIND>::B * (int)blockDim.x;
   for (int base = xbatch; base < M * kl_cells; base += xbatch) {  // activations beyond the first batch
     xst.load(x, M, k, g, kl_cells, base);
-    xst.store(M, g, kl_cells, base, xs);
+    xst.store(g, xs);
   }
   __syncthreads();
 
-  // a valid activation row for the padding rows of the A tiles (their outputs are dropped)
-  int arow[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) arow[mt] = (16 * mt + col) < M ? (16 * mt + col) : 0;
-
-  // output value (m, row) of this lane's accumulator element (mt, r)
-  auto emit = [&](int64_t row, int m, float val) {
-    if constexpr (KIND == kW8) val *= scales32[row];
-    if (split_out)
-      split_out[((int64_t)split * M + m) * n + row] = val;
-    else if (f16_out)
-      reinterpret_cast<uint16_t*>(y)[(int64_t)m * n + row] = f32_to_f16_bits(val);
-    else
-      reinterpret_cast<float*>(y)[(int64_t)m * n + row] = val;
-  };
-
-  if (f_beg < f_end) {
-    int64_t t = t_first;
-    int b = (int)(f_beg - t * g.S);
-    int piece_b0 = b;
-    float4_t acc[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[mt] = float4_t{0.f, 0.f, 0.f, 0.f};
+  if (cl < nch) {
+    // a valid activation row for the padding rows of the A tile (their outputs are dropped)
+    const int arow = col < M ? col : 0;
+    float4_t acc = float4_t{0.f, 0.f, 0.f, 0.f};
+    bool more = true;
 
     // masks and magic numbers in VGPRs, so each mask-and-insert is one v_and_or_b32
     uint32_t mlo = 0x000F000Fu, mhi = 0x00F000F0u, k1024 = 0x64006400u, k64 = 0x54005400u;
     asm("" : "+v"(mlo), "+v"(mhi), "+v"(k1024), "+v"(k64));
 
-    auto finish_piece = [&](bool whole) {
-      const int64_t row = t * 16 + col;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = 16 * mt + 4 * q + r;
-          if (m < M) {
-            if (whole) {
-              if (row < n) emit(row, m, acc[mt][r]);
-            } else {
-              pl[(((size_t)wv * 2 + (t == t_first ? 0 : 1)) * M + m) * 16 + col] = acc[mt][r];
-            }
-          }
-        }
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[mt] = float4_t{0.f, 0.f, 0.f, 0.f};
-    };
-
-    auto step = [&](auto prefetch, const Unit<KIND>& cur, Unit<KIND>& nxt) {
-      constexpr bool Prefetch = decltype(prefetch)::value;
+    auto step = [&](const Unit<KIND>& cur, Unit<KIND>& nxt) {
+      // the next unit: the chunk's next, else the first of the next chunk from
+      // the counter, else (none left) this one again, so that the load stays
+      // unconditional
       int64_t t_n = t;
-      int b_n = b + 1;
-      if (b_n == g.S) {
-        b_n = 0;
-        ++t_n;
+      int b_n = b + 1, be_n = b_end, cl_n = cl;
+      bool more_n = true;
+      if (b_n == b_end) {
+        int got = 0;
+        if (lane == 0) got = atomicAdd(&next_chunk, 1);
+        cl_n = __builtin_amdgcn_readfirstlane(got);
+        more_n = cl_n < nch;
+        if (more_n)
+          chunk_at(cl_n, t_n, b_n, be_n);
+        else
+          b_n = b;
       }
-      if constexpr (Prefetch) {
-        nxt = load_unit<KIND>(w, scales16, zeros16, g, t_n, b_n, lane);
-        __builtin_amdgcn_sched_barrier(0);  // issue the loads before the compute below
-      }
+      nxt = load_unit<KIND>(w, scales16, zeros16, g, t_n, b_n, lane);
+      __builtin_amdgcn_sched_barrier(0);  // issue the loads before the compute below
       uint32_t sc[4], zc[4];
       if constexpr (KIND == kW4) {
         quarters(cur.s[0], sc);
@@ -309,7 +323,7 @@ void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t ksl
           const half2_t z2 = __builtin_bit_cast(half2_t, zc[u] | (zc[u] << 16));
           const half2_t c1024 = z2 + half2_t{(half_t)1024.0f, (half_t)1024.0f};
           const half2_t c64 = z2 + half2_t{(half_t)64.0f, (half_t)64.0f};
-          float4_t gacc[MT];
+          float4_t gacc;
 #pragma unroll
           for (int wd = 0; wd < 4; ++wd) {
             const uint32_t qw = c[wd];
@@ -319,17 +333,12 @@ void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t ksl
             const half2_t d2 = __builtin_bit_cast(half2_t, (q8 & mlo) | k1024) - c1024;  // q2 - z, q6 - z
             const half2_t d3 = __builtin_bit_cast(half2_t, (q8 & mhi) | k64) - c64;      // q3 - z, q7 - z
             const half8_t bw = half8_t{d0[0], d0[1], d1[0], d1[1], d2[0], d2[1], d3[0], d3[1]};
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-              const half8_t a = as_h8(*reinterpret_cast<const u32x4*>(
-                  xs + ((size_t)arow[mt] * g.xs_stride + cell0 + wd) * 8));
-              gacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, wd == 0 ? float4_t{0.f, 0.f, 0.f, 0.f}
-                                                                               : gacc[mt], 0, 0, 0);
-            }
+            const half8_t a = as_h8(*reinterpret_cast<const u32x4*>(xs + ((size_t)arow * g.xs_stride + cell0 + wd) * 8));
+            gacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, wd == 0 ? float4_t{0.f, 0.f, 0.f, 0.f} : gacc, 0, 0,
+                                                          0);
           }
           const float s = valid ? f16_bits_to_f32((uint16_t)sc[u]) : 0.f;
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) acc[mt] += s * gacc[mt];
+          acc += s * gacc;
         } else if constexpr (KIND == kW8) {
 #pragma unroll
           for (int wd = 0; wd < 2; ++wd) {
@@ -339,92 +348,125 @@ void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t ksl
             const half2_t h2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w1, 1.0f, false);
             const half2_t h3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w1, 1.0f, true);
             const half8_t bw = half8_t{h0[0], h0[1], h1[0], h1[1], h2[0], h2[1], h3[0], h3[1]};
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-              const half8_t a = as_h8(*reinterpret_cast<const u32x4*>(
-                  xs + ((size_t)arow[mt] * g.xs_stride + cell0 + wd) * 8));
-              acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, acc[mt], 0, 0, 0);
-            }
+            const half8_t a = as_h8(*reinterpret_cast<const u32x4*>(xs + ((size_t)arow * g.xs_stride + cell0 + wd) * 8));
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, acc, 0, 0, 0);
           }
         } else {
           const half8_t bw = as_h8(c);
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            const half8_t a = as_h8(*reinterpret_cast<const u32x4*>(
-                xs + ((size_t)arow[mt] * g.xs_stride + cell0) * 8));
-            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, acc[mt], 0, 0, 0);
-          }
+          const half8_t a = as_h8(*reinterpret_cast<const u32x4*>(xs + ((size_t)arow * g.xs_stride + cell0) * 8));
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, acc, 0, 0, 0);
         }
       }
-      if (b == g.S - 1 || !Prefetch) {  // the end of this wavefront's piece of task t
-        finish_piece(piece_b0 == 0 && b == g.S - 1);
-        piece_b0 = 0;
+      if (b + 1 == b_end) {  // the chunk's last unit: its partial sum goes to the chunk's slot
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = 4 * q + r;
+          if (m < M) pl[((size_t)cl * M + m) * 16 + col] = acc[r];
+        }
+        acc = float4_t{0.f, 0.f, 0.f, 0.f};
       }
       t = t_n;
       b = b_n;
+      b_end = be_n;
+      cl = cl_n;
+      more = more_n;
     };
 
-    // units f_beg .. f_end - 1; every unit but the last prefetches its successor
-    int64_t left = f_end - f_beg;
-    for (; left > 2; left -= 2) {
-      step(BoolC<true>{}, fa, fb);
-      step(BoolC<true>{}, fb, fa);
-    }
-    if (left == 2) {
-      step(BoolC<true>{}, fa, fb);
-      step(BoolC<false>{}, fb, fa);
-    } else {
-      step(BoolC<false>{}, fa, fb);
+    while (true) {
+      step(fa, fb);
+      if (!more) break;
+      step(fb, fa);
+      if (!more) break;
     }
   }
   __syncthreads();
-  if (f_beg >= f_end) return;
 
-  // Tasks split between wavefronts or workgroups: the wavefront holding a
-  // task's last unit inside this workgroup sums its pieces in wavefront
-  // order, then stores the total or meets the other workgroup.
-  const int64_t t_last = (f_end - 1) / g.S;
-  for (int64_t t = t_first; t <= t_last; t += (t_last > t_first ? t_last - t_first : 1)) {
-    const int64_t w_start = t * g.S > u0 ? t * g.S : u0;
-    const int64_t w_stop = (t + 1) * g.S < u1 ? (t + 1) * g.S : u1;
-    const bool in_wg = t * g.S >= u0 && (t + 1) * g.S <= u1;
-    const bool in_wave = w_start >= f_beg && w_stop <= f_end;
-    const bool mine = w_stop - 1 >= f_beg && w_stop - 1 < f_end;
-    if (!(in_wave && in_wg) && mine) {
-      const int wv_lo = (int)part_owner(w_start - u0, U, NW);
-      const int64_t row = t * 16 + col;
-      // the pieces' slots, one per wavefront (-1: that wavefront holds no piece of t)
-      int slot[NW];
+  // the finished value (m, row): row scale (FP8), then y or this slice's partial output
+  auto store_y = [&](int64_t row, int m, float val) {
+    if constexpr (KIND == kW8) val *= scales32[row];
+    if (split_out)
+      split_out[((int64_t)split * M + m) * n + row] = val;
+    else if (f16_out)
+      reinterpret_cast<uint16_t*>(y)[(int64_t)m * n + row] = f32_to_f16_bits(val);
+    else
+      reinterpret_cast<float*>(y)[(int64_t)m * n + row] = val;
+  };
+
+  // Every task with chunks here: its chunks' partial sums are added in chunk
+  // order (wavefront wv takes tasks wv, wv + NW, ...).  A task whose chunks
+  // all lie here is finished; one shared with a neighbouring workgroup meets
+  // the other half in a 64-bit slot.  With two K slices each finished value
+  // then meets the other slice's the same way (slice 0's partial is the left
+  // operand).  The loops stay rolled: this tail runs once per launch, and
+  // unrolled it would be fetched into the instruction cache cold.
+  // Lane quarter q takes output rows m = q + 4 j.
+  constexpr int MQ = 4;
+  const int64_t t_lo = div_floor(c0, J), t_hi = div_floor(c1 - 1, J);
+#pragma unroll 1
+  for (int64_t tt = t_lo + wv; tt <= t_hi; tt += NW) {
+    const int64_t ca = tt * J > c0 ? tt * J : c0, cb = (tt + 1) * J < c1 ? (tt + 1) * J : c1;
+    const int64_t row = tt * 16 + col;
+    int mm[MQ];
+    float val[MQ];
+    bool ok[MQ];
 #pragma unroll
-      for (int u = 0; u < NW; ++u) {
-        const int64_t ub = part_begin(u, U, NW);
-        const bool has = u >= wv_lo && u <= wv && ub != part_begin(u + 1, U, NW);
-        slot[u] = has ? ((u0 + ub) / g.S == t ? 0 : 1) : -1;
+    for (int j = 0; j < MQ; ++j) {
+      mm[j] = q + 4 * j;
+      ok[j] = mm[j] < M;
+      val[j] = 0.f;
+    }
+#pragma unroll 1
+    for (int64_t c = ca; c < cb; ++c) {
+      const float* pc = pl + (size_t)(c - c0) * M * 16 + col;
+#pragma unroll
+      for (int j = 0; j < MQ; ++j)
+        if (ok[j]) val[j] += pc[mm[j] * 16];
+    }
+    unsigned long long oth[MQ];
+    if (ca != tt * J || cb != (tt + 1) * J) {  // shared with a neighbouring workgroup (uniform in the wavefront)
+      const bool upper = tt * J < c0;          // this workgroup holds the task's later chunks
+      unsigned long long* ws = xchg + ((size_t)split * nwg_max + (upper ? wg - 1 : wg)) * M * 16 + col;
+#pragma unroll
+      for (int j = 0; j < MQ; ++j) {
+        oth[j] = 0ull;
+        if (ok[j]) oth[j] = atomicExch(ws + mm[j] * 16, (1ull << 32) | __builtin_bit_cast(uint32_t, val[j]));
       }
-      for (int m = q; m < M; m += 4) {  // each lane quarter takes every fourth output row
-        // fixed trip count: every load is in flight at once; the sum runs in wavefront order
-        float v[NW];
 #pragma unroll
-        for (int u = 0; u < NW; ++u) v[u] = slot[u] >= 0 ? pl[(((size_t)u * 2 + slot[u]) * M + m) * 16 + col] : 0.f;
-        float tot = 0.f;
-#pragma unroll
-        for (int u = 0; u < NW; ++u)
-          if (slot[u] >= 0) tot += v[u];
-        if (!in_wg) {
-          const bool upper = t * g.S < u0;  // this workgroup holds the task's later units
-          const int64_t bnd = upper ? wg - 1 : wg;
-          unsigned long long* slot = xchg + (((size_t)split * nwg_max + bnd) * M + m) * 16 + col;
-          const unsigned long long me = (1ull << 32) | __builtin_bit_cast(uint32_t, tot);
-          const unsigned long long other = atomicExch(slot, me);
-          if (other == 0ull) continue;  // the other workgroup finishes this value
-          const float o = __builtin_bit_cast(float, (uint32_t)(other & 0xFFFFFFFFull));
-          tot = upper ? o + tot : tot + o;
-          atomicExch(slot, 0ull);  // empty for the next launch
+      for (int j = 0; j < MQ; ++j) {
+        if (!ok[j]) continue;
+        if (oth[j] == 0ull) {  // the other workgroup finishes this value
+          ok[j] = false;
+          continue;
         }
-        if (row < n) emit(row, m, tot);
+        const float o = __builtin_bit_cast(float, (uint32_t)(oth[j] & 0xFFFFFFFFull));
+        val[j] = upper ? o + val[j] : val[j] + o;
+        atomicExch(ws + mm[j] * 16, 0ull);  // empty for the next launch
       }
     }
-    if (t_last == t_first) break;
+#pragma unroll
+    for (int j = 0; j < MQ; ++j) ok[j] = ok[j] && row < n;
+    if (slice_xchg) {
+#pragma unroll
+      for (int j = 0; j < MQ; ++j) {
+        oth[j] = 0ull;
+        if (ok[j])
+          oth[j] = atomicExch(slice_xchg + (size_t)mm[j] * n + row, (1ull << 32) | __builtin_bit_cast(uint32_t, val[j]));
+      }
+#pragma unroll
+      for (int j = 0; j < MQ; ++j) {
+        if (!ok[j]) continue;
+        if (oth[j] == 0ull) {  // the other slice finishes this value
+          ok[j] = false;
+          continue;
+        }
+        const float o = __builtin_bit_cast(float, (uint32_t)(oth[j] & 0xFFFFFFFFull));
+        val[j] = split == 0 ? val[j] + o : o + val[j];
+        atomicExch(slice_xchg + (size_t)mm[j] * n + row, 0ull);  // empty for the next launch
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < MQ; ++j)
+      if (ok[j]) store_y(row, mm[j], val[j]);
   }
 }
 
@@ -438,16 +480,19 @@ __global__ __launch_bounds__(256) void slice_reduce_kernel(const float* __restri
   }
 }
 
-template <int KIND, int MT, int NW>
+#ifndef SQ_LINEAR_CHUNK_MIN
+#define SQ_LINEAR_CHUNK_MIN 4  // units per chunk, at least (measured: 4 beats 1 and 2)
+#endif
+constexpr size_t kLdsTotal = 150 * 1024;   // one workgroup per CU
+constexpr size_t kPieceBudget = 32 * 1024; // chunk partial sums
+
+template <int KIND, int NW>
 hipError_t linear_launch(const uint16_t* x, int m, int64_t k, const uint8_t* w, const uint16_t* scales16,
                          const uint16_t* zeros16, const float* scales32, int64_t n, void* y, bool f16_out,
                          hipStream_t stream) {
   constexpr int64_t UK = (int64_t)kU * k_per_slab<KIND>();
-  // LDS: one workgroup per CU; the pieces of split tasks sit there too when m <= 16
-  const size_t lds_pieces = MT == 1 ? (size_t)NW * 2 * m * 16 * sizeof(float) : 0;
-  const size_t x_lds_max = (size_t)150 * 1024 - lds_pieces;
   // K slices of whole units whose activations fit (2 bytes per k and row, plus a pad cell per row)
-  int64_t kmax = (int64_t)(x_lds_max / ((size_t)m * 2)) - 8;
+  int64_t kmax = (int64_t)((kLdsTotal - kPieceBudget) / ((size_t)m * 2)) - 8;
   kmax = kmax / UK * UK;
   if (kmax < UK) return hipErrorInvalidValue;
   const int splits = (int)((k + kmax - 1) / kmax);
@@ -456,30 +501,44 @@ hipError_t linear_launch(const uint16_t* x, int m, int64_t k, const uint8_t* w, 
   const int64_t kfirst = kslice < k ? kslice : k;
   const int64_t S = (kfirst + UK - 1) / UK;
   const int64_t cells = (S * UK / 8) | 1;
-  const size_t lds = ((size_t)m * cells * 16 + 15) / 16 * 16 + lds_pieces;
   const int64_t ntask = (n + 15) / 16;
-  // one workgroup per CU, shared by the slices; each owns at least one task
+  // one workgroup per CU, shared by the slices; each owns at least one task's chunks
   int64_t nwg_max = ntask;
   const int64_t cap = (int64_t)cu_count() * (16 / NW) / splits;
   if (nwg_max > cap) nwg_max = cap;
   if (nwg_max < 1) nwg_max = 1;
-
-  const size_t split_bytes = splits > 1 ? ((size_t)splits * m * n * sizeof(float) + 255) / 256 * 256 : 0;
-  const size_t piece_bytes = MT == 1 ? 0 : (size_t)splits * nwg_max * NW * 2 * m * 16 * sizeof(float);
-  char* ws = nullptr;
-  if (split_bytes + piece_bytes > 0) {
-    ws = static_cast<char*>(workspace(split_bytes + piece_bytes));
-    if (!ws) return hipErrorOutOfMemory;
+  // the smallest chunk whose partial sums ([chunks per workgroup][m][16] floats) fit the budget
+  int64_t C = SQ_LINEAR_CHUNK_MIN, nch_max = 0;
+  for (;; ++C) {
+    const int64_t J = (S + C - 1) / C;
+    nch_max = (ntask * J + nwg_max - 1) / nwg_max;
+    if ((size_t)nch_max * m * 16 * sizeof(float) <= kPieceBudget || C >= S) break;
   }
-  int32_t* slots = zeroed_counters((size_t)2 * splits * nwg_max * m * 16);  // 64-bit meeting slots
+  if ((size_t)nch_max * m * 16 * sizeof(float) > kPieceBudget) return hipErrorInvalidValue;
+  // the kernel's chunk arithmetic is exact below 2^52 (workgroup index x chunks per slice)
+  if ((double)(nwg_max + 1) * (double)(ntask * S) >= 4503599627370496.0) return hipErrorInvalidValue;
+  const size_t lds = ((size_t)m * cells * 16 + 15) / 16 * 16 + (size_t)nch_max * m * 16 * sizeof(float);
+
+  // two K slices meet per output value in a 64-bit slot; more are summed by a second kernel
+  const bool slice_meet = splits == 2;
+  const size_t split_bytes =
+      splits > 1 && !slice_meet ? ((size_t)splits * m * n * sizeof(float) + 255) / 256 * 256 : 0;
+  float* split_out = nullptr;
+  if (split_bytes > 0) {
+    split_out = static_cast<float*>(workspace(split_bytes));
+    if (!split_out) return hipErrorOutOfMemory;
+  }
+  // 64-bit meeting slots: workgroup boundaries of every slice, then one per output value
+  const size_t wg_slots = (size_t)splits * nwg_max * m * 16;
+  const size_t value_slots = slice_meet ? (size_t)m * n : 0;
+  int32_t* slots = zeroed_counters(2 * (wg_slots + value_slots));
   if (!slots) return hipErrorOutOfMemory;
-  float* split_out = splits > 1 ? reinterpret_cast<float*>(ws) : nullptr;
-  float* pieces = reinterpret_cast<float*>(ws + split_bytes);
-  hipLaunchKernelGGL((linear_kernel<KIND, MT, NW>), dim3((unsigned)nwg_max, (unsigned)splits), dim3(NW * 64), lds,
-                     stream, x, m, k, kslice, w, scales16, zeros16, scales32, n, y, (int)f16_out, split_out, nwg_max,
-                     pieces, reinterpret_cast<unsigned long long*>(slots));
+  unsigned long long* xchg = reinterpret_cast<unsigned long long*>(slots);
+  hipLaunchKernelGGL((linear_kernel<KIND, NW>), dim3((unsigned)nwg_max, (unsigned)splits), dim3(NW * 64), lds, stream,
+                     x, m, k, kslice, w, scales16, zeros16, scales32, n, y, (int)f16_out, split_out, nwg_max, (int)C,
+                     xchg, slice_meet ? xchg + wg_slots : nullptr);
   hipError_t err = hipGetLastError();
-  if (err != hipSuccess || splits == 1) return err;
+  if (err != hipSuccess || splits == 1 || slice_meet) return err;
   int64_t blocks = ((int64_t)m * n + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   if (f16_out)
@@ -495,13 +554,8 @@ template <int KIND>
 hipError_t linear_dispatch(const uint16_t* x, int m, int64_t k, const uint8_t* w, const uint16_t* scales16,
                            const uint16_t* zeros16, const float* scales32, int64_t n, void* y, bool f16_out,
                            hipStream_t stream) {
-  if (m <= 16) return linear_launch<KIND, 1, 16>(x, m, k, w, scales16, zeros16, scales32, n, y, f16_out, stream);
-  if constexpr (KIND == kF16) {
-    if (m <= 32) return linear_launch<KIND, 2, 16>(x, m, k, w, scales16, zeros16, scales32, n, y, f16_out, stream);
-    if (m <= 48) return linear_launch<KIND, 3, 16>(x, m, k, w, scales16, zeros16, scales32, n, y, f16_out, stream);
-    if (m <= 64) return linear_launch<KIND, 4, 16>(x, m, k, w, scales16, zeros16, scales32, n, y, f16_out, stream);
-  }
-  return hipErrorInvalidValue;
+  if (m < 1 || m > 16) return hipErrorInvalidValue;
+  return linear_launch<KIND, 16>(x, m, k, w, scales16, zeros16, scales32, n, y, f16_out, stream);
 }
 
 }  // namespace

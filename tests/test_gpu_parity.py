@@ -320,8 +320,9 @@ def test_repeat_runs_are_bitwise_identical():
 # Matrices of 64 MB and more stream through the matrix-core kernel: ragged
 # row counts and k (partial 16-byte slabs), and k long enough that the
 # activations are cut into slices summed by a second kernel.
+# the last three: K cut into two slices that meet per output value, and into nine
 LARGE_GEMM = [(1, 16384, 4096), (5, 16384, 4096), (16, 16384, 4096), (5, 16381, 4104), (7, 16381, 4104),
-              (16, 2048, 32768)]
+              (5, 2048, 18944), (3, 1100, 40000), (16, 2048, 32768)]
 
 
 @pytest.mark.parametrize("m,n,k", LARGE_GEMM)
@@ -336,7 +337,9 @@ def test_verify_gemm_f16_large_parity(m, n, k):
     assert torch.equal(sq.sq_verify_gemm_f16(xd, wd), sq.sq_verify_gemm_f16(xd, wd))
 
 
-LARGE_W8 = [(1, 16384, 4096), (4, 16384, 4096), (8, 16384, 4096), (4, 16381, 4112), (8, 4096, 16384)]
+# the last two: K cut into two slices
+LARGE_W8 = [(1, 16384, 4096), (4, 16384, 4096), (8, 16384, 4096), (4, 16381, 4112), (8, 4096, 16384),
+            (6, 4097, 16400)]
 
 
 @pytest.mark.parametrize("m,n,k", LARGE_W8)
