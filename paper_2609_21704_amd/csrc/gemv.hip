@@ -5,7 +5,8 @@
 // The kernels are HBM-bound: each weight byte is read once, with 16-byte
 // loads, 32 contiguous bytes per lane per row.  A task is a block of four
 // rows; one step of a task is 64 lanes x 32 bytes of each of its rows.  A
-// team of NW wavefronts (NW = min(4, steps per task)) works on one task at a
+// team of nw wavefronts (one per step of a task, up to eight; a task of more
+// steps is shared evenly) works on one task at a
 // time, its wavefronts splitting the task's steps; a workgroup holds T teams
 // and stages the activations of its K range in LDS once for all of them.  The
 // grid is persistent, about 16 wavefronts per CU: teams walk tasks with a
@@ -42,6 +43,7 @@ namespace {
 // for the 7B q|k|v / o / down shapes, two for gate|up, four for the LM head).
 constexpr int max_rows_for(int m) { return m <= 2 ? 4 : (m <= 4 ? 2 : 1); }
 constexpr int kLaneBytes = 32;              // code bytes per lane per row and step
+constexpr int kMaxTeam = 8;                 // wavefronts per team, at most
 constexpr size_t kLdsBudget = 64 * 1024;    // activation bytes one workgroup may stage
 #ifndef SQ_GEMV_WAVES_PER_CU
 #define SQ_GEMV_WAVES_PER_CU 16             // resident wavefronts per CU in the persistent grid
@@ -206,14 +208,14 @@ struct XStage {
   }
 };
 
-template <int M, bool W8, int R, int NW>
+template <int M, bool W8, int R, bool MULTI>
 __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__ x, int64_t k, int64_t kslice,
                                                        const uint8_t* __restrict__ codes,
                                                        const uint16_t* __restrict__ scales16,
                                                        const uint16_t* __restrict__ zeros16,
                                                        const float* __restrict__ scales32, int64_t n,
                                                        void* __restrict__ y, int f16_out,
-                                                       float* __restrict__ partial) {
+                                                       float* __restrict__ partial, int nw_team) {
   extern __shared__ __align__(16) char smem[];
   constexpr int kCells = W8 ? 4 : 8;
   constexpr int kChunkK = W8 ? 32 : 64;  // weights per 32-byte lane chunk
@@ -221,21 +223,22 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
   const int64_t k0 = (int64_t)split * kslice;
   const int64_t kl = (k - k0) < kslice ? (k - k0) : kslice;
   const int nchunk = (int)((kl + kChunkK - 1) / kChunkK);
-  const int nit = (nchunk + kWave - 1) / kWave;  // >= NW by the host's choice of NW
+  const int nit = (nchunk + kWave - 1) / kWave;  // >= nw by the host's choice of nw
+  const int nw = MULTI ? nw_team : 1;            // wavefronts per team
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int team = wave / NW, wt = wave % NW;         // team in the workgroup, wavefront in the team
-  const int nteam = (int)(blockDim.x >> 6) / NW;      // teams per workgroup
+  const int team = wave / nw, wt = wave - team * nw;  // team in the workgroup, wavefront in the team
+  const int nteam = (int)(blockDim.x >> 6) / nw;      // teams per workgroup
   const int64_t tstride = (int64_t)gridDim.x * nteam;  // teams in the grid: the task stride
   const int64_t ntask = (n + R - 1) / R;
   // multi-wavefront teams meet at barriers, so every team of the grid runs
   // the same number of tasks (ntask_pad / tstride); single-wavefront teams
   // stop at ntask
-  const int64_t ntask_pad = NW > 1 ? (ntask + tstride - 1) / tstride * tstride : ntask;
+  const int64_t ntask_pad = MULTI ? (ntask + tstride - 1) / tstride * tstride : ntask;
   int64_t task = (int64_t)blockIdx.x * nteam + team;
   int it = wt;
   half_t* xs = reinterpret_cast<half_t*>(smem);
-  float* red = reinterpret_cast<float*>(smem + (size_t)M * kCells * nchunk * 16);  // [teams][NW][R][M]
+  float* red = reinterpret_cast<float*>(smem + (size_t)M * kCells * nchunk * 16);  // [teams][nw][R][M]
 
   const int row_bytes = (int)(W8 ? k : (k >> 1));
   const int groups = (int)(k >> 7);
@@ -271,7 +274,7 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
   // Returns false when the workgroup has no tasks left.
   auto step = [&](const Frag<R>& cur, Frag<R>& nxt) -> bool {
     int64_t task_n = task;
-    int it_n = it + NW;
+    int it_n = it + nw;
     if (it_n >= nit) {
       it_n = wt;
       task_n = task + tstride;
@@ -400,7 +403,7 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
         else
           reinterpret_cast<float*>(y)[(int64_t)m * n + row] = val;
       };
-      if constexpr (NW == 1) {
+      if constexpr (!MULTI) {
         if (lead) {
 #pragma unroll
           for (int t = 0; t < T; ++t) {
@@ -418,9 +421,8 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
         }
         __syncthreads();
         if (wt == 0 && lane < R * M) {
-          float out = red[(team * NW) * R * M + lane];
-#pragma unroll
-          for (int wv = 1; wv < NW; ++wv) out += red[(team * NW + wv) * R * M + lane];
+          float out = red[(team * nw) * R * M + lane];
+          for (int wv = 1; wv < nw; ++wv) out += red[(team * nw + wv) * R * M + lane];
           emit(lane, out);
         }
         __syncthreads();
@@ -446,10 +448,10 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   }
 }
 
-template <int M, bool W8, int R, int NW>
+template <int M, bool W8, int R, bool MULTI>
 hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits, const uint8_t* codes,
                        const uint16_t* scales16, const uint16_t* zeros16, const float* scales32, int64_t n, void* y,
-                       bool f16_out, float* partial, hipStream_t stream) {
+                       bool f16_out, float* partial, int nw, hipStream_t stream) {
   constexpr int64_t chunk_k = W8 ? 32 : 64;
   const int64_t kfirst = kslice < k ? kslice : k;
   const int64_t nchunk = (kfirst + chunk_k - 1) / chunk_k;
@@ -457,19 +459,22 @@ hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits,
   const int64_t cus = cu_count();
   // teams: as many as the CUs hold (SQ_GEMV_WAVES_PER_CU wavefronts each) or
   // as there are tasks; teams per workgroup: enough to cover the CUs once
-  const int64_t per_cu = SQ_GEMV_WAVES_PER_CU / NW > 0 ? SQ_GEMV_WAVES_PER_CU / NW : 1;
+  const int64_t per_cu = SQ_GEMV_WAVES_PER_CU / nw > 0 ? SQ_GEMV_WAVES_PER_CU / nw : 1;
   int64_t teams = ntask < cus * per_cu / splits ? ntask : cus * per_cu / splits;
   if (teams < 1) teams = 1;
   int64_t T = (teams + cus / splits - 1) / (cus / splits > 0 ? cus / splits : 1);
   if (T > per_cu) T = per_cu;
-  const int64_t tmax = NW >= 4 ? (SQ_GEMV_TEAMS_MAX + 1) / 2 : SQ_GEMV_TEAMS_MAX;
+  // teams per workgroup: at most SQ_GEMV_TEAMS_MAX (half that for teams of four or
+  // more wavefronts), and a divisor of the teams per CU, so that workgroups tile the CUs
+  int64_t tmax = nw >= 4 ? (SQ_GEMV_TEAMS_MAX + 1) / 2 : SQ_GEMV_TEAMS_MAX;
+  while (tmax > 1 && per_cu % tmax != 0) --tmax;
   if (T > tmax) T = tmax;
   if (T < 1) T = 1;
   const int64_t blocks = (teams + T - 1) / T;
-  const size_t lds = (size_t)M * 2 * (size_t)(nchunk * chunk_k) + (NW > 1 ? (size_t)T * NW * R * M * 4 : 0);
+  const size_t lds = (size_t)M * 2 * (size_t)(nchunk * chunk_k) + (MULTI ? (size_t)T * nw * R * M * 4 : 0);
   const dim3 grid((unsigned)blocks, (unsigned)splits);
-  hipLaunchKernelGGL((gemv_kernel<M, W8, R, NW>), grid, dim3((unsigned)(T * NW * 64)), lds, stream, x, k, kslice, codes,
-                     scales16, zeros16, scales32, n, y, (int)f16_out, partial);
+  hipLaunchKernelGGL((gemv_kernel<M, W8, R, MULTI>), grid, dim3((unsigned)(T * nw * 64)), lds, stream, x, k, kslice,
+                     codes, scales16, zeros16, scales32, n, y, (int)f16_out, partial, nw);
   return hipGetLastError();
 }
 
@@ -496,7 +501,7 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
   const int64_t chunk_k = W8 ? 32 : 64;
   const int64_t kfirst = kslice < k ? kslice : k;
   const int64_t nit = ((kfirst + chunk_k - 1) / chunk_k + kWave - 1) / kWave;
-  // the last slice may be shorter: NW must not exceed its step count either
+  // the last slice may be shorter: nw must not exceed its step count either
   const int64_t klast = k - (int64_t)(splits - 1) * kslice;
   const int64_t nit_last = ((klast + chunk_k - 1) / chunk_k + kWave - 1) / kWave;
   const int64_t steps = nit < nit_last ? nit : nit_last;
@@ -510,22 +515,27 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
   else if (RMAX >= 2 && (n + 1) / 2 >= 2 * waves)
     rows = 2;
   // one wavefront per task when tasks outnumber the resident wavefronts;
-  // otherwise the workgroup's wavefronts split a task's steps
+  // otherwise a team of wavefronts splits each task's steps evenly: one step
+  // each up to eight steps, else the fewest steps each that keep the team at
+  // eight or fewer
   const int64_t ntask = (n + rows - 1) / rows;
-  const int nw = ntask >= waves ? 1 : (steps >= 4 ? 4 : (steps >= 2 ? 2 : 1));
+  int nw = 1;
+  if (ntask < waves && steps >= 2) {
+    const int64_t per_wave = (steps + kMaxTeam - 1) / kMaxTeam;
+    nw = (int)((steps + per_wave - 1) / per_wave);
+  }
   hipError_t err = hipErrorInvalidValue;
-  auto go = [&](auto r_tag, auto nw_tag) {
-    constexpr int RR = decltype(r_tag)::value, NN = decltype(nw_tag)::value;
-    err = gemv_launch<M, W8, RR, NN>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y, f16_out, partial,
-                                     stream);
+  auto go = [&](auto r_tag, auto multi_tag) {
+    constexpr int RR = decltype(r_tag)::value;
+    constexpr bool MM = decltype(multi_tag)::value != 0;
+    err = gemv_launch<M, W8, RR, MM>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y, f16_out, partial,
+                                     nw, stream);
   };
   auto with_nw = [&](auto r_tag) {
-    if (nw == 4)
-      go(r_tag, IntC<4>{});
-    else if (nw == 2)
-      go(r_tag, IntC<2>{});
-    else
+    if (nw > 1)
       go(r_tag, IntC<1>{});
+    else
+      go(r_tag, IntC<0>{});
   };
   if constexpr (RMAX >= 4) {
     if (rows == 4) with_nw(IntC<4>{});

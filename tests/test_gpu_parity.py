@@ -128,6 +128,25 @@ def test_qgemv_w8a16_parity(m, n, k):
         assert err <= GEMV_TOL, (dt, err)
 
 
+# Few rows with long rows: each task is split over a team of wavefronts, one
+# per step of the task.  W4 (64 k per lane step, 4096 k per team step): teams
+# of 3, 5, 6, 7 and 8, then two 8-step K slices.  W8 (2048 k per step): 3
+# steps; 10 and 15 steps shared by teams of 5 and 8 (two steps each, the last
+# wavefront of the 8 one).
+TEAM_W4 = [(1, 37, 12288), (1, 37, 18944), (1, 37, 24576), (1, 37, 28672), (1, 37, 32768), (1, 5, 65536)]
+TEAM_W8 = [(1, 37, 6144), (1, 37, 20480), (1, 37, 30720)]
+
+
+@pytest.mark.parametrize("m,n,k", TEAM_W4)
+def test_qgemv_w4a16_team_sizes(m, n, k):
+    test_qgemv_w4a16_parity(m, n, k)
+
+
+@pytest.mark.parametrize("m,n,k", TEAM_W8)
+def test_qgemv_w8a16_team_sizes(m, n, k):
+    test_qgemv_w8a16_parity(m, n, k)
+
+
 def test_qgemv_w8a16_every_code_decodes_exactly():
     """Row c holds code c at column 0 (NaN codes replaced by 0); x = e_0."""
     n, k = 256, 32
