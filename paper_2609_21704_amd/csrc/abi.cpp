@@ -16,7 +16,7 @@
 // than the others', dominates) and m > 16 use the vector-ALU GEMV and the
 // tile-per-workgroup GEMM, which measured faster there.  Thresholds in weight
 // bytes.
-constexpr int64_t kLinearMinBytesF16 = int64_t(32) << 20;
+constexpr int64_t kLinearMinBytesF16 = int64_t(28) << 20;  // between 3584^2 and 4608 x 3584 (7B o, q|k|v)
 constexpr int64_t kLinearMinBytesW8 = int64_t(64) << 20;
 
 namespace sq {

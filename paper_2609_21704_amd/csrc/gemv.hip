@@ -5,8 +5,8 @@
 // The kernels are HBM-bound: each weight byte is read once, with 16-byte
 // loads, 32 contiguous bytes per lane per row.  A task is a block of four
 // rows; one step of a task is 64 lanes x 32 bytes of each of its rows.  A
-// team of nw wavefronts (one per step of a task, up to eight; a task of more
-// steps is shared evenly) works on one task at a
+// team of nw wavefronts (nw = 4 from four steps per task, 2 from two, else 1)
+// works on one task at a
 // time, its wavefronts splitting the task's steps; a workgroup holds T teams
 // and stages the activations of its K range in LDS once for all of them.  The
 // grid is persistent, about 16 wavefronts per CU: teams walk tasks with a
@@ -43,7 +43,6 @@ namespace {
 // for the 7B q|k|v / o / down shapes, two for gate|up, four for the LM head).
 constexpr int max_rows_for(int m) { return m <= 2 ? 4 : (m <= 4 ? 2 : 1); }
 constexpr int kLaneBytes = 32;              // code bytes per lane per row and step
-constexpr int kMaxTeam = 8;                 // wavefronts per team, at most
 constexpr size_t kLdsBudget = 64 * 1024;    // activation bytes one workgroup may stage
 #ifndef SQ_GEMV_WAVES_PER_CU
 #define SQ_GEMV_WAVES_PER_CU 16             // resident wavefronts per CU in the persistent grid
@@ -515,15 +514,11 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
   else if (RMAX >= 2 && (n + 1) / 2 >= 2 * waves)
     rows = 2;
   // one wavefront per task when tasks outnumber the resident wavefronts;
-  // otherwise a team of wavefronts splits each task's steps evenly: one step
-  // each up to eight steps, else the fewest steps each that keep the team at
-  // eight or fewer
+  // otherwise a team of wavefronts splits each task's steps: four from four
+  // steps, two from two (measured: at five steps, four-wavefront teams beat
+  // teams of five, which leave a CU one wavefront short and pad more tasks)
   const int64_t ntask = (n + rows - 1) / rows;
-  int nw = 1;
-  if (ntask < waves && steps >= 2) {
-    const int64_t per_wave = (steps + kMaxTeam - 1) / kMaxTeam;
-    nw = (int)((steps + per_wave - 1) / per_wave);
-  }
+  const int nw = ntask >= waves ? 1 : (steps >= 4 ? 4 : (steps >= 2 ? 2 : 1));
   hipError_t err = hipErrorInvalidValue;
   auto go = [&](auto r_tag, auto multi_tag) {
     constexpr int RR = decltype(r_tag)::value;

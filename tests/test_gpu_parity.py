@@ -128,11 +128,10 @@ def test_qgemv_w8a16_parity(m, n, k):
         assert err <= GEMV_TOL, (dt, err)
 
 
-# Few rows with long rows: each task is split over a team of wavefronts, one
-# per step of the task.  W4 (64 k per lane step, 4096 k per team step): teams
-# of 3, 5, 6, 7 and 8, then two 8-step K slices.  W8 (2048 k per step): 3
-# steps; 10 and 15 steps shared by teams of 5 and 8 (two steps each, the last
-# wavefront of the 8 one).
+# Few rows with long rows: each task's steps are split over a team of
+# wavefronts, some of which take more steps than others.  W4 (4096 k per
+# step): 3, 5, 6, 7 and 8 steps, then two 8-step K slices.  W8 (2048 k per
+# step): 3, 10 and 15 steps.
 TEAM_W4 = [(1, 37, 12288), (1, 37, 18944), (1, 37, 24576), (1, 37, 28672), (1, 37, 32768), (1, 5, 65536)]
 TEAM_W8 = [(1, 37, 6144), (1, 37, 20480), (1, 37, 30720)]
 
