@@ -12,7 +12,8 @@
 //                draw weights R = rint(r * 2^60) in int64 (exact, so the total
 //                does not depend on the summation order);
 //   3. draw:     per sequence, locate the chunk holding t = floor(u Z / 2^24)
-//                from the chunk totals, then scan that chunk.
+//                with a block scan of the chunk totals, then block-scan that
+//                chunk.
 // Greedy uses per-chunk (max, first index) pairs and one decision pass.
 #include <math.h>
 
@@ -81,11 +82,38 @@ __device__ __forceinline__ const float* row_ptr(const float* draft, const float*
   return r < rows_t ? target + r * v : draft + (r - rows_t) * v;
 }
 
-__device__ __forceinline__ void merge_stats(const double2* st, int nchunk, double& L, double& S) {
+// Exclusive prefix sum of v over the 256 threads in thread order; `total`
+// receives the block's sum.  Integer, so exact.
+__device__ int64_t block_exclusive_scan_i64(int64_t v, int64_t* sh, int64_t& total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int64_t x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int64_t y = __shfl_up(x, off, 64);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) sh[w] = x;
+  __syncthreads();
+  int64_t base = 0;
+  for (int i = 0; i < w; ++i) base += sh[i];
+  total = (sh[0] + sh[1]) + (sh[2] + sh[3]);
+  __syncthreads();
+  return base + x - v;
+}
+
+// One wavefront merges a row's chunk partials: L = max over chunks, S = the
+// sum of S_c exp(L_c - L), each lane taking every 64th chunk and the lanes
+// combined in a fixed shuffle tree.  Lane 0's values are returned.
+__device__ void wave_merge(const double2* st, int nchunk, double& L, double& S) {
+  const int lane = threadIdx.x & 63;
   double mx = -INFINITY;
-  for (int c = 0; c < nchunk; ++c) mx = fmax(mx, st[c].x);
+  for (int c = lane; c < nchunk; c += 64) mx = fmax(mx, st[c].x);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off, 64));
   double s = 0.0;
-  for (int c = 0; c < nchunk; ++c) s += st[c].y * exp(st[c].x - mx);
+  for (int c = lane; c < nchunk; c += 64) s += st[c].y * exp(st[c].x - mx);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
   L = mx;
   S = s;
 }
@@ -128,7 +156,14 @@ __global__ __launch_bounds__(kThreads) void probs_kernel(const float* __restrict
   const int c = blockIdx.x % nchunk;
   float* out = row < rows_t ? (p_out ? p_out + row * v : nullptr) : (q_out ? q_out + (row - rows_t) * v : nullptr);
   if (!out) return;  // uniform across the block
-  if (threadIdx.x == 0) merge_stats(stats + row * nchunk, nchunk, sL, sS);
+  if (threadIdx.x < 64) {
+    double L, S;
+    wave_merge(stats + row * nchunk, nchunk, L, S);
+    if (threadIdx.x == 0) {
+      sL = L;
+      sS = S;
+    }
+  }
   __syncthreads();
   const double L = sL, S = sS;
   const float* l = row_ptr(draft, target, rows_t, row, v);
@@ -155,9 +190,15 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(const float* __restric
   const int s = blockIdx.x / nchunk;
   const int c = blockIdx.x % nchunk;
   const int64_t rows_t = (int64_t)b * (kd + 1);
-  for (int rr = threadIdx.x; rr < 2 * kd + 1; rr += kThreads) {
+  // the 2kd + 1 rows' statistics, one wavefront per row
+  for (int rr = threadIdx.x >> 6; rr < 2 * kd + 1; rr += kThreads / 64) {
     const int64_t row = rr <= kd ? (int64_t)s * (kd + 1) + rr : rows_t + (int64_t)(rr - kd - 1) * b + s;
-    merge_stats(stats + row * nchunk, nchunk, sL[rr], sS[rr]);
+    double L, S;
+    wave_merge(stats + row * nchunk, nchunk, L, S);
+    if ((threadIdx.x & 63) == 0) {
+      sL[rr] = L;
+      sS[rr] = S;
+    }
   }
   __syncthreads();
   if (threadIdx.x < kd) {
@@ -221,8 +262,10 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(const float* __restric
   }
 }
 
-// 3. per sequence: the draw.  The chunk is scanned with 16 consecutive logits
-// per thread so that a block-wide exclusive scan of the thread sums orders them.
+// 3. per sequence: the draw.  The chunk holding t is found with a block scan
+// over the chunk totals (256 chunks at a time), then the chunk is scanned
+// with 16 consecutive logits per thread, so that the block's exclusive scan
+// of the thread sums orders them.  All sums are int64, so exact.
 __global__ __launch_bounds__(kThreads) void draw_kernel(const float* __restrict__ draft,
                                                         const float* __restrict__ target,
                                                         const uint32_t* __restrict__ u24, int b, int kd, int v,
@@ -231,53 +274,62 @@ __global__ __launch_bounds__(kThreads) void draw_kernel(const float* __restrict_
                                                         int32_t* __restrict__ n_accepted,
                                                         int32_t* __restrict__ next_token) {
   __shared__ int64_t sOff;
-  __shared__ int sChunk, sWhich;
-  __shared__ int64_t sPre[kThreads];
+  __shared__ int sChunk;
+  __shared__ int64_t shi[4];
   const int s = blockIdx.x;
   const SeqInfo si = info[s];
   const int n = si.n;
-  if (threadIdx.x == 0) {
-    const int64_t* z = zs + (int64_t)s * nchunk * 2;
-    int which = 0;
-    int64_t Z = 0;
-    for (int c = 0; c < nchunk; ++c) Z += z[2 * c];
-    if (Z == 0 && n < kd) {
-      which = 1;
-      for (int c = 0; c < nchunk; ++c) Z += z[2 * c + 1];
-    }
-    int chunk = -1;
-    int64_t off = 0;
-    if (Z > 0) {
-      const uint64_t u = u24[(int64_t)s * (kd + 1) + kd] & 0xFFFFFFu;
-      const uint64_t lo = u * (uint64_t)Z;
-      const uint64_t hi = __umul64hi(u, (uint64_t)Z);
-      const int64_t t = (int64_t)((hi << 40) | (lo >> 24));  // floor(u * Z / 2^24) < Z
-      int64_t run = 0;
-      chunk = nchunk - 1;
-      for (int c = 0; c < nchunk; ++c) {
-        const int64_t zc = z[2 * c + which];
-        if (run + zc > t) {
-          chunk = c;
-          break;
-        }
-        run += zc;
-      }
-      off = t - run;
-    }
-    sChunk = chunk;
-    sWhich = which;
-    sOff = off;
+  const int64_t* z = zs + (int64_t)s * nchunk * 2;
+
+  // the total mass Z of the draw row (the residual's, else p_n's when that is zero on the grid)
+  int64_t part = 0;
+  for (int c = threadIdx.x; c < nchunk; c += kThreads) part += z[2 * c];
+  int64_t Z = block_sum_i64(part, shi);
+  int which = 0;
+  if (Z == 0 && n < kd) {  // uniform across the block
+    which = 1;
+    part = 0;
+    for (int c = threadIdx.x; c < nchunk; c += kThreads) part += z[2 * c + 1];
+    Z = block_sum_i64(part, shi);
   }
-  __syncthreads();
-  const int chunk = sChunk;
-  if (chunk < 0) {  // no mass on the fixed-point grid
+  if (Z == 0) {  // no mass on the fixed-point grid
     if (threadIdx.x == 0) {
       n_accepted[s] = n;
       next_token[s] = -1;
     }
     return;
   }
-  const bool resid = n < kd && sWhich == 0;
+  const uint64_t uu = u24[(int64_t)s * (kd + 1) + kd] & 0xFFFFFFu;
+  const uint64_t lo = uu * (uint64_t)Z;
+  const uint64_t hi = __umul64hi(uu, (uint64_t)Z);
+  const int64_t t = (int64_t)((hi << 40) | (lo >> 24));  // floor(u * Z / 2^24) < Z
+
+  // the chunk c with run(c) <= t < run(c) + z_c, 256 chunks at a time
+  if (threadIdx.x == 0) sChunk = -1;
+  int64_t run = 0;
+  for (int c0 = 0; c0 < nchunk; c0 += kThreads) {
+    const int c = c0 + (int)threadIdx.x;
+    const int64_t zc = c < nchunk ? z[2 * c + which] : 0;
+    int64_t tile;
+    const int64_t pre = run + block_exclusive_scan_i64(zc, shi, tile);
+    if (zc > 0 && pre <= t && t < pre + zc) {
+      sChunk = c;
+      sOff = t - pre;
+    }
+    __syncthreads();
+    if (sChunk >= 0) break;  // uniform across the block
+    run += tile;
+  }
+  const int chunk = sChunk;
+  if (chunk < 0) {  // cannot happen (t < Z); kept so that no index can leave the row
+    if (threadIdx.x == 0) {
+      n_accepted[s] = n;
+      next_token[s] = -1;
+    }
+    return;
+  }
+  const int64_t off = sOff;
+  const bool resid = n < kd && which == 0;
   const float* lp = target + ((int64_t)s * (kd + 1) + n) * v;
   const float* lq = resid ? draft + ((int64_t)n * b + s) * v : nullptr;
   int64_t R[kPer];
@@ -300,26 +352,15 @@ __global__ __launch_bounds__(kThreads) void draw_kernel(const float* __restrict_
     R[e] = w;
     local += w;
   }
-  sPre[threadIdx.x] = local;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int64_t run = 0;
-    for (int i = 0; i < kThreads; ++i) {
-      const int64_t t = sPre[i];
-      sPre[i] = run;
-      run += t;
-    }
-  }
-  __syncthreads();
-  const int64_t pre = sPre[threadIdx.x];
-  const int64_t off = sOff;
+  int64_t tot;
+  const int64_t pre = block_exclusive_scan_i64(local, shi, tot);
   if (local > 0 && pre <= off && off < pre + local) {
-    int64_t run = pre;
+    int64_t acc = pre;
     int tok = beg;
 #pragma unroll
     for (int e = 0; e < kPer; ++e) {
-      run += R[e];
-      if (run > off) {
+      acc += R[e];
+      if (acc > off) {
         tok = beg + e;
         break;
       }
