@@ -10,7 +10,9 @@ with the inputs resident in HBM.
 
 Prints one JSON line: tokens/s (emitted tokens = accepted drafts + 1 per
 sequence and round), the draft GEMV's achieved HBM bandwidth against the
-MI355X peak, and the CPU oracle timed on this host as a baseline.
+MI355X peak, the CPU oracle timed on this host as a baseline, and the same
+stack decoded directly with the FP16 parent (the paper's plain-decoding
+comparison) with the speedup over it.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
 """
@@ -191,6 +193,38 @@ def cpu_baseline(rnd, tokens_per_round: float):
     }
 
 
+def measure_direct(stack, temperature: float, steps: int, warmup: int):
+    """Direct parent inference (SS III-D.5), the paper's plain-decoding
+    baseline: one token per sequence per step from the FP16 parent alone,
+    timed over graph replays like the rounds."""
+    import torch
+
+    from paper_2609_21704_amd import synth
+    from paper_2609_21704_amd.rounds import DirectDecode
+
+    cfg = stack.cfg
+    dd = DirectDecode(stack, temperature=temperature)
+    dd.u.copy_(synth.uniform_u24((cfg.batch, 1), synth.stream_seed(cfg.seed, 99), dd.u.device))
+    dd.capture()
+    for _ in range(warmup):
+        dd.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        dd.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    sec = e0.elapsed_time(e1) * 1e-3
+    return {
+        "tokens_per_s": round(cfg.batch * steps / sec, 3),
+        "ms_per_token": round(sec / steps * 1e3, 4),
+        "steps": steps,
+        "what": "plain FP16 decoding at m = batch: every FP16 matrix streamed once per token, then a draw",
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -259,6 +293,7 @@ def main():
     tokens = int((n_acc + 1).sum())
     tokens_per_round = tokens / (args.steps * cfg.batch)
 
+    direct = measure_direct(stack, args.temperature, args.steps, args.warmup)
     gbytes, gsec, glaunch = measure_gemv(rnd, args.gemv_steps)
     achieved = gbytes / gsec / 1e9
     traffic = traffic_from_profile(stack.variant)
@@ -293,6 +328,8 @@ def main():
         "round_bytes": cfg.round_bytes(),
         "stack_gbs": round(cfg.round_bytes() * args.steps / elapsed / 1e9, 1),
         "wall_s": round(wall, 4),
+        "direct_parent": direct,
+        "speedup_vs_direct": round(tokens / elapsed / direct["tokens_per_s"], 3),
         "roofline": {
             "kernel": f"draft GEMV ({'W4A16' if stack.variant == 'int4' else 'W8A16'}, m={cfg.draft_m})",
             "bound": "hbm",

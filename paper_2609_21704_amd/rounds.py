@@ -23,7 +23,7 @@ from . import synth
 from .configs import Config
 
 # tensor ids for synth.stream_seed(config seed, kind, ...)
-_W, _XD, _XV, _XLMD, _XLMV, _EPS, _UD, _UA, _DL, _BONUS = range(10)
+_W, _XD, _XV, _XLMD, _XLMV, _EPS, _UD, _UA, _DL, _BONUS, _XDIRECT = range(11)
 
 
 class Stack:
@@ -185,6 +185,60 @@ class Round:
     def set_uniforms(self, u_draft: torch.Tensor, u_accept: torch.Tensor):
         self.buf.u_draft.copy_(u_draft)
         self.buf.u_accept.copy_(u_accept)
+
+    def replay(self):
+        self.graph.replay()
+
+
+class DirectDecode:
+    """Direct parent inference (SS III-D.5), the plain-decoding baseline the
+    paper compares against: one token per sequence per step, every FP16
+    matrix streamed once at m = batch rows (the verify call at m = B), then
+    a draw from softmax(logits / T).  Each projection reads its own pre-drawn
+    activation, as in a round."""
+
+    def __init__(self, stack: Stack, temperature: float = 1.0):
+        self.stack = stack
+        cfg = self.cfg = stack.cfg
+        dev = stack.device
+        self.temperature = float(temperature)
+        B, V, L = cfg.batch, cfg.vocab, stack.layers
+        self.x, self.y = {}, {}
+        for name, n, kin in cfg.layer_matrices():
+            self.y[name] = torch.empty((B, n), dtype=torch.float16, device=dev)
+            for l in range(L):
+                mid = 1000 * (l + 1) + ["qkv", "o", "gate_up", "down"].index(name)
+                self.x[(l, name)] = synth.normal_f16((B, kin), 1.0, synth.stream_seed(cfg.seed, _XDIRECT, mid), dev)
+        if cfg.lm_head:
+            self.x[(L, "lm_head")] = synth.normal_f16((B, cfg.hidden), 1.0, synth.stream_seed(cfg.seed, _XDIRECT), dev)
+            self.logits = torch.empty((B, V), dtype=torch.float32, device=dev)
+        else:
+            self.logits = synth.normal_f32((B, V), 2.0, synth.stream_seed(cfg.seed, _BONUS), dev)
+        self.u = torch.zeros((B, 1), dtype=torch.int32, device=dev)
+        self.n_accepted = torch.zeros((B,), dtype=torch.int32, device=dev)
+        self.token = torch.zeros((B,), dtype=torch.int32, device=dev)
+        self.graph = None
+
+    def run(self):
+        st, cfg = self.stack, self.cfg
+        for l in range(st.layers):
+            for name, _, _ in cfg.layer_matrices():
+                st.verify_gemm((l, name), self.x[(l, name)], self.y[name])
+        if cfg.lm_head:
+            st.verify_gemm((cfg.layers, "lm_head"), self.x[(st.layers, "lm_head")], self.logits)
+        B, V = cfg.batch, cfg.vocab
+        sq.sq_spec_accept(None, self.logits.view(B, 1, V), None, self.u, self.temperature,
+                          n_accepted=self.n_accepted, next_token=self.token)
+
+    def capture(self):
+        self.run()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.run()
+        torch.cuda.synchronize()
+        self.graph = g
+        return g
 
     def replay(self):
         self.graph.replay()

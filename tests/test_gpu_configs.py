@@ -16,7 +16,7 @@ import oracle
 import paper_2609_21704_amd as sq
 from paper_2609_21704_amd import synth
 from paper_2609_21704_amd.configs import CONFIGS
-from paper_2609_21704_amd.rounds import Round, Stack, round_uniforms
+from paper_2609_21704_amd.rounds import DirectDecode, Round, Stack, round_uniforms
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -146,3 +146,42 @@ def test_round_graph_replays_match_eager():
         ref = (b.draft_logits, b.target_logits, b.draft_tokens, b.n_accepted, b.next_token)
         for g, e in zip(got, ref):
             assert torch.equal(g, e), r
+
+
+@pytest.mark.parametrize("index", [0, 1])
+def test_direct_decode_matches_oracle(index):
+    """Direct parent inference (the plain-decoding baseline): every FP16
+    projection at m = batch, then the draw, against the oracle at sampled
+    rows; captured as a HIP graph, the replays give the eager step's bits."""
+    cfg = CONFIGS[index]
+    stack = Stack(cfg, DEV, layers=1)
+    dd = DirectDecode(stack, temperature=1.0)
+    dd.u.copy_(synth.uniform_u24((cfg.batch, 1), 77, DEV))
+    dd.run()
+    torch.cuda.synchronize()
+    for j, key in enumerate(sorted(k for k in stack.w16 if k[1] != "lm_head")):
+        w16 = stack.w16[key]
+        rows = sample_rows(w16.shape[0], cfg.seed * 10 + j)
+        idx = torch.from_numpy(rows).to(DEV)
+        y_ref, d_ref = oracle.gemm_f16(bits16(dd.x[key]), bits16(w16.index_select(0, idx)))
+        err = oracle.normalised_error(dd.y[key[1]].index_select(1, idx).float().cpu().numpy(), y_ref, d_ref)
+        assert err <= GEMV_TOL, (key, err)
+    if cfg.lm_head:
+        key = (cfg.layers, "lm_head")
+        rows = sample_rows(cfg.vocab, cfg.seed * 10 + 9)
+        idx = torch.from_numpy(rows).to(DEV)
+        y_ref, d_ref = oracle.gemm_f16(bits16(dd.x[(stack.layers, "lm_head")]), bits16(stack.w16[key].index_select(0, idx)))
+        err = oracle.normalised_error(dd.logits.index_select(1, idx).cpu().numpy(), y_ref, d_ref)
+        assert err <= GEMV_TOL, err
+    B, V = cfg.batch, cfg.vocab
+    logits = dd.logits.cpu().numpy().reshape(B, 1, V)
+    _, t_ref, _, _ = oracle.spec_accept(None, logits, None, dd.u.cpu().numpy().view(np.uint32), 1.0)
+    assert np.array_equal(dd.token.cpu().numpy(), t_ref)
+    eager = dd.token.clone()
+    dd.capture()
+    for _ in range(3):
+        dd.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(dd.token, eager)
+    del dd, stack
+    torch.cuda.empty_cache()
