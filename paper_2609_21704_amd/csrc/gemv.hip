@@ -437,6 +437,215 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
   }
 }
 
+// INT4 GEMV over long rows (k >= 4096, m <= 2).  One workgroup of 16
+// wavefronts per CU owns a contiguous block of rows, whose codes are one
+// contiguous byte range; the range is cut into 16 equal runs of 32-byte
+// pieces (64 codes, half a group), one run per wavefront, so no wavefront
+// waits on another's share.  A wavefront walks its run in steps of 64
+// consecutive pieces with D steps of loads in flight (the host takes D = 1:
+// with 16 wavefronts of a CU streaming, every deeper prefetch measured
+// slower).  A row holds at least 64 pieces, so a step meets at most
+// two rows: each lane adds its piece into the sum of its row, and when the
+// walk leaves a row the wavefront reduces that row's sum into an LDS slot
+// [row][wavefront].  After one barrier each row is the sum of its 16 slots in
+// wavefront order (deterministic).  Activations are staged in LDS chunk-major
+// with one pad cell per 64-element chunk (a 144-byte stride), so a lane reads
+// its eight cells at immediate offsets and the 16 lanes of one read fall in
+// different banks.
+struct PieceFrag {
+  u32x4 c[2];  // 32 bytes of codes
+  uint32_t s;  // group scale bits
+  uint32_t z;  // group zero bits
+};
+
+template <int M, int D, int XB>
+__global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restrict__ x, int64_t k,
+                                                        const uint8_t* __restrict__ codes,
+                                                        const uint16_t* __restrict__ scales16,
+                                                        const uint16_t* __restrict__ zeros16, int64_t n,
+                                                        void* __restrict__ y, int f16_out, int64_t rows_q,
+                                                        int rows_rem) {
+  extern __shared__ __align__(16) char smem[];
+  constexpr int kPad = 9;     // LDS cells per chunk: eight and one pad
+  constexpr int nwave = 16;   // wavefronts per workgroup (1024 threads)
+  // no integer division on the way to the first load: block b holds rows_q
+  // rows, plus one for b < rows_rem
+  const int b = blockIdx.x;
+  const int64_t r0 = (int64_t)b * rows_q + (b < rows_rem ? b : rows_rem);
+  const int nrows = (int)rows_q + (b < rows_rem ? 1 : 0);
+  const int ppr = (int)(k >> 6);  // pieces per row (and activation chunks)
+  const int P = nrows * ppr;      // pieces of the block (< 2^27 by the host's check)
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int ps = (P * wave) >> 4, pe = (P * (wave + 1)) >> 4;
+  const int nsteps = (pe - ps + 63) >> 6;
+  half_t* xs = reinterpret_cast<half_t*>(smem);
+  float* red = reinterpret_cast<float*>(smem + (size_t)M * ppr * kPad * 16);  // [M][nrows][nwave]
+  const uint8_t* bcodes = codes + r0 * (k >> 1);
+  const uint16_t* bscales = scales16 + r0 * (k >> 7);
+  const uint16_t* bzeros = zeros16 + r0 * (k >> 7);
+
+  // piece p of the block: codes at 32 p, group p / 2 (rows hold whole groups);
+  // a lane past the run reads the run's last piece again and adds nothing.
+  // Every load is unconditional, so that the compiler can count the loads in
+  // flight and wait only for the oldest.
+  auto load = [&](int s) -> PieceFrag {
+    PieceFrag f;
+    int p = ps + 64 * s + lane;
+    p = p < pe ? p : pe - 1;
+    p = p > 0 ? p : 0;  // a run without pieces reads piece 0
+    const u32x4* cp = reinterpret_cast<const u32x4*>(bcodes + (int64_t)p * 32);
+    f.c[0] = cp[0];
+    f.c[1] = cp[1];
+    f.s = bscales[p >> 1];
+    f.z = bzeros[p >> 1];
+    return f;
+  };
+
+  // activations first (XB cells per thread cover all of x: the host's
+  // choice), then the first D steps of codes
+  const int xtotal = M * ppr * 8, nthr = (int)blockDim.x;
+  u32x4 xv[XB];
+  auto xload = [&](int base) {
+#pragma unroll
+    for (int b = 0; b < XB; ++b) {
+      int idx = base + b * nthr + (int)threadIdx.x;
+      idx = idx < xtotal ? idx : xtotal - 1;
+      const int m = idx >= ppr * 8 ? 1 : 0, rem = idx - m * ppr * 8;  // m <= 2
+      xv[b] = x_cell<M, false>(x, k, 0, k, rem >> 3, m, rem & 7);
+    }
+  };
+  auto xstore = [&](int base) {
+#pragma unroll
+    for (int b = 0; b < XB; ++b) {
+      const int idx = base + b * nthr + (int)threadIdx.x;
+      if (idx < xtotal) {
+        const int m = idx >= ppr * 8 ? 1 : 0, rem = idx - m * ppr * 8;
+        *reinterpret_cast<u32x4*>(xs + (((size_t)m * ppr + (rem >> 3)) * kPad + (rem & 7)) * 8) = xv[b];
+      }
+    }
+  };
+  xload(0);
+  // every wavefront's activation loads go out before any code load: the
+  // memory system serves a CU's loads in order, so activations queued behind
+  // the other wavefronts' codes would hold the whole workgroup at its barrier
+  __builtin_amdgcn_s_barrier();
+  PieceFrag ring[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) ring[j] = load(j);
+  xstore(0);
+  for (int i = (int)threadIdx.x; i < M * nrows * nwave; i += nthr) red[i] = 0.f;
+  // LDS writes done, then the barrier: no wait for the code loads in flight
+  // (a full __syncthreads would wait for every outstanding global load)
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+
+  uint32_t mlo = 0x000F000Fu, mhi = 0x00F000F0u, k1024 = 0x64006400u, k64 = 0x54005400u;
+  asm("" : "+v"(mlo), "+v"(mhi), "+v"(k1024), "+v"(k64));
+
+  // the walk: step base piece `cb`, its row `crow` and offset `coff` in that row
+  int cb = ps;
+  int crow = (int)((double)ps / (double)ppr);  // exact: both below 2^27
+  crow -= crow * ppr > ps ? 1 : 0;
+  crow += (crow + 1) * ppr <= ps ? 1 : 0;
+  int coff = ps - crow * ppr;
+  int cur = crow;  // acc0 holds row cur, acc1 row cur + 1
+  float acc0[M], acc1[M];
+#pragma unroll
+  for (int m = 0; m < M; ++m) acc0[m] = acc1[m] = 0.f;
+
+  auto flush = [&](const float (&a)[M], int row) {
+    float v[4] = {a[0], M > 1 ? a[M - 1] : 0.f, 0.f, 0.f};
+    float w[1];
+    wave_sums<1>(v, w);
+    // lanes 0-15 hold the total of v[0], lanes 32-47 that of v[1]
+    if (lane == 0) red[row * nwave + wave] = w[0];
+    if (M > 1 && lane == 32) red[(nrows + row) * nwave + wave] = w[0];
+  };
+
+  auto compute = [&](const PieceFrag& f) {
+    const int lo = coff + lane;
+    const bool second = lo >= ppr;
+    const int chunk = second ? lo - ppr : lo;
+    const bool ok = cb + lane < pe;
+    const uint32_t zb = f.z;
+    const half2_t z2 = __builtin_bit_cast(half2_t, zb | (zb << 16));
+    const half2_t c1024 = z2 + half2_t{(half_t)1024.0f, (half_t)1024.0f};
+    const half2_t c64 = z2 + half2_t{(half_t)64.0f, (half_t)64.0f};
+    float a[M];
+#pragma unroll
+    for (int m = 0; m < M; ++m) a[m] = 0.f;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      const uint32_t q = f.c[w >> 2][w & 3];
+      const uint32_t q8 = q >> 8;
+      const half2_t d0 = __builtin_bit_cast(half2_t, (q & mlo) | k1024) - c1024;   // q0 - z, q4 - z
+      const half2_t d1 = __builtin_bit_cast(half2_t, (q & mhi) | k64) - c64;       // q1 - z, q5 - z
+      const half2_t d2 = __builtin_bit_cast(half2_t, (q8 & mlo) | k1024) - c1024;  // q2 - z, q6 - z
+      const half2_t d3 = __builtin_bit_cast(half2_t, (q8 & mhi) | k64) - c64;      // q3 - z, q7 - z
+#pragma unroll
+      for (int m = 0; m < M; ++m) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(xs + (((size_t)m * ppr + chunk) * kPad + w) * 8);
+        const uint32_t e0 = v[0], e1 = v[1], e2 = v[2], e3 = v[3];  // scalar copies, as elsewhere
+        float t = a[m];
+        t = __builtin_amdgcn_fdot2(d0, __builtin_bit_cast(half2_t, e0), t, false);
+        t = __builtin_amdgcn_fdot2(d1, __builtin_bit_cast(half2_t, e1), t, false);
+        t = __builtin_amdgcn_fdot2(d2, __builtin_bit_cast(half2_t, e2), t, false);
+        t = __builtin_amdgcn_fdot2(d3, __builtin_bit_cast(half2_t, e3), t, false);
+        a[m] = t;
+      }
+    }
+    const float sc = f16_bits_to_f32((uint16_t)f.s);
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+      const float v = ok ? sc * a[m] : 0.f;
+      acc0[m] += second ? 0.f : v;
+      acc1[m] += second ? v : 0.f;
+    }
+  };
+
+  for (int s0 = 0; s0 < nsteps; s0 += D) {
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      const int s = s0 + j;
+      if (s < nsteps) {
+        if (crow != cur) {  // the walk left row cur (a step advances by at most one row)
+          flush(acc0, cur);
+#pragma unroll
+          for (int m = 0; m < M; ++m) {
+            acc0[m] = acc1[m];
+            acc1[m] = 0.f;
+          }
+          cur = crow;
+        }
+        compute(ring[j]);
+        cb += 64;
+        coff += 64;
+        if (coff >= ppr) {
+          coff -= ppr;
+          ++crow;
+        }
+      }
+      ring[j] = load(s + D);
+    }
+  }
+  if (nsteps > 0) {
+    flush(acc0, cur);
+    if (cur + 1 < nrows) flush(acc1, cur + 1);
+  }
+  __syncthreads();
+  for (int t = (int)threadIdx.x; t < M * nrows; t += nthr) {
+    const int m = t >= nrows ? 1 : 0, row = t - m * nrows;
+    float v = 0.f;
+    for (int w = 0; w < nwave; ++w) v += red[t * nwave + w];
+    const int64_t o = (int64_t)m * n + r0 + row;
+    if (f16_out)
+      reinterpret_cast<uint16_t*>(y)[o] = f32_to_f16_bits(v);
+    else
+      reinterpret_cast<float*>(y)[o] = v;
+  }
+}
+
 template <bool F16Out>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ partial, int splits, int64_t mn,
                                                             void* __restrict__ y) {
@@ -474,6 +683,39 @@ hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits,
   const dim3 grid((unsigned)blocks, (unsigned)splits);
   hipLaunchKernelGGL((gemv_kernel<M, W8, R, MULTI>), grid, dim3((unsigned)(T * nw * 64)), lds, stream, x, k, kslice,
                      codes, scales16, zeros16, scales32, n, y, (int)f16_out, partial, nw);
+  return hipGetLastError();
+}
+
+#ifndef SQ_GEMV_ROWS_MIN_K
+#define SQ_GEMV_ROWS_MIN_K 4096  // shortest rows the long-row INT4 kernel takes
+#endif
+#ifndef SQ_GEMV_ROWS_DEPTH
+#define SQ_GEMV_ROWS_DEPTH 1     // steps of loads in flight per wavefront (measured: 1 < 2 < 3 < 4 in time)
+#endif
+constexpr size_t kRowsLdsMax = 150 * 1024;
+
+// Host side of the long-row INT4 kernel: one workgroup of 16 wavefronts per CU
+// (fewer workgroups than rows never), rows split evenly over the workgroups.
+// Returns hipErrorNotSupported when the shape is outside what it takes.
+template <int M>
+hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint16_t* scales16,
+                       const uint16_t* zeros16, int64_t n, void* y, bool f16_out, hipStream_t stream) {
+  if (M > 2 || k < SQ_GEMV_ROWS_MIN_K) return hipErrorNotSupported;
+  const int64_t cus = cu_count();
+  const int64_t blocks = n < cus ? n : cus;
+  const int64_t rows_max = (n + blocks - 1) / blocks;
+  const int64_t ppr = k >> 6;
+  const size_t lds = (size_t)M * ppr * 9 * 16 + (size_t)M * rows_max * 16 * sizeof(float);
+  const int64_t xcells = M * ppr * 8;  // 16-byte activation cells, staged by 1024 threads at once
+  if (lds > kRowsLdsMax || rows_max * ppr >= (int64_t(1) << 27) || xcells > 8 * 1024)
+    return hipErrorNotSupported;
+  constexpr int D = SQ_GEMV_ROWS_DEPTH;
+  if (xcells <= 4 * 1024)
+    hipLaunchKernelGGL((gemv_rows_kernel<M, D, 4>), dim3((unsigned)blocks), dim3(1024), lds, stream, x, k, codes,
+                       scales16, zeros16, n, y, (int)f16_out, n / blocks, (int)(n % blocks));
+  else
+    hipLaunchKernelGGL((gemv_rows_kernel<M, D, 8>), dim3((unsigned)blocks), dim3(1024), lds, stream, x, k, codes,
+                       scales16, zeros16, n, y, (int)f16_out, n / blocks, (int)(n % blocks));
   return hipGetLastError();
 }
 
@@ -519,6 +761,12 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
   // teams of five, which leave a CU one wavefront short and pad more tasks)
   const int64_t ntask = (n + rows - 1) / rows;
   const int nw = ntask >= waves ? 1 : (steps >= 4 ? 4 : (steps >= 2 ? 2 : 1));
+  if constexpr (!W8 && M <= 2) {
+    if (nw > 1) {  // fewer rows than resident wavefronts: the long-row kernel, where it applies
+      const hipError_t e = gemv_rows_m<M>(x, k, codes, scales16, zeros16, n, y, f16_out, stream);
+      if (e != hipErrorNotSupported) return e;
+    }
+  }
   hipError_t err = hipErrorInvalidValue;
   auto go = [&](auto r_tag, auto multi_tag) {
     constexpr int RR = decltype(r_tag)::value;

@@ -93,8 +93,9 @@ def traffic(fetch_dir, write_dir, copy_bytes):
     copy_key = fetch[-1][1]
     f_scale = fetch[-1][2] * 1024.0 / copy_bytes   # counters are in KiB
     w_scale = write[-1][2] * 1024.0 / copy_bytes
-    f_g = [v * 1024.0 for _, k, v in fetch if k.startswith("sq::gemv_kernel")]
-    w_g = [v * 1024.0 for _, k, v in write if k.startswith("sq::gemv_kernel")]
+    gemv = ("sq::gemv_kernel", "sq::gemv_rows_kernel")  # the draft GEMV's two kernels
+    f_g = [v * 1024.0 for _, k, v in fetch if k.startswith(gemv)]
+    w_g = [v * 1024.0 for _, k, v in write if k.startswith(gemv)]
     f_mean = sum(f_g) / len(f_g) / f_scale
     w_mean = sum(w_g) / len(w_g) / w_scale if w_g else 0.0
     sha = hashlib.sha256(open(GEMV_SRC, "rb").read()).hexdigest()

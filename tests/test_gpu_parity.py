@@ -146,6 +146,19 @@ def test_qgemv_w8a16_team_sizes(m, n, k):
     test_qgemv_w8a16_parity(m, n, k)
 
 
+# Long rows with fewer rows than resident wavefronts (INT4, m <= 2): a
+# workgroup per CU owns a block of rows and its wavefronts walk equal runs of
+# the block's bytes, which start and end inside rows.  Blocks of 14 rows (the
+# 7B down projection), of 3 or 4 rows (1000 and 511 over the CUs), of one row
+# (257), and activations of up to 147 KB in LDS.
+LONG_W4 = [(1, 3584, 18944), (2, 1000, 4864), (1, 511, 9600), (2, 511, 9600), (1, 257, 65536), (2, 300, 32768)]
+
+
+@pytest.mark.parametrize("m,n,k", LONG_W4)
+def test_qgemv_w4a16_long_rows(m, n, k):
+    test_qgemv_w4a16_parity(m, n, k)
+
+
 def test_qgemv_w8a16_every_code_decodes_exactly():
     """Row c holds code c at column 0 (NaN codes replaced by 0); x = e_0."""
     n, k = 256, 32
