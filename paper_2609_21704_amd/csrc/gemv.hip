@@ -437,18 +437,18 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
   }
 }
 
-// INT4 GEMV over long rows (k >= 4096, m <= 2).  One workgroup of 16
+// INT4 GEMV over row blocks (k >= 2048, m <= 2).  One workgroup of 16
 // wavefronts per CU owns a contiguous block of rows, whose codes are one
 // contiguous byte range; the range is cut into 16 equal runs of 32-byte
 // pieces (64 codes, half a group), one run per wavefront, so no wavefront
 // waits on another's share.  A wavefront walks its run in steps of 64
 // consecutive pieces with D steps of loads in flight (the host takes D = 1:
 // with 16 wavefronts of a CU streaming, every deeper prefetch measured
-// slower).  A row holds at least 64 pieces, so a step meets at most
-// two rows: each lane adds its piece into the sum of its row, and when the
-// walk leaves a row the wavefront reduces that row's sum into an LDS slot
-// [row][wavefront].  After one barrier each row is the sum of its 16 slots in
-// wavefront order (deterministic).  Activations are staged in LDS chunk-major
+// slower).  A row holds at least 32 pieces, so a step meets at most NA
+// rows (three, or two from 64 pieces a row on): each lane adds its piece into
+// the sum of its row, and when the walk leaves a row the wavefront reduces
+// that row's sum into an LDS slot [wavefront][row].  After one barrier each
+// row is the sum of its 16 slots in wavefront order (deterministic).  Activations are staged in LDS chunk-major
 // with one pad cell per 64-element chunk (a 144-byte stride), so a lane reads
 // its eight cells at immediate offsets and the 16 lanes of one read fall in
 // different banks.
@@ -458,7 +458,7 @@ struct PieceFrag {
   uint32_t z;  // group zero bits
 };
 
-template <int M, int D, int XB>
+template <int M, int D, int XB, int NA>
 __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restrict__ x, int64_t k,
                                                         const uint8_t* __restrict__ codes,
                                                         const uint16_t* __restrict__ scales16,
@@ -480,7 +480,7 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
   const int ps = (P * wave) >> 4, pe = (P * (wave + 1)) >> 4;
   const int nsteps = (pe - ps + 63) >> 6;
   half_t* xs = reinterpret_cast<half_t*>(smem);
-  float* red = reinterpret_cast<float*>(smem + (size_t)M * ppr * kPad * 16);  // [M][nrows][nwave]
+  float* red = reinterpret_cast<float*>(smem + (size_t)M * ppr * kPad * 16);  // [nwave][M][nrows]
   const uint8_t* bcodes = codes + r0 * (k >> 1);
   const uint16_t* bscales = scales16 + r0 * (k >> 7);
   const uint16_t* bzeros = zeros16 + r0 * (k >> 7);
@@ -549,24 +549,33 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
   crow -= crow * ppr > ps ? 1 : 0;
   crow += (crow + 1) * ppr <= ps ? 1 : 0;
   int coff = ps - crow * ppr;
-  int cur = crow;  // acc0 holds row cur, acc1 row cur + 1
-  float acc0[M], acc1[M];
+  int cur = crow;  // acc[i] holds row cur + i
+  float acc[NA][M];
 #pragma unroll
-  for (int m = 0; m < M; ++m) acc0[m] = acc1[m] = 0.f;
+  for (int i = 0; i < NA; ++i)
+#pragma unroll
+    for (int m = 0; m < M; ++m) acc[i][m] = 0.f;
 
   auto flush = [&](const float (&a)[M], int row) {
     float v[4] = {a[0], M > 1 ? a[M - 1] : 0.f, 0.f, 0.f};
     float w[1];
     wave_sums<1>(v, w);
     // lanes 0-15 hold the total of v[0], lanes 32-47 that of v[1]
-    if (lane == 0) red[row * nwave + wave] = w[0];
-    if (M > 1 && lane == 32) red[(nrows + row) * nwave + wave] = w[0];
+    if (lane == 0) red[wave * M * nrows + row] = w[0];
+    if (M > 1 && lane == 32) red[(wave * M + 1) * nrows + row] = w[0];
   };
 
   auto compute = [&](const PieceFrag& f) {
-    const int lo = coff + lane;
-    const bool second = lo >= ppr;
-    const int chunk = second ? lo - ppr : lo;
+    // the lane's row is crow + rel: a step of 64 pieces meets at most NA rows
+    int chunk = coff + lane, rel = 0;
+    if (chunk >= ppr) {
+      chunk -= ppr;
+      rel = 1;
+    }
+    if (NA > 2 && chunk >= ppr) {
+      chunk -= ppr;
+      rel = 2;
+    }
     const bool ok = cb + lane < pe;
     const uint32_t zb = f.z;
     const half2_t z2 = __builtin_bit_cast(half2_t, zb | (zb << 16));
@@ -599,8 +608,8 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
 #pragma unroll
     for (int m = 0; m < M; ++m) {
       const float v = ok ? sc * a[m] : 0.f;
-      acc0[m] += second ? 0.f : v;
-      acc1[m] += second ? v : 0.f;
+#pragma unroll
+      for (int i = 0; i < NA; ++i) acc[i][m] += rel == i ? v : 0.f;
     }
   };
 
@@ -609,19 +618,20 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
     for (int j = 0; j < D; ++j) {
       const int s = s0 + j;
       if (s < nsteps) {
-        if (crow != cur) {  // the walk left row cur (a step advances by at most one row)
-          flush(acc0, cur);
+        while (cur < crow) {  // the walk left row cur
+          flush(acc[0], cur);
 #pragma unroll
-          for (int m = 0; m < M; ++m) {
-            acc0[m] = acc1[m];
-            acc1[m] = 0.f;
-          }
-          cur = crow;
+          for (int i = 0; i + 1 < NA; ++i)
+#pragma unroll
+            for (int m = 0; m < M; ++m) acc[i][m] = acc[i + 1][m];
+#pragma unroll
+          for (int m = 0; m < M; ++m) acc[NA - 1][m] = 0.f;
+          ++cur;
         }
         compute(ring[j]);
         cb += 64;
         coff += 64;
-        if (coff >= ppr) {
+        while (coff >= ppr) {
           coff -= ppr;
           ++crow;
         }
@@ -630,14 +640,15 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
     }
   }
   if (nsteps > 0) {
-    flush(acc0, cur);
-    if (cur + 1 < nrows) flush(acc1, cur + 1);
+#pragma unroll
+    for (int i = 0; i < NA; ++i)
+      if (cur + i < nrows) flush(acc[i], cur + i);
   }
   __syncthreads();
   for (int t = (int)threadIdx.x; t < M * nrows; t += nthr) {
     const int m = t >= nrows ? 1 : 0, row = t - m * nrows;
     float v = 0.f;
-    for (int w = 0; w < nwave; ++w) v += red[t * nwave + w];
+    for (int w = 0; w < nwave; ++w) v += red[w * M * nrows + t];  // consecutive threads, consecutive words
     const int64_t o = (int64_t)m * n + r0 + row;
     if (f16_out)
       reinterpret_cast<uint16_t*>(y)[o] = f32_to_f16_bits(v);
@@ -687,20 +698,20 @@ hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits,
 }
 
 #ifndef SQ_GEMV_ROWS_MIN_K
-#define SQ_GEMV_ROWS_MIN_K 4096  // shortest rows the long-row INT4 kernel takes
+#define SQ_GEMV_ROWS_MIN_K 2048  // shortest rows the row-block INT4 kernel takes
 #endif
 #ifndef SQ_GEMV_ROWS_DEPTH
 #define SQ_GEMV_ROWS_DEPTH 1     // steps of loads in flight per wavefront (measured: 1 < 2 < 3 < 4 in time)
 #endif
 constexpr size_t kRowsLdsMax = 150 * 1024;
 
-// Host side of the long-row INT4 kernel: one workgroup of 16 wavefronts per CU
+// Host side of the row-block INT4 kernel: one workgroup of 16 wavefronts per CU
 // (fewer workgroups than rows never), rows split evenly over the workgroups.
 // Returns hipErrorNotSupported when the shape is outside what it takes.
 template <int M>
 hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint16_t* scales16,
                        const uint16_t* zeros16, int64_t n, void* y, bool f16_out, hipStream_t stream) {
-  if (M > 2 || k < SQ_GEMV_ROWS_MIN_K) return hipErrorNotSupported;
+  if (M > 2 || k < SQ_GEMV_ROWS_MIN_K || k < 2048) return hipErrorNotSupported;
   const int64_t cus = cu_count();
   const int64_t blocks = n < cus ? n : cus;
   const int64_t rows_max = (n + blocks - 1) / blocks;
@@ -710,12 +721,17 @@ hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const
   if (lds > kRowsLdsMax || rows_max * ppr >= (int64_t(1) << 27) || xcells > 8 * 1024)
     return hipErrorNotSupported;
   constexpr int D = SQ_GEMV_ROWS_DEPTH;
-  if (xcells <= 4 * 1024)
-    hipLaunchKernelGGL((gemv_rows_kernel<M, D, 4>), dim3((unsigned)blocks), dim3(1024), lds, stream, x, k, codes,
-                       scales16, zeros16, n, y, (int)f16_out, n / blocks, (int)(n % blocks));
+  const int64_t q = n / blocks;
+  const int rem = (int)(n % blocks);
+  if (ppr < 64)  // rows of 2048 .. 4095 k: a step meets up to three rows
+    hipLaunchKernelGGL((gemv_rows_kernel<M, D, 4, 3>), dim3((unsigned)blocks), dim3(1024), lds, stream, x, k, codes,
+                       scales16, zeros16, n, y, (int)f16_out, q, rem);
+  else if (xcells <= 4 * 1024)
+    hipLaunchKernelGGL((gemv_rows_kernel<M, D, 4, 2>), dim3((unsigned)blocks), dim3(1024), lds, stream, x, k, codes,
+                       scales16, zeros16, n, y, (int)f16_out, q, rem);
   else
-    hipLaunchKernelGGL((gemv_rows_kernel<M, D, 8>), dim3((unsigned)blocks), dim3(1024), lds, stream, x, k, codes,
-                       scales16, zeros16, n, y, (int)f16_out, n / blocks, (int)(n % blocks));
+    hipLaunchKernelGGL((gemv_rows_kernel<M, D, 8, 2>), dim3((unsigned)blocks), dim3(1024), lds, stream, x, k, codes,
+                       scales16, zeros16, n, y, (int)f16_out, q, rem);
   return hipGetLastError();
 }
 
@@ -762,7 +778,16 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
   const int64_t ntask = (n + rows - 1) / rows;
   const int nw = ntask >= waves ? 1 : (steps >= 4 ? 4 : (steps >= 2 ? 2 : 1));
   if constexpr (!W8 && M <= 2) {
-    if (nw > 1) {  // fewer rows than resident wavefronts: the long-row kernel, where it applies
+    // the row-block kernel, where it applies, when a task would be one row (no
+    // activation reuse across rows to lose) or when the last step of a row
+    // leaves more than a quarter of the lanes idle (measured crossover)
+    const int64_t row_chunks = k / 64;
+    const bool idle_lanes = 4 * row_chunks < 3 * 64 * ((row_chunks + 63) / 64);
+#ifdef SQ_GEMV_ROWS_ALL
+    if (true) {
+#else
+    if (rows == 1 || idle_lanes) {
+#endif
       const hipError_t e = gemv_rows_m<M>(x, k, codes, scales16, zeros16, n, y, f16_out, stream);
       if (e != hipErrorNotSupported) return e;
     }

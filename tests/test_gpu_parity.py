@@ -146,12 +146,15 @@ def test_qgemv_w8a16_team_sizes(m, n, k):
     test_qgemv_w8a16_parity(m, n, k)
 
 
-# Long rows with fewer rows than resident wavefronts (INT4, m <= 2): a
-# workgroup per CU owns a block of rows and its wavefronts walk equal runs of
-# the block's bytes, which start and end inside rows.  Blocks of 14 rows (the
-# 7B down projection), of 3 or 4 rows (1000 and 511 over the CUs), of one row
-# (257), and activations of up to 147 KB in LDS.
-LONG_W4 = [(1, 3584, 18944), (2, 1000, 4864), (1, 511, 9600), (2, 511, 9600), (1, 257, 65536), (2, 300, 32768)]
+# The row-block kernel (INT4, m <= 2): a workgroup per CU owns a block of
+# rows and its wavefronts walk equal runs of the block's bytes, which start
+# and end inside rows.  Blocks of 14 rows (the 7B down projection), of 3 or 4
+# rows (1000 and 511 over the CUs), of one row (257), activations of up to
+# 147 KB in LDS; rows of 2048 and 3584 k, where a step of 64 pieces meets
+# three rows, with many rows per block; 5120 k with four-row tasks in the
+# other kernel (the idle-lane rule picks this one).
+LONG_W4 = [(1, 3584, 18944), (2, 1000, 4864), (1, 511, 9600), (2, 511, 9600), (1, 257, 65536), (2, 300, 32768),
+           (1, 20000, 2048), (2, 9000, 3584), (1, 4608, 3584), (1, 40000, 5120)]
 
 
 @pytest.mark.parametrize("m,n,k", LONG_W4)
