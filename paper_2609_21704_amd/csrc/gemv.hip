@@ -437,28 +437,28 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
   }
 }
 
-// INT4 GEMV over row blocks (k >= 2048, m <= 2).  One workgroup of 16
-// wavefronts per CU owns a contiguous block of rows, whose codes are one
-// contiguous byte range; the range is cut into 16 equal runs of 32-byte
-// pieces (64 codes, half a group), one run per wavefront, so no wavefront
-// waits on another's share.  A wavefront walks its run in steps of 64
-// consecutive pieces with D steps of loads in flight (the host takes D = 1:
+// INT4 GEMV over row blocks (k >= 2048, m <= 2).  A workgroup of NWV
+// wavefronts (16 per CU in all) owns a contiguous block of rows, whose codes
+// are one contiguous byte range; the range is cut into NWV equal runs of
+// 32-byte pieces (64 codes, half a group), one run per wavefront, so no
+// wavefront waits on another's share.  A wavefront walks its run in steps of
+// 64 consecutive pieces with D steps of loads in flight (the host takes D = 1:
 // with 16 wavefronts of a CU streaming, every deeper prefetch measured
-// slower).  A row holds at least 32 pieces, so a step meets at most NA
-// rows (three, or two from 64 pieces a row on): each lane adds its piece into
-// the sum of its row, and when the walk leaves a row the wavefront reduces
-// that row's sum into an LDS slot [wavefront][row].  After one barrier each
-// row is the sum of its 16 slots in wavefront order (deterministic).  Activations are staged in LDS chunk-major
-// with one pad cell per 64-element chunk (a 144-byte stride), so a lane reads
-// its eight cells at immediate offsets and the 16 lanes of one read fall in
-// different banks.
+// slower).  A row holds at least 32 pieces, so a step meets at most NA rows
+// (three, or two from 64 pieces a row on): each lane adds its piece into the
+// sum of its row, and when the walk leaves a row the wavefront reduces that
+// row's sum into an LDS slot [wavefront][row].  After one barrier each row is
+// the sum of its NWV slots in wavefront order (deterministic).  Activations
+// are staged in LDS chunk-major with one pad cell per 64-element chunk (a
+// 144-byte stride), so a lane reads its eight cells at immediate offsets and
+// the 16 lanes of one read fall in different banks.
 struct PieceFrag {
   u32x4 c[2];  // 32 bytes of codes
   uint32_t s;  // group scale bits
   uint32_t z;  // group zero bits
 };
 
-template <int M, int D, int XB, int NA>
+template <int M, int D, int XB, int NA, int NWV>
 __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restrict__ x, int64_t k,
                                                         const uint8_t* __restrict__ codes,
                                                         const uint16_t* __restrict__ scales16,
@@ -467,7 +467,7 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
                                                         int rows_rem) {
   extern __shared__ __align__(16) char smem[];
   constexpr int kPad = 9;     // LDS cells per chunk: eight and one pad
-  constexpr int nwave = 16;   // wavefronts per workgroup (1024 threads)
+  constexpr int nwave = NWV;  // wavefronts per workgroup, a power of two
   // no integer division on the way to the first load: block b holds rows_q
   // rows, plus one for b < rows_rem
   const int b = blockIdx.x;
@@ -477,7 +477,7 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
   const int P = nrows * ppr;      // pieces of the block (< 2^27 by the host's check)
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int ps = (P * wave) >> 4, pe = (P * (wave + 1)) >> 4;
+  const int ps = (P * wave) / nwave, pe = (P * (wave + 1)) / nwave;  // nwave: a power of two
   const int nsteps = (pe - ps + 63) >> 6;
   half_t* xs = reinterpret_cast<half_t*>(smem);
   float* red = reinterpret_cast<float*>(smem + (size_t)M * ppr * kPad * 16);  // [nwave][M][nrows]
@@ -526,10 +526,6 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
     }
   };
   xload(0);
-  // every wavefront's activation loads go out before any code load: the
-  // memory system serves a CU's loads in order, so activations queued behind
-  // the other wavefronts' codes would hold the whole workgroup at its barrier
-  __builtin_amdgcn_s_barrier();
   PieceFrag ring[D];
 #pragma unroll
   for (int j = 0; j < D; ++j) ring[j] = load(j);
@@ -705,33 +701,41 @@ hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits,
 #endif
 constexpr size_t kRowsLdsMax = 150 * 1024;
 
-// Host side of the row-block INT4 kernel: one workgroup of 16 wavefronts per CU
+// Host side of the row-block INT4 kernel: 16 wavefronts per CU
 // (fewer workgroups than rows never), rows split evenly over the workgroups.
 // Returns hipErrorNotSupported when the shape is outside what it takes.
 template <int M>
 hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint16_t* scales16,
                        const uint16_t* zeros16, int64_t n, void* y, bool f16_out, hipStream_t stream) {
   if (M > 2 || k < SQ_GEMV_ROWS_MIN_K || k < 2048) return hipErrorNotSupported;
-  const int64_t cus = cu_count();
-  const int64_t blocks = n < cus ? n : cus;
+  // 16 wavefronts per CU: one workgroup of 16, or two of 8 for rows of 8192 k
+  // and more (measured: 7B down 13.5 -> 12.8 us, q|k|v 5.8 -> 6.0 us)
+  const int nwave = k >= 8192 && M * k <= 8 * 8 * 512 ? 8 : 16, nthr = 64 * nwave;  // 8: x staged in one pass
+  const int64_t wg_max = cu_count() * (16 / nwave);
+  const int64_t blocks = n < wg_max ? n : wg_max;
   const int64_t rows_max = (n + blocks - 1) / blocks;
   const int64_t ppr = k >> 6;
-  const size_t lds = (size_t)M * ppr * 9 * 16 + (size_t)M * rows_max * 16 * sizeof(float);
-  const int64_t xcells = M * ppr * 8;  // 16-byte activation cells, staged by 1024 threads at once
-  if (lds > kRowsLdsMax || rows_max * ppr >= (int64_t(1) << 27) || xcells > 8 * 1024)
+  const size_t lds = (size_t)M * ppr * 9 * 16 + (size_t)M * rows_max * nwave * sizeof(float);
+  const int64_t xcells = M * ppr * 8;  // 16-byte activation cells, staged by the workgroup at once
+  if (lds > kRowsLdsMax || rows_max * ppr >= (int64_t(1) << 27) || xcells > 8 * nthr)
     return hipErrorNotSupported;
   constexpr int D = SQ_GEMV_ROWS_DEPTH;
   const int64_t q = n / blocks;
   const int rem = (int)(n % blocks);
-  if (ppr < 64)  // rows of 2048 .. 4095 k: a step meets up to three rows
-    hipLaunchKernelGGL((gemv_rows_kernel<M, D, 4, 3>), dim3((unsigned)blocks), dim3(1024), lds, stream, x, k, codes,
-                       scales16, zeros16, n, y, (int)f16_out, q, rem);
-  else if (xcells <= 4 * 1024)
-    hipLaunchKernelGGL((gemv_rows_kernel<M, D, 4, 2>), dim3((unsigned)blocks), dim3(1024), lds, stream, x, k, codes,
-                       scales16, zeros16, n, y, (int)f16_out, q, rem);
+  // workgroups of 8 wavefronts take over a third of the LDS, so that a CU holds
+  // two of them (the registers would allow three)
+  const size_t lds_launch = nwave == 8 && lds < 54 * 1024 ? 54 * 1024 : lds;
+  auto go = [&](auto xb_tag, auto na_tag, auto nw_tag) {
+    constexpr int XB = decltype(xb_tag)::value, NA = decltype(na_tag)::value, NWV = decltype(nw_tag)::value;
+    hipLaunchKernelGGL((gemv_rows_kernel<M, D, XB, NA, NWV>), dim3((unsigned)blocks), dim3(nthr), lds_launch, stream,
+                       x, k, codes, scales16, zeros16, n, y, (int)f16_out, q, rem);
+  };
+  if (nwave == 8)  // k >= 8192: two rows per step at most
+    xcells <= 4 * nthr ? go(IntC<4>{}, IntC<2>{}, IntC<8>{}) : go(IntC<8>{}, IntC<2>{}, IntC<8>{});
+  else if (ppr < 64)  // rows of 2048 .. 4095 k: a step meets up to three rows
+    xcells <= 4 * nthr ? go(IntC<4>{}, IntC<3>{}, IntC<16>{}) : go(IntC<8>{}, IntC<3>{}, IntC<16>{});
   else
-    hipLaunchKernelGGL((gemv_rows_kernel<M, D, 8, 2>), dim3((unsigned)blocks), dim3(1024), lds, stream, x, k, codes,
-                       scales16, zeros16, n, y, (int)f16_out, q, rem);
+    xcells <= 4 * nthr ? go(IntC<4>{}, IntC<2>{}, IntC<16>{}) : go(IntC<8>{}, IntC<2>{}, IntC<16>{});
   return hipGetLastError();
 }
 
