@@ -232,9 +232,12 @@ sq_status sq_qgemv_w8a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t*
   const Range ins[] = {{x, (size_t)m * k * 2}, {codes, nk}, {scales, (size_t)n * 4}};
   if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
   (void)hipGetLastError();
-  return device_status(n * k >= kLinearMinBytesW8
-                           ? sq::launch_linear_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream)
-                           : sq::launch_gemv_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream));
+  // the matrix-core kernel from its size on, where its chunk bookkeeping fits
+  // (it enqueues nothing when it returns hipErrorNotSupported)
+  hipError_t e = hipErrorNotSupported;
+  if (n * k >= kLinearMinBytesW8) e = sq::launch_linear_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream);
+  if (e == hipErrorNotSupported) e = sq::launch_gemv_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream);
+  return device_status(e);
 }
 
 sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint16_t* w16, int64_t n, void* y,
@@ -248,9 +251,11 @@ sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint
   const Range ins[] = {{x, (size_t)m * k * 2}, {w16, (size_t)n * k * 2}};
   if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
   (void)hipGetLastError();
-  return device_status(m <= 16 && n * k * 2 >= kLinearMinBytesF16
-                           ? sq::launch_linear_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream)
-                           : sq::launch_gemm_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream));
+  hipError_t e = hipErrorNotSupported;
+  if (m <= 16 && n * k * 2 >= kLinearMinBytesF16)
+    e = sq::launch_linear_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream);
+  if (e == hipErrorNotSupported) e = sq::launch_gemm_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream);
+  return device_status(e);
 }
 
 sq_status sq_spec_accept(const float* draft_logits, const float* target_logits, const int32_t* draft_tokens,

@@ -494,7 +494,7 @@ hipError_t linear_launch(const uint16_t* x, int m, int64_t k, const uint8_t* w, 
   // K slices of whole units whose activations fit (2 bytes per k and row, plus a pad cell per row)
   int64_t kmax = (int64_t)((kLdsTotal - kPieceBudget) / ((size_t)m * 2)) - 8;
   kmax = kmax / UK * UK;
-  if (kmax < UK) return hipErrorInvalidValue;
+  if (kmax < UK) return hipErrorNotSupported;  // the caller takes another kernel
   const int splits = (int)((k + kmax - 1) / kmax);
   int64_t kslice = (k + splits - 1) / splits;
   kslice = (kslice + UK - 1) / UK * UK;
@@ -514,9 +514,9 @@ hipError_t linear_launch(const uint16_t* x, int m, int64_t k, const uint8_t* w, 
     nch_max = (ntask * J + nwg_max - 1) / nwg_max;
     if ((size_t)nch_max * m * 16 * sizeof(float) <= kPieceBudget || C >= S) break;
   }
-  if ((size_t)nch_max * m * 16 * sizeof(float) > kPieceBudget) return hipErrorInvalidValue;
+  if ((size_t)nch_max * m * 16 * sizeof(float) > kPieceBudget) return hipErrorNotSupported;
   // the kernel's chunk arithmetic is exact below 2^52 (workgroup index x chunks per slice)
-  if ((double)(nwg_max + 1) * (double)(ntask * S) >= 4503599627370496.0) return hipErrorInvalidValue;
+  if ((double)(nwg_max + 1) * (double)(ntask * S) >= 4503599627370496.0) return hipErrorNotSupported;
   const size_t lds = ((size_t)m * cells * 16 + 15) / 16 * 16 + (size_t)nch_max * m * 16 * sizeof(float);
 
   // two K slices meet per output value in a 64-bit slot; more are summed by a second kernel

@@ -162,6 +162,31 @@ def test_qgemv_w4a16_long_rows(m, n, k):
     test_qgemv_w4a16_parity(m, n, k)
 
 
+# Shapes past the matrix-core kernel's size threshold that it cannot take:
+# with many tiles per workgroup its chunk partial sums would not fit in LDS
+# (m = 16 verify, m = 8 FP8 draft), so the call takes the other kernel.
+def test_verify_gemm_many_tiles_m16():
+    m, n, k = 16, 140000, 128
+    w = synth.normal_f16((n, k), 0.02, 51)
+    x = synth.normal_f16((m, k), 1.0, 52)
+    y_ref, d_ref = oracle.gemm_f16(bits16(x), bits16(w))
+    y = sq.sq_verify_gemm_f16(x.to(DEV), w.to(DEV), y_dtype=torch.float32)
+    assert oracle.normalised_error(y.cpu().numpy(), y_ref, d_ref) <= GEMV_TOL
+
+
+def test_qgemv_w8a16_many_tiles_m8():
+    m, n, k = 8, 300000, 256
+    rng = np.random.default_rng(53)
+    codes = rng.integers(0, 256, size=(n, k), dtype=np.uint8)
+    codes[(codes & 0x7F) == 0x7F] = 0  # no NaN codes
+    scales = rng.uniform(1e-4, 1e-3, size=n).astype(np.float32)
+    x = synth.normal_f16((m, k), 1.0, 54)
+    y_ref, d_ref = oracle.qgemv_w8a16(bits16(x), codes, scales)
+    y = sq.sq_qgemv_w8a16(x.to(DEV), torch.from_numpy(codes).to(DEV), torch.from_numpy(scales).to(DEV),
+                          y_dtype=torch.float32)
+    assert oracle.normalised_error(y.cpu().numpy(), y_ref, d_ref) <= GEMV_TOL
+
+
 def test_qgemv_w8a16_every_code_decodes_exactly():
     """Row c holds code c at column 0 (NaN codes replaced by 0); x = e_0."""
     n, k = 256, 32
