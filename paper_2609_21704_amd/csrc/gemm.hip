@@ -139,7 +139,270 @@ hipError_t gemm_mt(const uint16_t* x, int m, int64_t k, const uint16_t* w, int64
   return hipGetLastError();
 }
 
+// Verification over row blocks for small m (m <= 8): at 5 flops per weight
+// byte the contraction is far below the matrix cores' ridge, and v_dot2
+// keeps up with HBM (m / 2 instructions per weight), so the weight rows
+// stream through the vector ALUs in the split of the INT4 row-block GEMV.  A
+// workgroup of NWV wavefronts (16 per CU in all) owns a contiguous block of
+// rows, whose weights are one contiguous range of 32-byte pieces (16 weights
+// of one row); each wavefront walks a run of whole steps of 64 pieces, the
+// odd steps going to the oldest wavefronts.  A row holds at least 32 pieces,
+// so a step meets at most NA rows; each lane adds its piece into the sum of
+// its row, and when the walk leaves a row the wavefront reduces that row's m
+// sums into LDS slots [wavefront][m][row], added in wavefront order after
+// one barrier.  The activations sit in LDS as [m][half][piece] cells of 8
+// halves, so the 64 lanes of one read take consecutive cells.
+template <int M, int NA, int NWV, int XB, int D>
+__global__ __launch_bounds__(1024) void gemm_rows_kernel(const uint16_t* __restrict__ x, int64_t k,
+                                                        const uint16_t* __restrict__ w, int64_t n,
+                                                        void* __restrict__ y, int f16_out, int64_t rows_q,
+                                                        int rows_rem) {
+  // every argument in one batch of scalar loads, before the first address needs one
+  asm volatile("" ::"s"(x), "s"(k), "s"(w), "s"(n), "s"(y), "s"(f16_out), "s"(rows_q), "s"(rows_rem));
+  extern __shared__ __align__(16) char smem[];
+  constexpr int nwave = NWV, nthr = 64 * NWV;
+  const int b = blockIdx.x;
+  const int64_t r0 = (int64_t)b * rows_q + (b < rows_rem ? b : rows_rem);
+  const int nrows = (int)rows_q + (b < rows_rem ? 1 : 0);
+  const int ppr = (int)(k >> 4);  // pieces per row
+  const int P = nrows * ppr;      // pieces of the block (< 2^27 by the host's check)
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // runs of whole steps: sb each, one more for the sx oldest wavefronts
+  const int T = (P + 63) >> 6;
+  const int sb = T / nwave, sx = T - sb * nwave;  // nwave: a power of two
+  const int ps0 = 64 * (wave * sb + (wave < sx ? wave : sx));
+  const int ps = ps0 < P ? ps0 : P, pe0 = ps0 + 64 * (sb + (wave < sx ? 1 : 0)), pe = pe0 < P ? pe0 : P;
+  const int nsteps = (pe - ps + 63) >> 6;
+  half_t* xs = reinterpret_cast<half_t*>(smem);
+  float* red = reinterpret_cast<float*>(smem + (size_t)M * 2 * ppr * 16);  // [nwave][M][nrows]
+  const uint16_t* bw = w + r0 * k;
+
+  // piece p of the block: weights 16 p .. 16 p + 15 of the block's range (rows
+  // are contiguous); a lane past the run reads the run's last piece again and
+  // adds nothing.  Unconditional, so the compiler waits only for the oldest.
+  struct Piece {
+    u32x4 c[2];
+  };
+  auto load = [&](int s) -> Piece {
+    Piece f;
+    int p = ps + 64 * s + lane;
+    p = p < pe ? p : pe - 1;
+    p = p > 0 ? p : 0;  // a run without pieces reads piece 0
+    const u32x4* cp = reinterpret_cast<const u32x4*>(bw + (int64_t)p * 16);
+    f.c[0] = cp[0];
+    f.c[1] = cp[1];
+    return f;
+  };
+
+  // activations first (XB cells per thread cover all of x), then the first step
+  const int xtotal = M * 2 * ppr;
+  u32x4 xv[XB];
+#pragma unroll
+  for (int i = 0; i < XB; ++i) {
+    int idx = i * nthr + (int)threadIdx.x;
+    idx = idx < xtotal ? idx : xtotal - 1;
+    int m = 0, c = idx;  // c: 8-element cell of row m
+#pragma unroll
+    for (int mm = 1; mm < M; ++mm)
+      if (c >= 2 * ppr) {
+        c -= 2 * ppr;
+        m = mm;
+      }
+    xv[i] = *reinterpret_cast<const u32x4*>(x + (int64_t)m * k + 8 * c);
+  }
+  Piece ring[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) ring[j] = load(j);
+#pragma unroll
+  for (int i = 0; i < XB; ++i) {
+    const int idx = i * nthr + (int)threadIdx.x;
+    if (idx < xtotal) {
+      int m = 0, c = idx;
+#pragma unroll
+      for (int mm = 1; mm < M; ++mm)
+        if (c >= 2 * ppr) {
+          c -= 2 * ppr;
+          m = mm;
+        }
+      *reinterpret_cast<u32x4*>(xs + (((size_t)m * 2 + (c & 1)) * ppr + (c >> 1)) * 8) = xv[i];
+    }
+  }
+  for (int i = (int)threadIdx.x; i < nwave * M * nrows; i += nthr) red[i] = 0.f;
+  // LDS writes done, then the barrier: no wait for the weight loads in flight
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+
+  // the walk: step base piece `cb`, its row `crow` and offset `coff` in that row
+  int cb = ps;
+  int crow = (int)((double)ps / (double)ppr);  // exact: both below 2^27
+  crow -= crow * ppr > ps ? 1 : 0;
+  crow += (crow + 1) * ppr <= ps ? 1 : 0;
+  int coff = ps - crow * ppr;
+  int cur = crow;  // acc[i] holds row cur + i
+  float acc[NA][M];
+#pragma unroll
+  for (int i = 0; i < NA; ++i)
+#pragma unroll
+    for (int m = 0; m < M; ++m) acc[i][m] = 0.f;
+
+  auto flush = [&](const float (&a)[M], int row) {
+    constexpr int TT = (M + 3) / 4;
+    float v[4 * TT];
+#pragma unroll
+    for (int i = 0; i < 4 * TT; ++i) v[i] = i < M ? a[i] : 0.f;
+    float ws[TT];
+    wave_sums<TT>(v, ws);
+    // lane 16 j holds value 4 t + (0, 2, 1, 3)[j] of ws[t]
+    const int j = lane >> 4;
+    const int which = j == 0 ? 0 : (j == 1 ? 2 : (j == 2 ? 1 : 3));
+    if ((lane & 15) == 0) {
+#pragma unroll
+      for (int t = 0; t < TT; ++t) {
+        const int m = 4 * t + which;
+        if (m < M) red[(wave * M + m) * nrows + row] = ws[t];
+      }
+    }
+  };
+
+  for (int s0 = 0; s0 < nsteps; s0 += D) {
+#pragma unroll
+   for (int jr = 0; jr < D; ++jr) {
+    const int s = s0 + jr;
+    if (s < nsteps) {
+    const Piece& f = ring[jr];
+    while (cur < crow) {  // the walk left row cur
+      flush(acc[0], cur);
+#pragma unroll
+      for (int i = 0; i + 1 < NA; ++i)
+#pragma unroll
+        for (int m = 0; m < M; ++m) acc[i][m] = acc[i + 1][m];
+#pragma unroll
+      for (int m = 0; m < M; ++m) acc[NA - 1][m] = 0.f;
+      ++cur;
+    }
+    // the lane's row is crow + rel
+    int chunk = coff + lane, rel = 0;
+    if (chunk >= ppr) {
+      chunk -= ppr;
+      rel = 1;
+    }
+    if (NA > 2 && chunk >= ppr) {
+      chunk -= ppr;
+      rel = 2;
+    }
+    const bool ok = cb + lane < pe;
+    float a[M];
+#pragma unroll
+    for (int m = 0; m < M; ++m) a[m] = 0.f;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+      for (int m = 0; m < M; ++m) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(xs + (((size_t)m * 2 + h) * ppr + chunk) * 8);
+        float t = a[m];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t we = f.c[h][e], xe = v[e];  // scalar copies
+          t = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, we), __builtin_bit_cast(half2_t, xe), t, false);
+        }
+        a[m] = t;
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+      const float v = ok ? a[m] : 0.f;
+#pragma unroll
+      for (int i = 0; i < NA; ++i) acc[i][m] += rel == i ? v : 0.f;
+    }
+    cb += 64;
+    coff += 64;
+    while (coff >= ppr) {
+      coff -= ppr;
+      ++crow;
+    }
+    }
+    ring[jr] = load(s + D);
+   }
+  }
+  if (nsteps > 0) {
+#pragma unroll
+    for (int i = 0; i < NA; ++i)
+      if (cur + i < nrows) flush(acc[i], cur + i);
+  }
+  __syncthreads();
+  for (int t = (int)threadIdx.x; t < M * nrows; t += nthr) {
+    float v = 0.f;
+    for (int q = 0; q < nwave; ++q) v += red[q * M * nrows + t];  // consecutive threads, consecutive words
+    int m = 0, row = t;
+#pragma unroll
+    for (int mm = 1; mm < M; ++mm)
+      if (row >= nrows) {
+        row -= nrows;
+        m = mm;
+      }
+    const int64_t o = (int64_t)m * n + r0 + row;
+    if (f16_out)
+      reinterpret_cast<uint16_t*>(y)[o] = f32_to_f16_bits(v);
+    else
+      reinterpret_cast<float*>(y)[o] = v;
+  }
+}
+
+template <int V>
+struct RowsIntC {
+  static constexpr int value = V;
+};
+
+constexpr size_t kRowsLds = 150 * 1024;
+
+template <int M>
+hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t n, void* y, bool f16_out,
+                       hipStream_t stream) {
+  if (k < 512 || k % 16 != 0) return hipErrorNotSupported;  // whole 16-weight pieces per row
+  constexpr int nwave = 16, nthr = 64 * nwave;
+  const int64_t blocks = n < cu_count() ? n : cu_count();
+  const int64_t rows_max = (n + blocks - 1) / blocks;
+  const int64_t ppr = k >> 4;
+  const int64_t xcells = (int64_t)M * 2 * ppr;
+  const size_t lds = (size_t)xcells * 16 + (size_t)nwave * M * rows_max * sizeof(float);
+  if (lds > kRowsLds || rows_max * ppr >= (int64_t(1) << 27) || xcells > 8 * nthr) return hipErrorNotSupported;
+  const int64_t q = n / blocks;
+  const int rem = (int)(n % blocks);
+  // at least half the LDS of a CU, so that no CU holds two of these workgroups
+  // while another holds none (the registers of the small-m kernels would allow two)
+  const size_t lds_launch = lds > 81 * 1024 ? lds : 81 * 1024;
+#ifndef SQ_VERIFY_ROWS_DEPTH
+#define SQ_VERIFY_ROWS_DEPTH 1
+#endif
+  auto go = [&](auto na_tag, auto xb_tag) {
+    constexpr int NA = decltype(na_tag)::value, XB = decltype(xb_tag)::value;
+    hipLaunchKernelGGL((gemm_rows_kernel<M, NA, nwave, XB, SQ_VERIFY_ROWS_DEPTH>), dim3((unsigned)blocks), dim3(nthr),
+                       lds_launch, stream, x, k, w, n, y, (int)f16_out, q, rem);
+  };
+  if (ppr < 64)  // rows of 512 .. 1023 k: a step meets up to three rows
+    xcells <= 4 * nthr ? go(RowsIntC<3>{}, RowsIntC<4>{}) : go(RowsIntC<3>{}, RowsIntC<8>{});
+  else
+    xcells <= 4 * nthr ? go(RowsIntC<2>{}, RowsIntC<4>{}) : go(RowsIntC<2>{}, RowsIntC<8>{});
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_gemm_rows_f16(const uint16_t* x, int m, int64_t k, const uint16_t* w, int64_t n, void* y,
+                                bool f16_out, hipStream_t stream) {
+  switch (m) {
+    case 1: return gemm_rows_m<1>(x, k, w, n, y, f16_out, stream);
+    case 2: return gemm_rows_m<2>(x, k, w, n, y, f16_out, stream);
+    case 3: return gemm_rows_m<3>(x, k, w, n, y, f16_out, stream);
+    case 4: return gemm_rows_m<4>(x, k, w, n, y, f16_out, stream);
+    case 5: return gemm_rows_m<5>(x, k, w, n, y, f16_out, stream);
+    case 6: return gemm_rows_m<6>(x, k, w, n, y, f16_out, stream);
+    case 7: return gemm_rows_m<7>(x, k, w, n, y, f16_out, stream);
+    case 8: return gemm_rows_m<8>(x, k, w, n, y, f16_out, stream);
+    default: return hipErrorNotSupported;
+  }
+}
 
 hipError_t launch_gemm_f16(const uint16_t* x, int m, int64_t k, const uint16_t* w, int64_t n, void* y, bool f16_out,
                            hipStream_t stream) {

@@ -51,41 +51,6 @@ constexpr size_t kLdsBudget = 64 * 1024;    // activation bytes one workgroup ma
 #define SQ_GEMV_TEAMS_MAX 4                 // teams per workgroup, at most (2 for 4-wavefront teams; measured)
 #endif
 
-template <int Ctrl>
-__device__ __forceinline__ float dpp_add(float v) {
-  return v + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), Ctrl, 0xF, 0xF,
-                                                                   false));
-}
-
-// Sums of V = 4T values across the 64 lanes of a wavefront, transposed: the
-// lane halves are folded with v_permlane32_swap, the row pairs with
-// v_permlane16_swap, and the 16-lane rows with DPP, 2.5 operations per value.
-// Afterwards every lane of row j of w[t] holds the total of value
-// 4t + (0, 2, 1, 3)[j].
-template <int T>
-__device__ __forceinline__ void wave_sums(const float (&v)[4 * T], float (&w)[T]) {
-#pragma unroll
-  for (int t = 0; t < T; ++t) {
-    float u[2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const auto p = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(int, v[4 * t + 2 * h]),
-                                                      __builtin_bit_cast(int, v[4 * t + 2 * h + 1]), false, false);
-      const int p0 = p[0], p1 = p[1];  // bit-cast scalar copies: vector element lvalues are misread
-      u[h] = __builtin_bit_cast(float, p0) + __builtin_bit_cast(float, p1);
-    }
-    const auto q = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(int, u[0]), __builtin_bit_cast(int, u[1]),
-                                                    false, false);
-    const int q0 = q[0], q1 = q[1];
-    float x = __builtin_bit_cast(float, q0) + __builtin_bit_cast(float, q1);
-    x = dpp_add<0xB1>(x);   // quad_perm [1,0,3,2]
-    x = dpp_add<0x4E>(x);   // quad_perm [2,3,0,1]
-    x = dpp_add<0x141>(x);  // row_half_mirror
-    x = dpp_add<0x140>(x);  // row_mirror: every lane holds its row's total
-    w[t] = x;
-  }
-}
-
 template <int V>
 struct IntC {
   static constexpr int value = V;
@@ -216,6 +181,9 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
                                                        void* __restrict__ y, int f16_out,
                                                        float* __restrict__ partial, int nw_team) {
   extern __shared__ __align__(16) char smem[];
+  // every argument in one batch of scalar loads, before the first address needs one
+  asm volatile("" ::"s"(x), "s"(k), "s"(kslice), "s"(codes), "s"(scales16), "s"(zeros16), "s"(scales32), "s"(n),
+               "s"(y), "s"(f16_out), "s"(partial), "s"(nw_team));
   constexpr int kCells = W8 ? 4 : 8;
   constexpr int kChunkK = W8 ? 32 : 64;  // weights per 32-byte lane chunk
   const int split = blockIdx.y;
@@ -469,6 +437,9 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
                                                         void* __restrict__ y, int f16_out, int64_t rows_q,
                                                         int rows_rem) {
   extern __shared__ __align__(16) char smem[];
+  // every argument in one batch of scalar loads, before the first address needs one
+  asm volatile("" ::"s"(x), "s"(k), "s"(codes), "s"(scales16), "s"(zeros16), "s"(n), "s"(y), "s"(f16_out),
+               "s"(rows_q), "s"(rows_rem));
   constexpr int kPad = 9;     // LDS cells per chunk: eight and one pad
   constexpr int nwave = NWV;  // wavefronts per workgroup, a power of two
   // no integer division on the way to the first load: block b holds rows_q

@@ -36,6 +36,10 @@ hipError_t launch_gemv_w8(const uint16_t* x, int m, int64_t k, const uint8_t* co
                           int64_t n, void* y, bool f16_out, hipStream_t stream);
 hipError_t launch_gemm_f16(const uint16_t* x, int m, int64_t k, const uint16_t* w, int64_t n, void* y,
                            bool f16_out, hipStream_t stream);
+// Verification over row blocks on the vector ALUs, 1 <= m <= 8; returns
+// hipErrorNotSupported (nothing enqueued) for shapes it does not take.
+hipError_t launch_gemm_rows_f16(const uint16_t* x, int m, int64_t k, const uint16_t* w, int64_t n, void* y,
+                                bool f16_out, hipStream_t stream);
 
 // The matrix-core streaming kernels (one implementation for the three weight
 // kinds; m <= 8 for INT4 / FP8, m <= 64 for FP16).

@@ -232,6 +232,19 @@ def test_verify_gemm_f16_parity(m, n, k):
         assert err <= GEMV_TOL, (dt, err)
 
 
+# The row-block verify kernel (m <= 8): the 7B q|k|v shape, activations of
+# 8 x 8192 (two staging batches), rows of 768 k (a step meets three rows),
+# 32768 rows of 512 k (the row limit), m = 7 at 5120 k, and k % 16 == 8
+# (not whole pieces: another kernel takes it).
+ROWS_VERIFY = [(5, 4608, 3584), (8, 3000, 8192), (3, 1500, 768), (1, 32768, 512), (7, 5000, 5120),
+               (5, 2000, 1032), (2, 33, 2048)]
+
+
+@pytest.mark.parametrize("m,n,k", ROWS_VERIFY)
+def test_verify_gemm_row_blocks(m, n, k):
+    test_verify_gemm_f16_parity(m, n, k)
+
+
 @pytest.mark.parametrize("m", [1, 5, 36])
 def test_verify_gemm_identity_is_exact(m):
     k = 384
