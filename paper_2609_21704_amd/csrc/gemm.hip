@@ -151,21 +151,28 @@ hipError_t gemm_mt(const uint16_t* x, int m, int64_t k, const uint16_t* w, int64
 // its row, and when the walk leaves a row the wavefront reduces that row's m
 // sums into LDS slots [wavefront][m][row], added in wavefront order after
 // one barrier.  The activations sit in LDS as [m][half][piece] cells of 8
-// halves, so the 64 lanes of one read take consecutive cells.
-template <int M, int NA, int NWV, int XB, int D>
+// halves, so the 64 lanes of one read take consecutive cells.  When the
+// activations of a whole row do not fit, KS = 2 workgroups share each row
+// block, one per half of K (blockIdx.y); the two partial sums of a value meet
+// in a 64-bit slot by atomic exchange (the value travels inside the atomic, so
+// no fence is needed): the second to arrive adds slice 0's + slice 1's in that
+// order, stores the result and empties the slot for the next launch.
+template <int M, int NA, int NWV, int XB, int D, int KS>
 __global__ __launch_bounds__(1024) void gemm_rows_kernel(const uint16_t* __restrict__ x, int64_t k,
                                                         const uint16_t* __restrict__ w, int64_t n,
                                                         void* __restrict__ y, int f16_out, int64_t rows_q,
-                                                        int rows_rem) {
+                                                        int rows_rem, unsigned long long* __restrict__ slots) {
   // every argument in one batch of scalar loads, before the first address needs one
-  asm volatile("" ::"s"(x), "s"(k), "s"(w), "s"(n), "s"(y), "s"(f16_out), "s"(rows_q), "s"(rows_rem));
+  asm volatile("" ::"s"(x), "s"(k), "s"(w), "s"(n), "s"(y), "s"(f16_out), "s"(rows_q), "s"(rows_rem), "s"(slots));
   extern __shared__ __align__(16) char smem[];
   constexpr int nwave = NWV, nthr = 64 * NWV;
   const int b = blockIdx.x;
   const int64_t r0 = (int64_t)b * rows_q + (b < rows_rem ? b : rows_rem);
   const int nrows = (int)rows_q + (b < rows_rem ? 1 : 0);
-  const int ppr = (int)(k >> 4);  // pieces per row
-  const int P = nrows * ppr;      // pieces of the block (< 2^27 by the host's check)
+  const int slice = KS > 1 ? (int)blockIdx.y : 0;
+  const int64_t kl = k / KS, k0 = slice * kl;  // this workgroup's part of K
+  const int ppr = (int)(kl >> 4);  // pieces per row
+  const int P = nrows * ppr;       // pieces of the block (< 2^27, or 2^24 when KS > 1, by the host's check)
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   // runs of whole steps: sb each, one more for the sx oldest wavefronts
@@ -176,11 +183,13 @@ __global__ __launch_bounds__(1024) void gemm_rows_kernel(const uint16_t* __restr
   const int nsteps = (pe - ps + 63) >> 6;
   half_t* xs = reinterpret_cast<half_t*>(smem);
   float* red = reinterpret_cast<float*>(smem + (size_t)M * 2 * ppr * 16);  // [nwave][M][nrows]
-  const uint16_t* bw = w + r0 * k;
+  const uint16_t* bw = w + r0 * k + k0;
+  const float rppr = 1.0f / (float)ppr;
 
   // piece p of the block: weights 16 p .. 16 p + 15 of the block's range (rows
-  // are contiguous); a lane past the run reads the run's last piece again and
-  // adds nothing.  Unconditional, so the compiler waits only for the oldest.
+  // are contiguous; with K slices, row p / ppr at piece p % ppr of the slice);
+  // a lane past the run reads the run's last piece again and adds nothing.
+  // Unconditional, so the compiler waits only for the oldest.
   struct Piece {
     u32x4 c[2];
   };
@@ -189,7 +198,20 @@ __global__ __launch_bounds__(1024) void gemm_rows_kernel(const uint16_t* __restr
     int p = ps + 64 * s + lane;
     p = p < pe ? p : pe - 1;
     p = p > 0 ? p : 0;  // a run without pieces reads piece 0
-    const u32x4* cp = reinterpret_cast<const u32x4*>(bw + (int64_t)p * 16);
+    int64_t off = (int64_t)p * 16;
+    if constexpr (KS > 1) {  // the float quotient is within one of p / ppr (p < 2^24)
+      int ri = (int)((float)p * rppr);
+      int ch = p - ri * ppr;
+      if (ch < 0) {
+        --ri;
+        ch += ppr;
+      } else if (ch >= ppr) {
+        ++ri;
+        ch -= ppr;
+      }
+      off = (int64_t)ri * k + ch * 16;
+    }
+    const u32x4* cp = reinterpret_cast<const u32x4*>(bw + off);
     f.c[0] = cp[0];
     f.c[1] = cp[1];
     return f;
@@ -209,7 +231,7 @@ __global__ __launch_bounds__(1024) void gemm_rows_kernel(const uint16_t* __restr
         c -= 2 * ppr;
         m = mm;
       }
-    xv[i] = *reinterpret_cast<const u32x4*>(x + (int64_t)m * k + 8 * c);
+    xv[i] = *reinterpret_cast<const u32x4*>(x + (int64_t)m * k + k0 + 8 * c);
   }
   Piece ring[D];
 #pragma unroll
@@ -342,6 +364,13 @@ __global__ __launch_bounds__(1024) void gemm_rows_kernel(const uint16_t* __restr
         m = mm;
       }
     const int64_t o = (int64_t)m * n + r0 + row;
+    if constexpr (KS > 1) {  // meet the other slice's partial sum of this value
+      const unsigned long long oth = atomicExch(slots + o, (1ull << 32) | __builtin_bit_cast(uint32_t, v));
+      if (oth == 0ull) continue;  // the other slice finishes this value
+      const float ov = __builtin_bit_cast(float, (uint32_t)(oth & 0xFFFFFFFFull));
+      v = slice == 0 ? v + ov : ov + v;
+      atomicExch(slots + o, 0ull);  // empty for the next launch
+    }
     if (f16_out)
       reinterpret_cast<uint16_t*>(y)[o] = f32_to_f16_bits(v);
     else
@@ -361,12 +390,31 @@ hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t 
                        hipStream_t stream) {
   if (k < 512 || k % 16 != 0) return hipErrorNotSupported;  // whole 16-weight pieces per row
   constexpr int nwave = 16, nthr = 64 * nwave;
-  const int64_t blocks = n < cu_count() ? n : cu_count();
-  const int64_t rows_max = (n + blocks - 1) / blocks;
-  const int64_t ppr = k >> 4;
-  const int64_t xcells = (int64_t)M * 2 * ppr;
-  const size_t lds = (size_t)xcells * 16 + (size_t)nwave * M * rows_max * sizeof(float);
-  if (lds > kRowsLds || rows_max * ppr >= (int64_t(1) << 27) || xcells > 8 * nthr) return hipErrorNotSupported;
+  // one K slice where the activations and row slots fit, else two (k % 32 == 0),
+  // with half as many row blocks so that the workgroups still fill the CUs once
+  auto fits = [&](int ks, int64_t& blocks, size_t& lds) {
+    const int64_t wg = cu_count() / ks;
+    blocks = n < wg ? n : wg;
+    const int64_t rows_max = (n + blocks - 1) / blocks;
+    const int64_t ppr = k / ks / 16;
+    const int64_t xcells = (int64_t)M * 2 * ppr;
+    lds = (size_t)xcells * 16 + (size_t)nwave * M * rows_max * sizeof(float);
+    const int64_t pmax = ks > 1 ? (int64_t(1) << 24) : (int64_t(1) << 27);
+    return k % (16 * ks) == 0 && ppr >= 32 && lds <= kRowsLds && rows_max * ppr < pmax && xcells <= 8 * nthr;
+  };
+  int64_t blocks = 0;
+  size_t lds = 0;
+  int ks = 1;
+  if (!fits(1, blocks, lds)) {
+    ks = 2;
+    if (!fits(2, blocks, lds)) return hipErrorNotSupported;
+  }
+  const int64_t ppr = k / ks / 16, xcells = (int64_t)M * 2 * ppr;
+  unsigned long long* slots = nullptr;
+  if (ks > 1) {  // one 64-bit meeting slot per output value
+    slots = reinterpret_cast<unsigned long long*>(zeroed_counters(2 * (size_t)M * n));
+    if (!slots) return hipErrorOutOfMemory;
+  }
   const int64_t q = n / blocks;
   const int rem = (int)(n % blocks);
   // at least half the LDS of a CU, so that no CU holds two of these workgroups
@@ -375,15 +423,30 @@ hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t 
 #ifndef SQ_VERIFY_ROWS_DEPTH
 #define SQ_VERIFY_ROWS_DEPTH 1
 #endif
-  auto go = [&](auto na_tag, auto xb_tag) {
-    constexpr int NA = decltype(na_tag)::value, XB = decltype(xb_tag)::value;
-    hipLaunchKernelGGL((gemm_rows_kernel<M, NA, nwave, XB, SQ_VERIFY_ROWS_DEPTH>), dim3((unsigned)blocks), dim3(nthr),
-                       lds_launch, stream, x, k, w, n, y, (int)f16_out, q, rem);
+  auto go = [&](auto na_tag, auto xb_tag, auto ks_tag) {
+    constexpr int NA = decltype(na_tag)::value, XB = decltype(xb_tag)::value, KS = decltype(ks_tag)::value;
+    hipLaunchKernelGGL((gemm_rows_kernel<M, NA, nwave, XB, SQ_VERIFY_ROWS_DEPTH, KS>),
+                       dim3((unsigned)blocks, (unsigned)KS), dim3(nthr), lds_launch, stream, x, k, w, n, y,
+                       (int)f16_out, q, rem, slots);
   };
-  if (ppr < 64)  // rows of 512 .. 1023 k: a step meets up to three rows
-    xcells <= 4 * nthr ? go(RowsIntC<3>{}, RowsIntC<4>{}) : go(RowsIntC<3>{}, RowsIntC<8>{});
-  else
-    xcells <= 4 * nthr ? go(RowsIntC<2>{}, RowsIntC<4>{}) : go(RowsIntC<2>{}, RowsIntC<8>{});
+  using C1 = RowsIntC<1>;
+  using C2 = RowsIntC<2>;
+  using C3 = RowsIntC<3>;
+  using C4 = RowsIntC<4>;
+  using C8 = RowsIntC<8>;
+  // rows (or slices of rows) of 32 .. 63 pieces: a step meets up to three rows
+  const bool three = ppr < 64, small = xcells <= 4 * nthr;
+  if (ks > 1) {
+    if (three)
+      small ? go(C3{}, C4{}, C2{}) : go(C3{}, C8{}, C2{});
+    else
+      small ? go(C2{}, C4{}, C2{}) : go(C2{}, C8{}, C2{});
+  } else {
+    if (three)
+      small ? go(C3{}, C4{}, C1{}) : go(C3{}, C8{}, C1{});
+    else
+      small ? go(C2{}, C4{}, C1{}) : go(C2{}, C8{}, C1{});
+  }
   return hipGetLastError();
 }
 

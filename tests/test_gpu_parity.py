@@ -234,10 +234,12 @@ def test_verify_gemm_f16_parity(m, n, k):
 
 # The row-block verify kernel (m <= 8): the 7B q|k|v shape, activations of
 # 8 x 8192 (two staging batches), rows of 768 k (a step meets three rows),
-# 32768 rows of 512 k (the row limit), m = 7 at 5120 k, and k % 16 == 8
-# (not whole pieces: another kernel takes it).
+# 32768 rows of 512 k (the row limit), m = 7 at 5120 k, k % 16 == 8 (not
+# whole pieces: another kernel takes it), and activations too large for one
+# workgroup, where two workgroups share each row block, one per half of K
+# (the 7B down projection among them).
 ROWS_VERIFY = [(5, 4608, 3584), (8, 3000, 8192), (3, 1500, 768), (1, 32768, 512), (7, 5000, 5120),
-               (5, 2000, 1032), (2, 33, 2048)]
+               (5, 2000, 1032), (2, 33, 2048), (5, 1000, 18944), (8, 700, 12288), (5, 3584, 18944)]
 
 
 @pytest.mark.parametrize("m,n,k", ROWS_VERIFY)
