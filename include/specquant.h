@@ -110,7 +110,7 @@ sq_status sq_qgemv_w8a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t*
 
 /* Parent verification of the drafted block with Q16 = W16 (SS III-D.3): the
  * FP16 parent processes the m = b * (kd + 1) drafted positions in one pass.
- *   y[i][r] = sum_c x[i][c] * w16[r][c]        (MFMA, fp32 accumulation)
+ *   y[i][r] = sum_c x[i][c] * w16[r][c]        (fp32 accumulation of exact products)
  * x [m][k] fp16, 1 <= m <= 64, k % 8 == 0, 8 <= k <= 2^20;
  * w16 [n][k] fp16; y [m][n] of y_dtype. */
 sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint16_t* w16,

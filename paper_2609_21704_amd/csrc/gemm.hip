@@ -1,5 +1,8 @@
 // Parent verification GEMM with the FP16 parent (SpecQuant SS III-D.3: the
 // parent Q16 = W16 checks all drafted positions of a block in one pass).
+// Two kernels here: gemm_rows_kernel (m <= 8, row blocks on the vector ALUs,
+// described at the kernel) and gemm_f16_kernel (the tiled matrix-core GEMM
+// below); the large matrices at m <= 16 stream through linear_kernel.
 //
 // y[m][n] = sum_c x[m][c] * W[n][c] with m = b * (kd + 1) rows (5 to 36 at the
 // configurations of interest).  The weight stream dominates (2 bytes per

@@ -3,18 +3,27 @@
 // quantized stack once at m = 1 .. 8 activation rows).
 //
 // The kernels are HBM-bound: each weight byte is read once, with 16-byte
-// loads, 32 contiguous bytes per lane per row.  A task is a block of four
-// rows; one step of a task is 64 lanes x 32 bytes of each of its rows.  A
-// team of nw wavefronts (nw = 4 from four steps per task, 2 from two, else 1)
-// works on one task at a
-// time, its wavefronts splitting the task's steps; a workgroup holds T teams
-// and stages the activations of its K range in LDS once for all of them.  The
-// grid is persistent, about 16 wavefronts per CU: teams walk tasks with a
-// stride of the total team count, fetching their next step while computing
-// the current one.  Row sums are reduced across a wavefront with DPP and across
-// a team's wavefronts through LDS, in a fixed order; teams of several
-// wavefronts advance through their tasks in step with the workgroup's
-// barriers (a team without a task left runs an unstored copy of its last).
+// loads, 32 contiguous bytes per lane per row.  Two work splits, chosen per
+// launch by measured crossover (gemv_m):
+//   gemv_kernel (tasks of rows): a task is a block of up to four rows; one
+//     step of a task is 64 lanes x 32 bytes of each of its rows.  A team of
+//     nw wavefronts (nw = 4 from four steps per task, 2 from two, else 1)
+//     works on one task at a time, its wavefronts splitting the task's steps;
+//     a workgroup holds T teams and stages the activations of its K range in
+//     LDS once for all of them.  The grid is persistent, about 16 wavefronts
+//     per CU: teams walk tasks with a stride of the total team count,
+//     fetching their next step while computing the current one.  Row sums are
+//     reduced across a wavefront with DPP and across a team's wavefronts
+//     through LDS, in a fixed order; teams of several wavefronts advance
+//     through their tasks in step with the workgroup's barriers (a team
+//     without a task left runs an unstored copy of its last).  Its tasks of
+//     two or four rows share each activation read: it takes the matrices with
+//     many rows (gate|up, the LM head).
+//   gemv_rows_kernel (row blocks, INT4, m <= 2): each CU's workgroups own a
+//     contiguous block of rows, walked by their wavefronts in runs of whole
+//     64-piece steps; it takes the launches where a task would be one row or
+//     would leave lanes idle (q|k|v, o and down at 7B).  Described at the
+//     kernel.
 //
 // INT4 (W4A16).  A lane's 32 bytes are 64 consecutive 4-bit codes of one row,
 // i.e. half of one 128-element group.  Each 32-bit word (codes of k..k+7) is
