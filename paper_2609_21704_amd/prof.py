@@ -8,6 +8,11 @@
         counters, each divided by what the same counter reads, per byte, for the
         plain copy pass over N bytes (read once, written once) that the profiled
         command dispatches last
+    python -m paper_2609_21704_amd.prof verify <MfmaUtil/MfmaFlopsF16 dir> <FETCH_SIZE dir> <WRITE_SIZE dir>
+            --copy-bytes N --m M --layers L --shapes NAME:NxK,... [--lm NxK]
+        per verify projection (the verify dispatches of one round, in their
+        order: the L layers' shapes in turn, then the LM head): duration,
+        executed matrix-core flops, matrix-core busy fraction, HBM bytes
 
 The inputs are the rocpd SQLite databases rocprofv3 writes (*.db).
 """
@@ -114,6 +119,78 @@ def traffic(fetch_dir, write_dir, copy_bytes):
     ])
 
 
+VERIFY_KERNELS = ("sq::linear_kernel", "sq::gemm_rows_kernel", "sq::gemm_f16_kernel", "sq::slice_reduce_kernel")
+
+
+def dispatch_counters(path):
+    """{dispatch_id: (short kernel name, duration ns, {counter: value})}."""
+    out = {}
+    for db in _dbs(path):
+        con = sqlite3.connect(db)
+        for d, k, c, v, dur in con.execute(
+                "select dispatch_id, kernel_name, counter_name, value, duration from counters_collection"):
+            e = out.setdefault(d, [short_name(k), dur, {}])
+            e[2][c] = v
+    return out
+
+
+def verify(mfma_dir, fetch_dir, write_dir, copy_bytes, m, layers, shapes, lm):
+    mf = dispatch_counters(mfma_dir)
+    fe = dispatch_counters(fetch_dir)
+    wr = dispatch_counters(write_dir)
+    # the copy pass is the last dispatch of every run: counter bytes per copied byte
+    f_scale = fe[max(fe)][2]["FETCH_SIZE"] * 1024.0 / copy_bytes
+    w_scale = wr[max(wr)][2]["WRITE_SIZE"] * 1024.0 / copy_bytes
+
+    def seq(runs):
+        return [runs[d] for d in sorted(runs) if runs[d][0].startswith(VERIFY_KERNELS)]
+
+    vm, vf, vw = seq(mf), seq(fe), seq(wr)
+    labels = [name for _ in range(layers) for name, _, _ in shapes] + (["lm_head"] if lm else [])
+    dims = {name: (n, k) for name, n, k in shapes}
+    if lm:
+        dims["lm_head"] = lm
+    # a projection may take two dispatches (a K-slice reduction follows); attach those to the previous one
+    groups = []
+    for i, e in enumerate(vm):
+        if e[0].startswith("sq::slice_reduce_kernel") and groups:
+            groups[-1].append(i)
+        else:
+            groups.append([i])
+    if len(groups) != len(labels):
+        raise SystemExit(f"{len(groups)} verify calls in the profile, {len(labels)} expected")
+    rows = collections.OrderedDict()
+    for name, idx in zip(labels, groups):
+        r = rows.setdefault(name, {"calls": 0, "dur": 0.0, "flops": 0.0, "busy": 0.0, "hbm": 0.0, "kernels": set()})
+        r["calls"] += 1
+        for i in idx:
+            r["kernels"].add(vm[i][0].replace("sq::", ""))
+            r["dur"] += vm[i][1]
+            r["flops"] += vm[i][2].get("MfmaFlopsF16", 0.0)
+            # busy fraction weighted by duration over the projection's dispatches
+            r["busy"] += vm[i][2].get("MfmaUtil", 0.0) / 100.0 * vm[i][1]
+            r["hbm"] += vf[i][2]["FETCH_SIZE"] * 1024.0 / f_scale + vw[i][2]["WRITE_SIZE"] * 1024.0 / w_scale
+    lines = [f"{'projection':10s} {'n x k':>14s} {'calls':>5s} {'us/call':>8s} {'alg MB':>8s} {'HBM MB':>8s} "
+             f"{'HBM/alg':>7s} {'TB/s':>6s} {'MFMA TF/s':>9s} {'MFMA busy':>9s}  kernels"]
+    for name, r in rows.items():
+        n, k = dims[name]
+        c = r["calls"]
+        alg = 2.0 * n * k + 2.0 * m * k + 4.0 * m * n
+        dur = r["dur"] / c
+        hbm = r["hbm"] / c
+        lines.append(f"{name:10s} {f'{n}x{k}':>14s} {c:>5d} {dur / 1e3:>8.2f} {alg / 1e6:>8.2f} {hbm / 1e6:>8.2f} "
+                     f"{hbm / alg:>7.3f} {alg / dur / 1e3:>6.2f} {r['flops'] / c / dur / 1e3:>9.1f} "
+                     f"{r['busy'] / r['dur']:>9.4f}  {','.join(sorted(r['kernels']))}")
+    lines.append(f"fetch_counter_bytes_per_copied_byte = {f_scale:.6f}")
+    lines.append(f"write_counter_bytes_per_copied_byte = {w_scale:.6f}")
+    return "\n".join(lines)
+
+
+def _nk(s):
+    n, k = s.lower().split("x")
+    return int(n), int(k)
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -124,11 +201,24 @@ def main():
     b.add_argument("fetch_dir")
     b.add_argument("write_dir")
     b.add_argument("--copy-bytes", type=int, required=True)
+    c = sub.add_parser("verify")
+    c.add_argument("mfma_dir")
+    c.add_argument("fetch_dir")
+    c.add_argument("write_dir")
+    c.add_argument("--copy-bytes", type=int, required=True)
+    c.add_argument("--m", type=int, required=True)
+    c.add_argument("--layers", type=int, required=True)
+    c.add_argument("--shapes", required=True, help="name:NxK,... in the order of one layer's verify calls")
+    c.add_argument("--lm", type=_nk, help="NxK of the LM head, verified after the layers")
     args = ap.parse_args()
     if args.cmd == "stats":
         print(stats(args.path, args.match))
-    else:
+    elif args.cmd == "traffic":
         print(traffic(args.fetch_dir, args.write_dir, args.copy_bytes))
+    else:
+        shapes = [(part.split(":")[0],) + _nk(part.split(":")[1]) for part in args.shapes.split(",")]
+        print(verify(args.mfma_dir, args.fetch_dir, args.write_dir, args.copy_bytes, args.m, args.layers, shapes,
+                     args.lm))
 
 
 if __name__ == "__main__":
