@@ -2,11 +2,18 @@
 round driver that the benchmark times, against the CPU oracle.
 
 Workload 0 (one Qwen2.5-0.5B-shaped layer) is checked in full.  Workloads 1-4
-build layer 0 and the LM head at full size; every matrix's quantized codes are
-checked bit for bit on 64 seeded rows plus the first and last row, and the
-draft GEMV and verify GEMM outputs at those rows within the normalised-error
-bound.  One whole round then runs through the driver, and its draft draws and
-accept step are checked bit for bit against the oracle on the round's own
+build every layer:
+  - quantized codes bit for bit: every row of every matrix for workloads 1
+    and 2; for workloads 3 and 4 every row of layers 0 and L-1 and the LM
+    head, and 1 % of the rows (at least 64, plus the first and last) of every
+    other matrix;
+  - the draft GEMV and the verify GEMM within the normalised-error bound: every
+    row of layers 0 and L-1 and the LM head, 64 seeded rows (plus the first
+    and last) of every other matrix.  At 36 verify rows (workload 3) the fp64
+    oracle GEMM over whole matrices would take minutes, so there the verify
+    GEMM is checked on 256 seeded rows of every matrix.
+Two whole rounds then run through the driver, and their draft draws and
+accept steps are checked bit for bit against the oracle on the rounds' own
 logits and uniforms."""
 import numpy as np
 import pytest
@@ -33,42 +40,63 @@ def sample_rows(n: int, seed: int, count: int = 64) -> np.ndarray:
     return np.unique(np.concatenate([rows, [0, n - 1]]))
 
 
-def check_matrix(stack: Stack, key, rows, seed: int):
-    """Quantized rows bit for bit, then the draft GEMV (m = B) and the verify
-    GEMM (m = B(k+1)) at those rows, with the output types the driver uses."""
-    cfg = stack.cfg
+def check_quant(stack: Stack, key, rows):
+    """The draft copy's codes, scales (and zeros) at `rows`, bit for bit."""
     w16 = stack.w16[key]
-    n, k = w16.shape
     idx = torch.from_numpy(rows).to(DEV)
     w_rows = bits16(w16.index_select(0, idx))
     pack = stack.draft[key]
     if stack.variant == "int4":
-        c_ref, s_ref, z_ref = oracle.quantize_int4_g128(w_rows)
-        assert np.array_equal(pack[0].index_select(0, idx).cpu().numpy(), c_ref), key
-        assert np.array_equal(bits16(pack[1].index_select(0, idx)), s_ref), key
-        assert np.array_equal(bits16(pack[2].index_select(0, idx)), z_ref), key
+        ref = oracle.quantize_int4_g128(w_rows)
+        assert np.array_equal(pack[0].index_select(0, idx).cpu().numpy(), ref[0]), key
+        assert np.array_equal(bits16(pack[1].index_select(0, idx)), ref[1]), key
+        assert np.array_equal(bits16(pack[2].index_select(0, idx)), ref[2]), key
     else:
-        c_ref, s_ref = oracle.quantize_fp8_e4m3(w_rows)
-        assert np.array_equal(pack[0].index_select(0, idx).cpu().numpy(), c_ref), key
-        assert np.array_equal(pack[1].index_select(0, idx).cpu().numpy().view(np.uint32), s_ref.view(np.uint32)), key
+        ref = oracle.quantize_fp8_e4m3(w_rows)
+        assert np.array_equal(pack[0].index_select(0, idx).cpu().numpy(), ref[0]), key
+        assert np.array_equal(pack[1].index_select(0, idx).cpu().numpy().view(np.uint32), ref[1].view(np.uint32)), key
+    return w_rows, ref
 
+
+def check_products(stack: Stack, key, rows, seed: int, w_rows=None, ref=None, draft=True, verify=True):
+    """The draft GEMV (m = B) and the verify GEMM (m = B(k+1)) at `rows`, with
+    the output types the driver uses."""
+    cfg = stack.cfg
+    if w_rows is None:
+        w_rows, ref = check_quant(stack, key, rows)
+    n, k = stack.w16[key].shape
+    idx = torch.from_numpy(rows).to(DEV)
     y_dtype = torch.float32 if key[1] == "lm_head" else torch.float16
-    xd = synth.normal_f16((cfg.draft_m, k), 1.0, synth.stream_seed(seed, 1), DEV)
-    y = torch.empty((cfg.draft_m, n), dtype=y_dtype, device=DEV)
-    stack.draft_gemv(key, xd, y)
-    if stack.variant == "int4":
-        y_ref, d_ref = oracle.qgemv_w4a16(bits16(xd), c_ref, s_ref, z_ref)
-    else:
-        y_ref, d_ref = oracle.qgemv_w8a16(bits16(xd), c_ref, s_ref)
-    err = oracle.normalised_error(y.index_select(1, idx).float().cpu().numpy(), y_ref, d_ref)
-    assert err <= GEMV_TOL, (key, "draft", err)
-
+    if draft:
+        check_draft(stack, key, idx, seed, ref, y_dtype)
+    if not verify:
+        return
     xv = synth.normal_f16((cfg.verify_m, k), 1.0, synth.stream_seed(seed, 2), DEV)
     yv = torch.empty((cfg.verify_m, n), dtype=y_dtype, device=DEV)
     stack.verify_gemm(key, xv, yv)
     yv_ref, dv_ref = oracle.gemm_f16(bits16(xv), w_rows)
     err = oracle.normalised_error(yv.index_select(1, idx).float().cpu().numpy(), yv_ref, dv_ref)
     assert err <= GEMV_TOL, (key, "verify", err)
+
+
+def check_draft(stack: Stack, key, idx, seed: int, ref, y_dtype):
+    cfg = stack.cfg
+    n, k = stack.w16[key].shape
+    xd = synth.normal_f16((cfg.draft_m, k), 1.0, synth.stream_seed(seed, 1), DEV)
+    y = torch.empty((cfg.draft_m, n), dtype=y_dtype, device=DEV)
+    stack.draft_gemv(key, xd, y)
+    if stack.variant == "int4":
+        y_ref, d_ref = oracle.qgemv_w4a16(bits16(xd), *ref)
+    else:
+        y_ref, d_ref = oracle.qgemv_w8a16(bits16(xd), *ref)
+    err = oracle.normalised_error(y.index_select(1, idx).float().cpu().numpy(), y_ref, d_ref)
+    assert err <= GEMV_TOL, (key, "draft", err)
+
+
+def check_matrix(stack: Stack, key, rows, seed: int):
+    """Quantized rows bit for bit, then the draft GEMV and verify GEMM at those rows."""
+    w_rows, ref = check_quant(stack, key, rows)
+    check_products(stack, key, rows, seed, w_rows, ref)
 
 
 def check_round(rnd: Round, round_index: int):
@@ -113,12 +141,30 @@ WORKLOADS = [(1, "int4"), (1, "fp8"), (2, "int4"), (3, "fp8"), (4, "int4")]
 
 
 @pytest.mark.parametrize("index,variant", WORKLOADS)
-def test_workload_full_shapes_sampled(index, variant):
+def test_workload_whole_stack(index, variant):
     cfg = CONFIGS[index]
-    stack = Stack(cfg, DEV, variant=variant, layers=1)
+    stack = Stack(cfg, DEV, variant=variant)
+    last = cfg.layers - 1
+    all_codes = index in (1, 2)  # every row's codes for the 1.5B and 7B stacks
     for j, key in enumerate(sorted(stack.w16)):
         n = stack.w16[key].shape[0]
-        check_matrix(stack, key, sample_rows(n, cfg.seed * 1000 + j), seed=cfg.seed * 100 + j)
+        full = key[0] in (0, last) or key[1] == "lm_head"
+        seed = cfg.seed * 100 + j
+        if full and cfg.verify_m <= 8:
+            check_matrix(stack, key, np.arange(n), seed)
+            continue
+        if full:  # codes and the draft GEMV on every row, the verify GEMM on sampled rows
+            w_rows, ref = check_quant(stack, key, np.arange(n))
+            check_products(stack, key, np.arange(n), seed, w_rows, ref, verify=False)
+            check_products(stack, key, sample_rows(n, cfg.seed * 3000 + j, count=256), seed, draft=False)
+            continue
+        prod_rows = sample_rows(n, cfg.seed * 1000 + j)
+        if all_codes:
+            check_quant(stack, key, np.arange(n))
+            check_products(stack, key, prod_rows, seed)
+        else:
+            check_quant(stack, key, sample_rows(n, cfg.seed * 2000 + j, count=max(64, n // 100)))
+            check_products(stack, key, prod_rows, seed)
     rnd = Round(stack, temperature=1.0)
     check_round(rnd, 0)
     check_round(rnd, 1)
