@@ -17,6 +17,7 @@
 // tile-per-workgroup GEMM, which measured faster there.  Thresholds in weight
 // bytes.
 constexpr int64_t kLinearMinBytesF16 = int64_t(28) << 20;  // between 3584^2 and 4608 x 3584 (7B o, q|k|v)
+constexpr int64_t kLinearMinBytesF16Wide = int64_t(4) << 20;  // m > 16: between 1152 x 896 and 896 x 4864
 constexpr int64_t kLinearMinBytesW8 = int64_t(64) << 20;
 constexpr int64_t kRowsMinBytesF16 = int64_t(4) << 20;  // 0.5B gate|up 896 x 4864 takes it, 896 x 896 not
 constexpr int64_t kRowsMaxRowsF16 = 32768;              // 14B gate|up 27648 x 5120 takes it, 7B 37888 x 3584 not
@@ -255,13 +256,14 @@ sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint
   (void)hipGetLastError();
   // row blocks on the vector ALUs for m <= 8 from 4 MiB of weights up to
   // 32768 rows (their activations and row slots must fit in LDS), the
-  // matrix-core streaming kernel for larger matrices, else the tiled GEMM
+  // matrix-core streaming kernel for larger matrices (m > 16: from 4 MiB),
+  // else the tiled GEMM
   // (measured crossovers; each returns hipErrorNotSupported, enqueuing
   // nothing, for a shape it does not take)
   hipError_t e = hipErrorNotSupported;
   if (m <= 8 && n * k * 2 >= kRowsMinBytesF16 && n <= kRowsMaxRowsF16)
     e = sq::launch_gemm_rows_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream);
-  if (e == hipErrorNotSupported && m <= 16 && n * k * 2 >= kLinearMinBytesF16)
+  if (e == hipErrorNotSupported && n * k * 2 >= (m > 16 ? kLinearMinBytesF16Wide : kLinearMinBytesF16))
     e = sq::launch_linear_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream);
   if (e == hipErrorNotSupported) e = sq::launch_gemm_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream);
   return device_status(e);

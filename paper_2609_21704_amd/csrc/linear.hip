@@ -1,7 +1,7 @@
 // Weight-streaming linear layers on the matrix cores: the draft projections
 // with the INT4 or FP8 parent (SpecQuant SS III-D.2) and the verification
 // pass with the FP16 parent (SS III-D.3),
-//   y[m][n] = sum_c x[m][c] * W'[n][c],   1 <= m <= 16,
+//   y[m][n] = sum_c x[m][c] * W'[n][c],   1 <= m <= 16 (FP16: m <= 64),
 // with W' the dequantized weight (INT4: (q - z) * s per 128-element group;
 // FP8: decode(c) * s per row; FP16: W itself).
 //
@@ -11,7 +11,8 @@
 // v_mfma_f32_16x16x32_f16 (lane l: B[8 j .. 8 j + 8)[l % 16]).  The
 // activations are the A operand, read from LDS in the same k order, and the
 // output tile D[m][n] accumulates in fp32 on the matrix cores; the m rows
-// are padded to one 16-row tile.
+// are padded to MT 16-row tiles (MT = 1 for INT4 and FP8), each a matrix-core
+// product with the same weight fragment.
 //   INT4: a 16-byte slab is one 128-element group of 16 rows (quarter j holds
 //     codes 32 j .. 32 j + 32); each 32-bit code word becomes 8 halves without
 //     a conversion instruction (a nibble masked into the mantissa of the
@@ -43,6 +44,13 @@
 // into slices.  Two slices meet per output value in a 64-bit slot the same
 // way (slice 0's partial is the left operand); the partial outputs of more
 // slices are added in slice order by a second kernel.
+//
+// Direct mode (m > 16, when the chunks' partial sums would not fit in LDS:
+// m x 16 floats per chunk): a chunk is a whole task, so a workgroup owns whole
+// tasks, a wavefront finishes each task it takes and writes its values at
+// once (or this K slice's partial outputs, added by the second kernel), and
+// the activations get all of the LDS.
+#include <type_traits>
 #include "sq_device.hpp"
 #include "sq_internal.hpp"
 
@@ -211,13 +219,15 @@ struct XStage {
 
 __device__ __forceinline__ half8_t as_h8(u32x4 v) { return __builtin_bit_cast(half8_t, v); }
 
-template <int KIND, int NW>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4)))
+// (several activation tiles hold more registers; a CU runs one workgroup of 8
+// wavefronts, two per SIMD)
+template <int KIND, int NW, int MT>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(MT == 1 ? 4 : 2)))
 void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t kslice, const uint8_t* __restrict__ w,
                    const uint16_t* __restrict__ scales16, const uint16_t* __restrict__ zeros16,
                    const float* __restrict__ scales32, int64_t n, void* __restrict__ y, int f16_out,
                    float* __restrict__ split_out, int64_t nwg_max, int chunk_units, unsigned long long* xchg,
-                   unsigned long long* slice_xchg) {
+                   unsigned long long* slice_xchg, int direct) {
   extern __shared__ __align__(16) char smem[];
   __shared__ int next_chunk;
   constexpr int KS = k_per_slab<KIND>();
@@ -281,10 +291,25 @@ void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t ksl
   }
   __syncthreads();
 
+  // the finished value (m, row): row scale (FP8), then y or this slice's partial output
+  auto store_y = [&](int64_t row, int m, float val) {
+    if constexpr (KIND == kW8) val *= scales32[row];
+    if (split_out)
+      split_out[((int64_t)split * M + m) * n + row] = val;
+    else if (f16_out)
+      reinterpret_cast<uint16_t*>(y)[(int64_t)m * n + row] = f32_to_f16_bits(val);
+    else
+      reinterpret_cast<float*>(y)[(int64_t)m * n + row] = val;
+  };
+
   if (cl < nch) {
-    // a valid activation row for the padding rows of the A tile (their outputs are dropped)
-    const int arow = col < M ? col : 0;
-    float4_t acc = float4_t{0.f, 0.f, 0.f, 0.f};
+    // a valid activation row for the padding rows of each A tile (their outputs are dropped)
+    int arow[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) arow[mt] = mt * 16 + col < M ? mt * 16 + col : 0;
+    float4_t acc[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[mt] = float4_t{0.f, 0.f, 0.f, 0.f};
     bool more = true;
 
     // masks and magic numbers in VGPRs, so each mask-and-insert is one v_and_or_b32
@@ -335,12 +360,12 @@ void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t ksl
             const half2_t d2 = __builtin_bit_cast(half2_t, (q8 & mlo) | k1024) - c1024;  // q2 - z, q6 - z
             const half2_t d3 = __builtin_bit_cast(half2_t, (q8 & mhi) | k64) - c64;      // q3 - z, q7 - z
             const half8_t bw = half8_t{d0[0], d0[1], d1[0], d1[1], d2[0], d2[1], d3[0], d3[1]};
-            const half8_t a = as_h8(*reinterpret_cast<const u32x4*>(xs + ((size_t)arow * g.xs_stride + cell0 + wd) * 8));
+            const half8_t a = as_h8(*reinterpret_cast<const u32x4*>(xs + ((size_t)arow[0] * g.xs_stride + cell0 + wd) * 8));
             gacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, wd == 0 ? float4_t{0.f, 0.f, 0.f, 0.f} : gacc, 0, 0,
                                                           0);
           }
           const float s = valid ? f16_bits_to_f32((uint16_t)sc[u]) : 0.f;
-          acc += s * gacc;
+          acc[0] += s * gacc;
         } else if constexpr (KIND == kW8) {
 #pragma unroll
           for (int wd = 0; wd < 2; ++wd) {
@@ -350,22 +375,52 @@ void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t ksl
             const half2_t h2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w1, 1.0f, false);
             const half2_t h3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w1, 1.0f, true);
             const half8_t bw = half8_t{h0[0], h0[1], h1[0], h1[1], h2[0], h2[1], h3[0], h3[1]};
-            const half8_t a = as_h8(*reinterpret_cast<const u32x4*>(xs + ((size_t)arow * g.xs_stride + cell0 + wd) * 8));
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, acc, 0, 0, 0);
+            const half8_t a = as_h8(*reinterpret_cast<const u32x4*>(xs + ((size_t)arow[0] * g.xs_stride + cell0 + wd) * 8));
+            acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, acc[0], 0, 0, 0);
           }
         } else {
           const half8_t bw = as_h8(c);
-          const half8_t a = as_h8(*reinterpret_cast<const u32x4*>(xs + ((size_t)arow * g.xs_stride + cell0) * 8));
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, acc, 0, 0, 0);
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            const half8_t a =
+                as_h8(*reinterpret_cast<const u32x4*>(xs + ((size_t)arow[mt] * g.xs_stride + cell0) * 8));
+            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, acc[mt], 0, 0, 0);
+          }
         }
       }
-      if (b + 1 == b_end) {  // the chunk's last unit: its partial sum goes to the chunk's slot
+      if (b + 1 == b_end) {  // the chunk's last unit
+        if (MT > 1 && direct) {
+          // the chunk is a whole task of this workgroup: its values are finished
+          // here (meeting the other K slice's in a 64-bit slot when there are two)
+          const int64_t row = t * 16 + col;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = 4 * q + r;
-          if (m < M) pl[((size_t)cl * M + m) * 16 + col] = acc[r];
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int m = mt * 16 + 4 * q + r;
+              if (m >= M || row >= n) continue;
+              float val = acc[mt][r];
+              if (slice_xchg) {
+                unsigned long long* sl = slice_xchg + (size_t)m * n + row;
+                const unsigned long long oth = atomicExch(sl, (1ull << 32) | __builtin_bit_cast(uint32_t, val));
+                if (oth == 0ull) continue;  // the other slice finishes this value
+                const float o = __builtin_bit_cast(float, (uint32_t)(oth & 0xFFFFFFFFull));
+                val = split == 0 ? val + o : o + val;
+                atomicExch(sl, 0ull);  // empty for the next launch
+              }
+              store_y(row, m, val);
+            }
+        } else {  // its partial sum goes to the chunk's slot
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int m = mt * 16 + 4 * q + r;
+              if (m < M) pl[((size_t)cl * M + m) * 16 + col] = acc[mt][r];
+            }
         }
-        acc = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[mt] = float4_t{0.f, 0.f, 0.f, 0.f};
       }
       t = t_n;
       b = b_n;
@@ -383,16 +438,6 @@ void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t ksl
   }
   __syncthreads();
 
-  // the finished value (m, row): row scale (FP8), then y or this slice's partial output
-  auto store_y = [&](int64_t row, int m, float val) {
-    if constexpr (KIND == kW8) val *= scales32[row];
-    if (split_out)
-      split_out[((int64_t)split * M + m) * n + row] = val;
-    else if (f16_out)
-      reinterpret_cast<uint16_t*>(y)[(int64_t)m * n + row] = f32_to_f16_bits(val);
-    else
-      reinterpret_cast<float*>(y)[(int64_t)m * n + row] = val;
-  };
 
   // Every task with chunks here: its chunks' partial sums are added in chunk
   // order (wavefront wv takes tasks wv, wv + NW, ...).  A task whose chunks
@@ -402,10 +447,10 @@ void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t ksl
   // operand).  The loops stay rolled: this tail runs once per launch, and
   // unrolled it would be fetched into the instruction cache cold.
   // Lane quarter q takes output rows m = q + 4 j.
-  constexpr int MQ = 4;
+  constexpr int MQ = 4 * MT;
   const int64_t t_lo = div_floor(c0, J), t_hi = div_floor(c1 - 1, J);
 #pragma unroll 1
-  for (int64_t tt = t_lo + wv; tt <= t_hi; tt += NW) {
+  for (int64_t tt = t_lo + wv; !(MT > 1 && direct) && tt <= t_hi; tt += NW) {
     const int64_t ca = tt * J > c0 ? tt * J : c0, cb = (tt + 1) * J < c1 ? (tt + 1) * J : c1;
     const int64_t row = tt * 16 + col;
     int mm[MQ];
@@ -488,13 +533,14 @@ __global__ __launch_bounds__(256) void slice_reduce_kernel(const float* __restri
 constexpr size_t kLdsTotal = 150 * 1024;   // one workgroup per CU
 constexpr size_t kPieceBudget = 32 * 1024; // chunk partial sums
 
-template <int KIND, int NW>
+template <int KIND, int NW, int MT>
 hipError_t linear_launch(const uint16_t* x, int m, int64_t k, const uint8_t* w, const uint16_t* scales16,
                          const uint16_t* zeros16, const float* scales32, int64_t n, void* y, bool f16_out,
-                         hipStream_t stream) {
+                         bool direct, hipStream_t stream) {
   constexpr int64_t UK = (int64_t)kU * k_per_slab<KIND>();
-  // K slices of whole units whose activations fit (2 bytes per k and row, plus a pad cell per row)
-  int64_t kmax = (int64_t)((kLdsTotal - kPieceBudget) / ((size_t)m * 2)) - 8;
+  // K slices of whole units whose activations fit (2 bytes per k and row, plus a pad cell per row);
+  // the direct mode keeps no chunk partial sums in LDS
+  int64_t kmax = (int64_t)((kLdsTotal - (direct ? 0 : kPieceBudget)) / ((size_t)m * 2)) - 8;
   kmax = kmax / UK * UK;
   if (kmax < UK) return hipErrorNotSupported;  // the caller takes another kernel
   const int splits = (int)((k + kmax - 1) / kmax);
@@ -509,20 +555,21 @@ hipError_t linear_launch(const uint16_t* x, int m, int64_t k, const uint8_t* w, 
   const int64_t cap = (int64_t)cu_count() / splits;
   if (nwg_max > cap) nwg_max = cap;
   if (nwg_max < 1) nwg_max = 1;
-  // the smallest chunk whose partial sums ([chunks per workgroup][m][16] floats) fit the budget
-  int64_t C = SQ_LINEAR_CHUNK_MIN, nch_max = 0;
+  // the smallest chunk whose partial sums ([chunks per workgroup][m][16] floats) fit the budget;
+  // direct: one chunk per task, no partial sums
+  int64_t C = direct ? S : SQ_LINEAR_CHUNK_MIN, nch_max = 0;
   for (;; ++C) {
     const int64_t J = (S + C - 1) / C;
     nch_max = (ntask * J + nwg_max - 1) / nwg_max;
-    if ((size_t)nch_max * m * 16 * sizeof(float) <= kPieceBudget || C >= S) break;
+    if (direct || (size_t)nch_max * m * 16 * sizeof(float) <= kPieceBudget || C >= S) break;
   }
-  if ((size_t)nch_max * m * 16 * sizeof(float) > kPieceBudget) return hipErrorNotSupported;
+  if (!direct && (size_t)nch_max * m * 16 * sizeof(float) > kPieceBudget) return hipErrorNotSupported;
   // the kernel's chunk arithmetic is exact below 2^52 (workgroup index x chunks per slice)
   if ((double)(nwg_max + 1) * (double)(ntask * S) >= 4503599627370496.0) return hipErrorNotSupported;
-  const size_t lds = ((size_t)m * cells * 16 + 15) / 16 * 16 + (size_t)nch_max * m * 16 * sizeof(float);
+  const size_t lds = ((size_t)m * cells * 16 + 15) / 16 * 16 + (direct ? 0 : (size_t)nch_max * m * 16 * sizeof(float));
 
   // two K slices meet per output value in a 64-bit slot; more are summed by a second kernel
-  const bool slice_meet = splits == 2;
+  const bool slice_meet = splits == 2 && !direct;
   const size_t split_bytes =
       splits > 1 && !slice_meet ? ((size_t)splits * m * n * sizeof(float) + 255) / 256 * 256 : 0;
   float* split_out = nullptr;
@@ -538,9 +585,9 @@ hipError_t linear_launch(const uint16_t* x, int m, int64_t k, const uint8_t* w, 
   unsigned long long* xchg = reinterpret_cast<unsigned long long*>(slots);
   // more than half the LDS, so that a CU holds one workgroup
   const size_t lds_launch = lds < 81 * 1024 ? 81 * 1024 : lds;
-  hipLaunchKernelGGL((linear_kernel<KIND, NW>), dim3((unsigned)nwg_max, (unsigned)splits), dim3(NW * 64), lds_launch,
-                     stream, x, m, k, kslice, w, scales16, zeros16, scales32, n, y, (int)f16_out, split_out, nwg_max,
-                     (int)C, xchg, slice_meet ? xchg + wg_slots : nullptr);
+  hipLaunchKernelGGL((linear_kernel<KIND, NW, MT>), dim3((unsigned)nwg_max, (unsigned)splits), dim3(NW * 64),
+                     lds_launch, stream, x, m, k, kslice, w, scales16, zeros16, scales32, n, y, (int)f16_out,
+                     split_out, nwg_max, (int)C, xchg, slice_meet ? xchg + wg_slots : nullptr, (int)direct);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || splits == 1 || slice_meet) return err;
   int64_t blocks = ((int64_t)m * n + 255) / 256;
@@ -558,8 +605,22 @@ template <int KIND>
 hipError_t linear_dispatch(const uint16_t* x, int m, int64_t k, const uint8_t* w, const uint16_t* scales16,
                            const uint16_t* zeros16, const float* scales32, int64_t n, void* y, bool f16_out,
                            hipStream_t stream) {
-  if (m < 1 || m > 16) return hipErrorInvalidValue;
-  return linear_launch<KIND, 8>(x, m, k, w, scales16, zeros16, scales32, n, y, f16_out, stream);
+  if (m < 1 || m > (KIND == kF16 ? 64 : 16)) return hipErrorInvalidValue;
+  // chunks of a task spread over the wavefronts where their partial sums fit
+  // in LDS, else whole tasks per wavefront (direct)
+  auto go = [&](auto mt_tag) {
+    constexpr int MT = decltype(mt_tag)::value;
+    hipError_t e = linear_launch<KIND, 8, MT>(x, m, k, w, scales16, zeros16, scales32, n, y, f16_out, false, stream);
+    if (e == hipErrorNotSupported && m > 16)
+      e = linear_launch<KIND, 8, MT>(x, m, k, w, scales16, zeros16, scales32, n, y, f16_out, true, stream);
+    return e;
+  };
+  if constexpr (KIND == kF16) {
+    if (m > 48) return go(std::integral_constant<int, 4>{});
+    if (m > 32) return go(std::integral_constant<int, 3>{});
+    if (m > 16) return go(std::integral_constant<int, 2>{});
+  }
+  return go(std::integral_constant<int, 1>{});
 }
 
 }  // namespace
