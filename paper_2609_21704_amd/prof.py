@@ -119,7 +119,10 @@ def traffic(fetch_dir, write_dir, copy_bytes):
     ])
 
 
-VERIFY_KERNELS = ("sq::linear_kernel", "sq::gemm_rows_kernel", "sq::gemm_f16_kernel", "sq::slice_reduce_kernel")
+# the FP16 verification kernels (linear_kernel<2, ...> is the FP16 instance; the
+# INT4 / FP8 instances serve draft projections)
+VERIFY_KERNELS = ("sq::linear_kernel<2,", "sq::gemm_rows_kernel", "sq::gemm_f16_kernel")
+REDUCE_KERNEL = "sq::slice_reduce_kernel"
 
 
 def dispatch_counters(path):
@@ -143,7 +146,16 @@ def verify(mfma_dir, fetch_dir, write_dir, copy_bytes, m, layers, shapes, lm):
     w_scale = wr[max(wr)][2]["WRITE_SIZE"] * 1024.0 / copy_bytes
 
     def seq(runs):
-        return [runs[d] for d in sorted(runs) if runs[d][0].startswith(VERIFY_KERNELS)]
+        # verify dispatches in order, each K-slice reduction that directly follows one attached to it
+        out, prev = [], False
+        for d in sorted(runs):
+            name = runs[d][0]
+            if name.startswith(VERIFY_KERNELS) or (prev and name.startswith(REDUCE_KERNEL)):
+                out.append(runs[d])
+                prev = not name.startswith(REDUCE_KERNEL)
+            else:
+                prev = False
+        return out
 
     vm, vf, vw = seq(mf), seq(fe), seq(wr)
     labels = [name for _ in range(layers) for name, _, _ in shapes] + (["lm_head"] if lm else [])
@@ -153,7 +165,7 @@ def verify(mfma_dir, fetch_dir, write_dir, copy_bytes, m, layers, shapes, lm):
     # a projection may take two dispatches (a K-slice reduction follows); attach those to the previous one
     groups = []
     for i, e in enumerate(vm):
-        if e[0].startswith("sq::slice_reduce_kernel") and groups:
+        if e[0].startswith(REDUCE_KERNEL) and groups:
             groups[-1].append(i)
         else:
             groups.append([i])
