@@ -2,7 +2,8 @@
 // parent Q16 = W16 checks all drafted positions of a block in one pass).
 // Two kernels here: gemm_rows_kernel (m <= 8, row blocks on the vector ALUs,
 // described at the kernel) and gemm_f16_kernel (the tiled matrix-core GEMM
-// below); the large matrices at m <= 16 stream through linear_kernel.
+// below); the large matrices stream through linear_kernel (m <= 16 from
+// 28 MiB of weights, m = 17..64 from 4 MiB).
 //
 // y[m][n] = sum_c x[m][c] * W[n][c] with m = b * (kd + 1) rows (5 to 36 at the
 // configurations of interest).  The weight stream dominates (2 bytes per
