@@ -411,6 +411,21 @@ def test_verify_gemm_f16_large_parity(m, n, k):
     assert torch.equal(sq.sq_verify_gemm_f16(xd, wd), sq.sq_verify_gemm_f16(xd, wd))
 
 
+# m = 17..64 on the matrix-core streaming kernel (several 16-row activation
+# tiles): chunks of a task spread over the wavefronts with their partial sums
+# in LDS (m = 17: two K slices meeting per value; m = 36 at 4104 k: a partial
+# slab and three slices added by the second kernel), and the direct mode,
+# where the partial sums would not fit (whole tasks per wavefront: one slice
+# at m = 20, several slices at m = 48, 64 and 33), over ragged row counts
+WIDE_GEMM = [(17, 16384, 4096), (36, 16381, 4104), (20, 151936, 1024), (48, 37888, 3584), (64, 9001, 5120),
+             (33, 2000, 18944)]
+
+
+@pytest.mark.parametrize("m,n,k", WIDE_GEMM)
+def test_verify_gemm_f16_wide_parity(m, n, k):
+    test_verify_gemm_f16_large_parity(m, n, k)
+
+
 # the last two: K cut into two slices
 LARGE_W8 = [(1, 16384, 4096), (4, 16384, 4096), (8, 16384, 4096), (4, 16381, 4112), (8, 4096, 16384),
             (6, 4097, 16400)]
