@@ -432,31 +432,39 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
 // cell per 64-element chunk (a 144-byte stride), so a lane reads its eight
 // cells at immediate offsets and the 16 lanes of one read fall in different
 // banks.
+//
+// FP8 (W8) takes the same walk with 32 codes to a piece: a lane converts its
+// codes two at a time (v_cvt_scalef32_pk_f16_fp8, exact), the activations are
+// staged in plain k order with four cells and one pad cell to a chunk (an
+// 80-byte stride, again 16 lanes on distinct banks), and the row scale
+// multiplies each finished row sum.  Up to four activation rows (m <= 4).
 struct PieceFrag {
   u32x4 c[2];  // 32 bytes of codes
-  uint32_t s;  // group scale bits
-  uint32_t z;  // group zero bits
+  uint32_t s;  // group scale bits (INT4)
+  uint32_t z;  // group zero bits (INT4)
 };
 
-template <int M, int D, int XB, int NA, int NWV>
+template <int M, bool W8, int D, int XB, int NA, int NWV>
 __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restrict__ x, int64_t k,
                                                         const uint8_t* __restrict__ codes,
                                                         const uint16_t* __restrict__ scales16,
-                                                        const uint16_t* __restrict__ zeros16, int64_t n,
+                                                        const uint16_t* __restrict__ zeros16,
+                                                        const float* __restrict__ scales32, int64_t n,
                                                         void* __restrict__ y, int f16_out, int64_t rows_q,
                                                         int rows_rem) {
   extern __shared__ __align__(16) char smem[];
   // every argument in one batch of scalar loads, before the first address needs one
-  asm volatile("" ::"s"(x), "s"(k), "s"(codes), "s"(scales16), "s"(zeros16), "s"(n), "s"(y), "s"(f16_out),
-               "s"(rows_q), "s"(rows_rem));
-  constexpr int kPad = 9;     // LDS cells per chunk: eight and one pad
-  constexpr int nwave = NWV;  // wavefronts per workgroup, a power of two
+  asm volatile("" ::"s"(x), "s"(k), "s"(codes), "s"(scales16), "s"(zeros16), "s"(scales32), "s"(n), "s"(y),
+               "s"(f16_out), "s"(rows_q), "s"(rows_rem));
+  constexpr int kCPC = W8 ? 4 : 8;  // activation cells (8 halves) per chunk of a piece
+  constexpr int kPad = kCPC + 1;    // LDS cells per chunk: the cells and one pad
+  constexpr int nwave = NWV;        // wavefronts per workgroup, a power of two
   // no integer division on the way to the first load: block b holds rows_q
   // rows, plus one for b < rows_rem
   const int b = blockIdx.x;
   const int64_t r0 = (int64_t)b * rows_q + (b < rows_rem ? b : rows_rem);
   const int nrows = (int)rows_q + (b < rows_rem ? 1 : 0);
-  const int ppr = (int)(k >> 6);  // pieces per row (and activation chunks)
+  const int ppr = (int)(k >> (W8 ? 5 : 6));  // pieces per row (and activation chunks)
   const int P = nrows * ppr;      // pieces of the block (< 2^27 by the host's check)
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -468,9 +476,9 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
   const int nsteps = (pe - ps + 63) >> 6;
   half_t* xs = reinterpret_cast<half_t*>(smem);
   float* red = reinterpret_cast<float*>(smem + (size_t)M * ppr * kPad * 16);  // [nwave][M][nrows]
-  const uint8_t* bcodes = codes + r0 * (k >> 1);
-  const uint16_t* bscales = scales16 + r0 * (k >> 7);
-  const uint16_t* bzeros = zeros16 + r0 * (k >> 7);
+  const uint8_t* bcodes = codes + r0 * (W8 ? k : (k >> 1));
+  const uint16_t* bscales = W8 ? nullptr : scales16 + r0 * (k >> 7);
+  const uint16_t* bzeros = W8 ? nullptr : zeros16 + r0 * (k >> 7);
 
   // piece p of the block: codes at 32 p, group p / 2 (rows hold whole groups);
   // a lane past the run reads the run's last piece again and adds nothing.
@@ -484,22 +492,38 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
     const u32x4* cp = reinterpret_cast<const u32x4*>(bcodes + (int64_t)p * 32);
     f.c[0] = cp[0];
     f.c[1] = cp[1];
-    f.s = bscales[p >> 1];
-    f.z = bzeros[p >> 1];
+    if constexpr (!W8) {
+      f.s = bscales[p >> 1];
+      f.z = bzeros[p >> 1];
+    } else {
+      f.s = f.z = 0u;
+    }
     return f;
   };
 
   // activations first (XB cells per thread cover all of x: the host's
   // choice), then the first D steps of codes
-  const int xtotal = M * ppr * 8, nthr = (int)blockDim.x;
+  const int cpm = ppr * kCPC, xtotal = M * cpm, nthr = (int)blockDim.x;  // cells per activation row, in all
   u32x4 xv[XB];
+  // flat cell index -> (activation row, cell within the row); m <= 4
+  auto xsplit = [&](int idx, int& m, int& rem) {
+    m = 0;
+    rem = idx;
+#pragma unroll
+    for (int i = 1; i < M; ++i)
+      if (rem >= cpm) {
+        rem -= cpm;
+        ++m;
+      }
+  };
   auto xload = [&](int base) {
 #pragma unroll
     for (int b = 0; b < XB; ++b) {
       int idx = base + b * nthr + (int)threadIdx.x;
       idx = idx < xtotal ? idx : xtotal - 1;
-      const int m = idx >= ppr * 8 ? 1 : 0, rem = idx - m * ppr * 8;  // m <= 2
-      xv[b] = x_cell<M, false>(x, k, 0, k, rem >> 3, m, rem & 7);
+      int m, rem;
+      xsplit(idx, m, rem);
+      xv[b] = x_cell<M, W8>(x, k, 0, k, rem / kCPC, m, rem % kCPC);
     }
   };
   auto xstore = [&](int base) {
@@ -507,8 +531,9 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
     for (int b = 0; b < XB; ++b) {
       const int idx = base + b * nthr + (int)threadIdx.x;
       if (idx < xtotal) {
-        const int m = idx >= ppr * 8 ? 1 : 0, rem = idx - m * ppr * 8;
-        *reinterpret_cast<u32x4*>(xs + (((size_t)m * ppr + (rem >> 3)) * kPad + (rem & 7)) * 8) = xv[b];
+        int m, rem;
+        xsplit(idx, m, rem);
+        *reinterpret_cast<u32x4*>(xs + (((size_t)m * ppr + rem / kCPC) * kPad + rem % kCPC) * 8) = xv[b];
       }
     }
   };
@@ -540,12 +565,14 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
     for (int m = 0; m < M; ++m) acc[i][m] = 0.f;
 
   auto flush = [&](const float (&a)[M], int row) {
-    float v[4] = {a[0], M > 1 ? a[M - 1] : 0.f, 0.f, 0.f};
+    float v[4] = {a[0], M > 1 ? a[1] : 0.f, M > 2 ? a[2] : 0.f, M > 3 ? a[3] : 0.f};
     float w[1];
     wave_sums<1>(v, w);
-    // lanes 0-15 hold the total of v[0], lanes 32-47 that of v[1]
+    // lane 16 j holds the total of v[(0, 2, 1, 3)[j]]
     if (lane == 0) red[wave * M * nrows + row] = w[0];
     if (M > 1 && lane == 32) red[(wave * M + 1) * nrows + row] = w[0];
+    if (M > 2 && lane == 16) red[(wave * M + 2) * nrows + row] = w[0];
+    if (M > 3 && lane == 48) red[(wave * M + 3) * nrows + row] = w[0];
   };
 
   auto compute = [&](const PieceFrag& f) {
@@ -560,6 +587,37 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
       rel = 2;
     }
     const bool ok = cb + lane < pe;
+    if constexpr (W8) {
+      float a[M];
+#pragma unroll
+      for (int m = 0; m < M; ++m) a[m] = 0.f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {  // cell w: codes 8 w .. 8 w + 7, the words 2 w and 2 w + 1
+        const uint32_t q0 = f.c[w >> 1][2 * (w & 1)], q1 = f.c[w >> 1][2 * (w & 1) + 1];
+        const half2_t h0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(q0, 1.0f, false);
+        const half2_t h1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(q0, 1.0f, true);
+        const half2_t h2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(q1, 1.0f, false);
+        const half2_t h3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(q1, 1.0f, true);
+#pragma unroll
+        for (int m = 0; m < M; ++m) {
+          const u32x4 v = *reinterpret_cast<const u32x4*>(xs + (((size_t)m * ppr + chunk) * kPad + w) * 8);
+          const uint32_t e0 = v[0], e1 = v[1], e2 = v[2], e3 = v[3];  // scalar copies, as elsewhere
+          float t = a[m];
+          t = __builtin_amdgcn_fdot2(h0, __builtin_bit_cast(half2_t, e0), t, false);
+          t = __builtin_amdgcn_fdot2(h1, __builtin_bit_cast(half2_t, e1), t, false);
+          t = __builtin_amdgcn_fdot2(h2, __builtin_bit_cast(half2_t, e2), t, false);
+          t = __builtin_amdgcn_fdot2(h3, __builtin_bit_cast(half2_t, e3), t, false);
+          a[m] = t;
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < M; ++m) {
+        const float v = ok ? a[m] : 0.f;
+#pragma unroll
+        for (int i = 0; i < NA; ++i) acc[i][m] += rel == i ? v : 0.f;
+      }
+      return;
+    }
     const uint32_t zb = f.z;
     const half2_t z2 = __builtin_bit_cast(half2_t, zb | (zb << 16));
     const half2_t c1024 = z2 + half2_t{(half_t)1024.0f, (half_t)1024.0f};
@@ -629,9 +687,16 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
   }
   __syncthreads();
   for (int t = (int)threadIdx.x; t < M * nrows; t += nthr) {
-    const int m = t >= nrows ? 1 : 0, row = t - m * nrows;
+    int m = 0, row = t;
+#pragma unroll
+    for (int i = 1; i < M; ++i)
+      if (row >= nrows) {
+        row -= nrows;
+        ++m;
+      }
     float v = 0.f;
     for (int w = 0; w < nwave; ++w) v += red[w * M * nrows + t];  // consecutive threads, consecutive words
+    if constexpr (W8) v *= scales32[r0 + row];
     const int64_t o = (int64_t)m * n + r0 + row;
     if (f16_out)
       reinterpret_cast<uint16_t*>(y)[o] = f32_to_f16_bits(v);
@@ -686,24 +751,32 @@ hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits,
 #ifndef SQ_GEMV_ROWS_DEPTH
 #define SQ_GEMV_ROWS_DEPTH 1     // steps of loads in flight per wavefront (measured: 1 < 2 < 3 < 4 in time)
 #endif
+#ifndef SQ_GEMV_ROWS_W8
+#define SQ_GEMV_ROWS_W8 1        // FP8 GEMVs at m <= 4 on the row-block kernel
+#endif
 constexpr size_t kRowsLdsMax = 150 * 1024;
 
-// Host side of the row-block INT4 kernel: 16 wavefronts per CU
-// (fewer workgroups than rows never), rows split evenly over the workgroups.
-// Returns hipErrorNotSupported when the shape is outside what it takes.
-template <int M>
+// Host side of the row-block kernel (INT4 m <= 2, FP8 m <= 4): 16 wavefronts
+// per CU (fewer workgroups than rows never), rows split evenly over the
+// workgroups.  Returns hipErrorNotSupported when the shape is outside what it
+// takes.
+template <int M, bool W8>
 hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint16_t* scales16,
-                       const uint16_t* zeros16, int64_t n, void* y, bool f16_out, hipStream_t stream) {
-  if (M > 2 || k < SQ_GEMV_ROWS_MIN_K || k < 2048) return hipErrorNotSupported;
-  // 16 wavefronts per CU: one workgroup of 16, or two of 8 for rows of 8192 k
-  // and more (measured: 7B down 13.5 -> 12.8 us, q|k|v 5.8 -> 6.0 us)
-  const int nwave = k >= 8192 && M * k <= 8 * 8 * 512 ? 8 : 16, nthr = 64 * nwave;  // 8: x staged in one pass
+                       const uint16_t* zeros16, const float* scales32, int64_t n, void* y, bool f16_out,
+                       hipStream_t stream) {
+  // whole pieces per row: 32 FP8 codes, or 64 INT4 codes (k % 128 == 0 already)
+  if (M > (W8 ? 4 : 2) || k < (W8 ? 1024 : SQ_GEMV_ROWS_MIN_K) || k < (W8 ? 1024 : 2048) || (W8 && k % 32 != 0))
+    return hipErrorNotSupported;
+  // 16 wavefronts per CU: one workgroup of 16, or two of 8 for INT4 rows of
+  // 8192 k and more (measured: 7B down 13.5 -> 12.8 us, q|k|v 5.8 -> 6.0 us)
+  const int nwave = !W8 && k >= 8192 && M * k <= 8 * 8 * 512 ? 8 : 16, nthr = 64 * nwave;  // 8: x in one pass
   const int64_t wg_max = cu_count() * (16 / nwave);
   const int64_t blocks = n < wg_max ? n : wg_max;
   const int64_t rows_max = (n + blocks - 1) / blocks;
-  const int64_t ppr = k >> 6;
-  const size_t lds = (size_t)M * ppr * 9 * 16 + (size_t)M * rows_max * nwave * sizeof(float);
-  const int64_t xcells = M * ppr * 8;  // 16-byte activation cells, staged by the workgroup at once
+  const int64_t ppr = k >> (W8 ? 5 : 6);
+  constexpr int64_t cpc = W8 ? 4 : 8;  // activation cells per chunk
+  const size_t lds = (size_t)M * ppr * (cpc + 1) * 16 + (size_t)M * rows_max * nwave * sizeof(float);
+  const int64_t xcells = M * ppr * cpc;  // 16-byte activation cells, staged by the workgroup at once
   if (lds > kRowsLdsMax || rows_max * ppr >= (int64_t(1) << 27) || xcells > 8 * nthr)
     return hipErrorNotSupported;
   constexpr int D = SQ_GEMV_ROWS_DEPTH;
@@ -714,12 +787,12 @@ hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const
   const size_t lds_launch = nwave == 8 && lds < 54 * 1024 ? 54 * 1024 : lds;
   auto go = [&](auto xb_tag, auto na_tag, auto nw_tag) {
     constexpr int XB = decltype(xb_tag)::value, NA = decltype(na_tag)::value, NWV = decltype(nw_tag)::value;
-    hipLaunchKernelGGL((gemv_rows_kernel<M, D, XB, NA, NWV>), dim3((unsigned)blocks), dim3(nthr), lds_launch, stream,
-                       x, k, codes, scales16, zeros16, n, y, (int)f16_out, q, rem);
+    hipLaunchKernelGGL((gemv_rows_kernel<M, W8, D, XB, NA, NWV>), dim3((unsigned)blocks), dim3(nthr), lds_launch,
+                       stream, x, k, codes, scales16, zeros16, scales32, n, y, (int)f16_out, q, rem);
   };
-  if (nwave == 8)  // k >= 8192: two rows per step at most
+  if (nwave == 8)  // INT4, k >= 8192: two rows per step at most
     xcells <= 4 * nthr ? go(IntC<4>{}, IntC<2>{}, IntC<8>{}) : go(IntC<8>{}, IntC<2>{}, IntC<8>{});
-  else if (ppr < 64)  // rows of 2048 .. 4095 k: a step meets up to three rows
+  else if (ppr < 64)  // rows of 32 .. 63 pieces: a step meets up to three rows
     xcells <= 4 * nthr ? go(IntC<4>{}, IntC<3>{}, IntC<16>{}) : go(IntC<8>{}, IntC<3>{}, IntC<16>{});
   else
     xcells <= 4 * nthr ? go(IntC<4>{}, IntC<2>{}, IntC<16>{}) : go(IntC<8>{}, IntC<2>{}, IntC<16>{});
@@ -779,9 +852,15 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
 #else
     if (rows == 1 || idle_lanes) {
 #endif
-      const hipError_t e = gemv_rows_m<M>(x, k, codes, scales16, zeros16, n, y, f16_out, stream);
+      const hipError_t e = gemv_rows_m<M, false>(x, k, codes, scales16, zeros16, nullptr, n, y, f16_out, stream);
       if (e != hipErrorNotSupported) return e;
     }
+  }
+  if constexpr (W8 && M <= 4) {
+#if SQ_GEMV_ROWS_W8
+    const hipError_t e = gemv_rows_m<M, true>(x, k, codes, nullptr, nullptr, scales32, n, y, f16_out, stream);
+    if (e != hipErrorNotSupported) return e;
+#endif
   }
   hipError_t err = hipErrorInvalidValue;
   auto go = [&](auto r_tag, auto multi_tag) {
