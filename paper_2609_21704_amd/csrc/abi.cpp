@@ -235,10 +235,12 @@ sq_status sq_qgemv_w8a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t*
   const Range ins[] = {{x, (size_t)m * k * 2}, {codes, nk}, {scales, (size_t)n * 4}};
   if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
   (void)hipGetLastError();
-  // the matrix-core kernel from its size on, where its chunk bookkeeping fits
-  // (it enqueues nothing when it returns hipErrorNotSupported)
+  // the matrix-core kernel from its size on at m >= 3, where its chunk
+  // bookkeeping fits (it enqueues nothing when it returns hipErrorNotSupported);
+  // at m <= 2 the GEMVs stream faster at every size (measured)
   hipError_t e = hipErrorNotSupported;
-  if (n * k >= kLinearMinBytesW8) e = sq::launch_linear_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream);
+  if (m >= 3 && n * k >= kLinearMinBytesW8)
+    e = sq::launch_linear_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream);
   if (e == hipErrorNotSupported) e = sq::launch_gemv_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream);
   return device_status(e);
 }
