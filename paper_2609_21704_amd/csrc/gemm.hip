@@ -438,19 +438,23 @@ hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t 
   using C3 = RowsIntC<3>;
   using C4 = RowsIntC<4>;
   using C8 = RowsIntC<8>;
-  // rows (or slices of rows) of 32 .. 63 pieces: a step meets up to three rows
-  const bool three = ppr < 64, small = xcells <= 4 * nthr;
-  if (ks > 1) {
-    if (three)
-      small ? go(C3{}, C4{}, C2{}) : go(C3{}, C8{}, C2{});
+  // rows (or slices of rows) of 32 .. 63 pieces: a step meets up to three rows;
+  // the fewest activation cells per thread that cover the activations
+  const bool three = ppr < 64;
+  auto pick = [&](auto na_tag, auto ks_tag) {
+    if (xcells <= 2 * nthr)
+      go(na_tag, C2{}, ks_tag);
+    else if (xcells <= 3 * nthr)
+      go(na_tag, C3{}, ks_tag);
+    else if (xcells <= 4 * nthr)
+      go(na_tag, C4{}, ks_tag);
     else
-      small ? go(C2{}, C4{}, C2{}) : go(C2{}, C8{}, C2{});
-  } else {
-    if (three)
-      small ? go(C3{}, C4{}, C1{}) : go(C3{}, C8{}, C1{});
-    else
-      small ? go(C2{}, C4{}, C1{}) : go(C2{}, C8{}, C1{});
-  }
+      go(na_tag, C8{}, ks_tag);
+  };
+  if (ks > 1)
+    three ? pick(C3{}, C2{}) : pick(C2{}, C2{});
+  else
+    three ? pick(C3{}, C1{}) : pick(C2{}, C1{});
   return hipGetLastError();
 }
 

@@ -790,12 +790,25 @@ hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const
     hipLaunchKernelGGL((gemv_rows_kernel<M, W8, D, XB, NA, NWV>), dim3((unsigned)blocks), dim3(nthr), lds_launch,
                        stream, x, k, codes, scales16, zeros16, scales32, n, y, (int)f16_out, q, rem);
   };
+  // the fewest activation cells per thread that cover the activations: the
+  // loads past the end are redundant and delay the code loads behind them
+  // (measured: 7B q|k|v 5.9 -> 5.5 us, o 5.45 -> 5.12 us with one cell)
+  auto pick = [&](auto na_tag, auto nw_tag) {
+    if (xcells <= nthr)
+      go(IntC<1>{}, na_tag, nw_tag);
+    else if (xcells <= 2 * nthr)
+      go(IntC<2>{}, na_tag, nw_tag);
+    else if (xcells <= 4 * nthr)
+      go(IntC<4>{}, na_tag, nw_tag);
+    else
+      go(IntC<8>{}, na_tag, nw_tag);
+  };
   if (nwave == 8)  // INT4, k >= 8192: two rows per step at most
-    xcells <= 4 * nthr ? go(IntC<4>{}, IntC<2>{}, IntC<8>{}) : go(IntC<8>{}, IntC<2>{}, IntC<8>{});
+    pick(IntC<2>{}, IntC<8>{});
   else if (ppr < 64)  // rows of 32 .. 63 pieces: a step meets up to three rows
-    xcells <= 4 * nthr ? go(IntC<4>{}, IntC<3>{}, IntC<16>{}) : go(IntC<8>{}, IntC<3>{}, IntC<16>{});
+    pick(IntC<3>{}, IntC<16>{});
   else
-    xcells <= 4 * nthr ? go(IntC<4>{}, IntC<2>{}, IntC<16>{}) : go(IntC<8>{}, IntC<2>{}, IntC<16>{});
+    pick(IntC<2>{}, IntC<16>{});
   return hipGetLastError();
 }
 
