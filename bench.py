@@ -41,6 +41,19 @@ def gemv_bytes(variant: str, m: int, n: int, k: int, out_bytes: int) -> float:
     return w + 2 * m * k + m * n * out_bytes
 
 
+def spin_cycles_per_ms() -> float:
+    """Cycles of torch's spin kernel per millisecond on this device."""
+    import torch
+
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    torch.cuda._sleep(1 << 22)
+    e1.record()
+    torch.cuda.synchronize()
+    return (1 << 22) / max(e0.elapsed_time(e1), 1e-3)
+
+
 def measure_gemv(rnd, steps: int):
     """Average duration of a draft-GEMV launch: HIP events on the launching
     stream bracket the back-to-back GEMV launches of a whole draft pass (every
@@ -50,15 +63,7 @@ def measure_gemv(rnd, steps: int):
     launch latency lands inside the interval."""
     import torch
 
-    # cycles of torch's spin kernel per millisecond on this device
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    torch.cuda._sleep(1 << 22)
-    e1.record()
-    torch.cuda.synchronize()
-    cycles_per_ms = (1 << 22) / max(e0.elapsed_time(e1), 1e-3)
-
+    cycles_per_ms = spin_cycles_per_ms()
     cfg, st = rnd.cfg, rnd.stack
     pass_bytes = 0.0
     n_launch = 0
@@ -86,6 +91,65 @@ def measure_gemv(rnd, steps: int):
         tot_bytes += pass_bytes
         launches += n_launch
     return tot_bytes, tot_s, launches
+
+
+def measure_probe(rnd, steps: int, big_bytes: int = 4 << 30):
+    """The measured read ceiling, with the library's streaming-read probe (one
+    plain 16-byte-load read, nothing else):
+      - `peak`: one read of a 4 GiB buffer (16 times the memory-side cache);
+      - `same_launches`: one probe launch per draft-GEMV launch of a pass, each
+        reading that launch's algorithmic bytes from a fresh place in the
+        buffer, back to back and timed like the GEMVs -- what a pass of plain
+        reads with the same launch sizes costs."""
+    import torch
+
+    from paper_2609_21704_amd import sq_probe_stream_read
+
+    buf = torch.zeros(big_bytes, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(2048, dtype=torch.int32, device="cuda")
+    for _ in range(2):
+        sq_probe_stream_read(buf, sink=sink)
+    torch.cuda.synchronize()
+    best = float("inf")
+    for _ in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        sq_probe_stream_read(buf, sink=sink)
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1) * 1e-3)
+    peak = big_bytes / best / 1e9
+
+    cfg, st = rnd.cfg, rnd.stack
+    sizes = []
+    for l, name, n, k in st.mats:
+        b = gemv_bytes(st.variant, cfg.draft_m, n, k, 4 if name == "lm_head" else 2)
+        sizes.append(max(16, int(b) // 16 * 16))
+    cycles_per_ms = spin_cycles_per_ms()
+    tot_s, tot_b, launches, off = 0.0, 0.0, 0, 0
+    for _ in range(steps):
+        torch.cuda.synchronize()
+        torch.cuda._sleep(int(40 * cycles_per_ms))  # queue every launch before the GPU reaches the first
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for b in sizes:
+            if off + b > big_bytes:
+                off = 0
+            sq_probe_stream_read(buf, b, off, sink=sink)
+            off += (b + 4095) // 4096 * 4096
+        e1.record()
+        torch.cuda.synchronize()
+        tot_s += e0.elapsed_time(e1) * 1e-3
+        tot_b += sum(sizes)
+        launches += len(sizes)
+    del buf
+    return {
+        "kernel": "sq_probe_stream_read (plain 16-byte streaming read)",
+        "peak_gbs": round(peak, 1),
+        "peak_bytes": big_bytes,
+        "same_launches_gbs": round(tot_b / tot_s / 1e9, 1),
+        "same_launches_avg_us": round(tot_s / launches * 1e6, 3),
+    }
 
 
 def traffic_from_profile(variant: str):
@@ -281,14 +345,19 @@ def main():
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps - 1)]
     t0 = time.perf_counter()
     e0.record()
-    for r in range(args.warmup, total):
+    for i, r in enumerate(range(args.warmup, total)):
+        if i:
+            marks[i - 1].record()
         one(r)
     e1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     elapsed = e0.elapsed_time(e1) * 1e-3
+    edges = [e0, *marks, e1]
+    round_ms = np.array([edges[i].elapsed_time(edges[i + 1]) for i in range(args.steps)])
     n_acc = n_hist[args.warmup:].cpu().numpy().astype(np.int64)
     tokens = int((n_acc + 1).sum())
     tokens_per_round = tokens / (args.steps * cfg.batch)
@@ -297,6 +366,7 @@ def main():
     gbytes, gsec, glaunch = measure_gemv(rnd, args.gemv_steps)
     achieved = gbytes / gsec / 1e9
     traffic = traffic_from_profile(stack.variant)
+    probe = measure_probe(rnd, args.gemv_steps)
 
     out = {
         "metric": METRIC,
@@ -323,6 +393,9 @@ def main():
             "graph": True,
         },
         "rounds_per_s": round(args.steps / elapsed, 3),
+        "round_ms": {"median": round(float(np.median(round_ms)), 4),
+                     "p10": round(float(np.percentile(round_ms, 10)), 4),
+                     "p90": round(float(np.percentile(round_ms, 90)), 4)},
         "tokens_per_round": round(tokens_per_round, 4),
         "acceptance_rate": round(float(n_acc.sum()) / (args.steps * cfg.batch * cfg.k), 4),
         "round_bytes": cfg.round_bytes(),
@@ -341,6 +414,10 @@ def main():
             "launches_timed": glaunch,
             "avg_launch_us": round(gsec / glaunch * 1e6, 3),
             "algorithmic_bytes_per_launch": round(gbytes / glaunch, 1),
+            "measured_peak": probe["peak_gbs"],
+            "frac_of_measured_peak": round(achieved / probe["peak_gbs"], 4),
+            "probe": probe,
+            "frac_of_probe_same_launches": round(achieved / probe["same_launches_gbs"], 4),
         },
     }
     if not args.no_cpu_baseline:

@@ -150,6 +150,18 @@ sq_status sq_spec_accept(const float* draft_logits, const float* target_logits,
                          int32_t v, float temperature, int32_t* n_accepted, int32_t* next_token,
                          float* q_out, float* p_out, hipStream_t stream);
 
+/* Streaming-read probe (a measurement aid beside the method, not one of its
+ * steps): reads `bytes` bytes of src once with 16-byte loads in grid-stride
+ * order and nothing else, so that the duration of the call on the stream is a
+ * plain read of that many bytes: the measured ceiling that the HBM-bound GEMVs
+ * are compared against.
+ * src   device memory, 16-B aligned; bytes a multiple of 16, 16 <= bytes <= 2^40
+ * sink  [SQ_PROBE_SINK_WORDS] uint32 device out: word j is the XOR of the
+ *       32-bit words workgroup j read, so the XOR of all the sink words is the
+ *       XOR of every 32-bit word of src.  Must not overlap src. */
+#define SQ_PROBE_SINK_WORDS 2048
+sq_status sq_probe_stream_read(const void* src, int64_t bytes, uint32_t* sink, hipStream_t stream);
+
 /* Human-readable name of a status code (static storage). */
 const char* sq_status_str(sq_status status);
 

@@ -17,6 +17,7 @@ from ._lib import (  # noqa: F401
     sq_qgemv_w8a16,
     sq_quantize_fp8_e4m3,
     sq_quantize_int4_g128,
+    sq_probe_stream_read,
     sq_spec_accept,
     sq_verify_gemm_f16,
 )

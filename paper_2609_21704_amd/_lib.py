@@ -52,6 +52,7 @@ def load() -> ctypes.CDLL:
             "sq_qgemv_w8a16": ([P, I64, I64, P, P, I64, P, S, P], S),
             "sq_verify_gemm_f16": ([P, I64, I64, P, I64, P, S, P], S),
             "sq_spec_accept": ([P, P, P, P, I32, I32, I32, F, P, P, P, P, P], S),
+            "sq_probe_stream_read": ([P, I64, P, P], S),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(lib, name)
@@ -62,7 +63,8 @@ def load() -> ctypes.CDLL:
 
 
 EXPORTED = ("sq_abi_version", "sq_status_str", "sq_quantize_int4_g128", "sq_quantize_fp8_e4m3",
-            "sq_qgemv_w4a16", "sq_qgemv_w8a16", "sq_verify_gemm_f16", "sq_spec_accept")
+            "sq_qgemv_w4a16", "sq_qgemv_w8a16", "sq_verify_gemm_f16", "sq_spec_accept",
+            "sq_probe_stream_read")
 
 
 def _ptr(t):
@@ -230,3 +232,24 @@ def sq_spec_accept(draft_logits, target_logits, draft_tokens, u24, temperature: 
                                  float(temperature), _ptr(n_accepted), _ptr(next_token), _ptr(q_out), _ptr(p_out),
                                  _stream(dev)), "sq_spec_accept")
     return n_accepted, next_token
+
+
+PROBE_SINK_WORDS = 2048  # SQ_PROBE_SINK_WORDS
+
+
+def sq_probe_stream_read(src: torch.Tensor, nbytes: int | None = None, offset: int = 0, sink=None):
+    """Streaming-read probe (a measurement aid, not a step of the method): one
+    plain read of `nbytes` bytes of the GPU tensor `src` from byte `offset` on
+    (default: all of it).  Returns the sink, uint32 words held in an int32
+    tensor [PROBE_SINK_WORDS] whose XOR is the XOR of the 32-bit words read."""
+    dev = src.device
+    total = src.numel() * src.element_size()
+    nbytes = total - offset if nbytes is None else nbytes
+    if offset < 0 or nbytes < 0 or offset + nbytes > total:
+        raise ValueError("byte range outside src")
+    sink = torch.empty((PROBE_SINK_WORDS,), dtype=torch.int32, device=dev) if sink is None else sink
+    _dev(src, sink)
+    _expect(sink, torch.int32, (PROBE_SINK_WORDS,), "sink")
+    _check(load().sq_probe_stream_read(src.data_ptr() + offset, nbytes, sink.data_ptr(), _stream(dev)),
+           "sq_probe_stream_read")
+    return sink

@@ -271,6 +271,17 @@ sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint
   return device_status(e);
 }
 
+sq_status sq_probe_stream_read(const void* src, int64_t bytes, uint32_t* sink, hipStream_t stream) {
+  if (!src || !sink) return SQ_ERR_NULL;
+  if (bytes < 16 || bytes > (int64_t(1) << 40) || bytes % 16 != 0) return SQ_ERR_SHAPE;
+  if (!aligned(src, 16) || !aligned(sink, 4)) return SQ_ERR_ALIGN;
+  const Range outs[] = {{sink, (size_t)SQ_PROBE_SINK_WORDS * 4}};
+  const Range ins[] = {{src, (size_t)bytes}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_stream_read(src, bytes, sink, SQ_PROBE_SINK_WORDS, stream));
+}
+
 sq_status sq_spec_accept(const float* draft_logits, const float* target_logits, const int32_t* draft_tokens,
                          const uint32_t* u24, int32_t b, int32_t kd, int32_t v, float temperature,
                          int32_t* n_accepted, int32_t* next_token, float* q_out, float* p_out, hipStream_t stream) {

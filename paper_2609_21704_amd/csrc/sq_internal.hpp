@@ -54,6 +54,10 @@ hipError_t launch_linear_f16(const uint16_t* x, int m, int64_t k, const uint16_t
 hipError_t launch_splitk_reduce(const float* partial, int splits, int64_t mn, void* y, bool f16_out,
                                 hipStream_t stream);
 
+// The streaming-read probe: `blocks` workgroups read bytes / 16 cells of src
+// and write one XOR word each to sink[0 .. blocks).
+hipError_t launch_stream_read(const void* src, int64_t bytes, uint32_t* sink, int blocks, hipStream_t stream);
+
 hipError_t launch_spec_accept(const float* draft, const float* target, const int32_t* tokens, const uint32_t* u24,
                               int b, int kd, int v, float temperature, int32_t* n_accepted, int32_t* next_token,
                               float* q_out, float* p_out, hipStream_t stream);

@@ -30,7 +30,8 @@ def test_library_exports_every_declared_symbol():
     lib = sq.load()
     names = declared_symbols()
     assert set(names) == {"sq_abi_version", "sq_status_str", "sq_quantize_int4_g128", "sq_quantize_fp8_e4m3",
-                          "sq_qgemv_w4a16", "sq_qgemv_w8a16", "sq_verify_gemm_f16", "sq_spec_accept"}
+                          "sq_qgemv_w4a16", "sq_qgemv_w8a16", "sq_verify_gemm_f16", "sq_spec_accept",
+                          "sq_probe_stream_read"}
     for n in names:
         assert hasattr(lib, n), n
     assert sq.sq_abi_version() == 1
@@ -96,6 +97,19 @@ def test_accept_validation():
     assert acc(A, B, C, D, 1, 4, 100, 1.0, E + 2, E + 64, None, None, None) == ALIGN
     assert acc(A, B, C, D, 1, 4, 100, 1.0, E, E, None, None, None) == ALIAS
     assert acc(A, B, C, D, 1, 4, 100, 1.0, E, E + 64, None, B + 40, None) == ALIAS
+
+
+def test_probe_validation():
+    probe = sq.load().sq_probe_stream_read
+    assert probe(None, 1024, B, None) == NULL
+    assert probe(A, 1024, None, None) == NULL
+    assert probe(A, 0, B, None) == SHAPE
+    assert probe(A, 1000, B, None) == SHAPE          # not a multiple of 16
+    assert probe(A, (1 << 40) + 16, B, None) == SHAPE
+    assert probe(A + 8, 1024, B, None) == ALIGN
+    assert probe(A, 1024, B + 2, None) == ALIGN
+    assert probe(A, 1024, A + 512, None) == ALIAS    # sink inside src
+    assert probe(A + 8176, 1024, A, None) == ALIAS   # src starts inside the 8 KiB sink
 
 
 def test_binding_fails_loudly_without_gpu_tensors():
