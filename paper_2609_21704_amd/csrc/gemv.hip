@@ -22,8 +22,8 @@
 //   gemv_rows_kernel (row blocks, INT4, m <= 2): each CU's workgroups own a
 //     contiguous block of rows, walked by their wavefronts in runs of whole
 //     64-piece steps; it takes the launches where a task would be one row or
-//     would leave lanes idle (q|k|v, o and down at 7B).  Described at the
-//     kernel.
+//     would leave lanes idle (q|k|v, o and down at 7B; every matrix with
+//     rows of 1024 .. 1920 k, as at 1.5B).  Described at the kernel.
 //
 // INT4 (W4A16).  A lane's 32 bytes are 64 consecutive 4-bit codes of one row,
 // i.e. half of one 128-element group.  Each 32-bit word (codes of k..k+7) is
@@ -414,7 +414,7 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
   }
 }
 
-// INT4 GEMV over row blocks (k >= 2048, m <= 2).  A workgroup of NWV
+// INT4 GEMV over row blocks (k >= 1024, m <= 2).  A workgroup of NWV
 // wavefronts (16 per CU in all) owns a contiguous block of rows, whose codes
 // are one contiguous byte range of 32-byte pieces (64 codes, half a group).
 // A wavefront walks a run of it in steps of 64 consecutive pieces.  The runs
@@ -423,10 +423,11 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
 // of equal bytes, whose last step often held a few pieces, were up to 1.3 us
 // slower on the 7B down projection).  D steps of loads are in flight (the
 // host takes D = 1: with 16 wavefronts of a CU streaming, every deeper
-// prefetch measured slower).  A row holds at least 32 pieces, so a step meets
-// at most NA rows (three, or two from 64 pieces a row on): each lane adds its
-// piece into the sum of its row, and when the walk leaves a row the wavefront
-// reduces that row's sum into an LDS slot [wavefront][row].  After one
+// prefetch measured slower).  A row holds at least 16 pieces, so a step meets
+// at most NA rows (five for 16 .. 21 pieces a row, four to 31, three to 63,
+// two from 64 on): each lane adds its piece into the sum of its row, and when
+// the walk leaves a row the wavefront reduces that row's sum into an LDS slot
+// [wavefront][row].  After one
 // barrier each row is the sum of its NWV slots in wavefront order
 // (deterministic).  Activations are staged in LDS chunk-major with one pad
 // cell per 64-element chunk (a 144-byte stride), so a lane reads its eight
@@ -578,14 +579,12 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
   auto compute = [&](const PieceFrag& f) {
     // the lane's row is crow + rel: a step of 64 pieces meets at most NA rows
     int chunk = coff + lane, rel = 0;
-    if (chunk >= ppr) {
-      chunk -= ppr;
-      rel = 1;
-    }
-    if (NA > 2 && chunk >= ppr) {
-      chunk -= ppr;
-      rel = 2;
-    }
+#pragma unroll
+    for (int i = 1; i < NA; ++i)
+      if (chunk >= ppr) {
+        chunk -= ppr;
+        rel = i;
+      }
     const bool ok = cb + lane < pe;
     if constexpr (W8) {
       float a[M];
@@ -746,7 +745,7 @@ hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits,
 }
 
 #ifndef SQ_GEMV_ROWS_MIN_K
-#define SQ_GEMV_ROWS_MIN_K 2048  // shortest rows the row-block INT4 kernel takes
+#define SQ_GEMV_ROWS_MIN_K 1024  // shortest rows the row-block INT4 kernel takes
 #endif
 #ifndef SQ_GEMV_ROWS_DEPTH
 #define SQ_GEMV_ROWS_DEPTH 1     // steps of loads in flight per wavefront (measured: 1 < 2 < 3 < 4 in time)
@@ -765,7 +764,7 @@ hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const
                        const uint16_t* zeros16, const float* scales32, int64_t n, void* y, bool f16_out,
                        hipStream_t stream) {
   // whole pieces per row: 32 FP8 codes, or 64 INT4 codes (k % 128 == 0 already)
-  if (M > (W8 ? 4 : 2) || k < (W8 ? 1024 : SQ_GEMV_ROWS_MIN_K) || k < (W8 ? 1024 : 2048) || (W8 && k % 32 != 0))
+  if (M > (W8 ? 4 : 2) || k < (W8 ? 1024 : SQ_GEMV_ROWS_MIN_K) || k < 1024 || (W8 && k % 32 != 0))
     return hipErrorNotSupported;
   // 16 wavefronts per CU: one workgroup of 16, or two of 8 for INT4 rows of
   // 8192 k and more (measured: 7B down 13.5 -> 12.8 us, q|k|v 5.8 -> 6.0 us)
@@ -805,6 +804,10 @@ hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const
   };
   if (nwave == 8)  // INT4, k >= 8192: two rows per step at most
     pick(IntC<2>{}, IntC<8>{});
+  else if (ppr < 22)  // rows of 16 .. 21 pieces: up to five rows
+    pick(IntC<5>{}, IntC<16>{});
+  else if (ppr < 32)  // rows of 22 .. 31 pieces: up to four rows
+    pick(IntC<4>{}, IntC<16>{});
   else if (ppr < 64)  // rows of 32 .. 63 pieces: a step meets up to three rows
     pick(IntC<3>{}, IntC<16>{});
   else
