@@ -246,10 +246,26 @@ def cpu_baseline(rnd, tokens_per_round: float):
                + cfg.layers * t_layer_verify + t_lm_verify + t_accept)
     measured = (len(layers) * t_layer_draft + t_lm_draft + t_sample
                 + len(layers) * t_layer_verify + t_lm_verify + t_accept)
+    # one layer's draft GEMVs (one draft step) on one thread
+    threads = oracle.num_threads()
+    oracle.set_num_threads(1)
+    t0 = time.perf_counter()
+    for name, _, _ in cfg.layer_matrices():
+        gemv((layers[0], name), xd[(0, layers[0], name)])
+    t_single = time.perf_counter() - t0
+    oracle.set_num_threads(threads)
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), None)
+    except OSError:
+        pass
     return {
         "value": round(tokens_per_round * cfg.batch / round_s, 4),
         "unit": "tokens/s",
-        "cores": oracle.num_threads(),
+        "cores": threads,
+        "cpu_model": cpu_model,
+        "single_thread_layer_draft_s": round(t_single, 3),
         "kind": "oracle",
         "sample": (f"layers {layers} of {cfg.layers} (4 projections each) and the LM head: one round of their "
                    f"draft GEMVs, draws, verify GEMMs and the accept step, timed in {measured:.1f} s and "

@@ -51,6 +51,7 @@ def _load():
     D = ctypes.c_double
     sigs = {
         "sqo_num_threads": ([], ctypes.c_int),
+        "sqo_set_num_threads": ([ctypes.c_int], None),
         "sqo_f16_to_f64": ([ctypes.c_uint16], D),
         "sqo_f16_round_up": ([D], D),
         "sqo_fp8_e4m3_decode": ([ctypes.c_uint8], D),
@@ -99,6 +100,11 @@ class OracleError(RuntimeError):
 
 def num_threads() -> int:
     return int(_load().sqo_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of later oracle calls (timing only: the results do not depend on it)."""
+    _load().sqo_set_num_threads(int(n))
 
 
 # ------------------------------------------------------------ scalar helpers

@@ -53,6 +53,17 @@ int sqo_num_threads(void) {
 #endif
 }
 
+/* Threads of the following calls (OpenMP over output rows); n >= 1.  Only
+   the timing of the oracle changes: every output is one thread's fp64 sum in
+   a fixed order whatever the count. */
+void sqo_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* ---------------------------------------------------------------- fp16 ---- */
 
 /* IEEE binary16 bit pattern -> exact double. */

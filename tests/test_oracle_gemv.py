@@ -99,3 +99,20 @@ def test_normalised_error_metric():
     d_ref = np.array([[2.0, 0.0]])
     assert abs(oracle.normalised_error(np.array([[1.002, 0.0]]), y_ref, d_ref) - 0.001) < 1e-15
     assert oracle.normalised_error(np.array([[1.0, 1e-30]]), y_ref, d_ref) == float("inf")
+
+
+def test_results_do_not_depend_on_the_thread_count():
+    rng = np.random.default_rng(7)
+    w = _f16(rng.normal(0, 0.02, (300, 512)))
+    x = _f16(rng.normal(0, 1, (3, 512)))
+    c, sc, z = oracle.quantize_int4_g128(w)
+    n = oracle.num_threads()
+    try:
+        oracle.set_num_threads(1)
+        one = (oracle.qgemv_w4a16(x, c, sc, z)[0], oracle.gemm_f16(x, w)[0])
+        oracle.set_num_threads(max(2, n))
+        many = (oracle.qgemv_w4a16(x, c, sc, z)[0], oracle.gemm_f16(x, w)[0])
+    finally:
+        oracle.set_num_threads(n)
+    for a, b in zip(one, many):
+        assert np.array_equal(a, b)
