@@ -152,6 +152,82 @@ def measure_probe(rnd, steps: int, big_bytes: int = 4 << 30):
     }
 
 
+def per_shape(cfg, rot_bytes: int = 3 << 30, iters: int = 40):
+    """Back-to-back launches of each draft GEMV and verify GEMM shape of the
+    workload, each over rotating copies of at least rot_bytes in all (so the
+    memory-side cache cannot serve them), beside the read probe on the same
+    bytes.  Weights are random bytes of the right layout (timing only)."""
+    import torch
+
+    import paper_2609_21704_amd as sq
+
+    dev = torch.device("cuda")
+    cpm = spin_cycles_per_ms()
+    sink = torch.empty(2048, dtype=torch.int32, device=dev)
+
+    def b2b(fn, copies):
+        for i in range(3):
+            fn(i % copies)
+        torch.cuda.synchronize()
+        torch.cuda._sleep(int(20 * cpm))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(iters):
+            fn(i % copies)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / iters
+
+    shapes = [(name, n, k) for name, n, k in cfg.layer_matrices()]
+    if cfg.lm_head:
+        shapes.append(("lm_head", cfg.vocab, cfg.hidden))
+    rows = []
+    for name, n, k in shapes:
+        m = cfg.draft_m
+        if cfg.draft_variant == "int4":
+            per = n * k // 2 + n * (k // 128) * 4
+            copies = max(2, rot_bytes // per)
+            codes = [torch.randint(0, 256, (n, k // 2), dtype=torch.uint8, device=dev) for _ in range(copies)]
+            sc = [torch.full((n, k // 128), 0.01, dtype=torch.float16, device=dev) for _ in range(copies)]
+            zz = [torch.full((n, k // 128), 8.0, dtype=torch.float16, device=dev) for _ in range(copies)]
+            x = torch.randn((m, k), device=dev).half()
+            y = torch.empty((m, n), device=dev, dtype=torch.float16)
+            t_d = b2b(lambda i: sq.sq_qgemv_w4a16(x, codes[i], sc[i], zz[i], y=y), copies)
+            b_d = gemv_bytes("int4", m, n, k, 2)
+            del codes, sc, zz
+        else:
+            per = n * k + 4 * n
+            copies = max(2, rot_bytes // per)
+            codes = [torch.randint(0, 126, (n, k), dtype=torch.uint8, device=dev) for _ in range(copies)]
+            sc = [torch.full((n,), 0.001, dtype=torch.float32, device=dev) for _ in range(copies)]
+            x = torch.randn((m, k), device=dev).half()
+            y = torch.empty((m, n), device=dev, dtype=torch.float16)
+            t_d = b2b(lambda i: sq.sq_qgemv_w8a16(x, codes[i], sc[i], y=y), copies)
+            b_d = gemv_bytes("fp8", m, n, k, 2)
+            del codes, sc
+        mv = cfg.verify_m
+        copies = max(2, rot_bytes // (2 * n * k))
+        w = [torch.empty((n, k), device=dev, dtype=torch.float16).normal_(0, 0.02) for _ in range(copies)]
+        xv = torch.randn((mv, k), device=dev).half()
+        yv = torch.empty((mv, n), device=dev, dtype=torch.float16)
+        t_v = b2b(lambda i: sq.sq_verify_gemm_f16(xv, w[i], y=yv), copies)
+        b_v = 2 * n * k + 2 * mv * k + 2 * mv * n
+        del w
+        buf = torch.zeros(rot_bytes, dtype=torch.uint8, device=dev)
+        probe = {}
+        for key, nb in (("draft", int(b_d) // 16 * 16), ("verify", int(b_v) // 16 * 16)):
+            slots = max(2, rot_bytes // ((nb + 4095) // 4096 * 4096))
+            step = (nb + 4095) // 4096 * 4096
+            probe[key] = b2b(lambda i: sq.sq_probe_stream_read(buf, nb, (i % slots) * step, sink=sink), slots)
+        del buf
+        rows.append({"matrix": name, "n": n, "k": k,
+                     "draft": {"m": m, "us": round(t_d, 2), "gbs": round(b_d / t_d / 1e3, 1),
+                               "probe_us": round(probe["draft"], 2)},
+                     "verify": {"m": mv, "us": round(t_v, 2), "gbs": round(b_v / t_v / 1e3, 1),
+                                "probe_us": round(probe["verify"], 2)}})
+    return rows
+
+
 def traffic_from_profile(variant: str):
     """HBM bytes per draft-GEMV launch from the committed rocprofv3 counter
     summary, if it was taken on the current kernel source; else None."""
@@ -314,6 +390,9 @@ def main():
     ap.add_argument("--temperature", type=float, default=1.0)
     ap.add_argument("--gemv-steps", type=int, default=2, help="draft passes timed per launch for the roofline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--per-shape", action="store_true",
+                    help="instead of rounds: back-to-back launches of each draft GEMV and verify GEMM shape of "
+                         "the workload, beside plain reads of the same bytes; one JSON line")
     ap.add_argument("--profile-only", action="store_true",
                     help="for rocprofv3 counter runs: one eager round, then a plain copy of COPY_BYTES bytes "
                          "(the counter calibration); prints nothing")
@@ -333,6 +412,9 @@ def main():
     cfg = CONFIGS[args.config]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.per_shape:
+        print(json.dumps({"workload": cfg.describe(), "per_shape": per_shape(cfg)}), flush=True)
+        return
     stack = Stack(cfg, dev)
     rnd = Round(stack, temperature=args.temperature)
     if args.profile_only:
