@@ -162,6 +162,18 @@ def test_qgemv_w4a16_long_rows(m, n, k):
     test_qgemv_w4a16_parity(m, n, k)
 
 
+# Short rows on the row-block kernel: 16 .. 30 pieces a row, so that a step of
+# 64 pieces meets up to five rows (1024 .. 1280 k) or four (1408 .. 1920 k);
+# ragged row counts, blocks of one row up to hundreds of rows.
+SHORT_W4 = [(1, 4097, 1024), (2, 777, 1024), (1, 300, 1152), (2, 20011, 1280), (1, 2048, 1536), (2, 1536, 1536),
+            (1, 151936, 1536), (1, 5003, 1408), (2, 257, 1920), (1, 33333, 1792)]
+
+
+@pytest.mark.parametrize("m,n,k", SHORT_W4)
+def test_qgemv_w4a16_short_rows(m, n, k):
+    test_qgemv_w4a16_parity(m, n, k)
+
+
 # Shapes past the matrix-core kernel's size threshold that it cannot take:
 # with many tiles per workgroup its chunk partial sums would not fit in LDS
 # (m = 16 verify, m = 8 FP8 draft), so the call takes the other kernel.
