@@ -399,8 +399,9 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only: every box here has a single MI355X, and the SpecQuant hot path "
-              f"is built and timed on one GPU (requested --gpus {args.gpus}).", file=sys.stderr)
+        print(f"bench.py measures one GPU only: the SpecQuant hot path is built and timed on a single MI355X; "
+              f"its sharding over several GPUs is a design, not code (requested --gpus {args.gpus}).",
+              file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
