@@ -65,6 +65,7 @@ def _load():
         "sqo_gemm_f16": ([P, I64, I64, P, I64, P, P], ctypes.c_int),
         "sqo_softmax": ([P, I64, I64, D, P], ctypes.c_int),
         "sqo_spec_accept": ([P, P, P, P, I32, I32, I32, D, P, P, P, P], ctypes.c_int),
+        "sqo_accept_probs": ([P, P, P, P, I32, I32, I32, P, P], ctypes.c_int),
     }
     for name, (args, res) in sigs.items():
         fn = getattr(lib, name)
@@ -220,7 +221,10 @@ def spec_accept(draft_logits, target_logits, draft_tokens, u24, temperature: flo
 
     draft_logits [kd][b][v] f32, target_logits [b][kd+1][v] f32,
     draft_tokens [kd][b] i32, u24 [b][kd+1] u32 (low 24 bits used).
-    Returns (n_accepted [b], next_token [b], q [kd][b][v] | None, p [b][kd+1][v] | None).
+    Returns (n_accepted [b], next_token [b], q [kd][b][v] | None, p [b][kd+1][v] | None);
+    q and p are the fp64 distributions (the decisions use their fp32 roundings).
+    A sequence with a row that has no distribution (a NaN or +inf logit, or no
+    finite logit) gets n_accepted = next_token = -1.
     """
     target_logits = np.ascontiguousarray(target_logits, np.float32)
     b, kd1, v = target_logits.shape
@@ -240,6 +244,27 @@ def spec_accept(draft_logits, target_logits, draft_tokens, u24, temperature: flo
                                    b, kd, v, float(temperature), _ptr(n_acc), _ptr(nxt), _ptr(q), _ptr(p)),
            "spec_accept")
     return n_acc, nxt, q, p
+
+
+def accept_probs(p, q, draft_tokens, u24):
+    """The decisions and draws of spec_accept (T > 0) from given fp32
+    distributions: p [b][kd+1][v] f32, q [kd][b][v] f32 (None when kd = 0),
+    draft_tokens [kd][b] i32, u24 [b][kd+1] u32.  Returns (n_accepted [b],
+    next_token [b])."""
+    p = np.ascontiguousarray(p, np.float32)
+    b, kd1, v = p.shape
+    kd = kd1 - 1
+    if kd > 0:
+        q = np.ascontiguousarray(q, np.float32).reshape(kd, b, v)
+        draft_tokens = np.ascontiguousarray(draft_tokens, np.int32).reshape(kd, b)
+    else:
+        q = draft_tokens = None
+    u24 = np.ascontiguousarray(u24, np.uint32).reshape(b, kd + 1)
+    n_acc = np.zeros(b, np.int32)
+    nxt = np.zeros(b, np.int32)
+    _check(_load().sqo_accept_probs(_ptr(p), _ptr(q), _ptr(draft_tokens), _ptr(u24), b, kd, v, _ptr(n_acc),
+                                    _ptr(nxt)), "accept_probs")
+    return n_acc, nxt
 
 
 def normalised_error(y_test, y_ref, d_ref) -> float:

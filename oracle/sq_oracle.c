@@ -28,7 +28,12 @@
  *                              u * q(x) < p(x), residual max(0, p - q)
  *                              renormalised at the first rejection, a bonus
  *                              draw from p when every draft is accepted; the
- *                              greedy "parent agrees" rule at T = 0.
+ *                              greedy "parent agrees" rule at T = 0.  The
+ *                              distributions are computed in fp64 and held in
+ *                              fp32, the precision the call hands back; the
+ *                              decisions and draws use those fp32 values.
+ *   sqo_accept_probs        -- the same decisions and draws taken directly from
+ *                              given fp32 distributions.
  *
  * Every floating-point step is fp64 with IEEE division and round-to-nearest-
  * even, compiled without contraction (-ffp-contract=off).  Parallelism is an
@@ -335,8 +340,21 @@ int sqo_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint16_t* w, int
 
 /* ------------------------------------------------------------- softmax --- */
 
-/* One row: p_j = exp(z_j - L) / sum_i exp(z_i - L), z = l / T, L = max z. */
-static void softmax_row(const float* l, int64_t v, double temp, double* p) {
+/* One row: p_j = exp(z_j - L) / sum_i exp(z_i - L), z = l / T, L = max z.
+ * A logit of -inf is a masked token: z = -inf, p = 0.  A row that holds a NaN
+ * or +inf logit, or no finite logit at all, has no distribution: the function
+ * returns 0 and sets every p_j to NaN.  Returns 1 for a valid row.  (For a
+ * finite fp32 logit and a finite fp32 T > 0, |z| < 2^280, so z is finite.) */
+static int softmax_row(const float* l, int64_t v, double temp, double* p) {
+  int finite = 0;
+  for (int64_t j = 0; j < v; ++j) {
+    if (isnan(l[j]) || l[j] == INFINITY) finite = -1;
+    if (finite == 0 && isfinite(l[j])) finite = 1;
+  }
+  if (finite != 1) {
+    for (int64_t j = 0; j < v; ++j) p[j] = NAN;
+    return 0;
+  }
   double L = -INFINITY;
   for (int64_t j = 0; j < v; ++j) {
     double z = (double)l[j] / temp;
@@ -345,6 +363,7 @@ static void softmax_row(const float* l, int64_t v, double temp, double* p) {
   double sum = 0.0;
   for (int64_t j = 0; j < v; ++j) sum += exp((double)l[j] / temp - L);
   for (int64_t j = 0; j < v; ++j) p[j] = exp((double)l[j] / temp - L) / sum;
+  return 1;
 }
 
 int sqo_softmax(const float* logits, int64_t rows, int64_t v, double temperature, double* p) {
@@ -358,10 +377,15 @@ int sqo_softmax(const float* logits, int64_t rows, int64_t v, double temperature
 
 /* ------------------------------------------------------ accept / resample --- */
 
+/* Greedy target of a row: the index of its largest logit, the smallest index
+ * on ties.  A row holding a NaN or +inf logit, or no finite logit, has none:
+ * returns -1. */
 static int64_t argmax_row(const float* l, int64_t v) {
-  int64_t best = 0;
-  for (int64_t j = 1; j < v; ++j)
-    if (l[j] > l[best]) best = j;   /* strict: ties keep the smallest index */
+  int64_t best = -1;
+  for (int64_t j = 0; j < v; ++j) {
+    if (isnan(l[j]) || l[j] == INFINITY) return -1;
+    if (isfinite(l[j]) && (best < 0 || l[j] > l[best])) best = j; /* strict: ties keep the smallest */
+  }
   return best;
 }
 
@@ -393,19 +417,95 @@ static int64_t draw_fixed_point(const double* r, int64_t v, uint32_t u24) {
   return tok;
 }
 
+/* Acceptance or correction of one sequence from its distributions held in
+ * fp32 (SS III-D.4; the standard speculative-sampling rule):
+ *   p[i] (i = 0..kd) the parent's rows, q[i] (i < kd) the draft's rows, each
+ *   v probabilities; x[i * xs] the drafted token of position i; u[i] the
+ *   24-bit uniforms, u[kd] driving the final draw.
+ * Position i is accepted iff u_i * q_i(x_i) < p_i(x_i) with u_i = u[i] / 2^24,
+ * formed in fp64 from the fp32 values (a 24-bit u times a 24-bit q is exact);
+ * a token outside [0, v) is rejected.  n = the first rejection (kd if none).
+ * At a rejection the token is drawn from max(0, p_n - q_n), each difference
+ * formed in fp64 from the fp32 values, and from p_n itself when that mass is
+ * zero on the grid; when all kd are accepted the bonus token is drawn from
+ * p_kd.  A row holding a NaN makes the sequence invalid: n = token = -1. */
+static void accept_from_rows(const float* const* p, const float* const* q, const int32_t* x, int64_t xs,
+                             const uint32_t* u, int32_t kd, int64_t v, int32_t* n_out, int32_t* tok_out) {
+  for (int32_t i = 0; i <= kd; ++i)
+    for (int64_t j = 0; j < v; ++j)
+      if (isnan(p[i][j]) || (i < kd && isnan(q[i][j]))) {
+        *n_out = -1;
+        *tok_out = -1;
+        return;
+      }
+  int32_t n = kd;
+  for (int32_t i = 0; i < kd; ++i) {
+    int32_t xi = x[(int64_t)i * xs];
+    double ui = ldexp((double)(u[i] & 0xFFFFFFu), -24);
+    int accept = 0;
+    if (xi >= 0 && xi < v) accept = (ui * (double)q[i][xi] < (double)p[i][xi]);
+    if (!accept) {
+      n = i;
+      break;
+    }
+  }
+  double* r = (double*)calloc((size_t)v, sizeof(double));
+  int64_t tok;
+  if (n < kd) {
+    for (int64_t j = 0; j < v; ++j) {
+      double diff = (double)p[n][j] - (double)q[n][j];
+      r[j] = diff > 0.0 ? diff : 0.0;
+    }
+    tok = draw_fixed_point(r, v, u[kd]);
+    if (tok < 0) { /* no residual mass on the grid: draw from p_n */
+      for (int64_t j = 0; j < v; ++j) r[j] = (double)p[n][j];
+      tok = draw_fixed_point(r, v, u[kd]);
+    }
+  } else {
+    for (int64_t j = 0; j < v; ++j) r[j] = (double)p[kd][j];
+    tok = draw_fixed_point(r, v, u[kd]);
+  }
+  free(r);
+  *n_out = n;
+  *tok_out = (int32_t)tok;
+}
+
+/* The decisions and draws of sqo_spec_accept (T > 0) taken directly from fp32
+ * distributions in the call's own layouts: p [b][kd+1][v], q [kd][b][v],
+ * draft_tokens [kd][b], u24 [b][kd+1].  Each row is a distribution (its
+ * values sum to at most 1 + 2^-20). */
+int sqo_accept_probs(const float* p, const float* q, const int32_t* draft_tokens, const uint32_t* u24, int32_t b,
+                     int32_t kd, int32_t v, int32_t* n_accepted, int32_t* next_token) {
+  if (!p || !u24 || !n_accepted || !next_token) return SQO_ERR_NULL;
+  if (kd > 0 && (!q || !draft_tokens)) return SQO_ERR_NULL;
+  if (b < 1 || kd < 0 || v < 1) return SQO_ERR_SHAPE;
+#pragma omp parallel for schedule(static)
+  for (int32_t s = 0; s < b; ++s) {
+    const float** prow = (const float**)malloc((size_t)(kd + 1) * sizeof(float*));
+    const float** qrow = (const float**)malloc((size_t)(kd > 0 ? kd : 1) * sizeof(float*));
+    for (int32_t i = 0; i <= kd; ++i) prow[i] = p + ((int64_t)s * (kd + 1) + i) * v;
+    for (int32_t i = 0; i < kd; ++i) qrow[i] = q + ((int64_t)i * b + s) * v;
+    accept_from_rows(prow, qrow, draft_tokens ? draft_tokens + s : NULL, b, u24 + (int64_t)s * (kd + 1), kd, v,
+                     n_accepted + s, next_token + s);
+    free(prow);
+    free(qrow);
+  }
+  return SQO_OK;
+}
+
 /* Speculative acceptance for b sequences with kd drafted tokens each.
  *   draft_logits  [kd][b][v]    (position-major: one draft step for all b)
  *   target_logits [b][kd+1][v]  (sequence-major: the parent's verify rows)
- *   draft_tokens  [kd][b] (position-major), u24 [b][kd+1] (low 24 bits used;
- *   u = u24 / 2^24)
- * T > 0: accept position i iff u_i * q_i(x_i) < p_i(x_i); n = first rejection
- * (kd if none); at a rejection draw from max(0, p_n - q_n) renormalised (p_n
- * if that mass rounds to zero), otherwise draw the bonus token from p_kd; the
- * draw uses u24[b][kd].  A draft token outside [0, v) is rejected.
+ *   draft_tokens  [kd][b] (position-major), u24 [b][kd+1] (low 24 bits used)
+ * T > 0: p_i = softmax(target_i / T) and q_i = softmax(draft_i / T) in fp64,
+ * each rounded once to fp32; then the rule of accept_from_rows on those fp32
+ * values.  A row with no distribution (softmax_row) makes its sequence
+ * invalid: n = token = -1.
  * T = 0: accept iff x_i == argmax p_i (smallest index on ties); the emitted
- * token is argmax of the first disagreeing row, or of row kd.
+ * token is argmax of the first disagreeing row, or of row kd; a target row
+ * without a greedy target (argmax_row) makes the sequence invalid.
  * q_out [kd][b][v] and p_out [b][kd+1][v] (optional, T > 0 only) receive the
- * fp64 distributions. */
+ * fp64 distributions (NaN rows for rows without one). */
 int sqo_spec_accept(const float* draft_logits, const float* target_logits, const int32_t* draft_tokens,
                     const uint32_t* u24, int32_t b, int32_t kd, int32_t v, double temperature,
                     int32_t* n_accepted, int32_t* next_token, double* q_out, double* p_out) {
@@ -420,6 +520,14 @@ int sqo_spec_accept(const float* draft_logits, const float* target_logits, const
   for (int32_t s = 0; s < b; ++s) {
     const float* tgt = target_logits + (int64_t)s * (kd + 1) * v;
     if (temperature == 0.0) {
+      int valid = 1;
+      for (int32_t i = 0; i <= kd; ++i)
+        if (argmax_row(tgt + (int64_t)i * v, v) < 0) valid = 0;
+      if (!valid) {
+        n_accepted[s] = -1;
+        next_token[s] = -1;
+        continue;
+      }
       int32_t n = kd;
       for (int32_t i = 0; i < kd; ++i) {
         int32_t x = draft_tokens[(int64_t)i * b + s];
@@ -432,44 +540,32 @@ int sqo_spec_accept(const float* draft_logits, const float* target_logits, const
       next_token[s] = (int32_t)argmax_row(tgt + (int64_t)n * v, v);
       continue;
     }
+    const int64_t nq = kd > 0 ? kd : 1;
     double* p = (double*)malloc((size_t)(kd + 1) * v * sizeof(double));
-    double* q = (double*)malloc((size_t)(kd > 0 ? kd : 1) * v * sizeof(double));
+    double* q = (double*)malloc((size_t)nq * v * sizeof(double));
+    float* p32 = (float*)malloc((size_t)(kd + 1) * v * sizeof(float));
+    float* q32 = (float*)malloc((size_t)nq * v * sizeof(float));
+    const float** prow = (const float**)malloc((size_t)(kd + 1) * sizeof(float*));
+    const float** qrow = (const float**)malloc((size_t)nq * sizeof(float*));
     for (int32_t i = 0; i <= kd; ++i) softmax_row(tgt + (int64_t)i * v, v, temperature, p + (int64_t)i * v);
     for (int32_t i = 0; i < kd; ++i)
       softmax_row(draft_logits + ((int64_t)i * b + s) * v, v, temperature, q + (int64_t)i * v);
-    int32_t n = kd;
-    for (int32_t i = 0; i < kd; ++i) {
-      int32_t x = draft_tokens[(int64_t)i * b + s];
-      double u = ldexp((double)(u24[(int64_t)s * (kd + 1) + i] & 0xFFFFFFu), -24);
-      int accept = 0;
-      if (x >= 0 && x < v) accept = (u * q[(int64_t)i * v + x] < p[(int64_t)i * v + x]);
-      if (!accept) {
-        n = i;
-        break;
-      }
-    }
-    uint32_t ufinal = u24[(int64_t)s * (kd + 1) + kd];
-    int64_t tok;
-    if (n < kd) {
-      double* r = (double*)malloc((size_t)v * sizeof(double));
-      for (int64_t j = 0; j < v; ++j) {
-        double diff = p[(int64_t)n * v + j] - q[(int64_t)n * v + j];
-        r[j] = diff > 0.0 ? diff : 0.0;
-      }
-      tok = draw_fixed_point(r, v, ufinal);
-      if (tok < 0) tok = draw_fixed_point(p + (int64_t)n * v, v, ufinal);
-      free(r);
-    } else {
-      tok = draw_fixed_point(p + (int64_t)kd * v, v, ufinal);
-    }
-    n_accepted[s] = n;
-    next_token[s] = (int32_t)tok;
+    for (int64_t j = 0; j < (kd + 1) * (int64_t)v; ++j) p32[j] = (float)p[j];
+    for (int64_t j = 0; j < kd * (int64_t)v; ++j) q32[j] = (float)q[j];
+    for (int32_t i = 0; i <= kd; ++i) prow[i] = p32 + (int64_t)i * v;
+    for (int32_t i = 0; i < kd; ++i) qrow[i] = q32 + (int64_t)i * v;
+    accept_from_rows(prow, qrow, kd > 0 ? draft_tokens + s : NULL, b, u24 + (int64_t)s * (kd + 1), kd, v,
+                     n_accepted + s, next_token + s);
     if (p_out) memcpy(p_out + (int64_t)s * (kd + 1) * v, p, (size_t)(kd + 1) * v * sizeof(double));
     if (q_out)
       for (int32_t i = 0; i < kd; ++i)
         memcpy(q_out + ((int64_t)i * b + s) * v, q + (int64_t)i * v, (size_t)v * sizeof(double));
     free(p);
     free(q);
+    free(p32);
+    free(q32);
+    free(prow);
+    free(qrow);
   }
   return SQO_OK;
 }

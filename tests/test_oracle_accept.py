@@ -215,3 +215,163 @@ def test_pq_outputs_and_errors():
         oracle.spec_accept(dl, tl, x, u24, -1.0)
     with pytest.raises(oracle.OracleError):
         oracle.spec_accept(dl, tl, x, u24, 0.0, want_pq=True)
+
+
+# ------------------------------------------- fp32 decisions, fallbacks, masks ---
+from fractions import Fraction  # noqa: E402
+
+
+def _law_of_final_draw(run):
+    """Exact law of the token returned by run(u_final) over all 2^24 uniforms
+    (the draw is monotone in u): P(token = y) for y = 0..v-1."""
+    toks = {}
+    lo = 0
+    while lo < U:
+        t = run(lo)
+        hi = _threshold(lambda u, t=t: u < lo or run(u) <= t)  # first u with a larger token
+        toks[t] = toks.get(t, 0) + (hi - lo)
+        lo = hi
+    return toks
+
+
+def test_decisions_use_the_fp32_distributions_exactly():
+    """The accept threshold over u24 is exactly ceil(2^24 p32(x) / q32(x)) for
+    the fp32 roundings of p and q: checked with exact rational arithmetic."""
+    rng = np.random.default_rng(17)
+    v = 64
+    for trial in range(6):
+        dl = rng.normal(0, 1.5, v).astype(np.float32)
+        tl = np.stack([dl + rng.normal(0, 0.7, v), rng.normal(0, 1, v)]).astype(np.float32)
+        p32 = oracle.softmax(tl[0]).astype(np.float32)[0]
+        q32 = oracle.softmax(dl).astype(np.float32)[0]
+        x = int(np.argmax(q32 - p32)) if trial % 2 == 0 else int(rng.integers(0, v))
+        ratio = Fraction(float(p32[x])) / Fraction(float(q32[x]))
+        expect = U if ratio >= 1 else -(-ratio.numerator * U // ratio.denominator)   # ceil
+        got = _threshold(lambda u: _accept_one(dl, tl, x, u, 0)[0] == 1)
+        assert got == min(expect, U), (trial, got, expect)
+
+
+def test_accept_probs_reproduces_spec_accept_from_its_fp32_distributions():
+    rng = np.random.default_rng(23)
+    b, kd, v = 40, 5, 700
+    dl = rng.normal(0, 2, (kd, b, v)).astype(np.float32)
+    tl = np.concatenate([dl.transpose(1, 0, 2) + rng.normal(0, 0.5, (b, kd, v)).astype(np.float32),
+                         rng.normal(0, 2, (b, 1, v)).astype(np.float32)], axis=1)
+    x = rng.integers(0, v, (kd, b)).astype(np.int32)
+    u24 = rng.integers(0, U, (b, kd + 1), dtype=np.uint32)
+    n, t, q, p = oracle.spec_accept(dl, tl, x, u24, 1.0, want_pq=True)
+    n2, t2 = oracle.accept_probs(p.astype(np.float32), q.astype(np.float32), x, u24)
+    assert np.array_equal(n, n2) and np.array_equal(t, t2)
+    assert len(set(n.tolist())) > 2   # the case exercises several rejection positions
+
+
+def _fallback_rows(v, rng):
+    """A drafted row q0 whose residual max(0, p0 - q0) is positive at one token
+    but below half a step of the 2^-60 grid, and p1 one-hot elsewhere."""
+    p0 = rng.dirichlet(np.ones(v)).astype(np.float32)
+    p0[0] += p0[1] + p0[2]                           # keep the row a distribution
+    p0[1] = np.float32(2.0 ** -70)
+    p0[2] = np.float32(2.0 ** -70 + 2.0 ** -93)      # exact in fp32: 2^-70 (1 + 2^-23)
+    q0 = p0.copy()
+    q0[1], q0[2] = p0[2], p0[1]                      # p0 - q0: -2^-93 at 1, +2^-93 at 2
+    p1 = np.zeros(v, np.float32)
+    p1[v - 1] = 1.0
+    return p0, q0, p1
+
+
+def test_zero_residual_on_the_grid_falls_back_to_p_n():
+    """Rejecting token 1 (u q0(1) >= p0(1) for u = 1 - 2^-24) leaves a residual
+    of 2^-93 at token 2, which is 0 on the 2^-60 grid: the draw falls back to
+    p0 itself.  Its exact law over all 2^24 final uniforms is p0 (not p1, not
+    the invalid token -1)."""
+    rng = np.random.default_rng(29)
+    v = 8
+    p0, q0, p1 = _fallback_rows(v, rng)
+    assert p0[2] - p0[1] == np.float32(2.0 ** -93) and q0[2] < p0[2]
+    p = np.stack([p0, p1])[None]                     # [b=1][kd+1=2][v]
+    q = q0[None, None]                               # [kd=1][b=1][v]
+
+    def run(uf):
+        n, t = oracle.accept_probs(p, q, np.array([[1]], np.int32), np.array([[U - 1, uf]], np.uint32))
+        assert n[0] == 0
+        return int(t[0])
+
+    law = _law_of_final_draw(run)
+    got = np.array([law.get(y, 0) for y in range(v)], np.float64) / U
+    assert set(law) <= set(range(v))
+    assert np.max(np.abs(got - p0.astype(np.float64))) <= 2.0 / U
+
+
+def test_rejected_invalid_token_with_equal_rows_falls_back_to_p_n():
+    """From logits: target row 0 equals draft row 0 and the drafted token is
+    outside [0, v), so position 0 is rejected with an all-zero residual; the
+    emitted token follows softmax(row 0), not row 1."""
+    rng = np.random.default_rng(31)
+    v = 8
+    row0 = rng.normal(0, 1, v).astype(np.float32)
+    row1 = np.full(v, -50.0, np.float32)
+    row1[v - 1] = 50.0
+    dl = row0[None, None]
+    tl = np.stack([row0, row1])[None]
+    p0 = special.softmax(row0.astype(np.float64))
+    for bad in (-1, v):
+        def run(uf, bad=bad):
+            n, t, _, _ = oracle.spec_accept(dl, tl, np.array([[bad]], np.int32), np.array([[0, uf]], np.uint32))
+            assert n[0] == 0
+            return int(t[0])
+
+        law = _law_of_final_draw(run)
+        got = np.array([law.get(y, 0) for y in range(v)], np.float64) / U
+        assert np.max(np.abs(got - p0)) <= 2.0 / U
+
+
+def test_masked_logits_have_zero_probability():
+    """-inf logits (masked tokens, here a whole block of 5000 of them) get
+    probability 0: the rest is scipy's softmax over the finite logits; a
+    drafted token masked in the parent is always rejected, and no masked token
+    is ever emitted."""
+    rng = np.random.default_rng(37)
+    v = 9000
+    tl = rng.normal(0, 2, (2, v)).astype(np.float32)
+    dl = rng.normal(0, 2, v).astype(np.float32)
+    tl[0, 1000:6000] = -np.inf
+    tl[1, :4096] = -np.inf
+    dl[7000:] = -np.inf
+    p = oracle.softmax(tl)
+    fin = np.isfinite(tl[0])
+    assert np.all(p[0, ~fin] == 0)
+    assert np.max(np.abs(p[0, fin] - special.softmax(tl[0, fin].astype(np.float64)))) < 1e-15
+    assert np.all(oracle.softmax(dl)[0, 7000:] == 0)
+    for u in (0, 12345, U - 1):
+        for uf in (0, U // 3, U - 1):
+            n, t = _accept_one(dl, tl, 2000, u, uf)     # p_0(2000) = 0 < q_0(2000)
+            assert n == 0 and np.isfinite(tl[0, t])
+            n, t = _accept_one(dl, tl, 500, 0, uf)       # u = 0: accepted, bonus row 1
+            assert n == 1 and t >= 4096
+
+
+@pytest.mark.parametrize("bad", ["nan", "+inf", "all-masked"])
+def test_rows_without_a_distribution_invalidate_their_sequence(bad):
+    rng = np.random.default_rng(41)
+    b, kd, v = 4, 2, 100
+    dl = rng.normal(0, 1, (kd, b, v)).astype(np.float32)
+    tl = rng.normal(0, 1, (b, kd + 1, v)).astype(np.float32)
+    x = rng.integers(0, v, (kd, b)).astype(np.int32)
+    u24 = rng.integers(0, U, (b, kd + 1), dtype=np.uint32)
+    val = {"nan": np.nan, "+inf": np.inf}.get(bad)
+    if val is None:
+        tl[1, 2, :] = -np.inf          # sequence 1: target row 2 fully masked
+        dl[1, 2, :] = -np.inf          # sequence 2: draft row 1 fully masked
+    else:
+        tl[1, 2, 7] = val
+        dl[1, 2, 9] = val
+    n_ok, t_ok, _, _ = oracle.spec_accept(dl[:, [0, 3]], tl[[0, 3]], x[:, [0, 3]], u24[[0, 3]], 1.0)
+    n, t, q, p = oracle.spec_accept(dl, tl, x, u24, 1.0, want_pq=True)
+    assert n[1] == -1 and t[1] == -1 and n[2] == -1 and t[2] == -1
+    assert np.array_equal(n[[0, 3]], n_ok) and np.array_equal(t[[0, 3]], t_ok)
+    assert np.all(np.isnan(p[1, 2])) and np.all(np.isnan(q[1, 2])) and not np.any(np.isnan(p[0]))
+    n2, t2 = oracle.accept_probs(p.astype(np.float32), q.astype(np.float32), x, u24)
+    assert np.array_equal(n2, n) and np.array_equal(t2, t)
+    # greedy reads the target rows only: sequence 1 is invalid, sequence 2 is not
+    ng, tg, _, _ = oracle.spec_accept(dl, tl, x, None, 0.0)
+    assert ng[1] == -1 and tg[1] == -1 and ng[2] >= 0 and tg[2] == int(np.argmax(tl[2, ng[2]]))
