@@ -28,10 +28,15 @@
  *     nothing was enqueued (SQ_ERR_DEVICE: a launch or an allocation failed).
  *   - Outputs must not overlap inputs or each other (SQ_ERR_ALIAS).
  *   - Some kernels use a library-owned device workspace (split-K partial sums,
- *     softmax row statistics).  It is allocated once per device on first use
- *     and grown when a larger one is needed; it is shared by all calls on that
- *     device, so calls on one device must be ordered on one stream (calls on
- *     concurrently running streams of the same device race on it).
+ *     K-slice meeting slots, softmax row statistics), one per device.  It is
+ *     allocated on first use and grows when a call needs more; a buffer it
+ *     outgrows is kept, never freed, until the process ends, because a graph
+ *     captured while it was current keeps using it.  The library never
+ *     allocates while `stream` is being captured: a call that would need a
+ *     larger workspace then returns SQ_ERR_CAPTURE and enqueues nothing (run
+ *     the same call once outside capture first).  The workspace is shared by
+ *     all calls on a device, so calls on one device must be ordered on one
+ *     stream (calls on concurrently running streams of a device race on it).
  *   - Results are deterministic: the same inputs give the same bits.
  */
 #ifndef SPECQUANT_H
@@ -44,16 +49,20 @@
 extern "C" {
 #endif
 
-#define SQ_ABI_VERSION 1
+#define SQ_ABI_VERSION 2
 
 typedef enum sq_status {
   SQ_OK = 0,
-  SQ_ERR_NULL = 1,    /* a required pointer is NULL                            */
-  SQ_ERR_SHAPE = 2,   /* a size is outside the supported range                 */
-  SQ_ERR_ALIGN = 3,   /* a pointer is misaligned                               */
-  SQ_ERR_ALIAS = 4,   /* an output overlaps an input or another output         */
-  SQ_ERR_VALUE = 5,   /* a scalar argument is invalid (dtype, temperature)     */
-  SQ_ERR_DEVICE = 6   /* the HIP runtime reported an error; nothing enqueued   */
+  SQ_ERR_NULL = 1,        /* a required pointer is NULL                              */
+  SQ_ERR_SHAPE = 2,       /* a size is outside the supported range                   */
+  SQ_ERR_ALIGN = 3,       /* a pointer is misaligned                                 */
+  SQ_ERR_ALIAS = 4,       /* an output overlaps an input or another output           */
+  SQ_ERR_NONFINITE = 5,   /* a scalar argument is NaN or infinite (temperature)      */
+  SQ_ERR_UNSUPPORTED = 6, /* a dtype or mode the call does not support (y_dtype,
+                             T < 0, q_out / p_out requested at T = 0)                */
+  SQ_ERR_DEVICE = 7,      /* the HIP runtime reported an error; nothing enqueued     */
+  SQ_ERR_CAPTURE = 8      /* the workspace would have to grow while `stream` is
+                             being captured; nothing enqueued                        */
 } sq_status;
 
 typedef enum sq_dtype { SQ_F16 = 0, SQ_F32 = 1 } sq_dtype;
@@ -119,7 +128,10 @@ sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint
 /* LM-head softmax and speculative acceptance or correction (SS III-D.4; the
  * guess-set rule of SS III-A), for b sequences with kd drafted tokens each:
  *   q_i = softmax(draft_logits_i / T), p_i = softmax(target_logits_i / T),
- *   computed in fp64 (z = l / T, exp(z - max z) / sum exp(z - max z)).
+ *   computed in fp64 (z = l / T, exp(z - max z) / sum exp(z - max z)) and held
+ *   in fp32 -- the values q_out / p_out return.  Decisions and draw weights
+ *   are formed in fp64 from those fp32 values, so q_out / p_out reproduce them
+ *   exactly.
  * T > 0 (stochastic): position i (0 <= i < kd) with draft token x_i is
  *   accepted iff u_i * q_i(x_i) < p_i(x_i), u_i = (u24[s][i] & 0xFFFFFF) / 2^24;
  *   n_accepted = index of the first rejection (kd if none).  At a rejection the
@@ -129,6 +141,10 @@ sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint
  *   R = rint(r * 2^60) (int64), Z = sum R, t = floor(u24 * Z / 2^24), and the
  *   token is the smallest j whose running sum of R exceeds t.  A draft token
  *   outside [0, v) is rejected.
+ * Logits of -inf are masked tokens (probability 0).  A row holding a NaN or
+ *   +inf logit, or no finite logit, has no distribution: its sequence gets
+ *   n_accepted = next_token = -1 (T > 0: any of its 2 kd + 1 rows; T = 0: its
+ *   kd + 1 target rows), and its rows of q_out / p_out are NaN.
  * T = 0 (greedy, the paper's "if parent agrees" rule): position i is accepted
  *   iff x_i == argmax p_i (smallest index on ties); the emitted token is the
  *   argmax of the first disagreeing row, or of row kd.  u24 may be NULL.

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_PKG, "libspecquant.so")
 
 SQ_F16, SQ_F32 = 0, 1
 _STATUS = {0: "SQ_OK", 1: "SQ_ERR_NULL", 2: "SQ_ERR_SHAPE", 3: "SQ_ERR_ALIGN", 4: "SQ_ERR_ALIAS",
-           5: "SQ_ERR_VALUE", 6: "SQ_ERR_DEVICE"}
+           5: "SQ_ERR_NONFINITE", 6: "SQ_ERR_UNSUPPORTED", 7: "SQ_ERR_DEVICE", 8: "SQ_ERR_CAPTURE"}
 
 _lib = None
 _lock = threading.Lock()

@@ -7,6 +7,7 @@
 #include <map>
 #include <mutex>
 #include <tuple>
+#include <vector>
 
 #include "sq_internal.hpp"
 #include "specquant.h"
@@ -27,15 +28,55 @@ namespace {
 
 constexpr int kMaxDevices = 64;
 
-struct Workspace {
+// A device buffer that only grows.  A buffer it outgrows is retired, never
+// freed: a graph captured while that buffer was current keeps its address and
+// may be replayed at any later time, and kernels enqueued earlier may still be
+// using it.  Retired buffers live until the process ends (at most as many
+// bytes again as the current one, since each growth at least doubles).
+struct Pool {
   void* ptr = nullptr;
   size_t bytes = 0;
+  std::vector<void*> retired;
 };
 
 std::mutex g_ws_mutex;
-Workspace g_ws[kMaxDevices];
-Workspace g_cnt[kMaxDevices];
+Pool g_ws[kMaxDevices];
+Pool g_cnt[kMaxDevices];
 int g_cus[kMaxDevices];
+
+// Current buffer of `pool` with at least `bytes` bytes.  A new buffer is
+// allocated only outside stream capture (allocating would invalidate the
+// capture); it is zeroed on `stream` when `zero` is set.
+hipError_t pool_get(Pool& pool, size_t bytes, size_t grain, bool zero, hipStream_t stream, void** out) {
+  *out = nullptr;
+  if (pool.ptr && pool.bytes >= bytes) {
+    *out = pool.ptr;
+    return hipSuccess;
+  }
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &cs) != hipSuccess) {
+    (void)hipGetLastError();
+    return hipErrorInvalidValue;
+  }
+  if (cs != hipStreamCaptureStatusNone) return hipErrorStreamCaptureUnsupported;
+  size_t want = bytes > 2 * pool.bytes ? bytes : 2 * pool.bytes;
+  want = (want + grain - 1) / grain * grain;
+  void* p = nullptr;
+  if (hipMalloc(&p, want) != hipSuccess) {
+    (void)hipGetLastError();
+    return hipErrorOutOfMemory;
+  }
+  if (zero && hipMemsetAsync(p, 0, want, stream) != hipSuccess) {
+    (void)hipGetLastError();
+    (void)hipFree(p);  // never handed out
+    return hipErrorOutOfMemory;
+  }
+  if (pool.ptr) pool.retired.push_back(pool.ptr);
+  pool.ptr = p;
+  pool.bytes = want;
+  *out = p;
+  return hipSuccess;
+}
 
 }  // namespace
 
@@ -67,61 +108,23 @@ int cu_count() {
   return g_cus[dev];
 }
 
-void* workspace(size_t bytes) {
+hipError_t workspace(size_t bytes, hipStream_t stream, void** out) {
+  *out = nullptr;
   int dev = -1;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
   std::lock_guard<std::mutex> lock(g_ws_mutex);
-  Workspace& ws = g_ws[dev];
-  if (ws.bytes >= bytes && ws.ptr) return ws.ptr;
-  size_t want = bytes > 2 * ws.bytes ? bytes : 2 * ws.bytes;
-  const size_t grain = size_t(2) << 20;
-  want = (want + grain - 1) / grain * grain;
-  if (ws.ptr) {
-    // kernels enqueued earlier may still read the old buffer
-    if (hipDeviceSynchronize() != hipSuccess) return nullptr;
-    (void)hipFree(ws.ptr);
-    ws.ptr = nullptr;
-    ws.bytes = 0;
-  }
-  void* p = nullptr;
-  if (hipMalloc(&p, want) != hipSuccess) {
-    (void)hipGetLastError();
-    return nullptr;
-  }
-  ws.ptr = p;
-  ws.bytes = want;
-  return p;
+  return pool_get(g_ws[dev], bytes, size_t(2) << 20, false, stream, out);
 }
 
-int32_t* zeroed_counters(size_t count) {
+hipError_t zeroed_counters(size_t count, hipStream_t stream, int32_t** out) {
+  *out = nullptr;
   int dev = -1;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
-  const size_t bytes = count * sizeof(int32_t);
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
   std::lock_guard<std::mutex> lock(g_ws_mutex);
-  Workspace& c = g_cnt[dev];
-  if (c.bytes >= bytes && c.ptr) return static_cast<int32_t*>(c.ptr);
-  size_t want = bytes > 2 * c.bytes ? bytes : 2 * c.bytes;
-  const size_t grain = size_t(64) << 10;
-  want = (want + grain - 1) / grain * grain;
-  if (c.ptr) {
-    if (hipDeviceSynchronize() != hipSuccess) return nullptr;
-    (void)hipFree(c.ptr);
-    c.ptr = nullptr;
-    c.bytes = 0;
-  }
   void* p = nullptr;
-  if (hipMalloc(&p, want) != hipSuccess) {
-    (void)hipGetLastError();
-    return nullptr;
-  }
-  if (hipMemset(p, 0, want) != hipSuccess) {
-    (void)hipGetLastError();
-    (void)hipFree(p);
-    return nullptr;
-  }
-  c.ptr = p;
-  c.bytes = want;
-  return static_cast<int32_t*>(p);
+  const hipError_t e = pool_get(g_cnt[dev], count * sizeof(int32_t), size_t(64) << 10, true, stream, &p);
+  *out = static_cast<int32_t*>(p);
+  return e;
 }
 
 }  // namespace sq
@@ -154,7 +157,11 @@ bool any_alias(const Range (&outs)[NO], const Range (&ins)[NI]) {
   return false;
 }
 
-inline sq_status device_status(hipError_t e) { return e == hipSuccess ? SQ_OK : SQ_ERR_DEVICE; }
+inline sq_status device_status(hipError_t e) {
+  if (e == hipSuccess) return SQ_OK;
+  if (e == hipErrorStreamCaptureUnsupported) return SQ_ERR_CAPTURE;  // the workspace would have to grow
+  return SQ_ERR_DEVICE;
+}
 
 constexpr int64_t kMaxK = int64_t(1) << 20;
 constexpr int64_t kMaxN = 0x7FFFFFFF;
@@ -172,8 +179,11 @@ const char* sq_status_str(sq_status s) {
     case SQ_ERR_SHAPE: return "SQ_ERR_SHAPE: a size is outside the supported range";
     case SQ_ERR_ALIGN: return "SQ_ERR_ALIGN: a pointer is misaligned";
     case SQ_ERR_ALIAS: return "SQ_ERR_ALIAS: an output overlaps an input or another output";
-    case SQ_ERR_VALUE: return "SQ_ERR_VALUE: a scalar argument is invalid";
+    case SQ_ERR_NONFINITE: return "SQ_ERR_NONFINITE: a scalar argument is NaN or infinite";
+    case SQ_ERR_UNSUPPORTED: return "SQ_ERR_UNSUPPORTED: a dtype or mode outside what the call supports";
     case SQ_ERR_DEVICE: return "SQ_ERR_DEVICE: the HIP runtime reported an error";
+    case SQ_ERR_CAPTURE:
+      return "SQ_ERR_CAPTURE: the library workspace would have to grow while the stream is captured";
   }
   return "unknown sq_status";
 }
@@ -211,7 +221,7 @@ sq_status sq_qgemv_w4a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t*
                          const uint16_t* zeros, int64_t n, void* y, sq_dtype y_dtype, hipStream_t stream) {
   if (!x || !codes || !scales || !zeros || !y) return SQ_ERR_NULL;
   if (m < 1 || m > 8 || n < 1 || n > kMaxN || k < 128 || k > kMaxK || k % 128 != 0) return SQ_ERR_SHAPE;
-  if (y_dtype != SQ_F16 && y_dtype != SQ_F32) return SQ_ERR_VALUE;
+  if (y_dtype != SQ_F16 && y_dtype != SQ_F32) return SQ_ERR_UNSUPPORTED;
   const size_t ysz = y_dtype == SQ_F16 ? 2 : 4;
   if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 2) || !aligned(zeros, 2) || !aligned(y, ysz))
     return SQ_ERR_ALIGN;
@@ -227,7 +237,7 @@ sq_status sq_qgemv_w8a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t*
                          int64_t n, void* y, sq_dtype y_dtype, hipStream_t stream) {
   if (!x || !codes || !scales || !y) return SQ_ERR_NULL;
   if (m < 1 || m > 8 || n < 1 || n > kMaxN || k < 16 || k > kMaxK || k % 16 != 0) return SQ_ERR_SHAPE;
-  if (y_dtype != SQ_F16 && y_dtype != SQ_F32) return SQ_ERR_VALUE;
+  if (y_dtype != SQ_F16 && y_dtype != SQ_F32) return SQ_ERR_UNSUPPORTED;
   const size_t ysz = y_dtype == SQ_F16 ? 2 : 4;
   if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(y, ysz)) return SQ_ERR_ALIGN;
   const size_t nk = (size_t)n * (size_t)k;
@@ -249,7 +259,7 @@ sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint
                              sq_dtype y_dtype, hipStream_t stream) {
   if (!x || !w16 || !y) return SQ_ERR_NULL;
   if (m < 1 || m > 64 || n < 1 || n > kMaxN || k < 8 || k > kMaxK || k % 8 != 0) return SQ_ERR_SHAPE;
-  if (y_dtype != SQ_F16 && y_dtype != SQ_F32) return SQ_ERR_VALUE;
+  if (y_dtype != SQ_F16 && y_dtype != SQ_F32) return SQ_ERR_UNSUPPORTED;
   const size_t ysz = y_dtype == SQ_F16 ? 2 : 4;
   if (!aligned(x, 16) || !aligned(w16, 16) || !aligned(y, ysz)) return SQ_ERR_ALIGN;
   const Range outs[] = {{y, (size_t)m * n * ysz}};
@@ -291,8 +301,9 @@ sq_status sq_spec_accept(const float* draft_logits, const float* target_logits, 
   const int64_t nchunk = (v + 4095) / 4096;
   // every kernel grid stays below 2^24 workgroups of 256 threads (2^32 work-items)
   if ((int64_t)b * (2 * kd + 1) * nchunk >= (int64_t(1) << 24)) return SQ_ERR_SHAPE;
-  if (!isfinite(temperature) || temperature < 0.0f) return SQ_ERR_VALUE;
-  if (temperature == 0.0f && (q_out || p_out)) return SQ_ERR_VALUE;
+  if (!isfinite(temperature)) return SQ_ERR_NONFINITE;
+  if (temperature < 0.0f) return SQ_ERR_UNSUPPORTED;
+  if (temperature == 0.0f && (q_out || p_out)) return SQ_ERR_UNSUPPORTED;
   if (temperature > 0.0f && !u24) return SQ_ERR_NULL;
   if (!aligned(draft_logits, 4) || !aligned(target_logits, 4) || !aligned(draft_tokens, 4) || !aligned(u24, 4) ||
       !aligned(n_accepted, 4) || !aligned(next_token, 4) || !aligned(q_out, 4) || !aligned(p_out, 4))

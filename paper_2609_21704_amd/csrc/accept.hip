@@ -7,13 +7,19 @@
 //   1. stats:    per (row, chunk) the max of z = l / T and sum exp(z - max),
 //                fp64 (online-softmax partials, merged later in chunk order);
 //   2. decide:   per (sequence, chunk) merge the row partials, take the kd
-//                accept decisions u * q(x) < p(x) in fp64 (one thread each),
-//                find the first rejection n, and sum the chunk's share of the
-//                draw weights R = rint(r * 2^60) in int64 (exact, so the total
+//                accept decisions u * q(x) < p(x) (one thread each), find the
+//                first rejection n, and sum the chunk's share of the draw
+//                weights R = rint(r * 2^60) in int64 (exact, so the total
 //                does not depend on the summation order);
 //   3. draw:     per sequence, locate the chunk holding t = floor(u Z / 2^24)
 //                with a block scan of the chunk totals, then block-scan that
 //                chunk.
+// Probabilities are computed in fp64 and held in fp32 (prob32), the values
+// q_out / p_out hand back; the decisions and the draw weights are formed in
+// fp64 from those fp32 values, so that they can be reproduced exactly from
+// q_out / p_out.  A -inf logit is a masked token (probability 0).  A row
+// holding a NaN or +inf logit, or no finite logit, has no distribution: its
+// sequence gets n_accepted = next_token = -1 (and NaN rows in q_out / p_out).
 // Greedy uses per-chunk (max, first index) pairs and one decision pass.
 #include <math.h>
 
@@ -43,6 +49,12 @@ struct ArgMax {
 __device__ __forceinline__ double zval(float l, float t) { return t == 1.0f ? (double)l : (double)l / (double)t; }
 
 __device__ __forceinline__ int64_t grid_weight(double r) { return llrint(ldexp(r, 60)); }
+
+// A probability exp(z - L) / S in fp64, held in fp32: the one expression
+// behind q_out / p_out, the decisions and the draw weights.
+__device__ __forceinline__ float prob32(float l, float t, double L, double S) {
+  return (float)(exp(zval(l, t) - L) / S);
+}
 
 // Deterministic block reductions over 256 threads (4 wavefronts).
 __device__ double block_max(double v, double* sh) {
@@ -103,17 +115,34 @@ __device__ int64_t block_exclusive_scan_i64(int64_t v, int64_t* sh, int64_t& tot
 
 // One wavefront merges a row's chunk partials: L = max over chunks, S = the
 // sum of S_c exp(L_c - L), each lane taking every 64th chunk and the lanes
-// combined in a fixed shuffle tree.  Lane 0's values are returned.
+// combined in a fixed shuffle tree.  A fully masked chunk (S_c = 0) adds
+// nothing; a chunk marked invalid (S_c NaN), or a row without any mass, gives
+// L = S = NaN.  Every lane returns the values.
 __device__ void wave_merge(const double2* st, int nchunk, double& L, double& S) {
   const int lane = threadIdx.x & 63;
   double mx = -INFINITY;
-  for (int c = lane; c < nchunk; c += 64) mx = fmax(mx, st[c].x);
+  int bad = 0;
+  for (int c = lane; c < nchunk; c += 64) {
+    const double2 e = st[c];
+    bad |= isnan(e.y) ? 1 : 0;
+    if (e.y > 0.0) mx = fmax(mx, e.x);
+  }
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) mx = fmax(mx, __shfl_xor(mx, off, 64));
+  for (int off = 32; off >= 1; off >>= 1) {
+    mx = fmax(mx, __shfl_xor(mx, off, 64));
+    bad |= __shfl_xor(bad, off, 64);
+  }
   double s = 0.0;
-  for (int c = lane; c < nchunk; c += 64) s += st[c].y * exp(st[c].x - mx);
+  for (int c = lane; c < nchunk; c += 64) {
+    const double2 e = st[c];
+    if (e.y > 0.0) s += e.y * exp(e.x - mx);
+  }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+  if (bad || !(s > 0.0)) {
+    mx = NAN;
+    s = NAN;
+  }
   L = mx;
   S = s;
 }
@@ -129,21 +158,25 @@ __global__ __launch_bounds__(kThreads) void stats_kernel(const float* __restrict
   const int beg = c * kChunk;
   double z[kPer];
   double mx = -INFINITY;
+  int bad = 0;
 #pragma unroll
   for (int e = 0; e < kPer; ++e) {
     const int j = beg + e * kThreads + threadIdx.x;
-    z[e] = j < v ? zval(l[j], temp) : -INFINITY;
-    mx = fmax(mx, z[e]);
+    const float lj = j < v ? l[j] : -INFINITY;
+    bad |= (isnan(lj) || lj == INFINITY) ? 1 : 0;
+    z[e] = zval(lj, temp);
+    if (!isnan(z[e])) mx = fmax(mx, z[e]);
   }
+  bad = __syncthreads_or(bad);
   mx = block_max(mx, sh);
   double s = 0.0;
+  if (mx > -INFINITY && !bad) {  // uniform across the block
 #pragma unroll
-  for (int e = 0; e < kPer; ++e) {
-    const int j = beg + e * kThreads + threadIdx.x;
-    if (j < v) s += exp(z[e] - mx);
+    for (int e = 0; e < kPer; ++e) s += exp(z[e] - mx);  // masked and padded cells add exp(-inf) = 0
   }
   s = block_sum(s, sh);
-  if (threadIdx.x == 0) stats[row * nchunk + c] = make_double2(mx, s);
+  // (max, sum); a fully masked chunk is (-inf, 0); an invalid one (NaN, NaN)
+  if (threadIdx.x == 0) stats[row * nchunk + c] = bad ? make_double2(NAN, NAN) : make_double2(mx, s);
 }
 
 // Optional copies of the distributions: p or q = exp(z - L) / S as fp32.
@@ -165,18 +198,20 @@ __global__ __launch_bounds__(kThreads) void probs_kernel(const float* __restrict
     }
   }
   __syncthreads();
-  const double L = sL, S = sS;
+  const double L = sL, S = sS;  // NaN for a row without a distribution: NaN out
   const float* l = row_ptr(draft, target, rows_t, row, v);
   for (int e = 0; e < kPer; ++e) {
     const int j = c * kChunk + e * kThreads + threadIdx.x;
-    if (j < v) out[j] = (float)(exp(zval(l[j], temp) - L) / S);
+    if (j < v) out[j] = prob32(l[j], temp, L, S);
   }
 }
 
 // 2. per (sequence, chunk): decisions, first rejection, chunk share of the draw weights.
 // zs[(s * nchunk + c) * 2 + 0] = sum of R over the chunk for the draw row
 // (residual max(0, p_n - q_n) when n < kd, else p_kd); [.. + 1] = sum of R for
-// p_n (the fallback when the residual mass is zero).  blockIdx.x = s * nchunk + c.
+// p_n (the fallback when the residual mass is zero).  A sequence with a row
+// without a distribution gets n = -1 and zero weights.
+// blockIdx.x = s * nchunk + c.
 __global__ __launch_bounds__(kThreads) void decide_kernel(const float* __restrict__ draft,
                                                           const float* __restrict__ target,
                                                           const int32_t* __restrict__ tokens,
@@ -201,15 +236,19 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(const float* __restric
     }
   }
   __syncthreads();
-  if (threadIdx.x < kd) {
+  int invalid = 0;
+  for (int rr = threadIdx.x; rr < 2 * kd + 1; rr += kThreads) invalid |= isnan(sS[rr]) ? 1 : 0;
+  invalid = __syncthreads_or(invalid);
+  if (threadIdx.x < kd && !invalid) {
     const int i = threadIdx.x;
     const int32_t xt = tokens[(int64_t)i * b + s];
     int acc = 0;
     if (xt >= 0 && xt < v) {
-      const double p = exp(zval(target[((int64_t)s * (kd + 1) + i) * v + xt], temp) - sL[i]) / sS[i];
-      const double q = exp(zval(draft[((int64_t)i * b + s) * v + xt], temp) - sL[kd + 1 + i]) / sS[kd + 1 + i];
+      // fp32 probabilities; u (24 bits) times q (24 bits) is exact in fp64
+      const float p = prob32(target[((int64_t)s * (kd + 1) + i) * v + xt], temp, sL[i], sS[i]);
+      const float q = prob32(draft[((int64_t)i * b + s) * v + xt], temp, sL[kd + 1 + i], sS[kd + 1 + i]);
       const double u = ldexp((double)(u24[(int64_t)s * (kd + 1) + i] & 0xFFFFFFu), -24);
-      acc = (u * q < p) ? 1 : 0;
+      acc = (u * (double)q < (double)p) ? 1 : 0;
     }
     sAcc[i] = acc;
   }
@@ -221,10 +260,24 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(const float* __restric
         n = i;
         break;
       }
-    sN = n;
+    sN = invalid ? -1 : n;
   }
   __syncthreads();
   const int n = sN;
+  if (n < 0) {  // uniform across the block
+    if (threadIdx.x == 0) {
+      zs[((int64_t)s * nchunk + c) * 2 + 0] = 0;
+      zs[((int64_t)s * nchunk + c) * 2 + 1] = 0;
+      if (c == 0) {
+        SeqInfo si;
+        si.n = -1;
+        si.pad = 0;
+        si.lp = si.sp = si.lq = si.sq = 0.0;
+        info[s] = si;
+      }
+    }
+    return;
+  }
   const float* lp = target + ((int64_t)s * (kd + 1) + n) * v;
   const double Lp = sL[n], Sp = sS[n];
   const bool resid = n < kd;
@@ -234,14 +287,14 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(const float* __restric
   for (int e = 0; e < kPer; ++e) {
     const int j = c * kChunk + e * kThreads + threadIdx.x;
     if (j >= v) break;
-    const double p = exp(zval(lp[j], temp) - Lp) / Sp;
+    const float p = prob32(lp[j], temp, Lp, Sp);
     if (resid) {
-      const double q = exp(zval(lq[j], temp) - Lq) / Sq;
-      const double r = p - q;
+      const float q = prob32(lq[j], temp, Lq, Sq);
+      const double r = (double)p - (double)q;
       z0 += grid_weight(r > 0.0 ? r : 0.0);
-      z1 += grid_weight(p);
+      z1 += grid_weight((double)p);
     } else {
-      z0 += grid_weight(p);
+      z0 += grid_weight((double)p);
     }
   }
   z0 = block_sum_i64(z0, shi);
@@ -279,6 +332,13 @@ __global__ __launch_bounds__(kThreads) void draw_kernel(const float* __restrict_
   const int s = blockIdx.x;
   const SeqInfo si = info[s];
   const int n = si.n;
+  if (n < 0) {  // a row without a distribution
+    if (threadIdx.x == 0) {
+      n_accepted[s] = -1;
+      next_token[s] = -1;
+    }
+    return;
+  }
   const int64_t* z = zs + (int64_t)s * nchunk * 2;
 
   // the total mass Z of the draw row (the residual's, else p_n's when that is zero on the grid)
@@ -340,13 +400,13 @@ __global__ __launch_bounds__(kThreads) void draw_kernel(const float* __restrict_
     const int j = beg + e;
     int64_t w = 0;
     if (j < v) {
-      const double p = exp(zval(lp[j], temp) - si.lp) / si.sp;
+      const float p = prob32(lp[j], temp, si.lp, si.sp);
       if (resid) {
-        const double q = exp(zval(lq[j], temp) - si.lq) / si.sq;
-        const double r = p - q;
+        const float q = prob32(lq[j], temp, si.lq, si.sq);
+        const double r = (double)p - (double)q;
         w = grid_weight(r > 0.0 ? r : 0.0);
       } else {
-        w = grid_weight(p);
+        w = grid_weight((double)p);
       }
     }
     R[e] = w;
@@ -370,7 +430,12 @@ __global__ __launch_bounds__(kThreads) void draw_kernel(const float* __restrict_
   }
 }
 
-// Greedy: per (target row, chunk) the max logit and its smallest index.
+// Greedy: per (target row, chunk) the max finite logit and its smallest
+// index (index kNone when the chunk has no finite logit, kBad when it holds a
+// NaN or +inf).
+constexpr int kNone = 0x7FFFFFFF;
+constexpr int kBad = -1;
+
 __global__ __launch_bounds__(kThreads) void argmax_kernel(const float* __restrict__ target, int v, int nchunk,
                                                           ArgMax* __restrict__ out) {
   __shared__ float sv[4];
@@ -379,22 +444,25 @@ __global__ __launch_bounds__(kThreads) void argmax_kernel(const float* __restric
   const int c = blockIdx.x % nchunk;
   const float* l = target + row * v;
   float best = -INFINITY;
-  int bi = 0x7FFFFFFF;
+  int bi = kNone;
+  int bad = 0;
   for (int e = 0; e < kPer; ++e) {
     const int j = c * kChunk + e * kThreads + threadIdx.x;
     if (j < v) {
       const float x = l[j];
-      if (x > best || (x == best && j < bi)) {
+      bad |= (isnan(x) || x == INFINITY) ? 1 : 0;
+      if (isfinite(x) && (bi == kNone || x > best || (x == best && j < bi))) {
         best = x;
         bi = j;
       }
     }
   }
+  bad = __syncthreads_or(bad);
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
     const float ov = __shfl_xor(best, off, 64);
     const int oi = __shfl_xor(bi, off, 64);
-    if (ov > best || (ov == best && oi < bi)) {
+    if (oi != kNone && (bi == kNone || ov > best || (ov == best && oi < bi))) {
       best = ov;
       bi = oi;
     }
@@ -406,13 +474,13 @@ __global__ __launch_bounds__(kThreads) void argmax_kernel(const float* __restric
   __syncthreads();
   if (threadIdx.x == 0) {
     for (int w = 1; w < 4; ++w)
-      if (sv[w] > best || (sv[w] == best && si[w] < bi)) {
+      if (si[w] != kNone && (bi == kNone || sv[w] > best || (sv[w] == best && si[w] < bi))) {
         best = sv[w];
         bi = si[w];
       }
     ArgMax a;
     a.v = best;
-    a.i = bi;
+    a.i = bad ? kBad : bi;
     out[row * nchunk + c] = a;
   }
 }
@@ -425,17 +493,28 @@ __global__ __launch_bounds__(kThreads) void greedy_kernel(const int32_t* __restr
   const int s = blockIdx.x;
   for (int i = threadIdx.x; i <= kd; i += kThreads) {
     const ArgMax* a = am + ((int64_t)s * (kd + 1) + i) * nchunk;
-    float best = a[0].v;
-    int bi = a[0].i;
-    for (int c = 1; c < nchunk; ++c)
-      if (a[c].v > best) {  // chunks ascend, so ties keep the earlier index
-        best = a[c].v;
-        bi = a[c].i;
+    float best = -INFINITY;
+    int bi = kNone;
+    bool bad = false;
+    for (int c = 0; c < nchunk; ++c) {
+      const ArgMax e = a[c];
+      bad |= e.i == kBad;
+      if (e.i != kBad && e.i != kNone && (bi == kNone || e.v > best)) {  // chunks ascend: ties keep the earlier
+        best = e.v;
+        bi = e.i;
       }
-    sArg[i] = bi;
+    }
+    sArg[i] = (bad || bi == kNone) ? -1 : bi;  // -1: the row has no greedy target
   }
   __syncthreads();
   if (threadIdx.x == 0) {
+    bool invalid = false;
+    for (int i = 0; i <= kd; ++i) invalid |= sArg[i] < 0;
+    if (invalid) {
+      n_accepted[s] = -1;
+      next_token[s] = -1;
+      return;
+    }
     int n = kd;
     for (int i = 0; i < kd; ++i) {
       const int32_t xt = tokens[(int64_t)i * b + s];
@@ -457,8 +536,10 @@ hipError_t launch_spec_accept(const float* draft, const float* target, const int
   const int nchunk = (v + kChunk - 1) / kChunk;
   const int64_t rows_t = (int64_t)b * (kd + 1);
   if (temperature == 0.0f) {
-    ArgMax* am = static_cast<ArgMax*>(workspace((size_t)rows_t * nchunk * sizeof(ArgMax)));
-    if (!am) return hipErrorOutOfMemory;
+    void* ws = nullptr;
+    const hipError_t e = workspace((size_t)rows_t * nchunk * sizeof(ArgMax), stream, &ws);
+    if (e != hipSuccess) return e;
+    ArgMax* am = static_cast<ArgMax*>(ws);
     hipLaunchKernelGGL(argmax_kernel, dim3((unsigned)(rows_t * nchunk)), dim3(kThreads), 0, stream, target, v, nchunk,
                        am);
     hipLaunchKernelGGL(greedy_kernel, dim3((unsigned)b), dim3(kThreads), 0, stream, tokens, b, kd, v, nchunk, am,
@@ -469,8 +550,10 @@ hipError_t launch_spec_accept(const float* draft, const float* target, const int
   const size_t st_bytes = ((size_t)rows * nchunk * sizeof(double2) + 255) / 256 * 256;
   const size_t zs_bytes = ((size_t)b * nchunk * 2 * sizeof(int64_t) + 255) / 256 * 256;
   const size_t in_bytes = (size_t)b * sizeof(SeqInfo);
-  char* ws = static_cast<char*>(workspace(st_bytes + zs_bytes + in_bytes));
-  if (!ws) return hipErrorOutOfMemory;
+  void* wsp = nullptr;
+  const hipError_t e = workspace(st_bytes + zs_bytes + in_bytes, stream, &wsp);
+  if (e != hipSuccess) return e;
+  char* ws = static_cast<char*>(wsp);
   double2* stats = reinterpret_cast<double2*>(ws);
   int64_t* zs = reinterpret_cast<int64_t*>(ws + st_bytes);
   SeqInfo* info = reinterpret_cast<SeqInfo*>(ws + st_bytes + zs_bytes);

@@ -388,6 +388,7 @@ struct RowsIntC {
 };
 
 constexpr size_t kRowsLds = 150 * 1024;
+constexpr int kVerifyRowsDepth = 1;  // steps of loads in flight per wavefront (measured: 1 < 2 < 3 in time)
 
 template <int M>
 hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t n, void* y, bool f16_out,
@@ -416,20 +417,19 @@ hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t 
   const int64_t ppr = k / ks / 16, xcells = (int64_t)M * 2 * ppr;
   unsigned long long* slots = nullptr;
   if (ks > 1) {  // one 64-bit meeting slot per output value
-    slots = reinterpret_cast<unsigned long long*>(zeroed_counters(2 * (size_t)M * n));
-    if (!slots) return hipErrorOutOfMemory;
+    int32_t* c = nullptr;
+    const hipError_t e = zeroed_counters(2 * (size_t)M * n, stream, &c);
+    if (e != hipSuccess) return e;
+    slots = reinterpret_cast<unsigned long long*>(c);
   }
   const int64_t q = n / blocks;
   const int rem = (int)(n % blocks);
   // at least half the LDS of a CU, so that no CU holds two of these workgroups
   // while another holds none (the registers of the small-m kernels would allow two)
   const size_t lds_launch = lds > 81 * 1024 ? lds : 81 * 1024;
-#ifndef SQ_VERIFY_ROWS_DEPTH
-#define SQ_VERIFY_ROWS_DEPTH 1
-#endif
   auto go = [&](auto na_tag, auto xb_tag, auto ks_tag) {
     constexpr int NA = decltype(na_tag)::value, XB = decltype(xb_tag)::value, KS = decltype(ks_tag)::value;
-    hipLaunchKernelGGL((gemm_rows_kernel<M, NA, nwave, XB, SQ_VERIFY_ROWS_DEPTH, KS>),
+    hipLaunchKernelGGL((gemm_rows_kernel<M, NA, nwave, XB, kVerifyRowsDepth, KS>),
                        dim3((unsigned)blocks, (unsigned)KS), dim3(nthr), lds_launch, stream, x, k, w, n, y,
                        (int)f16_out, q, rem, slots);
   };

@@ -53,12 +53,8 @@ namespace {
 constexpr int max_rows_for(int m) { return m <= 2 ? 4 : (m <= 4 ? 2 : 1); }
 constexpr int kLaneBytes = 32;              // code bytes per lane per row and step
 constexpr size_t kLdsBudget = 64 * 1024;    // activation bytes one workgroup may stage
-#ifndef SQ_GEMV_WAVES_PER_CU
-#define SQ_GEMV_WAVES_PER_CU 16             // resident wavefronts per CU in the persistent grid
-#endif
-#ifndef SQ_GEMV_TEAMS_MAX
-#define SQ_GEMV_TEAMS_MAX 4                 // teams per workgroup, at most (2 for 4-wavefront teams; measured)
-#endif
+constexpr int kWavesPerCu = 16;            // resident wavefronts per CU in the persistent grid
+constexpr int kTeamsMax = 4;               // teams per workgroup, at most (2 for 4-wavefront teams; measured)
 
 template <int V>
 struct IntC {
@@ -723,16 +719,16 @@ hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits,
   const int64_t nchunk = (kfirst + chunk_k - 1) / chunk_k;
   const int64_t ntask = (n + R - 1) / R;
   const int64_t cus = cu_count();
-  // teams: as many as the CUs hold (SQ_GEMV_WAVES_PER_CU wavefronts each) or
+  // teams: as many as the CUs hold (kWavesPerCu wavefronts each) or
   // as there are tasks; teams per workgroup: enough to cover the CUs once
-  const int64_t per_cu = SQ_GEMV_WAVES_PER_CU / nw > 0 ? SQ_GEMV_WAVES_PER_CU / nw : 1;
+  const int64_t per_cu = kWavesPerCu / nw > 0 ? kWavesPerCu / nw : 1;
   int64_t teams = ntask < cus * per_cu / splits ? ntask : cus * per_cu / splits;
   if (teams < 1) teams = 1;
   int64_t T = (teams + cus / splits - 1) / (cus / splits > 0 ? cus / splits : 1);
   if (T > per_cu) T = per_cu;
-  // teams per workgroup: at most SQ_GEMV_TEAMS_MAX (half that for teams of four or
+  // teams per workgroup: at most kTeamsMax (half that for teams of four or
   // more wavefronts), and a divisor of the teams per CU, so that workgroups tile the CUs
-  int64_t tmax = nw >= 4 ? (SQ_GEMV_TEAMS_MAX + 1) / 2 : SQ_GEMV_TEAMS_MAX;
+  int64_t tmax = nw >= 4 ? (kTeamsMax + 1) / 2 : kTeamsMax;
   while (tmax > 1 && per_cu % tmax != 0) --tmax;
   if (T > tmax) T = tmax;
   if (T < 1) T = 1;
@@ -744,15 +740,8 @@ hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits,
   return hipGetLastError();
 }
 
-#ifndef SQ_GEMV_ROWS_MIN_K
-#define SQ_GEMV_ROWS_MIN_K 1024  // shortest rows the row-block INT4 kernel takes
-#endif
-#ifndef SQ_GEMV_ROWS_DEPTH
-#define SQ_GEMV_ROWS_DEPTH 1     // steps of loads in flight per wavefront (measured: 1 < 2 < 3 < 4 in time)
-#endif
-#ifndef SQ_GEMV_ROWS_W8
-#define SQ_GEMV_ROWS_W8 1        // FP8 GEMVs at m <= 4 on the row-block kernel
-#endif
+constexpr int64_t kRowsMinK = 1024;  // shortest rows the row-block kernel takes
+constexpr int kRowsDepth = 1;        // steps of loads in flight per wavefront (measured: 1 < 2 < 3 < 4 in time)
 constexpr size_t kRowsLdsMax = 150 * 1024;
 
 // Host side of the row-block kernel (INT4 m <= 2, FP8 m <= 4): 16 wavefronts
@@ -764,7 +753,7 @@ hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const
                        const uint16_t* zeros16, const float* scales32, int64_t n, void* y, bool f16_out,
                        hipStream_t stream) {
   // whole pieces per row: 32 FP8 codes, or 64 INT4 codes (k % 128 == 0 already)
-  if (M > (W8 ? 4 : 2) || k < (W8 ? 1024 : SQ_GEMV_ROWS_MIN_K) || k < 1024 || (W8 && k % 32 != 0))
+  if (M > (W8 ? 4 : 2) || k < kRowsMinK || (W8 && k % 32 != 0))
     return hipErrorNotSupported;
   // 16 wavefronts per CU: one workgroup of 16, or two of 8 for INT4 rows of
   // 8192 k and more (measured: 7B down 13.5 -> 12.8 us, q|k|v 5.8 -> 6.0 us)
@@ -778,7 +767,7 @@ hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const
   const int64_t xcells = M * ppr * cpc;  // 16-byte activation cells, staged by the workgroup at once
   if (lds > kRowsLdsMax || rows_max * ppr >= (int64_t(1) << 27) || xcells > 8 * nthr)
     return hipErrorNotSupported;
-  constexpr int D = SQ_GEMV_ROWS_DEPTH;
+  constexpr int D = kRowsDepth;
   const int64_t q = n / blocks;
   const int rem = (int)(n % blocks);
   // workgroups of 8 wavefronts take over a third of the LDS, so that a CU holds
@@ -822,18 +811,10 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
   // the activations of a K slice sit in LDS (M * 2 bytes per k); slices are
   // whole 128-element groups
   const int64_t grain = 128;
-  int64_t kmax = (int64_t)(kLdsBudget / ((size_t)M * 2)) / grain * grain;
-#ifdef SQ_GEMV_KSLICE_MAX
-  if (kmax > SQ_GEMV_KSLICE_MAX) kmax = SQ_GEMV_KSLICE_MAX;
-#endif
+  const int64_t kmax = (int64_t)(kLdsBudget / ((size_t)M * 2)) / grain * grain;
   const int splits = (int)((k + kmax - 1) / kmax);
   int64_t kslice = (k + splits - 1) / splits;
   kslice = (kslice + grain - 1) / grain * grain;
-  float* partial = nullptr;
-  if (splits > 1) {
-    partial = static_cast<float*>(workspace((size_t)splits * M * n * sizeof(float)));
-    if (!partial) return hipErrorOutOfMemory;
-  }
   // wavefronts per workgroup: one per step of a task, at most four
   const int64_t chunk_k = W8 ? 32 : 64;
   const int64_t kfirst = kslice < k ? kslice : k;
@@ -844,7 +825,7 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
   const int64_t steps = nit < nit_last ? nit : nit_last;
   // rows per task: the most that still give each resident wavefront at least
   // two tasks (four rows: eight), one row otherwise
-  const int64_t waves = (int64_t)cu_count() * SQ_GEMV_WAVES_PER_CU;
+  const int64_t waves = (int64_t)cu_count() * kWavesPerCu;
   constexpr int RMAX = max_rows_for(M);
   int rows = 1;
   if (RMAX >= 4 && (n + 3) / 4 >= 8 * waves)
@@ -863,20 +844,22 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
     // leaves more than a quarter of the lanes idle (measured crossover)
     const int64_t row_chunks = k / 64;
     const bool idle_lanes = 4 * row_chunks < 3 * 64 * ((row_chunks + 63) / 64);
-#ifdef SQ_GEMV_ROWS_ALL
-    if (true) {
-#else
     if (rows == 1 || idle_lanes) {
-#endif
       const hipError_t e = gemv_rows_m<M, false>(x, k, codes, scales16, zeros16, nullptr, n, y, f16_out, stream);
       if (e != hipErrorNotSupported) return e;
     }
   }
   if constexpr (W8 && M <= 4) {
-#if SQ_GEMV_ROWS_W8
     const hipError_t e = gemv_rows_m<M, true>(x, k, codes, nullptr, nullptr, scales32, n, y, f16_out, stream);
     if (e != hipErrorNotSupported) return e;
-#endif
+  }
+  // split-K partial sums: only the tasks-of-rows kernel needs them
+  float* partial = nullptr;
+  if (splits > 1) {
+    void* ws = nullptr;
+    const hipError_t e = workspace((size_t)splits * M * n * sizeof(float), stream, &ws);
+    if (e != hipSuccess) return e;
+    partial = static_cast<float*>(ws);
   }
   hipError_t err = hipErrorInvalidValue;
   auto go = [&](auto r_tag, auto multi_tag) {

@@ -527,9 +527,7 @@ __global__ __launch_bounds__(256) void slice_reduce_kernel(const float* __restri
   }
 }
 
-#ifndef SQ_LINEAR_CHUNK_MIN
-#define SQ_LINEAR_CHUNK_MIN 4  // units per chunk, at least (measured: 4 beats 1 and 2)
-#endif
+constexpr int64_t kChunkMinUnits = 4;  // units per chunk, at least (measured: 4 beats 1 and 2)
 constexpr size_t kLdsTotal = 150 * 1024;   // one workgroup per CU
 constexpr size_t kPieceBudget = 32 * 1024; // chunk partial sums
 
@@ -557,7 +555,7 @@ hipError_t linear_launch(const uint16_t* x, int m, int64_t k, const uint8_t* w, 
   if (nwg_max < 1) nwg_max = 1;
   // the smallest chunk whose partial sums ([chunks per workgroup][m][16] floats) fit the budget;
   // direct: one chunk per task, no partial sums
-  int64_t C = direct ? S : SQ_LINEAR_CHUNK_MIN, nch_max = 0;
+  int64_t C = direct ? S : kChunkMinUnits, nch_max = 0;
   for (;; ++C) {
     const int64_t J = (S + C - 1) / C;
     nch_max = (ntask * J + nwg_max - 1) / nwg_max;
@@ -574,14 +572,17 @@ hipError_t linear_launch(const uint16_t* x, int m, int64_t k, const uint8_t* w, 
       splits > 1 && !slice_meet ? ((size_t)splits * m * n * sizeof(float) + 255) / 256 * 256 : 0;
   float* split_out = nullptr;
   if (split_bytes > 0) {
-    split_out = static_cast<float*>(workspace(split_bytes));
-    if (!split_out) return hipErrorOutOfMemory;
+    void* ws = nullptr;
+    const hipError_t e = workspace(split_bytes, stream, &ws);
+    if (e != hipSuccess) return e;
+    split_out = static_cast<float*>(ws);
   }
   // 64-bit meeting slots: workgroup boundaries of every slice, then one per output value
   const size_t wg_slots = (size_t)splits * nwg_max * m * 16;
   const size_t value_slots = slice_meet ? (size_t)m * n : 0;
-  int32_t* slots = zeroed_counters(2 * (wg_slots + value_slots));
-  if (!slots) return hipErrorOutOfMemory;
+  int32_t* slots = nullptr;
+  const hipError_t ce = zeroed_counters(2 * (wg_slots + value_slots), stream, &slots);
+  if (ce != hipSuccess) return ce;
   unsigned long long* xchg = reinterpret_cast<unsigned long long*>(slots);
   // more than half the LDS, so that a CU holds one workgroup
   const size_t lds_launch = lds < 81 * 1024 ? 81 * 1024 : lds;

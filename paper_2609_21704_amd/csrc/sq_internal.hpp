@@ -9,14 +9,17 @@
 namespace sq {
 
 // Library-owned device workspace of at least `bytes` bytes on the current
-// device (grown on demand, never shrunk).  Returns nullptr on failure.
-void* workspace(size_t bytes);
+// device, in *out.  It only grows; a buffer it outgrows stays allocated until
+// the process ends (graphs captured earlier may still use it).  Growing is
+// refused while `stream` is being captured (hipErrorStreamCaptureUnsupported);
+// hipErrorOutOfMemory when the allocation fails.
+hipError_t workspace(size_t bytes, hipStream_t stream, void** out);
 
 // At least `count` int32 counters on the current device that are zero
-// between launches: zeroed when allocated (grown on demand, never shrunk);
-// every kernel that counts on them returns them to zero before it ends.
-// Returns nullptr on failure.
-int32_t* zeroed_counters(size_t count);
+// between launches, in *out: zeroed on `stream` when allocated (same growth
+// rules as the workspace); every kernel that counts on them returns them to
+// zero before it ends.
+hipError_t zeroed_counters(size_t count, hipStream_t stream, int32_t** out);
 
 // Compute units of the current device (cached per device).
 int cu_count();

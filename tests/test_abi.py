@@ -12,7 +12,7 @@ import paper_2609_21704_amd as sq
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "specquant.h")
 
-OK, NULL, SHAPE, ALIGN, ALIAS, VALUE = 0, 1, 2, 3, 4, 5
+OK, NULL, SHAPE, ALIGN, ALIAS, NONFINITE, UNSUPPORTED, DEVICE, CAPTURE = 0, 1, 2, 3, 4, 5, 6, 7, 8
 A = 0x7F0000000000          # 16-byte aligned fake addresses, far apart
 B = A + (1 << 32)
 C = A + (2 << 32)
@@ -34,9 +34,10 @@ def test_library_exports_every_declared_symbol():
                           "sq_probe_stream_read"}
     for n in names:
         assert hasattr(lib, n), n
-    assert sq.sq_abi_version() == 1
-    for s in range(7):
+    assert sq.sq_abi_version() == 2
+    for s in range(9):
         assert lib.sq_status_str(s).startswith(b"SQ_")
+    assert lib.sq_status_str(9) == b"unknown sq_status"
 
 
 def test_quantize_validation():
@@ -63,7 +64,7 @@ def test_gemv_gemm_validation():
     assert w4(A, 0, 256, B, C, D, 10, E, F32, None) == SHAPE
     assert w4(A, 1, 200, B, C, D, 10, E, F32, None) == SHAPE
     assert w4(A, 1, 256, B, C, D, 0, E, F32, None) == SHAPE
-    assert w4(A, 1, 256, B, C, D, 10, E, 7, None) == VALUE
+    assert w4(A, 1, 256, B, C, D, 10, E, 7, None) == UNSUPPORTED
     assert w4(A + 8, 1, 256, B, C, D, 10, E, F32, None) == ALIGN
     assert w4(A, 1, 256, B, C, D, 10, E + 2, F32, None) == ALIGN
     assert w4(A, 1, 256, B, C, D, 10, A + 64, F32, None) == ALIAS   # y overlaps x
@@ -91,9 +92,10 @@ def test_accept_validation():
     assert acc(None, B, None, D, 1 << 24, 0, 1, 1.0, E, E + (1 << 26), None, None, None) == SHAPE
     assert acc(None, B, None, D, 1 << 23, 0, 4097, 1.0, E, E + (1 << 25), None, None, None) == SHAPE
     assert acc(A, B, C, D, 1, 1, (1 << 26) + 1, 1.0, E, E + 64, None, None, None) == SHAPE
-    assert acc(A, B, C, D, 1, 4, 100, -1.0, E, E + 64, None, None, None) == VALUE
-    assert acc(A, B, C, D, 1, 4, 100, float("nan"), E, E + 64, None, None, None) == VALUE
-    assert acc(A, B, C, D, 1, 4, 100, 0.0, E, E + 64, E + 128, None, None) == VALUE
+    assert acc(A, B, C, D, 1, 4, 100, -1.0, E, E + 64, None, None, None) == UNSUPPORTED
+    assert acc(A, B, C, D, 1, 4, 100, float("nan"), E, E + 64, None, None, None) == NONFINITE
+    assert acc(A, B, C, D, 1, 4, 100, float("inf"), E, E + 64, None, None, None) == NONFINITE
+    assert acc(A, B, C, D, 1, 4, 100, 0.0, E, E + 64, E + 128, None, None) == UNSUPPORTED
     assert acc(A, B, C, D, 1, 4, 100, 1.0, E + 2, E + 64, None, None, None) == ALIGN
     assert acc(A, B, C, D, 1, 4, 100, 1.0, E, E, None, None, None) == ALIAS
     assert acc(A, B, C, D, 1, 4, 100, 1.0, E, E + 64, None, B + 40, None) == ALIAS

@@ -12,9 +12,10 @@ build every layer:
     and last) of every other matrix.  At 36 verify rows (workload 3) the fp64
     oracle GEMM over whole matrices would take minutes, so there the verify
     GEMM is checked on 256 seeded rows of every matrix.
-Two whole rounds then run through the driver, and their draft draws and
-accept steps are checked bit for bit against the oracle on the rounds' own
-logits and uniforms."""
+Two whole rounds then run through the driver.  Their draft draws and accept
+steps are checked bit for bit against the oracle run on the kernels' own fp32
+distributions, and end to end against the oracle's own softmax of the
+rounds' logits up to counted near-ties (none expected)."""
 import numpy as np
 import pytest
 import torch
@@ -24,6 +25,7 @@ import paper_2609_21704_amd as sq
 from paper_2609_21704_amd import synth
 from paper_2609_21704_amd.configs import CONFIGS
 from paper_2609_21704_amd.rounds import DirectDecode, Round, Stack, round_uniforms
+from accept_compare import check_accept
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -114,13 +116,29 @@ def check_round(rnd: Round, round_index: int):
     tokens = b.draft_tokens.cpu().numpy()
     u_d = b.u_draft.cpu().numpy().view(np.uint32)
     u_a = b.u_accept.cpu().numpy().view(np.uint32)
+    dev = b.n_accepted.device
     for i in range(k):  # draft draw i: a plain sampler over draft row i
-        _, nxt, _, _ = oracle.spec_accept(None, draft[i].reshape(B, 1, V), None, u_d[i].reshape(B, 1), T)
-        assert np.array_equal(nxt, tokens[i]), ("draft draw", i)
-    n_ref, t_ref, _, _ = oracle.spec_accept(draft, target, tokens, u_a if T > 0 else None, T)
-    assert np.array_equal(b.n_accepted.cpu().numpy(), n_ref)
-    assert np.array_equal(b.next_token.cpu().numpy(), t_ref)
-    return n_ref
+        if T > 0:
+            p_i = torch.empty((B, 1, V), dtype=torch.float32, device=dev)
+            n_i, t_i = sq.sq_spec_accept(None, b.draft_logits[i].view(B, 1, V), None, b.u_draft[i].view(B, 1), T,
+                                         p_out=p_i)
+            assert np.array_equal(t_i.cpu().numpy(), tokens[i]), ("draft draw", i)
+            check_accept(None, draft[i].reshape(B, 1, V), np.zeros((0, B), np.int32), u_d[i].reshape(B, 1), T,
+                         n_i.cpu().numpy(), tokens[i], None, p_i.cpu().numpy())
+        else:
+            check_accept(None, draft[i].reshape(B, 1, V), np.zeros((0, B), np.int32), None, T,
+                         np.zeros(B, np.int32), tokens[i])
+    n_gpu, t_gpu = b.n_accepted.cpu().numpy(), b.next_token.cpu().numpy()
+    if T > 0:  # the accept step again with its distributions, to check it on the kernel's own p / q
+        q_o = torch.empty((k, B, V), dtype=torch.float32, device=dev)
+        p_o = torch.empty((B, k + 1, V), dtype=torch.float32, device=dev)
+        n2, t2 = sq.sq_spec_accept(b.draft_logits, b.target_logits, b.draft_tokens, b.u_accept, T, q_out=q_o,
+                                   p_out=p_o)
+        assert np.array_equal(n2.cpu().numpy(), n_gpu) and np.array_equal(t2.cpu().numpy(), t_gpu)
+        check_accept(draft, target, tokens, u_a, T, n_gpu, t_gpu, q_o.cpu().numpy(), p_o.cpu().numpy())
+    else:
+        check_accept(draft, target, tokens, None, T, n_gpu, t_gpu)
+    return n_gpu
 
 
 @pytest.mark.parametrize("variant", ["int4", "fp8"])
@@ -221,8 +239,11 @@ def test_direct_decode_matches_oracle(index):
         assert err <= GEMV_TOL, err
     B, V = cfg.batch, cfg.vocab
     logits = dd.logits.cpu().numpy().reshape(B, 1, V)
-    _, t_ref, _, _ = oracle.spec_accept(None, logits, None, dd.u.cpu().numpy().view(np.uint32), 1.0)
-    assert np.array_equal(dd.token.cpu().numpy(), t_ref)
+    p_o = torch.empty((B, 1, V), dtype=torch.float32, device=DEV)   # the same draw again, with its distribution
+    n2, t2 = sq.sq_spec_accept(None, dd.logits.view(B, 1, V), None, dd.u, 1.0, p_out=p_o)
+    assert torch.equal(t2, dd.token) and torch.equal(n2, dd.n_accepted)
+    check_accept(None, logits, np.zeros((0, B), np.int32), dd.u.cpu().numpy(), 1.0, dd.n_accepted.cpu().numpy(),
+                 dd.token.cpu().numpy(), None, p_o.cpu().numpy())
     eager = dd.token.clone()
     dd.capture()
     for _ in range(3):

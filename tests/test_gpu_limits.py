@@ -6,6 +6,7 @@ import torch
 
 import oracle
 import paper_2609_21704_amd as sq
+from accept_compare import check_accept
 from paper_2609_21704_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -59,21 +60,24 @@ def test_spec_accept_largest_vocabulary():
     target = synth.normal_f32((b, kd + 1, v), 2.0, 38)
     target[:, :kd] += draft.permute(1, 0, 2)
     tok = torch.tensor([[v - 5]], dtype=torch.int32)
+    q_out = torch.empty((kd, b, v), dtype=torch.float32, device=DEV)
+    p_out = torch.empty((b, kd + 1, v), dtype=torch.float32, device=DEV)
     for u in (0, 1 << 23, (1 << 24) - 1):
         u24 = torch.tensor([[u, (u * 7 + 12345) & 0xFFFFFF]], dtype=torch.int32)
-        n, t = sq.sq_spec_accept(draft.to(DEV), target.to(DEV), tok.to(DEV), u24.to(DEV), 1.0)
-        n_ref, t_ref, _, _ = oracle.spec_accept(draft.numpy(), target.numpy(), tok.numpy(),
-                                                u24.numpy().view(np.uint32), 1.0)
-        assert np.array_equal(n.cpu().numpy(), n_ref) and np.array_equal(t.cpu().numpy(), t_ref)
+        n, t = sq.sq_spec_accept(draft.to(DEV), target.to(DEV), tok.to(DEV), u24.to(DEV), 1.0,
+                                 q_out=q_out, p_out=p_out)
+        check_accept(draft.numpy(), target.numpy(), tok.numpy(), u24.numpy(), 1.0, n.cpu().numpy(),
+                     t.cpu().numpy(), q_out.cpu().numpy(), p_out.cpu().numpy())
 
 
 def test_spec_accept_most_sequences():
     b, kd, v = (1 << 24) - 1, 0, 3
     target = synth.normal_f32((b, 1, v), 2.0, 39)
     u24 = synth.uniform_u24((b, 1), 40)
-    n, t = sq.sq_spec_accept(None, target.to(DEV), None, u24.to(DEV), 1.0)
-    n_ref, t_ref, _, _ = oracle.spec_accept(None, target.numpy(), None, u24.numpy().view(np.uint32), 1.0)
-    assert np.array_equal(n.cpu().numpy(), n_ref) and np.array_equal(t.cpu().numpy(), t_ref)
+    p_out = torch.empty((b, 1, v), dtype=torch.float32, device=DEV)
+    n, t = sq.sq_spec_accept(None, target.to(DEV), None, u24.to(DEV), 1.0, p_out=p_out)
+    check_accept(None, target.numpy(), np.zeros((0, b), np.int32), u24.numpy(), 1.0, n.cpu().numpy(),
+                 t.cpu().numpy(), None, p_out.cpu().numpy())
 
 
 @pytest.mark.parametrize("temp", [1.0, 0.0])

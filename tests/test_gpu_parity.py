@@ -11,6 +11,7 @@ from scipy import special, stats
 import oracle
 import paper_2609_21704_amd as sq
 from paper_2609_21704_amd import synth
+from accept_compare import check_accept
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -307,13 +308,93 @@ ACCEPT_CASES = [
 @pytest.mark.parametrize("b,kd,v,temp", ACCEPT_CASES)
 @pytest.mark.parametrize("token_mode", ["sampled", "uniform"])
 def test_spec_accept_parity(b, kd, v, temp, token_mode):
+    """Decisions and draws bit-exact against the oracle run on the kernel's
+    own fp32 distributions; end to end against the oracle's own softmax up to
+    counted near-ties; the same bits without q_out / p_out."""
     temp = float(np.float32(temp))
     draft, target, tok, u24 = _accept_case(b, kd, v, 100 + b + kd, temp, token_mode)
-    n, t, _, _ = _run_accept(draft, target, tok, u24, temp)
-    n_ref, t_ref, _, _ = oracle.spec_accept(draft.numpy(), target.numpy(), tok.numpy(),
-                                            u24.numpy().view(np.uint32), temp)
-    assert np.array_equal(n, n_ref)
-    assert np.array_equal(t, t_ref)
+    n, t, q_out, p_out = _run_accept(draft, target, tok, u24, temp, want_pq=True)
+    check_accept(draft.numpy(), target.numpy(), tok.numpy(), u24.numpy(), temp, n, t,
+                 q_out.cpu().numpy() if q_out is not None else None, p_out.cpu().numpy())
+    n2, t2, _, _ = _run_accept(draft, target, tok, u24, temp)
+    assert np.array_equal(n, n2) and np.array_equal(t, t2)
+
+
+def test_spec_accept_zero_residual_falls_back_to_p_n():
+    """Rejections that leave no residual mass on the 2^-60 grid: a drafted
+    token outside [0, v) or masked in both rows (p(x) = q(x) = 0), with the
+    parent's row equal to the draft's row, so max(0, p - q) = 0 everywhere and
+    the token is drawn from p_n.  Other sequences keep the ordinary path."""
+    b, kd, v = 12, 4, 9000
+    draft, target, tok, u24 = _accept_case(b, kd, v, 61, 1.0, "uniform")
+    for s in range(b):
+        i = s % kd
+        target[s, i] = draft[i, s]
+        if s % 3 == 0:
+            tok[i, s] = -1 if s % 2 else v
+        elif s % 3 == 1:
+            draft[i, s, 17] = -np.inf
+            target[s, i, 17] = -np.inf
+            tok[i, s] = 17
+        # s % 3 == 2: an ordinary sequence whose row i happens to equal the draft
+        for j in range(i):
+            target[s, j] = draft[j, s]          # earlier positions: p = q, always accepted
+    n, t, q_out, p_out = _run_accept(draft, target, tok, u24, 1.0, want_pq=True)
+    check_accept(draft.numpy(), target.numpy(), tok.numpy(), u24.numpy(), 1.0, n, t,
+                 q_out.cpu().numpy(), p_out.cpu().numpy())
+    for s in range(b):
+        if s % 3 != 2:
+            assert n[s] == s % kd
+            assert 0 <= t[s] < v and np.isfinite(target[s, n[s], t[s]].item())
+
+
+def test_spec_accept_masked_chunks():
+    """-inf logits over whole 4096-logit chunks and scattered tokens: masked
+    tokens get probability 0 and are never emitted; rows of masked chunks
+    merge like the oracle's softmax."""
+    b, kd, v = 6, 3, 20000
+    draft, target, tok, u24 = _accept_case(b, kd, v, 67, 1.0, "uniform")
+    target[0, 0, 4096:8192] = -np.inf        # one whole chunk
+    target[1, :, :12288] = -np.inf           # three whole chunks of every target row
+    draft[:, 2, 8192:] = -np.inf             # every chunk but the first two of the draft rows
+    target[3, 1, ::3] = -np.inf              # scattered
+    draft[2, 4, 12288:16384] = -np.inf
+    target[5, 3, :19999] = -np.inf           # a bonus row with one finite logit
+    tok[0, 1] = 5                            # masked in the parent: always rejected
+    n, t, q_out, p_out = _run_accept(draft, target, tok, u24, 1.0, want_pq=True)
+    check_accept(draft.numpy(), target.numpy(), tok.numpy(), u24.numpy(), 1.0, n, t,
+                 q_out.cpu().numpy(), p_out.cpu().numpy())
+    _, _, q_ref, p_ref = oracle.spec_accept(draft.numpy(), target.numpy(), tok.numpy(),
+                                            u24.numpy().view(np.uint32), 1.0, want_pq=True)
+    assert np.max(np.abs(p_out.cpu().numpy() - p_ref)) <= PROB_TOL
+    assert np.max(np.abs(q_out.cpu().numpy() - q_ref)) <= PROB_TOL
+    assert np.all(p_out.cpu().numpy()[np.isinf(target.numpy())] == 0)
+    assert n[1] == 0 and all(np.isfinite(target[s, n[s], t[s]].item()) for s in range(b))
+
+
+@pytest.mark.parametrize("temp", [1.0, 0.0])
+def test_spec_accept_rows_without_a_distribution(temp):
+    """A NaN or +inf logit, or a row with no finite logit, makes its sequence
+    return n_accepted = next_token = -1 (NaN rows in p_out / q_out); the other
+    sequences are unaffected."""
+    b, kd, v = 8, 2, 5000
+    draft, target, tok, u24 = _accept_case(b, kd, v, 71, 1.0, "uniform")
+    target[1, 2, 4500] = float("nan")
+    target[2, 0, 7] = float("inf")
+    target[3, 1, :] = -np.inf
+    draft[1, 4, 100] = float("nan")          # draft rows matter only at T > 0
+    draft[0, 5, :] = -np.inf
+    target[6, 0, :4096] = -np.inf            # a masked chunk only: valid
+    want = temp > 0
+    n, t, q_out, p_out = _run_accept(draft, target, tok, u24, temp, want_pq=want)
+    check_accept(draft.numpy(), target.numpy(), tok.numpy(), u24.numpy(), temp, n, t,
+                 q_out.cpu().numpy() if want else None, p_out.cpu().numpy() if want else None)
+    bad = [1, 2, 3, 4, 5] if temp > 0 else [1, 2, 3]
+    assert all(n[s] == -1 and t[s] == -1 for s in bad)
+    assert all(n[s] >= 0 and t[s] >= 0 for s in range(b) if s not in bad)
+    if want:
+        assert np.all(np.isnan(p_out[1, 2].cpu().numpy())) and np.all(np.isnan(q_out[1, 4].cpu().numpy()))
+        assert not np.any(np.isnan(p_out[6].cpu().numpy()))
 
 
 @pytest.mark.parametrize("b,kd,v,temp", [(1, 4, 4096, 1.0), (4, 8, 151936, 1.0), (3, 0, 1000, 0.8)])
@@ -326,7 +407,8 @@ def test_spec_accept_probabilities(b, kd, v, temp):
     assert np.max(np.abs(p_out.cpu().numpy() - p_ref)) <= PROB_TOL
     if kd > 0:
         assert np.max(np.abs(q_out.cpu().numpy() - q_ref)) <= PROB_TOL
-    assert np.array_equal(n, n_ref) and np.array_equal(t, t_ref)
+    check_accept(draft.numpy(), target.numpy(), tok.numpy(), u24.numpy(), temp, n, t,
+                 q_out.cpu().numpy() if kd > 0 else None, p_out.cpu().numpy())
 
 
 @pytest.mark.parametrize("b,kd,v", [(5, 4, 4096), (3, 0, 100), (200, 3, 50), (2, 8, 151936)])
@@ -351,10 +433,9 @@ def test_spec_accept_edge_tokens_and_equal_distributions():
     target[3, :kd] = draft[:, 3]                     # p = q for sequence 3: all accepted
     u24[4] = (1 << 24) - 1
     u24[5] = 0
-    n, t, _, _ = _run_accept(draft, target, tok, u24, 1.0)
-    n_ref, t_ref, _, _ = oracle.spec_accept(draft.numpy(), target.numpy(), tok.numpy(),
-                                            u24.numpy().view(np.uint32), 1.0)
-    assert np.array_equal(n, n_ref) and np.array_equal(t, t_ref)
+    n, t, q_out, p_out = _run_accept(draft, target, tok, u24, 1.0, want_pq=True)
+    check_accept(draft.numpy(), target.numpy(), tok.numpy(), u24.numpy(), 1.0, n, t,
+                 q_out.cpu().numpy(), p_out.cpu().numpy())
     assert n[0] == 0 and n[3] == kd
 
 
