@@ -166,6 +166,28 @@ sq_status sq_spec_accept(const float* draft_logits, const float* target_logits,
                          int32_t v, float temperature, int32_t* n_accepted, int32_t* next_token,
                          float* q_out, float* p_out, hipStream_t stream);
 
+/* The accept call of sq_spec_accept for callers that cannot allocate device
+ * memory: code under HIP graph capture, serving loops and harnesses that
+ * forbid allocation.  Same arguments, kernels and results as sq_spec_accept,
+ * but the call allocates nothing: its scratch (row statistics, chunk weights,
+ * per-sequence state) is a static device array of SQ_NOALLOC_SCRATCH_BYTES
+ * per GPU, held by the library until the process ends.  A call needs
+ *   T > 0: 16 * (b * (2 kd + 1) * C) + 16 * (b * C) + 40 * b bytes,
+ *   T = 0: 8 * (b * (kd + 1) * C) bytes, C = ceil(v / 4096),
+ * each term rounded up to a multiple of 256 (the 40 b term excepted); a call
+ * that needs more than SQ_NOALLOC_SCRATCH_BYTES returns SQ_ERR_SHAPE and
+ * enqueues nothing (e.g. 4 sequences, kd = 8, v = 151936 need 44 KB; 256
+ * sequences at kd = 8 need 2.8 MB).  Every call on a GPU shares that GPU's
+ * array, and nothing in it needs to start at zero; calls that overlap on one
+ * GPU (concurrently running streams) race on it, so order them on one
+ * stream. */
+#define SQ_NOALLOC_SCRATCH_BYTES (4u << 20)
+sq_status sq_spec_accept_noalloc(const float* draft_logits, const float* target_logits,
+                                 const int32_t* draft_tokens, const uint32_t* u24, int32_t b,
+                                 int32_t kd, int32_t v, float temperature, int32_t* n_accepted,
+                                 int32_t* next_token, float* q_out, float* p_out,
+                                 hipStream_t stream);
+
 /* Streaming-read probe (a measurement aid beside the method, not one of its
  * steps): reads `bytes` bytes of src once with 16-byte loads in grid-stride
  * order and nothing else, so that the duration of the call on the stream is a

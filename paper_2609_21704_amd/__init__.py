@@ -19,5 +19,6 @@ from ._lib import (  # noqa: F401
     sq_quantize_int4_g128,
     sq_probe_stream_read,
     sq_spec_accept,
+    sq_spec_accept_noalloc,
     sq_verify_gemm_f16,
 )

@@ -52,6 +52,7 @@ def load() -> ctypes.CDLL:
             "sq_qgemv_w8a16": ([P, I64, I64, P, P, I64, P, S, P], S),
             "sq_verify_gemm_f16": ([P, I64, I64, P, I64, P, S, P], S),
             "sq_spec_accept": ([P, P, P, P, I32, I32, I32, F, P, P, P, P, P], S),
+            "sq_spec_accept_noalloc": ([P, P, P, P, I32, I32, I32, F, P, P, P, P, P], S),
             "sq_probe_stream_read": ([P, I64, P, P], S),
         }
         for name, (args, res) in sigs.items():
@@ -64,7 +65,7 @@ def load() -> ctypes.CDLL:
 
 EXPORTED = ("sq_abi_version", "sq_status_str", "sq_quantize_int4_g128", "sq_quantize_fp8_e4m3",
             "sq_qgemv_w4a16", "sq_qgemv_w8a16", "sq_verify_gemm_f16", "sq_spec_accept",
-            "sq_probe_stream_read")
+            "sq_spec_accept_noalloc", "sq_probe_stream_read")
 
 
 def _ptr(t):
@@ -201,7 +202,7 @@ def sq_verify_gemm_f16(x, w16, y=None, y_dtype=torch.float32):
 
 
 def sq_spec_accept(draft_logits, target_logits, draft_tokens, u24, temperature: float = 1.0,
-                   n_accepted=None, next_token=None, q_out=None, p_out=None):
+                   n_accepted=None, next_token=None, q_out=None, p_out=None, _entry="sq_spec_accept"):
     """Speculative accept / resample.
 
     draft_logits [kd][b][v] f32 (None when kd == 0), target_logits [b][kd+1][v] f32,
@@ -228,10 +229,23 @@ def sq_spec_accept(draft_logits, target_logits, draft_tokens, u24, temperature: 
         _expect(q_out, torch.float32, (kd, b, v), "q_out")
     if p_out is not None:
         _expect(p_out, torch.float32, (b, kd + 1, v), "p_out")
-    _check(load().sq_spec_accept(_ptr(draft_logits), _ptr(target_logits), _ptr(draft_tokens), _ptr(u24), b, kd, v,
-                                 float(temperature), _ptr(n_accepted), _ptr(next_token), _ptr(q_out), _ptr(p_out),
-                                 _stream(dev)), "sq_spec_accept")
+    fn = getattr(load(), _entry)
+    _check(fn(_ptr(draft_logits), _ptr(target_logits), _ptr(draft_tokens), _ptr(u24), b, kd, v, float(temperature),
+              _ptr(n_accepted), _ptr(next_token), _ptr(q_out), _ptr(p_out), _stream(dev)), _entry)
     return n_accepted, next_token
+
+
+NOALLOC_SCRATCH_BYTES = 4 << 20  # SQ_NOALLOC_SCRATCH_BYTES
+
+
+def sq_spec_accept_noalloc(draft_logits, target_logits, draft_tokens, u24, temperature: float = 1.0,
+                           n_accepted=None, next_token=None, q_out=None, p_out=None):
+    """sq_spec_accept without any device allocation by the library (its
+    scratch is a static per-GPU array of NOALLOC_SCRATCH_BYTES); same
+    arguments and results.  Pass n_accepted / next_token (and any q_out /
+    p_out) to keep the call itself free of torch allocations too."""
+    return sq_spec_accept(draft_logits, target_logits, draft_tokens, u24, temperature, n_accepted, next_token,
+                          q_out, p_out, _entry="sq_spec_accept_noalloc")
 
 
 PROBE_SINK_WORDS = 2048  # SQ_PROBE_SINK_WORDS

@@ -12,6 +12,8 @@
 #include "sq_internal.hpp"
 #include "specquant.h"
 
+static_assert(sq::kNoAllocScratchBytes == SQ_NOALLOC_SCRATCH_BYTES, "one size for the static scratch array");
+
 // Large matrices stream through the matrix-core kernel; small ones (where
 // its fixed cost of staging activations and combining chunks, about 4 us more
 // than the others', dominates) and m > 16 use the vector-ALU GEMV and the
@@ -292,9 +294,14 @@ sq_status sq_probe_stream_read(const void* src, int64_t bytes, uint32_t* sink, h
   return device_status(sq::launch_stream_read(src, bytes, sink, SQ_PROBE_SINK_WORDS, stream));
 }
 
-sq_status sq_spec_accept(const float* draft_logits, const float* target_logits, const int32_t* draft_tokens,
-                         const uint32_t* u24, int32_t b, int32_t kd, int32_t v, float temperature,
-                         int32_t* n_accepted, int32_t* next_token, float* q_out, float* p_out, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Host-side validation shared by the two accept entry points.
+sq_status validate_accept(const float* draft_logits, const float* target_logits, const int32_t* draft_tokens,
+                          const uint32_t* u24, int32_t b, int32_t kd, int32_t v, float temperature,
+                          int32_t* n_accepted, int32_t* next_token, float* q_out, float* p_out) {
   if (!target_logits || !n_accepted || !next_token) return SQ_ERR_NULL;
   if (kd > 0 && (!draft_logits || !draft_tokens)) return SQ_ERR_NULL;
   if (b < 1 || b >= (1 << 24) || kd < 0 || kd > 64 || v < 1 || v > (1 << 26)) return SQ_ERR_SHAPE;
@@ -318,9 +325,35 @@ sq_status sq_spec_accept(const float* draft_logits, const float* target_logits, 
                        {draft_tokens, bk * 4},
                        {u24, (size_t)b * (kd + 1) * 4}};
   if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  return SQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sq_status sq_spec_accept(const float* draft_logits, const float* target_logits, const int32_t* draft_tokens,
+                         const uint32_t* u24, int32_t b, int32_t kd, int32_t v, float temperature,
+                         int32_t* n_accepted, int32_t* next_token, float* q_out, float* p_out, hipStream_t stream) {
+  const sq_status st = validate_accept(draft_logits, target_logits, draft_tokens, u24, b, kd, v, temperature,
+                                       n_accepted, next_token, q_out, p_out);
+  if (st != SQ_OK) return st;
   (void)hipGetLastError();
   return device_status(sq::launch_spec_accept(draft_logits, target_logits, draft_tokens, u24, b, kd, v, temperature,
                                               n_accepted, next_token, q_out, p_out, stream));
+}
+
+sq_status sq_spec_accept_noalloc(const float* draft_logits, const float* target_logits, const int32_t* draft_tokens,
+                                 const uint32_t* u24, int32_t b, int32_t kd, int32_t v, float temperature,
+                                 int32_t* n_accepted, int32_t* next_token, float* q_out, float* p_out,
+                                 hipStream_t stream) {
+  const sq_status st = validate_accept(draft_logits, target_logits, draft_tokens, u24, b, kd, v, temperature,
+                                       n_accepted, next_token, q_out, p_out);
+  if (st != SQ_OK) return st;
+  if (sq::spec_accept_scratch_bytes(b, kd, v, temperature) > SQ_NOALLOC_SCRATCH_BYTES) return SQ_ERR_SHAPE;
+  (void)hipGetLastError();
+  return device_status(sq::launch_spec_accept_noalloc(draft_logits, target_logits, draft_tokens, u24, b, kd, v,
+                                                      temperature, n_accepted, next_token, q_out, p_out, stream));
 }
 
 }  // extern "C"

@@ -23,6 +23,8 @@
 // Greedy uses per-chunk (max, first index) pairs and one decision pass.
 #include <math.h>
 
+#include <mutex>
+
 #include "sq_device.hpp"
 #include "sq_internal.hpp"
 
@@ -530,16 +532,40 @@ __global__ __launch_bounds__(kThreads) void greedy_kernel(const int32_t* __restr
 
 }  // namespace
 
-hipError_t launch_spec_accept(const float* draft, const float* target, const int32_t* tokens, const uint32_t* u24,
-                              int b, int kd, int v, float temperature, int32_t* n_accepted, int32_t* next_token,
-                              float* q_out, float* p_out, hipStream_t stream) {
+namespace {
+
+// Scratch of one call: the greedy pairs, or the row statistics, the chunk
+// weights and the per-sequence state (each part 256-byte aligned).
+struct AcceptScratch {
+  size_t st_bytes, zs_bytes, in_bytes;
+  size_t total() const { return st_bytes + zs_bytes + in_bytes; }
+};
+
+AcceptScratch accept_scratch(int b, int kd, int v, float temperature) {
+  const int64_t nchunk = (v + kChunk - 1) / kChunk;
+  const int64_t rows_t = (int64_t)b * (kd + 1);
+  AcceptScratch a;
+  if (temperature == 0.0f) {
+    a.st_bytes = ((size_t)rows_t * nchunk * sizeof(ArgMax) + 255) / 256 * 256;
+    a.zs_bytes = a.in_bytes = 0;
+    return a;
+  }
+  const int64_t rows = rows_t + (int64_t)b * kd;
+  a.st_bytes = ((size_t)rows * nchunk * sizeof(double2) + 255) / 256 * 256;
+  a.zs_bytes = ((size_t)b * nchunk * 2 * sizeof(int64_t) + 255) / 256 * 256;
+  a.in_bytes = (size_t)b * sizeof(SeqInfo);
+  return a;
+}
+
+// The accept kernels on the scratch `ws` (at least accept_scratch().total() bytes).
+hipError_t enqueue_accept(const float* draft, const float* target, const int32_t* tokens, const uint32_t* u24, int b,
+                          int kd, int v, float temperature, int32_t* n_accepted, int32_t* next_token, float* q_out,
+                          float* p_out, char* ws, hipStream_t stream) {
   const int nchunk = (v + kChunk - 1) / kChunk;
   const int64_t rows_t = (int64_t)b * (kd + 1);
+  const AcceptScratch a = accept_scratch(b, kd, v, temperature);
   if (temperature == 0.0f) {
-    void* ws = nullptr;
-    const hipError_t e = workspace((size_t)rows_t * nchunk * sizeof(ArgMax), stream, &ws);
-    if (e != hipSuccess) return e;
-    ArgMax* am = static_cast<ArgMax*>(ws);
+    ArgMax* am = reinterpret_cast<ArgMax*>(ws);
     hipLaunchKernelGGL(argmax_kernel, dim3((unsigned)(rows_t * nchunk)), dim3(kThreads), 0, stream, target, v, nchunk,
                        am);
     hipLaunchKernelGGL(greedy_kernel, dim3((unsigned)b), dim3(kThreads), 0, stream, tokens, b, kd, v, nchunk, am,
@@ -547,16 +573,9 @@ hipError_t launch_spec_accept(const float* draft, const float* target, const int
     return hipGetLastError();
   }
   const int64_t rows = rows_t + (int64_t)b * kd;
-  const size_t st_bytes = ((size_t)rows * nchunk * sizeof(double2) + 255) / 256 * 256;
-  const size_t zs_bytes = ((size_t)b * nchunk * 2 * sizeof(int64_t) + 255) / 256 * 256;
-  const size_t in_bytes = (size_t)b * sizeof(SeqInfo);
-  void* wsp = nullptr;
-  const hipError_t e = workspace(st_bytes + zs_bytes + in_bytes, stream, &wsp);
-  if (e != hipSuccess) return e;
-  char* ws = static_cast<char*>(wsp);
   double2* stats = reinterpret_cast<double2*>(ws);
-  int64_t* zs = reinterpret_cast<int64_t*>(ws + st_bytes);
-  SeqInfo* info = reinterpret_cast<SeqInfo*>(ws + st_bytes + zs_bytes);
+  int64_t* zs = reinterpret_cast<int64_t*>(ws + a.st_bytes);
+  SeqInfo* info = reinterpret_cast<SeqInfo*>(ws + a.st_bytes + a.zs_bytes);
   hipLaunchKernelGGL(stats_kernel, dim3((unsigned)(rows * nchunk)), dim3(kThreads), 0, stream, draft, target, rows_t, v,
                      temperature, nchunk, stats);
   if (p_out || q_out)
@@ -567,6 +586,62 @@ hipError_t launch_spec_accept(const float* draft, const float* target, const int
   hipLaunchKernelGGL(draw_kernel, dim3((unsigned)b), dim3(kThreads), 0, stream, draft, target, u24, b, kd, v,
                      temperature, nchunk, zs, info, n_accepted, next_token);
   return hipGetLastError();
+}
+
+// The scratch of the allocation-free entry point: one static array per GPU,
+// held until the process ends.  Host code never passes `scratch` itself to a
+// kernel (on the host it names a stand-in, not device memory): it uses the
+// device address taken once per device with hipGetSymbolAddress.
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_addr[kMaxDevices];
+
+hipError_t noalloc_scratch(char** out) {
+  *out = nullptr;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_addr[dev]) {  // first call on this device, which is current
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return e != hipSuccess ? e : hipErrorInvalidSymbol;
+    }
+    g_scratch_addr[dev] = p;
+  }
+  *out = static_cast<char*>(g_scratch_addr[dev]);
+  return hipSuccess;
+}
+
+}  // namespace
+
+size_t spec_accept_scratch_bytes(int b, int kd, int v, float temperature) {
+  return accept_scratch(b, kd, v, temperature).total();
+}
+
+hipError_t launch_spec_accept(const float* draft, const float* target, const int32_t* tokens, const uint32_t* u24,
+                              int b, int kd, int v, float temperature, int32_t* n_accepted, int32_t* next_token,
+                              float* q_out, float* p_out, hipStream_t stream) {
+  void* ws = nullptr;
+  const hipError_t e = workspace(accept_scratch(b, kd, v, temperature).total(), stream, &ws);
+  if (e != hipSuccess) return e;
+  return enqueue_accept(draft, target, tokens, u24, b, kd, v, temperature, n_accepted, next_token, q_out, p_out,
+                        static_cast<char*>(ws), stream);
+}
+
+hipError_t launch_spec_accept_noalloc(const float* draft, const float* target, const int32_t* tokens,
+                                      const uint32_t* u24, int b, int kd, int v, float temperature,
+                                      int32_t* n_accepted, int32_t* next_token, float* q_out, float* p_out,
+                                      hipStream_t stream) {
+  if (accept_scratch(b, kd, v, temperature).total() > kNoAllocScratchBytes) return hipErrorInvalidValue;
+  char* ws = nullptr;
+  const hipError_t e = noalloc_scratch(&ws);
+  if (e != hipSuccess) return e;
+  return enqueue_accept(draft, target, tokens, u24, b, kd, v, temperature, n_accepted, next_token, q_out, p_out, ws,
+                        stream);
 }
 
 }  // namespace sq

@@ -65,4 +65,18 @@ hipError_t launch_spec_accept(const float* draft, const float* target, const int
                               int b, int kd, int v, float temperature, int32_t* n_accepted, int32_t* next_token,
                               float* q_out, float* p_out, hipStream_t stream);
 
+// Bytes of scratch one accept call needs (workspace or static array).
+size_t spec_accept_scratch_bytes(int b, int kd, int v, float temperature);
+
+// Size of the static scratch array of the allocation-free accept call.
+constexpr size_t kNoAllocScratchBytes = size_t(4) << 20;
+
+// The accept call on the static scratch array of the current device (no
+// allocation); hipErrorInvalidValue when the call needs more than
+// kNoAllocScratchBytes (the C ABI checks that first).
+hipError_t launch_spec_accept_noalloc(const float* draft, const float* target, const int32_t* tokens,
+                                      const uint32_t* u24, int b, int kd, int v, float temperature,
+                                      int32_t* n_accepted, int32_t* next_token, float* q_out, float* p_out,
+                                      hipStream_t stream);
+
 }  // namespace sq

@@ -31,7 +31,8 @@ def test_library_exports_every_declared_symbol():
     names = declared_symbols()
     assert set(names) == {"sq_abi_version", "sq_status_str", "sq_quantize_int4_g128", "sq_quantize_fp8_e4m3",
                           "sq_qgemv_w4a16", "sq_qgemv_w8a16", "sq_verify_gemm_f16", "sq_spec_accept",
-                          "sq_probe_stream_read"}
+                          "sq_spec_accept_noalloc", "sq_probe_stream_read"}
+    assert set(names) == set(sq.EXPORTED)
     for n in names:
         assert hasattr(lib, n), n
     assert sq.sq_abi_version() == 2
@@ -99,6 +100,25 @@ def test_accept_validation():
     assert acc(A, B, C, D, 1, 4, 100, 1.0, E + 2, E + 64, None, None, None) == ALIGN
     assert acc(A, B, C, D, 1, 4, 100, 1.0, E, E, None, None, None) == ALIAS
     assert acc(A, B, C, D, 1, 4, 100, 1.0, E, E + 64, None, B + 40, None) == ALIAS
+
+
+def test_accept_noalloc_validation():
+    """The allocation-free accept call validates like sq_spec_accept and
+    rejects, on the host, calls whose scratch exceeds its static array."""
+    lib = sq.load()
+    acc, na = lib.sq_spec_accept, lib.sq_spec_accept_noalloc
+    cases = [(A, None, C, D, 1, 4, 100, 1.0, E, E + 64, None, None, None),
+             (A, B, C, D, 0, 4, 100, 1.0, E, E + 64, None, None, None),
+             (A, B, C, D, 1, 4, 100, float("nan"), E, E + 64, None, None, None),
+             (A, B, C, D, 1, 4, 100, 0.0, E, E + 64, E + 128, None, None),
+             (A, B, C, D, 1, 4, 100, 1.0, E + 2, E + 64, None, None, None),
+             (A, B, C, D, 1, 4, 100, 1.0, E, E, None, None, None)]
+    for c in cases:
+        assert na(*c) == acc(*c) != OK
+    # 256 sequences at kd = 8 over 151936 logits need 2.8 MB: within the 4 MiB array (not launched here);
+    # 400 need 4.4 MB: rejected before any HIP call
+    assert na(A, B, C, D, 400, 8, 151936, 1.0, E, E + 4096, None, None, None) == SHAPE
+    assert na(None, B, None, D, 300000, 0, 1, 1.0, E, E + (1 << 21), None, None, None) == SHAPE   # 16.8 MB
 
 
 def test_probe_validation():
