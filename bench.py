@@ -31,7 +31,10 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, GB/s
 METRIC = "draft+verify tokens/s at Qwen2.5-7B shape (k=4); INT4/FP8 GEMV HBM TB/s vs peak"
-GEMV_SRC = os.path.join(ROOT, "paper_2609_21704_amd", "csrc", "gemv.hip")
+CSRC = os.path.join(ROOT, "paper_2609_21704_amd", "csrc")
+# the sources of each draft GEMV variant's kernels (a traffic profile is valid while they are unchanged)
+GEMV_SOURCES = {"int4": ["gemv.hip"], "fp8": ["gemv.hip", "linear.hip"]}
+FP8_CONFIG = 3         # the Qwen2.5-7B-shaped workload with the FP8 draft (m = 4)
 COPY_BYTES = 1 << 30   # the plain copy that calibrates the HBM byte counters
 
 
@@ -228,13 +231,20 @@ def per_shape(cfg, rot_bytes: int = 3 << 30, iters: int = 40):
     return rows
 
 
+def sources_sha(variant: str) -> str:
+    h = hashlib.sha256()
+    for f in GEMV_SOURCES[variant]:
+        h.update(open(os.path.join(CSRC, f), "rb").read())
+    return h.hexdigest()
+
+
 def traffic_from_profile(variant: str):
-    """HBM bytes per draft-GEMV launch from the committed rocprofv3 counter
-    summary, if it was taken on the current kernel source; else None."""
+    """HBM bytes per draft-GEMV call from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel sources; else None."""
     path = os.path.join(ROOT, "profiles", f"gemv_{variant}_traffic.txt")
     if not os.path.exists(path):
         return None
-    sha = hashlib.sha256(open(GEMV_SRC, "rb").read()).hexdigest()
+    sha = sources_sha(variant)
     vals = {}
     for line in open(path):
         if "=" in line and not line.startswith("#"):
@@ -331,11 +341,19 @@ def cpu_baseline(rnd, tokens_per_round: float):
     t_single = time.perf_counter() - t0
     oracle.set_num_threads(threads)
     cpu_model = None
-    try:
-        with open("/proc/cpuinfo") as f:
-            cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), None)
-    except OSError:
+    try:  # lscpu's model name, else /proc/cpuinfo's
+        import subprocess
+
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=20).stdout
+        cpu_model = next((l.split(":", 1)[1].strip() for l in out.splitlines() if l.startswith("Model name")), None)
+    except (OSError, subprocess.SubprocessError):
         pass
+    if not cpu_model:
+        try:
+            with open("/proc/cpuinfo") as f:
+                cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), None)
+        except OSError:
+            pass
     return {
         "value": round(tokens_per_round * cfg.batch / round_s, 4),
         "unit": "tokens/s",
@@ -347,6 +365,69 @@ def cpu_baseline(rnd, tokens_per_round: float):
                    f"draft GEMVs, draws, verify GEMMs and the accept step, timed in {measured:.1f} s and "
                    f"extrapolated to {cfg.layers} layers ({round_s:.1f} s per round)"),
     }
+
+
+def expected_tokens(rnd, ud, ua, rounds, n_hist):
+    """The expected tokens per round of each timed round from its own
+    distributions: with draft rows q_j and parent rows p_j fixed in a round,
+    position j is accepted with probability beta_j = sum_x min(p_j(x), q_j(x))
+    independently of the others, so E[n + 1] = 1 + sum_{i=1..k} prod_{j<i} beta_j.
+    Each round is run again eagerly with its uniforms (its n_accepted must equal
+    the timed replay's), and its accept step once more with q_out / p_out."""
+    import torch
+
+    from paper_2609_21704_amd import sq_spec_accept
+
+    cfg, b = rnd.cfg, rnd.buf
+    B, k, V = cfg.batch, cfg.k, cfg.vocab
+    q = torch.empty((k, B, V), dtype=torch.float32, device=b.n_accepted.device)
+    p = torch.empty((B, k + 1, V), dtype=torch.float32, device=b.n_accepted.device)
+    per_round = []
+    for r in rounds:
+        rnd.set_uniforms(ud[r], ua[r])
+        rnd.run()
+        n2, _ = sq_spec_accept(b.draft_logits, b.target_logits, b.draft_tokens, b.u_accept, rnd.temperature,
+                               q_out=q, p_out=p)
+        if not torch.equal(n2, n_hist[r]) or not torch.equal(b.n_accepted, n_hist[r]):
+            raise RuntimeError(f"round {r} did not reproduce its timed replay")
+        beta = torch.minimum(p[:, :k].double(), q.permute(1, 0, 2).double()).sum(dim=2)   # [B][k]
+        e = 1.0 + torch.cumprod(beta, dim=1).sum(dim=1)                                   # [B]
+        per_round.append(e.mean().item())
+    return sum(per_round) / len(per_round), beta.mean(dim=0).tolist()
+
+
+def measure_fp8(steps: int, dev):
+    """The W8A16 draft GEMVs at m = 4 over the Qwen2.5-7B FP8 workload's shapes
+    (28 layers' projections and the LM head), timed like the INT4 ones."""
+    import torch
+
+    from paper_2609_21704_amd.configs import CONFIGS
+    from paper_2609_21704_amd.rounds import Round, Stack
+
+    cfg = CONFIGS[FP8_CONFIG]
+    stack = Stack(cfg, dev, keep_f16=False)
+    rnd = Round(stack, temperature=1.0)
+    for i in range(cfg.k):  # one untimed pass of every draft step first
+        rnd.draft_step(i)
+    torch.cuda.synchronize()
+    gbytes, gsec, glaunch = measure_gemv(rnd, steps)
+    achieved = gbytes / gsec / 1e9
+    out = {
+        "kernel": f"draft GEMV (W8A16, m={cfg.draft_m})",
+        "workload": cfg.describe(),
+        "bound": "hbm",
+        "achieved": round(achieved, 1),
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "traffic": traffic_from_profile("fp8"),
+        "launches_timed": glaunch,
+        "avg_launch_us": round(gsec / glaunch * 1e6, 3),
+        "algorithmic_bytes_per_launch": round(gbytes / glaunch, 1),
+    }
+    del rnd, stack
+    torch.cuda.empty_cache()
+    return out
 
 
 def measure_direct(stack, temperature: float, steps: int, warmup: int):
@@ -396,6 +477,10 @@ def main():
     ap.add_argument("--profile-only", action="store_true",
                     help="for rocprofv3 counter runs: one eager round, then a plain copy of COPY_BYTES bytes "
                          "(the counter calibration); prints nothing")
+    ap.add_argument("--profile-draft", action="store_true",
+                    help="for rocprofv3 counter runs: one eager pass of every draft step (GEMVs and draws), then "
+                         "the plain copy; prints nothing")
+    ap.add_argument("--no-fp8", action="store_true", help="skip the FP8 draft GEMV roofline block")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -416,12 +501,16 @@ def main():
     if args.per_shape:
         print(json.dumps({"workload": cfg.describe(), "per_shape": per_shape(cfg)}), flush=True)
         return
-    stack = Stack(cfg, dev)
+    stack = Stack(cfg, dev, keep_f16=not args.profile_draft)
     rnd = Round(stack, temperature=args.temperature)
-    if args.profile_only:
+    if args.profile_only or args.profile_draft:
         ud, ua = round_uniforms(cfg, 1, dev)
         rnd.set_uniforms(ud[0], ua[0])
-        rnd.run()
+        if args.profile_draft:
+            for i in range(cfg.k):
+                rnd.draft_step(i)
+        else:
+            rnd.run()
         src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev).fill_(1)
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
@@ -461,6 +550,7 @@ def main():
     tokens = int((n_acc + 1).sum())
     tokens_per_round = tokens / (args.steps * cfg.batch)
 
+    expected, beta = expected_tokens(rnd, ud, ua, range(args.warmup, total), n_hist)
     direct = measure_direct(stack, args.temperature, args.steps, args.warmup)
     gbytes, gsec, glaunch = measure_gemv(rnd, args.gemv_steps)
     achieved = gbytes / gsec / 1e9
@@ -496,6 +586,8 @@ def main():
                      "p10": round(float(np.percentile(round_ms, 10)), 4),
                      "p90": round(float(np.percentile(round_ms, 90)), 4)},
         "tokens_per_round": round(tokens_per_round, 4),
+        "expected_tokens_per_round": round(expected, 4),
+        "acceptance_beta": [round(x, 4) for x in beta],
         "acceptance_rate": round(float(n_acc.sum()) / (args.steps * cfg.batch * cfg.k), 4),
         "round_bytes": cfg.round_bytes(),
         "stack_gbs": round(cfg.round_bytes() * args.steps / elapsed / 1e9, 1),
@@ -519,6 +611,8 @@ def main():
             "frac_of_probe_same_launches": round(achieved / probe["same_launches_gbs"], 4),
         },
     }
+    if not args.no_fp8 and cfg.draft_variant == "int4":
+        out["roofline_fp8"] = measure_fp8(args.gemv_steps, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(rnd, tokens_per_round)
     print(json.dumps(out), flush=True)

@@ -4,10 +4,15 @@
         per-kernel dispatch count and duration (avg / min / max), kernels grouped
         by name and grid size
     python -m paper_2609_21704_amd.prof traffic <FETCH_SIZE dir> <WRITE_SIZE dir> --copy-bytes N
-        HBM bytes per draft-GEMV dispatch from the FETCH_SIZE / WRITE_SIZE
+            [--variant int4|fp8] [--calls C]
+        HBM bytes per draft-GEMV call from the FETCH_SIZE / WRITE_SIZE
         counters, each divided by what the same counter reads, per byte, for the
         plain copy pass over N bytes (read once, written once) that the profiled
-        command dispatches last
+        command dispatches last; the draft-GEMV dispatches of the variant are
+        summed and divided by C calls (default: one call per dispatch)
+    python -m paper_2609_21704_amd.prof gemv <rocprofv3 output dir> --variant int4|fp8 [--calls C]
+        the draft-GEMV dispatches of the variant: count, total and average
+        duration (per call when C is given)
     python -m paper_2609_21704_amd.prof verify <MfmaUtil/MfmaFlopsF16 dir> <FETCH_SIZE dir> <WRITE_SIZE dir>
             --copy-bytes N --m M --layers L --shapes NAME:NxK,... [--lm NxK]
         per verify projection (the verify dispatches of one round, in their
@@ -27,7 +32,26 @@ import re
 import sqlite3
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-GEMV_SRC = os.path.join(ROOT, "paper_2609_21704_amd", "csrc", "gemv.hip")
+CSRC = os.path.join(ROOT, "paper_2609_21704_amd", "csrc")
+# the sources of each draft GEMV variant's kernels, and its dispatches: the
+# GEMV kernels with the variant's weight kind (second template argument: fp8
+# or not), and for FP8 the matrix-core streaming instance (kind 1) that takes
+# the large matrices at m >= 3
+GEMV_SOURCES = {"int4": ["gemv.hip"], "fp8": ["gemv.hip", "linear.hip"]}
+
+
+def is_draft_gemv(name: str, variant: str) -> bool:
+    if name.startswith(("sq::gemv_kernel<", "sq::gemv_rows_kernel<")):
+        fp8 = name.split(",")[1].strip() == "true"
+        return fp8 == (variant == "fp8")
+    return variant == "fp8" and name.startswith("sq::linear_kernel<1,")
+
+
+def sources_sha(variant: str) -> str:
+    h = hashlib.sha256()
+    for f in GEMV_SOURCES[variant]:
+        h.update(open(os.path.join(CSRC, f), "rb").read())
+    return h.hexdigest()
 
 
 def _dbs(path):
@@ -92,30 +116,43 @@ def counter_values(path, counter):
     return rows
 
 
-def traffic(fetch_dir, write_dir, copy_bytes):
+def traffic(fetch_dir, write_dir, copy_bytes, variant="int4", calls=None):
     fetch = counter_values(fetch_dir, "FETCH_SIZE")
     write = counter_values(write_dir, "WRITE_SIZE")
     copy_key = fetch[-1][1]
     f_scale = fetch[-1][2] * 1024.0 / copy_bytes   # counters are in KiB
     w_scale = write[-1][2] * 1024.0 / copy_bytes
-    gemv = ("sq::gemv_kernel", "sq::gemv_rows_kernel")  # the draft GEMV's two kernels
-    f_g = [v * 1024.0 for _, k, v in fetch if k.startswith(gemv)]
-    w_g = [v * 1024.0 for _, k, v in write if k.startswith(gemv)]
-    f_mean = sum(f_g) / len(f_g) / f_scale
-    w_mean = sum(w_g) / len(w_g) / w_scale if w_g else 0.0
-    sha = hashlib.sha256(open(GEMV_SRC, "rb").read()).hexdigest()
+    f_g = [v * 1024.0 for _, k, v in fetch if is_draft_gemv(k, variant)]
+    w_g = [v * 1024.0 for _, k, v in write if is_draft_gemv(k, variant)]
+    n = calls or len(f_g)
+    f_mean = sum(f_g) / n / f_scale
+    w_mean = sum(w_g) / n / w_scale if w_g else 0.0
     return "\n".join([
         f"copy_kernel = {copy_key}",
         f"copy_bytes = {copy_bytes}",
         f"fetch_counter_bytes_per_copied_byte = {f_scale:.6f}",
         f"write_counter_bytes_per_copied_byte = {w_scale:.6f}",
+        f"variant = {variant}",
         f"gemv_dispatches = {len(f_g)}",
-        f"fetch_bytes_per_launch_raw = {sum(f_g) / len(f_g):.1f}",
-        f"write_bytes_per_launch_raw = {sum(w_g) / max(len(w_g), 1):.1f}",
+        f"gemv_calls = {n}",
+        f"fetch_bytes_per_launch_raw = {sum(f_g) / n:.1f}",
+        f"write_bytes_per_launch_raw = {sum(w_g) / n:.1f}",
         f"hbm_read_bytes_per_launch = {f_mean:.1f}",
         f"hbm_write_bytes_per_launch = {w_mean:.1f}",
         f"hbm_bytes_per_launch = {f_mean + w_mean:.1f}",
-        f"gemv_source_sha256 = {sha}",
+        f"gemv_source_sha256 = {sources_sha(variant)}",
+    ])
+
+
+def gemv_trace(path, variant, calls=None):
+    d = [dur for name, _, _, _, dur in kernel_rows(path) if is_draft_gemv(short_name(name), variant)]
+    n = calls or len(d)
+    return "\n".join([
+        f"variant = {variant}",
+        f"gemv_dispatches = {len(d)}",
+        f"gemv_calls = {n}",
+        f"total_ms = {sum(d) / 1e6:.3f}",
+        f"avg_us_per_call = {sum(d) / n / 1e3:.3f}",
     ])
 
 
@@ -213,6 +250,12 @@ def main():
     b.add_argument("fetch_dir")
     b.add_argument("write_dir")
     b.add_argument("--copy-bytes", type=int, required=True)
+    b.add_argument("--variant", default="int4", choices=["int4", "fp8"])
+    b.add_argument("--calls", type=int)
+    g = sub.add_parser("gemv")
+    g.add_argument("path")
+    g.add_argument("--variant", default="int4", choices=["int4", "fp8"])
+    g.add_argument("--calls", type=int)
     c = sub.add_parser("verify")
     c.add_argument("mfma_dir")
     c.add_argument("fetch_dir")
@@ -226,7 +269,9 @@ def main():
     if args.cmd == "stats":
         print(stats(args.path, args.match))
     elif args.cmd == "traffic":
-        print(traffic(args.fetch_dir, args.write_dir, args.copy_bytes))
+        print(traffic(args.fetch_dir, args.write_dir, args.copy_bytes, args.variant, args.calls))
+    elif args.cmd == "gemv":
+        print(gemv_trace(args.path, args.variant, args.calls))
     else:
         shapes = [(part.split(":")[0],) + _nk(part.split(":")[1]) for part in args.shapes.split(",")]
         print(verify(args.mfma_dir, args.fetch_dir, args.write_dir, args.copy_bytes, args.m, args.layers, shapes,

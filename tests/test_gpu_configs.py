@@ -252,3 +252,44 @@ def test_direct_decode_matches_oracle(index):
         assert torch.equal(dd.token, eager)
     del dd, stack
     torch.cuda.empty_cache()
+
+
+def test_round_acceptance_law_from_its_own_distributions():
+    """Over 4000 rounds of workload 0 (its draft and parent rows are the same
+    every round; only the uniforms change), n_accepted follows the closed form
+    P(n = i) = prod_{j<i} beta_j (1 - beta_i), P(n = k) = prod beta, with
+    beta_j = sum_x min(p_j(x), q_j(x)) from the round's own distributions, and
+    the mean tokens per round (n + 1) is within sampling error of
+    1 + sum_{i=1..k} prod_{j<i} beta_j, the figure the benchmark reports."""
+    from scipy import stats
+
+    cfg = CONFIGS[0]
+    B, k, V = cfg.batch, cfg.k, cfg.vocab
+    stack = Stack(cfg, DEV)
+    rnd = Round(stack, temperature=1.0)
+    R = 4000
+    ud, ua = round_uniforms(cfg, R, DEV)
+    rnd.set_uniforms(ud[0], ua[0])
+    rnd.capture()
+    n_hist = torch.empty((R, B), dtype=torch.int32, device=DEV)
+    for r in range(R):
+        rnd.set_uniforms(ud[r], ua[r])
+        rnd.replay()
+        n_hist[r].copy_(rnd.buf.n_accepted)
+    torch.cuda.synchronize()
+    b = rnd.buf
+    q = torch.empty((k, B, V), dtype=torch.float32, device=DEV)
+    p = torch.empty((B, k + 1, V), dtype=torch.float32, device=DEV)
+    sq.sq_spec_accept(b.draft_logits, b.target_logits, b.draft_tokens, b.u_accept, 1.0, q_out=q, p_out=p)
+    pn, qn = p.cpu().numpy().astype(np.float64), q.cpu().numpy().astype(np.float64)
+    beta = np.minimum(pn[0, :k], qn[:, 0]).sum(axis=1)
+    law = np.array([np.prod(beta[:i]) * (1 - beta[i]) for i in range(k)] + [np.prod(beta)])
+    assert abs(law.sum() - 1) < 1e-12
+    n = n_hist.cpu().numpy().ravel()
+    obs = np.bincount(n, minlength=k + 1)
+    chi2 = np.sum((obs - n.size * law) ** 2 / (n.size * law))
+    assert chi2 < stats.chi2.ppf(1 - 1e-3, k), (chi2, obs, n.size * law)
+    expected = 1.0 + np.cumprod(beta).sum()
+    assert abs(expected - (np.arange(k + 1) + 1) @ law) < 1e-12
+    sd = np.sqrt(((np.arange(k + 1) + 1) ** 2) @ law - expected ** 2)
+    assert abs((n + 1).mean() - expected) < 4 * sd / np.sqrt(n.size), ((n + 1).mean(), expected)
