@@ -1,7 +1,9 @@
 """SpecQuant CPU oracle -- test infrastructure only.
 
-A plain fp64 C implementation (``sq_oracle.c``) of what the SpecQuant hot
-path computes, wrapped with ctypes for numpy arrays.  Only the test suite,
+A plain fp64 C implementation (``sq_oracle.c``, and ``sq_decoder.c`` for the
+operations of the decoder layer around the projections) of what the SpecQuant
+hot path computes, wrapped with ctypes for numpy arrays; ``decoder.py``
+composes them into the decoder and the speculative round with its cache.  Only the test suite,
 ``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py`` may use
 it; the product path (the HIP library and its binding) never imports it, and
 it imports nothing from the product path.
@@ -20,7 +22,7 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRC = os.path.join(_HERE, "sq_oracle.c")
+_SRCS = [os.path.join(_HERE, "sq_oracle.c"), os.path.join(_HERE, "sq_decoder.c")]
 _LIB_PATH = os.path.join(_HERE, "libsq_oracle.so")
 _lib = None
 
@@ -32,7 +34,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB_PATH):
         tmp = _LIB_PATH + ".tmp"
         cmd = ["gcc", "-std=c11", "-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
-               "-fPIC", "-shared", "-Wall", _SRC, "-o", tmp, "-lm"]
+               "-fPIC", "-shared", "-Wall", *_SRCS, "-o", tmp, "-lm"]
         subprocess.run(cmd, check=True)
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
@@ -66,6 +68,10 @@ def _load():
         "sqo_softmax": ([P, I64, I64, D, P], ctypes.c_int),
         "sqo_spec_accept": ([P, P, P, P, I32, I32, I32, D, P, P, P, P], ctypes.c_int),
         "sqo_accept_probs": ([P, P, P, P, I32, I32, I32, P, P], ctypes.c_int),
+        "sqo_rmsnorm": ([P, I64, I64, P, D, P], ctypes.c_int),
+        "sqo_rope": ([P, I64, I64, I64, P, D], ctypes.c_int),
+        "sqo_attention": ([P, I64, I64, I64, I64, P, P, I64, P, P], ctypes.c_int),
+        "sqo_silu_mul": ([P, I64, I64, P], ctypes.c_int),
     }
     for name, (args, res) in sigs.items():
         fn = getattr(lib, name)
@@ -265,6 +271,51 @@ def accept_probs(p, q, draft_tokens, u24):
     _check(_load().sqo_accept_probs(_ptr(p), _ptr(q), _ptr(draft_tokens), _ptr(u24), b, kd, v, _ptr(n_acc),
                                     _ptr(nxt)), "accept_probs")
     return n_acc, nxt
+
+
+def rmsnorm(h, w, eps: float) -> np.ndarray:
+    """y = h / sqrt(mean(h^2) + eps) * w per row, fp64 (h [m][d], w [d])."""
+    h = np.ascontiguousarray(np.atleast_2d(h), np.float64)
+    m, d = h.shape
+    w = np.ascontiguousarray(w, np.float64).reshape(d)
+    y = np.zeros((m, d), np.float64)
+    _check(_load().sqo_rmsnorm(_ptr(h), m, d, _ptr(w), float(eps), _ptr(y)), "rmsnorm")
+    return y
+
+
+def rope(x, pos, theta: float) -> np.ndarray:
+    """Rotary embedding of x [n][heads][hd] at positions pos [n] (returns a new array)."""
+    x = np.array(x, np.float64, order="C", copy=True)
+    n, heads, hd = x.shape
+    pos = np.ascontiguousarray(pos, np.int64).reshape(n)
+    _check(_load().sqo_rope(_ptr(x), n, heads, hd, _ptr(pos), float(theta)), "rope")
+    return x
+
+
+def attention(q, kc, vc, pos) -> np.ndarray:
+    """Causal GQA attention of one sequence: q [n][hq][hd], kc / vc [hkv][len][hd],
+    row i attends to positions 0 .. pos[i].  Returns [n][hq][hd] fp64."""
+    q = np.ascontiguousarray(q, np.float64)
+    kc = np.ascontiguousarray(kc, np.float64)
+    vc = np.ascontiguousarray(vc, np.float64)
+    n, hq, hd = q.shape
+    hkv, length, hd2 = kc.shape
+    if vc.shape != kc.shape or hd2 != hd:
+        raise ValueError("attention: cache shapes do not match")
+    pos = np.ascontiguousarray(pos, np.int64).reshape(n)
+    out = np.zeros((n, hq, hd), np.float64)
+    _check(_load().sqo_attention(_ptr(q), n, hq, hkv, hd, _ptr(kc), _ptr(vc), length, _ptr(pos), _ptr(out)),
+           "attention")
+    return out
+
+
+def silu_mul(gu) -> np.ndarray:
+    """g / (1 + exp(-g)) * u with gate | up = the two halves of each row of gu [m][2 I]."""
+    gu = np.ascontiguousarray(np.atleast_2d(gu), np.float64)
+    m, two_i = gu.shape
+    out = np.zeros((m, two_i // 2), np.float64)
+    _check(_load().sqo_silu_mul(_ptr(gu), m, two_i // 2, _ptr(out)), "silu_mul")
+    return out
 
 
 def normalised_error(y_test, y_ref, d_ref) -> float:
