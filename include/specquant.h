@@ -15,6 +15,17 @@
  *   sq_verify_gemm_f16     parent verification y = x . W16^T, m <= 64 rows
  *   sq_spec_accept         LM-head softmax + accept / reject / resample
  *
+ * and the decoder layer around those projections, for the Qwen2.5 family the
+ * paper evaluates (SS IV), with a key/value cache that the round rolls back by
+ * position (SS III-D.4):
+ *
+ *   sq_embed_block_f16     token embedding of a speculative block
+ *   sq_add_rmsnorm_f16     residual add + RMS normalisation
+ *   sq_rope_kv_f16         q|k|v bias + rotary embedding + cache write
+ *   sq_attention_f16       causal grouped-query attention over the cache
+ *   sq_silu_mul_f16        SiLU-gated product of the gate|up projection
+ *   sq_spec_commit         emitted tokens and restart position of a round
+ *
  * Conventions shared by every call
  *   - Matrices are row-major and contiguous.  A weight matrix is W[n][k]
  *     (n output features, k reduction features); activations are x[m][k];
@@ -49,7 +60,7 @@
 extern "C" {
 #endif
 
-#define SQ_ABI_VERSION 2
+#define SQ_ABI_VERSION 3
 
 typedef enum sq_status {
   SQ_OK = 0,
@@ -187,6 +198,112 @@ sq_status sq_spec_accept_noalloc(const float* draft_logits, const float* target_
                                  int32_t kd, int32_t v, float temperature, int32_t* n_accepted,
                                  int32_t* next_token, float* q_out, float* p_out,
                                  hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * The decoder layer (SS III-D.2 / III-D.3 for the Qwen2.5 family of SS IV;
+ * the paper describes neither the layer nor the cache, so these are the
+ * textbook operations of that family).  Activations between calls: the
+ * residual stream h is fp32 [m][hidden]; projection inputs are fp16; the
+ * projection outputs these calls take are fp32 (y_dtype SQ_F32).  Heads are
+ * 128 wide.  Rows come in blocks: row r = s * rows_per_seq + j of sequence s
+ * sits at position pos_base[s] + pos_offset + j (pos_base a device array, so
+ * that a captured graph follows the positions the round moves).
+ *
+ * Key/value cache of one model and layer (caller-owned, fp16):
+ *   keys   k_cache [b][hkv][capacity][128]
+ *   values v_cache [b][hkv][128][capacity]   (position-minor)
+ * capacity % 64 == 0.  A row attends to the positions 0 .. its own position
+ * of its sequence, which must all hold written entries; rolling back a
+ * rejected block is moving pos_base (sq_spec_commit): entries past it are
+ * rewritten before any later row can attend to them.
+ *
+ * Device status word (int32, nullable, caller-owned): the kernels OR these
+ * bits into it for conditions the host cannot see; it is never cleared. */
+#define SQ_DEV_BAD_TOKEN 1 /* a token outside [0, vocab): its row is NaN             */
+#define SQ_DEV_BAD_POS 2   /* a position outside [0, len_bound): nothing written for
+                              that row, its q / attention output NaN                */
+#define SQ_DEV_OVERFLOW 4  /* emitted tokens past out_capacity were not stored      */
+#define SQ_DEV_NO_DIST 8   /* a round with n_accepted < 0: that sequence kept its
+                              state                                                 */
+
+/* Token embedding of a block: h[s][j] = table[tok(s, j)] widened to fp32, with
+ * tok(s, 0) = first[s] and tok(s, 1 + i) = rest[i][s] (rest position-major
+ * [kd][b], as draft_tokens of sq_spec_accept): the pending token followed by
+ * the drafted ones is the block the parent verifies.
+ * table [vocab][hidden] fp16 (16-B aligned), hidden % 8 == 0, hidden <= 65536,
+ * 1 <= vocab < 2^31; first [b]; rest [kd][b] (NULL when kd == 0);
+ * h [b][kd+1][hidden] f32 out (16-B aligned); 1 <= b, 0 <= kd <= 63. */
+sq_status sq_embed_block_f16(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* first,
+                             const int32_t* rest, int32_t b, int32_t kd, float* h, int32_t* status,
+                             hipStream_t stream);
+
+/* Residual add and RMS normalisation (eps inside the root):
+ *   h[i] += delta[i] for every row i (when delta is not NULL);
+ *   x[r] = f16(h[i] / sqrt(mean_c h[i][c]^2 + eps) * w), i = r * group + group - 1,
+ * so group = rows_per_seq normalises only the last row of each sequence (the
+ * row whose logits a draft step needs).  Sum of squares in fp32, the
+ * reciprocal root in fp64.
+ * h [m][hidden] f32 in/out; delta [m][hidden] f32 or NULL; w [hidden] fp16;
+ * x [m / group][hidden] fp16 out.  hidden % 8 == 0, 8 <= hidden <= 65536,
+ * 1 <= m < 2^31, m % group == 0; eps finite, >= 0.  16-B aligned arrays. */
+sq_status sq_add_rmsnorm_f16(float* h, const float* delta, int64_t m, int64_t hidden, const uint16_t* w,
+                             float eps, int32_t group, uint16_t* x, hipStream_t stream);
+
+/* Bias, rotary position embedding and cache write of a block of m = b *
+ * rows_per_seq rows: with u = qkv[r] + bias (fp32; bias NULL for none) split
+ * into hq query heads, hkv key heads and hkv value heads of 128,
+ *   q_out[r][h] = f16(rope(u_q[h], pos)),  k_cache[s][g][pos] = f16(rope(u_k[g], pos)),
+ *   v_cache[s][g][:][pos] = f16(u_v[g]),
+ * rope pairing element t with t + 64 and turning the pair by
+ * pos * theta^(-2t/128) (angle, cosine and sine in fp64, the turn in fp32).
+ * qkv [m][(hq + 2 hkv) * 128] f32; bias [(hq + 2 hkv) * 128] fp16;
+ * pos_base [b]; q_out [m][hq][128] fp16 out; caches as above.
+ * 1 <= hkv <= hq, hq % hkv == 0, hq <= 128; 1 <= rows_per_seq <= 64;
+ * 64 <= capacity < 2^31, capacity % 64 == 0; 1 <= len_bound <= capacity (an
+ * upper bound on every position + 1 of the call); theta > 1 finite.
+ * A row at a position outside [0, len_bound) writes nothing to the caches, gets
+ * NaN in q_out and sets SQ_DEV_BAD_POS. */
+sq_status sq_rope_kv_f16(const float* qkv, const uint16_t* bias, int32_t b, int32_t rows_per_seq, int32_t hq,
+                         int32_t hkv, const int32_t* pos_base, int32_t pos_offset, int64_t len_bound,
+                         int64_t capacity, double theta, uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache,
+                         int32_t* status, hipStream_t stream);
+
+/* Causal grouped-query attention of a block over the cache: for row r of
+ * sequence s at position p and query head h (kv head g = h / (hq / hkv)),
+ *   out[r][h] = f16( sum_{t <= p} e_t v_t / sum_{t <= p} e_t ),
+ *   e_t = exp(q[r][h] . k_t / sqrt(128) - max),
+ * computed per 64-position chunk on the matrix cores (scores in fp32; each
+ * weight e_t enters the product with the values as the sum of two fp16 terms,
+ * accurate to about 2^-22; fp32 sums) and merged in chunk order.  q [m][hq][128] fp16 (as sq_rope_kv_f16 writes it);
+ * out [m][hq][128] fp16 out; limits as sq_rope_kv_f16.  Uses the library
+ * workspace (b * hkv * ceil(len_bound / 64) * 16 ceil(rows_per_seq * hq / hkv
+ * / 16) * 520 bytes).  A row at a position outside [0, len_bound) gets NaN. */
+sq_status sq_attention_f16(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t b,
+                           int32_t rows_per_seq, int32_t hq, int32_t hkv, const int32_t* pos_base,
+                           int32_t pos_offset, int64_t len_bound, int64_t capacity, uint16_t* out,
+                           hipStream_t stream);
+
+/* SiLU-gated product of the fused gate|up projection output:
+ *   t[i][c] = f16(g / (1 + exp(-g)) * u),  g = gu[i][c], u = gu[i][inter + c]  (fp32).
+ * gu [m][2 inter] f32; t [m][inter] fp16 out; 1 <= m, 1 <= inter,
+ * m * inter < 2^40. */
+sq_status sq_silu_mul_f16(const float* gu, int64_t m, int64_t inter, uint16_t* t, hipStream_t stream);
+
+/* Commit of a round (SS III-D.4: the accepted drafts and the corrected or bonus
+ * token are emitted; the rest of the block is removed and decoding restarts
+ * from the emitted token).  Per sequence s with n = n_accepted[s] (0 <= n <= kd):
+ *   out_tokens[s][out_len[s] + i] = draft_tokens[i][s] (i < n), then next_token[s]
+ *     (entries at or past out_capacity are not stored: SQ_DEV_OVERFLOW);
+ *   out_len[s] += n + 1;  prev[s] = n > 0 ? draft_tokens[n - 1][s] : pending[s];
+ *   pending[s] = next_token[s];  pos_base[s] += n + 1.
+ * A sequence with n outside [0, kd] keeps its state (SQ_DEV_NO_DIST).
+ * draft_tokens [kd][b] (NULL when kd == 0); pending, prev, pos_base, out_len [b]
+ * in/out; out_tokens [b][out_capacity] out, NULL to keep no history (then
+ * out_len may be NULL). 1 <= b < 2^24, 0 <= kd <= 64. */
+sq_status sq_spec_commit(const int32_t* n_accepted, const int32_t* next_token, const int32_t* draft_tokens,
+                         int32_t b, int32_t kd, int32_t* pending, int32_t* prev, int32_t* pos_base,
+                         int32_t* out_tokens, int64_t out_capacity, int32_t* out_len, int32_t* status,
+                         hipStream_t stream);
 
 /* Streaming-read probe (a measurement aid beside the method, not one of its
  * steps): reads `bytes` bytes of src once with 16-byte loads in grid-stride

@@ -54,6 +54,12 @@ def load() -> ctypes.CDLL:
             "sq_spec_accept": ([P, P, P, P, I32, I32, I32, F, P, P, P, P, P], S),
             "sq_spec_accept_noalloc": ([P, P, P, P, I32, I32, I32, F, P, P, P, P, P], S),
             "sq_probe_stream_read": ([P, I64, P, P], S),
+            "sq_embed_block_f16": ([P, I64, I64, P, P, I32, I32, P, P, P], S),
+            "sq_add_rmsnorm_f16": ([P, P, I64, I64, P, F, I32, P, P], S),
+            "sq_rope_kv_f16": ([P, P, I32, I32, I32, I32, P, I32, I64, I64, ctypes.c_double, P, P, P, P, P], S),
+            "sq_attention_f16": ([P, P, P, I32, I32, I32, I32, P, I32, I64, I64, P, P], S),
+            "sq_silu_mul_f16": ([P, I64, I64, P, P], S),
+            "sq_spec_commit": ([P, P, P, I32, I32, P, P, P, P, I64, P, P, P], S),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(lib, name)
@@ -65,7 +71,11 @@ def load() -> ctypes.CDLL:
 
 EXPORTED = ("sq_abi_version", "sq_status_str", "sq_quantize_int4_g128", "sq_quantize_fp8_e4m3",
             "sq_qgemv_w4a16", "sq_qgemv_w8a16", "sq_verify_gemm_f16", "sq_spec_accept",
-            "sq_spec_accept_noalloc", "sq_probe_stream_read")
+            "sq_spec_accept_noalloc", "sq_probe_stream_read", "sq_embed_block_f16", "sq_add_rmsnorm_f16",
+            "sq_rope_kv_f16", "sq_attention_f16", "sq_silu_mul_f16", "sq_spec_commit")
+
+# device status bits (SQ_DEV_* of include/specquant.h)
+DEV_BAD_TOKEN, DEV_BAD_POS, DEV_OVERFLOW, DEV_NO_DIST = 1, 2, 4, 8
 
 
 def _ptr(t):
@@ -267,3 +277,131 @@ def sq_probe_stream_read(src: torch.Tensor, nbytes: int | None = None, offset: i
     _check(load().sq_probe_stream_read(src.data_ptr() + offset, nbytes, sink.data_ptr(), _stream(dev)),
            "sq_probe_stream_read")
     return sink
+
+
+# ------------------------------------------------------------ decoder layer
+HEAD_DIM = 128
+
+
+def sq_embed_block_f16(table, first, rest=None, h=None, status=None):
+    """h [b][kd+1][hidden] f32 = table[tokens] for the block (first [b], rest [kd][b])."""
+    vocab, hidden = table.shape
+    b = first.shape[0]
+    kd = 0 if rest is None else rest.shape[0]
+    h = torch.empty((b, kd + 1, hidden), dtype=torch.float32, device=table.device) if h is None else h
+    _dev(table, first, rest, h, status)
+    _expect(table, torch.float16, (vocab, hidden), "table")
+    _expect(first, torch.int32, (b,), "first")
+    if rest is not None:
+        _expect(rest, torch.int32, (kd, b), "rest")
+    if h.dtype != torch.float32 or h.numel() != b * (kd + 1) * hidden:
+        raise ValueError("h must be float32 [b][kd+1][hidden]")
+    _check(load().sq_embed_block_f16(_ptr(table), vocab, hidden, _ptr(first), _ptr(rest), b, kd, _ptr(h),
+                                     _ptr(status), _stream(table.device)), "sq_embed_block_f16")
+    return h
+
+
+def sq_add_rmsnorm_f16(h, w, eps: float, delta=None, group: int = 1, x=None):
+    """h += delta (in place); x = f16(rmsnorm(h rows group-1, 2 group-1, ...))."""
+    hidden = w.shape[0]
+    m = h.numel() // hidden
+    x = torch.empty((m // group, hidden), dtype=torch.float16, device=h.device) if x is None else x
+    _dev(h, w, delta, x)
+    if h.dtype != torch.float32 or h.numel() != m * hidden:
+        raise ValueError("h must be float32 [m][hidden]")
+    if delta is not None and (delta.dtype != torch.float32 or delta.numel() != m * hidden):
+        raise ValueError("delta must be float32 [m][hidden]")
+    _expect(w, torch.float16, (hidden,), "w")
+    if x.dtype != torch.float16 or x.numel() != (m // group) * hidden:
+        raise ValueError("x must be float16 [m / group][hidden]")
+    _check(load().sq_add_rmsnorm_f16(_ptr(h), _ptr(delta), m, hidden, _ptr(w), float(eps), int(group), _ptr(x),
+                                     _stream(h.device)), "sq_add_rmsnorm_f16")
+    return x
+
+
+def _cache_dims(k_cache, v_cache):
+    b, hkv, cap, hd = k_cache.shape
+    if hd != HEAD_DIM:
+        raise ValueError("k_cache must be [b][hkv][capacity][128]")
+    _expect(v_cache, torch.float16, (b, hkv, HEAD_DIM, cap), "v_cache")
+    if k_cache.dtype != torch.float16:
+        raise TypeError("k_cache must be float16")
+    return b, hkv, cap
+
+
+def sq_rope_kv_f16(qkv, bias, pos_base, pos_offset: int, rows_per_seq: int, hq: int, k_cache, v_cache,
+                   len_bound: int | None = None, theta: float = 1e6, q_out=None, status=None):
+    """Bias + RoPE of the q|k|v rows, keys and values into the cache; returns q_out [m][hq][128] fp16."""
+    b, hkv, cap = _cache_dims(k_cache, v_cache)
+    m = b * rows_per_seq
+    nh = hq + 2 * hkv
+    len_bound = cap if len_bound is None else len_bound
+    q_out = torch.empty((m, hq, HEAD_DIM), dtype=torch.float16, device=qkv.device) if q_out is None else q_out
+    _dev(qkv, bias, pos_base, q_out, k_cache, v_cache, status)
+    if qkv.dtype != torch.float32 or qkv.numel() != m * nh * HEAD_DIM:
+        raise ValueError("qkv must be float32 [m][(hq + 2 hkv) * 128]")
+    if bias is not None:
+        _expect(bias, torch.float16, (nh * HEAD_DIM,), "bias")
+    _expect(pos_base, torch.int32, (b,), "pos_base")
+    _expect(q_out, torch.float16, (m, hq, HEAD_DIM), "q_out")
+    _check(load().sq_rope_kv_f16(_ptr(qkv), _ptr(bias), b, rows_per_seq, hq, hkv, _ptr(pos_base), int(pos_offset),
+                                 int(len_bound), cap, float(theta), _ptr(q_out), _ptr(k_cache), _ptr(v_cache),
+                                 _ptr(status), _stream(qkv.device)), "sq_rope_kv_f16")
+    return q_out
+
+
+def sq_attention_f16(q, k_cache, v_cache, pos_base, pos_offset: int, rows_per_seq: int,
+                     len_bound: int | None = None, out=None):
+    """Causal GQA attention of the block rows over the cache; returns out [m][hq][128] fp16."""
+    b, hkv, cap = _cache_dims(k_cache, v_cache)
+    m, hq, hd = q.shape
+    if hd != HEAD_DIM or m != b * rows_per_seq:
+        raise ValueError("q must be [b * rows_per_seq][hq][128]")
+    len_bound = cap if len_bound is None else len_bound
+    out = torch.empty((m, hq, HEAD_DIM), dtype=torch.float16, device=q.device) if out is None else out
+    _dev(q, k_cache, v_cache, pos_base, out)
+    if q.dtype != torch.float16:
+        raise TypeError("q must be float16")
+    _expect(pos_base, torch.int32, (b,), "pos_base")
+    if out.dtype != torch.float16 or out.numel() != m * hq * HEAD_DIM:
+        raise ValueError("out must be float16 [m][hq][128]")
+    _check(load().sq_attention_f16(_ptr(q), _ptr(k_cache), _ptr(v_cache), b, rows_per_seq, hq, hkv, _ptr(pos_base),
+                                   int(pos_offset), int(len_bound), cap, _ptr(out), _stream(q.device)),
+           "sq_attention_f16")
+    return out
+
+
+def sq_silu_mul_f16(gu, t=None):
+    """t [m][I] fp16 = silu(gate) * up of gu [m][2 I] f32."""
+    m, two_i = gu.shape
+    inter = two_i // 2
+    t = torch.empty((m, inter), dtype=torch.float16, device=gu.device) if t is None else t
+    _dev(gu, t)
+    if gu.dtype != torch.float32 or two_i % 2:
+        raise ValueError("gu must be float32 [m][2 I]")
+    if t.dtype != torch.float16 or t.numel() != m * inter:
+        raise ValueError("t must be float16 [m][I]")
+    _check(load().sq_silu_mul_f16(_ptr(gu), m, inter, _ptr(t), _stream(gu.device)), "sq_silu_mul_f16")
+    return t
+
+
+def sq_spec_commit(n_accepted, next_token, draft_tokens, pending, prev, pos_base, out_tokens=None, out_len=None,
+                   status=None):
+    """Commit a round: append the emitted tokens, move pending / prev / pos_base."""
+    b = n_accepted.shape[0]
+    kd = 0 if draft_tokens is None else draft_tokens.shape[0]
+    _dev(n_accepted, next_token, draft_tokens, pending, prev, pos_base, out_tokens, out_len, status)
+    for t, name in ((n_accepted, "n_accepted"), (next_token, "next_token"), (pending, "pending"), (prev, "prev"),
+                    (pos_base, "pos_base")):
+        _expect(t, torch.int32, (b,), name)
+    if draft_tokens is not None:
+        _expect(draft_tokens, torch.int32, (kd, b), "draft_tokens")
+    cap = 0
+    if out_tokens is not None:
+        if out_tokens.dtype != torch.int32 or out_tokens.dim() != 2 or out_tokens.shape[0] != b:
+            raise ValueError("out_tokens must be int32 [b][capacity]")
+        cap = out_tokens.shape[1]
+        _expect(out_len, torch.int32, (b,), "out_len")
+    _check(load().sq_spec_commit(_ptr(n_accepted), _ptr(next_token), _ptr(draft_tokens), b, kd, _ptr(pending),
+                                 _ptr(prev), _ptr(pos_base), _ptr(out_tokens), cap, _ptr(out_len), _ptr(status),
+                                 _stream(n_accepted.device)), "sq_spec_commit")

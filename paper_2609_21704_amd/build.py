@@ -12,7 +12,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB_PATH = os.path.join(PKG, "libspecquant.so")
 
-SOURCES = ["quant.hip", "gemv.hip", "gemm.hip", "linear.hip", "accept.hip", "probe.hip", "abi.cpp"]
+SOURCES = ["quant.hip", "gemv.hip", "gemm.hip", "linear.hip", "accept.hip", "decoder.hip", "probe.hip", "abi.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -167,6 +167,18 @@ inline sq_status device_status(hipError_t e) {
 
 constexpr int64_t kMaxK = int64_t(1) << 20;
 constexpr int64_t kMaxN = 0x7FFFFFFF;
+constexpr int64_t kMaxHidden = 65536;
+
+// Shared limits of the block layout of the rope / attention calls.
+sq_status check_block(int32_t b, int32_t rows_per_seq, int32_t hq, int32_t hkv, int64_t len_bound,
+                      int64_t capacity) {
+  if (b < 1 || rows_per_seq < 1 || rows_per_seq > 64 || hkv < 1 || hq < hkv || hq > 128 || hq % hkv != 0)
+    return SQ_ERR_SHAPE;
+  if (capacity < 64 || capacity > kMaxN || capacity % 64 != 0 || len_bound < 1 || len_bound > capacity)
+    return SQ_ERR_SHAPE;
+  if ((int64_t)b * rows_per_seq > kMaxN || (int64_t)b * hkv > 65535) return SQ_ERR_SHAPE;
+  return SQ_OK;
+}
 
 }  // namespace
 
@@ -292,6 +304,118 @@ sq_status sq_probe_stream_read(const void* src, int64_t bytes, uint32_t* sink, h
   if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
   (void)hipGetLastError();
   return device_status(sq::launch_stream_read(src, bytes, sink, SQ_PROBE_SINK_WORDS, stream));
+}
+
+// ------------------------------------------------------------ decoder layer
+sq_status sq_embed_block_f16(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* first,
+                             const int32_t* rest, int32_t b, int32_t kd, float* h, int32_t* status,
+                             hipStream_t stream) {
+  if (!table || !first || !h || (kd > 0 && !rest)) return SQ_ERR_NULL;
+  if (vocab < 1 || vocab > kMaxN || hidden < 8 || hidden > kMaxHidden || hidden % 8 != 0 || b < 1 || kd < 0 ||
+      kd > 63 || (int64_t)b * (kd + 1) > kMaxN)
+    return SQ_ERR_SHAPE;
+  if (!aligned(table, 16) || !aligned(first, 4) || !aligned(rest, 4) || !aligned(h, 16) || !aligned(status, 4))
+    return SQ_ERR_ALIGN;
+  const size_t rows = (size_t)b * (kd + 1);
+  const Range outs[] = {{h, rows * hidden * 4}, {status, 4}};
+  const Range ins[] = {{table, (size_t)vocab * hidden * 2}, {first, (size_t)b * 4}, {rest, (size_t)kd * b * 4}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_embed_block(table, vocab, (int)hidden, first, rest, b, kd, h, status, stream));
+}
+
+sq_status sq_add_rmsnorm_f16(float* h, const float* delta, int64_t m, int64_t hidden, const uint16_t* w,
+                             float eps, int32_t group, uint16_t* x, hipStream_t stream) {
+  if (!h || !w || !x) return SQ_ERR_NULL;
+  if (m < 1 || m > kMaxN || hidden < 8 || hidden > kMaxHidden || hidden % 8 != 0 || group < 1 || m % group != 0)
+    return SQ_ERR_SHAPE;
+  if (!isfinite(eps)) return SQ_ERR_NONFINITE;
+  if (eps < 0.f) return SQ_ERR_SHAPE;
+  if (!aligned(h, 16) || !aligned(delta, 16) || !aligned(w, 16) || !aligned(x, 16)) return SQ_ERR_ALIGN;
+  const size_t mh = (size_t)m * hidden;
+  const Range outs[] = {{h, mh * 4}, {x, mh / group * 2}};
+  const Range ins[] = {{delta, mh * 4}, {w, (size_t)hidden * 2}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_add_rmsnorm(h, delta, m, (int)hidden, w, eps, group, x, stream));
+}
+
+sq_status sq_rope_kv_f16(const float* qkv, const uint16_t* bias, int32_t b, int32_t rows_per_seq, int32_t hq,
+                         int32_t hkv, const int32_t* pos_base, int32_t pos_offset, int64_t len_bound,
+                         int64_t capacity, double theta, uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache,
+                         int32_t* status, hipStream_t stream) {
+  if (!qkv || !pos_base || !q_out || !k_cache || !v_cache) return SQ_ERR_NULL;
+  const sq_status bs = check_block(b, rows_per_seq, hq, hkv, len_bound, capacity);
+  if (bs != SQ_OK) return bs;
+  if (!isfinite(theta)) return SQ_ERR_NONFINITE;
+  if (!(theta > 1.0)) return SQ_ERR_SHAPE;
+  if (!aligned(qkv, 16) || !aligned(bias, 16) || !aligned(pos_base, 4) || !aligned(q_out, 16) ||
+      !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(status, 4))
+    return SQ_ERR_ALIGN;
+  const size_t m = (size_t)b * rows_per_seq, nh = (size_t)hq + 2 * (size_t)hkv;
+  const size_t cache = (size_t)b * hkv * capacity * 128 * 2;
+  const Range outs[] = {{q_out, m * hq * 128 * 2}, {k_cache, cache}, {v_cache, cache}, {status, 4}};
+  const Range ins[] = {{qkv, m * nh * 128 * 4}, {bias, nh * 128 * 2}, {pos_base, (size_t)b * 4}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_rope_kv(qkv, bias, (int)m, hq, hkv, rows_per_seq, pos_base, pos_offset, len_bound,
+                                          capacity, theta, q_out, k_cache, v_cache, status, stream));
+}
+
+sq_status sq_attention_f16(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t b,
+                           int32_t rows_per_seq, int32_t hq, int32_t hkv, const int32_t* pos_base,
+                           int32_t pos_offset, int64_t len_bound, int64_t capacity, uint16_t* out,
+                           hipStream_t stream) {
+  if (!q || !k_cache || !v_cache || !pos_base || !out) return SQ_ERR_NULL;
+  const sq_status bs = check_block(b, rows_per_seq, hq, hkv, len_bound, capacity);
+  if (bs != SQ_OK) return bs;
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(pos_base, 4) ||
+      !aligned(out, 16))
+    return SQ_ERR_ALIGN;
+  const size_t m = (size_t)b * rows_per_seq;
+  const size_t cache = (size_t)b * hkv * capacity * 128 * 2;
+  const Range outs[] = {{out, m * hq * 128 * 2}};
+  const Range ins[] = {{q, m * hq * 128 * 2}, {k_cache, cache}, {v_cache, cache}, {pos_base, (size_t)b * 4}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_attention(q, k_cache, v_cache, b, rows_per_seq, hq, hkv, capacity, pos_base,
+                                            pos_offset, len_bound, out, stream));
+}
+
+sq_status sq_silu_mul_f16(const float* gu, int64_t m, int64_t inter, uint16_t* t, hipStream_t stream) {
+  if (!gu || !t) return SQ_ERR_NULL;
+  if (m < 1 || inter < 1 || m > kMaxN || inter > kMaxN || m * inter >= (int64_t(1) << 40)) return SQ_ERR_SHAPE;
+  if (!aligned(gu, 4) || !aligned(t, 2)) return SQ_ERR_ALIGN;
+  const Range outs[] = {{t, (size_t)(m * inter) * 2}};
+  const Range ins[] = {{gu, (size_t)(m * inter) * 8}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_silu_mul(gu, m, inter, t, stream));
+}
+
+sq_status sq_spec_commit(const int32_t* n_accepted, const int32_t* next_token, const int32_t* draft_tokens,
+                         int32_t b, int32_t kd, int32_t* pending, int32_t* prev, int32_t* pos_base,
+                         int32_t* out_tokens, int64_t out_capacity, int32_t* out_len, int32_t* status,
+                         hipStream_t stream) {
+  if (!n_accepted || !next_token || !pending || !prev || !pos_base || (kd > 0 && !draft_tokens) ||
+      (out_tokens && !out_len))
+    return SQ_ERR_NULL;
+  if (b < 1 || b >= (1 << 24) || kd < 0 || kd > 64 || (out_tokens && (out_capacity < 1 || out_capacity > kMaxN)))
+    return SQ_ERR_SHAPE;
+  if (!aligned(n_accepted, 4) || !aligned(next_token, 4) || !aligned(draft_tokens, 4) || !aligned(pending, 4) ||
+      !aligned(prev, 4) || !aligned(pos_base, 4) || !aligned(out_tokens, 4) || !aligned(out_len, 4) ||
+      !aligned(status, 4))
+    return SQ_ERR_ALIGN;
+  const size_t b4 = (size_t)b * 4;
+  const size_t hist = out_tokens ? (size_t)b * (size_t)out_capacity * 4 : 0;
+  const Range outs[] = {{pending, b4}, {prev, b4}, {pos_base, b4}, {out_tokens, hist},
+                        {out_tokens ? out_len : nullptr, b4}, {status, 4}};
+  const Range ins[] = {{n_accepted, b4}, {next_token, b4}, {draft_tokens, (size_t)kd * b4}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_spec_commit(n_accepted, next_token, draft_tokens, b, kd, pending, prev, pos_base,
+                                              out_tokens, out_capacity, out_tokens ? out_len : nullptr, status,
+                                              stream));
 }
 
 }  // extern "C"

@@ -1,0 +1,420 @@
+// The decoder layer around the projections of a SpecQuant pass (draft
+// generation, SS III-D.2; parent verification, SS III-D.3) for the Qwen2.5
+// family the paper evaluates (SS IV), and the commit that restarts a
+// sequence at its first rejected token (SS III-D.4):
+//   embed_kernel        h = table[token] (fp32 residual stream)
+//   add_rmsnorm_kernel  h += delta; x = f16(h / sqrt(mean(h^2) + eps) * w)
+//   rope_kv_kernel      bias, rotary embedding of q and k, cache write of k, v
+//   attn_chunk_kernel   causal grouped-query attention of one 64-position chunk
+//                       of the cache on the matrix cores (partial softmax)
+//   attn_merge_kernel   merge of the chunks in chunk order
+//   silu_mul_kernel     t = f16(g / (1 + exp(-g)) * u)
+//   commit_kernel       emitted tokens, next pending token, position
+//
+// Cache layout, per model and layer: keys [b][hkv][capacity][128] (a key is
+// 256 contiguous bytes) and values position-minor, [b][hkv][128][capacity],
+// so that the matrix-core product P.V reads each value fragment as two 8-byte
+// runs of positions.  A row of a block of rows_per_seq rows of sequence b sits
+// at position pos_base[b] + pos_offset + j.  The round never moves cache data:
+// removing the rejected part of a block only moves pos_base, and the entries
+// past it are overwritten before any row can attend to them.
+#include "sq_device.hpp"
+#include "sq_internal.hpp"
+
+namespace sq {
+namespace {
+
+constexpr int kHd = 128;    // head dimension of the family
+constexpr int kChunk = 64;  // cache positions per attention wavefront
+
+// device status bits (the SQ_DEV_* values of the C header)
+constexpr int32_t kBadToken = 1, kBadPos = 2, kOverflow = 4, kNoDist = 8;
+
+typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void flag(int32_t* status, int32_t bit) {
+  if (status) atomicOr(status, bit);
+}
+
+constexpr uint16_t kNanF16 = 0x7E00;
+
+// ------------------------------------------------------------------ embed
+__global__ __launch_bounds__(256) void embed_kernel(const uint16_t* __restrict__ table, int64_t vocab, int hidden,
+                                                    const int32_t* __restrict__ first,
+                                                    const int32_t* __restrict__ rest, int b, int kd,
+                                                    float* __restrict__ h, int32_t* __restrict__ status) {
+  const int row = blockIdx.x;  // row = bi * (kd + 1) + j
+  const int bi = row / (kd + 1), j = row - bi * (kd + 1);
+  const int32_t tok = j == 0 ? first[bi] : rest[(int64_t)(j - 1) * b + bi];
+  float* out = h + (int64_t)row * hidden;
+  if (tok < 0 || tok >= vocab) {
+    for (int c = threadIdx.x; c < hidden; c += blockDim.x) out[c] = __builtin_nanf("");
+    if (threadIdx.x == 0) flag(status, kBadToken);
+    return;
+  }
+  const uint16_t* src = table + (int64_t)tok * hidden;
+  for (int c = threadIdx.x * 8; c < hidden; c += blockDim.x * 8) {
+    const half8_t v = *reinterpret_cast<const half8_t*>(src + c);
+    float4_t lo = {(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+    float4_t hi = {(float)v[4], (float)v[5], (float)v[6], (float)v[7]};
+    *reinterpret_cast<float4_t*>(out + c) = lo;
+    *reinterpret_cast<float4_t*>(out + c + 4) = hi;
+  }
+}
+
+// ---------------------------------------------------- residual add + norm
+// One workgroup per row of h.  Every row gets the residual add; the rows
+// r * group + group - 1 are normalised into output row r.
+__global__ __launch_bounds__(256) void add_rmsnorm_kernel(float* __restrict__ h, const float* __restrict__ delta,
+                                                          int hidden, const uint16_t* __restrict__ w, float eps,
+                                                          int group, uint16_t* __restrict__ x) {
+  __shared__ float red[4];
+  const int64_t row = blockIdx.x;
+  float* hr = h + row * hidden;
+  const bool out_row = (row % group) == group - 1;
+  float ss = 0.f;
+  for (int c = threadIdx.x * 4; c < hidden; c += 1024) {
+    float4_t v = *reinterpret_cast<float4_t*>(hr + c);
+    if (delta) {
+      v += *reinterpret_cast<const float4_t*>(delta + row * hidden + c);
+      *reinterpret_cast<float4_t*>(hr + c) = v;
+    }
+    if (out_row) ss += (v[0] * v[0] + v[1] * v[1]) + (v[2] * v[2] + v[3] * v[3]);
+  }
+  if (!out_row) return;  // uniform across the workgroup
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();  // the residual writes of this workgroup are visible after it too
+  const float total = (red[0] + red[1]) + (red[2] + red[3]);
+  const float r = (float)(1.0 / sqrt((double)total / (double)hidden + (double)eps));
+  uint16_t* xr = x + (row / group) * hidden;
+  for (int c = threadIdx.x * 4; c < hidden; c += 1024) {
+    const float4_t v = *reinterpret_cast<const float4_t*>(hr + c);
+    const uint2 wb = *reinterpret_cast<const uint2*>(w + c);
+    const half4_t wh = __builtin_bit_cast(half4_t, wb);
+    half4_t o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = (half_t)(v[e] * r * (float)wh[e]);
+    *reinterpret_cast<uint2*>(xr + c) = __builtin_bit_cast(uint2, o);
+  }
+}
+
+// ------------------------------------------------- bias + RoPE + cache write
+// One wavefront per row; lane t handles the pair (t, t + 64) of every head.
+__global__ __launch_bounds__(64) void rope_kv_kernel(const float* __restrict__ qkv, const uint16_t* __restrict__ bias,
+                                                     int hq, int hkv, int rps, const int32_t* __restrict__ pos_base,
+                                                     int pos_offset, int64_t len_bound, int64_t capacity, double theta,
+                                                     uint16_t* __restrict__ q_out, uint16_t* __restrict__ kc,
+                                                     uint16_t* __restrict__ vc, int32_t* __restrict__ status) {
+  const int r = blockIdx.x;
+  const int bi = r / rps, j = r - bi * rps;
+  const int64_t pos = (int64_t)pos_base[bi] + pos_offset + j;
+  const int t = threadIdx.x;
+  const int nh = hq + 2 * hkv;
+  const float* row = qkv + (int64_t)r * nh * kHd;
+  if (pos < 0 || pos >= len_bound) {
+    for (int hh = 0; hh < hq; ++hh) {
+      q_out[((int64_t)r * hq + hh) * kHd + t] = kNanF16;
+      q_out[((int64_t)r * hq + hh) * kHd + t + 64] = kNanF16;
+    }
+    if (t == 0) flag(status, kBadPos);
+    return;
+  }
+  // angle pos * theta^(-2t/128) and its cosine and sine in fp64
+  const double ang = (double)pos * pow(theta, -2.0 * (double)t / (double)kHd);
+  double sn, cs;
+  sincos(ang, &sn, &cs);
+  const float c = (float)cs, s = (float)sn;
+  for (int hh = 0; hh < nh; ++hh) {
+    float a = row[hh * kHd + t], e = row[hh * kHd + t + 64];
+    if (bias) {
+      a += f16_bits_to_f32(bias[hh * kHd + t]);
+      e += f16_bits_to_f32(bias[hh * kHd + t + 64]);
+    }
+    if (hh < hq + hkv) {
+      const float ra = a * c - e * s, re = e * c + a * s;
+      if (hh < hq) {
+        uint16_t* qo = q_out + ((int64_t)r * hq + hh) * kHd;
+        qo[t] = f32_to_f16_bits(ra);
+        qo[t + 64] = f32_to_f16_bits(re);
+      } else {
+        uint16_t* ko = kc + (((int64_t)bi * hkv + (hh - hq)) * capacity + pos) * kHd;
+        ko[t] = f32_to_f16_bits(ra);
+        ko[t + 64] = f32_to_f16_bits(re);
+      }
+    } else {
+      uint16_t* vo = vc + ((int64_t)bi * hkv + (hh - hq - hkv)) * kHd * capacity + pos;
+      vo[(int64_t)t * capacity] = f32_to_f16_bits(a);
+      vo[(int64_t)(t + 64) * capacity] = f32_to_f16_bits(e);
+    }
+  }
+}
+
+// ------------------------------------------------------- attention chunks
+// One wavefront per (64-position chunk c, sequence bi, kv head g).  Its query
+// rows are the block's rows of bi times the G = hq / hkv heads of g, ordered
+// qi = j * G + gg, in tiles of 16.  On the matrix cores
+// (v_mfma_f32_16x16x32_f16; lane l holds A[l%16][8(l/16) .. +8) and
+// B[8(l/16) .. +8)[l%16], D[4(l/16) + i][l%16]):
+//   S^T = K . Q^T  -- A: 16 keys x 32 of the head dimension (lane l: key l%16,
+//                     dims 32(l/16) + 8s .. +8 for step s), B: the same dims of
+//                     16 query rows; lane l ends with the scores of keys
+//                     4(l/16) + i of query l%16;
+//   O = P . V      -- the lane's 8 scores of two adjacent key tiles are
+//                     exactly its A fragment of P (keys 4(l/16) + i and
+//                     16 + 4(l/16) + i of query l%16), and B takes the values
+//                     of the same 8 keys at dim l%16 (+16 per output tile)
+//                     from the position-minor value cache.
+// The partial result of each query row is (m, l, O): m the largest scaled
+// score (log2 units) of the chunk, l = sum of the weights p = 2^(s - m),
+// O = sum p v with each p split into two binary16 terms.  Keys after a row's position get p = 0; keys
+// after the last row's position are not read (their fragments are zero).
+__global__ __launch_bounds__(64) void attn_chunk_kernel(const uint16_t* __restrict__ q,
+                                                        const uint16_t* __restrict__ kc,
+                                                        const uint16_t* __restrict__ vc, int hq, int hkv, int rps,
+                                                        int64_t capacity, const int32_t* __restrict__ pos_base,
+                                                        int pos_offset, int nch, int nq_pad,
+                                                        float* __restrict__ part_o, float2* __restrict__ part_ml) {
+  const int c = blockIdx.x;
+  const int bg = blockIdx.y;  // bi * hkv + g
+  const int bi = bg / hkv, g = bg - bi * hkv;
+  const int G = hq / hkv, nq = rps * G;
+  const int64_t p0 = (int64_t)pos_base[bi] + pos_offset;
+  const int64_t pmax = p0 + rps - 1;
+  const int64_t key0 = (int64_t)c * kChunk;
+  if (key0 > pmax) return;  // no row reads this chunk (uniform); rows at negative positions mask every key
+  const int lane = threadIdx.x, li = lane & 15, lg = lane >> 4;
+  const half8_t zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
+
+  half8_t kf[4][4];
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt) {
+    const int64_t key = key0 + 16 * kt + li;
+    const half8_t* kp = reinterpret_cast<const half8_t*>(kc + ((int64_t)bg * capacity + key) * kHd + 32 * lg);
+    const bool ok = key <= pmax;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) kf[kt][s] = ok ? kp[s] : zero8;
+  }
+  half8_t vf[2][8];
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2) {
+    const int64_t ka = key0 + 32 * t2 + 4 * lg, kb = ka + 16;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) {
+      const uint16_t* vp = vc + ((int64_t)bg * kHd + 16 * dt + li) * capacity;
+      const half4_t a = *reinterpret_cast<const half4_t*>(vp + ka);
+      const half4_t b = *reinterpret_cast<const half4_t*>(vp + kb);
+      half8_t f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        f[e] = ka + e <= pmax ? a[e] : (half_t)0;
+        f[4 + e] = kb + e <= pmax ? b[e] : (half_t)0;
+      }
+      vf[t2][dt] = f;
+    }
+  }
+
+  const float sl2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
+  const int nqt = (nq + 15) >> 4;
+  float* po = part_o + ((int64_t)bg * nch + c) * nq_pad * kHd;
+  float2* pml = part_ml + ((int64_t)bg * nch + c) * nq_pad;
+  for (int qt = 0; qt < nqt; ++qt) {
+    const int qi = 16 * qt + li;
+    const bool qok = qi < nq;
+    const int j = qok ? qi / G : 0, gg = qok ? qi - (qi / G) * G : 0;
+    const half8_t* qp =
+        reinterpret_cast<const half8_t*>(q + (((int64_t)bi * rps + j) * hq + g * G + gg) * kHd + 32 * lg);
+    half8_t qf[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) qf[s] = qok ? qp[s] : zero8;
+    float4_t st[4];
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+      float4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf[kt][s], qf[s], acc, 0, 0, 0);
+      st[kt] = acc;
+    }
+    const int64_t qpos = p0 + j;
+    float mx = -__builtin_inff();
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t key = key0 + 16 * kt + 4 * lg + i;
+        const float v = (qok && key <= qpos) ? st[kt][i] * sl2 : -__builtin_inff();
+        st[kt][i] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    // p = hi + lo, both binary16 (hi = f16(p), lo = f16(p - hi), the difference
+    // exact in fp32): two products with the values carry p to about 2^-22
+    float lsum = 0.f;
+    half8_t pf[2], pl[2];
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = mx == -__builtin_inff() ? 0.f : exp2f(st[kt][i] - mx);
+        const half_t ph = (half_t)p;
+        lsum += p;
+        pf[kt >> 1][(kt & 1) * 4 + i] = ph;
+        pl[kt >> 1][(kt & 1) * 4 + i] = (half_t)(p - (float)ph);
+      }
+    lsum += __shfl_xor(lsum, 16, kWave);
+    lsum += __shfl_xor(lsum, 32, kWave);
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) {
+      float4_t o = {0.f, 0.f, 0.f, 0.f};
+      o = __builtin_amdgcn_mfma_f32_16x16x32_f16(pl[0], vf[0][dt], o, 0, 0, 0);
+      o = __builtin_amdgcn_mfma_f32_16x16x32_f16(pl[1], vf[1][dt], o, 0, 0, 0);
+      o = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[0], vf[0][dt], o, 0, 0, 0);
+      o = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[1], vf[1][dt], o, 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) po[(int64_t)(16 * qt + 4 * lg + i) * kHd + 16 * dt + li] = o[i];
+    }
+    if (lg == 0) pml[16 * qt + li] = make_float2(mx, lsum);
+  }
+}
+
+// One workgroup of 128 threads (one per dim) per (row, query head): the
+// chunks 0 .. pos / 64 in order, out = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c.
+__global__ __launch_bounds__(128) void attn_merge_kernel(const float* __restrict__ part_o,
+                                                         const float2* __restrict__ part_ml, int hq, int hkv,
+                                                         int rps, int nch, int nq_pad,
+                                                         const int32_t* __restrict__ pos_base, int pos_offset,
+                                                         int64_t len_bound, uint16_t* __restrict__ out) {
+  const int r = blockIdx.x, hh = blockIdx.y, d = threadIdx.x;
+  const int bi = r / rps, j = r - bi * rps;
+  const int G = hq / hkv, g = hh / G, gg = hh - g * G;
+  const int qi = j * G + gg;
+  const int64_t pos = (int64_t)pos_base[bi] + pos_offset + j;
+  uint16_t* o = out + ((int64_t)r * hq + hh) * kHd + d;
+  if (pos < 0 || pos >= len_bound) {
+    *o = kNanF16;
+    return;
+  }
+  const int last = (int)(pos / kChunk);
+  const int64_t bg = (int64_t)bi * hkv + g;
+  const float2* ml = part_ml + bg * nch * nq_pad + qi;
+  const float* po = part_o + (bg * nch * nq_pad + qi) * kHd + d;
+  float mx = -__builtin_inff();
+  for (int c = 0; c <= last; ++c) mx = fmaxf(mx, ml[(int64_t)c * nq_pad].x);
+  float l = 0.f, acc = 0.f;
+  for (int c = 0; c <= last; ++c) {
+    const float2 v = ml[(int64_t)c * nq_pad];
+    const float w = exp2f(v.x - mx);
+    l += v.y * w;
+    acc += po[(int64_t)c * nq_pad * kHd] * w;
+  }
+  *o = f32_to_f16_bits(acc / l);
+}
+
+// ------------------------------------------------------------- SiLU . up
+__global__ __launch_bounds__(256) void silu_mul_kernel(const float* __restrict__ gu, int64_t m, int64_t inter,
+                                                       uint16_t* __restrict__ t) {
+  const int64_t total = m * inter;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = i / inter, col = i - row * inter;
+    const float gv = gu[row * 2 * inter + col], uv = gu[row * 2 * inter + inter + col];
+    t[i] = f32_to_f16_bits(gv / (1.f + expf(-gv)) * uv);
+  }
+}
+
+// ---------------------------------------------------------------- commit
+__global__ __launch_bounds__(256) void commit_kernel(const int32_t* __restrict__ n_accepted,
+                                                     const int32_t* __restrict__ next_token,
+                                                     const int32_t* __restrict__ drafts, int b, int kd,
+                                                     int32_t* __restrict__ pending, int32_t* __restrict__ prev,
+                                                     int32_t* __restrict__ pos_base, int32_t* __restrict__ out_tokens,
+                                                     int64_t out_capacity, int32_t* __restrict__ out_len,
+                                                     int32_t* __restrict__ status) {
+  const int bi = blockIdx.x * blockDim.x + threadIdx.x;
+  if (bi >= b) return;
+  const int n = n_accepted[bi];
+  if (n < 0 || n > kd) {  // the round had no distribution for this sequence
+    flag(status, kNoDist);
+    return;
+  }
+  if (out_tokens) {
+    const int64_t len = out_len[bi];
+    int32_t* dst = out_tokens + (int64_t)bi * out_capacity;
+    for (int i = 0; i <= n; ++i) {
+      const int32_t tok = i < n ? drafts[(int64_t)i * b + bi] : next_token[bi];
+      if (len + i >= 0 && len + i < out_capacity)
+        dst[len + i] = tok;
+      else
+        flag(status, kOverflow);
+    }
+    out_len[bi] = (int32_t)(len + n + 1);
+  }
+  prev[bi] = n >= 1 ? drafts[(int64_t)(n - 1) * b + bi] : pending[bi];
+  pending[bi] = next_token[bi];
+  pos_base[bi] += n + 1;
+}
+
+}  // namespace
+
+hipError_t launch_embed_block(const uint16_t* table, int64_t vocab, int hidden, const int32_t* first,
+                              const int32_t* rest, int b, int kd, float* h, int32_t* status, hipStream_t stream) {
+  hipLaunchKernelGGL(embed_kernel, dim3((unsigned)(b * (kd + 1))), dim3(256), 0, stream, table, vocab, hidden, first,
+                     rest, b, kd, h, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_add_rmsnorm(float* h, const float* delta, int64_t m, int hidden, const uint16_t* w, float eps,
+                              int group, uint16_t* x, hipStream_t stream) {
+  hipLaunchKernelGGL(add_rmsnorm_kernel, dim3((unsigned)m), dim3(256), 0, stream, h, delta, hidden, w, eps, group, x);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_kv(const float* qkv, const uint16_t* bias, int m, int hq, int hkv, int rps,
+                          const int32_t* pos_base, int pos_offset, int64_t len_bound, int64_t capacity, double theta,
+                          uint16_t* q_out, uint16_t* kc, uint16_t* vc, int32_t* status, hipStream_t stream) {
+  hipLaunchKernelGGL(rope_kv_kernel, dim3((unsigned)m), dim3(64), 0, stream, qkv, bias, hq, hkv, rps, pos_base,
+                     pos_offset, len_bound, capacity, theta, q_out, kc, vc, status);
+  return hipGetLastError();
+}
+
+size_t attention_workspace_bytes(int b, int hq, int hkv, int rps, int64_t len_bound) {
+  const int nch = (int)((len_bound + kChunk - 1) / kChunk);
+  const int nq_pad = (rps * (hq / hkv) + 15) / 16 * 16;
+  return (size_t)b * hkv * nch * nq_pad * (kHd * sizeof(float) + sizeof(float2));
+}
+
+hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, int b, int rps, int hq,
+                            int hkv, int64_t capacity, const int32_t* pos_base, int pos_offset, int64_t len_bound,
+                            uint16_t* out, hipStream_t stream) {
+  const int nch = (int)((len_bound + kChunk - 1) / kChunk);
+  const int nq_pad = (rps * (hq / hkv) + 15) / 16 * 16;
+  void* ws = nullptr;
+  const hipError_t e = workspace(attention_workspace_bytes(b, hq, hkv, rps, len_bound), stream, &ws);
+  if (e != hipSuccess) return e;
+  float* part_o = static_cast<float*>(ws);
+  float2* part_ml = reinterpret_cast<float2*>(part_o + (size_t)b * hkv * nch * nq_pad * kHd);
+  hipLaunchKernelGGL(attn_chunk_kernel, dim3((unsigned)nch, (unsigned)(b * hkv)), dim3(64), 0, stream, q, kc, vc, hq,
+                     hkv, rps, capacity, pos_base, pos_offset, nch, nq_pad, part_o, part_ml);
+  hipLaunchKernelGGL(attn_merge_kernel, dim3((unsigned)(b * rps), (unsigned)hq), dim3(kHd), 0, stream, part_o,
+                     part_ml, hq, hkv, rps, nch, nq_pad, pos_base, pos_offset, len_bound, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_silu_mul(const float* gu, int64_t m, int64_t inter, uint16_t* t, hipStream_t stream) {
+  const int64_t total = m * inter;
+  int64_t blocks = (total + 255) / 256;
+  const int64_t cap = (int64_t)cu_count() * 8;
+  if (blocks > cap) blocks = cap;
+  hipLaunchKernelGGL(silu_mul_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, gu, m, inter, t);
+  return hipGetLastError();
+}
+
+hipError_t launch_spec_commit(const int32_t* n_accepted, const int32_t* next_token, const int32_t* drafts, int b,
+                              int kd, int32_t* pending, int32_t* prev, int32_t* pos_base, int32_t* out_tokens,
+                              int64_t out_capacity, int32_t* out_len, int32_t* status, hipStream_t stream) {
+  hipLaunchKernelGGL(commit_kernel, dim3((unsigned)((b + 255) / 256)), dim3(256), 0, stream, n_accepted, next_token,
+                     drafts, b, kd, pending, prev, pos_base, out_tokens, out_capacity, out_len, status);
+  return hipGetLastError();
+}
+
+}  // namespace sq

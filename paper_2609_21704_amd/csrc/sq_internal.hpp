@@ -79,4 +79,22 @@ hipError_t launch_spec_accept_noalloc(const float* draft, const float* target, c
                                       int32_t* n_accepted, int32_t* next_token, float* q_out, float* p_out,
                                       hipStream_t stream);
 
+// The decoder layer around the projections (decoder.hip).
+hipError_t launch_embed_block(const uint16_t* table, int64_t vocab, int hidden, const int32_t* first,
+                              const int32_t* rest, int b, int kd, float* h, int32_t* status, hipStream_t stream);
+hipError_t launch_add_rmsnorm(float* h, const float* delta, int64_t m, int hidden, const uint16_t* w, float eps,
+                              int group, uint16_t* x, hipStream_t stream);
+hipError_t launch_rope_kv(const float* qkv, const uint16_t* bias, int m, int hq, int hkv, int rps,
+                          const int32_t* pos_base, int pos_offset, int64_t len_bound, int64_t capacity, double theta,
+                          uint16_t* q_out, uint16_t* kc, uint16_t* vc, int32_t* status, hipStream_t stream);
+// Workspace bytes of one attention call (chunk partials).
+size_t attention_workspace_bytes(int b, int hq, int hkv, int rps, int64_t len_bound);
+hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, int b, int rps, int hq,
+                            int hkv, int64_t capacity, const int32_t* pos_base, int pos_offset, int64_t len_bound,
+                            uint16_t* out, hipStream_t stream);
+hipError_t launch_silu_mul(const float* gu, int64_t m, int64_t inter, uint16_t* t, hipStream_t stream);
+hipError_t launch_spec_commit(const int32_t* n_accepted, const int32_t* next_token, const int32_t* drafts, int b,
+                              int kd, int32_t* pending, int32_t* prev, int32_t* pos_base, int32_t* out_tokens,
+                              int64_t out_capacity, int32_t* out_len, int32_t* status, hipStream_t stream);
+
 }  // namespace sq

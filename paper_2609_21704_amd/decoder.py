@@ -1,0 +1,274 @@
+"""SpecQuant rounds through a full decoder with a key/value cache.
+
+The weight-streaming stack of ``rounds`` reads a fresh activation per
+projection.  Here the same projections sit inside Qwen2.5-shaped decoder
+layers (the model family of SS IV): the token embedding, per layer RMSNorm ->
+q|k|v (+ bias) -> RoPE -> causal grouped-query attention over the cache -> o
+-> residual -> RMSNorm -> gate|up -> SiLU . up -> down -> residual, then the
+final RMSNorm and the LM head.  A round drafts k tokens with the quantized
+copy (SS III-D.2), verifies the block with the FP16 parent (SS III-D.3),
+accepts or corrects (SS III-D.4) and commits: the emitted tokens are
+appended, and the sequence restarts at the emitted token, which rolls both
+caches back to the accepted prefix by moving the position alone.
+
+Every step runs in the library's HIP kernels; torch holds the buffers, and a
+whole round can be captured as one HIP graph because all positions and
+tokens live on the device.
+
+Block layout per pass (b sequences, rows_per_seq rows each, rows at
+pos_base + offset + j):
+  draft step 0:   the previous token and the pending one at P-1, P (the entry
+                  at P-1 is recomputed; it is missing after a round that
+                  accepted every draft)
+  draft step i:   draft i-1 at P+i
+  verification:   the pending token and the k drafts at P .. P+k
+
+Synthetic parameters (no checkpoints): the projection matrices are those of
+``rounds.Stack`` (N(0, 0.02)); the embedding is N(0, 0.02), the norm weights
+N(1, 0.02) and the q|k|v biases N(0, 0.02), all fp16, shared unquantized by
+the draft copy.
+"""
+from __future__ import annotations
+
+import dataclasses
+
+import torch
+
+from . import _lib as sq
+from . import synth
+from .configs import HEAD_DIM, Config
+from .rounds import Stack, round_uniforms  # noqa: F401  (round_uniforms: per-round uniforms, same layout)
+
+EPS = 1e-6
+THETA = 1e6
+# tensor ids for synth.stream_seed (distinct from those of rounds)
+_EMBED, _NORM_IN, _NORM_POST, _NORM_FINAL, _BIAS, _PROMPT = range(20, 26)
+
+
+class DecoderWeights:
+    """The FP16 parent and its quantized draft copy (``Stack``) plus the
+    embedding, norms and biases they share."""
+
+    def __init__(self, cfg: Config, device, layers: int | None = None, variant: str | None = None):
+        cfg = dataclasses.replace(cfg, lm_head=True)
+        self.cfg = cfg
+        self.device = dev = torch.device(device)
+        self.stack = Stack(cfg, dev, variant=variant, layers=layers)
+        self.layers = self.stack.layers
+        H = cfg.hidden
+        n_qkv = cfg.q_dim + 2 * cfg.kv_dim
+        s = cfg.seed
+        self.embed = synth.normal_f16((cfg.vocab, H), 0.02, synth.stream_seed(s, _EMBED), dev)
+        self.final_norm = (synth.normal_f32((H,), 0.02, synth.stream_seed(s, _NORM_FINAL), dev) + 1.0).half()
+        self.in_norm, self.post_norm, self.qkv_bias = [], [], []
+        for l in range(self.layers):
+            self.in_norm.append((synth.normal_f32((H,), 0.02, synth.stream_seed(s, _NORM_IN, l), dev) + 1.0).half())
+            self.post_norm.append(
+                (synth.normal_f32((H,), 0.02, synth.stream_seed(s, _NORM_POST, l), dev) + 1.0).half())
+            self.qkv_bias.append(synth.normal_f16((n_qkv,), 0.02, synth.stream_seed(s, _BIAS, l), dev))
+
+    def params(self) -> dict:
+        """Every parameter by the oracle's names (host float16 copies)."""
+        p = {"embed": self.embed, "final_norm": self.final_norm,
+             "lm_head": self.stack.w16[(self.cfg.layers, "lm_head")]}
+        for l in range(self.layers):
+            p[f"{l}.in_norm"] = self.in_norm[l]
+            p[f"{l}.qkv_bias"] = self.qkv_bias[l]
+            p[f"{l}.post_norm"] = self.post_norm[l]
+            for name in ("qkv", "o", "gate_up", "down"):
+                p[f"{l}.{name}"] = self.stack.w16[(l, name)]
+        return {k: v.cpu().numpy() for k, v in p.items()}
+
+
+class KVCache:
+    """Keys [b][hkv][capacity][128] and position-minor values
+    [b][hkv][128][capacity] per layer, fp16."""
+
+    def __init__(self, cfg: Config, layers: int, batch: int, capacity: int, device):
+        if capacity % 64:
+            raise ValueError("the cache capacity must be a multiple of 64")
+        self.capacity = capacity
+        self.k = [torch.zeros((batch, cfg.kv_heads, capacity, HEAD_DIM), dtype=torch.float16, device=device)
+                  for _ in range(layers)]
+        self.v = [torch.zeros((batch, cfg.kv_heads, HEAD_DIM, capacity), dtype=torch.float16, device=device)
+                  for _ in range(layers)]
+
+
+class _Buffers:
+    """Activations of a pass of up to `rows` rows."""
+
+    def __init__(self, cfg: Config, rows: int, device):
+        H, I = cfg.hidden, cfg.intermediate
+        n_qkv = cfg.q_dim + 2 * cfg.kv_dim
+        f32, f16 = torch.float32, torch.float16
+        self.h = torch.empty((rows, H), dtype=f32, device=device)
+        self.x = torch.empty((rows, H), dtype=f16, device=device)
+        self.qkv = torch.empty((rows, n_qkv), dtype=f32, device=device)
+        self.q = torch.empty((rows, cfg.q_heads, HEAD_DIM), dtype=f16, device=device)
+        self.a = torch.empty((rows, cfg.q_heads, HEAD_DIM), dtype=f16, device=device)
+        self.y = torch.empty((rows, H), dtype=f32, device=device)
+        self.gu = torch.empty((rows, 2 * I), dtype=f32, device=device)
+        self.t = torch.empty((rows, I), dtype=f16, device=device)
+        self.xf = torch.empty((rows, H), dtype=f16, device=device)
+
+
+class SpecDecoder:
+    """Speculative rounds of one batch of sequences through the decoder."""
+
+    def __init__(self, weights: DecoderWeights, batch: int | None = None, k: int | None = None,
+                 capacity: int = 1024, temperature: float = 1.0, history: int = 4096, keep_pq: bool = False):
+        self.w = weights
+        cfg = self.cfg = weights.cfg
+        dev = self.device = weights.device
+        self.B = B = cfg.batch if batch is None else batch
+        self.k = k = cfg.k if k is None else k
+        self.T = float(temperature)
+        V = cfg.vocab
+        L = weights.layers
+        if B * 2 > 8:
+            raise ValueError("draft step 0 runs 2 rows per sequence; the draft GEMV takes at most 8")
+        if B * (k + 1) > 64:
+            raise ValueError("the verification pass takes at most 64 rows")
+        self.dcache = KVCache(cfg, L, B, capacity, dev)
+        self.pcache = KVCache(cfg, L, B, capacity, dev)
+        self.capacity = capacity
+        self.buf = _Buffers(cfg, 64, dev)  # the largest pass: 64 rows (verification, prefill chunks)
+        i32, f32 = torch.int32, torch.float32
+        self.pos_base = torch.zeros((B,), dtype=i32, device=dev)
+        self.pending = torch.zeros((B,), dtype=i32, device=dev)
+        self.prev = torch.zeros((B,), dtype=i32, device=dev)
+        self.draft_tokens = torch.zeros((k, B), dtype=i32, device=dev)
+        self.draft_logits = torch.empty((k, B, V), dtype=f32, device=dev)
+        self.target_logits = torch.empty((B, k + 1, V), dtype=f32, device=dev)
+        self.u_draft = torch.zeros((k, B), dtype=i32, device=dev)
+        self.u_accept = torch.zeros((B, k + 1), dtype=i32, device=dev)
+        self.n_accepted = torch.zeros((B,), dtype=i32, device=dev)
+        self.next_token = torch.zeros((B,), dtype=i32, device=dev)
+        self.scratch_n = torch.zeros((B,), dtype=i32, device=dev)
+        self.out_tokens = torch.zeros((B, history), dtype=i32, device=dev)
+        self.out_len = torch.zeros((B,), dtype=i32, device=dev)
+        self.status = torch.zeros((1,), dtype=i32, device=dev)
+        self.keep_pq = keep_pq
+        if keep_pq:
+            self.q_draft = torch.empty((k, B, V), dtype=f32, device=dev)   # draft-step distributions
+            self.q_out = torch.empty((k, B, V), dtype=f32, device=dev)
+            self.p_out = torch.empty((B, k + 1, V), dtype=f32, device=dev)
+        self.graph = None
+
+    # ------------------------------------------------------------- passes
+    def _linear(self, draft: bool, key, x, y):
+        st = self.w.stack
+        if draft:
+            st.draft_gemv(key, x, y)
+        else:
+            st.verify_gemm(key, x, y)
+
+    def forward(self, draft: bool, first, rest, rps: int, offset: int, logits, last_only: bool,
+                len_bound: int | None = None):
+        """One pass of the block (first [B], rest [rps-1][B]) at positions
+        pos_base + offset + j through the draft (or parent) model, writing its
+        cache entries; logits [B * (1 or rps)][V] f32 out."""
+        cfg, w, b = self.cfg, self.w, self.buf
+        B = self.B
+        M = B * rps
+        if M > b.h.shape[0] or (draft and M > 8):
+            raise ValueError("a pass takes at most 64 rows (8 for the draft GEMVs)")
+        cache = self.dcache if draft else self.pcache
+        lb = self.capacity if len_bound is None else len_bound
+        h, x, qkv, q, a, y, gu, t = (b.h[:M], b.x[:M], b.qkv[:M], b.q[:M], b.a[:M], b.y[:M], b.gu[:M], b.t[:M])
+        sq.sq_embed_block_f16(w.embed, first, rest, h=h, status=self.status)
+        delta = None
+        for l in range(w.layers):
+            sq.sq_add_rmsnorm_f16(h, w.in_norm[l], EPS, delta=delta, x=x)
+            self._linear(draft, (l, "qkv"), x, qkv)
+            sq.sq_rope_kv_f16(qkv, w.qkv_bias[l], self.pos_base, offset, rps, cfg.q_heads, cache.k[l], cache.v[l],
+                              len_bound=lb, theta=THETA, q_out=q, status=self.status)
+            sq.sq_attention_f16(q, cache.k[l], cache.v[l], self.pos_base, offset, rps, len_bound=lb, out=a)
+            self._linear(draft, (l, "o"), a.view(M, cfg.q_dim), y)
+            sq.sq_add_rmsnorm_f16(h, w.post_norm[l], EPS, delta=y, x=x)
+            self._linear(draft, (l, "gate_up"), x, gu)
+            sq.sq_silu_mul_f16(gu, t)
+            self._linear(draft, (l, "down"), t, y)
+            delta = y
+        group = rps if last_only else 1
+        xf = b.xf[:M // group]
+        sq.sq_add_rmsnorm_f16(h, w.final_norm, EPS, delta=delta, group=group, x=xf)
+        self._linear(draft, (cfg.layers, "lm_head"), xf, logits)
+
+    def prefill(self, prompt: torch.Tensor, chunk: int | None = None):
+        """Feed prompt [B][Lp] (int32, Lp >= 2) but its last token to both
+        models; the last token becomes the pending one at position Lp - 1."""
+        B, Lp = prompt.shape
+        if B != self.B or Lp < 2 or Lp > self.capacity:
+            raise ValueError("prompt must be [batch][2 .. capacity]")
+        prompt = prompt.to(device=self.device, dtype=torch.int32)
+        self.pos_base.zero_()
+        V = self.cfg.vocab
+        for draft in (True, False):
+            limit = 8 if draft else 64
+            c = max(1, min(chunk or limit, limit // B))
+            for s in range(0, Lp - 1, c):
+                n = min(c, Lp - 1 - s)
+                first = prompt[:, s].contiguous()
+                rest = prompt[:, s + 1:s + n].t().contiguous() if n > 1 else None
+                logits = torch.empty((B * n, V), dtype=torch.float32, device=self.device)
+                self.forward(draft, first, rest, n, s, logits, last_only=False, len_bound=s + n)
+        self.pos_base.fill_(Lp - 1)
+        self.pending.copy_(prompt[:, Lp - 1])
+        self.prev.copy_(prompt[:, Lp - 2])
+        self.out_len.zero_()
+
+    # -------------------------------------------------------------- round
+    def draft_step(self, i: int):
+        B, V = self.B, self.cfg.vocab
+        if i == 0:
+            self.forward(True, self.prev, self.pending.view(1, B), 2, -1, self.draft_logits[0], last_only=True)
+        else:
+            self.forward(True, self.draft_tokens[i - 1], None, 1, i, self.draft_logits[i], last_only=True)
+        p_out = self.q_draft[i].view(B, 1, V) if self.keep_pq and self.T > 0 else None
+        sq.sq_spec_accept(None, self.draft_logits[i].view(B, 1, V), None, self.u_draft[i].view(B, 1), self.T,
+                          n_accepted=self.scratch_n, next_token=self.draft_tokens[i], p_out=p_out)
+
+    def verify(self):
+        B, k, V = self.B, self.k, self.cfg.vocab
+        self.forward(False, self.pending, self.draft_tokens, k + 1, 0, self.target_logits.view(B * (k + 1), V),
+                     last_only=False)
+
+    def accept_and_commit(self):
+        keep = self.keep_pq and self.T > 0
+        sq.sq_spec_accept(self.draft_logits, self.target_logits, self.draft_tokens, self.u_accept, self.T,
+                          n_accepted=self.n_accepted, next_token=self.next_token,
+                          q_out=self.q_out if keep else None, p_out=self.p_out if keep else None)
+        sq.sq_spec_commit(self.n_accepted, self.next_token, self.draft_tokens, self.pending, self.prev,
+                          self.pos_base, out_tokens=self.out_tokens, out_len=self.out_len, status=self.status)
+
+    def run(self):
+        for i in range(self.k):
+            self.draft_step(i)
+        self.verify()
+        self.accept_and_commit()
+
+    def set_uniforms(self, u_draft: torch.Tensor, u_accept: torch.Tensor):
+        self.u_draft.copy_(u_draft)
+        self.u_accept.copy_(u_accept)
+
+    def capture(self):
+        """Capture one round as a HIP graph.  Runs one round eagerly first (it
+        advances the sequences by one round), so that the library workspace
+        has its final size before capture."""
+        self.run()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.run()
+        torch.cuda.synchronize()
+        self.graph = g
+        return g
+
+    def replay(self):
+        self.graph.replay()
+
+
+def synthetic_prompt(cfg: Config, batch: int, length: int, device) -> torch.Tensor:
+    """Uniform random token ids [batch][length] from the config seed."""
+    return synth.tokens((batch, length), cfg.vocab, synth.stream_seed(cfg.seed, _PROMPT, length), device)

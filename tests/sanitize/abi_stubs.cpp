@@ -70,6 +70,16 @@ STUB(launch_spec_accept, const float*, const float*, const int32_t*, const uint3
      int32_t*, float*, float*, hipStream_t)
 STUB(launch_spec_accept_noalloc, const float*, const float*, const int32_t*, const uint32_t*, int, int, int, float,
      int32_t*, int32_t*, float*, float*, hipStream_t)
+STUB(launch_embed_block, const uint16_t*, int64_t, int, const int32_t*, const int32_t*, int, int, float*, int32_t*,
+     hipStream_t)
+STUB(launch_add_rmsnorm, float*, const float*, int64_t, int, const uint16_t*, float, int, uint16_t*, hipStream_t)
+STUB(launch_rope_kv, const float*, const uint16_t*, int, int, int, int, const int32_t*, int, int64_t, int64_t, double,
+     uint16_t*, uint16_t*, uint16_t*, int32_t*, hipStream_t)
+STUB(launch_attention, const uint16_t*, const uint16_t*, const uint16_t*, int, int, int, int, int64_t, const int32_t*,
+     int, int64_t, uint16_t*, hipStream_t)
+STUB(launch_silu_mul, const float*, int64_t, int64_t, uint16_t*, hipStream_t)
+STUB(launch_spec_commit, const int32_t*, const int32_t*, const int32_t*, int, int, int32_t*, int32_t*, int32_t*,
+     int32_t*, int64_t, int32_t*, int32_t*, hipStream_t)
 size_t spec_accept_scratch_bytes(int b, int kd, int v, float) {
   const size_t c = (size_t)(v + 4095) / 4096;
   return 16 * (size_t)b * (2 * kd + 1) * c + 16 * (size_t)b * c + 40 * (size_t)b;

@@ -31,11 +31,13 @@ def test_library_exports_every_declared_symbol():
     names = declared_symbols()
     assert set(names) == {"sq_abi_version", "sq_status_str", "sq_quantize_int4_g128", "sq_quantize_fp8_e4m3",
                           "sq_qgemv_w4a16", "sq_qgemv_w8a16", "sq_verify_gemm_f16", "sq_spec_accept",
-                          "sq_spec_accept_noalloc", "sq_probe_stream_read"}
+                          "sq_spec_accept_noalloc", "sq_probe_stream_read", "sq_embed_block_f16",
+                          "sq_add_rmsnorm_f16", "sq_rope_kv_f16", "sq_attention_f16", "sq_silu_mul_f16",
+                          "sq_spec_commit"}
     assert set(names) == set(sq.EXPORTED)
     for n in names:
         assert hasattr(lib, n), n
-    assert sq.sq_abi_version() == 2
+    assert sq.sq_abi_version() == 3
     for s in range(9):
         assert lib.sq_status_str(s).startswith(b"SQ_")
     assert lib.sq_status_str(9) == b"unknown sq_status"
@@ -138,3 +140,61 @@ def test_binding_fails_loudly_without_gpu_tensors():
     torch = pytest.importorskip("torch")
     with pytest.raises(ValueError):
         sq.sq_quantize_int4_g128(torch.zeros((4, 128), dtype=torch.float16))
+
+
+def test_decoder_layer_validation():
+    lib = sq.load()
+    emb = lib.sq_embed_block_f16
+    assert emb(None, 100, 64, B, None, 2, 0, C, None, None) == NULL
+    assert emb(A, 100, 64, B, None, 2, 3, C, None, None) == NULL          # kd > 0 needs rest
+    assert emb(A, 100, 60, B, None, 2, 0, C, None, None) == SHAPE         # hidden % 8
+    assert emb(A, 100, 64, B, D, 2, 64, C, None, None) == SHAPE           # kd <= 63
+    assert emb(A, 0, 64, B, None, 2, 0, C, None, None) == SHAPE
+    assert emb(A + 8, 100, 64, B, None, 2, 0, C, None, None) == ALIGN
+    assert emb(A, 100, 64, B, None, 2, 0, C + 4, None, None) == ALIGN
+    assert emb(A, 100, 64, B, None, 2, 0, A + 256, None, None) == ALIAS    # h inside the table
+    nrm = lib.sq_add_rmsnorm_f16
+    assert nrm(A, None, 4, 64, None, 1e-6, 1, C, None) == NULL
+    assert nrm(A, None, 5, 64, B, 1e-6, 2, C, None) == SHAPE              # m % group
+    assert nrm(A, None, 4, 68, B, 1e-6, 1, C, None) == SHAPE
+    assert nrm(A, None, 4, 64, B, float("nan"), 1, C, None) == NONFINITE
+    assert nrm(A, None, 4, 64, B, -1.0, 1, C, None) == SHAPE
+    assert nrm(A, D + 4, 4, 64, B, 1e-6, 1, C, None) == ALIGN
+    assert nrm(A, None, 4, 64, B, 1e-6, 1, A + 512, None) == ALIAS        # x inside h
+    assert nrm(A, A + 16, 4, 64, B, 1e-6, 1, C, None) == ALIAS            # delta overlaps h
+    rope = lib.sq_rope_kv_f16
+    args = dict(qkv=A, bias=None, b=1, rps=5, hq=28, hkv=4, pos=B, off=0, lb=1024, cap=1024, theta=1e6,
+                q=C, kc=D, vc=E, st=None)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return rope(a["qkv"], a["bias"], a["b"], a["rps"], a["hq"], a["hkv"], a["pos"], a["off"], a["lb"],
+                    a["cap"], a["theta"], a["q"], a["kc"], a["vc"], a["st"], None)
+    assert call(qkv=None) == NULL
+    assert call(cap=1000, lb=1000) == SHAPE            # capacity % 64
+    assert call(lb=2048) == SHAPE                      # len_bound > capacity
+    assert call(hq=30) == SHAPE                        # hq % hkv
+    assert call(rps=65) == SHAPE
+    assert call(theta=float("inf")) == NONFINITE
+    assert call(theta=1.0) == SHAPE
+    assert call(pos=B + 2) == ALIGN
+    assert call(q=D + 4096) == ALIAS                   # q_out inside the key cache
+    assert call(vc=D + 64) == ALIAS                    # the two caches overlap
+    att = lib.sq_attention_f16
+    assert att(A, None, E, 1, 5, 28, 4, B, 0, 1024, 1024, C, None) == NULL
+    assert att(A, D, E, 1, 5, 28, 4, B, 0, 1024, 1000, C, None) == SHAPE
+    assert att(A, D, E, 1, 5, 28, 4, B, 0, 0, 1024, C, None) == SHAPE
+    assert att(A, D, E, 1, 5, 28, 4, B, 0, 1024, 1024, A + 128, None) == ALIAS   # out overlaps q
+    assert att(A, D + 8, E, 1, 5, 28, 4, B, 0, 1024, 1024, C, None) == ALIGN
+    silu = lib.sq_silu_mul_f16
+    assert silu(None, 4, 8, B, None) == NULL
+    assert silu(A, 1 << 21, 1 << 20, B, None) == SHAPE
+    assert silu(A, 4, 8, A + 16, None) == ALIAS
+    com = lib.sq_spec_commit
+    assert com(A, B, None, 4, 3, C, D, E, None, 0, None, None, None) == NULL     # kd > 0 needs draft tokens
+    assert com(A, B, A + 4096, 4, 3, C, D, E, C + 4096, 16, None, None, None) == NULL  # history needs out_len
+    assert com(A, B, A + 4096, 0, 3, C, D, E, None, 0, None, None, None) == SHAPE
+    assert com(A, B, A + 4096, 4, 65, C, D, E, None, 0, None, None, None) == SHAPE
+    assert com(A, B, A + 4096, 4, 3, C, C + 8, E, None, 0, None, None, None) == ALIAS   # prev overlaps pending
+    assert com(A, B, A + 4096, 4, 3, C, D, A + 4, None, 0, None, None, None) == ALIAS   # pos_base on n_accepted
+    assert com(A, B, A + 4096, 4, 3, C + 2, D, E, None, 0, None, None, None) == ALIGN

@@ -1,0 +1,378 @@
+"""GPU parity of the decoder layer around the projections (SS III-D.2 /
+III-D.3 for the Qwen2.5 family of SS IV) and of speculative rounds that carry
+their key/value caches from round to round (restart after a rejection,
+SS III-D.4), against the fp64 oracle in ``oracle.decoder``.
+
+Per operation, the oracle gets the exact bytes the kernel got.  Tolerances:
+  - rmsnorm / rope / silu write binary16: at most one binary16 ulp from the
+    oracle's value rounded once (the kernels compute in fp32, the oracle in
+    fp64, so a value within 2^-20 relative of a rounding boundary may round
+    the other way);
+  - attention: the kernel carries each softmax weight as two binary16 terms
+    (about 2^-22 relative) into the matrix-core product with the values and
+    rounds its output once to binary16, so |out - ref| <= ulp16(ref) + 2^-16
+    max |v|;
+  - whole passes and rounds are teacher-forced: the oracle runs the GPU's
+    tokens through its own layers and its own cache.  Both sides round at the
+    same binary16 boundaries (attention output, normalised activations, the
+    SiLU product, the cache), and each boundary turns the other side's tiny
+    relative differences into 1-ulp flips that the next projection sums: one
+    layer measured a -> x2 -> t -> final x flip fractions of 5%, 19%, 52%, 55%
+    and logits within 2.2e-3 (max) and 3.5e-4 (mean) of their rms, while the
+    LM head alone, given the same input, agrees to 4e-7.  The bound is max
+    1e-2 and mean 2e-3 of the rms, for logits and cache entries alike, which
+    any wiring, position or cache error exceeds by orders of magnitude; every
+    draw and accept decision must equal the oracle's decision on the kernel's
+    own fp32 distributions, bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import decoder as od
+
+import paper_2609_21704_amd as sq
+from paper_2609_21704_amd import decoder as dec
+from paper_2609_21704_amd import synth
+from paper_2609_21704_amd.configs import CONFIGS
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+D = 128
+
+
+def gen(seed):
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    return g
+
+
+def ulp16(ref):
+    """binary16 ulp at |ref| (subnormal spacing below 2^-14)."""
+    a = np.abs(np.asarray(ref, np.float64))
+    e = np.floor(np.log2(np.maximum(a, 2.0 ** -14)))
+    return 2.0 ** (e - 10)
+
+
+def assert_within_ulp16(got, ref, what):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    err = np.abs(got - ref)
+    ok = err <= ulp16(ref) * 1.0000001
+    assert ok.all(), f"{what}: {np.count_nonzero(~ok)} values beyond one ulp, worst {err.max():.3e}"
+
+
+# ------------------------------------------------------------------- embed
+def test_embed_block_exact_and_bad_tokens():
+    V, H, B, kd = 1000, 896, 3, 4
+    table = torch.randn((V, H), generator=gen(1)).half().to(DEV)
+    first = torch.tensor([5, 999, 0], dtype=torch.int32, device=DEV)
+    rest = torch.randint(0, V, (kd, B), generator=gen(2), dtype=torch.int32).to(DEV)
+    rest[2, 1] = -1
+    rest[3, 2] = V
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    h = sq.sq_embed_block_f16(table, first, rest, status=status)
+    torch.cuda.synchronize()
+    tab = table.cpu().float().numpy()
+    toks = np.concatenate([first.cpu().numpy()[:, None], rest.cpu().numpy().T], axis=1)
+    got = h.cpu().numpy()
+    for b in range(B):
+        for j in range(kd + 1):
+            t = toks[b, j]
+            if 0 <= t < V:
+                assert np.array_equal(got[b, j], tab[t])
+            else:
+                assert np.isnan(got[b, j]).all()
+    assert status.item() == sq._lib.DEV_BAD_TOKEN
+
+
+# ------------------------------------------------------------ add + rmsnorm
+@pytest.mark.parametrize("m,hidden,group", [(6, 3584, 1), (6, 3584, 3), (5, 896, 5), (2, 8, 1), (3, 5120, 1)])
+def test_add_rmsnorm(m, hidden, group):
+    g = gen(m * hidden + group)
+    h0 = (torch.randn((m, hidden), generator=g) * 5).float()
+    delta = (torch.randn((m, hidden), generator=g) * 3).float()
+    w = (1 + 0.1 * torch.randn((hidden,), generator=g)).half()
+    h = h0.to(DEV)
+    x = sq.sq_add_rmsnorm_f16(h, w.to(DEV), 1e-6, delta=delta.to(DEV), group=group)
+    torch.cuda.synchronize()
+    hn = (h0.numpy() + delta.numpy()).astype(np.float32)  # one IEEE fp32 add
+    assert np.array_equal(h.cpu().numpy(), hn)
+    rows = np.arange(group - 1, m, group)
+    ref = oracle.rmsnorm(hn[rows].astype(np.float64), w.float().numpy(), 1e-6)
+    assert_within_ulp16(x.cpu().float().numpy(), od.f16(ref).astype(np.float64), "rmsnorm")
+    # no delta: plain normalisation, h untouched
+    h2 = h0.to(DEV)
+    x2 = sq.sq_add_rmsnorm_f16(h2, w.to(DEV), 1e-6)
+    torch.cuda.synchronize()
+    assert torch.equal(h2.cpu(), h0)
+    ref2 = oracle.rmsnorm(h0.numpy().astype(np.float64), w.float().numpy(), 1e-6)
+    assert_within_ulp16(x2.cpu().float().numpy(), od.f16(ref2).astype(np.float64), "rmsnorm without delta")
+
+
+# -------------------------------------------------------- rope + cache write
+@pytest.mark.parametrize("hq,hkv,rps,pos_base,offset", [(28, 4, 5, [0, 200], 3), (12, 2, 1, [7, 4000], 0),
+                                                        (7, 1, 64, [0], 0), (40, 8, 2, [63, 1], -1)])
+def test_rope_kv(hq, hkv, rps, pos_base, offset):
+    B = len(pos_base)
+    cap = 4096
+    m = B * rps
+    nh = hq + 2 * hkv
+    g = gen(hq * 100 + rps)
+    qkv = (torch.randn((m, nh * D), generator=g) * 1.2).float()
+    bias = (torch.randn((nh * D,), generator=g) * 0.02).half()
+    kc = torch.full((B, hkv, cap, D), 1.0, dtype=torch.float16, device=DEV)
+    vc = torch.full((B, hkv, D, cap), 1.0, dtype=torch.float16, device=DEV)
+    pb = torch.tensor(pos_base, dtype=torch.int32, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    q = sq.sq_rope_kv_f16(qkv.to(DEV), bias.to(DEV), pb, offset, rps, hq, kc, vc, theta=1e6, status=status)
+    torch.cuda.synchronize()
+    assert status.item() == 0
+    u = qkv.numpy().astype(np.float64) + bias.float().numpy().astype(np.float64)
+    pos = np.array([p + offset + j for p in pos_base for j in range(rps)])
+    rq = oracle.rope(u[:, :hq * D].reshape(m, hq, D), pos, 1e6)
+    rk = oracle.rope(u[:, hq * D:(hq + hkv) * D].reshape(m, hkv, D), pos, 1e6)
+    # values: the fp32 sum qkv + bias (one IEEE fp32 add, as the call defines u) rounded once to binary16
+    u32 = (qkv.numpy() + bias.float().numpy()).astype(np.float32)
+    rv = u32[:, (hq + hkv) * D:].reshape(m, hkv, D).astype(np.float64)
+    assert_within_ulp16(q.cpu().float().numpy(), od.f16(rq).astype(np.float64), "q")
+    kn = kc.cpu().float().numpy()
+    vn = vc.cpu().float().numpy()
+    written = np.zeros((B, cap), bool)
+    for r in range(m):
+        b = r // rps
+        written[b, pos[r]] = True
+        assert_within_ulp16(kn[b, :, pos[r]], od.f16(rk[r]).astype(np.float64), "k")
+        assert np.array_equal(vn[b, :, :, pos[r]], od.f16(rv[r]).astype(np.float64))
+    assert (kn[~written[:, None, :].repeat(hkv, 1)] == 1.0).all()
+    assert (np.moveaxis(vn, 3, 2)[~written[:, None, :].repeat(hkv, 1)] == 1.0).all()
+
+
+def test_rope_kv_bad_positions():
+    B, rps, hq, hkv, cap = 2, 5, 8, 2, 256
+    nh = hq + 2 * hkv
+    qkv = torch.randn((B * rps, nh * D), generator=gen(5)).float().to(DEV)
+    kc = torch.zeros((B, hkv, cap, D), dtype=torch.float16, device=DEV)
+    vc = torch.zeros((B, hkv, D, cap), dtype=torch.float16, device=DEV)
+    pb = torch.tensor([250, 0], dtype=torch.int32, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    q = sq.sq_rope_kv_f16(qkv, None, pb, 3, rps, hq, kc, vc, status=status)
+    torch.cuda.synchronize()
+    assert status.item() == sq._lib.DEV_BAD_POS
+    qn = q.cpu().float().numpy()
+    # sequence 0 rows at 253 .. 257: the last two are past the cache
+    assert np.isfinite(qn[:3]).all() and np.isnan(qn[3:5]).all() and np.isfinite(qn[5:]).all()
+    assert kc[0, :, 253:256].abs().sum().item() > 0
+
+
+# ---------------------------------------------------------------- attention
+ATT_CASES = [
+    # hq, hkv, rps, pos_base, offset, capacity, q scale
+    (28, 4, 5, [700], 0, 1024, 1.5),         # 7B verification block
+    (28, 4, 1, [1000], 0, 1024, 1.5),        # 7B draft step
+    (28, 4, 2, [1, 63, 64, 500], -1, 1024, 1.5),  # draft step 0, chunk edges
+    (12, 2, 9, [5, 130, 257, 900], 0, 1024, 4.0),  # 1.5B heads, k = 8, peaked scores
+    (40, 8, 7, [2000], 0, 2048, 1.5),        # 32B heads
+    (7, 1, 64, [0], 0, 128, 1.5),            # a 64-row prefill chunk, 448 query rows
+    (8, 8, 3, [127, 128], 0, 256, 1.5),      # one query head per kv head
+]
+
+
+@pytest.mark.parametrize("hq,hkv,rps,pos_base,offset,cap,qs", ATT_CASES)
+def test_attention(hq, hkv, rps, pos_base, offset, cap, qs):
+    B = len(pos_base)
+    m = B * rps
+    g = gen(hq * 7 + rps * 3 + cap)
+    q = (torch.randn((m, hq, D), generator=g) * qs).half()
+    kc = torch.randn((B, hkv, cap, D), generator=g).half()
+    vc = torch.randn((B, hkv, D, cap), generator=g).half()
+    last = [p + offset + rps - 1 for p in pos_base]
+    for b in range(B):  # stale entries past the block: NaN, never read
+        kc[b, :, last[b] + 1:] = float("nan")
+        vc[b, :, :, last[b] + 1:] = float("nan")
+    pb = torch.tensor(pos_base, dtype=torch.int32, device=DEV)
+    out = sq.sq_attention_f16(q.to(DEV), kc.to(DEV), vc.to(DEV), pb, offset, rps)
+    torch.cuda.synchronize()
+    got = out.cpu().float().numpy()
+    assert np.isfinite(got).all()
+    for b in range(B):
+        L = last[b] + 1
+        pos = np.array([pos_base[b] + offset + j for j in range(rps)])
+        K = kc[b, :, :L].float().numpy().astype(np.float64)
+        Vv = np.swapaxes(vc[b, :, :, :L].float().numpy(), 1, 2).astype(np.float64)
+        ref = oracle.attention(q[b * rps:(b + 1) * rps].float().numpy().astype(np.float64), K, Vv, pos)
+        vmax = np.abs(Vv).max()
+        err = np.abs(got[b * rps:(b + 1) * rps] - ref)
+        tol = ulp16(ref) + 2.0 ** -16 * vmax
+        assert (err <= tol).all(), f"sequence {b}: worst {err.max():.3e}"
+
+
+# --------------------------------------------------------------------- silu
+@pytest.mark.parametrize("m,inter", [(5, 18944), (1, 8960), (3, 7)])
+def test_silu_mul(m, inter):
+    gu = (torch.randn((m, 2 * inter), generator=gen(inter)) * 3).float()
+    t = sq.sq_silu_mul_f16(gu.to(DEV))
+    torch.cuda.synchronize()
+    ref = oracle.silu_mul(gu.numpy().astype(np.float64))
+    assert_within_ulp16(t.cpu().float().numpy(), od.f16(ref).astype(np.float64), "silu")
+
+
+# ------------------------------------------------------------------- commit
+def test_spec_commit_matches_oracle():
+    B, kd, cap = 5, 4, 6
+    n = torch.tensor([0, 4, 2, -1, 3], dtype=torch.int32)
+    nxt = torch.tensor([11, 12, 13, 14, 15], dtype=torch.int32)
+    drafts = torch.randint(0, 1000, (kd, B), generator=gen(9), dtype=torch.int32)
+    pending = torch.tensor([1, 2, 3, 4, 5], dtype=torch.int32)
+    prev = torch.tensor([6, 7, 8, 9, 10], dtype=torch.int32)
+    pos = torch.tensor([10, 20, 30, 40, 50], dtype=torch.int32)
+    out = torch.full((B, cap), -7, dtype=torch.int32)
+    out_len = torch.tensor([0, 1, 5, 0, 2], dtype=torch.int32)
+    d = {k: v.to(DEV) for k, v in dict(n=n, nxt=nxt, drafts=drafts, pending=pending, prev=prev, pos=pos,
+                                       out=out, out_len=out_len).items()}
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    sq.sq_spec_commit(d["n"], d["nxt"], d["drafts"], d["pending"], d["prev"], d["pos"], out_tokens=d["out"],
+                      out_len=d["out_len"], status=status)
+    torch.cuda.synchronize()
+    st = od.SpecState(pos=pos.numpy().astype(np.int64), pending=pending.numpy().astype(np.int64),
+                      prev=prev.numpy().astype(np.int64), emitted=[[] for _ in range(B)])
+    od.commit(st, n.numpy(), nxt.numpy(), drafts.numpy())
+    assert d["pos"].cpu().tolist() == st.pos.tolist()
+    assert d["pending"].cpu().tolist() == st.pending.tolist()
+    assert d["prev"].cpu().tolist() == st.prev.tolist()
+    got_out, got_len = d["out"].cpu().numpy(), d["out_len"].cpu().numpy()
+    for b in range(B):
+        L0 = int(out_len[b])
+        exp_len = L0 + len(st.emitted[b])
+        assert got_len[b] == exp_len
+        hist = [-7] * cap
+        for i, t in enumerate(st.emitted[b]):
+            if L0 + i < cap:
+                hist[L0 + i] = t
+        assert got_out[b].tolist() == hist
+    assert status.item() == (sq._lib.DEV_OVERFLOW | sq._lib.DEV_NO_DIST)
+
+
+# ------------------------------------------- passes and rounds, teacher-forced
+def oracle_models(w, variant):
+    cfg = w.cfg
+    dims = od.Dims(w.layers, cfg.hidden, cfg.intermediate, cfg.q_heads, cfg.kv_heads, cfg.vocab,
+                   eps=dec.EPS, theta=dec.THETA)
+    params = w.params()
+    return dims, od.Model(dims, params, "f16"), od.Model(dims, params, variant)
+
+
+def gpu_cache(c, b, L):
+    """Host copy of sequence b's entries 0 .. L-1 in the oracle layout [layer][hkv][L][128]."""
+    k = np.stack([c.k[l][b, :, :L].float().cpu().numpy() for l in range(len(c.k))])
+    v = np.stack([np.swapaxes(c.v[l][b, :, :, :L].float().cpu().numpy(), 1, 2) for l in range(len(c.v))])
+    return k, v
+
+
+def check_close(got, ref, what, max_tol=1e-2, mean_tol=2e-3):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert np.isfinite(ref).all() and np.isfinite(got).all(), what
+    rms = np.sqrt(np.mean(ref * ref))
+    d = np.abs(got - ref) / rms
+    assert d.max() <= max_tol and d.mean() <= mean_tol, \
+        f"{what}: |error| / rms max {d.max():.3e} mean {d.mean():.3e}"
+    return d.max()
+
+
+check_logits = check_close
+
+
+def check_probs(got, ref_logits, gpu_logits, what):
+    """The kernel's fp32 distribution against the oracle's softmax of the
+    oracle's logits: they differ through the logits, by about p * |dlogit|."""
+    ref = oracle.softmax(np.asarray(ref_logits, np.float32))
+    dl = np.abs(np.asarray(gpu_logits, np.float64) - ref_logits).max()
+    err = np.abs(np.asarray(got, np.float64) - ref)
+    assert (err <= 1e-7 + ref * (2.5 * dl + 1e-5)).all(), f"{what}: worst {err.max():.3e} (logit error {dl:.2e})"
+
+
+def check_cache(sd_cache, o_cache, b, L, what):
+    k, v = gpu_cache(sd_cache, b, L)
+    for name, g, r in (("k", k, o_cache.k[:, b, :, :L]), ("v", v, o_cache.v[:, b, :, :L])):
+        check_close(g, r, f"{what} {name}")
+
+
+ROUND_CASES = [
+    # config, layers, batch, k, temperature, rounds, prompt length, variant
+    (0, 1, 1, 4, 1.0, 4, 40, "int4"),
+    (0, 1, 2, 3, 0.0, 3, 70, "fp8"),
+    (1, 2, 1, 4, 1.0, 3, 24, "int4"),
+    (1, 2, 4, 8, 1.0, 2, 9, "fp8"),
+]
+
+
+@pytest.mark.parametrize("ci,layers,B,k,T,rounds,lp,variant", ROUND_CASES)
+def test_rounds_teacher_forced(ci, layers, B, k, T, rounds, lp, variant):
+    cfg = CONFIGS[ci]
+    print(f"\n[rounds] config {ci} layers {layers} B {B} k {k} T {T} {variant}", flush=True)
+    w = dec.DecoderWeights(cfg, DEV, layers=layers, variant=variant)
+    cap = 128
+    sd = dec.SpecDecoder(w, batch=B, k=k, capacity=cap, temperature=T, keep_pq=True)
+    prompt = dec.synthetic_prompt(cfg, B, lp, DEV)
+    sd.prefill(prompt)
+    torch.cuda.synchronize()
+    dims, parent, draft = oracle_models(w, variant)
+    dc, pc = od.Cache(dims, B, cap), od.Cache(dims, B, cap)
+    st = od.prefill([draft, parent], [dc, pc], prompt.cpu().numpy())
+    for b in range(B):
+        check_cache(sd.pcache, pc, b, lp - 1, "parent cache after prefill")
+        check_cache(sd.dcache, dc, b, lp - 1, "draft cache after prefill")
+    V = w.cfg.vocab
+    ud = synth.uniform_u24((rounds, k, B), synth.stream_seed(cfg.seed, 90, B, k), DEV)
+    ua = synth.uniform_u24((rounds, B, k + 1), synth.stream_seed(cfg.seed, 91, B, k), DEV)
+    worst = 0.0
+    n_all = []
+    for r in range(rounds):
+        sd.set_uniforms(ud[r], ua[r])
+        sd.run()
+        torch.cuda.synchronize()
+        assert sd.status.item() == 0
+        dt = sd.draft_tokens.cpu().numpy().astype(np.int64)
+        dl = sd.draft_logits.cpu().numpy()
+        tl = sd.target_logits.cpu().numpy()
+        n_gpu = sd.n_accepted.cpu().numpy()
+        nx_gpu = sd.next_token.cpu().numpy()
+        P = st.pos.copy()
+        for i in range(k):
+            if i == 0:
+                toks, pos = np.stack([st.prev, st.pending], 1), np.stack([P - 1, P], 1)
+            else:
+                toks, pos = dt[i - 1][:, None], (P + i)[:, None]
+            ref = od.forward(draft, dc, toks, pos)[:, -1]
+            worst = max(worst, check_logits(dl[i], ref, f"round {r} draft step {i}"))
+            if T > 0:
+                qd = sd.q_draft[i].cpu().numpy()  # the sampler's fp32 distribution [B][V]
+                _, tok = oracle.accept_probs(qd[:, None, :], None, None,
+                                             ud[r, i].cpu().numpy().astype(np.uint32)[:, None])
+                assert np.array_equal(tok, dt[i]), f"round {r} draft draw {i}"
+                check_probs(qd, ref, dl[i], f"round {r} draft distribution {i}")
+            else:
+                assert np.array_equal(np.argmax(dl[i], axis=1), dt[i])
+        block = np.concatenate([st.pending[:, None], dt.T], 1)
+        ref_t = od.forward(parent, pc, block, P[:, None] + np.arange(k + 1)[None, :])
+        worst = max(worst, check_logits(tl, ref_t, f"round {r} verification"))
+        if T > 0:
+            p_out, q_out = sd.p_out.cpu().numpy(), sd.q_out.cpu().numpy()
+            n_o, nx_o = oracle.accept_probs(p_out, q_out, dt.astype(np.int32), ua[r].cpu().numpy().astype(np.uint32))
+            check_probs(p_out.reshape(-1, V), ref_t.reshape(-1, V), tl.reshape(-1, V), f"round {r} parent distribution")
+        else:
+            n_o, nx_o, _, _ = oracle.spec_accept(dl, tl, dt.astype(np.int32), None, 0.0)
+        assert np.array_equal(n_o, n_gpu) and np.array_equal(nx_o, nx_gpu), f"round {r} decisions"
+        od.commit(st, n_gpu, nx_gpu, dt)
+        n_all.extend(n_gpu.tolist())
+        assert sd.pos_base.cpu().tolist() == st.pos.tolist()
+        assert sd.pending.cpu().tolist() == st.pending.tolist()
+        assert sd.prev.cpu().tolist() == st.prev.tolist()
+        out, out_len = sd.out_tokens.cpu().numpy(), sd.out_len.cpu().numpy()
+        for b in range(B):
+            assert out[b, :out_len[b]].tolist() == st.emitted[b]
+            check_cache(sd.pcache, pc, b, int(st.pos[b]), f"round {r} parent cache")
+            check_cache(sd.dcache, dc, b, int(st.pos[b]) - 1, f"round {r} draft cache")
+    print(f"[rounds] worst logit error / rms {worst:.2e}; accepted per round {n_all}", flush=True)
