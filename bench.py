@@ -462,6 +462,153 @@ def measure_direct(stack, temperature: float, steps: int, warmup: int):
     }
 
 
+DECODER_CONTEXT = 1024   # prompt tokens in both caches when the timed decoder rounds start
+DECODER_CAPACITY = 2048  # cache positions per sequence
+
+
+def measure_decoder(stack, temperature: float, steps: int, warmup: int):
+    """The same rounds through full decoder layers with key/value caches
+    (embedding, RMSNorm, q|k|v + bias, RoPE, causal GQA attention over the
+    cache, SiLU-gated product, residuals; the matrices are the stack's): a
+    synthetic prompt of DECODER_CONTEXT tokens is prefilled, then graph
+    replays of whole rounds are timed; each round commits its tokens and rolls
+    both caches back to the accepted prefix.  The attention calls of one eager
+    round are timed with events for their roofline (HBM: 512 bytes per cached
+    position and kv head, plus the queries and outputs)."""
+    import numpy as np
+    import torch
+
+    from paper_2609_21704_amd import decoder as dec
+    from paper_2609_21704_amd import synth
+
+    cfg = stack.cfg
+    B, k = cfg.batch, cfg.k
+    w = dec.DecoderWeights(cfg, stack.device, stack=stack)
+    sd = dec.SpecDecoder(w, capacity=DECODER_CAPACITY, temperature=temperature)
+    sd.prefill(dec.synthetic_prompt(cfg, B, DECODER_CONTEXT, stack.device))
+    total = 2 + warmup + steps  # round 0: eager attention timing, round 1: the eager run of capture
+    ud = synth.uniform_u24((total, k, B), synth.stream_seed(cfg.seed, 120), stack.device)
+    ua = synth.uniform_u24((total, B, k + 1), synth.stream_seed(cfg.seed, 121), stack.device)
+    n_hist = torch.zeros((total, B), dtype=torch.int32, device=stack.device)
+
+    # round 0, eager: events around every attention call (positions are fixed until the commit)
+    calls = []
+
+    def hook(start, rps, offset):
+        ev = torch.cuda.Event(enable_timing=True)
+        ev.record()
+        if start:
+            calls.append([ev, None, rps, offset])
+        else:
+            calls[-1][1] = ev
+
+    pos = sd.pos_base.cpu().numpy().astype(np.int64)
+    sd.attn_hook = hook
+    sd.set_uniforms(ud[0], ua[0])
+    sd.run()
+    sd.attn_hook = None
+    torch.cuda.synchronize()
+    n_hist[0].copy_(sd.n_accepted)
+    att_bytes, att_sec = 0.0, 0.0
+    for e0, e1, rps, offset in calls:
+        att_sec += e0.elapsed_time(e1) * 1e-3
+        last = pos + offset + rps - 1
+        att_bytes += float(((last + 1) * 512 * cfg.kv_heads).sum()) + 2 * B * rps * cfg.q_dim * 2
+
+    sd.set_uniforms(ud[1], ua[1])
+    sd.capture()
+    n_hist[1].copy_(sd.n_accepted)
+
+    def one(r):
+        sd.set_uniforms(ud[r], ua[r])
+        sd.replay()
+        n_hist[r].copy_(sd.n_accepted)
+
+    for r in range(2, 2 + warmup):
+        one(r)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    pos0 = sd.pos_base.clone()
+    e0.record()
+    for r in range(2 + warmup, total):
+        one(r)
+    e1.record()
+    torch.cuda.synchronize()
+    sec = e0.elapsed_time(e1) * 1e-3
+    n_acc = n_hist[2 + warmup:].cpu().numpy().astype(np.int64)
+    tokens = int((n_acc + 1).sum())
+    assert int((sd.pos_base - pos0).sum().item()) == tokens, "positions moved by the emitted tokens"
+    assert sd.status.item() == 0, "device status flags raised"
+    achieved = att_bytes / att_sec / 1e9
+    return {
+        "tokens_per_s": round(tokens / sec, 3),
+        "ms_per_round": round(sec / steps * 1e3, 4),
+        "rounds": steps,
+        "tokens_per_round": round(tokens / (steps * B), 4),
+        "acceptance_rate": round(float(n_acc.sum()) / (steps * B * k), 4),
+        "context_at_start": DECODER_CONTEXT,
+        "cache_capacity": DECODER_CAPACITY,
+        "what": "rounds through Qwen2.5-7B-shaped decoder layers (RMSNorm, q|k|v + bias, RoPE, GQA attention "
+                "over the KV cache, SiLU-gated MLP, residuals; random weights), the caches rolled back to the "
+                "accepted prefix each round",
+        "roofline_attention": {
+            "kernel": "attention over the cache (chunk partials + ordered merge), one eager round",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "calls": len(calls),
+            "avg_call_us": round(att_sec / len(calls) * 1e6, 3),
+            "algorithmic_bytes_per_call": round(att_bytes / len(calls), 1),
+        },
+    }
+
+
+def measure_attention_long(dev, context: int = 8192, batch: int = 4, rows: int = 9, iters: int = 20):
+    """The attention call alone at a bandwidth-sized shape: 4 sequences of
+    8192 cached positions with Qwen2.5-7B heads (28 q / 4 kv), 9 rows per
+    sequence (a k = 8 verification block), over rotating caches (so that no
+    cache level holds them between calls); HBM roofline of 512 bytes per
+    cached position and kv head plus the queries and outputs."""
+    import torch
+
+    import paper_2609_21704_amd as sq
+
+    hq, hkv = 28, 4
+    copies = 4
+    kc = [torch.randn((batch, hkv, context, 128), device=dev).half() for _ in range(copies)]
+    vc = [torch.randn((batch, hkv, 128, context), device=dev).half() for _ in range(copies)]
+    q = torch.randn((batch * rows, hq, 128), device=dev).half()
+    out = torch.empty_like(q)
+    pb = torch.full((batch,), context - rows, dtype=torch.int32, device=dev)
+    for i in range(3):
+        sq.sq_attention_f16(q, kc[i % copies], vc[i % copies], pb, 0, rows, out=out)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(iters):
+        sq.sq_attention_f16(q, kc[i % copies], vc[i % copies], pb, 0, rows, out=out)
+    e1.record()
+    torch.cuda.synchronize()
+    sec = e0.elapsed_time(e1) * 1e-3 / iters
+    nbytes = batch * hkv * context * 512 + 2 * batch * rows * hq * 128 * 2
+    del kc, vc
+    return {
+        "kernel": "attention over the cache (chunk partials + ordered merge)",
+        "shape": f"{batch} sequences x {context} cached positions, 28 q / 4 kv heads of 128, {rows} rows each",
+        "bound": "hbm",
+        "achieved": round(nbytes / sec / 1e9, 1),
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(nbytes / sec / 1e9 / HBM_PEAK_GBS, 4),
+        "avg_call_us": round(sec * 1e6, 3),
+        "algorithmic_bytes_per_call": nbytes,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -481,6 +628,7 @@ def main():
                     help="for rocprofv3 counter runs: one eager pass of every draft step (GEMVs and draws), then "
                          "the plain copy; prints nothing")
     ap.add_argument("--no-fp8", action="store_true", help="skip the FP8 draft GEMV roofline block")
+    ap.add_argument("--no-decoder", action="store_true", help="skip the rounds through full decoder layers")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -611,6 +759,9 @@ def main():
             "frac_of_probe_same_launches": round(achieved / probe["same_launches_gbs"], 4),
         },
     }
+    if not args.no_decoder:
+        out["decoder"] = measure_decoder(stack, args.temperature, args.steps, args.warmup)
+        out["decoder"]["roofline_attention_long"] = measure_attention_long(dev)
     if not args.no_fp8 and cfg.draft_variant == "int4":
         out["roofline_fp8"] = measure_fp8(args.gemv_steps, dev)
     if not args.no_cpu_baseline:

@@ -230,7 +230,7 @@ sq_status sq_spec_accept_noalloc(const float* draft_logits, const float* target_
  * tok(s, 0) = first[s] and tok(s, 1 + i) = rest[i][s] (rest position-major
  * [kd][b], as draft_tokens of sq_spec_accept): the pending token followed by
  * the drafted ones is the block the parent verifies.
- * table [vocab][hidden] fp16 (16-B aligned), hidden % 8 == 0, hidden <= 65536,
+ * table [vocab][hidden] fp16 (16-B aligned), hidden % 8 == 0, hidden <= 16384,
  * 1 <= vocab < 2^31; first [b]; rest [kd][b] (NULL when kd == 0);
  * h [b][kd+1][hidden] f32 out (16-B aligned); 1 <= b, 0 <= kd <= 63. */
 sq_status sq_embed_block_f16(const uint16_t* table, int64_t vocab, int64_t hidden, const int32_t* first,
@@ -244,7 +244,7 @@ sq_status sq_embed_block_f16(const uint16_t* table, int64_t vocab, int64_t hidde
  * row whose logits a draft step needs).  Sum of squares in fp32, the
  * reciprocal root in fp64.
  * h [m][hidden] f32 in/out; delta [m][hidden] f32 or NULL; w [hidden] fp16;
- * x [m / group][hidden] fp16 out.  hidden % 8 == 0, 8 <= hidden <= 65536,
+ * x [m / group][hidden] fp16 out.  hidden % 8 == 0, 8 <= hidden <= 16384,
  * 1 <= m < 2^31, m % group == 0; eps finite, >= 0.  16-B aligned arrays. */
 sq_status sq_add_rmsnorm_f16(float* h, const float* delta, int64_t m, int64_t hidden, const uint16_t* w,
                              float eps, int32_t group, uint16_t* x, hipStream_t stream);

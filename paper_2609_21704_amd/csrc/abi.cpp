@@ -167,7 +167,7 @@ inline sq_status device_status(hipError_t e) {
 
 constexpr int64_t kMaxK = int64_t(1) << 20;
 constexpr int64_t kMaxN = 0x7FFFFFFF;
-constexpr int64_t kMaxHidden = 65536;
+constexpr int64_t kMaxHidden = 16384;
 
 // Shared limits of the block layout of the rope / attention calls.
 sq_status check_block(int32_t b, int32_t rows_per_seq, int32_t hq, int32_t hkv, int64_t len_bound,

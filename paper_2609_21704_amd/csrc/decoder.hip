@@ -63,8 +63,12 @@ __global__ __launch_bounds__(256) void embed_kernel(const uint16_t* __restrict__
 }
 
 // ---------------------------------------------------- residual add + norm
-// One workgroup per row of h.  Every row gets the residual add; the rows
-// r * group + group - 1 are normalised into output row r.
+// One workgroup of 256 threads per row of h; thread i holds the float4 cells
+// i, i + 256, ... of the row in registers (NV of them: hidden <= 1024 NV), so
+// that every load of the row is issued before the first use.  Every row gets
+// the residual add; the rows r * group + group - 1 are normalised into output
+// row r.
+template <int NV>
 __global__ __launch_bounds__(256) void add_rmsnorm_kernel(float* __restrict__ h, const float* __restrict__ delta,
                                                           int hidden, const uint16_t* __restrict__ w, float eps,
                                                           int group, uint16_t* __restrict__ x) {
@@ -72,81 +76,87 @@ __global__ __launch_bounds__(256) void add_rmsnorm_kernel(float* __restrict__ h,
   const int64_t row = blockIdx.x;
   float* hr = h + row * hidden;
   const bool out_row = (row % group) == group - 1;
-  float ss = 0.f;
-  for (int c = threadIdx.x * 4; c < hidden; c += 1024) {
-    float4_t v = *reinterpret_cast<float4_t*>(hr + c);
-    if (delta) {
-      v += *reinterpret_cast<const float4_t*>(delta + row * hidden + c);
-      *reinterpret_cast<float4_t*>(hr + c) = v;
+  const int n4 = hidden >> 2;
+  float4_t v[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = (int)threadIdx.x + 256 * i;
+    v[i] = c < n4 ? reinterpret_cast<const float4_t*>(hr)[c] : float4_t{0.f, 0.f, 0.f, 0.f};
+  }
+  if (delta) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = (int)threadIdx.x + 256 * i;
+      if (c < n4) {
+        v[i] += reinterpret_cast<const float4_t*>(delta + row * hidden)[c];
+        reinterpret_cast<float4_t*>(hr)[c] = v[i];
+      }
     }
-    if (out_row) ss += (v[0] * v[0] + v[1] * v[1]) + (v[2] * v[2] + v[3] * v[3]);
   }
   if (!out_row) return;  // uniform across the workgroup
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) ss += (v[i][0] * v[i][0] + v[i][1] * v[i][1]) + (v[i][2] * v[i][2] + v[i][3] * v[i][3]);
   ss = wave_sum(ss);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
-  __syncthreads();  // the residual writes of this workgroup are visible after it too
+  __syncthreads();
   const float total = (red[0] + red[1]) + (red[2] + red[3]);
   const float r = (float)(1.0 / sqrt((double)total / (double)hidden + (double)eps));
   uint16_t* xr = x + (row / group) * hidden;
-  for (int c = threadIdx.x * 4; c < hidden; c += 1024) {
-    const float4_t v = *reinterpret_cast<const float4_t*>(hr + c);
-    const uint2 wb = *reinterpret_cast<const uint2*>(w + c);
-    const half4_t wh = __builtin_bit_cast(half4_t, wb);
-    half4_t o;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) o[e] = (half_t)(v[e] * r * (float)wh[e]);
-    *reinterpret_cast<uint2*>(xr + c) = __builtin_bit_cast(uint2, o);
+  for (int i = 0; i < NV; ++i) {
+    const int c = (int)threadIdx.x + 256 * i;
+    if (c < n4) {
+      const half4_t wh = __builtin_bit_cast(half4_t, reinterpret_cast<const uint2*>(w)[c]);
+      half4_t o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = (half_t)(v[i][e] * r * (float)wh[e]);
+      reinterpret_cast<uint2*>(xr)[c] = __builtin_bit_cast(uint2, o);
+    }
   }
 }
 
 // ------------------------------------------------- bias + RoPE + cache write
-// One wavefront per row; lane t handles the pair (t, t + 64) of every head.
+// One wavefront per (row, head); lane t handles the pair (t, t + 64).
 __global__ __launch_bounds__(64) void rope_kv_kernel(const float* __restrict__ qkv, const uint16_t* __restrict__ bias,
                                                      int hq, int hkv, int rps, const int32_t* __restrict__ pos_base,
                                                      int pos_offset, int64_t len_bound, int64_t capacity, double theta,
                                                      uint16_t* __restrict__ q_out, uint16_t* __restrict__ kc,
                                                      uint16_t* __restrict__ vc, int32_t* __restrict__ status) {
-  const int r = blockIdx.x;
+  const int r = blockIdx.x, hh = blockIdx.y;
   const int bi = r / rps, j = r - bi * rps;
   const int64_t pos = (int64_t)pos_base[bi] + pos_offset + j;
   const int t = threadIdx.x;
   const int nh = hq + 2 * hkv;
-  const float* row = qkv + (int64_t)r * nh * kHd;
   if (pos < 0 || pos >= len_bound) {
-    for (int hh = 0; hh < hq; ++hh) {
+    if (hh < hq) {
       q_out[((int64_t)r * hq + hh) * kHd + t] = kNanF16;
       q_out[((int64_t)r * hq + hh) * kHd + t + 64] = kNanF16;
     }
-    if (t == 0) flag(status, kBadPos);
+    if (t == 0 && hh == 0) flag(status, kBadPos);
     return;
   }
-  // angle pos * theta^(-2t/128) and its cosine and sine in fp64
-  const double ang = (double)pos * pow(theta, -2.0 * (double)t / (double)kHd);
-  double sn, cs;
-  sincos(ang, &sn, &cs);
-  const float c = (float)cs, s = (float)sn;
-  for (int hh = 0; hh < nh; ++hh) {
-    float a = row[hh * kHd + t], e = row[hh * kHd + t + 64];
-    if (bias) {
-      a += f16_bits_to_f32(bias[hh * kHd + t]);
-      e += f16_bits_to_f32(bias[hh * kHd + t + 64]);
-    }
-    if (hh < hq + hkv) {
-      const float ra = a * c - e * s, re = e * c + a * s;
-      if (hh < hq) {
-        uint16_t* qo = q_out + ((int64_t)r * hq + hh) * kHd;
-        qo[t] = f32_to_f16_bits(ra);
-        qo[t + 64] = f32_to_f16_bits(re);
-      } else {
-        uint16_t* ko = kc + (((int64_t)bi * hkv + (hh - hq)) * capacity + pos) * kHd;
-        ko[t] = f32_to_f16_bits(ra);
-        ko[t + 64] = f32_to_f16_bits(re);
-      }
-    } else {
-      uint16_t* vo = vc + ((int64_t)bi * hkv + (hh - hq - hkv)) * kHd * capacity + pos;
-      vo[(int64_t)t * capacity] = f32_to_f16_bits(a);
-      vo[(int64_t)(t + 64) * capacity] = f32_to_f16_bits(e);
-    }
+  const float* src = qkv + ((int64_t)r * nh + hh) * kHd;
+  float a = src[t], e = src[t + 64];
+  if (bias) {
+    a += f16_bits_to_f32(bias[hh * kHd + t]);
+    e += f16_bits_to_f32(bias[hh * kHd + t + 64]);
+  }
+  if (hh < hq + hkv) {
+    // angle pos * theta^(-2t/128) and its cosine and sine in fp64, the turn in fp32
+    const double ang = (double)pos * pow(theta, -2.0 * (double)t / (double)kHd);
+    double sn, cs;
+    sincos(ang, &sn, &cs);
+    const float c = (float)cs, sv = (float)sn;
+    const float ra = a * c - e * sv, re = e * c + a * sv;
+    uint16_t* dst = hh < hq ? q_out + ((int64_t)r * hq + hh) * kHd
+                            : kc + (((int64_t)bi * hkv + (hh - hq)) * capacity + pos) * kHd;
+    dst[t] = f32_to_f16_bits(ra);
+    dst[t + 64] = f32_to_f16_bits(re);
+  } else {
+    uint16_t* vo = vc + ((int64_t)bi * hkv + (hh - hq - hkv)) * kHd * capacity + pos;
+    vo[(int64_t)t * capacity] = f32_to_f16_bits(a);
+    vo[(int64_t)(t + 64) * capacity] = f32_to_f16_bits(e);
   }
 }
 
@@ -185,6 +195,28 @@ __global__ __launch_bounds__(64) void attn_chunk_kernel(const uint16_t* __restri
   if (key0 > pmax) return;  // no row reads this chunk (uniform); rows at negative positions mask every key
   const int lane = threadIdx.x, li = lane & 15, lg = lane >> 4;
   const half8_t zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
+  const int nqt = (nq + 15) >> 4;
+
+  // query fragments of tile qt: rows qi = 16 qt + li, dims 32 lg + 8 s .. +8
+  auto load_q = [&](int qt, half8_t(&qf)[4]) {
+    const int qi = 16 * qt + li;
+    const bool qok = qi < nq;
+    const int j = qok ? qi / G : 0, gg = qok ? qi - (qi / G) * G : 0;
+    const half8_t* qp =
+        reinterpret_cast<const half8_t*>(q + (((int64_t)bi * rps + j) * hq + g * G + gg) * kHd + 32 * lg);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) qf[s] = qok ? qp[s] : zero8;
+  };
+  // up to kPreTiles query tiles are loaded before the cache fragments, so
+  // that all of the wavefront's loads are in flight together
+  constexpr int kPreTiles = 4;
+  half8_t qpre[kPreTiles][4];
+  const bool pre = nqt <= kPreTiles;
+  if (pre) {
+#pragma unroll
+    for (int qt = 0; qt < kPreTiles; ++qt)
+      if (qt < nqt) load_q(qt, qpre[qt]);
+  }
 
   half8_t kf[4][4];
 #pragma unroll
@@ -215,18 +247,12 @@ __global__ __launch_bounds__(64) void attn_chunk_kernel(const uint16_t* __restri
   }
 
   const float sl2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
-  const int nqt = (nq + 15) >> 4;
   float* po = part_o + ((int64_t)bg * nch + c) * nq_pad * kHd;
   float2* pml = part_ml + ((int64_t)bg * nch + c) * nq_pad;
-  for (int qt = 0; qt < nqt; ++qt) {
+  auto tile = [&](int qt, const half8_t(&qf)[4]) {
     const int qi = 16 * qt + li;
     const bool qok = qi < nq;
-    const int j = qok ? qi / G : 0, gg = qok ? qi - (qi / G) * G : 0;
-    const half8_t* qp =
-        reinterpret_cast<const half8_t*>(q + (((int64_t)bi * rps + j) * hq + g * G + gg) * kHd + 32 * lg);
-    half8_t qf[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) qf[s] = qok ? qp[s] : zero8;
+    const int j = qok ? qi / G : 0;
     float4_t st[4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
@@ -275,40 +301,81 @@ __global__ __launch_bounds__(64) void attn_chunk_kernel(const uint16_t* __restri
       for (int i = 0; i < 4; ++i) po[(int64_t)(16 * qt + 4 * lg + i) * kHd + 16 * dt + li] = o[i];
     }
     if (lg == 0) pml[16 * qt + li] = make_float2(mx, lsum);
+  };
+  if (pre) {
+#pragma unroll
+    for (int qt = 0; qt < kPreTiles; ++qt)
+      if (qt < nqt) tile(qt, qpre[qt]);
+  } else {
+    for (int qt = 0; qt < nqt; ++qt) {
+      half8_t qf[4];
+      load_q(qt, qf);
+      tile(qt, qf);
+    }
   }
 }
 
-// One workgroup of 128 threads (one per dim) per (row, query head): the
-// chunks 0 .. pos / 64 in order, out = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c.
-__global__ __launch_bounds__(128) void attn_merge_kernel(const float* __restrict__ part_o,
-                                                         const float2* __restrict__ part_ml, int hq, int hkv,
-                                                         int rps, int nch, int nq_pad,
-                                                         const int32_t* __restrict__ pos_base, int pos_offset,
-                                                         int64_t len_bound, uint16_t* __restrict__ out) {
-  const int r = blockIdx.x, hh = blockIdx.y, d = threadIdx.x;
+// One wavefront per (row, query head): the chunks 0 .. pos / 64, in order,
+//   out = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c,  M = max_c m_c.
+// Lane c (mod 64) reads chunk c's (m, l); lane t then sums dims 2t, 2t + 1
+// over the chunks, the loads of several chunks in flight at once.
+__global__ __launch_bounds__(64) void attn_merge_kernel(const float* __restrict__ part_o,
+                                                        const float2* __restrict__ part_ml, int hq, int hkv, int rps,
+                                                        int nch, int nq_pad, const int32_t* __restrict__ pos_base,
+                                                        int pos_offset, int64_t len_bound,
+                                                        uint16_t* __restrict__ out) {
+  const int r = blockIdx.x, hh = blockIdx.y, lane = threadIdx.x;
   const int bi = r / rps, j = r - bi * rps;
   const int G = hq / hkv, g = hh / G, gg = hh - g * G;
   const int qi = j * G + gg;
   const int64_t pos = (int64_t)pos_base[bi] + pos_offset + j;
-  uint16_t* o = out + ((int64_t)r * hq + hh) * kHd + d;
+  uint16_t* o = out + ((int64_t)r * hq + hh) * kHd + 2 * lane;
   if (pos < 0 || pos >= len_bound) {
-    *o = kNanF16;
+    o[0] = kNanF16;
+    o[1] = kNanF16;
     return;
   }
   const int last = (int)(pos / kChunk);
   const int64_t bg = (int64_t)bi * hkv + g;
   const float2* ml = part_ml + bg * nch * nq_pad + qi;
-  const float* po = part_o + (bg * nch * nq_pad + qi) * kHd + d;
+  const float* po = part_o + (bg * nch * nq_pad + qi) * kHd + 2 * lane;
   float mx = -__builtin_inff();
-  for (int c = 0; c <= last; ++c) mx = fmaxf(mx, ml[(int64_t)c * nq_pad].x);
-  float l = 0.f, acc = 0.f;
-  for (int c = 0; c <= last; ++c) {
-    const float2 v = ml[(int64_t)c * nq_pad];
-    const float w = exp2f(v.x - mx);
-    l += v.y * w;
-    acc += po[(int64_t)c * nq_pad * kHd] * w;
+  for (int c = lane; c <= last; c += 64) mx = fmaxf(mx, ml[(int64_t)c * nq_pad].x);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
+  float l = 0.f, a0 = 0.f, a1 = 0.f;
+  for (int c0 = 0; c0 <= last; c0 += 64) {
+    const int c = c0 + lane;
+    float wl = 0.f;
+    if (c <= last) {
+      const float2 v = ml[(int64_t)c * nq_pad];
+      wl = exp2f(v.x - mx);
+      l += v.y * wl;
+    }
+    const int n = last - c0 + 1 < 64 ? last - c0 + 1 : 64;
+    int i = 0;
+    for (; i + 4 <= n; i += 4) {
+      float2 p[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) p[u] = *reinterpret_cast<const float2*>(po + (int64_t)(c0 + i + u) * nq_pad * kHd);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float wc = __shfl(wl, i + u, kWave);
+        a0 += p[u].x * wc;
+        a1 += p[u].y * wc;
+      }
+    }
+    for (; i < n; ++i) {
+      const float2 p = *reinterpret_cast<const float2*>(po + (int64_t)(c0 + i) * nq_pad * kHd);
+      const float wc = __shfl(wl, i, kWave);
+      a0 += p.x * wc;
+      a1 += p.y * wc;
+    }
   }
-  *o = f32_to_f16_bits(acc / l);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) l += __shfl_xor(l, off, kWave);
+  o[0] = f32_to_f16_bits(a0 / l);
+  o[1] = f32_to_f16_bits(a1 / l);
 }
 
 // ------------------------------------------------------------- SiLU . up
@@ -365,15 +432,26 @@ hipError_t launch_embed_block(const uint16_t* table, int64_t vocab, int hidden, 
 
 hipError_t launch_add_rmsnorm(float* h, const float* delta, int64_t m, int hidden, const uint16_t* w, float eps,
                               int group, uint16_t* x, hipStream_t stream) {
-  hipLaunchKernelGGL(add_rmsnorm_kernel, dim3((unsigned)m), dim3(256), 0, stream, h, delta, hidden, w, eps, group, x);
+  const int n4 = hidden / 4;
+  const dim3 grid((unsigned)m), block(256);
+  if (n4 <= 256)
+    hipLaunchKernelGGL(add_rmsnorm_kernel<1>, grid, block, 0, stream, h, delta, hidden, w, eps, group, x);
+  else if (n4 <= 512)
+    hipLaunchKernelGGL(add_rmsnorm_kernel<2>, grid, block, 0, stream, h, delta, hidden, w, eps, group, x);
+  else if (n4 <= 1024)
+    hipLaunchKernelGGL(add_rmsnorm_kernel<4>, grid, block, 0, stream, h, delta, hidden, w, eps, group, x);
+  else if (n4 <= 2048)
+    hipLaunchKernelGGL(add_rmsnorm_kernel<8>, grid, block, 0, stream, h, delta, hidden, w, eps, group, x);
+  else
+    hipLaunchKernelGGL(add_rmsnorm_kernel<16>, grid, block, 0, stream, h, delta, hidden, w, eps, group, x);
   return hipGetLastError();
 }
 
 hipError_t launch_rope_kv(const float* qkv, const uint16_t* bias, int m, int hq, int hkv, int rps,
                           const int32_t* pos_base, int pos_offset, int64_t len_bound, int64_t capacity, double theta,
                           uint16_t* q_out, uint16_t* kc, uint16_t* vc, int32_t* status, hipStream_t stream) {
-  hipLaunchKernelGGL(rope_kv_kernel, dim3((unsigned)m), dim3(64), 0, stream, qkv, bias, hq, hkv, rps, pos_base,
-                     pos_offset, len_bound, capacity, theta, q_out, kc, vc, status);
+  hipLaunchKernelGGL(rope_kv_kernel, dim3((unsigned)m, (unsigned)(hq + 2 * hkv)), dim3(64), 0, stream, qkv, bias, hq,
+                     hkv, rps, pos_base, pos_offset, len_bound, capacity, theta, q_out, kc, vc, status);
   return hipGetLastError();
 }
 
@@ -395,7 +473,7 @@ hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_
   float2* part_ml = reinterpret_cast<float2*>(part_o + (size_t)b * hkv * nch * nq_pad * kHd);
   hipLaunchKernelGGL(attn_chunk_kernel, dim3((unsigned)nch, (unsigned)(b * hkv)), dim3(64), 0, stream, q, kc, vc, hq,
                      hkv, rps, capacity, pos_base, pos_offset, nch, nq_pad, part_o, part_ml);
-  hipLaunchKernelGGL(attn_merge_kernel, dim3((unsigned)(b * rps), (unsigned)hq), dim3(kHd), 0, stream, part_o,
+  hipLaunchKernelGGL(attn_merge_kernel, dim3((unsigned)(b * rps), (unsigned)hq), dim3(64), 0, stream, part_o,
                      part_ml, hq, hkv, rps, nch, nq_pad, pos_base, pos_offset, len_bound, out);
   return hipGetLastError();
 }

@@ -49,11 +49,17 @@ class DecoderWeights:
     """The FP16 parent and its quantized draft copy (``Stack``) plus the
     embedding, norms and biases they share."""
 
-    def __init__(self, cfg: Config, device, layers: int | None = None, variant: str | None = None):
+    def __init__(self, cfg: Config, device, layers: int | None = None, variant: str | None = None,
+                 stack: Stack | None = None):
         cfg = dataclasses.replace(cfg, lm_head=True)
         self.cfg = cfg
         self.device = dev = torch.device(device)
-        self.stack = Stack(cfg, dev, variant=variant, layers=layers)
+        if stack is not None:  # reuse the matrices of an existing stack (with its LM head and FP16 copies)
+            if not stack.cfg.lm_head or not stack.w16:
+                raise ValueError("the stack needs its LM head and its FP16 matrices")
+            self.stack = stack
+        else:
+            self.stack = Stack(cfg, dev, variant=variant, layers=layers)
         self.layers = self.stack.layers
         H = cfg.hidden
         n_qkv = cfg.q_dim + 2 * cfg.kv_dim
@@ -149,6 +155,7 @@ class SpecDecoder:
         self.out_len = torch.zeros((B,), dtype=i32, device=dev)
         self.status = torch.zeros((1,), dtype=i32, device=dev)
         self.keep_pq = keep_pq
+        self.attn_hook = None  # called as hook(True / False, rows_per_seq, offset) around each attention call
         if keep_pq:
             self.q_draft = torch.empty((k, B, V), dtype=f32, device=dev)   # draft-step distributions
             self.q_out = torch.empty((k, B, V), dtype=f32, device=dev)
@@ -183,7 +190,11 @@ class SpecDecoder:
             self._linear(draft, (l, "qkv"), x, qkv)
             sq.sq_rope_kv_f16(qkv, w.qkv_bias[l], self.pos_base, offset, rps, cfg.q_heads, cache.k[l], cache.v[l],
                               len_bound=lb, theta=THETA, q_out=q, status=self.status)
+            if self.attn_hook:
+                self.attn_hook(True, rps, offset)
             sq.sq_attention_f16(q, cache.k[l], cache.v[l], self.pos_base, offset, rps, len_bound=lb, out=a)
+            if self.attn_hook:
+                self.attn_hook(False, rps, offset)
             self._linear(draft, (l, "o"), a.view(M, cfg.q_dim), y)
             sq.sq_add_rmsnorm_f16(h, w.post_norm[l], EPS, delta=y, x=x)
             self._linear(draft, (l, "gate_up"), x, gu)

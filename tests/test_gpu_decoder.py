@@ -305,6 +305,7 @@ ROUND_CASES = [
     (0, 1, 2, 3, 0.0, 3, 70, "fp8"),
     (1, 2, 1, 4, 1.0, 3, 24, "int4"),
     (1, 2, 4, 8, 1.0, 2, 9, "fp8"),
+    (2, 1, 1, 4, 1.0, 2, 20, "int4"),  # the 7B shape of the benchmark: its layer and its full LM head
 ]
 
 
@@ -376,3 +377,40 @@ def test_rounds_teacher_forced(ci, layers, B, k, T, rounds, lp, variant):
             check_cache(sd.pcache, pc, b, int(st.pos[b]), f"round {r} parent cache")
             check_cache(sd.dcache, dc, b, int(st.pos[b]) - 1, f"round {r} draft cache")
     print(f"[rounds] worst logit error / rms {worst:.2e}; accepted per round {n_all}", flush=True)
+
+
+def test_decoder_graph_replays_match_eager_rounds():
+    """A captured round, replayed with eager work and synchronisations in
+    between, reproduces eager rounds bit for bit (tokens, positions, caches)."""
+    cfg = CONFIGS[1]
+    B, k, R, cap = 2, 3, 5, 128
+    w = dec.DecoderWeights(cfg, DEV, layers=2)
+    a = dec.SpecDecoder(w, batch=B, k=k, capacity=cap)
+    g = dec.SpecDecoder(w, batch=B, k=k, capacity=cap)
+    prompt = dec.synthetic_prompt(cfg, B, 12, DEV)
+    a.prefill(prompt)
+    g.prefill(prompt)
+    ud = synth.uniform_u24((R, k, B), synth.stream_seed(cfg.seed, 95), DEV)
+    ua = synth.uniform_u24((R, B, k + 1), synth.stream_seed(cfg.seed, 96), DEV)
+    snaps = []
+    for r in range(R):
+        a.set_uniforms(ud[r], ua[r])
+        a.run()
+        torch.cuda.synchronize()
+        snaps.append((a.out_tokens.clone(), a.out_len.clone(), a.pos_base.clone(), a.pending.clone(),
+                      [t.clone() for t in a.pcache.k + a.pcache.v + a.dcache.k + a.dcache.v]))
+    g.set_uniforms(ud[0], ua[0])
+    g.capture()  # round 0, eagerly; then the graph
+    for r in range(1, R):
+        g.set_uniforms(ud[r], ua[r])
+        g.replay()
+        torch.cuda.synchronize()
+        junk = torch.randn(1 << 20, device=DEV).sum()  # eager work between replays
+        torch.cuda.synchronize()
+        del junk
+        out, ln, pos, pend, caches = snaps[r]
+        assert torch.equal(g.out_len, ln) and torch.equal(g.out_tokens, out), f"replay {r}: tokens"
+        assert torch.equal(g.pos_base, pos) and torch.equal(g.pending, pend), f"replay {r}: positions"
+        for x, y in zip(g.pcache.k + g.pcache.v + g.dcache.k + g.dcache.v, caches):
+            assert torch.equal(x, y), f"replay {r}: caches"
+    assert g.status.item() == 0
