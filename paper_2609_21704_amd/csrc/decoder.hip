@@ -5,8 +5,8 @@
 //   embed_kernel        h = table[token] (fp32 residual stream)
 //   add_rmsnorm_kernel  h += delta; x = f16(h / sqrt(mean(h^2) + eps) * w)
 //   rope_kv_kernel      bias, rotary embedding of q and k, cache write of k, v
-//   attn_chunk_kernel   causal grouped-query attention of one 64-position chunk
-//                       of the cache on the matrix cores (partial softmax)
+//   attn_chunk_kernel   causal grouped-query attention over a slot of 64-position
+//                       chunks of the cache on the matrix cores (partial softmax)
 //   attn_merge_kernel   merge of the chunks in chunk order
 //   silu_mul_kernel     t = f16(g / (1 + exp(-g)) * u)
 //   commit_kernel       emitted tokens, next pending token, position
@@ -161,9 +161,12 @@ __global__ __launch_bounds__(64) void rope_kv_kernel(const float* __restrict__ q
 }
 
 // ------------------------------------------------------- attention chunks
-// One wavefront per (64-position chunk c, sequence bi, kv head g).  Its query
-// rows are the block's rows of bi times the G = hq / hkv heads of g, ordered
-// qi = j * G + gg, in tiles of 16.  On the matrix cores
+// One workgroup per (slot, sequence bi, kv head g); slot s covers the `span`
+// consecutive 64-position chunks s * span .. s * span + span - 1 of the cache.
+// Its query rows are the block's rows of bi times the G = hq / hkv heads of
+// g, ordered qi = j * G + gg, in tiles of 16, one tile per wavefront (up to 4
+// wavefronts, which read the same cache fragments; with more tiles, span 1
+// and each wavefront takes every 4th tile).  On the matrix cores
 // (v_mfma_f32_16x16x32_f16; lane l holds A[l%16][8(l/16) .. +8) and
 // B[8(l/16) .. +8)[l%16], D[4(l/16) + i][l%16]):
 //   S^T = K . Q^T  -- A: 16 keys x 32 of the head dimension (lane l: key l%16,
@@ -175,29 +178,32 @@ __global__ __launch_bounds__(64) void rope_kv_kernel(const float* __restrict__ q
 //                     16 + 4(l/16) + i of query l%16), and B takes the values
 //                     of the same 8 keys at dim l%16 (+16 per output tile)
 //                     from the position-minor value cache.
-// The partial result of each query row is (m, l, O): m the largest scaled
-// score (log2 units) of the chunk, l = sum of the weights p = 2^(s - m),
-// O = sum p v with each p split into two binary16 terms.  Keys after a row's position get p = 0; keys
-// after the last row's position are not read (their fragments are zero).
-__global__ __launch_bounds__(64) void attn_chunk_kernel(const uint16_t* __restrict__ q,
-                                                        const uint16_t* __restrict__ kc,
-                                                        const uint16_t* __restrict__ vc, int hq, int hkv, int rps,
-                                                        int64_t capacity, const int32_t* __restrict__ pos_base,
-                                                        int pos_offset, int nch, int nq_pad,
-                                                        float* __restrict__ part_o, float2* __restrict__ part_ml) {
-  const int c = blockIdx.x;
+// Across the chunks of its slot the wavefront keeps, per query row, the
+// running maximum m of the scaled scores (log2 units), l = sum of the
+// weights p = 2^(s - m) and O = sum p v, rescaled by 2^(m_old - m_new) when
+// m grows; the slot's (m, l, O) is its partial result.  Keys after a row's
+// position get p = 0; keys after the last row's position are not read (their
+// fragments are zero).
+__global__ __launch_bounds__(256) void attn_chunk_kernel(const uint16_t* __restrict__ q,
+                                                         const uint16_t* __restrict__ kc,
+                                                         const uint16_t* __restrict__ vc, int hq, int hkv, int rps,
+                                                         int64_t capacity, const int32_t* __restrict__ pos_base,
+                                                         int pos_offset, int nslots, int span, int nq_pad,
+                                                         float* __restrict__ part_o, float2* __restrict__ part_ml) {
+  const int slot = blockIdx.x;
   const int bg = blockIdx.y;  // bi * hkv + g
   const int bi = bg / hkv, g = bg - bi * hkv;
   const int G = hq / hkv, nq = rps * G;
   const int64_t p0 = (int64_t)pos_base[bi] + pos_offset;
   const int64_t pmax = p0 + rps - 1;
-  const int64_t key0 = (int64_t)c * kChunk;
-  if (key0 > pmax) return;  // no row reads this chunk (uniform); rows at negative positions mask every key
-  const int lane = threadIdx.x, li = lane & 15, lg = lane >> 4;
+  const int64_t slot0 = (int64_t)slot * span * kChunk;
+  if (slot0 > pmax) return;  // no row reads this slot (uniform); rows at negative positions mask every key
+  const int lane = threadIdx.x & 63, li = lane & 15, lg = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nwave = blockDim.x >> 6;
   const half8_t zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
   const int nqt = (nq + 15) >> 4;
 
-  // query fragments of tile qt: rows qi = 16 qt + li, dims 32 lg + 8 s .. +8
   auto load_q = [&](int qt, half8_t(&qf)[4]) {
     const int qi = 16 * qt + li;
     const bool qok = qi < nq;
@@ -207,49 +213,39 @@ __global__ __launch_bounds__(64) void attn_chunk_kernel(const uint16_t* __restri
 #pragma unroll
     for (int s = 0; s < 4; ++s) qf[s] = qok ? qp[s] : zero8;
   };
-  // up to kPreTiles query tiles are loaded before the cache fragments, so
-  // that all of the wavefront's loads are in flight together
-  constexpr int kPreTiles = 4;
-  half8_t qpre[kPreTiles][4];
-  const bool pre = nqt <= kPreTiles;
-  if (pre) {
-#pragma unroll
-    for (int qt = 0; qt < kPreTiles; ++qt)
-      if (qt < nqt) load_q(qt, qpre[qt]);
-  }
 
-  half8_t kf[4][4];
+  half8_t kf[4][4], vf[2][8];
+  auto load_kv = [&](int64_t key0) {
 #pragma unroll
-  for (int kt = 0; kt < 4; ++kt) {
-    const int64_t key = key0 + 16 * kt + li;
-    const half8_t* kp = reinterpret_cast<const half8_t*>(kc + ((int64_t)bg * capacity + key) * kHd + 32 * lg);
-    const bool ok = key <= pmax;
+    for (int kt = 0; kt < 4; ++kt) {
+      const int64_t key = key0 + 16 * kt + li;
+      const half8_t* kp = reinterpret_cast<const half8_t*>(kc + ((int64_t)bg * capacity + key) * kHd + 32 * lg);
+      const bool ok = key <= pmax;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) kf[kt][s] = ok ? kp[s] : zero8;
-  }
-  half8_t vf[2][8];
-#pragma unroll
-  for (int t2 = 0; t2 < 2; ++t2) {
-    const int64_t ka = key0 + 32 * t2 + 4 * lg, kb = ka + 16;
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-      const uint16_t* vp = vc + ((int64_t)bg * kHd + 16 * dt + li) * capacity;
-      const half4_t a = *reinterpret_cast<const half4_t*>(vp + ka);
-      const half4_t b = *reinterpret_cast<const half4_t*>(vp + kb);
-      half8_t f;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        f[e] = ka + e <= pmax ? a[e] : (half_t)0;
-        f[4 + e] = kb + e <= pmax ? b[e] : (half_t)0;
-      }
-      vf[t2][dt] = f;
+      for (int s = 0; s < 4; ++s) kf[kt][s] = ok ? kp[s] : zero8;
     }
-  }
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+      const int64_t ka = key0 + 32 * t2 + 4 * lg, kb = ka + 16;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) {
+        const uint16_t* vp = vc + ((int64_t)bg * kHd + 16 * dt + li) * capacity;
+        const half4_t a = *reinterpret_cast<const half4_t*>(vp + ka);
+        const half4_t b = *reinterpret_cast<const half4_t*>(vp + kb);
+        half8_t f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          f[e] = ka + e <= pmax ? a[e] : (half_t)0;
+          f[4 + e] = kb + e <= pmax ? b[e] : (half_t)0;
+        }
+        vf[t2][dt] = f;
+      }
+    }
+  };
 
   const float sl2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
-  float* po = part_o + ((int64_t)bg * nch + c) * nq_pad * kHd;
-  float2* pml = part_ml + ((int64_t)bg * nch + c) * nq_pad;
-  auto tile = [&](int qt, const half8_t(&qf)[4]) {
+  // one chunk (keys key0 .. key0 + 63) into tile qt's running (m, l, O)
+  auto update = [&](int qt, const half8_t(&qf)[4], int64_t key0, float& m, float& l, float4_t(&o)[8]) {
     const int qi = 16 * qt + li;
     const bool qok = qi < nq;
     const int j = qok ? qi / G : 0;
@@ -262,7 +258,7 @@ __global__ __launch_bounds__(64) void attn_chunk_kernel(const uint16_t* __restri
       st[kt] = acc;
     }
     const int64_t qpos = p0 + j;
-    float mx = -__builtin_inff();
+    float cm = -__builtin_inff();
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
@@ -270,58 +266,96 @@ __global__ __launch_bounds__(64) void attn_chunk_kernel(const uint16_t* __restri
         const int64_t key = key0 + 16 * kt + 4 * lg + i;
         const float v = (qok && key <= qpos) ? st[kt][i] * sl2 : -__builtin_inff();
         st[kt][i] = v;
-        mx = fmaxf(mx, v);
+        cm = fmaxf(cm, v);
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    cm = fmaxf(cm, __shfl_xor(cm, 16, kWave));
+    cm = fmaxf(cm, __shfl_xor(cm, 32, kWave));
+    const float mn = fmaxf(m, cm);
+    const bool none = mn == -__builtin_inff();  // no key of this row so far
+    const float alpha = none ? 1.f : exp2f(m - mn);
     // p = hi + lo, both binary16 (hi = f16(p), lo = f16(p - hi), the difference
     // exact in fp32): two products with the values carry p to about 2^-22
-    float lsum = 0.f;
+    float psum = 0.f;
     half8_t pf[2], pl[2];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float p = mx == -__builtin_inff() ? 0.f : exp2f(st[kt][i] - mx);
+        const float p = none ? 0.f : exp2f(st[kt][i] - mn);
         const half_t ph = (half_t)p;
-        lsum += p;
+        psum += p;
         pf[kt >> 1][(kt & 1) * 4 + i] = ph;
         pl[kt >> 1][(kt & 1) * 4 + i] = (half_t)(p - (float)ph);
       }
-    lsum += __shfl_xor(lsum, 16, kWave);
-    lsum += __shfl_xor(lsum, 32, kWave);
+    psum += __shfl_xor(psum, 16, kWave);
+    psum += __shfl_xor(psum, 32, kWave);
+    l = l * alpha + psum;
+    m = mn;
+    // rows 4 lg + i of the output tile take the factor of query 4 lg + i
+    float ar[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ar[i] = __shfl(alpha, 4 * lg + i, kWave);
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
-      float4_t o = {0.f, 0.f, 0.f, 0.f};
-      o = __builtin_amdgcn_mfma_f32_16x16x32_f16(pl[0], vf[0][dt], o, 0, 0, 0);
-      o = __builtin_amdgcn_mfma_f32_16x16x32_f16(pl[1], vf[1][dt], o, 0, 0, 0);
-      o = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[0], vf[0][dt], o, 0, 0, 0);
-      o = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[1], vf[1][dt], o, 0, 0, 0);
+      float4_t acc = o[dt];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) po[(int64_t)(16 * qt + 4 * lg + i) * kHd + 16 * dt + li] = o[i];
+      for (int i = 0; i < 4; ++i) acc[i] *= ar[i];
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pl[0], vf[0][dt], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pl[1], vf[1][dt], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[0], vf[0][dt], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[1], vf[1][dt], acc, 0, 0, 0);
+      o[dt] = acc;
     }
-    if (lg == 0) pml[16 * qt + li] = make_float2(mx, lsum);
   };
-  if (pre) {
+
+  float* po = part_o + ((int64_t)bg * nslots + slot) * nq_pad * kHd;
+  float2* pml = part_ml + ((int64_t)bg * nslots + slot) * nq_pad;
+  auto store = [&](int qt, float m, float l, const float4_t(&o)[8]) {
 #pragma unroll
-    for (int qt = 0; qt < kPreTiles; ++qt)
-      if (qt < nqt) tile(qt, qpre[qt]);
-  } else {
-    for (int qt = 0; qt < nqt; ++qt) {
+    for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) po[(int64_t)(16 * qt + 4 * lg + i) * kHd + 16 * dt + li] = o[dt][i];
+    if (lg == 0) pml[16 * qt + li] = make_float2(m, l);
+  };
+
+  if (nqt <= nwave) {  // one query tile per wavefront, its running sums kept across the slot's chunks
+    const int qt = wave;
+    float m = -__builtin_inff(), l = 0.f;
+    float4_t o[8];
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) o[dt] = float4_t{0.f, 0.f, 0.f, 0.f};
+    half8_t qf[4];
+    load_q(qt, qf);
+    for (int t = 0; t < span; ++t) {
+      const int64_t key0 = slot0 + (int64_t)t * kChunk;
+      if (key0 > pmax) break;  // uniform
+      load_kv(key0);
+      update(qt, qf, key0, m, l, o);
+    }
+    store(qt, m, l, o);
+  } else {  // more query tiles than wavefronts: span 1, tiles wave, wave + nwave, ...
+    load_kv(slot0);
+    for (int qt = wave; qt < nqt; qt += nwave) {
       half8_t qf[4];
       load_q(qt, qf);
-      tile(qt, qf);
+      float m = -__builtin_inff(), l = 0.f;
+      float4_t o[8];
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) o[dt] = float4_t{0.f, 0.f, 0.f, 0.f};
+      update(qt, qf, slot0, m, l, o);
+      store(qt, m, l, o);
     }
   }
 }
 
-// One wavefront per (row, query head): the chunks 0 .. pos / 64, in order,
-//   out = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c,  M = max_c m_c.
-// Lane c (mod 64) reads chunk c's (m, l); lane t then sums dims 2t, 2t + 1
-// over the chunks, the loads of several chunks in flight at once.
+// One wavefront per (row, query head): the slots 0 .. pos / (64 span), in
+// order, out = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s, M = max_s m_s.
+// Lane c (mod 64) reads slot c's (m, l); lane t then sums dims 2t, 2t + 1
+// over the slots, the loads of several slots in flight at once.
 __global__ __launch_bounds__(64) void attn_merge_kernel(const float* __restrict__ part_o,
                                                         const float2* __restrict__ part_ml, int hq, int hkv, int rps,
-                                                        int nch, int nq_pad, const int32_t* __restrict__ pos_base,
+                                                        int nch, int span, int nq_pad,
+                                                        const int32_t* __restrict__ pos_base,
                                                         int pos_offset, int64_t len_bound,
                                                         uint16_t* __restrict__ out) {
   const int r = blockIdx.x, hh = blockIdx.y, lane = threadIdx.x;
@@ -335,7 +369,7 @@ __global__ __launch_bounds__(64) void attn_merge_kernel(const float* __restrict_
     o[1] = kNanF16;
     return;
   }
-  const int last = (int)(pos / kChunk);
+  const int last = (int)(pos / kChunk / span);  // the last slot holding a key of this row
   const int64_t bg = (int64_t)bi * hkv + g;
   const float2* ml = part_ml + bg * nch * nq_pad + qi;
   const float* po = part_o + (bg * nch * nq_pad + qi) * kHd + 2 * lane;
@@ -455,26 +489,44 @@ hipError_t launch_rope_kv(const float* qkv, const uint16_t* bias, int m, int hq,
   return hipGetLastError();
 }
 
+namespace {
+// Chunks per wavefront: about 512 wavefronts in all (two per CU) once the
+// cache is long enough, at most 16 chunks each; a single chunk when the
+// block has more than 4 query tiles.
+int attention_span(int b, int hq, int hkv, int rps, int64_t len_bound) {
+  const int64_t nch = (len_bound + kChunk - 1) / kChunk;
+  const int nqt = (rps * (hq / hkv) + 15) / 16;
+  if (nqt > 4) return 1;
+  int64_t span = nch * b * hkv / 512;
+  span = span < 1 ? 1 : (span > 16 ? 16 : span);
+  return (int)span;
+}
+}  // namespace
+
 size_t attention_workspace_bytes(int b, int hq, int hkv, int rps, int64_t len_bound) {
-  const int nch = (int)((len_bound + kChunk - 1) / kChunk);
+  const int span = attention_span(b, hq, hkv, rps, len_bound);
+  const int64_t nslots = ((len_bound + kChunk - 1) / kChunk + span - 1) / span;
   const int nq_pad = (rps * (hq / hkv) + 15) / 16 * 16;
-  return (size_t)b * hkv * nch * nq_pad * (kHd * sizeof(float) + sizeof(float2));
+  return (size_t)b * hkv * nslots * nq_pad * (kHd * sizeof(float) + sizeof(float2));
 }
 
 hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, int b, int rps, int hq,
                             int hkv, int64_t capacity, const int32_t* pos_base, int pos_offset, int64_t len_bound,
                             uint16_t* out, hipStream_t stream) {
-  const int nch = (int)((len_bound + kChunk - 1) / kChunk);
+  const int span = attention_span(b, hq, hkv, rps, len_bound);
+  const int nslots = (int)(((len_bound + kChunk - 1) / kChunk + span - 1) / span);
   const int nq_pad = (rps * (hq / hkv) + 15) / 16 * 16;
   void* ws = nullptr;
   const hipError_t e = workspace(attention_workspace_bytes(b, hq, hkv, rps, len_bound), stream, &ws);
   if (e != hipSuccess) return e;
   float* part_o = static_cast<float*>(ws);
-  float2* part_ml = reinterpret_cast<float2*>(part_o + (size_t)b * hkv * nch * nq_pad * kHd);
-  hipLaunchKernelGGL(attn_chunk_kernel, dim3((unsigned)nch, (unsigned)(b * hkv)), dim3(64), 0, stream, q, kc, vc, hq,
-                     hkv, rps, capacity, pos_base, pos_offset, nch, nq_pad, part_o, part_ml);
+  float2* part_ml = reinterpret_cast<float2*>(part_o + (size_t)b * hkv * nslots * nq_pad * kHd);
+  const int nqt = nq_pad / 16;
+  const int waves = nqt < 4 ? nqt : 4;  // one query tile per wavefront (16 rows each), at most 4
+  hipLaunchKernelGGL(attn_chunk_kernel, dim3((unsigned)nslots, (unsigned)(b * hkv)), dim3(64 * waves), 0, stream, q, kc,
+                     vc, hq, hkv, rps, capacity, pos_base, pos_offset, nslots, span, nq_pad, part_o, part_ml);
   hipLaunchKernelGGL(attn_merge_kernel, dim3((unsigned)(b * rps), (unsigned)hq), dim3(64), 0, stream, part_o,
-                     part_ml, hq, hkv, rps, nch, nq_pad, pos_base, pos_offset, len_bound, out);
+                     part_ml, hq, hkv, rps, nslots, span, nq_pad, pos_base, pos_offset, len_bound, out);
   return hipGetLastError();
 }
 

@@ -176,6 +176,9 @@ ATT_CASES = [
     (40, 8, 7, [2000], 0, 2048, 1.5),        # 32B heads
     (7, 1, 64, [0], 0, 128, 1.5),            # a 64-row prefill chunk, 448 query rows
     (8, 8, 3, [127, 128], 0, 256, 1.5),      # one query head per kv head
+    (28, 4, 9, [3000, 8000, 100, 6000], 0, 8192, 1.5),  # 4 chunks per wavefront, 4 query tiles
+    (8, 2, 1, [16000, 9000], 0, 16384, 3.0),  # 2 chunks per wavefront, one query tile
+    (7, 1, 64, [4000], 0, 4096, 1.5),        # a prefill chunk deep into the cache
 ]
 
 
