@@ -19,6 +19,11 @@
         order: the L layers' shapes in turn, then the LM head): duration,
         executed matrix-core flops, matrix-core busy fraction, HBM bytes
 
+    python -m paper_2609_21704_amd.prof rounds <rocprofv3 output dir> --end SUBSTR [--rounds R]
+        the last R rounds of a trace, each ending with a dispatch whose name
+        contains SUBSTR (the decoder rounds end with sq::commit_kernel): time
+        per round, busy time per kernel and the gaps between dispatches
+
 The inputs are the rocpd SQLite databases rocprofv3 writes (*.db).
 """
 from __future__ import annotations
@@ -235,6 +240,38 @@ def verify(mfma_dir, fetch_dir, write_dir, copy_bytes, m, layers, shapes, lm):
     return "\n".join(lines)
 
 
+def rounds(path, end, count=20):
+    rows = []
+    for db in _dbs(path):
+        con = sqlite3.connect(db)
+        rows += list(con.execute("select name, start, end from kernels order by start"))
+    rows.sort(key=lambda r: r[1])
+    ends = [i for i, r in enumerate(rows) if end in short_name(r[0])]
+    if len(ends) < 2:
+        return f"fewer than two dispatches matching '{end}'"
+    sel = ends[-(count + 1):]
+    n = len(sel) - 1
+    busy = collections.Counter()
+    calls = collections.Counter()
+    total = gaps = 0
+    for a, b in zip(sel[:-1], sel[1:]):
+        total += rows[b][2] - rows[a][2]
+        prev = rows[a][2]
+        for name, st, en in rows[a + 1:b + 1]:
+            sn = re.sub(r"<.*", "", short_name(name))
+            busy[sn] += en - st
+            calls[sn] += 1
+            gaps += max(0, st - prev)
+            prev = max(prev, en)
+    lines = [f"rounds: {n} (ending with '{end}'); {total / n / 1e3:.1f} us per round, dispatches "
+             f"{sum(calls.values()) / n:.0f} per round, busy {sum(busy.values()) / n / 1e3:.1f} us, gaps "
+             f"{gaps / n / 1e3:.1f} us",
+             f"{'kernel':44s} {'calls/round':>11s} {'us/round':>10s} {'avg_us':>8s}"]
+    for sn, t in busy.most_common():
+        lines.append(f"{sn[:44]:44s} {calls[sn] / n:>11.0f} {t / n / 1e3:>10.1f} {t / calls[sn] / 1e3:>8.2f}")
+    return "\n".join(lines)
+
+
 def _nk(s):
     n, k = s.lower().split("x")
     return int(n), int(k)
@@ -265,8 +302,14 @@ def main():
     c.add_argument("--layers", type=int, required=True)
     c.add_argument("--shapes", required=True, help="name:NxK,... in the order of one layer's verify calls")
     c.add_argument("--lm", type=_nk, help="NxK of the LM head, verified after the layers")
+    r = sub.add_parser("rounds")
+    r.add_argument("path")
+    r.add_argument("--end", required=True)
+    r.add_argument("--rounds", type=int, default=20)
     args = ap.parse_args()
-    if args.cmd == "stats":
+    if args.cmd == "rounds":
+        print(rounds(args.path, args.end, args.rounds))
+    elif args.cmd == "stats":
         print(stats(args.path, args.match))
     elif args.cmd == "traffic":
         print(traffic(args.fetch_dir, args.write_dir, args.copy_bytes, args.variant, args.calls))
