@@ -1,7 +1,8 @@
 """SpecQuant CPU oracle -- test infrastructure only.
 
-A plain fp64 C implementation (``sq_oracle.c``, and ``sq_decoder.c`` for the
-operations of the decoder layer around the projections) of what the SpecQuant
+A plain fp64 C implementation (``sq_oracle.c``; ``sq_decoder.c`` for the
+operations of the decoder layer around the projections; ``sq_multi.c`` for
+the acceptance of several draft chains per sequence) of what the SpecQuant
 hot path computes, wrapped with ctypes for numpy arrays; ``decoder.py``
 composes them into the decoder and the speculative round with its cache.  Only the test suite,
 ``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py`` may use
@@ -22,7 +23,7 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRCS = [os.path.join(_HERE, "sq_oracle.c"), os.path.join(_HERE, "sq_decoder.c")]
+_SRCS = [os.path.join(_HERE, f) for f in ("sq_oracle.c", "sq_decoder.c", "sq_multi.c")]
 _LIB_PATH = os.path.join(_HERE, "libsq_oracle.so")
 _lib = None
 
@@ -72,6 +73,8 @@ def _load():
         "sqo_rope": ([P, I64, I64, I64, P, D], ctypes.c_int),
         "sqo_attention": ([P, I64, I64, I64, I64, P, P, I64, P, P], ctypes.c_int),
         "sqo_silu_mul": ([P, I64, I64, P], ctypes.c_int),
+        "sqo_multi_accept_probs": ([P, P, P, P, I32, I32, I32, I32, P, P, P], ctypes.c_int),
+        "sqo_multi_accept_greedy": ([P, P, I32, I32, I32, I32, P, P, P], ctypes.c_int),
     }
     for name, (args, res) in sigs.items():
         fn = getattr(lib, name)
@@ -271,6 +274,60 @@ def accept_probs(p, q, draft_tokens, u24):
     _check(_load().sqo_accept_probs(_ptr(p), _ptr(q), _ptr(draft_tokens), _ptr(u24), b, kd, v, _ptr(n_acc),
                                     _ptr(nxt)), "accept_probs")
     return n_acc, nxt
+
+
+def multi_accept_probs(p, q, drafts, u24):
+    """Multi-candidate acceptance (recursive rejection over c draft chains)
+    from fp32 distributions: p [b][c][kd+1][v], q [kd][b][c][v],
+    drafts [kd][b][c] i32, u24 [b][c kd + 1].  Returns (n_accepted [b],
+    next_token [b], chain [b])."""
+    p = np.ascontiguousarray(p, np.float32)
+    b, c, kd1, v = p.shape
+    kd = kd1 - 1
+    if kd > 0:
+        q = np.ascontiguousarray(q, np.float32).reshape(kd, b, c, v)
+        drafts = np.ascontiguousarray(drafts, np.int32).reshape(kd, b, c)
+    else:
+        q = drafts = None
+    u24 = np.ascontiguousarray(u24, np.uint32).reshape(b, c * kd + 1)
+    n = np.zeros(b, np.int32)
+    t = np.zeros(b, np.int32)
+    ch = np.zeros(b, np.int32)
+    _check(_load().sqo_multi_accept_probs(_ptr(p), _ptr(q), _ptr(drafts), _ptr(u24), b, c, kd, v, _ptr(n), _ptr(t),
+                                          _ptr(ch)), "multi_accept_probs")
+    return n, t, ch
+
+
+def multi_accept_greedy(target_logits, drafts):
+    """Greedy multi-candidate acceptance from target logits [b][c][kd+1][v]
+    and drafts [kd][b][c].  Returns (n_accepted, next_token, chain)."""
+    target_logits = np.ascontiguousarray(target_logits, np.float32)
+    b, c, kd1, v = target_logits.shape
+    kd = kd1 - 1
+    drafts = None if kd == 0 else np.ascontiguousarray(drafts, np.int32).reshape(kd, b, c)
+    n = np.zeros(b, np.int32)
+    t = np.zeros(b, np.int32)
+    ch = np.zeros(b, np.int32)
+    _check(_load().sqo_multi_accept_greedy(_ptr(target_logits), _ptr(drafts), b, c, kd, v, _ptr(n), _ptr(t), _ptr(ch)),
+           "multi_accept_greedy")
+    return n, t, ch
+
+
+def multi_accept(draft_logits, target_logits, drafts, u24, temperature: float = 1.0):
+    """Multi-candidate acceptance from logits: draft_logits [kd][b][c][v],
+    target_logits [b][c][kd+1][v]; T > 0: the distributions are fp64
+    softmaxes held in fp32, then multi_accept_probs; T = 0: greedy."""
+    target_logits = np.ascontiguousarray(target_logits, np.float32)
+    b, c, kd1, v = target_logits.shape
+    kd = kd1 - 1
+    if temperature == 0.0:
+        return multi_accept_greedy(target_logits, drafts)
+    p = softmax(target_logits.reshape(-1, v), temperature).astype(np.float32).reshape(b, c, kd1, v)
+    q = None
+    if kd > 0:
+        q = softmax(np.ascontiguousarray(draft_logits, np.float32).reshape(-1, v), temperature)
+        q = q.astype(np.float32).reshape(kd, b, c, v)
+    return multi_accept_probs(p, q, drafts, u24)
 
 
 def rmsnorm(h, w, eps: float) -> np.ndarray:
