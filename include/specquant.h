@@ -26,6 +26,12 @@
  *   sq_silu_mul_f16        SiLU-gated product of the gate|up projection
  *   sq_spec_commit         emitted tokens and restart position of a round
  *
+ * and several draft chains per sequence (multi-candidate drafting, SS III-D.2):
+ *
+ *   sq_spec_accept_multi   accept / correct over c chains (recursive rejection)
+ *   sq_kv_adopt_f16        the accepted chain's cache entries to the other chains
+ *   sq_spec_commit_multi   emitted tokens and restart position with c chains
+ *
  * Conventions shared by every call
  *   - Matrices are row-major and contiguous.  A weight matrix is W[n][k]
  *     (n output features, k reduction features); activations are x[m][k];
@@ -60,7 +66,7 @@
 extern "C" {
 #endif
 
-#define SQ_ABI_VERSION 3
+#define SQ_ABI_VERSION 4
 
 typedef enum sq_status {
   SQ_OK = 0,
@@ -304,6 +310,82 @@ sq_status sq_spec_commit(const int32_t* n_accepted, const int32_t* next_token, c
                          int32_t b, int32_t kd, int32_t* pending, int32_t* prev, int32_t* pos_base,
                          int32_t* out_tokens, int64_t out_capacity, int32_t* out_len, int32_t* status,
                          hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Several draft chains per sequence (multi-candidate drafting; SS III-D.2
+ * lets a draft variant produce many candidate tokens in one step, and the
+ * paper gives no verification rule for them).  Each sequence s drafts c
+ * chains of kd tokens; chain j samples its own tokens from the quantized
+ * parent (the rows of s are the c chains, as b * c rows of every draft step),
+ * so the candidates at any node of the chains' common prefix tree are
+ * independent draws from the draft distribution there.  The FP16 parent
+ * verifies every chain in one pass (b * c * (kd + 1) rows).  Acceptance walks
+ * the tree by recursive rejection sampling, which keeps the parent's
+ * distribution exact and is the rule of sq_spec_accept when c = 1. */
+
+/* Multi-candidate acceptance or correction (SS III-D.4 over c chains):
+ * at the node reached by the accepted prefix, with q and p the draft's and
+ * the parent's distributions there (the lowest alive chain's rows), the alive
+ * chains' tokens x are tested in ascending chain order against a residual r
+ * (r = p at first): x is accepted iff u * q(x) < r(x); after a rejection
+ * r <- max(0, r - q), renormalised.  An accepted token continues with the
+ * chains that drafted it; when every alive chain is rejected the emitted
+ * token is drawn from r; after kd accepted tokens, the bonus token from p of
+ * the last node.  Arithmetic: q, p as in sq_spec_accept (fp64 softmax held in
+ * fp32); the first test u q(x) < p(x) in fp64; its residual
+ * R = rint(max(0, p - q) 2^60) with Z = sum R (or R = rint(p 2^60) when Z = 0);
+ * later tests u q(x) Z < R(x) and later residuals R <- max(0, R - floor(q Z))
+ * in exact integer arithmetic (same fallback); the draw takes the smallest y
+ * whose running sum of R exceeds floor(u24 Z / 2^24).
+ * T = 0 (greedy): the argmax of the node's parent row (smallest index on
+ * ties) is accepted when an alive chain drafted it; else it is emitted.
+ * draft_logits  [kd][b][c][v] f32 (draft step d for every chain)
+ * target_logits [b][c][kd+1][v] f32 (chain j's verification rows)
+ * draft_tokens  [kd][b][c] int32
+ * u24           [b][c kd + 1] uint32: u24[s][d c + j] tests chain j at depth d,
+ *               u24[s][c kd] drives the final draw (NULL allowed at T = 0)
+ * n_accepted, next_token [b] out; chain [b] out: the lowest chain whose first
+ *   n tokens are the accepted ones (its draft_tokens[0..n)[s] and next_token
+ *   are the emitted tokens).  A sequence with a row without a distribution
+ *   (T > 0: any of its rows; T = 0: any target row) gets -1 in all three.
+ * q_out [kd][b][c][v], p_out [b][c][kd+1][v]: optional fp32 copies, T > 0 only.
+ * Limits: 1 <= b <= 65535, 1 <= c <= 64, 0 <= kd <= 64, 1 <= v <= 2^26,
+ *   b c (2 kd + 1) ceil(v / 4096) < 2^24; T finite and >= 0.  Uses the library
+ *   workspace (row statistics, the fp32 rows unless q_out / p_out are given,
+ *   and one int64 row per sequence). */
+sq_status sq_spec_accept_multi(const float* draft_logits, const float* target_logits, const int32_t* draft_tokens,
+                               const uint32_t* u24, int32_t b, int32_t c, int32_t kd, int32_t v, float temperature,
+                               int32_t* n_accepted, int32_t* next_token, int32_t* chain, float* q_out, float* p_out,
+                               hipStream_t stream);
+
+/* The accepted chain's cache entries to the other chains of its sequence
+ * (before sq_spec_commit_multi moves the positions): for every layer, kv head
+ * and sequence s with 0 <= chain[s] < c and n_accepted[s] >= 0, the entries of
+ * row s c + chain[s] at positions pos + lo_offset .. pos + n_accepted[s] +
+ * hi_offset (pos = pos_base[s c + chain[s]]; clipped to [0, capacity)) are
+ * copied to rows s c + j, j != chain[s].  The parent's
+ * cache takes lo_offset = hi_offset = 0 (the pending token and the accepted
+ * drafts), the draft's lo_offset = hi_offset = -1.
+ * k_cache [layers][b c][hkv][capacity][128] fp16, v_cache
+ * [layers][b c][hkv][128][capacity] fp16 (the layout of sq_rope_kv_f16, layers
+ * contiguous); chain, n_accepted [b]; pos_base [b c].  1 <= layers, b c,
+ * hkv <= 65535; c <= 64; capacity as for sq_rope_kv_f16; |offsets| <= 64. */
+sq_status sq_kv_adopt_f16(uint16_t* k_cache, uint16_t* v_cache, int32_t layers, int32_t b, int32_t c, int32_t hkv,
+                          int64_t capacity, const int32_t* chain, const int32_t* n_accepted, const int32_t* pos_base,
+                          int32_t lo_offset, int32_t hi_offset, hipStream_t stream);
+
+/* The commit of sq_spec_commit for c chains per sequence: with n =
+ * n_accepted[s] and a = chain[s], the emitted tokens draft_tokens[i][s][a]
+ * (i < n) and next_token[s] are appended to out_tokens[s]; every chain j of s
+ * gets pending[s c + j] = next_token[s], prev[s c + j] = the last emitted
+ * draft (pending[s c + a] when n = 0) and pos_base[s c + j] = pos_base[s c + a]
+ * + n + 1.  A sequence with n outside [0, kd] or a outside [0, c) keeps its
+ * state (SQ_DEV_NO_DIST).  pending, prev, pos_base [b c]; other arrays as in
+ * sq_spec_commit.  1 <= b < 2^24, 1 <= c <= 64, 0 <= kd <= 64. */
+sq_status sq_spec_commit_multi(const int32_t* n_accepted, const int32_t* next_token, const int32_t* chain,
+                               const int32_t* draft_tokens, int32_t b, int32_t c, int32_t kd, int32_t* pending,
+                               int32_t* prev, int32_t* pos_base, int32_t* out_tokens, int64_t out_capacity,
+                               int32_t* out_len, int32_t* status, hipStream_t stream);
 
 /* Streaming-read probe (a measurement aid beside the method, not one of its
  * steps): reads `bytes` bytes of src once with 16-byte loads in grid-stride

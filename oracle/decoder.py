@@ -34,6 +34,12 @@ The round (k drafts per sequence, position P of the pending token):
   token, the pending token is that next token at P+n+1: cache entries from that
   position on belong to the removed block and are never read again before being
   overwritten.
+
+With c draft chains per sequence (spec_round_multi) the caches hold c rows per
+sequence (row s c + j for chain j, each started from the sequence's prompt);
+every chain drafts its own tokens, the parent verifies all of them, acceptance
+walks the chains' prefix tree (``multi_accept``), and the accepted chain's new
+entries are copied to the other chains before all of them restart.
 """
 from __future__ import annotations
 
@@ -41,8 +47,8 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-from . import (attention, dequant_fp8, dequant_int4, quantize_fp8_e4m3, quantize_int4_g128, rmsnorm, rope,
-               silu_mul, spec_accept)
+from . import (attention, dequant_fp8, dequant_int4, multi_accept, quantize_fp8_e4m3, quantize_int4_g128, rmsnorm,
+               rope, silu_mul, spec_accept)
 
 HEAD_DIM = 128
 MATRICES = ("qkv", "o", "gate_up", "down")
@@ -246,3 +252,66 @@ def spec_round(draft: Model, parent: Model, dcache: Cache, pcache: Cache, state:
     commit(state, n_acc, nxt, dt)
     return {"draft_tokens": dt, "draft_logits": dl, "target_logits": target, "n_accepted": n_acc,
             "next_token": nxt, "positions": P}
+
+
+def prefill_chains(models, caches, prompt, c: int) -> SpecState:
+    """prefill with every sequence repeated for its c chains (cache rows s c + j)."""
+    prompt = np.asarray(prompt, np.int64)
+    st = prefill(models, caches, np.repeat(prompt, c, axis=0))
+    B = prompt.shape[0]
+    return SpecState(pos=st.pos[::c].copy(), pending=st.pending[::c].copy(), prev=st.prev[::c].copy(),
+                     emitted=[[] for _ in range(B)])
+
+
+def spec_round_multi(draft: Model, parent: Model, dcache: Cache, pcache: Cache, state: SpecState, c: int, k: int,
+                     u_draft, u_accept, temperature: float = 1.0) -> dict:
+    """One round with c chains per sequence: u_draft [k][B c] (each chain's own
+    draws), u_accept [B][c k + 1]."""
+    B = len(state.pos)
+    R = B * c
+    P = np.repeat(state.pos, c)
+    prev, pend = np.repeat(state.prev, c), np.repeat(state.pending, c)
+    if u_draft is not None:
+        u_draft = np.asarray(u_draft, np.uint32).reshape(k, R)
+    drafts, qlog = [], []
+    for i in range(k):
+        if i == 0:
+            toks, pos = np.stack([prev, pend], 1), np.stack([P - 1, P], 1)
+        else:
+            toks, pos = drafts[-1][:, None], (P + i)[:, None]
+        lg32 = forward(draft, dcache, toks, pos)[:, -1].astype(np.float32)
+        qlog.append(lg32)
+        u = None if u_draft is None else u_draft[i][:, None]
+        _, tok, _, _ = spec_accept(None, lg32[:, None, :], None, u, temperature)
+        drafts.append(tok.astype(np.int64))
+    vt = np.concatenate([pend[:, None], np.stack(drafts, 1)], 1)
+    target = forward(parent, pcache, vt, P[:, None] + np.arange(k + 1)[None, :]).astype(np.float32)
+    V = target.shape[-1]
+    dl = np.stack(qlog, 0).reshape(k, B, c, V)
+    dt = np.stack(drafts, 0).reshape(k, B, c)
+    n, nxt, ch = multi_accept(dl, target.reshape(B, c, k + 1, V), dt.astype(np.int32), u_accept, temperature)
+    adopt(pcache, dcache, state.pos, n, ch, c)
+    sel = np.zeros((k, B), np.int64)
+    for s in range(B):
+        if n[s] >= 0:
+            sel[:, s] = dt[:, s, ch[s]]
+    commit(state, n, nxt, sel)
+    return {"draft_tokens": dt, "draft_logits": dl, "target_logits": target.reshape(B, c, k + 1, V),
+            "n_accepted": n, "next_token": nxt, "chain": ch, "positions": P}
+
+
+def adopt(pcache: Cache, dcache: Cache, pos, n, ch, c: int) -> None:
+    """Copy the accepted chain's new entries to the other chains of each
+    sequence: the parent's at P .. P + n, the draft's at P - 1 .. P + n - 1."""
+    for s in range(len(pos)):
+        if n[s] < 0:
+            continue
+        src = s * c + int(ch[s])
+        P = int(pos[s])
+        for j in range(c):
+            dst = s * c + j
+            if dst == src:
+                continue
+            for cache, lo, hi in ((pcache, P, P + n[s]), (dcache, max(P - 1, 0), P + n[s] - 1)):
+                cache.k[:, dst, :, lo:hi + 1] = cache.k[:, src, :, lo:hi + 1]
+                cache.v[:, dst, :, lo:hi + 1] = cache.v[:, src, :, lo:hi + 1]

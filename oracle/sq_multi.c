@@ -228,8 +228,8 @@ int sqo_multi_accept_probs(const float* p, const float* q, const int32_t* drafts
  * lowest alive chain's; smallest index on ties) is accepted when an alive
  * chain drafted it, and those chains continue; else it is the emitted token.
  * After kd accepted tokens the emitted token is the argmax of the last node.
- * A row holding a NaN or +inf, or no finite logit, makes the sequence
- * invalid (n = token = chain = -1). */
+ * A target row of the sequence (any chain, any depth) holding a NaN or +inf,
+ * or no finite logit, makes the sequence invalid (n = token = chain = -1). */
 int sqo_multi_accept_greedy(const float* target, const int32_t* drafts, int32_t b, int32_t c, int32_t kd,
                             int32_t v, int32_t* n_accepted, int32_t* next_token, int32_t* chain) {
   if (!target || !n_accepted || !next_token || !chain || (kd > 0 && !drafts)) return SQM_ERR_NULL;
@@ -238,21 +238,22 @@ int sqo_multi_accept_greedy(const float* target, const int32_t* drafts, int32_t 
   for (int32_t s = 0; s < b; ++s) {
     int alive[64], nalive = c, bad = 0;
     for (int j = 0; j < c; ++j) alive[j] = j;
+    /* every target row of the sequence needs a greedy target */
+    for (int64_t r = 0; r < (int64_t)c * (kd + 1) && !bad; ++r) {
+      const float* row = target + ((int64_t)s * c * (kd + 1) + r) * v;
+      int finite = 0;
+      for (int64_t y = 0; y < v; ++y) {
+        if (isnan(row[y]) || row[y] == INFINITY) bad = 1;
+        if (isfinite(row[y])) finite = 1;
+      }
+      if (!finite) bad = 1;
+    }
     int32_t n = kd, tok = -1;
     for (int d = 0; d <= kd && !bad; ++d) {
       const float* row = target + (((int64_t)s * c + alive[0]) * (kd + 1) + d) * v;
       int64_t best = -1;
-      for (int64_t y = 0; y < v; ++y) {
-        if (isnan(row[y]) || row[y] == INFINITY) {
-          bad = 1;
-          break;
-        }
-        if (isfinite(row[y]) && (best < 0 || row[y] > row[best])) best = y;
-      }
-      if (bad || best < 0) {
-        bad = 1;
-        break;
-      }
+      for (int64_t y = 0; y < v; ++y)
+        if (isfinite(row[y]) && (best < 0 || row[y] > row[best])) best = y; /* strict: ties keep the smallest */
       if (d == kd) {
         tok = (int32_t)best;
         break;

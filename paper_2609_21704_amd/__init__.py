@@ -18,6 +18,7 @@ from ._lib import (  # noqa: F401
     sq_add_rmsnorm_f16,
     sq_attention_f16,
     sq_embed_block_f16,
+    sq_kv_adopt_f16,
     sq_qgemv_w4a16,
     sq_qgemv_w8a16,
     sq_quantize_fp8_e4m3,
@@ -26,7 +27,9 @@ from ._lib import (  # noqa: F401
     sq_rope_kv_f16,
     sq_silu_mul_f16,
     sq_spec_accept,
+    sq_spec_accept_multi,
     sq_spec_accept_noalloc,
     sq_spec_commit,
+    sq_spec_commit_multi,
     sq_verify_gemm_f16,
 )

@@ -60,6 +60,9 @@ def load() -> ctypes.CDLL:
             "sq_attention_f16": ([P, P, P, I32, I32, I32, I32, P, I32, I64, I64, P, P], S),
             "sq_silu_mul_f16": ([P, I64, I64, P, P], S),
             "sq_spec_commit": ([P, P, P, I32, I32, P, P, P, P, I64, P, P, P], S),
+            "sq_spec_accept_multi": ([P, P, P, P, I32, I32, I32, I32, F, P, P, P, P, P, P], S),
+            "sq_kv_adopt_f16": ([P, P, I32, I32, I32, I32, I64, P, P, P, I32, I32, P], S),
+            "sq_spec_commit_multi": ([P, P, P, P, I32, I32, I32, P, P, P, P, I64, P, P, P], S),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(lib, name)
@@ -72,7 +75,8 @@ def load() -> ctypes.CDLL:
 EXPORTED = ("sq_abi_version", "sq_status_str", "sq_quantize_int4_g128", "sq_quantize_fp8_e4m3",
             "sq_qgemv_w4a16", "sq_qgemv_w8a16", "sq_verify_gemm_f16", "sq_spec_accept",
             "sq_spec_accept_noalloc", "sq_probe_stream_read", "sq_embed_block_f16", "sq_add_rmsnorm_f16",
-            "sq_rope_kv_f16", "sq_attention_f16", "sq_silu_mul_f16", "sq_spec_commit")
+            "sq_rope_kv_f16", "sq_attention_f16", "sq_silu_mul_f16", "sq_spec_commit", "sq_spec_accept_multi",
+            "sq_kv_adopt_f16", "sq_spec_commit_multi")
 
 # device status bits (SQ_DEV_* of include/specquant.h)
 DEV_BAD_TOKEN, DEV_BAD_POS, DEV_OVERFLOW, DEV_NO_DIST = 1, 2, 4, 8
@@ -405,3 +409,75 @@ def sq_spec_commit(n_accepted, next_token, draft_tokens, pending, prev, pos_base
     _check(load().sq_spec_commit(_ptr(n_accepted), _ptr(next_token), _ptr(draft_tokens), b, kd, _ptr(pending),
                                  _ptr(prev), _ptr(pos_base), _ptr(out_tokens), cap, _ptr(out_len), _ptr(status),
                                  _stream(n_accepted.device)), "sq_spec_commit")
+
+
+# ------------------------------------------------------ several draft chains
+def sq_spec_accept_multi(draft_logits, target_logits, draft_tokens, u24, temperature: float = 1.0,
+                         n_accepted=None, next_token=None, chain=None, q_out=None, p_out=None):
+    """Multi-candidate accept / correct: draft_logits [kd][b][c][v],
+    target_logits [b][c][kd+1][v] f32, draft_tokens [kd][b][c] int32,
+    u24 [b][c kd + 1] int32 (uint32 bits).  Returns (n_accepted, next_token, chain)."""
+    b, c, kd1, v = target_logits.shape
+    kd = kd1 - 1
+    dev = target_logits.device
+    n_accepted = torch.empty((b,), dtype=torch.int32, device=dev) if n_accepted is None else n_accepted
+    next_token = torch.empty((b,), dtype=torch.int32, device=dev) if next_token is None else next_token
+    chain = torch.empty((b,), dtype=torch.int32, device=dev) if chain is None else chain
+    _dev(draft_logits, target_logits, draft_tokens, u24, n_accepted, next_token, chain, q_out, p_out)
+    if target_logits.dtype != torch.float32 or (draft_logits is not None and draft_logits.dtype != torch.float32):
+        raise TypeError("logits must be float32")
+    if draft_logits is not None and draft_logits.numel() != kd * b * c * v:
+        raise ValueError("draft_logits must be [kd][b][c][v]")
+    if draft_tokens is not None and (draft_tokens.dtype != torch.int32 or draft_tokens.numel() != kd * b * c):
+        raise ValueError("draft_tokens must be int32 [kd][b][c]")
+    if u24 is not None and (u24.dtype != torch.int32 or u24.numel() != b * (c * kd + 1)):
+        raise ValueError("u24 must be int32 [b][c kd + 1]")
+    for t, name in ((n_accepted, "n_accepted"), (next_token, "next_token"), (chain, "chain")):
+        _expect(t, torch.int32, (b,), name)
+    if q_out is not None:
+        _expect(q_out, torch.float32, (kd, b, c, v), "q_out")
+    if p_out is not None:
+        _expect(p_out, torch.float32, (b, c, kd + 1, v), "p_out")
+    _check(load().sq_spec_accept_multi(_ptr(draft_logits), _ptr(target_logits), _ptr(draft_tokens), _ptr(u24), b, c,
+                                       kd, v, float(temperature), _ptr(n_accepted), _ptr(next_token), _ptr(chain),
+                                       _ptr(q_out), _ptr(p_out), _stream(dev)), "sq_spec_accept_multi")
+    return n_accepted, next_token, chain
+
+
+def sq_kv_adopt_f16(k_cache, v_cache, b: int, c: int, chain, n_accepted, pos_base, lo_offset: int, hi_offset: int):
+    """Copy the accepted chain's cache entries to the other chains:
+    k_cache [layers][b c][hkv][capacity][128], v_cache [layers][b c][hkv][128][capacity]."""
+    layers, bc, hkv, cap, hd = k_cache.shape
+    if bc != b * c or hd != HEAD_DIM:
+        raise ValueError("k_cache must be [layers][b c][hkv][capacity][128]")
+    _expect(v_cache, torch.float16, (layers, bc, hkv, HEAD_DIM, cap), "v_cache")
+    _dev(k_cache, v_cache, chain, n_accepted, pos_base)
+    _expect(chain, torch.int32, (b,), "chain")
+    _expect(n_accepted, torch.int32, (b,), "n_accepted")
+    _expect(pos_base, torch.int32, (bc,), "pos_base")
+    _check(load().sq_kv_adopt_f16(_ptr(k_cache), _ptr(v_cache), layers, b, c, hkv, cap, _ptr(chain), _ptr(n_accepted),
+                                  _ptr(pos_base), int(lo_offset), int(hi_offset), _stream(k_cache.device)),
+           "sq_kv_adopt_f16")
+
+
+def sq_spec_commit_multi(n_accepted, next_token, chain, draft_tokens, c: int, pending, prev, pos_base,
+                         out_tokens=None, out_len=None, status=None):
+    """Commit a round of c chains per sequence (pending / prev / pos_base are [b c])."""
+    b = n_accepted.shape[0]
+    kd = 0 if draft_tokens is None else draft_tokens.shape[0]
+    _dev(n_accepted, next_token, chain, draft_tokens, pending, prev, pos_base, out_tokens, out_len, status)
+    for t, name in ((n_accepted, "n_accepted"), (next_token, "next_token"), (chain, "chain")):
+        _expect(t, torch.int32, (b,), name)
+    for t, name in ((pending, "pending"), (prev, "prev"), (pos_base, "pos_base")):
+        _expect(t, torch.int32, (b * c,), name)
+    if draft_tokens is not None and (draft_tokens.dtype != torch.int32 or draft_tokens.numel() != kd * b * c):
+        raise ValueError("draft_tokens must be int32 [kd][b][c]")
+    cap = 0
+    if out_tokens is not None:
+        if out_tokens.dtype != torch.int32 or out_tokens.dim() != 2 or out_tokens.shape[0] != b:
+            raise ValueError("out_tokens must be int32 [b][capacity]")
+        cap = out_tokens.shape[1]
+        _expect(out_len, torch.int32, (b,), "out_len")
+    _check(load().sq_spec_commit_multi(_ptr(n_accepted), _ptr(next_token), _ptr(chain), _ptr(draft_tokens), b, c, kd,
+                                       _ptr(pending), _ptr(prev), _ptr(pos_base), _ptr(out_tokens), cap, _ptr(out_len),
+                                       _ptr(status), _stream(n_accepted.device)), "sq_spec_commit_multi")

@@ -418,6 +418,84 @@ sq_status sq_spec_commit(const int32_t* n_accepted, const int32_t* next_token, c
                                               stream));
 }
 
+// ------------------------------------------------------ several draft chains
+sq_status sq_spec_accept_multi(const float* draft_logits, const float* target_logits, const int32_t* draft_tokens,
+                               const uint32_t* u24, int32_t b, int32_t c, int32_t kd, int32_t v, float temperature,
+                               int32_t* n_accepted, int32_t* next_token, int32_t* chain, float* q_out, float* p_out,
+                               hipStream_t stream) {
+  if (!target_logits || !n_accepted || !next_token || !chain) return SQ_ERR_NULL;
+  if (kd > 0 && (!draft_logits || !draft_tokens)) return SQ_ERR_NULL;
+  if (b < 1 || b > 65535 || c < 1 || c > 64 || kd < 0 || kd > 64 || v < 1 || v > (1 << 26)) return SQ_ERR_SHAPE;
+  const int64_t nchunk = (v + 4095) / 4096;
+  if ((int64_t)b * c * (2 * kd + 1) * nchunk >= (int64_t(1) << 24)) return SQ_ERR_SHAPE;
+  if (!isfinite(temperature)) return SQ_ERR_NONFINITE;
+  if (temperature < 0.0f) return SQ_ERR_UNSUPPORTED;
+  if (temperature == 0.0f && (q_out || p_out)) return SQ_ERR_UNSUPPORTED;
+  if (temperature > 0.0f && !u24) return SQ_ERR_NULL;
+  if (!aligned(draft_logits, 4) || !aligned(target_logits, 4) || !aligned(draft_tokens, 4) || !aligned(u24, 4) ||
+      !aligned(n_accepted, 4) || !aligned(next_token, 4) || !aligned(chain, 4) || !aligned(q_out, 4) ||
+      !aligned(p_out, 4))
+    return SQ_ERR_ALIGN;
+  const size_t bc = (size_t)b * c, bcv = bc * v;
+  const Range outs[] = {{n_accepted, (size_t)b * 4}, {next_token, (size_t)b * 4}, {chain, (size_t)b * 4},
+                        {q_out, (size_t)kd * bcv * 4}, {p_out, (size_t)(kd + 1) * bcv * 4}};
+  const Range ins[] = {{draft_logits, (size_t)kd * bcv * 4},
+                       {target_logits, (size_t)(kd + 1) * bcv * 4},
+                       {draft_tokens, (size_t)kd * bc * 4},
+                       {u24, temperature > 0.0f ? (size_t)b * (c * kd + 1) * 4 : 0}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_spec_accept_multi(draft_logits, target_logits, draft_tokens, u24, b, c, kd, v,
+                                                    temperature, n_accepted, next_token, chain, q_out, p_out,
+                                                    stream));
+}
+
+sq_status sq_kv_adopt_f16(uint16_t* k_cache, uint16_t* v_cache, int32_t layers, int32_t b, int32_t c, int32_t hkv,
+                          int64_t capacity, const int32_t* chain, const int32_t* n_accepted, const int32_t* pos_base,
+                          int32_t lo_offset, int32_t hi_offset, hipStream_t stream) {
+  if (!k_cache || !v_cache || !chain || !n_accepted || !pos_base) return SQ_ERR_NULL;
+  if (layers < 1 || layers > 65535 || b < 1 || c < 1 || c > 64 || (int64_t)b * c > 65535 || hkv < 1 ||
+      hkv > 65535 || capacity < 64 || capacity > kMaxN || capacity % 64 != 0 || lo_offset < -64 || lo_offset > 64 ||
+      hi_offset < -64 || hi_offset > 64)
+    return SQ_ERR_SHAPE;
+  if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(chain, 4) || !aligned(n_accepted, 4) ||
+      !aligned(pos_base, 4))
+    return SQ_ERR_ALIGN;
+  const size_t cache = (size_t)layers * b * c * hkv * capacity * 128 * 2;
+  const Range outs[] = {{k_cache, cache}, {v_cache, cache}};
+  const Range ins[] = {{chain, (size_t)b * 4}, {n_accepted, (size_t)b * 4}, {pos_base, (size_t)b * c * 4}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_kv_adopt(k_cache, v_cache, layers, b, c, hkv, capacity, chain, n_accepted, pos_base,
+                                           lo_offset, hi_offset, stream));
+}
+
+sq_status sq_spec_commit_multi(const int32_t* n_accepted, const int32_t* next_token, const int32_t* chain,
+                               const int32_t* draft_tokens, int32_t b, int32_t c, int32_t kd, int32_t* pending,
+                               int32_t* prev, int32_t* pos_base, int32_t* out_tokens, int64_t out_capacity,
+                               int32_t* out_len, int32_t* status, hipStream_t stream) {
+  if (!n_accepted || !next_token || !chain || !pending || !prev || !pos_base || (kd > 0 && !draft_tokens) ||
+      (out_tokens && !out_len))
+    return SQ_ERR_NULL;
+  if (b < 1 || b >= (1 << 24) || c < 1 || c > 64 || kd < 0 || kd > 64 ||
+      (out_tokens && (out_capacity < 1 || out_capacity > kMaxN)))
+    return SQ_ERR_SHAPE;
+  if (!aligned(n_accepted, 4) || !aligned(next_token, 4) || !aligned(chain, 4) || !aligned(draft_tokens, 4) ||
+      !aligned(pending, 4) || !aligned(prev, 4) || !aligned(pos_base, 4) || !aligned(out_tokens, 4) ||
+      !aligned(out_len, 4) || !aligned(status, 4))
+    return SQ_ERR_ALIGN;
+  const size_t b4 = (size_t)b * 4, bc4 = b4 * c;
+  const size_t hist = out_tokens ? (size_t)b * (size_t)out_capacity * 4 : 0;
+  const Range outs[] = {{pending, bc4}, {prev, bc4}, {pos_base, bc4}, {out_tokens, hist},
+                        {out_tokens ? out_len : nullptr, b4}, {status, 4}};
+  const Range ins[] = {{n_accepted, b4}, {next_token, b4}, {chain, b4}, {draft_tokens, (size_t)kd * bc4}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  return device_status(sq::launch_spec_commit_multi(n_accepted, next_token, chain, draft_tokens, b, c, kd, pending,
+                                                    prev, pos_base, out_tokens, out_capacity,
+                                                    out_tokens ? out_len : nullptr, status, stream));
+}
+
 }  // extern "C"
 
 namespace {

@@ -530,6 +530,293 @@ __global__ __launch_bounds__(kThreads) void greedy_kernel(const int32_t* __restr
   }
 }
 
+// ----------------------------------------------------- several draft chains
+// Multi-candidate acceptance: each sequence has c draft chains of kd tokens;
+// target rows [b][c][kd+1], draft rows [kd][b][c], tokens [kd][b][c],
+// uniforms [b][c kd + 1] (u[d c + j] tests chain j at depth d, u[c kd] drives
+// the final draw).  The fp32 distributions are materialised first (probs
+// kernel); then one workgroup of kMThreads per sequence walks the chains'
+// prefix tree with recursive rejection sampling on the int64 grid:
+//   first candidate at a node:   u q(x) < p(x) in fp64 (exact);
+//   its rejection:               R = rint(max(0, p - q) 2^60), Z = sum R;
+//   later candidates:            u q(x) Z < R(x), exact in 128-bit integers;
+//   their rejection:             R <- max(0, R - floor(q Z)), Z = sum R;
+//   Z == 0 after an update:      R = rint(p 2^60) (the node's p);
+//   all alive candidates fail:   draw from R; after kd accepted: from p_kd.
+// Integer sums do not depend on their order, so the results are those of the
+// same rule applied to the fp32 distributions in any order.
+constexpr int kMThreads = 1024;
+constexpr int kMWaves = kMThreads / 64;
+
+__device__ __forceinline__ int64_t mblock_sum_i64(int64_t v, int64_t* sh) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  __syncthreads();  // sh may still be read by an earlier call
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
+  __syncthreads();
+  int64_t t = 0;
+  for (int w = 0; w < kMWaves; ++w) t += sh[w];
+  return t;
+}
+
+// q = m 2^e exactly (m < 2^24), from the bits of a finite q >= 0.
+__device__ __forceinline__ void split_f32(float q, uint64_t& m, int& e) {
+  const uint32_t bits = __float_as_uint(q);
+  const uint32_t ex = (bits >> 23) & 0xFFu, man = bits & 0x7FFFFFu;
+  if (ex == 0) {
+    m = man;
+    e = -149;
+  } else {
+    m = man | 0x800000u;
+    e = (int)ex - 150;
+  }
+}
+
+// floor(q Z), q in [0, 1], 0 <= Z < 2^62, exactly.
+__device__ __forceinline__ int64_t floor_qz(float q, int64_t z) {
+  uint64_t m;
+  int e;
+  split_f32(q, m, e);
+  if (m == 0 || z == 0) return 0;
+  const uint64_t lo = m * (uint64_t)z, hi = __umul64hi(m, (uint64_t)z);
+  const int sh = -e;  // >= 23 for q <= 1
+  if (sh >= 128) return 0;
+  if (sh >= 64) return (int64_t)(hi >> (sh - 64));
+  return (int64_t)((hi << (64 - sh)) | (lo >> sh));
+}
+
+// u24 / 2^24 q Z < R, exactly.
+__device__ __forceinline__ bool test_grid(uint32_t u24, float q, int64_t z, int64_t r) {
+  if (r <= 0) return false;
+  uint64_t m;
+  int e;
+  split_f32(q, m, e);
+  const uint64_t a = (uint64_t)(u24 & 0xFFFFFFu) * m;  // < 2^48
+  const uint64_t llo = a * (uint64_t)z, lhi = __umul64hi(a, (uint64_t)z);
+  const int sh = 24 - e;  // >= 47 for q <= 1
+  const int bits = 64 - __clzll((unsigned long long)r);
+  if (bits + sh >= 127) return true;  // r 2^sh >= 2^126 > lhs
+  uint64_t rhi, rlo;
+  if (sh >= 64) {
+    rhi = (uint64_t)r << (sh - 64);
+    rlo = 0;
+  } else {
+    rhi = (uint64_t)r >> (64 - sh);
+    rlo = (uint64_t)r << sh;
+  }
+  return lhi < rhi || (lhi == rhi && llo < rlo);
+}
+
+__global__ __launch_bounds__(kMThreads) void multi_kernel(const float* __restrict__ p32, const float* __restrict__ q32,
+                                                          const int32_t* __restrict__ tokens,
+                                                          const uint32_t* __restrict__ u24, int b, int c, int kd,
+                                                          int v, int nchunk, const double2* __restrict__ stats,
+                                                          int64_t* __restrict__ grid, int32_t* __restrict__ n_accepted,
+                                                          int32_t* __restrict__ next_token,
+                                                          int32_t* __restrict__ chain) {
+  __shared__ int64_t sh[kMWaves];
+  __shared__ int sBad;
+  __shared__ int64_t sR;
+  __shared__ int sTok;
+  const int s = blockIdx.x;
+  const int t = threadIdx.x;
+  const int64_t rows_t = (int64_t)b * c * (kd + 1);
+  // every row of the sequence must have a distribution (its merged statistics finite)
+  if (t == 0) sBad = 0;
+  __syncthreads();
+  for (int rr = t >> 6; rr < c * (2 * kd + 1); rr += kMWaves) {
+    int64_t row;
+    if (rr < c * (kd + 1)) {
+      row = (int64_t)s * c * (kd + 1) + rr;
+    } else {
+      const int k2 = rr - c * (kd + 1);  // draft row d * c + j
+      row = rows_t + ((int64_t)(k2 / c) * b + s) * c + k2 % c;
+    }
+    double L, S;
+    wave_merge(stats + row * nchunk, nchunk, L, S);
+    if ((t & 63) == 0 && isnan(S)) atomicOr(&sBad, 1);
+  }
+  __syncthreads();
+  if (sBad) {
+    if (t == 0) n_accepted[s] = next_token[s] = chain[s] = -1;
+    return;
+  }
+  int64_t* R = grid + (int64_t)s * v;
+  const uint32_t* u = u24 + (int64_t)s * (c * kd + 1);
+  const uint64_t all = c == 64 ? ~0ull : ((1ull << c) - 1ull);
+  uint64_t alive = all;
+  int n = kd;
+  int64_t z = 0;
+  auto tok_of = [&](int d, int j) { return tokens[((int64_t)d * b + s) * c + j]; };
+  auto grid_p = [&](const float* p) -> int64_t {  // R = rint(p 2^60), returns Z
+    int64_t part = 0;
+    for (int y = t; y < v; y += kMThreads) {
+      const int64_t w = grid_weight((double)p[y]);
+      R[y] = w;
+      part += w;
+    }
+    return mblock_sum_i64(part, sh);
+  };
+  for (int d = 0; d < kd; ++d) {
+    const int j0 = __ffsll((unsigned long long)alive) - 1;
+    const float* p = p32 + (((int64_t)s * c + j0) * (kd + 1) + d) * v;
+    const float* q = q32 + (((int64_t)d * b + s) * c + j0) * v;
+    int accepted = -1;
+    bool first = true;
+    for (uint64_t rest = alive; rest; rest &= rest - 1) {
+      const int j = __ffsll((unsigned long long)rest) - 1;
+      const int32_t x = tok_of(d, j);
+      const uint32_t uj = u[d * c + j];
+      bool acc = false;
+      if (x >= 0 && x < v) {
+        if (first) {
+          acc = ldexp((double)(uj & 0xFFFFFFu), -24) * (double)q[x] < (double)p[x];
+        } else {
+          if (t == 0) sR = R[x];
+          __syncthreads();
+          acc = test_grid(uj, q[x], z, sR);
+          __syncthreads();
+        }
+      }
+      if (acc) {  // uniform: every thread took the same decision
+        accepted = x;
+        break;
+      }
+      int64_t part = 0;
+      if (first) {
+        for (int y = t; y < v; y += kMThreads) {
+          const double r = (double)p[y] - (double)q[y];
+          const int64_t w = grid_weight(r > 0.0 ? r : 0.0);
+          R[y] = w;
+          part += w;
+        }
+      } else {
+        const int64_t z0 = z;
+        for (int y = t; y < v; y += kMThreads) {
+          const int64_t w0 = R[y] - floor_qz(q[y], z0);
+          const int64_t w = w0 > 0 ? w0 : 0;
+          R[y] = w;
+          part += w;
+        }
+      }
+      z = mblock_sum_i64(part, sh);  // its barrier also publishes R to the workgroup
+      if (z == 0) z = grid_p(p);     // no residual mass on the grid: back to p
+      first = false;
+    }
+    if (accepted < 0) {
+      n = d;
+      break;
+    }
+    uint64_t keep = 0;
+    for (uint64_t rest = alive; rest; rest &= rest - 1) {
+      const int j = __ffsll((unsigned long long)rest) - 1;
+      if (tok_of(d, j) == accepted) keep |= 1ull << j;
+    }
+    alive = keep;
+  }
+  const int jf = __ffsll((unsigned long long)alive) - 1;
+  if (n == kd) z = grid_p(p32 + (((int64_t)s * c + jf) * (kd + 1) + kd) * v);
+  // the draw: t = floor(u Z / 2^24); thread i owns a contiguous segment of the row
+  if (t == 0) sTok = -1;
+  __syncthreads();
+  if (z > 0) {
+    const uint64_t uu = u[c * kd] & 0xFFFFFFu;
+    const int64_t tt = (int64_t)((__umul64hi(uu, (uint64_t)z) << 40) | ((uu * (uint64_t)z) >> 24));
+    const int seg = (v + kMThreads - 1) / kMThreads;
+    const int beg = t * seg, end = beg + seg < v ? beg + seg : v;
+    int64_t local = 0;
+    for (int y = beg; y < end; ++y) local += R[y];
+    // exclusive scan of the segment totals in thread order
+    const int lane = t & 63, w = t >> 6;
+    int64_t x = local;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int64_t yv = __shfl_up(x, off, 64);
+      if (lane >= off) x += yv;
+    }
+    __syncthreads();
+    if (lane == 63) sh[w] = x;
+    __syncthreads();
+    int64_t base = 0;
+    for (int i = 0; i < w; ++i) base += sh[i];
+    const int64_t pre = base + x - local;
+    if (local > 0 && pre <= tt && tt < pre + local) {
+      int64_t acc = pre;
+      for (int y = beg; y < end; ++y) {
+        acc += R[y];
+        if (acc > tt) {
+          sTok = y;
+          break;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  if (t == 0) {
+    n_accepted[s] = n;
+    next_token[s] = sTok;
+    chain[s] = jf;
+  }
+}
+
+// Greedy (T = 0) over several chains: per sequence, the argmax of the lowest
+// alive chain's row at each depth is accepted when an alive chain drafted it.
+__global__ __launch_bounds__(kThreads) void multi_greedy_kernel(const int32_t* __restrict__ tokens, int b, int c,
+                                                                int kd, int nchunk, const ArgMax* __restrict__ am,
+                                                                int32_t* __restrict__ n_accepted,
+                                                                int32_t* __restrict__ next_token,
+                                                                int32_t* __restrict__ chain) {
+  __shared__ int sArg[64 * 65];
+  const int s = blockIdx.x;
+  const int rows = c * (kd + 1);
+  for (int r = threadIdx.x; r < rows; r += kThreads) {
+    const ArgMax* a = am + ((int64_t)s * rows + r) * nchunk;
+    float best = -INFINITY;
+    int bi = kNone;
+    bool bad = false;
+    for (int k = 0; k < nchunk; ++k) {
+      const ArgMax e = a[k];
+      bad |= e.i == kBad;
+      if (e.i != kBad && e.i != kNone && (bi == kNone || e.v > best)) {  // chunks ascend: ties keep the earlier
+        best = e.v;
+        bi = e.i;
+      }
+    }
+    sArg[r] = (bad || bi == kNone) ? -1 : bi;
+  }
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  for (int r = 0; r < rows; ++r)
+    if (sArg[r] < 0) {
+      n_accepted[s] = next_token[s] = chain[s] = -1;
+      return;
+    }
+  uint64_t alive = c == 64 ? ~0ull : ((1ull << c) - 1ull);
+  int n = kd, tok = -1;
+  for (int d = 0; d <= kd; ++d) {
+    const int j0 = __ffsll((unsigned long long)alive) - 1;
+    const int g = sArg[j0 * (kd + 1) + d];
+    if (d == kd) {
+      tok = g;
+      break;
+    }
+    uint64_t keep = 0;
+    for (uint64_t rest = alive; rest; rest &= rest - 1) {
+      const int j = __ffsll((unsigned long long)rest) - 1;
+      if (tokens[((int64_t)d * b + s) * c + j] == g) keep |= 1ull << j;
+    }
+    if (!keep) {
+      n = d;
+      tok = g;
+      break;
+    }
+    alive = keep;
+  }
+  n_accepted[s] = n;
+  next_token[s] = tok;
+  chain[s] = __ffsll((unsigned long long)alive) - 1;
+}
+
 }  // namespace
 
 namespace {
@@ -642,6 +929,60 @@ hipError_t launch_spec_accept_noalloc(const float* draft, const float* target, c
   if (e != hipSuccess) return e;
   return enqueue_accept(draft, target, tokens, u24, b, kd, v, temperature, n_accepted, next_token, q_out, p_out, ws,
                         stream);
+}
+
+
+size_t spec_accept_multi_scratch_bytes(int b, int c, int kd, int v, float temperature, bool have_q, bool have_p) {
+  const int64_t nchunk = (v + kChunk - 1) / kChunk;
+  const int64_t rows_t = (int64_t)b * c * (kd + 1);
+  if (temperature == 0.0f) return ((size_t)rows_t * nchunk * sizeof(ArgMax) + 255) / 256 * 256;
+  const int64_t rows_d = (int64_t)kd * b * c;
+  size_t bytes = ((size_t)(rows_t + rows_d) * nchunk * sizeof(double2) + 255) / 256 * 256;  // stats
+  bytes += ((size_t)b * v * sizeof(int64_t) + 255) / 256 * 256;                              // residual grid
+  if (!have_p) bytes += ((size_t)rows_t * v * sizeof(float) + 255) / 256 * 256;
+  if (!have_q) bytes += ((size_t)rows_d * v * sizeof(float) + 255) / 256 * 256;
+  return bytes;
+}
+
+hipError_t launch_spec_accept_multi(const float* draft, const float* target, const int32_t* tokens,
+                                    const uint32_t* u24, int b, int c, int kd, int v, float temperature,
+                                    int32_t* n_accepted, int32_t* next_token, int32_t* chain, float* q_out,
+                                    float* p_out, hipStream_t stream) {
+  void* wsv = nullptr;
+  const hipError_t e =
+      workspace(spec_accept_multi_scratch_bytes(b, c, kd, v, temperature, q_out != nullptr, p_out != nullptr), stream,
+                &wsv);
+  if (e != hipSuccess) return e;
+  char* ws = static_cast<char*>(wsv);
+  const int nchunk = (v + kChunk - 1) / kChunk;
+  const int64_t rows_t = (int64_t)b * c * (kd + 1);
+  if (temperature == 0.0f) {
+    ArgMax* am = reinterpret_cast<ArgMax*>(ws);
+    hipLaunchKernelGGL(argmax_kernel, dim3((unsigned)(rows_t * nchunk)), dim3(kThreads), 0, stream, target, v, nchunk,
+                       am);
+    hipLaunchKernelGGL(multi_greedy_kernel, dim3((unsigned)b), dim3(kThreads), 0, stream, tokens, b, c, kd, nchunk, am,
+                       n_accepted, next_token, chain);
+    return hipGetLastError();
+  }
+  const int64_t rows_d = (int64_t)kd * b * c, rows = rows_t + rows_d;
+  double2* stats = reinterpret_cast<double2*>(ws);
+  ws += ((size_t)rows * nchunk * sizeof(double2) + 255) / 256 * 256;
+  int64_t* grid = reinterpret_cast<int64_t*>(ws);
+  ws += ((size_t)b * v * sizeof(int64_t) + 255) / 256 * 256;
+  float* p32 = p_out;
+  if (!p32) {
+    p32 = reinterpret_cast<float*>(ws);
+    ws += ((size_t)rows_t * v * sizeof(float) + 255) / 256 * 256;
+  }
+  float* q32 = q_out;
+  if (!q32 && rows_d > 0) q32 = reinterpret_cast<float*>(ws);
+  hipLaunchKernelGGL(stats_kernel, dim3((unsigned)(rows * nchunk)), dim3(kThreads), 0, stream, draft, target, rows_t,
+                     v, temperature, nchunk, stats);
+  hipLaunchKernelGGL(probs_kernel, dim3((unsigned)(rows * nchunk)), dim3(kThreads), 0, stream, draft, target, rows_t,
+                     v, temperature, nchunk, stats, q32, p32);
+  hipLaunchKernelGGL(multi_kernel, dim3((unsigned)b), dim3(kMThreads), 0, stream, p32, q32, tokens, u24, b, c, kd, v,
+                     nchunk, stats, grid, n_accepted, next_token, chain);
+  return hipGetLastError();
 }
 
 }  // namespace sq

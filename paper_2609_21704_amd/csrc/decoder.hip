@@ -10,6 +10,7 @@
 //   attn_merge_kernel   merge of the chunks in chunk order
 //   silu_mul_kernel     t = f16(g / (1 + exp(-g)) * u)
 //   commit_kernel       emitted tokens, next pending token, position
+//   kv_adopt_kernel, commit_multi_kernel  the same with several draft chains per sequence
 //
 // Cache layout, per model and layer: keys [b][hkv][capacity][128] (a key is
 // 256 contiguous bytes) and values position-minor, [b][hkv][128][capacity],
@@ -455,6 +456,80 @@ __global__ __launch_bounds__(256) void commit_kernel(const int32_t* __restrict__
   pos_base[bi] += n + 1;
 }
 
+// ------------------------------------------------ several chains per sequence
+// Sequence s drafts c chains, held as cache rows s * c + j of every layer
+// ([layers][b c][hkv][capacity][128] keys, [layers][b c][hkv][128][capacity]
+// values).  After acceptance the chain `chain[s]` holds the accepted prefix;
+// its entries at positions pos + lo_offset .. pos + n + hi_offset are copied
+// to the other chains of s (one workgroup per (layer, destination row, kv
+// head), lane d one dimension), so that every chain continues from it.
+__global__ __launch_bounds__(128) void kv_adopt_kernel(uint16_t* __restrict__ kc, uint16_t* __restrict__ vc, int bc,
+                                                       int c, int hkv, int64_t capacity,
+                                                       const int32_t* __restrict__ chain,
+                                                       const int32_t* __restrict__ n_accepted,
+                                                       const int32_t* __restrict__ pos_base, int lo_offset,
+                                                       int hi_offset) {
+  const int l = blockIdx.x, dst = blockIdx.y, g = blockIdx.z, d = threadIdx.x;
+  const int s = dst / c;
+  const int src_j = chain[s], n = n_accepted[s];
+  if (src_j < 0 || src_j >= c || n < 0 || dst == s * c + src_j) return;
+  const int src = s * c + src_j;
+  const int64_t pos = pos_base[src];
+  int64_t lo = pos + lo_offset, hi = pos + n + hi_offset;
+  lo = lo < 0 ? 0 : lo;
+  hi = hi >= capacity ? capacity - 1 : hi;
+  const int64_t kl = (int64_t)l * bc * hkv;
+  const uint16_t* ks = kc + ((kl + (int64_t)src * hkv + g) * capacity) * kHd;
+  uint16_t* kd_ = kc + ((kl + (int64_t)dst * hkv + g) * capacity) * kHd;
+  const uint16_t* vs = vc + ((kl + (int64_t)src * hkv + g) * kHd + d) * capacity;
+  uint16_t* vd = vc + ((kl + (int64_t)dst * hkv + g) * kHd + d) * capacity;
+  for (int64_t p = lo; p <= hi; ++p) {
+    kd_[p * kHd + d] = ks[p * kHd + d];
+    vd[p] = vs[p];
+  }
+}
+
+// The commit with c chains per sequence: the accepted chain's drafts, then
+// the next token, are emitted; every chain of the sequence restarts from it.
+__global__ __launch_bounds__(256) void commit_multi_kernel(const int32_t* __restrict__ n_accepted,
+                                                           const int32_t* __restrict__ next_token,
+                                                           const int32_t* __restrict__ chain,
+                                                           const int32_t* __restrict__ drafts, int b, int c, int kd,
+                                                           int32_t* __restrict__ pending, int32_t* __restrict__ prev,
+                                                           int32_t* __restrict__ pos_base,
+                                                           int32_t* __restrict__ out_tokens, int64_t out_capacity,
+                                                           int32_t* __restrict__ out_len,
+                                                           int32_t* __restrict__ status) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= b) return;
+  const int n = n_accepted[s], src = chain[s];
+  if (n < 0 || n > kd || src < 0 || src >= c) {  // the round had no distribution for this sequence
+    flag(status, kNoDist);
+    return;
+  }
+  auto draft = [&](int i) { return drafts[((int64_t)i * b + s) * c + src]; };
+  if (out_tokens) {
+    const int64_t len = out_len[s];
+    int32_t* dst = out_tokens + (int64_t)s * out_capacity;
+    for (int i = 0; i <= n; ++i) {
+      const int32_t tok = i < n ? draft(i) : next_token[s];
+      if (len + i >= 0 && len + i < out_capacity)
+        dst[len + i] = tok;
+      else
+        flag(status, kOverflow);
+    }
+    out_len[s] = (int32_t)(len + n + 1);
+  }
+  const int32_t pv = n >= 1 ? draft(n - 1) : pending[s * c + src];
+  const int32_t nx = next_token[s];
+  const int32_t pb = pos_base[s * c + src] + n + 1;
+  for (int j = 0; j < c; ++j) {
+    prev[s * c + j] = pv;
+    pending[s * c + j] = nx;
+    pos_base[s * c + j] = pb;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_embed_block(const uint16_t* table, int64_t vocab, int hidden, const int32_t* first,
@@ -544,6 +619,28 @@ hipError_t launch_spec_commit(const int32_t* n_accepted, const int32_t* next_tok
                               int64_t out_capacity, int32_t* out_len, int32_t* status, hipStream_t stream) {
   hipLaunchKernelGGL(commit_kernel, dim3((unsigned)((b + 255) / 256)), dim3(256), 0, stream, n_accepted, next_token,
                      drafts, b, kd, pending, prev, pos_base, out_tokens, out_capacity, out_len, status);
+  return hipGetLastError();
+}
+
+}  // namespace sq
+
+namespace sq {
+
+hipError_t launch_kv_adopt(uint16_t* kc, uint16_t* vc, int layers, int b, int c, int hkv, int64_t capacity,
+                           const int32_t* chain, const int32_t* n_accepted, const int32_t* pos_base, int lo_offset,
+                           int hi_offset, hipStream_t stream) {
+  hipLaunchKernelGGL(kv_adopt_kernel, dim3((unsigned)layers, (unsigned)(b * c), (unsigned)hkv), dim3(kHd), 0, stream,
+                     kc, vc, b * c, c, hkv, capacity, chain, n_accepted, pos_base, lo_offset, hi_offset);
+  return hipGetLastError();
+}
+
+hipError_t launch_spec_commit_multi(const int32_t* n_accepted, const int32_t* next_token, const int32_t* chain,
+                                    const int32_t* drafts, int b, int c, int kd, int32_t* pending, int32_t* prev,
+                                    int32_t* pos_base, int32_t* out_tokens, int64_t out_capacity, int32_t* out_len,
+                                    int32_t* status, hipStream_t stream) {
+  hipLaunchKernelGGL(commit_multi_kernel, dim3((unsigned)((b + 255) / 256)), dim3(256), 0, stream, n_accepted,
+                     next_token, chain, drafts, b, c, kd, pending, prev, pos_base, out_tokens, out_capacity, out_len,
+                     status);
   return hipGetLastError();
 }
 

@@ -97,4 +97,20 @@ hipError_t launch_spec_commit(const int32_t* n_accepted, const int32_t* next_tok
                               int kd, int32_t* pending, int32_t* prev, int32_t* pos_base, int32_t* out_tokens,
                               int64_t out_capacity, int32_t* out_len, int32_t* status, hipStream_t stream);
 
+// Multi-candidate acceptance over c draft chains per sequence (accept.hip).
+size_t spec_accept_multi_scratch_bytes(int b, int c, int kd, int v, float temperature, bool have_q, bool have_p);
+hipError_t launch_spec_accept_multi(const float* draft, const float* target, const int32_t* tokens,
+                                    const uint32_t* u24, int b, int c, int kd, int v, float temperature,
+                                    int32_t* n_accepted, int32_t* next_token, int32_t* chain, float* q_out,
+                                    float* p_out, hipStream_t stream);
+// Copy the accepted chain's cache entries to the other chains of its sequence;
+// the commit of a round with several chains (decoder.hip).
+hipError_t launch_kv_adopt(uint16_t* kc, uint16_t* vc, int layers, int b, int c, int hkv, int64_t capacity,
+                           const int32_t* chain, const int32_t* n_accepted, const int32_t* pos_base, int lo_offset,
+                           int hi_offset, hipStream_t stream);
+hipError_t launch_spec_commit_multi(const int32_t* n_accepted, const int32_t* next_token, const int32_t* chain,
+                                    const int32_t* drafts, int b, int c, int kd, int32_t* pending, int32_t* prev,
+                                    int32_t* pos_base, int32_t* out_tokens, int64_t out_capacity, int32_t* out_len,
+                                    int32_t* status, hipStream_t stream);
+
 }  // namespace sq

@@ -87,17 +87,18 @@ class DecoderWeights:
 
 
 class KVCache:
-    """Keys [b][hkv][capacity][128] and position-minor values
-    [b][hkv][128][capacity] per layer, fp16."""
+    """Keys [layers][rows][hkv][capacity][128] and position-minor values
+    [layers][rows][hkv][128][capacity], fp16, one allocation each; k[l] and
+    v[l] are the layer views the layer calls take."""
 
-    def __init__(self, cfg: Config, layers: int, batch: int, capacity: int, device):
+    def __init__(self, cfg: Config, layers: int, rows: int, capacity: int, device):
         if capacity % 64:
             raise ValueError("the cache capacity must be a multiple of 64")
         self.capacity = capacity
-        self.k = [torch.zeros((batch, cfg.kv_heads, capacity, HEAD_DIM), dtype=torch.float16, device=device)
-                  for _ in range(layers)]
-        self.v = [torch.zeros((batch, cfg.kv_heads, HEAD_DIM, capacity), dtype=torch.float16, device=device)
-                  for _ in range(layers)]
+        self.k_all = torch.zeros((layers, rows, cfg.kv_heads, capacity, HEAD_DIM), dtype=torch.float16, device=device)
+        self.v_all = torch.zeros((layers, rows, cfg.kv_heads, HEAD_DIM, capacity), dtype=torch.float16, device=device)
+        self.k = [self.k_all[l] for l in range(layers)]
+        self.v = [self.v_all[l] for l in range(layers)]
 
 
 class _Buffers:
@@ -119,47 +120,57 @@ class _Buffers:
 
 
 class SpecDecoder:
-    """Speculative rounds of one batch of sequences through the decoder."""
+    """Speculative rounds of one batch of sequences through the decoder.
+
+    With chains = c > 1 every sequence drafts c independent chains (its rows
+    s c .. s c + c - 1 in every draft and verification pass, each with its own
+    cache rows), and sq_spec_accept_multi accepts over them; the accepted
+    chain's cache entries are then copied to the other chains and all of them
+    restart from the emitted token."""
 
     def __init__(self, weights: DecoderWeights, batch: int | None = None, k: int | None = None,
-                 capacity: int = 1024, temperature: float = 1.0, history: int = 4096, keep_pq: bool = False):
+                 capacity: int = 1024, temperature: float = 1.0, history: int = 4096, keep_pq: bool = False,
+                 chains: int = 1):
         self.w = weights
         cfg = self.cfg = weights.cfg
         dev = self.device = weights.device
         self.B = B = cfg.batch if batch is None else batch
+        self.c = c = int(chains)
+        self.R = R = B * c  # rows of a draft step: one per chain
         self.k = k = cfg.k if k is None else k
         self.T = float(temperature)
         V = cfg.vocab
         L = weights.layers
-        if B * 2 > 8:
-            raise ValueError("draft step 0 runs 2 rows per sequence; the draft GEMV takes at most 8")
-        if B * (k + 1) > 64:
+        if R * 2 > 8:
+            raise ValueError("draft step 0 runs 2 rows per chain; the draft GEMV takes at most 8")
+        if R * (k + 1) > 64:
             raise ValueError("the verification pass takes at most 64 rows")
-        self.dcache = KVCache(cfg, L, B, capacity, dev)
-        self.pcache = KVCache(cfg, L, B, capacity, dev)
+        self.dcache = KVCache(cfg, L, R, capacity, dev)
+        self.pcache = KVCache(cfg, L, R, capacity, dev)
         self.capacity = capacity
         self.buf = _Buffers(cfg, 64, dev)  # the largest pass: 64 rows (verification, prefill chunks)
         i32, f32 = torch.int32, torch.float32
-        self.pos_base = torch.zeros((B,), dtype=i32, device=dev)
-        self.pending = torch.zeros((B,), dtype=i32, device=dev)
-        self.prev = torch.zeros((B,), dtype=i32, device=dev)
-        self.draft_tokens = torch.zeros((k, B), dtype=i32, device=dev)
-        self.draft_logits = torch.empty((k, B, V), dtype=f32, device=dev)
-        self.target_logits = torch.empty((B, k + 1, V), dtype=f32, device=dev)
-        self.u_draft = torch.zeros((k, B), dtype=i32, device=dev)
-        self.u_accept = torch.zeros((B, k + 1), dtype=i32, device=dev)
+        self.pos_base = torch.zeros((R,), dtype=i32, device=dev)
+        self.pending = torch.zeros((R,), dtype=i32, device=dev)
+        self.prev = torch.zeros((R,), dtype=i32, device=dev)
+        self.draft_tokens = torch.zeros((k, R), dtype=i32, device=dev)      # [k][B][c]
+        self.draft_logits = torch.empty((k, R, V), dtype=f32, device=dev)   # [k][B][c][V]
+        self.target_logits = torch.empty((R, k + 1, V), dtype=f32, device=dev)  # [B][c][k+1][V]
+        self.u_draft = torch.zeros((k, R), dtype=i32, device=dev)
+        self.u_accept = torch.zeros((B, c * k + 1), dtype=i32, device=dev)
         self.n_accepted = torch.zeros((B,), dtype=i32, device=dev)
         self.next_token = torch.zeros((B,), dtype=i32, device=dev)
-        self.scratch_n = torch.zeros((B,), dtype=i32, device=dev)
+        self.chain = torch.zeros((B,), dtype=i32, device=dev)
+        self.scratch_n = torch.zeros((R,), dtype=i32, device=dev)
         self.out_tokens = torch.zeros((B, history), dtype=i32, device=dev)
         self.out_len = torch.zeros((B,), dtype=i32, device=dev)
         self.status = torch.zeros((1,), dtype=i32, device=dev)
         self.keep_pq = keep_pq
         self.attn_hook = None  # called as hook(True / False, rows_per_seq, offset) around each attention call
         if keep_pq:
-            self.q_draft = torch.empty((k, B, V), dtype=f32, device=dev)   # draft-step distributions
-            self.q_out = torch.empty((k, B, V), dtype=f32, device=dev)
-            self.p_out = torch.empty((B, k + 1, V), dtype=f32, device=dev)
+            self.q_draft = torch.empty((k, R, V), dtype=f32, device=dev)   # draft-step distributions
+            self.q_out = torch.empty((k, R, V), dtype=f32, device=dev)
+            self.p_out = torch.empty((R, k + 1, V), dtype=f32, device=dev)
         self.graph = None
 
     # ------------------------------------------------------------- passes
@@ -172,12 +183,12 @@ class SpecDecoder:
 
     def forward(self, draft: bool, first, rest, rps: int, offset: int, logits, last_only: bool,
                 len_bound: int | None = None):
-        """One pass of the block (first [B], rest [rps-1][B]) at positions
-        pos_base + offset + j through the draft (or parent) model, writing its
-        cache entries; logits [B * (1 or rps)][V] f32 out."""
+        """One pass of the block (first [R], rest [rps-1][R], R = batch x
+        chains) at positions pos_base + offset + j through the draft (or
+        parent) model, writing its cache entries; logits [R * (1 or rps)][V]
+        f32 out."""
         cfg, w, b = self.cfg, self.w, self.buf
-        B = self.B
-        M = B * rps
+        M = self.R * rps
         if M > b.h.shape[0] or (draft and M > 8):
             raise ValueError("a pass takes at most 64 rows (8 for the draft GEMVs)")
         cache = self.dcache if draft else self.pcache
@@ -208,21 +219,23 @@ class SpecDecoder:
 
     def prefill(self, prompt: torch.Tensor, chunk: int | None = None):
         """Feed prompt [B][Lp] (int32, Lp >= 2) but its last token to both
-        models; the last token becomes the pending one at position Lp - 1."""
+        models (every chain of a sequence gets the sequence's prompt); the
+        last token becomes the pending one at position Lp - 1."""
         B, Lp = prompt.shape
         if B != self.B or Lp < 2 or Lp > self.capacity:
             raise ValueError("prompt must be [batch][2 .. capacity]")
-        prompt = prompt.to(device=self.device, dtype=torch.int32)
+        prompt = prompt.to(device=self.device, dtype=torch.int32).repeat_interleave(self.c, dim=0)
+        R = self.R
         self.pos_base.zero_()
         V = self.cfg.vocab
         for draft in (True, False):
             limit = 8 if draft else 64
-            c = max(1, min(chunk or limit, limit // B))
+            c = max(1, min(chunk or limit, limit // R))
             for s in range(0, Lp - 1, c):
                 n = min(c, Lp - 1 - s)
                 first = prompt[:, s].contiguous()
                 rest = prompt[:, s + 1:s + n].t().contiguous() if n > 1 else None
-                logits = torch.empty((B * n, V), dtype=torch.float32, device=self.device)
+                logits = torch.empty((R * n, V), dtype=torch.float32, device=self.device)
                 self.forward(draft, first, rest, n, s, logits, last_only=False, len_bound=s + n)
         self.pos_base.fill_(Lp - 1)
         self.pending.copy_(prompt[:, Lp - 1])
@@ -231,27 +244,44 @@ class SpecDecoder:
 
     # -------------------------------------------------------------- round
     def draft_step(self, i: int):
-        B, V = self.B, self.cfg.vocab
+        R, V = self.R, self.cfg.vocab
         if i == 0:
-            self.forward(True, self.prev, self.pending.view(1, B), 2, -1, self.draft_logits[0], last_only=True)
+            self.forward(True, self.prev, self.pending.view(1, R), 2, -1, self.draft_logits[0], last_only=True)
         else:
             self.forward(True, self.draft_tokens[i - 1], None, 1, i, self.draft_logits[i], last_only=True)
-        p_out = self.q_draft[i].view(B, 1, V) if self.keep_pq and self.T > 0 else None
-        sq.sq_spec_accept(None, self.draft_logits[i].view(B, 1, V), None, self.u_draft[i].view(B, 1), self.T,
+        p_out = self.q_draft[i].view(R, 1, V) if self.keep_pq and self.T > 0 else None
+        sq.sq_spec_accept(None, self.draft_logits[i].view(R, 1, V), None, self.u_draft[i].view(R, 1), self.T,
                           n_accepted=self.scratch_n, next_token=self.draft_tokens[i], p_out=p_out)
 
     def verify(self):
-        B, k, V = self.B, self.k, self.cfg.vocab
-        self.forward(False, self.pending, self.draft_tokens, k + 1, 0, self.target_logits.view(B * (k + 1), V),
+        R, k, V = self.R, self.k, self.cfg.vocab
+        self.forward(False, self.pending, self.draft_tokens, k + 1, 0, self.target_logits.view(R * (k + 1), V),
                      last_only=False)
 
     def accept_and_commit(self):
         keep = self.keep_pq and self.T > 0
-        sq.sq_spec_accept(self.draft_logits, self.target_logits, self.draft_tokens, self.u_accept, self.T,
-                          n_accepted=self.n_accepted, next_token=self.next_token,
-                          q_out=self.q_out if keep else None, p_out=self.p_out if keep else None)
-        sq.sq_spec_commit(self.n_accepted, self.next_token, self.draft_tokens, self.pending, self.prev,
-                          self.pos_base, out_tokens=self.out_tokens, out_len=self.out_len, status=self.status)
+        B, c, k, V = self.B, self.c, self.k, self.cfg.vocab
+        if c == 1:
+            sq.sq_spec_accept(self.draft_logits, self.target_logits, self.draft_tokens, self.u_accept, self.T,
+                              n_accepted=self.n_accepted, next_token=self.next_token,
+                              q_out=self.q_out if keep else None, p_out=self.p_out if keep else None)
+            sq.sq_spec_commit(self.n_accepted, self.next_token, self.draft_tokens, self.pending, self.prev,
+                              self.pos_base, out_tokens=self.out_tokens, out_len=self.out_len, status=self.status)
+            return
+        sq.sq_spec_accept_multi(self.draft_logits.view(k, B, c, V), self.target_logits.view(B, c, k + 1, V),
+                                self.draft_tokens.view(k, B, c), self.u_accept, self.T, n_accepted=self.n_accepted,
+                                next_token=self.next_token, chain=self.chain,
+                                q_out=self.q_out.view(k, B, c, V) if keep else None,
+                                p_out=self.p_out.view(B, c, k + 1, V) if keep else None)
+        # the accepted chain's entries to the other chains: the parent's at P .. P + n,
+        # the draft's at P - 1 .. P + n - 1
+        sq.sq_kv_adopt_f16(self.pcache.k_all, self.pcache.v_all, B, c, self.chain, self.n_accepted, self.pos_base,
+                           0, 0)
+        sq.sq_kv_adopt_f16(self.dcache.k_all, self.dcache.v_all, B, c, self.chain, self.n_accepted, self.pos_base,
+                           -1, -1)
+        sq.sq_spec_commit_multi(self.n_accepted, self.next_token, self.chain, self.draft_tokens, c, self.pending,
+                                self.prev, self.pos_base, out_tokens=self.out_tokens, out_len=self.out_len,
+                                status=self.status)
 
     def run(self):
         for i in range(self.k):

@@ -80,6 +80,12 @@ STUB(launch_attention, const uint16_t*, const uint16_t*, const uint16_t*, int, i
 STUB(launch_silu_mul, const float*, int64_t, int64_t, uint16_t*, hipStream_t)
 STUB(launch_spec_commit, const int32_t*, const int32_t*, const int32_t*, int, int, int32_t*, int32_t*, int32_t*,
      int32_t*, int64_t, int32_t*, int32_t*, hipStream_t)
+STUB(launch_spec_accept_multi, const float*, const float*, const int32_t*, const uint32_t*, int, int, int, int, float,
+     int32_t*, int32_t*, int32_t*, float*, float*, hipStream_t)
+STUB(launch_kv_adopt, uint16_t*, uint16_t*, int, int, int, int, int64_t, const int32_t*, const int32_t*, const int32_t*,
+     int, int, hipStream_t)
+STUB(launch_spec_commit_multi, const int32_t*, const int32_t*, const int32_t*, const int32_t*, int, int, int, int32_t*,
+     int32_t*, int32_t*, int32_t*, int64_t, int32_t*, int32_t*, hipStream_t)
 size_t spec_accept_scratch_bytes(int b, int kd, int v, float) {
   const size_t c = (size_t)(v + 4095) / 4096;
   return 16 * (size_t)b * (2 * kd + 1) * c + 16 * (size_t)b * c + 40 * (size_t)b;

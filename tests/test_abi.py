@@ -33,11 +33,11 @@ def test_library_exports_every_declared_symbol():
                           "sq_qgemv_w4a16", "sq_qgemv_w8a16", "sq_verify_gemm_f16", "sq_spec_accept",
                           "sq_spec_accept_noalloc", "sq_probe_stream_read", "sq_embed_block_f16",
                           "sq_add_rmsnorm_f16", "sq_rope_kv_f16", "sq_attention_f16", "sq_silu_mul_f16",
-                          "sq_spec_commit"}
+                          "sq_spec_commit", "sq_spec_accept_multi", "sq_kv_adopt_f16", "sq_spec_commit_multi"}
     assert set(names) == set(sq.EXPORTED)
     for n in names:
         assert hasattr(lib, n), n
-    assert sq.sq_abi_version() == 3
+    assert sq.sq_abi_version() == 4
     for s in range(9):
         assert lib.sq_status_str(s).startswith(b"SQ_")
     assert lib.sq_status_str(9) == b"unknown sq_status"
@@ -198,3 +198,30 @@ def test_decoder_layer_validation():
     assert com(A, B, A + 4096, 4, 3, C, C + 8, E, None, 0, None, None, None) == ALIAS   # prev overlaps pending
     assert com(A, B, A + 4096, 4, 3, C, D, A + 4, None, 0, None, None, None) == ALIAS   # pos_base on n_accepted
     assert com(A, B, A + 4096, 4, 3, C + 2, D, E, None, 0, None, None, None) == ALIGN
+
+
+def test_multi_chain_validation():
+    lib = sq.load()
+    acc = lib.sq_spec_accept_multi
+    # draft, target, tokens, u24, b, c, kd, v, T, n, next, chain, q_out, p_out, stream
+    assert acc(A, B, C, D, 2, 3, 4, 100, 1.0, E, E + 64, None, None, None, None) == NULL   # chain
+    assert acc(A, B, C, D, 2, 65, 4, 100, 1.0, E, E + 64, E + 128, None, None, None) == SHAPE   # c <= 64
+    assert acc(A, B, C, D, 2, 3, 65, 100, 1.0, E, E + 64, E + 128, None, None, None) == SHAPE   # kd <= 64
+    assert acc(A, B, C, D, 2, 3, 4, 100, float("nan"), E, E + 64, E + 128, None, None, None) == NONFINITE
+    assert acc(A, B, C, D, 2, 3, 4, 100, 0.0, E, E + 64, E + 128, E + 4096, None, None) == UNSUPPORTED
+    assert acc(A, B, C, None, 2, 3, 4, 100, 1.0, E, E + 64, E + 128, None, None, None) == NULL   # u24 at T > 0
+    assert acc(A, B, C, D, 2, 3, 4, 100, 1.0, E, E + 64, E + 130, None, None, None) == ALIGN
+    assert acc(A, B, C, D, 2, 3, 4, 100, 1.0, E, E + 4, E + 128, None, None, None) == ALIAS    # next on n
+    assert acc(A, B, C, D, 2, 3, 4, 100, 1.0, B + 64, E + 64, E + 128, None, None, None) == ALIAS  # n in target
+    ad = lib.sq_kv_adopt_f16
+    assert ad(None, B, 28, 1, 4, 4, 1024, C, D, E, 0, 0, None) == NULL
+    assert ad(A, B, 28, 1, 65, 4, 1024, C, D, E, 0, 0, None) == SHAPE
+    assert ad(A, B, 28, 1, 4, 4, 1000, C, D, E, 0, 0, None) == SHAPE
+    assert ad(A, B, 28, 1, 4, 4, 1024, C, D, E, -65, 0, None) == SHAPE
+    assert ad(A + 8, B, 28, 1, 4, 4, 1024, C, D, E, 0, 0, None) == ALIGN
+    assert ad(A, A + 1024, 28, 1, 4, 4, 1024, C, D, E, 0, 0, None) == ALIAS   # the caches overlap
+    cm = lib.sq_spec_commit_multi
+    assert cm(A, B, C, None, 2, 3, 4, D, D + 4096, E, None, 0, None, None, None) == NULL     # drafts
+    assert cm(A, B, C, A + 4096, 2, 0, 4, D, D + 4096, E, None, 0, None, None, None) == SHAPE
+    assert cm(A, B, C, A + 4096, 2, 3, 4, D, D + 8, E, None, 0, None, None, None) == ALIAS   # prev on pending
+    assert cm(A, B, C, A + 4096, 2, 3, 4, D + 2, D + 4096, E, None, 0, None, None, None) == ALIGN

@@ -303,34 +303,39 @@ def check_cache(sd_cache, o_cache, b, L, what):
 
 
 ROUND_CASES = [
-    # config, layers, batch, k, temperature, rounds, prompt length, variant
-    (0, 1, 1, 4, 1.0, 4, 40, "int4"),
-    (0, 1, 2, 3, 0.0, 3, 70, "fp8"),
-    (1, 2, 1, 4, 1.0, 3, 24, "int4"),
-    (1, 2, 4, 8, 1.0, 2, 9, "fp8"),
-    (2, 1, 1, 4, 1.0, 2, 20, "int4"),  # the 7B shape of the benchmark: its layer and its full LM head
+    # config, layers, batch, k, temperature, rounds, prompt length, variant, chains
+    (0, 1, 1, 4, 1.0, 4, 40, "int4", 1),
+    (0, 1, 2, 3, 0.0, 3, 70, "fp8", 1),
+    (1, 2, 1, 4, 1.0, 3, 24, "int4", 1),
+    (1, 2, 4, 8, 1.0, 2, 9, "fp8", 1),
+    (2, 1, 1, 4, 1.0, 2, 20, "int4", 1),  # the 7B shape of the benchmark: its layer and its full LM head
+    (0, 1, 1, 4, 1.0, 4, 33, "int4", 4),  # several draft chains per sequence
+    (1, 2, 2, 3, 1.0, 3, 10, "fp8", 2),
+    (0, 1, 2, 2, 0.0, 3, 21, "int4", 2),
+    (2, 1, 1, 4, 1.0, 2, 12, "int4", 4),
 ]
 
 
-@pytest.mark.parametrize("ci,layers,B,k,T,rounds,lp,variant", ROUND_CASES)
-def test_rounds_teacher_forced(ci, layers, B, k, T, rounds, lp, variant):
+@pytest.mark.parametrize("ci,layers,B,k,T,rounds,lp,variant,c", ROUND_CASES)
+def test_rounds_teacher_forced(ci, layers, B, k, T, rounds, lp, variant, c):
     cfg = CONFIGS[ci]
-    print(f"\n[rounds] config {ci} layers {layers} B {B} k {k} T {T} {variant}", flush=True)
+    print(f"\n[rounds] config {ci} layers {layers} B {B} k {k} T {T} {variant} chains {c}", flush=True)
     w = dec.DecoderWeights(cfg, DEV, layers=layers, variant=variant)
     cap = 128
-    sd = dec.SpecDecoder(w, batch=B, k=k, capacity=cap, temperature=T, keep_pq=True)
+    R = B * c
+    sd = dec.SpecDecoder(w, batch=B, k=k, capacity=cap, temperature=T, keep_pq=True, chains=c)
     prompt = dec.synthetic_prompt(cfg, B, lp, DEV)
     sd.prefill(prompt)
     torch.cuda.synchronize()
     dims, parent, draft = oracle_models(w, variant)
-    dc, pc = od.Cache(dims, B, cap), od.Cache(dims, B, cap)
-    st = od.prefill([draft, parent], [dc, pc], prompt.cpu().numpy())
-    for b in range(B):
-        check_cache(sd.pcache, pc, b, lp - 1, "parent cache after prefill")
-        check_cache(sd.dcache, dc, b, lp - 1, "draft cache after prefill")
+    dc, pc = od.Cache(dims, R, cap), od.Cache(dims, R, cap)
+    st = od.prefill_chains([draft, parent], [dc, pc], prompt.cpu().numpy(), c)
+    for row in range(R):
+        check_cache(sd.pcache, pc, row, lp - 1, "parent cache after prefill")
+        check_cache(sd.dcache, dc, row, lp - 1, "draft cache after prefill")
     V = w.cfg.vocab
-    ud = synth.uniform_u24((rounds, k, B), synth.stream_seed(cfg.seed, 90, B, k), DEV)
-    ua = synth.uniform_u24((rounds, B, k + 1), synth.stream_seed(cfg.seed, 91, B, k), DEV)
+    ud = synth.uniform_u24((rounds, k, R), synth.stream_seed(cfg.seed, 90, B, k), DEV)
+    ua = synth.uniform_u24((rounds, B, c * k + 1), synth.stream_seed(cfg.seed, 91, B, k), DEV)
     worst = 0.0
     n_all = []
     for r in range(rounds):
@@ -338,47 +343,60 @@ def test_rounds_teacher_forced(ci, layers, B, k, T, rounds, lp, variant):
         sd.run()
         torch.cuda.synchronize()
         assert sd.status.item() == 0
-        dt = sd.draft_tokens.cpu().numpy().astype(np.int64)
-        dl = sd.draft_logits.cpu().numpy()
-        tl = sd.target_logits.cpu().numpy()
+        dt = sd.draft_tokens.cpu().numpy().astype(np.int64)      # [k][R]
+        dl = sd.draft_logits.cpu().numpy()                       # [k][R][V]
+        tl = sd.target_logits.cpu().numpy()                      # [R][k+1][V]
         n_gpu = sd.n_accepted.cpu().numpy()
         nx_gpu = sd.next_token.cpu().numpy()
-        P = st.pos.copy()
+        ch_gpu = sd.chain.cpu().numpy()
+        P = np.repeat(st.pos, c)
+        prev, pend = np.repeat(st.prev, c), np.repeat(st.pending, c)
         for i in range(k):
             if i == 0:
-                toks, pos = np.stack([st.prev, st.pending], 1), np.stack([P - 1, P], 1)
+                toks, pos = np.stack([prev, pend], 1), np.stack([P - 1, P], 1)
             else:
                 toks, pos = dt[i - 1][:, None], (P + i)[:, None]
             ref = od.forward(draft, dc, toks, pos)[:, -1]
             worst = max(worst, check_logits(dl[i], ref, f"round {r} draft step {i}"))
             if T > 0:
-                qd = sd.q_draft[i].cpu().numpy()  # the sampler's fp32 distribution [B][V]
+                qd = sd.q_draft[i].cpu().numpy()  # the sampler's fp32 distribution [R][V]
                 _, tok = oracle.accept_probs(qd[:, None, :], None, None,
                                              ud[r, i].cpu().numpy().astype(np.uint32)[:, None])
                 assert np.array_equal(tok, dt[i]), f"round {r} draft draw {i}"
                 check_probs(qd, ref, dl[i], f"round {r} draft distribution {i}")
             else:
                 assert np.array_equal(np.argmax(dl[i], axis=1), dt[i])
-        block = np.concatenate([st.pending[:, None], dt.T], 1)
+        block = np.concatenate([pend[:, None], dt.T], 1)
         ref_t = od.forward(parent, pc, block, P[:, None] + np.arange(k + 1)[None, :])
         worst = max(worst, check_logits(tl, ref_t, f"round {r} verification"))
+        u32 = ua[r].cpu().numpy().astype(np.uint32)
         if T > 0:
             p_out, q_out = sd.p_out.cpu().numpy(), sd.q_out.cpu().numpy()
-            n_o, nx_o = oracle.accept_probs(p_out, q_out, dt.astype(np.int32), ua[r].cpu().numpy().astype(np.uint32))
+            if c == 1:
+                n_o, nx_o = oracle.accept_probs(p_out, q_out, dt.astype(np.int32), u32)
+                ch_o = np.zeros_like(n_o)
+            else:
+                n_o, nx_o, ch_o = oracle.multi_accept_probs(p_out.reshape(B, c, k + 1, V), q_out.reshape(k, B, c, V),
+                                                            dt.reshape(k, B, c).astype(np.int32), u32)
             check_probs(p_out.reshape(-1, V), ref_t.reshape(-1, V), tl.reshape(-1, V), f"round {r} parent distribution")
         else:
-            n_o, nx_o, _, _ = oracle.spec_accept(dl, tl, dt.astype(np.int32), None, 0.0)
+            n_o, nx_o, ch_o = oracle.multi_accept_greedy(tl.reshape(B, c, k + 1, V), dt.reshape(k, B, c))
         assert np.array_equal(n_o, n_gpu) and np.array_equal(nx_o, nx_gpu), f"round {r} decisions"
-        od.commit(st, n_gpu, nx_gpu, dt)
+        if c > 1:
+            assert np.array_equal(ch_o, ch_gpu), f"round {r} chains"
+        od.adopt(pc, dc, st.pos, n_gpu, ch_o, c)
+        sel = np.stack([dt.reshape(k, B, c)[:, s, ch_o[s]] for s in range(B)], 1)
+        od.commit(st, n_gpu, nx_gpu, sel)
         n_all.extend(n_gpu.tolist())
-        assert sd.pos_base.cpu().tolist() == st.pos.tolist()
-        assert sd.pending.cpu().tolist() == st.pending.tolist()
-        assert sd.prev.cpu().tolist() == st.prev.tolist()
+        assert sd.pos_base.cpu().tolist() == np.repeat(st.pos, c).tolist()
+        assert sd.pending.cpu().tolist() == np.repeat(st.pending, c).tolist()
+        assert sd.prev.cpu().tolist() == np.repeat(st.prev, c).tolist()
         out, out_len = sd.out_tokens.cpu().numpy(), sd.out_len.cpu().numpy()
         for b in range(B):
             assert out[b, :out_len[b]].tolist() == st.emitted[b]
-            check_cache(sd.pcache, pc, b, int(st.pos[b]), f"round {r} parent cache")
-            check_cache(sd.dcache, dc, b, int(st.pos[b]) - 1, f"round {r} draft cache")
+            for j in range(c):
+                check_cache(sd.pcache, pc, b * c + j, int(st.pos[b]), f"round {r} parent cache")
+                check_cache(sd.dcache, dc, b * c + j, int(st.pos[b]) - 1, f"round {r} draft cache")
     print(f"[rounds] worst logit error / rms {worst:.2e}; accepted per round {n_all}", flush=True)
 
 
@@ -390,11 +408,25 @@ def test_decoder_graph_replays_match_eager_rounds():
     w = dec.DecoderWeights(cfg, DEV, layers=2)
     a = dec.SpecDecoder(w, batch=B, k=k, capacity=cap)
     g = dec.SpecDecoder(w, batch=B, k=k, capacity=cap)
+    _replays_match(cfg, a, g, B, k, R)
+
+
+def test_decoder_graph_replays_match_eager_rounds_with_chains():
+    cfg = CONFIGS[1]
+    B, k, R, cap, c = 2, 2, 4, 128, 2
+    w = dec.DecoderWeights(cfg, DEV, layers=2)
+    a = dec.SpecDecoder(w, batch=B, k=k, capacity=cap, chains=c)
+    g = dec.SpecDecoder(w, batch=B, k=k, capacity=cap, chains=c)
+    _replays_match(cfg, a, g, B, k, R)
+
+
+def _replays_match(cfg, a, g, B, k, R):
     prompt = dec.synthetic_prompt(cfg, B, 12, DEV)
     a.prefill(prompt)
     g.prefill(prompt)
-    ud = synth.uniform_u24((R, k, B), synth.stream_seed(cfg.seed, 95), DEV)
-    ua = synth.uniform_u24((R, B, k + 1), synth.stream_seed(cfg.seed, 96), DEV)
+    c = a.c
+    ud = synth.uniform_u24((R, k, B * c), synth.stream_seed(cfg.seed, 95), DEV)
+    ua = synth.uniform_u24((R, B, c * k + 1), synth.stream_seed(cfg.seed, 96), DEV)
     snaps = []
     for r in range(R):
         a.set_uniforms(ud[r], ua[r])

@@ -243,3 +243,42 @@ def test_identical_draft_accepts_every_token():
         res = od.spec_round(m, m, dc, pc, st, k, ud, ua, temperature=1.0)
         assert np.all(res["n_accepted"] == k)
     assert st.pos.tolist() == [3 + 3 * (k + 1)] * B
+
+
+@pytest.mark.parametrize("variant", ["int4", "fp8"])
+def test_greedy_speculation_with_chains_emits_the_parent_greedy_decode(variant):
+    params = small_params(DIMS, 4)
+    parent = od.Model(DIMS, params, "f16")
+    draft = od.Model(DIMS, params, variant)
+    B, c, Lp, k, cap = 2, 3, 5, 3, 64
+    prompt = RNG.integers(0, DIMS.vocab, (B, Lp))
+    dc, pc = od.Cache(DIMS, B * c, cap), od.Cache(DIMS, B * c, cap)
+    st = od.prefill_chains([draft, parent], [dc, pc], prompt, c)
+    for _ in range(5):
+        od.spec_round_multi(draft, parent, dc, pc, st, c, k, None, None, temperature=0.0)
+    steps = min(len(e) for e in st.emitted)
+    ref = greedy_decode(parent, prompt, steps, cap)
+    for b in range(B):
+        assert st.emitted[b][:steps] == ref[b].tolist()
+        seq = np.concatenate([prompt[b], np.array(st.emitted[b][:-1])])
+        n = len(seq)
+        one = od.Cache(DIMS, 1, cap)
+        od.forward(parent, one, seq[None, :], np.arange(n)[None, :])
+        for j in range(c):  # every chain of the sequence holds the committed prefix
+            assert np.allclose(pc.k[:, b * c + j, :, :n], one.k[:, 0, :, :n], rtol=0, atol=2e-3)
+
+
+def test_chains_with_an_identical_draft_accept_every_token():
+    """Several chains at T = 1: a draft identical to the parent accepts every
+    token, from the lowest chain."""
+    params = small_params(DIMS, 5)
+    parent = od.Model(DIMS, params, "f16")
+    B, c, k = 2, 3, 3
+    prompt = RNG.integers(0, DIMS.vocab, (B, 4))
+    dc, pc = od.Cache(DIMS, B * c, 32), od.Cache(DIMS, B * c, 32)
+    st = od.prefill_chains([parent, parent], [dc, pc], prompt, c)
+    for _ in range(2):
+        ud = RNG.integers(0, 1 << 24, (k, B * c))
+        ua = RNG.integers(0, 1 << 24, (B, c * k + 1))
+        res = od.spec_round_multi(parent, parent, dc, pc, st, c, k, ud, ua, temperature=1.0)
+        assert (res["n_accepted"] == k).all() and (res["chain"] == 0).all()
