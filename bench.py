@@ -466,7 +466,7 @@ DECODER_CONTEXT = 1024   # prompt tokens in both caches when the timed decoder r
 DECODER_CAPACITY = 2048  # cache positions per sequence
 
 
-def measure_decoder(stack, temperature: float, steps: int, warmup: int):
+def measure_decoder(stack, temperature: float, steps: int, warmup: int, chains: int = 1):
     """The same rounds through full decoder layers with key/value caches
     (embedding, RMSNorm, q|k|v + bias, RoPE, causal GQA attention over the
     cache, SiLU-gated product, residuals; the matrices are the stack's): a
@@ -474,7 +474,9 @@ def measure_decoder(stack, temperature: float, steps: int, warmup: int):
     replays of whole rounds are timed; each round commits its tokens and rolls
     both caches back to the accepted prefix.  The attention calls of one eager
     round are timed with events for their roofline (HBM: 512 bytes per cached
-    position and kv head, plus the queries and outputs)."""
+    position and kv head, plus the queries and outputs).  With chains > 1 each
+    sequence drafts that many independent chains, verified in one pass and
+    accepted over their prefix tree."""
     import numpy as np
     import torch
 
@@ -484,11 +486,11 @@ def measure_decoder(stack, temperature: float, steps: int, warmup: int):
     cfg = stack.cfg
     B, k = cfg.batch, cfg.k
     w = dec.DecoderWeights(cfg, stack.device, stack=stack)
-    sd = dec.SpecDecoder(w, capacity=DECODER_CAPACITY, temperature=temperature)
+    sd = dec.SpecDecoder(w, capacity=DECODER_CAPACITY, temperature=temperature, chains=chains)
     sd.prefill(dec.synthetic_prompt(cfg, B, DECODER_CONTEXT, stack.device))
     total = 2 + warmup + steps  # round 0: eager attention timing, round 1: the eager run of capture
-    ud = synth.uniform_u24((total, k, B), synth.stream_seed(cfg.seed, 120), stack.device)
-    ua = synth.uniform_u24((total, B, k + 1), synth.stream_seed(cfg.seed, 121), stack.device)
+    ud = synth.uniform_u24((total, k, B * chains), synth.stream_seed(cfg.seed, 120, chains), stack.device)
+    ua = synth.uniform_u24((total, B, chains * k + 1), synth.stream_seed(cfg.seed, 121, chains), stack.device)
     n_hist = torch.zeros((total, B), dtype=torch.int32, device=stack.device)
 
     # round 0, eager: events around every attention call (positions are fixed until the commit)
@@ -513,7 +515,7 @@ def measure_decoder(stack, temperature: float, steps: int, warmup: int):
     for e0, e1, rps, offset in calls:
         att_sec += e0.elapsed_time(e1) * 1e-3
         last = pos + offset + rps - 1
-        att_bytes += float(((last + 1) * 512 * cfg.kv_heads).sum()) + 2 * B * rps * cfg.q_dim * 2
+        att_bytes += float(((last + 1) * 512 * cfg.kv_heads).sum()) + 2 * B * chains * rps * cfg.q_dim * 2
 
     sd.set_uniforms(ud[1], ua[1])
     sd.capture()
@@ -529,7 +531,7 @@ def measure_decoder(stack, temperature: float, steps: int, warmup: int):
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
-    pos0 = sd.pos_base.clone()
+    pos0 = sd.pos_base[::chains].clone()
     e0.record()
     for r in range(2 + warmup, total):
         one(r)
@@ -538,7 +540,7 @@ def measure_decoder(stack, temperature: float, steps: int, warmup: int):
     sec = e0.elapsed_time(e1) * 1e-3
     n_acc = n_hist[2 + warmup:].cpu().numpy().astype(np.int64)
     tokens = int((n_acc + 1).sum())
-    assert int((sd.pos_base - pos0).sum().item()) == tokens, "positions moved by the emitted tokens"
+    assert int((sd.pos_base[::chains] - pos0).sum().item()) == tokens, "positions moved by the emitted tokens"
     assert sd.status.item() == 0, "device status flags raised"
     achieved = att_bytes / att_sec / 1e9
     return {
@@ -547,6 +549,7 @@ def measure_decoder(stack, temperature: float, steps: int, warmup: int):
         "rounds": steps,
         "tokens_per_round": round(tokens / (steps * B), 4),
         "acceptance_rate": round(float(n_acc.sum()) / (steps * B * k), 4),
+        "chains": chains,
         "context_at_start": DECODER_CONTEXT,
         "cache_capacity": DECODER_CAPACITY,
         "what": "rounds through Qwen2.5-7B-shaped decoder layers (RMSNorm, q|k|v + bias, RoPE, GQA attention "
@@ -762,6 +765,8 @@ def main():
     if not args.no_decoder:
         out["decoder"] = measure_decoder(stack, args.temperature, args.steps, args.warmup)
         out["decoder"]["roofline_attention_long"] = measure_attention_long(dev)
+        out["decoder_chains"] = measure_decoder(stack, args.temperature, args.steps, args.warmup, chains=4)
+        del out["decoder_chains"]["roofline_attention"]
     if not args.no_fp8 and cfg.draft_variant == "int4":
         out["roofline_fp8"] = measure_fp8(args.gemv_steps, dev)
     if not args.no_cpu_baseline:
