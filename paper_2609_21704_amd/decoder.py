@@ -73,6 +73,13 @@ class DecoderWeights:
                 (synth.normal_f32((H,), 0.02, synth.stream_seed(s, _NORM_POST, l), dev) + 1.0).half())
             self.qkv_bias.append(synth.normal_f16((n_qkv,), 0.02, synth.stream_seed(s, _BIAS, l), dev))
 
+    def sibling(self, variant: str) -> "DecoderWeights":
+        """The same parent, embedding, norms and biases with another draft copy."""
+        other = DecoderWeights.__new__(DecoderWeights)
+        other.__dict__.update(self.__dict__)
+        other.stack = self.stack.sibling(variant)
+        return other
+
     def params(self) -> dict:
         """Every parameter by the oracle's names (host float16 copies)."""
         p = {"embed": self.embed, "final_norm": self.final_norm,
@@ -217,18 +224,36 @@ class SpecDecoder:
         sq.sq_add_rmsnorm_f16(h, w.final_norm, EPS, delta=delta, group=group, x=xf)
         self._linear(draft, (cfg.layers, "lm_head"), xf, logits)
 
-    def prefill(self, prompt: torch.Tensor, chunk: int | None = None):
-        """Feed prompt [B][Lp] (int32, Lp >= 2) but its last token to both
-        models (every chain of a sequence gets the sequence's prompt); the
-        last token becomes the pending one at position Lp - 1."""
+    def prefill(self, prompt: torch.Tensor, chunk: int | None = None, models=(True, False), lengths=None):
+        """Feed prompt [B][Lp] (int32) but its last token to both models
+        (every chain of a sequence gets the sequence's prompt); the last token
+        becomes the pending one at position Lp - 1.  `models` lists the passes
+        to run (True: the draft, False: the parent).
+
+        With lengths [B] (2 <= lengths[s] <= Lp) the prompts are ragged:
+        sequence s is prompt[s][:lengths[s]], and the tokens past it are
+        padding.  Every row is fed Lp - 1 tokens; a short row's entries from
+        its last prompt position on are rewritten before any row attends to
+        them, as a rolled-back draft block's are, so the padding is never
+        read."""
         B, Lp = prompt.shape
         if B != self.B or Lp < 2 or Lp > self.capacity:
             raise ValueError("prompt must be [batch][2 .. capacity]")
-        prompt = prompt.to(device=self.device, dtype=torch.int32).repeat_interleave(self.c, dim=0)
+        if lengths is None:
+            lens = torch.full((B,), Lp, dtype=torch.int64)
+        else:
+            lens = torch.as_tensor(lengths, dtype=torch.int64).cpu()
+            if lens.shape != (B,) or int(lens.min()) < 2 or int(lens.max()) > Lp:
+                raise ValueError("lengths must be [batch] in 2 .. prompt length")
+        host = prompt.to(device="cpu", dtype=torch.int32).repeat_interleave(self.c, dim=0)
+        lens = lens.repeat_interleave(self.c)
+        rows = torch.arange(self.R)
+        last, before = host[rows, lens - 1].contiguous(), host[rows, lens - 2].contiguous()
+        prompt = host.to(self.device)
         R = self.R
         self.pos_base.zero_()
         V = self.cfg.vocab
-        for draft in (True, False):
+        for draft in models:
             limit = 8 if draft else 64
             c = max(1, min(chunk or limit, limit // R))
             for s in range(0, Lp - 1, c):
@@ -237,9 +262,9 @@ class SpecDecoder:
                 rest = prompt[:, s + 1:s + n].t().contiguous() if n > 1 else None
                 logits = torch.empty((R * n, V), dtype=torch.float32, device=self.device)
                 self.forward(draft, first, rest, n, s, logits, last_only=False, len_bound=s + n)
-        self.pos_base.fill_(Lp - 1)
-        self.pending.copy_(prompt[:, Lp - 1])
-        self.prev.copy_(prompt[:, Lp - 2])
+        self.pos_base.copy_((lens - 1).to(torch.int32))
+        self.pending.copy_(last)
+        self.prev.copy_(before)
         self.out_len.zero_()
 
     # -------------------------------------------------------------- round
@@ -308,6 +333,56 @@ class SpecDecoder:
 
     def replay(self):
         self.graph.replay()
+
+
+class DirectDecoder(SpecDecoder):
+    """Direct parent inference (SS III-D.5) through the decoder: one token per
+    sequence and step from the FP16 parent alone (its pass at one row per
+    sequence, a draw from softmax(logits / T) or the argmax, the commit).  The
+    route of high-complexity prompts, and the plain-decoding baseline."""
+
+    def __init__(self, weights: DecoderWeights, batch: int | None = None, capacity: int = 1024,
+                 temperature: float = 1.0, history: int = 4096):
+        self.w = weights
+        cfg = self.cfg = weights.cfg
+        dev = self.device = weights.device
+        self.B = self.R = B = cfg.batch if batch is None else batch
+        self.c, self.k = 1, 0
+        self.T = float(temperature)
+        if B > 64:
+            raise ValueError("a parent pass takes at most 64 rows")
+        self.dcache = None
+        self.pcache = KVCache(cfg, weights.layers, B, capacity, dev)
+        self.capacity = capacity
+        self.buf = _Buffers(cfg, 64, dev)
+        i32 = torch.int32
+        self.pos_base = torch.zeros((B,), dtype=i32, device=dev)
+        self.pending = torch.zeros((B,), dtype=i32, device=dev)
+        self.prev = torch.zeros((B,), dtype=i32, device=dev)
+        self.logits = torch.empty((B, cfg.vocab), dtype=torch.float32, device=dev)
+        self.u = torch.zeros((B, 1), dtype=i32, device=dev)
+        self.n_accepted = torch.zeros((B,), dtype=i32, device=dev)
+        self.next_token = torch.zeros((B,), dtype=i32, device=dev)
+        self.out_tokens = torch.zeros((B, history), dtype=i32, device=dev)
+        self.out_len = torch.zeros((B,), dtype=i32, device=dev)
+        self.status = torch.zeros((1,), dtype=i32, device=dev)
+        self.keep_pq = False
+        self.attn_hook = None
+        self.graph = None
+
+    def prefill(self, prompt: torch.Tensor, chunk: int | None = None, models=(False,), lengths=None):
+        super().prefill(prompt, chunk, models=models, lengths=lengths)
+
+    def set_uniforms(self, u: torch.Tensor, _unused=None):
+        self.u.copy_(u.view(self.B, 1))
+
+    def run(self):
+        B, V = self.B, self.cfg.vocab
+        self.forward(False, self.pending, None, 1, 0, self.logits, last_only=False)
+        sq.sq_spec_accept(None, self.logits.view(B, 1, V), None, self.u, self.T, n_accepted=self.n_accepted,
+                          next_token=self.next_token)
+        sq.sq_spec_commit(self.n_accepted, self.next_token, None, self.pending, self.prev, self.pos_base,
+                          out_tokens=self.out_tokens, out_len=self.out_len, status=self.status)
 
 
 def synthetic_prompt(cfg: Config, batch: int, length: int, device) -> torch.Tensor:

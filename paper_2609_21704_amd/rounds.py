@@ -44,12 +44,29 @@ class Stack:
             w = synth.normal_f16((n, k), 0.02, synth.stream_seed(cfg.seed, _W, mid), self.device)
             if self.variant == "int4":
                 self.draft[(l, name)] = sq.sq_quantize_int4_g128(w)
-            else:
+            elif self.variant == "fp8":
                 self.draft[(l, name)] = sq.sq_quantize_fp8_e4m3(w)
+            elif self.variant != "none":  # "none": the parent alone, no draft copy
+                raise ValueError(f"unknown draft variant {self.variant!r}")
             if keep_f16:
                 self.w16[(l, name)] = w
             else:
                 del w
+
+    def sibling(self, variant: str) -> "Stack":
+        """The same FP16 parent with another quantized copy (every variant of
+        SS III-A derives from the one parent): shares the FP16 matrices."""
+        if not self.w16:
+            raise ValueError("a sibling needs the FP16 matrices")
+        if variant not in ("int4", "fp8"):
+            raise ValueError(f"unknown draft variant {variant!r}")
+        other = Stack.__new__(Stack)
+        other.cfg, other.device, other.variant, other.layers, other.mats = (self.cfg, self.device, variant, self.layers,
+                                                                             self.mats)
+        other.w16 = self.w16
+        other.draft = {key: (sq.sq_quantize_int4_g128(w) if variant == "int4" else sq.sq_quantize_fp8_e4m3(w))
+                       for key, w in self.w16.items()}
+        return other
 
     def draft_gemv(self, key, x, y):
         if self.variant == "int4":

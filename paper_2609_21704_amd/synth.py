@@ -50,3 +50,54 @@ def uniform_u24(shape, seed: int, device="cpu") -> torch.Tensor:
 def tokens(shape, vocab: int, seed: int, device="cpu") -> torch.Tensor:
     g = _gen(seed, device)
     return torch.randint(0, vocab, shape, generator=g, device=device, dtype=torch.int64).to(torch.int32)
+
+
+# ------------------------------------------------------------ prompt texts
+# Words of the synthetic prompt grammar (invented names and plain vocabulary).
+_NOUNS = ("river", "engine", "market", "garden", "signal", "ledger", "bridge", "harvest", "circuit", "library",
+          "orbit", "painting", "contract", "forest", "protein", "budget", "voyage", "lantern", "theory", "village")
+_VERBS = ("explain", "compare", "describe", "estimate", "summarise", "predict", "measure", "design", "justify",
+          "translate")
+_ADJS = ("ancient", "rapid", "fragile", "distant", "efficient", "hidden", "modest", "curious", "stable", "narrow")
+_NAMES = ("Varenholt", "Quillon", "Maribeth Oduya", "Port Celestine", "the Haldane Institute", "Tovrik", "NORDAX",
+          "Elsbeth Crane", "Lake Imari", "the Corvanne Group", "Dr. Pell", "Ashgrove")
+_SUBS = ("because", "although", "which", "while", "if", "that", "unless", "whereas", "since", "when")
+
+
+def prompt_texts(n: int, seed: int) -> list[str]:
+    """n seeded prompts with a mix of lengths and structures: short direct
+    questions, instructions of a few sentences, and long multi-clause
+    problems with numbers, names and parentheses."""
+    import random
+    rng = random.Random(stream_seed(seed, 0x7E47))
+    out = []
+    for _ in range(n):
+        style = rng.random()
+        if style < 0.3:
+            sents = 1
+            clause_p, entity_p, words = 0.05, 0.15, rng.randint(3, 9)
+        elif style < 0.8:
+            sents = rng.randint(1, 4)
+            clause_p, entity_p, words = 0.2, 0.3, rng.randint(6, 16)
+        else:
+            sents = rng.randint(3, 12)
+            clause_p, entity_p, words = 0.45, 0.5, rng.randint(10, 26)
+        text = []
+        for _ in range(sents):
+            w = [rng.choice(_VERBS).capitalize(), "the", rng.choice(_ADJS), rng.choice(_NOUNS)]
+            while len(w) < words:
+                r = rng.random()
+                if r < clause_p:
+                    w += [",", rng.choice(_SUBS), "the", rng.choice(_NOUNS), rng.choice(("is", "was", "seems"))]
+                elif r < clause_p + entity_p * 0.5:
+                    w += ["of", rng.choice(_NAMES)]
+                elif r < clause_p + entity_p * 0.7:
+                    w += ["in", str(rng.randint(2, 2099))]
+                elif r < clause_p + entity_p * 0.8:
+                    w += ["(", "see", rng.choice(_NAMES), ")"]
+                else:
+                    w += [rng.choice(("and", "with", "for", "near")), rng.choice(_ADJS), rng.choice(_NOUNS)]
+            text.append(" ".join(w).replace(" ,", ",").replace("( ", "(").replace(" )", ")") +
+                        rng.choice((".", "?", ".")))
+        out.append(" ".join(text))
+    return out
