@@ -569,6 +569,79 @@ def measure_decoder(stack, temperature: float, steps: int, warmup: int, chains: 
     }
 
 
+ROUTED_REQUESTS = 16  # text requests of the routed measurement
+ROUTED_NEW = 32       # tokens generated per request
+
+
+def measure_routed(stack, temperature: float):
+    """The execution pipeline end to end: ROUTED_REQUESTS synthetic text
+    requests are scored by the router and served by speculative decoding with
+    the INT4 or FP8 draft or by direct FP16 decoding (one parent, both drafts
+    resident), four sequences per batch, ROUTED_NEW tokens each; then the same
+    requests all decoded directly.  Wall time covers tokenisation, ragged
+    prefill of both caches, graph replays of the rounds and the host's checks
+    between rounds; the prefill and round phases are also given apart."""
+    import time
+
+    import torch
+
+    from paper_2609_21704_amd import decoder as dec
+    from paper_2609_21704_amd import synth
+    from paper_2609_21704_amd.engine import Engine
+    from paper_2609_21704_amd.router import ROUTES
+
+    cfg = stack.cfg
+    w = dec.DecoderWeights(cfg, stack.device, stack=stack)
+    eng = Engine(cfg, stack.device, k=cfg.k, batch=4, capacity=1024, temperature=temperature, parent=w,
+                 timed=True)
+    texts = synth.prompt_texts(ROUTED_REQUESTS, cfg.seed)
+    # untimed: every route once (library workspace, graph capture)
+    eng.generate([texts[0]] * 3, 4, routes=list(ROUTES))
+
+    def run(routes):
+        before = eng.stats()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        res = eng.generate(texts, ROUTED_NEW, routes=routes)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        after = eng.stats()
+        sec = {key: after["seconds"][key] - before["seconds"][key] for key in after["seconds"]}
+        rounds = {r: after["rounds"][r] - before["rounds"][r] for r in ROUTES}
+        tokens = sum(len(x.tokens) for x in res)
+        pre = sum(v for key, v in sec.items() if key.endswith("prefill"))
+        dec_s = sum(v for key, v in sec.items() if key.endswith("rounds"))
+        per_route = {}
+        for r in ROUTES:
+            n = sum(x.served_by == r for x in res)
+            if n:
+                per_route[r] = {"requests": n, "rounds": rounds[r],
+                                "decode_tokens_per_s": round(n * ROUTED_NEW / sec[f"{r}_rounds"], 2),
+                                "prefill_s": round(sec[f"{r}_prefill"], 4)}
+        return res, {"tokens_per_s": round(tokens / wall, 2), "wall_s": round(wall, 4), "prefill_s": round(pre, 4),
+                     "rounds_s": round(dec_s, 4), "decode_tokens_per_s": round(tokens / dec_s, 2),
+                     "per_route": per_route}
+
+    res, routed = run(None)
+    _, direct = run(["f16"] * len(texts))
+    del eng, w
+    torch.cuda.empty_cache()
+    mix = {r: sum(x.route == r for x in res) for r in ROUTES}
+    return {
+        "what": "synthetic text requests routed by prompt complexity (INT4 / FP8 speculative, FP16 direct) through "
+                "the 7B-shaped decoder, against the same requests all decoded directly",
+        "requests": len(texts),
+        "new_tokens_each": ROUTED_NEW,
+        "prompt_tokens": [x.prompt_tokens for x in res],
+        "mix": mix,
+        "temperature": temperature,
+        "routed": routed,
+        "all_direct": direct,
+        "speedup_vs_all_direct": round(routed["tokens_per_s"] / direct["tokens_per_s"], 3),
+        "decode_speedup_vs_all_direct": round(routed["decode_tokens_per_s"] / direct["decode_tokens_per_s"], 3),
+    }
+
+
 def measure_attention_long(dev, context: int = 8192, batch: int = 4, rows: int = 9, iters: int = 20):
     """The attention call alone at a bandwidth-sized shape: 4 sequences of
     8192 cached positions with Qwen2.5-7B heads (28 q / 4 kv), 9 rows per
@@ -767,6 +840,7 @@ def main():
         out["decoder"]["roofline_attention_long"] = measure_attention_long(dev)
         out["decoder_chains"] = measure_decoder(stack, args.temperature, args.steps, args.warmup, chains=4)
         del out["decoder_chains"]["roofline_attention"]
+        out["pipeline"] = measure_routed(stack, args.temperature)
     if not args.no_fp8 and cfg.draft_variant == "int4":
         out["roofline_fp8"] = measure_fp8(args.gemv_steps, dev)
     if not args.no_cpu_baseline:

@@ -22,6 +22,7 @@ beside the parent of every Qwen2.5 shape up to 72B, so no host path exists.
 from __future__ import annotations
 
 import dataclasses
+import time
 
 import torch
 
@@ -96,7 +97,11 @@ class Engine:
 
     def __init__(self, cfg: Config, device, layers: int | None = None, k: int | None = None, batch: int = 4,
                  capacity: int = 1024, temperature: float = 0.0, router: Router | None = None,
-                 chains: int = 1, free_bytes: int | None = None, seed: int | None = None):
+                 chains: int = 1, free_bytes: int | None = None, seed: int | None = None,
+                 parent: DecoderWeights | None = None, timed: bool = False):
+        """`parent`: existing FP16 parent weights (with one draft copy) to serve
+        from instead of building new ones.  `timed`: synchronise around each
+        batch's prefill and rounds and add their wall time to `seconds`."""
         self.cfg = cfg
         self.device = torch.device(device)
         self.k = cfg.k if k is None else k
@@ -108,8 +113,12 @@ class Engine:
             free_bytes = torch.cuda.mem_get_info(self.device)[0]
         self.plan = placement(cfg, free_bytes, batch * chains, capacity, self.k, L)
         resident = self.plan["resident"]
-        first = "int4" if "int4" in resident else ("fp8" if "fp8" in resident else "none")
-        parent = DecoderWeights(cfg, self.device, layers=L, variant=first)
+        if parent is None:
+            first = "int4" if "int4" in resident else ("fp8" if "fp8" in resident else "none")
+            parent = DecoderWeights(cfg, self.device, layers=L, variant=first)
+        elif parent.layers != L or parent.cfg.vocab != cfg.vocab or parent.cfg.hidden != cfg.hidden:
+            raise ValueError("the parent weights do not have this configuration's shape")
+        first = parent.stack.variant
         self.weights = {"f16": parent}
         for v in ("int4", "fp8"):
             if v in resident:
@@ -118,6 +127,8 @@ class Engine:
         self.rounds = {r: 0 for r in ROUTES}   # rounds run per variant
         self.emitted = {r: 0 for r in ROUTES}  # tokens kept per variant
         self._batches = 0
+        self.timed = timed
+        self.seconds = {(r, phase): 0.0 for r in ROUTES for phase in ("prefill", "rounds")}
 
     def decoder(self, variant: str):
         if variant not in self.decoders:
@@ -182,7 +193,9 @@ class Engine:
         prompt = torch.zeros((self.batch, Lp), dtype=torch.int32)
         for i, t in enumerate(rows):
             prompt[i, :len(t)] = torch.tensor(t, dtype=torch.int32)
+        t0 = self._clock()
         dec.prefill(prompt, lengths=[len(t) for t in rows])
+        t1 = self._clock()
         per_round = 1 if variant == "f16" else self.k + 1
         r = 0
         while True:
@@ -197,6 +210,10 @@ class Engine:
                 break
             if r > max_new:
                 raise RuntimeError("a round emitted no token")
+        t2 = self._clock()
+        if self.timed:
+            self.seconds[(variant, "prefill")] += t1 - t0
+            self.seconds[(variant, "rounds")] += t2 - t1
         if int(dec.status.item()) != 0:
             raise RuntimeError(f"device status flags {int(dec.status.item())} raised")
         self._batches += 1
@@ -204,6 +221,15 @@ class Engine:
         self.emitted[variant] += n * max_new
         return dec.out_tokens[:n, :max_new].cpu().tolist()
 
+    def _clock(self) -> float:
+        if not self.timed:
+            return 0.0
+        torch.cuda.synchronize(self.device)
+        return time.perf_counter()
+
     def stats(self) -> dict:
-        return {"rounds": dict(self.rounds), "emitted": dict(self.emitted)}
+        out = {"rounds": dict(self.rounds), "emitted": dict(self.emitted)}
+        if self.timed:
+            out["seconds"] = {f"{r}_{ph}": round(v, 6) for (r, ph), v in self.seconds.items()}
+        return out
 
