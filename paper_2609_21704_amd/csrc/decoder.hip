@@ -7,7 +7,7 @@
 //   rope_kv_kernel      bias, rotary embedding of q and k, cache write of k, v
 //   attn_chunk_kernel   causal grouped-query attention over a slot of 64-position
 //                       chunks of the cache on the matrix cores (partial softmax)
-//   attn_merge_kernel   merge of the chunks in chunk order
+//   attn_merge_kernel   merge of the slots in slot order
 //   silu_mul_kernel     t = f16(g / (1 + exp(-g)) * u)
 //   commit_kernel       emitted tokens, next pending token, position
 //   kv_adopt_kernel, commit_multi_kernel  the same with several draft chains per sequence
@@ -65,8 +65,9 @@ __global__ __launch_bounds__(256) void embed_kernel(const uint16_t* __restrict__
 
 // ---------------------------------------------------- residual add + norm
 // One workgroup of 256 threads per row of h; thread i holds the float4 cells
-// i, i + 256, ... of the row in registers (NV of them: hidden <= 1024 NV), so
-// that every load of the row is issued before the first use.  Every row gets
+// i, i + 256, ... of the row in registers (NV of them: hidden <= 1024 NV).
+// Every global load (the row of h, of delta and the norm weights) is issued
+// before the first use, so the kernel waits for memory once.  Every row gets
 // the residual add; the rows r * group + group - 1 are normalised into output
 // row r.
 template <int NV>
@@ -78,18 +79,22 @@ __global__ __launch_bounds__(256) void add_rmsnorm_kernel(float* __restrict__ h,
   float* hr = h + row * hidden;
   const bool out_row = (row % group) == group - 1;
   const int n4 = hidden >> 2;
-  float4_t v[NV];
+  float4_t v[NV], d[NV];
+  uint2 wv[NV];
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
     const int c = (int)threadIdx.x + 256 * i;
-    v[i] = c < n4 ? reinterpret_cast<const float4_t*>(hr)[c] : float4_t{0.f, 0.f, 0.f, 0.f};
+    const bool ok = c < n4;
+    v[i] = ok ? reinterpret_cast<const float4_t*>(hr)[c] : float4_t{0.f, 0.f, 0.f, 0.f};
+    d[i] = ok && delta ? reinterpret_cast<const float4_t*>(delta + row * hidden)[c] : float4_t{0.f, 0.f, 0.f, 0.f};
+    wv[i] = ok && out_row ? reinterpret_cast<const uint2*>(w)[c] : uint2{0u, 0u};
   }
   if (delta) {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int c = (int)threadIdx.x + 256 * i;
       if (c < n4) {
-        v[i] += reinterpret_cast<const float4_t*>(delta + row * hidden)[c];
+        v[i] += d[i];
         reinterpret_cast<float4_t*>(hr)[c] = v[i];
       }
     }
@@ -108,7 +113,7 @@ __global__ __launch_bounds__(256) void add_rmsnorm_kernel(float* __restrict__ h,
   for (int i = 0; i < NV; ++i) {
     const int c = (int)threadIdx.x + 256 * i;
     if (c < n4) {
-      const half4_t wh = __builtin_bit_cast(half4_t, reinterpret_cast<const uint2*>(w)[c]);
+      const half4_t wh = __builtin_bit_cast(half4_t, wv[i]);
       half4_t o;
 #pragma unroll
       for (int e = 0; e < 4; ++e) o[e] = (half_t)(v[i][e] * r * (float)wh[e]);
@@ -126,9 +131,20 @@ __global__ __launch_bounds__(64) void rope_kv_kernel(const float* __restrict__ q
                                                      uint16_t* __restrict__ vc, int32_t* __restrict__ status) {
   const int r = blockIdx.x, hh = blockIdx.y;
   const int bi = r / rps, j = r - bi * rps;
-  const int64_t pos = (int64_t)pos_base[bi] + pos_offset + j;
   const int t = threadIdx.x;
   const int nh = hq + 2 * hkv;
+  // the loads first (their addresses do not depend on the position), and the
+  // frequency theta^(-2t/128) while they are in flight
+  const int64_t pos = (int64_t)pos_base[bi] + pos_offset + j;
+  const float* src = qkv + ((int64_t)r * nh + hh) * kHd;
+  float a = src[t], e = src[t + 64];
+  float ba = 0.f, be = 0.f;
+  if (bias) {
+    ba = f16_bits_to_f32(bias[hh * kHd + t]);
+    be = f16_bits_to_f32(bias[hh * kHd + t + 64]);
+  }
+  const bool rot = hh < hq + hkv;
+  const double freq = rot ? pow(theta, -2.0 * (double)t / (double)kHd) : 0.0;
   if (pos < 0 || pos >= len_bound) {
     if (hh < hq) {
       q_out[((int64_t)r * hq + hh) * kHd + t] = kNanF16;
@@ -137,15 +153,13 @@ __global__ __launch_bounds__(64) void rope_kv_kernel(const float* __restrict__ q
     if (t == 0 && hh == 0) flag(status, kBadPos);
     return;
   }
-  const float* src = qkv + ((int64_t)r * nh + hh) * kHd;
-  float a = src[t], e = src[t + 64];
   if (bias) {
-    a += f16_bits_to_f32(bias[hh * kHd + t]);
-    e += f16_bits_to_f32(bias[hh * kHd + t + 64]);
+    a += ba;
+    e += be;
   }
-  if (hh < hq + hkv) {
+  if (rot) {
     // angle pos * theta^(-2t/128) and its cosine and sine in fp64, the turn in fp32
-    const double ang = (double)pos * pow(theta, -2.0 * (double)t / (double)kHd);
+    const double ang = (double)pos * freq;
     double sn, cs;
     sincos(ang, &sn, &cs);
     const float c = (float)cs, sv = (float)sn;
@@ -161,15 +175,12 @@ __global__ __launch_bounds__(64) void rope_kv_kernel(const float* __restrict__ q
   }
 }
 
-// ------------------------------------------------------- attention chunks
-// One workgroup per (slot, sequence bi, kv head g); slot s covers the `span`
-// consecutive 64-position chunks s * span .. s * span + span - 1 of the cache.
-// Its query rows are the block's rows of bi times the G = hq / hkv heads of
-// g, ordered qi = j * G + gg, in tiles of 16, one tile per wavefront (up to 4
-// wavefronts, which read the same cache fragments; with more tiles, span 1
-// and each wavefront takes every 4th tile).  On the matrix cores
-// (v_mfma_f32_16x16x32_f16; lane l holds A[l%16][8(l/16) .. +8) and
-// B[8(l/16) .. +8)[l%16], D[4(l/16) + i][l%16]):
+// ------------------------------------------------------------- attention
+// Query rows of a block, per (sequence bi, kv head g): the block's rows of bi
+// times the G = hq / hkv heads of g, ordered qi = j * G + gg, in tiles of 16.
+// A wavefront takes one tile over a run of 64-position chunks of the cache,
+// on the matrix cores (v_mfma_f32_16x16x32_f16; lane l holds A[l%16][8(l/16)
+// .. +8) and B[8(l/16) .. +8)[l%16], D[4(l/16) + i][l%16]):
 //   S^T = K . Q^T  -- A: 16 keys x 32 of the head dimension (lane l: key l%16,
 //                     dims 32(l/16) + 8s .. +8 for step s), B: the same dims of
 //                     16 query rows; lane l ends with the scores of keys
@@ -179,135 +190,172 @@ __global__ __launch_bounds__(64) void rope_kv_kernel(const float* __restrict__ q
 //                     16 + 4(l/16) + i of query l%16), and B takes the values
 //                     of the same 8 keys at dim l%16 (+16 per output tile)
 //                     from the position-minor value cache.
-// Across the chunks of its slot the wavefront keeps, per query row, the
-// running maximum m of the scaled scores (log2 units), l = sum of the
-// weights p = 2^(s - m) and O = sum p v, rescaled by 2^(m_old - m_new) when
-// m grows; the slot's (m, l, O) is its partial result.  Keys after a row's
-// position get p = 0; keys after the last row's position are not read (their
-// fragments are zero).
-__global__ __launch_bounds__(256) void attn_chunk_kernel(const uint16_t* __restrict__ q,
-                                                         const uint16_t* __restrict__ kc,
-                                                         const uint16_t* __restrict__ vc, int hq, int hkv, int rps,
-                                                         int64_t capacity, const int32_t* __restrict__ pos_base,
-                                                         int pos_offset, int nslots, int span, int nq_pad,
-                                                         float* __restrict__ part_o, float2* __restrict__ part_ml) {
+// Across its chunks the wavefront keeps, per query row, the running maximum m
+// of the scaled scores (log2 units), l = sum of the weights p = 2^(s - m) and
+// O = sum p v, rescaled by 2^(m_old - m_new) when m grows.  Keys after a row's
+// position get p = 0.  Partial results (m, l, O) of several wavefronts merge
+// as out = sum_w 2^(m_w - M) O_w / sum_w 2^(m_w - M) l_w, M = max_w m_w.
+struct AttnTile {
+  int hq, rps, G, nq;
+};
+
+__device__ __forceinline__ void attn_load_q(const uint16_t* __restrict__ q, const AttnTile& a, int bi, int g, int qt,
+                                            int li, int lg, half8_t (&qf)[4]) {
+  const half8_t zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
+  const int qi = 16 * qt + li;
+  const bool qok = qi < a.nq;
+  const int j = qok ? qi / a.G : 0, gg = qok ? qi - (qi / a.G) * a.G : 0;
+  const half8_t* qp =
+      reinterpret_cast<const half8_t*>(q + (((int64_t)bi * a.rps + j) * a.hq + g * a.G + gg) * kHd + 32 * lg);
+#pragma unroll
+  for (int s = 0; s < 4; ++s) qf[s] = qok ? qp[s] : zero8;
+}
+
+// A chunk's key and value fragments, loaded whole (the caller keeps key0 + 63
+// inside the cache).
+__device__ __forceinline__ void attn_load_kv(const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
+                                             int64_t bg, int64_t capacity, int64_t key0, int li, int lg,
+                                             half8_t (&kf)[4][4], half8_t (&vf)[2][8]) {
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt) {
+    const int64_t key = key0 + 16 * kt + li;
+    const half8_t* kp = reinterpret_cast<const half8_t*>(kc + (bg * capacity + key) * kHd + 32 * lg);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) kf[kt][s] = kp[s];
+  }
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2) {
+    const int64_t ka = key0 + 32 * t2 + 4 * lg, kb = ka + 16;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) {
+      const uint16_t* vp = vc + (bg * kHd + 16 * dt + li) * capacity;
+      const half4_t a = *reinterpret_cast<const half4_t*>(vp + ka);
+      const half4_t b = *reinterpret_cast<const half4_t*>(vp + kb);
+      half8_t f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        f[e] = a[e];
+        f[4 + e] = b[e];
+      }
+      vf[t2][dt] = f;
+    }
+  }
+}
+
+// Zero the values of keys after the last row's position: stale entries may
+// hold anything, and a zero weight times a NaN value is NaN.  Their keys need
+// no mask: such a key's score only reaches its own entry of S, which the
+// causal mask replaces by -inf.
+__device__ __forceinline__ void attn_mask_v(int64_t key0, int64_t pmax, int lg, half8_t (&vf)[2][8]) {
+  if (key0 + kChunk - 1 <= pmax) return;  // uniform: every key of the chunk is read
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2) {
+    const int64_t ka = key0 + 32 * t2 + 4 * lg, kb = ka + 16;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) {
+      half8_t f = vf[t2][dt];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        f[e] = ka + e <= pmax ? f[e] : (half_t)0;
+        f[4 + e] = kb + e <= pmax ? f[4 + e] : (half_t)0;
+      }
+      vf[t2][dt] = f;
+    }
+  }
+}
+
+// One chunk (keys key0 .. key0 + 63) into tile qt's running (m, l, O).
+__device__ __forceinline__ void attn_update(const AttnTile& a, int64_t p0, int qt, int li, int lg,
+                                            const half8_t (&qf)[4], const half8_t (&kf)[4][4],
+                                            const half8_t (&vf)[2][8], int64_t key0, float& m, float& l,
+                                            float4_t (&o)[8]) {
+  const float sl2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
+  const int qi = 16 * qt + li;
+  const bool qok = qi < a.nq;
+  const int j = qok ? qi / a.G : 0;
+  float4_t st[4];
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt) {
+    float4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf[kt][s], qf[s], acc, 0, 0, 0);
+    st[kt] = acc;
+  }
+  const int64_t qpos = p0 + j;
+  float cm = -__builtin_inff();
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t key = key0 + 16 * kt + 4 * lg + i;
+      const float v = (qok && key <= qpos) ? st[kt][i] * sl2 : -__builtin_inff();
+      st[kt][i] = v;
+      cm = fmaxf(cm, v);
+    }
+  cm = fmaxf(cm, __shfl_xor(cm, 16, kWave));
+  cm = fmaxf(cm, __shfl_xor(cm, 32, kWave));
+  const float mn = fmaxf(m, cm);
+  const bool none = mn == -__builtin_inff();  // no key of this row so far
+  const float alpha = none ? 1.f : exp2f(m - mn);
+  // p = hi + lo, both binary16 (hi = f16(p), lo = f16(p - hi), the difference
+  // exact in fp32): two products with the values carry p to about 2^-22
+  float psum = 0.f;
+  half8_t pf[2], pl[2];
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float p = none ? 0.f : exp2f(st[kt][i] - mn);
+      const half_t ph = (half_t)p;
+      psum += p;
+      pf[kt >> 1][(kt & 1) * 4 + i] = ph;
+      pl[kt >> 1][(kt & 1) * 4 + i] = (half_t)(p - (float)ph);
+    }
+  psum += __shfl_xor(psum, 16, kWave);
+  psum += __shfl_xor(psum, 32, kWave);
+  l = l * alpha + psum;
+  m = mn;
+  // rows 4 lg + i of the output tile take the factor of query 4 lg + i
+  float ar[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) ar[i] = __shfl(alpha, 4 * lg + i, kWave);
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) {
+    float4_t acc = o[dt];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] *= ar[i];
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pl[0], vf[0][dt], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pl[1], vf[1][dt], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[0], vf[0][dt], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[1], vf[1][dt], acc, 0, 0, 0);
+    o[dt] = acc;
+  }
+}
+
+// One workgroup per (slot, sequence bi, kv head g); slot s covers the `span`
+// consecutive chunks s * span .. s * span + span - 1, its tiles one per
+// wavefront (up to 4 wavefronts, which read the same cache fragments; with
+// more tiles, span 1 and each wavefront takes every 4th tile).  The slot's
+// (m, l, O) go to global partials that attn_merge_kernel merges in slot
+// order.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void attn_chunk_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int hq, int hkv,
+    int rps, int64_t capacity, const int32_t* __restrict__ pos_base, int pos_offset, int nslots, int span, int nq_pad,
+    float* __restrict__ part_o, float2* __restrict__ part_ml) {
   const int slot = blockIdx.x;
   const int bg = blockIdx.y;  // bi * hkv + g
   const int bi = bg / hkv, g = bg - bi * hkv;
-  const int G = hq / hkv, nq = rps * G;
+  const AttnTile a{hq, rps, hq / hkv, rps * (hq / hkv)};
   const int64_t p0 = (int64_t)pos_base[bi] + pos_offset;
   const int64_t pmax = p0 + rps - 1;
+  // slot0 < len_bound <= capacity, so the slot's first chunk lies in the cache
+  // whatever the positions: its loads are issued before the positions arrive
   const int64_t slot0 = (int64_t)slot * span * kChunk;
-  if (slot0 > pmax) return;  // no row reads this slot (uniform); rows at negative positions mask every key
   const int lane = threadIdx.x & 63, li = lane & 15, lg = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nwave = blockDim.x >> 6;
-  const half8_t zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
-  const int nqt = (nq + 15) >> 4;
-
-  auto load_q = [&](int qt, half8_t(&qf)[4]) {
-    const int qi = 16 * qt + li;
-    const bool qok = qi < nq;
-    const int j = qok ? qi / G : 0, gg = qok ? qi - (qi / G) * G : 0;
-    const half8_t* qp =
-        reinterpret_cast<const half8_t*>(q + (((int64_t)bi * rps + j) * hq + g * G + gg) * kHd + 32 * lg);
-#pragma unroll
-    for (int s = 0; s < 4; ++s) qf[s] = qok ? qp[s] : zero8;
-  };
-
+  const int nqt = (a.nq + 15) >> 4;
   half8_t kf[4][4], vf[2][8];
-  auto load_kv = [&](int64_t key0) {
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-      const int64_t key = key0 + 16 * kt + li;
-      const half8_t* kp = reinterpret_cast<const half8_t*>(kc + ((int64_t)bg * capacity + key) * kHd + 32 * lg);
-      const bool ok = key <= pmax;
-#pragma unroll
-      for (int s = 0; s < 4; ++s) kf[kt][s] = ok ? kp[s] : zero8;
-    }
-#pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2) {
-      const int64_t ka = key0 + 32 * t2 + 4 * lg, kb = ka + 16;
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) {
-        const uint16_t* vp = vc + ((int64_t)bg * kHd + 16 * dt + li) * capacity;
-        const half4_t a = *reinterpret_cast<const half4_t*>(vp + ka);
-        const half4_t b = *reinterpret_cast<const half4_t*>(vp + kb);
-        half8_t f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          f[e] = ka + e <= pmax ? a[e] : (half_t)0;
-          f[4 + e] = kb + e <= pmax ? b[e] : (half_t)0;
-        }
-        vf[t2][dt] = f;
-      }
-    }
-  };
-
-  const float sl2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
-  // one chunk (keys key0 .. key0 + 63) into tile qt's running (m, l, O)
-  auto update = [&](int qt, const half8_t(&qf)[4], int64_t key0, float& m, float& l, float4_t(&o)[8]) {
-    const int qi = 16 * qt + li;
-    const bool qok = qi < nq;
-    const int j = qok ? qi / G : 0;
-    float4_t st[4];
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-      float4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf[kt][s], qf[s], acc, 0, 0, 0);
-      st[kt] = acc;
-    }
-    const int64_t qpos = p0 + j;
-    float cm = -__builtin_inff();
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int64_t key = key0 + 16 * kt + 4 * lg + i;
-        const float v = (qok && key <= qpos) ? st[kt][i] * sl2 : -__builtin_inff();
-        st[kt][i] = v;
-        cm = fmaxf(cm, v);
-      }
-    cm = fmaxf(cm, __shfl_xor(cm, 16, kWave));
-    cm = fmaxf(cm, __shfl_xor(cm, 32, kWave));
-    const float mn = fmaxf(m, cm);
-    const bool none = mn == -__builtin_inff();  // no key of this row so far
-    const float alpha = none ? 1.f : exp2f(m - mn);
-    // p = hi + lo, both binary16 (hi = f16(p), lo = f16(p - hi), the difference
-    // exact in fp32): two products with the values carry p to about 2^-22
-    float psum = 0.f;
-    half8_t pf[2], pl[2];
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float p = none ? 0.f : exp2f(st[kt][i] - mn);
-        const half_t ph = (half_t)p;
-        psum += p;
-        pf[kt >> 1][(kt & 1) * 4 + i] = ph;
-        pl[kt >> 1][(kt & 1) * 4 + i] = (half_t)(p - (float)ph);
-      }
-    psum += __shfl_xor(psum, 16, kWave);
-    psum += __shfl_xor(psum, 32, kWave);
-    l = l * alpha + psum;
-    m = mn;
-    // rows 4 lg + i of the output tile take the factor of query 4 lg + i
-    float ar[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) ar[i] = __shfl(alpha, 4 * lg + i, kWave);
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-      float4_t acc = o[dt];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) acc[i] *= ar[i];
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pl[0], vf[0][dt], acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pl[1], vf[1][dt], acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[0], vf[0][dt], acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[1], vf[1][dt], acc, 0, 0, 0);
-      o[dt] = acc;
-    }
-  };
 
   float* po = part_o + ((int64_t)bg * nslots + slot) * nq_pad * kHd;
   float2* pml = part_ml + ((int64_t)bg * nslots + slot) * nq_pad;
@@ -321,29 +369,34 @@ __global__ __launch_bounds__(256) void attn_chunk_kernel(const uint16_t* __restr
 
   if (nqt <= nwave) {  // one query tile per wavefront, its running sums kept across the slot's chunks
     const int qt = wave;
+    half8_t qf[4];
+    attn_load_q(q, a, bi, g, qt, li, lg, qf);
+    attn_load_kv(kc, vc, bg, capacity, slot0, li, lg, kf, vf);
+    if (slot0 > pmax) return;  // no row reads this slot (uniform); rows at negative positions mask every key
     float m = -__builtin_inff(), l = 0.f;
     float4_t o[8];
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) o[dt] = float4_t{0.f, 0.f, 0.f, 0.f};
-    half8_t qf[4];
-    load_q(qt, qf);
     for (int t = 0; t < span; ++t) {
       const int64_t key0 = slot0 + (int64_t)t * kChunk;
       if (key0 > pmax) break;  // uniform
-      load_kv(key0);
-      update(qt, qf, key0, m, l, o);
+      if (t > 0) attn_load_kv(kc, vc, bg, capacity, key0, li, lg, kf, vf);
+      attn_mask_v(key0, pmax, lg, vf);
+      attn_update(a, p0, qt, li, lg, qf, kf, vf, key0, m, l, o);
     }
     store(qt, m, l, o);
   } else {  // more query tiles than wavefronts: span 1, tiles wave, wave + nwave, ...
-    load_kv(slot0);
+    attn_load_kv(kc, vc, bg, capacity, slot0, li, lg, kf, vf);
+    if (slot0 > pmax) return;
+    attn_mask_v(slot0, pmax, lg, vf);
     for (int qt = wave; qt < nqt; qt += nwave) {
       half8_t qf[4];
-      load_q(qt, qf);
+      attn_load_q(q, a, bi, g, qt, li, lg, qf);
       float m = -__builtin_inff(), l = 0.f;
       float4_t o[8];
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) o[dt] = float4_t{0.f, 0.f, 0.f, 0.f};
-      update(qt, qf, slot0, m, l, o);
+      attn_update(a, p0, qt, li, lg, qf, kf, vf, slot0, m, l, o);
       store(qt, m, l, o);
     }
   }
@@ -364,6 +417,13 @@ __global__ __launch_bounds__(64) void attn_merge_kernel(const float* __restrict_
   const int G = hq / hkv, g = hh / G, gg = hh - g * G;
   const int qi = j * G + gg;
   const int64_t pos = (int64_t)pos_base[bi] + pos_offset + j;
+  const int64_t bg = (int64_t)bi * hkv + g;
+  const float2* ml = part_ml + bg * nch * nq_pad + qi;
+  const float* po = part_o + (bg * nch * nq_pad + qi) * kHd + 2 * lane;
+  // the first 64 slots' (m, l) and the first slot's O before the position
+  // arrives (slots past the row's last one are ignored below)
+  const float2 ml0 = ml[(int64_t)(lane < nch ? lane : nch - 1) * nq_pad];
+  const float2 o0 = *reinterpret_cast<const float2*>(po);
   uint16_t* o = out + ((int64_t)r * hq + hh) * kHd + 2 * lane;
   if (pos < 0 || pos >= len_bound) {
     o[0] = kNanF16;
@@ -371,19 +431,22 @@ __global__ __launch_bounds__(64) void attn_merge_kernel(const float* __restrict_
     return;
   }
   const int last = (int)(pos / kChunk / span);  // the last slot holding a key of this row
-  const int64_t bg = (int64_t)bi * hkv + g;
-  const float2* ml = part_ml + bg * nch * nq_pad + qi;
-  const float* po = part_o + (bg * nch * nq_pad + qi) * kHd + 2 * lane;
-  float mx = -__builtin_inff();
-  for (int c = lane; c <= last; c += 64) mx = fmaxf(mx, ml[(int64_t)c * nq_pad].x);
+  float mx = lane <= last ? ml0.x : -__builtin_inff();
+  for (int c = lane + 64; c <= last; c += 64) mx = fmaxf(mx, ml[(int64_t)c * nq_pad].x);
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
   float l = 0.f, a0 = 0.f, a1 = 0.f;
+  if (last == 0) {  // one slot: O / l (what the sums below give with one slot)
+    const float l0 = __shfl(ml0.y, 0, kWave);
+    o[0] = f32_to_f16_bits(o0.x / l0);
+    o[1] = f32_to_f16_bits(o0.y / l0);
+    return;
+  }
   for (int c0 = 0; c0 <= last; c0 += 64) {
     const int c = c0 + lane;
     float wl = 0.f;
     if (c <= last) {
-      const float2 v = ml[(int64_t)c * nq_pad];
+      const float2 v = c0 == 0 ? ml0 : ml[(int64_t)c * nq_pad];
       wl = exp2f(v.x - mx);
       l += v.y * wl;
     }
