@@ -10,8 +10,8 @@
  *
  *   sq_quantize_int4_g128  FP16 parent -> INT4 group-128 draft copy (offline)
  *   sq_quantize_fp8_e4m3   FP16 parent -> FP8 E4M3 draft copy (offline)
- *   sq_qgemv_w4a16         draft projection y = x . W4'^T, m <= 8 rows
- *   sq_qgemv_w8a16         draft projection y = x . W8'^T, m <= 8 rows
+ *   sq_qgemv_w4a16         draft projection y = x . W4'^T, m <= 64 rows
+ *   sq_qgemv_w8a16         draft projection y = x . W8'^T, m <= 64 rows
  *   sq_verify_gemm_f16     parent verification y = x . W16^T, m <= 64 rows
  *   sq_spec_accept         LM-head softmax + accept / reject / resample
  *
@@ -66,7 +66,7 @@
 extern "C" {
 #endif
 
-#define SQ_ABI_VERSION 4
+#define SQ_ABI_VERSION 5
 
 typedef enum sq_status {
   SQ_OK = 0,
@@ -118,7 +118,9 @@ sq_status sq_quantize_fp8_e4m3(const uint16_t* w16, int64_t n, int64_t k, uint8_
 /* Draft projection with the INT4 parent (draft generation, SS III-D.2):
  *   y[i][r] = sum_c x[i][c] * (q[r][c] - z[r][c/128]) * s[r][c/128]
  * dequantized in registers; fp32 accumulation; y rounded once to y_dtype.
- * x [m][k] fp16, 1 <= m <= 8; k % 128 == 0, 128 <= k <= 2^20
+ * x [m][k] fp16, 1 <= m <= 64 (m <= 8: the draft GEMV; above, the matrix
+ * cores, for passes over many rows such as a prompt's); k % 128 == 0,
+ * 128 <= k <= 2^20
  * codes/scales/zeros as produced by sq_quantize_int4_g128 for an [n][k] matrix
  * y [m][n] of y_dtype (SQ_F16 or SQ_F32), 1 <= n <= 2^31 - 1. */
 sq_status sq_qgemv_w4a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t* codes,
@@ -127,7 +129,7 @@ sq_status sq_qgemv_w4a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t*
 
 /* Draft projection with the FP8 parent (draft generation, SS III-D.2):
  *   y[i][r] = s[r] * sum_c x[i][c] * decode(codes[r][c])
- * x [m][k] fp16, 1 <= m <= 8, k % 16 == 0, 16 <= k <= 2^20;
+ * x [m][k] fp16, 1 <= m <= 64, k % 16 == 0, 16 <= k <= 2^20;
  * codes [n][k] u8, scales [n] f32 as produced by sq_quantize_fp8_e4m3;
  * y [m][n] of y_dtype. */
 sq_status sq_qgemv_w8a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t* codes,

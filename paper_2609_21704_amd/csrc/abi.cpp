@@ -234,7 +234,7 @@ sq_status sq_quantize_fp8_e4m3(const uint16_t* w16, int64_t n, int64_t k, uint8_
 sq_status sq_qgemv_w4a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t* codes, const uint16_t* scales,
                          const uint16_t* zeros, int64_t n, void* y, sq_dtype y_dtype, hipStream_t stream) {
   if (!x || !codes || !scales || !zeros || !y) return SQ_ERR_NULL;
-  if (m < 1 || m > 8 || n < 1 || n > kMaxN || k < 128 || k > kMaxK || k % 128 != 0) return SQ_ERR_SHAPE;
+  if (m < 1 || m > 64 || n < 1 || n > kMaxN || k < 128 || k > kMaxK || k % 128 != 0) return SQ_ERR_SHAPE;
   if (y_dtype != SQ_F16 && y_dtype != SQ_F32) return SQ_ERR_UNSUPPORTED;
   const size_t ysz = y_dtype == SQ_F16 ? 2 : 4;
   if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 2) || !aligned(zeros, 2) || !aligned(y, ysz))
@@ -244,13 +244,16 @@ sq_status sq_qgemv_w4a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t*
   const Range ins[] = {{x, (size_t)m * k * 2}, {codes, nk / 2}, {scales, nk / 64}, {zeros, nk / 64}};
   if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
   (void)hipGetLastError();
+  // the GEMVs up to m = 8, the matrix-core kernel (activation tiles of 16 rows) beyond
+  if (m > 8)
+    return device_status(sq::launch_linear_w4(x, (int)m, k, codes, scales, zeros, n, y, y_dtype == SQ_F16, stream));
   return device_status(sq::launch_gemv_w4(x, (int)m, k, codes, scales, zeros, n, y, y_dtype == SQ_F16, stream));
 }
 
 sq_status sq_qgemv_w8a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t* codes, const float* scales,
                          int64_t n, void* y, sq_dtype y_dtype, hipStream_t stream) {
   if (!x || !codes || !scales || !y) return SQ_ERR_NULL;
-  if (m < 1 || m > 8 || n < 1 || n > kMaxN || k < 16 || k > kMaxK || k % 16 != 0) return SQ_ERR_SHAPE;
+  if (m < 1 || m > 64 || n < 1 || n > kMaxN || k < 16 || k > kMaxK || k % 16 != 0) return SQ_ERR_SHAPE;
   if (y_dtype != SQ_F16 && y_dtype != SQ_F32) return SQ_ERR_UNSUPPORTED;
   const size_t ysz = y_dtype == SQ_F16 ? 2 : 4;
   if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(y, ysz)) return SQ_ERR_ALIGN;
@@ -262,9 +265,11 @@ sq_status sq_qgemv_w8a16(const uint16_t* x, int64_t m, int64_t k, const uint8_t*
   // the matrix-core kernel from its size on at m >= 3, where its chunk
   // bookkeeping fits (it enqueues nothing when it returns hipErrorNotSupported);
   // at m <= 2 the GEMVs stream faster at every size (measured)
+  // (above m = 8 only the matrix-core kernel)
   hipError_t e = hipErrorNotSupported;
-  if (m >= 3 && n * k >= kLinearMinBytesW8)
+  if (m > 8 || (m >= 3 && n * k >= kLinearMinBytesW8))
     e = sq::launch_linear_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream);
+  if (m > 8) return device_status(e);
   if (e == hipErrorNotSupported) e = sq::launch_gemv_w8(x, (int)m, k, codes, scales, n, y, y_dtype == SQ_F16, stream);
   return device_status(e);
 }

@@ -1,7 +1,7 @@
 // Weight-streaming linear layers on the matrix cores: the draft projections
 // with the INT4 or FP8 parent (SpecQuant SS III-D.2) and the verification
 // pass with the FP16 parent (SS III-D.3),
-//   y[m][n] = sum_c x[m][c] * W'[n][c],   1 <= m <= 16 (FP16: m <= 64),
+//   y[m][n] = sum_c x[m][c] * W'[n][c],   1 <= m <= 64,
 // with W' the dequantized weight (INT4: (q - z) * s per 128-element group;
 // FP8: decode(c) * s per row; FP16: W itself).
 //
@@ -11,8 +11,8 @@
 // v_mfma_f32_16x16x32_f16 (lane l: B[8 j .. 8 j + 8)[l % 16]).  The
 // activations are the A operand, read from LDS in the same k order, and the
 // output tile D[m][n] accumulates in fp32 on the matrix cores; the m rows
-// are padded to MT 16-row tiles (MT = 1 for INT4 and FP8), each a matrix-core
-// product with the same weight fragment.
+// are padded to MT 16-row tiles, each a matrix-core product with the same
+// (dequantized) weight fragment.
 //   INT4: a 16-byte slab is one 128-element group of 16 rows (quarter j holds
 //     codes 32 j .. 32 j + 32); each 32-bit code word becomes 8 halves without
 //     a conversion instruction (a nibble masked into the mantissa of the
@@ -350,7 +350,8 @@ void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t ksl
           const half2_t z2 = __builtin_bit_cast(half2_t, zc[u] | (zc[u] << 16));
           const half2_t c1024 = z2 + half2_t{(half_t)1024.0f, (half_t)1024.0f};
           const half2_t c64 = z2 + half2_t{(half_t)64.0f, (half_t)64.0f};
-          float4_t gacc;
+          // every activation tile meets the same dequantized fragment
+          float4_t gacc[MT];
 #pragma unroll
           for (int wd = 0; wd < 4; ++wd) {
             const uint32_t qw = c[wd];
@@ -360,12 +361,17 @@ void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t ksl
             const half2_t d2 = __builtin_bit_cast(half2_t, (q8 & mlo) | k1024) - c1024;  // q2 - z, q6 - z
             const half2_t d3 = __builtin_bit_cast(half2_t, (q8 & mhi) | k64) - c64;      // q3 - z, q7 - z
             const half8_t bw = half8_t{d0[0], d0[1], d1[0], d1[1], d2[0], d2[1], d3[0], d3[1]};
-            const half8_t a = as_h8(*reinterpret_cast<const u32x4*>(xs + ((size_t)arow[0] * g.xs_stride + cell0 + wd) * 8));
-            gacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, wd == 0 ? float4_t{0.f, 0.f, 0.f, 0.f} : gacc, 0, 0,
-                                                          0);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+              const half8_t a =
+                  as_h8(*reinterpret_cast<const u32x4*>(xs + ((size_t)arow[mt] * g.xs_stride + cell0 + wd) * 8));
+              gacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, wd == 0 ? float4_t{0.f, 0.f, 0.f, 0.f} : gacc[mt],
+                                                                0, 0, 0);
+            }
           }
           const float s = valid ? f16_bits_to_f32((uint16_t)sc[u]) : 0.f;
-          acc[0] += s * gacc;
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) acc[mt] += s * gacc[mt];
         } else if constexpr (KIND == kW8) {
 #pragma unroll
           for (int wd = 0; wd < 2; ++wd) {
@@ -375,8 +381,12 @@ void linear_kernel(const uint16_t* __restrict__ x, int M, int64_t k, int64_t ksl
             const half2_t h2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w1, 1.0f, false);
             const half2_t h3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w1, 1.0f, true);
             const half8_t bw = half8_t{h0[0], h0[1], h1[0], h1[1], h2[0], h2[1], h3[0], h3[1]};
-            const half8_t a = as_h8(*reinterpret_cast<const u32x4*>(xs + ((size_t)arow[0] * g.xs_stride + cell0 + wd) * 8));
-            acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, acc[0], 0, 0, 0);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+              const half8_t a =
+                  as_h8(*reinterpret_cast<const u32x4*>(xs + ((size_t)arow[mt] * g.xs_stride + cell0 + wd) * 8));
+              acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bw, acc[mt], 0, 0, 0);
+            }
           }
         } else {
           const half8_t bw = as_h8(c);
@@ -606,22 +616,23 @@ template <int KIND>
 hipError_t linear_dispatch(const uint16_t* x, int m, int64_t k, const uint8_t* w, const uint16_t* scales16,
                            const uint16_t* zeros16, const float* scales32, int64_t n, void* y, bool f16_out,
                            hipStream_t stream) {
-  if (m < 1 || m > (KIND == kF16 ? 64 : 16)) return hipErrorInvalidValue;
+  if (m < 1 || m > 64) return hipErrorInvalidValue;
   // chunks of a task spread over the wavefronts where their partial sums fit
-  // in LDS, else whole tasks per wavefront (direct)
+  // in LDS, else whole tasks per wavefront (direct; its epilogue needs MT > 1)
   auto go = [&](auto mt_tag) {
     constexpr int MT = decltype(mt_tag)::value;
     hipError_t e = linear_launch<KIND, 8, MT>(x, m, k, w, scales16, zeros16, scales32, n, y, f16_out, false, stream);
-    if (e == hipErrorNotSupported && m > 16)
+    if (e == hipErrorNotSupported && MT > 1)
       e = linear_launch<KIND, 8, MT>(x, m, k, w, scales16, zeros16, scales32, n, y, f16_out, true, stream);
     return e;
   };
-  if constexpr (KIND == kF16) {
-    if (m > 48) return go(std::integral_constant<int, 4>{});
-    if (m > 32) return go(std::integral_constant<int, 3>{});
-    if (m > 16) return go(std::integral_constant<int, 2>{});
-  }
-  return go(std::integral_constant<int, 1>{});
+  if (m > 48) return go(std::integral_constant<int, 4>{});
+  if (m > 32) return go(std::integral_constant<int, 3>{});
+  if (m > 16) return go(std::integral_constant<int, 2>{});
+  const hipError_t e = go(std::integral_constant<int, 1>{});
+  // the quantized copies have no other kernel above m = 8: two tiles, the second one padding
+  if (e == hipErrorNotSupported && KIND != kF16 && m > 8) return go(std::integral_constant<int, 2>{});
+  return e;
 }
 
 }  // namespace

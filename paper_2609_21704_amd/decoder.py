@@ -148,8 +148,8 @@ class SpecDecoder:
         self.T = float(temperature)
         V = cfg.vocab
         L = weights.layers
-        if R * 2 > 8:
-            raise ValueError("draft step 0 runs 2 rows per chain; the draft GEMV takes at most 8")
+        if R * 2 > 64:
+            raise ValueError("draft step 0 runs 2 rows per chain; a pass takes at most 64 rows")
         if R * (k + 1) > 64:
             raise ValueError("the verification pass takes at most 64 rows")
         self.dcache = KVCache(cfg, L, R, capacity, dev)
@@ -196,8 +196,8 @@ class SpecDecoder:
         f32 out."""
         cfg, w, b = self.cfg, self.w, self.buf
         M = self.R * rps
-        if M > b.h.shape[0] or (draft and M > 8):
-            raise ValueError("a pass takes at most 64 rows (8 for the draft GEMVs)")
+        if M > b.h.shape[0]:
+            raise ValueError("a pass takes at most 64 rows")
         cache = self.dcache if draft else self.pcache
         lb = self.capacity if len_bound is None else len_bound
         h, x, qkv, q, a, y, gu, t = (b.h[:M], b.x[:M], b.qkv[:M], b.q[:M], b.a[:M], b.y[:M], b.gu[:M], b.t[:M])
@@ -254,8 +254,7 @@ class SpecDecoder:
         self.pos_base.zero_()
         V = self.cfg.vocab
         for draft in models:
-            limit = 8 if draft else 64
-            c = max(1, min(chunk or limit, limit // R))
+            c = max(1, min(chunk or 64, 64 // R))
             for s in range(0, Lp - 1, c):
                 n = min(c, Lp - 1 - s)
                 first = prompt[:, s].contiguous()

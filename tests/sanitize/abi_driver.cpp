@@ -49,7 +49,7 @@ int main() {
   EXPECT(sq_quantize_fp8_e4m3(at<uint16_t>(A), 4, 32, at<uint8_t>(B), at<float>(C + 2), nullptr, s), SQ_ERR_ALIGN);
   EXPECT(sq_quantize_fp8_e4m3(at<uint16_t>(A), 4, 32, at<uint8_t>(B), at<float>(C), nullptr, s), SQ_OK);
   // GEMVs and the verify GEMM
-  EXPECT(sq_qgemv_w4a16(at<uint16_t>(A), 9, 256, at<uint8_t>(B), at<uint16_t>(C), at<uint16_t>(D), 10, at<void>(E),
+  EXPECT(sq_qgemv_w4a16(at<uint16_t>(A), 65, 256, at<uint8_t>(B), at<uint16_t>(C), at<uint16_t>(D), 10, at<void>(E),
                         SQ_F32, s),
          SQ_ERR_SHAPE);
   EXPECT(sq_qgemv_w4a16(at<uint16_t>(A), 1, 256, at<uint8_t>(B), at<uint16_t>(C), at<uint16_t>(D), 10, at<void>(E),

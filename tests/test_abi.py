@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == set(sq.EXPORTED)
     for n in names:
         assert hasattr(lib, n), n
-    assert sq.sq_abi_version() == 4
+    assert sq.sq_abi_version() == 5
     for s in range(9):
         assert lib.sq_status_str(s).startswith(b"SQ_")
     assert lib.sq_status_str(9) == b"unknown sq_status"
@@ -63,7 +63,8 @@ def test_gemv_gemm_validation():
     lib = sq.load()
     w4, w8, gm = lib.sq_qgemv_w4a16, lib.sq_qgemv_w8a16, lib.sq_verify_gemm_f16
     assert w4(A, 1, 256, B, C, D, 10, None, F32, None) == NULL
-    assert w4(A, 9, 256, B, C, D, 10, E, F32, None) == SHAPE
+    assert w4(A, 65, 256, B, C, D, 10, E, F32, None) == SHAPE
+    assert w8(A, 65, 32, B, C, 10, E, F32, None) == SHAPE
     assert w4(A, 0, 256, B, C, D, 10, E, F32, None) == SHAPE
     assert w4(A, 1, 200, B, C, D, 10, E, F32, None) == SHAPE
     assert w4(A, 1, 256, B, C, D, 0, E, F32, None) == SHAPE

@@ -537,3 +537,37 @@ def test_qgemv_w8a16_large_parity(m, n, k):
         err = oracle.normalised_error(y.float().cpu().numpy(), y_ref, d_ref)
         assert err <= GEMV_TOL, (dt, err)
     assert torch.equal(sq.sq_qgemv_w8a16(xd, codes, scales), sq.sq_qgemv_w8a16(xd, codes, scales))
+
+
+# ------------------------------------------ draft projections over many rows
+# Above m = 8 the quantized copies run on the matrix cores (activation tiles
+# of 16 rows): one, two, three and four tiles; K cut into slices (k = 18944 at
+# m = 64); and a matrix with too many tiles per workgroup for the chunk
+# partial sums at m = 16, which takes whole tasks per wavefront instead.
+MANY_ROWS = [(9, 37, 384), (16, 896, 896), (17, 4864, 896), (33, 896, 4864), (48, 257, 3584), (64, 130, 3584),
+             (64, 1024, 18944), (16, 140000, 256), (12, 4608, 3584)]
+
+
+@pytest.mark.parametrize("m,n,k", MANY_ROWS)
+def test_qgemv_many_rows_parity(m, n, k):
+    w, x = _gemv_inputs(m, n, k, 16)
+    wd, xd = w.to(DEV), x.to(DEV)
+    codes, scales, zeros = sq.sq_quantize_int4_g128(wd)
+    c_ref, s_ref, z_ref = oracle.quantize_int4_g128(bits16(w))
+    y_ref, d_ref = oracle.qgemv_w4a16(bits16(x), c_ref, s_ref, z_ref)
+    c8, s8 = sq.sq_quantize_fp8_e4m3(wd)
+    c8_ref, s8_ref = oracle.quantize_fp8_e4m3(bits16(w))
+    y8_ref, d8_ref = oracle.qgemv_w8a16(bits16(x), c8_ref, s8_ref)
+    for dt in (torch.float32, torch.float16):
+        y = sq.sq_qgemv_w4a16(xd, codes, scales, zeros, y_dtype=dt)
+        err = oracle.normalised_error(y.float().cpu().numpy(), y_ref, d_ref)
+        assert err <= GEMV_TOL, ("int4", dt, err)
+        y8 = sq.sq_qgemv_w8a16(xd, c8, s8, y_dtype=dt)
+        err = oracle.normalised_error(y8.float().cpu().numpy(), y8_ref, d8_ref)
+        assert err <= GEMV_TOL, ("fp8", dt, err)
+    # deterministic, and each row of the block is the single-row product of its row
+    y1 = sq.sq_qgemv_w4a16(xd, codes, scales, zeros)
+    assert torch.equal(y1, sq.sq_qgemv_w4a16(xd, codes, scales, zeros))
+    row = sq.sq_qgemv_w4a16(xd[m - 1:m].contiguous(), codes, scales, zeros).cpu().numpy()[0]
+    err = oracle.normalised_error(row, y_ref[m - 1], d_ref[m - 1])
+    assert err <= GEMV_TOL
