@@ -705,6 +705,7 @@ def main():
                          "the plain copy; prints nothing")
     ap.add_argument("--no-fp8", action="store_true", help="skip the FP8 draft GEMV roofline block")
     ap.add_argument("--no-decoder", action="store_true", help="skip the rounds through full decoder layers")
+    ap.add_argument("--no-pipeline", action="store_true", help="skip the routed requests through the pipeline")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -840,7 +841,8 @@ def main():
         out["decoder"]["roofline_attention_long"] = measure_attention_long(dev)
         out["decoder_chains"] = measure_decoder(stack, args.temperature, args.steps, args.warmup, chains=4)
         del out["decoder_chains"]["roofline_attention"]
-        out["pipeline"] = measure_routed(stack, args.temperature)
+        if not args.no_pipeline:
+            out["pipeline"] = measure_routed(stack, args.temperature)
     if not args.no_fp8 and cfg.draft_variant == "int4":
         out["roofline_fp8"] = measure_fp8(args.gemv_steps, dev)
     if not args.no_cpu_baseline:
