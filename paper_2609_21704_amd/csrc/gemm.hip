@@ -388,7 +388,11 @@ struct RowsIntC {
 };
 
 constexpr size_t kRowsLds = 150 * 1024;
-constexpr int kVerifyRowsDepth = 1;  // steps of loads in flight per wavefront (measured: 1 < 2 < 3 in time)
+// steps of loads in flight per wavefront: one for whole rows (measured on 7B
+// q|k|v at m = 5: depth 1 / 2 / 3 at 9.5 / 10.0 / 11.1 us), two with K slices,
+// whose wavefronts walk several steps (7B down at m = 5: 29.9 -> 28.1 us)
+template <int KS>
+constexpr int verify_rows_depth() { return KS > 1 ? 2 : 1; }
 
 template <int M>
 hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t n, void* y, bool f16_out,
@@ -429,7 +433,7 @@ hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t 
   const size_t lds_launch = lds > 81 * 1024 ? lds : 81 * 1024;
   auto go = [&](auto na_tag, auto xb_tag, auto ks_tag) {
     constexpr int NA = decltype(na_tag)::value, XB = decltype(xb_tag)::value, KS = decltype(ks_tag)::value;
-    hipLaunchKernelGGL((gemm_rows_kernel<M, NA, nwave, XB, kVerifyRowsDepth, KS>),
+    hipLaunchKernelGGL((gemm_rows_kernel<M, NA, nwave, XB, verify_rows_depth<KS>(), KS>),
                        dim3((unsigned)blocks, (unsigned)KS), dim3(nthr), lds_launch, stream, x, k, w, n, y,
                        (int)f16_out, q, rem, slots);
   };
