@@ -264,11 +264,13 @@ __device__ __forceinline__ void attn_mask_v(int64_t key0, int64_t pmax, int lg, 
   }
 }
 
-// One chunk (keys key0 .. key0 + 63) into tile qt's running (m, l, O).
-__device__ __forceinline__ void attn_update(const AttnTile& a, int64_t p0, int qt, int li, int lg,
-                                            const half8_t (&qf)[4], const half8_t (&kf)[4][4],
-                                            const half8_t (&vf)[2][8], int64_t key0, float& m, float& l,
-                                            float4_t (&o)[8]) {
+// One chunk (keys key0 .. key0 + 63) into tile qt's running (m, l, O); the
+// key fragment (kt, s) and value fragment (t2, dt) come from kfrag / vfrag,
+// each called where the matrix cores take it.
+template <class KF, class VF>
+__device__ __forceinline__ void attn_update_src(const AttnTile& a, int64_t p0, int qt, int li, int lg,
+                                                const half8_t (&qf)[4], KF kfrag, VF vfrag, int64_t key0, float& m,
+                                                float& l, float4_t (&o)[8]) {
   const float sl2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e) / sqrt(128)
   const int qi = 16 * qt + li;
   const bool qok = qi < a.nq;
@@ -278,7 +280,7 @@ __device__ __forceinline__ void attn_update(const AttnTile& a, int64_t p0, int q
   for (int kt = 0; kt < 4; ++kt) {
     float4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf[kt][s], qf[s], acc, 0, 0, 0);
+    for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(kfrag(kt, s), qf[s], acc, 0, 0, 0);
     st[kt] = acc;
   }
   const int64_t qpos = p0 + j;
@@ -324,12 +326,22 @@ __device__ __forceinline__ void attn_update(const AttnTile& a, int64_t p0, int q
     float4_t acc = o[dt];
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[i] *= ar[i];
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pl[0], vf[0][dt], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pl[1], vf[1][dt], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[0], vf[0][dt], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[1], vf[1][dt], acc, 0, 0, 0);
+    const half8_t v0 = vfrag(0, dt), v1 = vfrag(1, dt);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pl[0], v0, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pl[1], v1, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[0], v0, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(pf[1], v1, acc, 0, 0, 0);
     o[dt] = acc;
   }
+}
+
+__device__ __forceinline__ void attn_update(const AttnTile& a, int64_t p0, int qt, int li, int lg,
+                                            const half8_t (&qf)[4], const half8_t (&kf)[4][4],
+                                            const half8_t (&vf)[2][8], int64_t key0, float& m, float& l,
+                                            float4_t (&o)[8]) {
+  attn_update_src(
+      a, p0, qt, li, lg, qf, [&](int kt, int s) { return kf[kt][s]; }, [&](int t2, int dt) { return vf[t2][dt]; },
+      key0, m, l, o);
 }
 
 // One workgroup per (slot, sequence bi, kv head g); slot s covers the `span`
@@ -379,7 +391,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     for (int dt = 0; dt < 8; ++dt) o[dt] = float4_t{0.f, 0.f, 0.f, 0.f};
     for (int t = 0; t < span; ++t) {
       const int64_t key0 = slot0 + (int64_t)t * kChunk;
-      if (key0 > pmax) break;  // uniform
+      if (key0 > pmax || key0 >= capacity) break;  // uniform; rows past the cache read none of it
       if (t > 0) attn_load_kv(kc, vc, bg, capacity, key0, li, lg, kf, vf);
       attn_mask_v(key0, pmax, lg, vf);
       attn_update(a, p0, qt, li, lg, qf, kf, vf, key0, m, l, o);
@@ -400,6 +412,120 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
       store(qt, m, l, o);
     }
   }
+}
+
+// The same slots with the chunks staged through LDS, for blocks of 2 .. 4
+// query tiles (whose wavefronts would otherwise each load the same key and
+// value fragments) and for slots of several chunks: the workgroup's four
+// wavefronts load each chunk once, as 16-byte cells of contiguous memory
+// (keys: 16 KB in a row; values: 128 rows of 128 B), into one of two LDS
+// buffers, while the wavefronts that own a query tile work on the previous
+// chunk from the other buffer; each reads its fragments from LDS.  Rows are
+// padded (keys to 272 B, values to 144 B), so that the lanes of one fragment
+// read fall in distinct banks.  One barrier per chunk: it follows the issue
+// of the next chunk's loads and waits only for the LDS writes.
+constexpr int kLdsKeyStride = 136;  // halves per key row in LDS (128 + 8)
+constexpr int kLdsValStride = 72;   // halves per value row in LDS (64 positions + 8)
+constexpr int kLdsChunk = 64 * kLdsKeyStride + kHd * kLdsValStride;  // halves per chunk buffer
+constexpr int kLdsThreads = 256;
+constexpr int kLdsCells = 2 * kChunk * kHd * 2 / 16 / kLdsThreads;  // 16-byte cells per thread and chunk: 8
+
+__global__ __launch_bounds__(kLdsThreads) __attribute__((amdgpu_waves_per_eu(2))) void attn_chunk_lds_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int hq, int hkv,
+    int rps, int64_t capacity, const int32_t* __restrict__ pos_base, int pos_offset, int nslots, int span, int nq_pad,
+    float* __restrict__ part_o, float2* __restrict__ part_ml) {
+  extern __shared__ __align__(16) char smem[];
+  half_t* lbuf = reinterpret_cast<half_t*>(smem);  // [2][kLdsChunk]
+  const int slot = blockIdx.x;
+  const int bg = blockIdx.y;  // bi * hkv + g
+  const int bi = bg / hkv, g = bg - bi * hkv;
+  const AttnTile a{hq, rps, hq / hkv, rps * (hq / hkv)};
+  const int tid = threadIdx.x, lane = tid & 63, li = lane & 15, lg = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nqt = (a.nq + 15) >> 4;
+  const int64_t slot0 = (int64_t)slot * span * kChunk;  // < len_bound <= capacity
+
+  // cells of chunk key0 for this thread: i < 4 keys (key c / 16, part c % 16),
+  // i >= 4 values (dim c' / 8, positions 8 (c' % 8) .. +8), c = tid + 256 i
+  u32x4 pre[kLdsCells];
+  auto load_chunk = [&](int64_t key0) {
+#pragma unroll
+    for (int i = 0; i < kLdsCells; ++i) {
+      const int c = tid + kLdsThreads * i;
+      if (i < kLdsCells / 2) {
+        pre[i] = *reinterpret_cast<const u32x4*>(kc + ((int64_t)bg * capacity + key0 + (c >> 4)) * kHd + (c & 15) * 8);
+      } else {
+        const int c2 = c - kChunk * kHd / 8;
+        pre[i] = *reinterpret_cast<const u32x4*>(vc + ((int64_t)bg * kHd + (c2 >> 3)) * capacity + key0 + (c2 & 7) * 8);
+      }
+    }
+  };
+  auto store_chunk = [&](half_t* b) {
+#pragma unroll
+    for (int i = 0; i < kLdsCells; ++i) {
+      const int c = tid + kLdsThreads * i;
+      if (i < kLdsCells / 2) {
+        *reinterpret_cast<u32x4*>(b + (c >> 4) * kLdsKeyStride + (c & 15) * 8) = pre[i];
+      } else {
+        const int c2 = c - kChunk * kHd / 8;
+        *reinterpret_cast<u32x4*>(b + 64 * kLdsKeyStride + (c2 >> 3) * kLdsValStride + (c2 & 7) * 8) = pre[i];
+      }
+    }
+  };
+
+  load_chunk(slot0);  // before the positions arrive: the slot's first chunk lies in the cache
+  const int64_t p0 = (int64_t)pos_base[bi] + pos_offset;
+  const int64_t pmax = p0 + rps - 1;
+  if (slot0 > pmax) return;  // uniform across the workgroup: no row reads this slot
+  const int64_t klast = pmax < capacity - 1 ? pmax : capacity - 1;  // rows past the cache read none of it
+  const int64_t nt64 = (klast - slot0) / kChunk + 1;
+  const int nt = nt64 < span ? (int)nt64 : span;  // chunks of the slot with a key at or before pmax
+  const bool owner = wave < nqt;
+  half8_t qf[4];
+  if (owner) attn_load_q(q, a, bi, g, wave, li, lg, qf);
+  store_chunk(lbuf);
+  float m = -__builtin_inff(), l = 0.f;
+  float4_t o[8];
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) o[dt] = float4_t{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < nt; ++t) {
+    const int64_t key0 = slot0 + (int64_t)t * kChunk;
+    if (t + 1 < nt) load_chunk(key0 + kChunk);
+    // the LDS writes of buffer t % 2 are done; the next chunk's loads stay in flight
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    const half_t* b = lbuf + (t & 1) * kLdsChunk;
+    if (owner) {
+      const bool tail = key0 + kChunk - 1 > pmax;  // values of keys after pmax are zeroed (stale entries)
+      auto kfrag = [&](int kt, int s4) {
+        return *reinterpret_cast<const half8_t*>(b + (16 * kt + li) * kLdsKeyStride + 32 * lg + 8 * s4);
+      };
+      auto vfrag = [&](int t2, int dt) {
+        const int ka = 32 * t2 + 4 * lg, kb = ka + 16;
+        const half_t* vr = b + 64 * kLdsKeyStride + (16 * dt + li) * kLdsValStride;
+        const half4_t va = *reinterpret_cast<const half4_t*>(vr + ka);
+        const half4_t vb = *reinterpret_cast<const half4_t*>(vr + kb);
+        half8_t f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          f[e] = (!tail || key0 + ka + e <= pmax) ? va[e] : (half_t)0;
+          f[4 + e] = (!tail || key0 + kb + e <= pmax) ? vb[e] : (half_t)0;
+        }
+        return f;
+      };
+      attn_update_src(a, p0, wave, li, lg, qf, kfrag, vfrag, key0, m, l, o);
+    }
+    // buffer (t + 1) % 2 was last read before this chunk's barrier
+    if (t + 1 < nt) store_chunk(lbuf + ((t + 1) & 1) * kLdsChunk);
+  }
+  if (!owner) return;
+  float* po = part_o + ((int64_t)bg * nslots + slot) * nq_pad * kHd;
+  float2* pml = part_ml + ((int64_t)bg * nslots + slot) * nq_pad;
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) po[(int64_t)(16 * wave + 4 * lg + i) * kHd + 16 * dt + li] = o[dt][i];
+  if (lg == 0) pml[16 * wave + li] = make_float2(m, l);
 }
 
 // One wavefront per (row, query head): the slots 0 .. pos / (64 span), in
@@ -660,9 +786,17 @@ hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_
   float* part_o = static_cast<float*>(ws);
   float2* part_ml = reinterpret_cast<float2*>(part_o + (size_t)b * hkv * nslots * nq_pad * kHd);
   const int nqt = nq_pad / 16;
-  const int waves = nqt < 4 ? nqt : 4;  // one query tile per wavefront (16 rows each), at most 4
-  hipLaunchKernelGGL(attn_chunk_kernel, dim3((unsigned)nslots, (unsigned)(b * hkv)), dim3(64 * waves), 0, stream, q, kc,
-                     vc, hq, hkv, rps, capacity, pos_base, pos_offset, nslots, span, nq_pad, part_o, part_ml);
+  if ((nqt >= 2 && nqt <= 4) || (nqt == 1 && span >= 2)) {
+    // chunks through LDS: loaded once for the block's tiles, the next one in flight
+    const size_t lds = (size_t)2 * kLdsChunk * sizeof(uint16_t);
+    hipLaunchKernelGGL(attn_chunk_lds_kernel, dim3((unsigned)nslots, (unsigned)(b * hkv)), dim3(kLdsThreads), lds,
+                       stream, q, kc, vc, hq, hkv, rps, capacity, pos_base, pos_offset, nslots, span, nq_pad, part_o,
+                       part_ml);
+  } else {
+    const int waves = nqt < 4 ? nqt : 4;  // one query tile per wavefront (16 rows each), at most 4
+    hipLaunchKernelGGL(attn_chunk_kernel, dim3((unsigned)nslots, (unsigned)(b * hkv)), dim3(64 * waves), 0, stream, q,
+                       kc, vc, hq, hkv, rps, capacity, pos_base, pos_offset, nslots, span, nq_pad, part_o, part_ml);
+  }
   hipLaunchKernelGGL(attn_merge_kernel, dim3((unsigned)(b * rps), (unsigned)hq), dim3(64), 0, stream, part_o,
                      part_ml, hq, hkv, rps, nslots, span, nq_pad, pos_base, pos_offset, len_bound, out);
   return hipGetLastError();
