@@ -24,6 +24,11 @@
  *   sq_rope_kv_f16         q|k|v bias + rotary embedding + cache write
  *   sq_attention_f16       causal grouped-query attention over the cache
  *   sq_silu_mul_f16        SiLU-gated product of the gate|up projection
+ *   sq_qgemv_w4a16_rmsnorm, sq_verify_gemm_f16_rmsnorm
+ *                          a projection of RMS-normalised rows of h (the norm
+ *                          inside the projection's activation staging)
+ *   sq_qgemv_w4a16_acc, sq_verify_gemm_f16_acc
+ *                          a projection added into the residual stream
  *   sq_spec_commit         emitted tokens and restart position of a round
  *
  * and several draft chains per sequence (multi-candidate drafting, SS III-D.2):
@@ -66,7 +71,7 @@
 extern "C" {
 #endif
 
-#define SQ_ABI_VERSION 5
+#define SQ_ABI_VERSION 6
 
 typedef enum sq_status {
   SQ_OK = 0,
@@ -290,6 +295,35 @@ sq_status sq_attention_f16(const uint16_t* q, const uint16_t* k_cache, const uin
                            int32_t rows_per_seq, int32_t hq, int32_t hkv, const int32_t* pos_base,
                            int32_t pos_offset, int64_t len_bound, int64_t capacity, uint16_t* out,
                            hipStream_t stream);
+
+/* The projections of a decoder layer with the residual add and the RMS
+ * normalisation folded in (one launch instead of two at every norm):
+ *
+ * sq_qgemv_w4a16_rmsnorm / sq_verify_gemm_f16_rmsnorm: sq_qgemv_w4a16 /
+ * sq_verify_gemm_f16 of x = the rows sq_add_rmsnorm_f16(h, w = norm_w, eps,
+ * group, delta = NULL) would write, bit for bit the same x and y: row r of x
+ * is h row r * group + group - 1 ([m * group][k] f32, 16-B aligned), normalised
+ * with the same fp32 sum of squares, fp64 reciprocal root and fp32 products,
+ * inside the projection's activation staging.  k <= 4096; m <= 2 (INT4) or
+ * m <= 8 (FP16, matrices of the row-block kernel: 2 n k >= 4 MiB and
+ * n <= 32768).  Other shapes return SQ_ERR_UNSUPPORTED and enqueue nothing.
+ *
+ * sq_qgemv_w4a16_acc / sq_verify_gemm_f16_acc: y[i][r] += the projection
+ * (y [m][n] f32 in/out; one fp32 add per value, as sq_add_rmsnorm_f16 adds
+ * delta), for the output and down projections that feed the residual
+ * stream.  m <= 8 (INT4) or the FP16 row-block shapes above; one K slice for
+ * INT4 (k * m * 2 <= 64 KiB); other shapes return SQ_ERR_UNSUPPORTED.
+ * Other arguments and limits as the plain calls. */
+sq_status sq_qgemv_w4a16_rmsnorm(const float* h, int32_t group, const uint16_t* norm_w, float eps, int64_t m,
+                                 int64_t k, const uint8_t* codes, const uint16_t* scales, const uint16_t* zeros,
+                                 int64_t n, void* y, sq_dtype y_dtype, hipStream_t stream);
+sq_status sq_verify_gemm_f16_rmsnorm(const float* h, int32_t group, const uint16_t* norm_w, float eps, int64_t m,
+                                     int64_t k, const uint16_t* w16, int64_t n, void* y, sq_dtype y_dtype,
+                                     hipStream_t stream);
+sq_status sq_qgemv_w4a16_acc(const uint16_t* x, int64_t m, int64_t k, const uint8_t* codes, const uint16_t* scales,
+                             const uint16_t* zeros, int64_t n, float* y, hipStream_t stream);
+sq_status sq_verify_gemm_f16_acc(const uint16_t* x, int64_t m, int64_t k, const uint16_t* w16, int64_t n, float* y,
+                                 hipStream_t stream);
 
 /* SiLU-gated product of the fused gate|up projection output:
  *   t[i][c] = f16(g / (1 + exp(-g)) * u),  g = gu[i][c], u = gu[i][inter + c]  (fp32).

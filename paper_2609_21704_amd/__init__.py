@@ -20,6 +20,8 @@ from ._lib import (  # noqa: F401
     sq_embed_block_f16,
     sq_kv_adopt_f16,
     sq_qgemv_w4a16,
+    sq_qgemv_w4a16_acc,
+    sq_qgemv_w4a16_rmsnorm,
     sq_qgemv_w8a16,
     sq_quantize_fp8_e4m3,
     sq_quantize_int4_g128,
@@ -32,4 +34,6 @@ from ._lib import (  # noqa: F401
     sq_spec_commit,
     sq_spec_commit_multi,
     sq_verify_gemm_f16,
+    sq_verify_gemm_f16_acc,
+    sq_verify_gemm_f16_rmsnorm,
 )

@@ -59,6 +59,10 @@ def load() -> ctypes.CDLL:
             "sq_rope_kv_f16": ([P, P, I32, I32, I32, I32, P, I32, I64, I64, ctypes.c_double, P, P, P, P, P], S),
             "sq_attention_f16": ([P, P, P, I32, I32, I32, I32, P, I32, I64, I64, P, P], S),
             "sq_silu_mul_f16": ([P, I64, I64, P, P], S),
+            "sq_qgemv_w4a16_rmsnorm": ([P, I32, P, F, I64, I64, P, P, P, I64, P, S, P], S),
+            "sq_verify_gemm_f16_rmsnorm": ([P, I32, P, F, I64, I64, P, I64, P, S, P], S),
+            "sq_qgemv_w4a16_acc": ([P, I64, I64, P, P, P, I64, P, P], S),
+            "sq_verify_gemm_f16_acc": ([P, I64, I64, P, I64, P, P], S),
             "sq_spec_commit": ([P, P, P, I32, I32, P, P, P, P, I64, P, P, P], S),
             "sq_spec_accept_multi": ([P, P, P, P, I32, I32, I32, I32, F, P, P, P, P, P, P], S),
             "sq_kv_adopt_f16": ([P, P, I32, I32, I32, I32, I64, P, P, P, I32, I32, P], S),
@@ -76,7 +80,8 @@ EXPORTED = ("sq_abi_version", "sq_status_str", "sq_quantize_int4_g128", "sq_quan
             "sq_qgemv_w4a16", "sq_qgemv_w8a16", "sq_verify_gemm_f16", "sq_spec_accept",
             "sq_spec_accept_noalloc", "sq_probe_stream_read", "sq_embed_block_f16", "sq_add_rmsnorm_f16",
             "sq_rope_kv_f16", "sq_attention_f16", "sq_silu_mul_f16", "sq_spec_commit", "sq_spec_accept_multi",
-            "sq_kv_adopt_f16", "sq_spec_commit_multi")
+            "sq_kv_adopt_f16", "sq_spec_commit_multi", "sq_qgemv_w4a16_rmsnorm", "sq_verify_gemm_f16_rmsnorm",
+            "sq_qgemv_w4a16_acc", "sq_verify_gemm_f16_acc")
 
 # device status bits (SQ_DEV_* of include/specquant.h)
 DEV_BAD_TOKEN, DEV_BAD_POS, DEV_OVERFLOW, DEV_NO_DIST = 1, 2, 4, 8
@@ -180,6 +185,81 @@ def sq_qgemv_w4a16(x, codes, scales, zeros, y=None, y_dtype=torch.float32):
     _check(load().sq_qgemv_w4a16(_ptr(x), m, k, _ptr(codes), _ptr(scales), _ptr(zeros), n, _ptr(y),
                                  _dtype_code(y.dtype), _stream(x.device)), "sq_qgemv_w4a16")
     return y
+
+
+SQ_ERR_UNSUPPORTED = 6
+
+
+def _fused(status: int, fn: str) -> bool:
+    """True when the fused call ran; False when its shape has no fused form (nothing enqueued)."""
+    if status == SQ_ERR_UNSUPPORTED:
+        return False
+    _check(status, fn)
+    return True
+
+
+def _norm_src(h, norm_w, group: int):
+    if h.dtype != torch.float32 or h.dim() != 2 or h.shape[0] % group:
+        raise ValueError("h must be float32 [m * group][k]")
+    _expect(norm_w, torch.float16, (h.shape[1],), "norm_w")
+    return h.shape[0] // group, h.shape[1]
+
+
+def sq_qgemv_w4a16_rmsnorm(h, norm_w, eps: float, codes, scales, zeros, group: int = 1, y=None,
+                           y_dtype=torch.float32) -> bool:
+    """y = x . W4'^T with x the rows sq_add_rmsnorm_f16(h, norm_w, eps, group) writes, normalised inside the
+    projection; False (nothing enqueued) where the projection's kernel has no such form."""
+    m, k = _norm_src(h, norm_w, group)
+    n = codes.shape[0]
+    _dev(h, norm_w, codes, scales, zeros, y)
+    _expect(codes, torch.uint8, (n, k // 2), "codes")
+    _expect(scales, torch.float16, (n, k // 128), "scales")
+    _expect(zeros, torch.float16, (n, k // 128), "zeros")
+    if y.numel() != m * n:
+        raise ValueError("y must hold m * n elements")
+    return _fused(load().sq_qgemv_w4a16_rmsnorm(_ptr(h), int(group), _ptr(norm_w), float(eps), m, k, _ptr(codes),
+                                                _ptr(scales), _ptr(zeros), n, _ptr(y), _dtype_code(y.dtype),
+                                                _stream(h.device)), "sq_qgemv_w4a16_rmsnorm")
+
+
+def sq_verify_gemm_f16_rmsnorm(h, norm_w, eps: float, w16, group: int = 1, y=None) -> bool:
+    """y = x . W16^T with x the rows sq_add_rmsnorm_f16(h, norm_w, eps, group) writes, normalised inside the
+    projection; False (nothing enqueued) where the projection's kernel has no such form."""
+    m, k = _norm_src(h, norm_w, group)
+    n = w16.shape[0]
+    _dev(h, norm_w, w16, y)
+    _expect(w16, torch.float16, (n, k), "w16")
+    if y.numel() != m * n:
+        raise ValueError("y must hold m * n elements")
+    return _fused(load().sq_verify_gemm_f16_rmsnorm(_ptr(h), int(group), _ptr(norm_w), float(eps), m, k, _ptr(w16),
+                                                    n, _ptr(y), _dtype_code(y.dtype), _stream(h.device)),
+                  "sq_verify_gemm_f16_rmsnorm")
+
+
+def sq_qgemv_w4a16_acc(x, codes, scales, zeros, y) -> bool:
+    """y += x . W4'^T (y float32); False (nothing enqueued) where the projection's kernel has no such form."""
+    m, k = x.shape
+    n = codes.shape[0]
+    if x.dtype != torch.float16 or y.dtype != torch.float32 or y.numel() != m * n:
+        raise ValueError("x must be float16 [m][k] and y float32 with m * n elements")
+    _dev(x, codes, scales, zeros, y)
+    _expect(codes, torch.uint8, (n, k // 2), "codes")
+    _expect(scales, torch.float16, (n, k // 128), "scales")
+    _expect(zeros, torch.float16, (n, k // 128), "zeros")
+    return _fused(load().sq_qgemv_w4a16_acc(_ptr(x), m, k, _ptr(codes), _ptr(scales), _ptr(zeros), n, _ptr(y),
+                                            _stream(x.device)), "sq_qgemv_w4a16_acc")
+
+
+def sq_verify_gemm_f16_acc(x, w16, y) -> bool:
+    """y += x . W16^T (y float32); False (nothing enqueued) where the projection's kernel has no such form."""
+    m, k = x.shape
+    n = w16.shape[0]
+    if x.dtype != torch.float16 or y.dtype != torch.float32 or y.numel() != m * n:
+        raise ValueError("x must be float16 [m][k] and y float32 with m * n elements")
+    _dev(x, w16, y)
+    _expect(w16, torch.float16, (n, k), "w16")
+    return _fused(load().sq_verify_gemm_f16_acc(_ptr(x), m, k, _ptr(w16), n, _ptr(y), _stream(x.device)),
+                  "sq_verify_gemm_f16_acc")
 
 
 def sq_qgemv_w8a16(x, codes, scales, y=None, y_dtype=torch.float32):

@@ -165,6 +165,12 @@ inline sq_status device_status(hipError_t e) {
   return SQ_ERR_DEVICE;
 }
 
+// The fused projections: a kernel without the fused form returns
+// hipErrorNotSupported before it enqueues anything.
+inline sq_status fused_status(hipError_t e) {
+  return e == hipErrorNotSupported ? SQ_ERR_UNSUPPORTED : device_status(e);
+}
+
 constexpr int64_t kMaxK = int64_t(1) << 20;
 constexpr int64_t kMaxN = 0x7FFFFFFF;
 constexpr int64_t kMaxHidden = 16384;
@@ -177,6 +183,16 @@ sq_status check_block(int32_t b, int32_t rows_per_seq, int32_t hq, int32_t hkv, 
   if (capacity < 64 || capacity > kMaxN || capacity % 64 != 0 || len_bound < 1 || len_bound > capacity)
     return SQ_ERR_SHAPE;
   if ((int64_t)b * rows_per_seq > kMaxN || (int64_t)b * hkv > 65535) return SQ_ERR_SHAPE;
+  return SQ_OK;
+}
+
+// Shared checks of a normalised input (h rows m * group + group - 1, norm weights).
+sq_status check_norm_src(const float* h, int32_t group, const uint16_t* norm_w, float eps, int64_t m, int64_t k) {
+  if (!h || !norm_w) return SQ_ERR_NULL;
+  if (group < 1 || m * group > kMaxN || k > kMaxHidden) return SQ_ERR_SHAPE;
+  if (!isfinite(eps)) return SQ_ERR_NONFINITE;
+  if (eps < 0.f) return SQ_ERR_SHAPE;
+  if (!aligned(h, 16) || !aligned(norm_w, 16)) return SQ_ERR_ALIGN;
   return SQ_OK;
 }
 
@@ -298,6 +314,77 @@ sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint
     e = sq::launch_linear_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream);
   if (e == hipErrorNotSupported) e = sq::launch_gemm_f16(x, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream);
   return device_status(e);
+}
+
+sq_status sq_qgemv_w4a16_rmsnorm(const float* h, int32_t group, const uint16_t* norm_w, float eps, int64_t m,
+                                 int64_t k, const uint8_t* codes, const uint16_t* scales, const uint16_t* zeros,
+                                 int64_t n, void* y, sq_dtype y_dtype, hipStream_t stream) {
+  if (!codes || !scales || !zeros || !y) return SQ_ERR_NULL;
+  if (m < 1 || m > 64 || n < 1 || n > kMaxN || k < 128 || k > kMaxK || k % 128 != 0) return SQ_ERR_SHAPE;
+  const sq_status ns = check_norm_src(h, group, norm_w, eps, m, k);
+  if (ns != SQ_OK) return ns;
+  if (y_dtype != SQ_F16 && y_dtype != SQ_F32) return SQ_ERR_UNSUPPORTED;
+  const size_t ysz = y_dtype == SQ_F16 ? 2 : 4;
+  if (!aligned(codes, 16) || !aligned(scales, 2) || !aligned(zeros, 2) || !aligned(y, ysz)) return SQ_ERR_ALIGN;
+  const size_t nk = (size_t)n * (size_t)k;
+  const Range outs[] = {{y, (size_t)m * n * ysz}};
+  const Range ins[] = {{h, (size_t)m * group * k * 4}, {norm_w, (size_t)k * 2}, {codes, nk / 2}, {scales, nk / 64},
+                       {zeros, nk / 64}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  if (m > 8) return SQ_ERR_UNSUPPORTED;
+  const sq::NormSrc nrm{h, norm_w, eps, group};
+  return fused_status(sq::launch_gemv_w4(nullptr, (int)m, k, codes, scales, zeros, n, y, y_dtype == SQ_F16, stream,
+                                         &nrm, false));
+}
+
+sq_status sq_qgemv_w4a16_acc(const uint16_t* x, int64_t m, int64_t k, const uint8_t* codes, const uint16_t* scales,
+                             const uint16_t* zeros, int64_t n, float* y, hipStream_t stream) {
+  if (!x || !codes || !scales || !zeros || !y) return SQ_ERR_NULL;
+  if (m < 1 || m > 64 || n < 1 || n > kMaxN || k < 128 || k > kMaxK || k % 128 != 0) return SQ_ERR_SHAPE;
+  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 2) || !aligned(zeros, 2) || !aligned(y, 4))
+    return SQ_ERR_ALIGN;
+  const size_t nk = (size_t)n * (size_t)k;
+  const Range outs[] = {{y, (size_t)m * n * 4}};
+  const Range ins[] = {{x, (size_t)m * k * 2}, {codes, nk / 2}, {scales, nk / 64}, {zeros, nk / 64}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  if (m > 8) return SQ_ERR_UNSUPPORTED;
+  return fused_status(sq::launch_gemv_w4(x, (int)m, k, codes, scales, zeros, n, y, false, stream, nullptr, true));
+}
+
+sq_status sq_verify_gemm_f16_rmsnorm(const float* h, int32_t group, const uint16_t* norm_w, float eps, int64_t m,
+                                     int64_t k, const uint16_t* w16, int64_t n, void* y, sq_dtype y_dtype,
+                                     hipStream_t stream) {
+  if (!w16 || !y) return SQ_ERR_NULL;
+  if (m < 1 || m > 64 || n < 1 || n > kMaxN || k < 8 || k > kMaxK || k % 8 != 0) return SQ_ERR_SHAPE;
+  const sq_status ns = check_norm_src(h, group, norm_w, eps, m, k);
+  if (ns != SQ_OK) return ns;
+  if (y_dtype != SQ_F16 && y_dtype != SQ_F32) return SQ_ERR_UNSUPPORTED;
+  const size_t ysz = y_dtype == SQ_F16 ? 2 : 4;
+  if (!aligned(w16, 16) || !aligned(y, ysz)) return SQ_ERR_ALIGN;
+  const Range outs[] = {{y, (size_t)m * n * ysz}};
+  const Range ins[] = {{h, (size_t)m * group * k * 4}, {norm_w, (size_t)k * 2}, {w16, (size_t)n * k * 2}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  // the row blocks, where sq_verify_gemm_f16 takes them
+  if (!(m <= 8 && n * k * 2 >= kRowsMinBytesF16 && n <= kRowsMaxRowsF16)) return SQ_ERR_UNSUPPORTED;
+  const sq::NormSrc nrm{h, norm_w, eps, group};
+  return fused_status(
+      sq::launch_gemm_rows_f16(nullptr, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream, &nrm, false));
+}
+
+sq_status sq_verify_gemm_f16_acc(const uint16_t* x, int64_t m, int64_t k, const uint16_t* w16, int64_t n, float* y,
+                                 hipStream_t stream) {
+  if (!x || !w16 || !y) return SQ_ERR_NULL;
+  if (m < 1 || m > 64 || n < 1 || n > kMaxN || k < 8 || k > kMaxK || k % 8 != 0) return SQ_ERR_SHAPE;
+  if (!aligned(x, 16) || !aligned(w16, 16) || !aligned(y, 4)) return SQ_ERR_ALIGN;
+  const Range outs[] = {{y, (size_t)m * n * 4}};
+  const Range ins[] = {{x, (size_t)m * k * 2}, {w16, (size_t)n * k * 2}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  (void)hipGetLastError();
+  if (!(m <= 8 && n * k * 2 >= kRowsMinBytesF16 && n <= kRowsMaxRowsF16)) return SQ_ERR_UNSUPPORTED;
+  return fused_status(sq::launch_gemm_rows_f16(x, (int)m, k, w16, n, y, false, stream, nullptr, true));
 }
 
 sq_status sq_probe_stream_read(const void* src, int64_t bytes, uint32_t* sink, hipStream_t stream) {

@@ -69,7 +69,8 @@ __global__ __launch_bounds__(256) void embed_kernel(const uint16_t* __restrict__
 // Every global load (the row of h, of delta and the norm weights) is issued
 // before the first use, so the kernel waits for memory once.  Every row gets
 // the residual add; the rows r * group + group - 1 are normalised into output
-// row r.
+// row r (the arithmetic of rms_cell_sq / rms_inverse / rms_scale, shared with
+// the projections that normalise their own input: the same bits).
 template <int NV>
 __global__ __launch_bounds__(256) void add_rmsnorm_kernel(float* __restrict__ h, const float* __restrict__ delta,
                                                           int hidden, const uint16_t* __restrict__ w, float eps,
@@ -102,12 +103,14 @@ __global__ __launch_bounds__(256) void add_rmsnorm_kernel(float* __restrict__ h,
   if (!out_row) return;  // uniform across the workgroup
   float ss = 0.f;
 #pragma unroll
-  for (int i = 0; i < NV; ++i) ss += (v[i][0] * v[i][0] + v[i][1] * v[i][1]) + (v[i][2] * v[i][2] + v[i][3] * v[i][3]);
+  for (int i = 0; i < NV; ++i) {
+    const int c = (int)threadIdx.x + 256 * i;
+    if (c < n4) ss += rms_cell_sq(v[i]);
+  }
   ss = wave_sum(ss);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
-  const float total = (red[0] + red[1]) + (red[2] + red[3]);
-  const float r = (float)(1.0 / sqrt((double)total / (double)hidden + (double)eps));
+  const float r = rms_inverse(red, hidden, eps);
   uint16_t* xr = x + (row / group) * hidden;
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
@@ -116,7 +119,7 @@ __global__ __launch_bounds__(256) void add_rmsnorm_kernel(float* __restrict__ h,
       const half4_t wh = __builtin_bit_cast(half4_t, wv[i]);
       half4_t o;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) o[e] = (half_t)(v[i][e] * r * (float)wh[e]);
+      for (int e = 0; e < 4; ++e) o[e] = rms_scale(v[i][e], r, wh[e]);
       reinterpret_cast<uint2*>(xr)[c] = __builtin_bit_cast(uint2, o);
     }
   }

@@ -161,13 +161,17 @@ hipError_t gemm_mt(const uint16_t* x, int m, int64_t k, const uint16_t* w, int64
 // in a 64-bit slot by atomic exchange (the value travels inside the atomic, so
 // no fence is needed): the second to arrive adds slice 0's + slice 1's in that
 // order, stores the result and empties the slot for the next launch.
-template <int M, int NA, int NWV, int XB, int D, int KS>
+// Output modes: y fp32, y fp16, or y fp32 added to.
+enum : int { kOutF32 = 0, kOutF16 = 1, kOutAcc = 2 };
+
+template <int M, int NA, int NWV, int XB, int D, int KS, bool NRM>
 __global__ __launch_bounds__(1024) void gemm_rows_kernel(const uint16_t* __restrict__ x, int64_t k,
                                                         const uint16_t* __restrict__ w, int64_t n,
-                                                        void* __restrict__ y, int f16_out, int64_t rows_q,
-                                                        int rows_rem, unsigned long long* __restrict__ slots) {
+                                                        void* __restrict__ y, int out_mode, int64_t rows_q,
+                                                        int rows_rem, unsigned long long* __restrict__ slots,
+                                                        NormSrc nr) {
   // every argument in one batch of scalar loads, before the first address needs one
-  asm volatile("" ::"s"(x), "s"(k), "s"(w), "s"(n), "s"(y), "s"(f16_out), "s"(rows_q), "s"(rows_rem), "s"(slots));
+  asm volatile("" ::"s"(x), "s"(k), "s"(w), "s"(n), "s"(y), "s"(out_mode), "s"(rows_q), "s"(rows_rem), "s"(slots));
   extern __shared__ __align__(16) char smem[];
   constexpr int nwave = NWV, nthr = 64 * NWV;
   const int b = blockIdx.x;
@@ -186,7 +190,9 @@ __global__ __launch_bounds__(1024) void gemm_rows_kernel(const uint16_t* __restr
   const int ps = ps0 < P ? ps0 : P, pe0 = ps0 + 64 * (sb + (wave < sx ? 1 : 0)), pe = pe0 < P ? pe0 : P;
   const int nsteps = (pe - ps + 63) >> 6;
   half_t* xs = reinterpret_cast<half_t*>(smem);
-  float* red = reinterpret_cast<float*>(smem + (size_t)M * 2 * ppr * 16);  // [nwave][M][nrows]
+  // NRM: the rows' wavefront sums of squares [M][4] after the activations, then the row sums
+  float* wsum = reinterpret_cast<float*>(smem + (size_t)M * 2 * ppr * 16);
+  float* red = reinterpret_cast<float*>(smem + (size_t)M * 2 * ppr * 16 + (NRM ? 128 : 0));  // [nwave][M][nrows]
   const uint16_t* bw = w + r0 * k + k0;
   const float rppr = 1.0f / (float)ppr;
 
@@ -221,9 +227,14 @@ __global__ __launch_bounds__(1024) void gemm_rows_kernel(const uint16_t* __restr
     return f;
   };
 
-  // activations first (XB cells per thread cover all of x), then the first step
+  // activations first (XB cells per thread cover all of x), then the first step;
+  // NRM: the rows' sums of squares first, then the cells' h and norm weights
   const int xtotal = M * 2 * ppr;
+  RmsRows<2> rr;  // NRM: M <= 8 rows over the four groups of 256 threads
+  if constexpr (NRM) rr.load(nr.h + (int64_t)(nr.group - 1) * k, (int64_t)nr.group * k, M, (int)k);
   u32x4 xv[XB];
+  float4_t xh[NRM ? XB : 1][2];
+  u32x4 xw[NRM ? XB : 1];
 #pragma unroll
   for (int i = 0; i < XB; ++i) {
     int idx = i * nthr + (int)threadIdx.x;
@@ -235,11 +246,42 @@ __global__ __launch_bounds__(1024) void gemm_rows_kernel(const uint16_t* __restr
         c -= 2 * ppr;
         m = mm;
       }
-    xv[i] = *reinterpret_cast<const u32x4*>(x + (int64_t)m * k + k0 + 8 * c);
+    if constexpr (NRM) {
+      const float* hr = nr.h + ((int64_t)m * nr.group + nr.group - 1) * k + k0 + 8 * c;
+      xh[i][0] = *reinterpret_cast<const float4_t*>(hr);
+      xh[i][1] = *reinterpret_cast<const float4_t*>(hr + 4);
+      xw[i] = *reinterpret_cast<const u32x4*>(nr.w + k0 + 8 * c);
+    } else {
+      xv[i] = *reinterpret_cast<const u32x4*>(x + (int64_t)m * k + k0 + 8 * c);
+    }
   }
   Piece ring[D];
 #pragma unroll
   for (int j = 0; j < D; ++j) ring[j] = load(j);
+  if constexpr (NRM) {
+    rr.finish(M, (int)k, wsum);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    float r[M];
+#pragma unroll
+    for (int m = 0; m < M; ++m) r[m] = rms_inverse(wsum + 4 * m, (int)k, nr.eps);
+#pragma unroll
+    for (int i = 0; i < XB; ++i) {
+      int idx = i * nthr + (int)threadIdx.x;
+      idx = idx < xtotal ? idx : xtotal - 1;
+      int m = 0, c = idx;
+#pragma unroll
+      for (int mm = 1; mm < M; ++mm)
+        if (c >= 2 * ppr) {
+          c -= 2 * ppr;
+          m = mm;
+        }
+      float rm = r[0];
+#pragma unroll
+      for (int mm = 1; mm < M; ++mm) rm = m == mm ? r[mm] : rm;
+      xv[i] = rms_cell(xh[i][0], xh[i][1], xw[i], rm);
+    }
+  }
 #pragma unroll
   for (int i = 0; i < XB; ++i) {
     const int idx = i * nthr + (int)threadIdx.x;
@@ -255,6 +297,18 @@ __global__ __launch_bounds__(1024) void gemm_rows_kernel(const uint16_t* __restr
     }
   }
   for (int i = (int)threadIdx.x; i < nwave * M * nrows; i += nthr) red[i] = 0.f;
+  // an accumulated output: this thread's first value read now, its latency under the walk
+  float yold = 0.f;
+  if (out_mode == kOutAcc && (int)threadIdx.x < M * nrows) {
+    int m = 0, row = (int)threadIdx.x;
+#pragma unroll
+    for (int mm = 1; mm < M; ++mm)
+      if (row >= nrows) {
+        row -= nrows;
+        m = mm;
+      }
+    yold = reinterpret_cast<const float*>(y)[(int64_t)m * n + r0 + row];
+  }
   // LDS writes done, then the barrier: no wait for the weight loads in flight
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   __builtin_amdgcn_s_barrier();
@@ -375,8 +429,10 @@ __global__ __launch_bounds__(1024) void gemm_rows_kernel(const uint16_t* __restr
       v = slice == 0 ? v + ov : ov + v;
       atomicExch(slots + o, 0ull);  // empty for the next launch
     }
-    if (f16_out)
+    if (out_mode == kOutF16)
       reinterpret_cast<uint16_t*>(y)[o] = f32_to_f16_bits(v);
+    else if (out_mode == kOutAcc)
+      reinterpret_cast<float*>(y)[o] = (t == (int)threadIdx.x ? yold : reinterpret_cast<const float*>(y)[o]) + v;
     else
       reinterpret_cast<float*>(y)[o] = v;
   }
@@ -395,9 +451,11 @@ template <int KS>
 constexpr int verify_rows_depth() { return KS > 1 ? 2 : 1; }
 
 template <int M>
-hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t n, void* y, bool f16_out,
-                       hipStream_t stream) {
+hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t n, void* y, int out_mode,
+                       const NormSrc* nrm, hipStream_t stream) {
   if (k < 512 || k % 16 != 0) return hipErrorNotSupported;  // whole 16-weight pieces per row
+  if (nrm && k > 4096) return hipErrorNotSupported;          // normalised rows of at most 4096 values
+  const NormSrc nr = nrm ? *nrm : NormSrc{nullptr, nullptr, 0.f, 1};
   constexpr int nwave = 16, nthr = 64 * nwave;
   // one K slice where the activations and row slots fit, else two (k % 32 == 0),
   // with half as many row blocks so that the workgroups still fill the CUs once
@@ -407,7 +465,7 @@ hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t 
     const int64_t rows_max = (n + blocks - 1) / blocks;
     const int64_t ppr = k / ks / 16;
     const int64_t xcells = (int64_t)M * 2 * ppr;
-    lds = (size_t)xcells * 16 + (size_t)nwave * M * rows_max * sizeof(float);
+    lds = (size_t)xcells * 16 + (nrm ? 128 : 0) + (size_t)nwave * M * rows_max * sizeof(float);
     const int64_t pmax = ks > 1 ? (int64_t(1) << 24) : (int64_t(1) << 27);
     return k % (16 * ks) == 0 && ppr >= 32 && lds <= kRowsLds && rows_max * ppr < pmax && xcells <= 8 * nthr;
   };
@@ -419,6 +477,8 @@ hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t 
     if (!fits(2, blocks, lds)) return hipErrorNotSupported;
   }
   const int64_t ppr = k / ks / 16, xcells = (int64_t)M * 2 * ppr;
+  // normalised rows: one K slice, at most four cells per thread
+  if (nrm && (ks != 1 || xcells > 4 * nthr)) return hipErrorNotSupported;
   unsigned long long* slots = nullptr;
   if (ks > 1) {  // one 64-bit meeting slot per output value
     int32_t* c = nullptr;
@@ -433,9 +493,17 @@ hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t 
   const size_t lds_launch = lds > 81 * 1024 ? lds : 81 * 1024;
   auto go = [&](auto na_tag, auto xb_tag, auto ks_tag) {
     constexpr int NA = decltype(na_tag)::value, XB = decltype(xb_tag)::value, KS = decltype(ks_tag)::value;
-    hipLaunchKernelGGL((gemm_rows_kernel<M, NA, nwave, XB, verify_rows_depth<KS>(), KS>),
-                       dim3((unsigned)blocks, (unsigned)KS), dim3(nthr), lds_launch, stream, x, k, w, n, y,
-                       (int)f16_out, q, rem, slots);
+    if constexpr (KS == 1 && XB <= 4) {
+      if (nrm) {
+        hipLaunchKernelGGL((gemm_rows_kernel<M, NA, nwave, XB, verify_rows_depth<KS>(), KS, true>),
+                           dim3((unsigned)blocks, (unsigned)KS), dim3(nthr), lds_launch, stream, x, k, w, n, y,
+                           out_mode, q, rem, slots, nr);
+        return;
+      }
+    }
+    hipLaunchKernelGGL((gemm_rows_kernel<M, NA, nwave, XB, verify_rows_depth<KS>(), KS, false>),
+                       dim3((unsigned)blocks, (unsigned)KS), dim3(nthr), lds_launch, stream, x, k, w, n, y, out_mode,
+                       q, rem, slots, nr);
   };
   using C1 = RowsIntC<1>;
   using C2 = RowsIntC<2>;
@@ -465,16 +533,17 @@ hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t 
 }  // namespace
 
 hipError_t launch_gemm_rows_f16(const uint16_t* x, int m, int64_t k, const uint16_t* w, int64_t n, void* y,
-                                bool f16_out, hipStream_t stream) {
+                                bool f16_out, hipStream_t stream, const NormSrc* nrm, bool accum) {
+  const int mode = accum ? kOutAcc : (f16_out ? kOutF16 : kOutF32);
   switch (m) {
-    case 1: return gemm_rows_m<1>(x, k, w, n, y, f16_out, stream);
-    case 2: return gemm_rows_m<2>(x, k, w, n, y, f16_out, stream);
-    case 3: return gemm_rows_m<3>(x, k, w, n, y, f16_out, stream);
-    case 4: return gemm_rows_m<4>(x, k, w, n, y, f16_out, stream);
-    case 5: return gemm_rows_m<5>(x, k, w, n, y, f16_out, stream);
-    case 6: return gemm_rows_m<6>(x, k, w, n, y, f16_out, stream);
-    case 7: return gemm_rows_m<7>(x, k, w, n, y, f16_out, stream);
-    case 8: return gemm_rows_m<8>(x, k, w, n, y, f16_out, stream);
+    case 1: return gemm_rows_m<1>(x, k, w, n, y, mode, nrm, stream);
+    case 2: return gemm_rows_m<2>(x, k, w, n, y, mode, nrm, stream);
+    case 3: return gemm_rows_m<3>(x, k, w, n, y, mode, nrm, stream);
+    case 4: return gemm_rows_m<4>(x, k, w, n, y, mode, nrm, stream);
+    case 5: return gemm_rows_m<5>(x, k, w, n, y, mode, nrm, stream);
+    case 6: return gemm_rows_m<6>(x, k, w, n, y, mode, nrm, stream);
+    case 7: return gemm_rows_m<7>(x, k, w, n, y, mode, nrm, stream);
+    case 8: return gemm_rows_m<8>(x, k, w, n, y, mode, nrm, stream);
     default: return hipErrorNotSupported;
   }
 }

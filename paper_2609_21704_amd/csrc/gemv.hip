@@ -128,41 +128,85 @@ __device__ __forceinline__ Frag<R> load_frag(const TaskPtr& t, int row_bytes, in
 // halves of word w in the order x[8w+0], x[8w+4], x[8w+1], x[8w+5], x[8w+2],
 // x[8w+6], x[8w+3], x[8w+7] -- the nibble pairs of a code word.
 // FP8 layout: xs [M][4 cells][nchunk][8 halves] in natural order.
+// halves (x0,x1),(x2,x3),(x4,x5),(x6,x7) -> (x0,x4),(x1,x5),(x2,x6),(x3,x7):
+// the nibble pairs of an INT4 code word
+__device__ __forceinline__ u32x4 pair_order(u32x4 raw) {
+  u32x4 out;
+  out[0] = __builtin_amdgcn_perm(raw[2], raw[0], 0x05040100u);
+  out[1] = __builtin_amdgcn_perm(raw[2], raw[0], 0x07060302u);
+  out[2] = __builtin_amdgcn_perm(raw[3], raw[1], 0x05040100u);
+  out[3] = __builtin_amdgcn_perm(raw[3], raw[1], 0x07060302u);
+  return out;
+}
+
 template <int M, bool W8>
 __device__ __forceinline__ u32x4 x_cell(const uint16_t* __restrict__ x, int64_t k, int64_t k0, int64_t kl, int c,
                                         int m, int w) {
   const int64_t kk = (int64_t)c * (W8 ? 32 : 64) + 8 * w;
   const u32x4 raw = kk < kl ? *reinterpret_cast<const u32x4*>(x + (int64_t)m * k + k0 + kk) : u32x4{0u, 0u, 0u, 0u};
-  u32x4 out = raw;
-  if constexpr (!W8) {
-    // halves (x0,x1),(x2,x3),(x4,x5),(x6,x7) -> (x0,x4),(x1,x5),(x2,x6),(x3,x7)
-    out[0] = __builtin_amdgcn_perm(raw[2], raw[0], 0x05040100u);
-    out[1] = __builtin_amdgcn_perm(raw[2], raw[0], 0x07060302u);
-    out[2] = __builtin_amdgcn_perm(raw[3], raw[1], 0x05040100u);
-    out[3] = __builtin_amdgcn_perm(raw[3], raw[1], 0x07060302u);
-  }
-  return out;
+  return W8 ? raw : pair_order(raw);
+}
+
+// The same cell from a normalised row (INT4 order): h and norm weights of
+// row m at k index kk = 64 c + 8 w, converted by rms_cell once r is known.
+struct NormCell {
+  float4_t h0, h1;
+  u32x4 w;
+};
+
+__device__ __forceinline__ NormCell norm_cell_load(const NormSrc& nr, int64_t k, int c, int m, int w) {
+  const int64_t kk = (int64_t)c * 64 + 8 * w;
+  const float* hr = nr.h + ((int64_t)m * nr.group + nr.group - 1) * k + kk;
+  NormCell f;
+  f.h0 = *reinterpret_cast<const float4_t*>(hr);
+  f.h1 = *reinterpret_cast<const float4_t*>(hr + 4);
+  f.w = *reinterpret_cast<const u32x4*>(nr.w + kk);
+  return f;
 }
 
 // Activations staged in LDS by the whole workgroup.  The loads of the first
 // batch (B cells per thread, all of x for up to B * blockDim.x cells) are
 // issued before the weight prefetch, so that they do not queue behind it in
 // HBM; their stores follow once the weight loads are in flight.
-template <int M, bool W8>
+// NRM (INT4, one K slice, 256 threads): the cells come from normalised rows;
+// load() fetches their h and norm weights, convert() forms them once the
+// rows' 1 / rms are known (2 M cells per thread cover K <= 4096).
+template <int M, bool W8, bool NRM = false>
 struct XStage {
   static constexpr int kCells = W8 ? 4 : 8;  // 16-byte cells of x per chunk and row
-  static constexpr int B = M <= 4 ? 8 : 2;   // fewer held cells where the activation fragments need registers
+  // fewer held cells where the activation fragments need registers
+  static constexpr int B = NRM ? 2 * M : (M <= 4 ? 8 : 2);
   u32x4 v[B];
+  NormCell nc[NRM ? B : 1];
 
   __device__ __forceinline__ void load(const uint16_t* __restrict__ x, int64_t k, int64_t k0, int64_t kl, int nchunk,
-                                       int base) {
+                                       int base, const NormSrc& nr) {
     const int total = nchunk * M * kCells, nthreads = (int)blockDim.x;
 #pragma unroll
     for (int i = 0; i < B; ++i) {
       int idx = base + i * nthreads + (int)threadIdx.x;
       idx = idx < total ? idx : total - 1;
       const int c = idx / (M * kCells), rem = idx % (M * kCells);
-      v[i] = x_cell<M, W8>(x, k, k0, kl, c, rem / kCells, rem % kCells);
+      if constexpr (NRM)
+        nc[i] = norm_cell_load(nr, k, c, rem / kCells, rem % kCells);
+      else
+        v[i] = x_cell<M, W8>(x, k, k0, kl, c, rem / kCells, rem % kCells);
+    }
+  }
+
+  __device__ __forceinline__ void convert(int nchunk, int base, const float (&r)[M]) {
+    if constexpr (NRM) {
+      const int total = nchunk * M * kCells, nthreads = (int)blockDim.x;
+#pragma unroll
+      for (int i = 0; i < B; ++i) {
+        int idx = base + i * nthreads + (int)threadIdx.x;
+        idx = idx < total ? idx : total - 1;
+        const int m = (idx % (M * kCells)) / kCells;
+        float rm = r[0];
+#pragma unroll
+        for (int mm = 1; mm < M; ++mm) rm = m == mm ? r[mm] : rm;
+        v[i] = pair_order(rms_cell(nc[i].h0, nc[i].h1, nc[i].w, rm));
+      }
     }
   }
 
@@ -179,18 +223,30 @@ struct XStage {
   }
 };
 
-template <int M, bool W8, int R, bool MULTI, bool XR>
+// Output modes of the projection kernels: y fp32, y fp16, or y fp32 added to.
+enum : int { kOutF32 = 0, kOutF16 = 1, kOutAcc = 2 };
+
+__device__ __forceinline__ void store_mode(void* y, int64_t idx, float v, int out_mode) {
+  if (out_mode == kOutF16)
+    reinterpret_cast<uint16_t*>(y)[idx] = f32_to_f16_bits(v);
+  else if (out_mode == kOutAcc)
+    reinterpret_cast<float*>(y)[idx] += v;
+  else
+    reinterpret_cast<float*>(y)[idx] = v;
+}
+
+template <int M, bool W8, int R, bool MULTI, bool XR, bool NRM>
 __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__ x, int64_t k, int64_t kslice,
                                                        const uint8_t* __restrict__ codes,
                                                        const uint16_t* __restrict__ scales16,
                                                        const uint16_t* __restrict__ zeros16,
                                                        const float* __restrict__ scales32, int64_t n,
-                                                       void* __restrict__ y, int f16_out,
-                                                       float* __restrict__ partial, int nw_team) {
+                                                       void* __restrict__ y, int out_mode,
+                                                       float* __restrict__ partial, int nw_team, NormSrc nr) {
   extern __shared__ __align__(16) char smem[];
   // every argument in one batch of scalar loads, before the first address needs one
   asm volatile("" ::"s"(x), "s"(k), "s"(kslice), "s"(codes), "s"(scales16), "s"(zeros16), "s"(scales32), "s"(n),
-               "s"(y), "s"(f16_out), "s"(partial), "s"(nw_team));
+               "s"(y), "s"(out_mode), "s"(partial), "s"(nw_team));
   constexpr int kCells = W8 ? 4 : 8;
   constexpr int kChunkK = W8 ? 32 : 64;  // weights per 32-byte lane chunk
   const int split = blockIdx.y;
@@ -219,15 +275,30 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
 
   // activations first, then the first fragment, so that x is not queued
   // behind the weight stream
-  XStage<M, W8> xst;
-  xst.load(x, k, k0, kl, nchunk, 0);
+  // NRM: the rows' sums of squares are loaded first, then the cells' h and
+  // norm weights; 1 / rms meets in LDS (after the activation cells) before the
+  // cells are formed
+  RmsRows<NRM ? M : 1> rr;
+  if constexpr (NRM) rr.load(nr.h + (int64_t)(nr.group - 1) * k, (int64_t)nr.group * k, M, (int)k);
+  XStage<M, W8, NRM> xst;
+  xst.load(x, k, k0, kl, nchunk, 0, nr);
   Frag<R> fa, fb;
   TaskPtr tp = task_ptr<W8, R>(codes, scales16, zeros16, n, k, k0, task < ntask ? task : ntask - 1);
   fa = load_frag<W8, R>(tp, row_bytes, groups, kl, nchunk, it, lane);
+  if constexpr (NRM) {
+    float* wsum = reinterpret_cast<float*>(smem + (size_t)M * kCells * nchunk * 16);  // [M][4]
+    rr.finish(M, (int)k, wsum);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    float r[M];
+#pragma unroll
+    for (int m = 0; m < M; ++m) r[m] = rms_inverse(wsum + 4 * m, (int)k, nr.eps);
+    xst.convert(nchunk, 0, r);
+  }
   xst.store(nchunk, 0, xs);
-  const int xtotal = nchunk * M * kCells, xbatch = XStage<M, W8>::B * (int)blockDim.x;
-  for (int base = xbatch; base < xtotal; base += xbatch) {  // activations beyond the first batch
-    xst.load(x, k, k0, kl, nchunk, base);
+  const int xtotal = nchunk * M * kCells, xbatch = XStage<M, W8, NRM>::B * (int)blockDim.x;
+  for (int base = xbatch; !NRM && base < xtotal; base += xbatch) {  // activations beyond the first batch
+    xst.load(x, k, k0, kl, nchunk, base, nr);
     xst.store(nchunk, base, xs);
   }
   __syncthreads();
@@ -387,10 +458,8 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
         if constexpr (W8) val *= scales32[row];
         if (partial)
           partial[((int64_t)split * M + m) * n + row] = val;
-        else if (f16_out)
-          reinterpret_cast<uint16_t*>(y)[(int64_t)m * n + row] = f32_to_f16_bits(val);
         else
-          reinterpret_cast<float*>(y)[(int64_t)m * n + row] = val;
+          store_mode(y, (int64_t)m * n + row, val, out_mode);
       };
       if constexpr (!MULTI) {
         if (lead) {
@@ -458,18 +527,18 @@ struct PieceFrag {
   uint32_t z;  // group zero bits (INT4)
 };
 
-template <int M, bool W8, int D, int XB, int NA, int NWV>
+template <int M, bool W8, int D, int XB, int NA, int NWV, bool NRM>
 __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restrict__ x, int64_t k,
                                                         const uint8_t* __restrict__ codes,
                                                         const uint16_t* __restrict__ scales16,
                                                         const uint16_t* __restrict__ zeros16,
                                                         const float* __restrict__ scales32, int64_t n,
-                                                        void* __restrict__ y, int f16_out, int64_t rows_q,
-                                                        int rows_rem) {
+                                                        void* __restrict__ y, int out_mode, int64_t rows_q,
+                                                        int rows_rem, NormSrc nr) {
   extern __shared__ __align__(16) char smem[];
   // every argument in one batch of scalar loads, before the first address needs one
   asm volatile("" ::"s"(x), "s"(k), "s"(codes), "s"(scales16), "s"(zeros16), "s"(scales32), "s"(n), "s"(y),
-               "s"(f16_out), "s"(rows_q), "s"(rows_rem));
+               "s"(out_mode), "s"(rows_q), "s"(rows_rem));
   constexpr int kCPC = W8 ? 4 : 8;  // activation cells (8 halves) per chunk of a piece
   constexpr int kPad = kCPC + 1;    // LDS cells per chunk: the cells and one pad
   constexpr int nwave = NWV;        // wavefronts per workgroup, a power of two
@@ -489,7 +558,9 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
   const int ps = ps0 < P ? ps0 : P, pe0 = ps0 + 64 * (sb + (wave < sx ? 1 : 0)), pe = pe0 < P ? pe0 : P;
   const int nsteps = (pe - ps + 63) >> 6;
   half_t* xs = reinterpret_cast<half_t*>(smem);
-  float* red = reinterpret_cast<float*>(smem + (size_t)M * ppr * kPad * 16);  // [nwave][M][nrows]
+  // NRM: the rows' wavefront sums of squares [M][4] after the activations, then the row sums
+  float* wsum = reinterpret_cast<float*>(smem + (size_t)M * ppr * kPad * 16);
+  float* red = reinterpret_cast<float*>(smem + (size_t)M * ppr * kPad * 16 + (NRM ? 64 : 0));  // [nwave][M][nrows]
   const uint8_t* bcodes = codes + r0 * (W8 ? k : (k >> 1));
   const uint16_t* bscales = W8 ? nullptr : scales16 + r0 * (k >> 7);
   const uint16_t* bzeros = W8 ? nullptr : zeros16 + r0 * (k >> 7);
@@ -530,6 +601,7 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
         ++m;
       }
   };
+  NormCell xn[NRM ? XB : 1];
   auto xload = [&](int base) {
 #pragma unroll
     for (int b = 0; b < XB; ++b) {
@@ -537,7 +609,10 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
       idx = idx < xtotal ? idx : xtotal - 1;
       int m, rem;
       xsplit(idx, m, rem);
-      xv[b] = x_cell<M, W8>(x, k, 0, k, rem / kCPC, m, rem % kCPC);
+      if constexpr (NRM)
+        xn[b] = norm_cell_load(nr, k, rem / kCPC, m, rem % kCPC);
+      else
+        xv[b] = x_cell<M, W8>(x, k, 0, k, rem / kCPC, m, rem % kCPC);
     }
   };
   auto xstore = [&](int base) {
@@ -551,12 +626,45 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
       }
     }
   };
+  RmsRows<1> rr;  // NRM: M <= 2 rows over groups of 256 threads (512 or 1024)
+  if constexpr (NRM) rr.load(nr.h + (int64_t)(nr.group - 1) * k, (int64_t)nr.group * k, M, (int)k);
   xload(0);
   PieceFrag ring[D];
 #pragma unroll
   for (int j = 0; j < D; ++j) ring[j] = load(j);
+  if constexpr (NRM) {
+    rr.finish(M, (int)k, wsum);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    float r[M];
+#pragma unroll
+    for (int m = 0; m < M; ++m) r[m] = rms_inverse(wsum + 4 * m, (int)k, nr.eps);
+#pragma unroll
+    for (int b = 0; b < XB; ++b) {
+      int idx = b * nthr + (int)threadIdx.x;
+      idx = idx < xtotal ? idx : xtotal - 1;
+      int m, rem;
+      xsplit(idx, m, rem);
+      float rm = r[0];
+#pragma unroll
+      for (int mm = 1; mm < M; ++mm) rm = m == mm ? r[mm] : rm;
+      xv[b] = pair_order(rms_cell(xn[b].h0, xn[b].h1, xn[b].w, rm));
+    }
+  }
   xstore(0);
   for (int i = (int)threadIdx.x; i < M * nrows * nwave; i += nthr) red[i] = 0.f;
+  // an accumulated output: this thread's first value read now, its latency under the walk
+  float yold = 0.f;
+  if (out_mode == kOutAcc && (int)threadIdx.x < M * nrows) {
+    int m = 0, row = (int)threadIdx.x;
+#pragma unroll
+    for (int i = 1; i < M; ++i)
+      if (row >= nrows) {
+        row -= nrows;
+        ++m;
+      }
+    yold = reinterpret_cast<const float*>(y)[(int64_t)m * n + r0 + row];
+  }
   // LDS writes done, then the barrier: no wait for the code loads in flight
   // (a full __syncthreads would wait for every outstanding global load)
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -710,10 +818,10 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
     for (int w = 0; w < nwave; ++w) v += red[w * M * nrows + t];  // consecutive threads, consecutive words
     if constexpr (W8) v *= scales32[r0 + row];
     const int64_t o = (int64_t)m * n + r0 + row;
-    if (f16_out)
-      reinterpret_cast<uint16_t*>(y)[o] = f32_to_f16_bits(v);
+    if (out_mode == kOutAcc && t == (int)threadIdx.x)  // the value read at the start
+      reinterpret_cast<float*>(y)[o] = yold + v;
     else
-      reinterpret_cast<float*>(y)[o] = v;
+      store_mode(y, o, v, out_mode);
   }
 }
 
@@ -727,10 +835,10 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   }
 }
 
-template <int M, bool W8, int R, bool MULTI, bool XR>
+template <int M, bool W8, int R, bool MULTI, bool XR, bool NRM>
 hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits, const uint8_t* codes,
                        const uint16_t* scales16, const uint16_t* zeros16, const float* scales32, int64_t n, void* y,
-                       bool f16_out, float* partial, int nw, hipStream_t stream) {
+                       int out_mode, float* partial, int nw, const NormSrc& nr, hipStream_t stream) {
   constexpr int64_t chunk_k = W8 ? 32 : 64;
   const int64_t kfirst = kslice < k ? kslice : k;
   const int64_t nchunk = (kfirst + chunk_k - 1) / chunk_k;
@@ -750,10 +858,13 @@ hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits,
   if (T > tmax) T = tmax;
   if (T < 1) T = 1;
   const int64_t blocks = (teams + T - 1) / T;
-  const size_t lds = (size_t)M * 2 * (size_t)(nchunk * chunk_k) + (MULTI ? (size_t)T * nw * R * M * 4 : 0);
+  // normalised rows: one K slice staged by 256 threads, 2 M cells each
+  if (NRM && (splits != 1 || T * nw != 4 || nchunk > 64)) return hipErrorNotSupported;
+  const size_t lds = (size_t)M * 2 * (size_t)(nchunk * chunk_k) + (MULTI ? (size_t)T * nw * R * M * 4 : 0) +
+                     (NRM ? (size_t)M * 4 * sizeof(float) : 0);
   const dim3 grid((unsigned)blocks, (unsigned)splits);
-  hipLaunchKernelGGL((gemv_kernel<M, W8, R, MULTI, XR>), grid, dim3((unsigned)(T * nw * 64)), lds, stream, x, k, kslice,
-                     codes, scales16, zeros16, scales32, n, y, (int)f16_out, partial, nw);
+  hipLaunchKernelGGL((gemv_kernel<M, W8, R, MULTI, XR, NRM>), grid, dim3((unsigned)(T * nw * 64)), lds, stream, x, k,
+                     kslice, codes, scales16, zeros16, scales32, n, y, out_mode, partial, nw, nr);
   return hipGetLastError();
 }
 
@@ -765,12 +876,13 @@ constexpr size_t kRowsLdsMax = 150 * 1024;
 // per CU (fewer workgroups than rows never), rows split evenly over the
 // workgroups.  Returns hipErrorNotSupported when the shape is outside what it
 // takes.
-template <int M, bool W8>
+template <int M, bool W8, bool NRM>
 hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint16_t* scales16,
-                       const uint16_t* zeros16, const float* scales32, int64_t n, void* y, bool f16_out,
-                       hipStream_t stream) {
-  // whole pieces per row: 32 FP8 codes, or 64 INT4 codes (k % 128 == 0 already)
-  if (M > (W8 ? 4 : 2) || k < kRowsMinK || (W8 && k % 32 != 0))
+                       const uint16_t* zeros16, const float* scales32, int64_t n, void* y, int out_mode,
+                       const NormSrc& nr, hipStream_t stream) {
+  // whole pieces per row: 32 FP8 codes, or 64 INT4 codes (k % 128 == 0 already);
+  // normalised rows (INT4) of at most 4096 values, two cells per thread at most
+  if (M > (W8 ? 4 : 2) || k < kRowsMinK || (W8 && k % 32 != 0) || (NRM && (W8 || k > 4096)))
     return hipErrorNotSupported;
   // 16 wavefronts per CU: one workgroup of 16, or two of 8 for INT4 rows of
   // 8192 k and more (measured: 7B down 13.5 -> 12.8 us, q|k|v 5.8 -> 6.0 us)
@@ -780,9 +892,10 @@ hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const
   const int64_t rows_max = (n + blocks - 1) / blocks;
   const int64_t ppr = k >> (W8 ? 5 : 6);
   constexpr int64_t cpc = W8 ? 4 : 8;  // activation cells per chunk
-  const size_t lds = (size_t)M * ppr * (cpc + 1) * 16 + (size_t)M * rows_max * nwave * sizeof(float);
+  const size_t lds =
+      (size_t)M * ppr * (cpc + 1) * 16 + (NRM ? 64 : 0) + (size_t)M * rows_max * nwave * sizeof(float);
   const int64_t xcells = M * ppr * cpc;  // 16-byte activation cells, staged by the workgroup at once
-  if (lds > kRowsLdsMax || rows_max * ppr >= (int64_t(1) << 27) || xcells > 8 * nthr)
+  if (lds > kRowsLdsMax || rows_max * ppr >= (int64_t(1) << 27) || xcells > (NRM ? 2 : 8) * nthr)
     return hipErrorNotSupported;
   constexpr int D = kRowsDepth;
   const int64_t q = n / blocks;
@@ -792,8 +905,8 @@ hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const
   const size_t lds_launch = nwave == 8 && lds < 54 * 1024 ? 54 * 1024 : lds;
   auto go = [&](auto xb_tag, auto na_tag, auto nw_tag) {
     constexpr int XB = decltype(xb_tag)::value, NA = decltype(na_tag)::value, NWV = decltype(nw_tag)::value;
-    hipLaunchKernelGGL((gemv_rows_kernel<M, W8, D, XB, NA, NWV>), dim3((unsigned)blocks), dim3(nthr), lds_launch,
-                       stream, x, k, codes, scales16, zeros16, scales32, n, y, (int)f16_out, q, rem);
+    hipLaunchKernelGGL((gemv_rows_kernel<M, W8, D, XB, NA, NWV, NRM>), dim3((unsigned)blocks), dim3(nthr),
+                       lds_launch, stream, x, k, codes, scales16, zeros16, scales32, n, y, out_mode, q, rem, nr);
   };
   // the fewest activation cells per thread that cover the activations: the
   // loads past the end are redundant and delay the code loads behind them
@@ -801,6 +914,8 @@ hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const
   auto pick = [&](auto na_tag, auto nw_tag) {
     if (xcells <= nthr)
       go(IntC<1>{}, na_tag, nw_tag);
+    else if constexpr (NRM)  // at most two cells (the host's check above)
+      go(IntC<2>{}, na_tag, nw_tag);
     else if (xcells <= 2 * nthr)
       go(IntC<2>{}, na_tag, nw_tag);
     else if (xcells <= 4 * nthr)
@@ -823,8 +938,10 @@ hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const
 
 template <int M, bool W8>
 hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint16_t* scales16,
-                  const uint16_t* zeros16, const float* scales32, int64_t n, void* y, bool f16_out,
-                  hipStream_t stream) {
+                  const uint16_t* zeros16, const float* scales32, int64_t n, void* y, int out_mode,
+                  const NormSrc* nrm, hipStream_t stream) {
+  if (nrm && (W8 || M > 2)) return hipErrorNotSupported;
+  const NormSrc nr = nrm ? *nrm : NormSrc{nullptr, nullptr, 0.f, 1};
   // the activations of a K slice sit in LDS (M * 2 bytes per k); slices are
   // whole 128-element groups
   const int64_t grain = 128;
@@ -862,14 +979,19 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
     const int64_t row_chunks = k / 64;
     const bool idle_lanes = 4 * row_chunks < 3 * 64 * ((row_chunks + 63) / 64);
     if (rows == 1 || idle_lanes) {
-      const hipError_t e = gemv_rows_m<M, false>(x, k, codes, scales16, zeros16, nullptr, n, y, f16_out, stream);
+      const hipError_t e =
+          nrm ? gemv_rows_m<M, false, true>(x, k, codes, scales16, zeros16, nullptr, n, y, out_mode, nr, stream)
+              : gemv_rows_m<M, false, false>(x, k, codes, scales16, zeros16, nullptr, n, y, out_mode, nr, stream);
       if (e != hipErrorNotSupported) return e;
     }
   }
   if constexpr (W8 && M <= 4) {
-    const hipError_t e = gemv_rows_m<M, true>(x, k, codes, nullptr, nullptr, scales32, n, y, f16_out, stream);
+    const hipError_t e =
+        gemv_rows_m<M, true, false>(x, k, codes, nullptr, nullptr, scales32, n, y, out_mode, nr, stream);
     if (e != hipErrorNotSupported) return e;
   }
+  // normalised rows and accumulated outputs: one K slice, one wavefront per task
+  if ((nrm || out_mode == kOutAcc) && (splits != 1 || (nrm && nw != 1))) return hipErrorNotSupported;
   // split-K partial sums: only the tasks-of-rows kernel needs them
   float* partial = nullptr;
   if (splits > 1) {
@@ -885,12 +1007,21 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
     // activations in registers where a task is one step (one row of 32
     // activation VGPRs beside the fragments: at most 128 VGPRs with four rows)
     constexpr bool XRok = !W8 && !MM && M == 1;
-    if (XRok && splits == 1 && nit == 1)
-      err = gemv_launch<M, W8, RR, MM, XRok>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y, f16_out,
-                                             partial, nw, stream);
-    else
-      err = gemv_launch<M, W8, RR, MM, false>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y, f16_out,
-                                              partial, nw, stream);
+    constexpr bool NRok = !W8 && !MM && M <= 2;
+    if (NRok && nrm) {
+      if (XRok && nit == 1)
+        err = gemv_launch<M, W8, RR, MM, XRok, NRok>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y,
+                                                     out_mode, partial, nw, nr, stream);
+      else
+        err = gemv_launch<M, W8, RR, MM, false, NRok>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y,
+                                                      out_mode, partial, nw, nr, stream);
+    } else if (XRok && splits == 1 && nit == 1) {
+      err = gemv_launch<M, W8, RR, MM, XRok, false>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y,
+                                                    out_mode, partial, nw, nr, stream);
+    } else {
+      err = gemv_launch<M, W8, RR, MM, false, false>(x, k, kslice, splits, codes, scales16, zeros16, scales32, n, y,
+                                                     out_mode, partial, nw, nr, stream);
+    }
   };
   auto with_nw = [&](auto r_tag) {
     if (nw > 1)
@@ -906,22 +1037,22 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
   }
   if (rows == 1) with_nw(IntC<1>{});
   if (err != hipSuccess || splits == 1) return err;
-  return launch_splitk_reduce(partial, splits, (int64_t)M * n, y, f16_out, stream);
+  return launch_splitk_reduce(partial, splits, (int64_t)M * n, y, out_mode == kOutF16, stream);
 }
 
 template <bool W8>
 hipError_t gemv_dispatch(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const uint16_t* scales16,
-                         const uint16_t* zeros16, const float* scales32, int64_t n, void* y, bool f16_out,
-                         hipStream_t stream) {
+                         const uint16_t* zeros16, const float* scales32, int64_t n, void* y, int out_mode,
+                         const NormSrc* nrm, hipStream_t stream) {
   switch (m) {
-    case 1: return gemv_m<1, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
-    case 2: return gemv_m<2, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
-    case 3: return gemv_m<3, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
-    case 4: return gemv_m<4, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
-    case 5: return gemv_m<5, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
-    case 6: return gemv_m<6, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
-    case 7: return gemv_m<7, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
-    case 8: return gemv_m<8, W8>(x, k, codes, scales16, zeros16, scales32, n, y, f16_out, stream);
+    case 1: return gemv_m<1, W8>(x, k, codes, scales16, zeros16, scales32, n, y, out_mode, nrm, stream);
+    case 2: return gemv_m<2, W8>(x, k, codes, scales16, zeros16, scales32, n, y, out_mode, nrm, stream);
+    case 3: return gemv_m<3, W8>(x, k, codes, scales16, zeros16, scales32, n, y, out_mode, nrm, stream);
+    case 4: return gemv_m<4, W8>(x, k, codes, scales16, zeros16, scales32, n, y, out_mode, nrm, stream);
+    case 5: return gemv_m<5, W8>(x, k, codes, scales16, zeros16, scales32, n, y, out_mode, nrm, stream);
+    case 6: return gemv_m<6, W8>(x, k, codes, scales16, zeros16, scales32, n, y, out_mode, nrm, stream);
+    case 7: return gemv_m<7, W8>(x, k, codes, scales16, zeros16, scales32, n, y, out_mode, nrm, stream);
+    case 8: return gemv_m<8, W8>(x, k, codes, scales16, zeros16, scales32, n, y, out_mode, nrm, stream);
     default: return hipErrorInvalidValue;
   }
 }
@@ -942,13 +1073,16 @@ hipError_t launch_splitk_reduce(const float* partial, int splits, int64_t mn, vo
 }
 
 hipError_t launch_gemv_w4(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const uint16_t* scales,
-                          const uint16_t* zeros, int64_t n, void* y, bool f16_out, hipStream_t stream) {
-  return gemv_dispatch<false>(x, m, k, codes, scales, zeros, nullptr, n, y, f16_out, stream);
+                          const uint16_t* zeros, int64_t n, void* y, bool f16_out, hipStream_t stream,
+                          const NormSrc* nrm, bool accum) {
+  const int mode = accum ? kOutAcc : (f16_out ? kOutF16 : kOutF32);
+  return gemv_dispatch<false>(x, m, k, codes, scales, zeros, nullptr, n, y, mode, nrm, stream);
 }
 
 hipError_t launch_gemv_w8(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const float* scales, int64_t n,
                           void* y, bool f16_out, hipStream_t stream) {
-  return gemv_dispatch<true>(x, m, k, codes, nullptr, nullptr, scales, n, y, f16_out, stream);
+  return gemv_dispatch<true>(x, m, k, codes, nullptr, nullptr, scales, n, y, f16_out ? kOutF16 : kOutF32, nullptr,
+                             stream);
 }
 
 }  // namespace sq

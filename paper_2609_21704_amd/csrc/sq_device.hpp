@@ -64,6 +64,81 @@ __device__ __forceinline__ void wave_sums(const float (&v)[4 * T], float (&w)[T]
   }
 }
 
+// RMS normalisation shared by the residual-add kernel and the projections
+// that normalise their own input rows, so that both give the same bits.
+// A row of k fp32 values is summed in squares by 256 threads: thread t takes
+// the float4 cells t, t + 256, ... in order, each as (a^2 + b^2) + (c^2 + d^2)
+// (no fused multiply-add); the threads' sums meet by wave_sum and then as
+// (w0 + w1) + (w2 + w3) over the four wavefronts.
+__device__ __forceinline__ float rms_cell_sq(float4_t v) {
+#pragma clang fp contract(off)
+  return (v[0] * v[0] + v[1] * v[1]) + (v[2] * v[2] + v[3] * v[3]);
+}
+
+// 1 / sqrt(mean + eps) of a row from its four wavefront sums, in fp64,
+// rounded once to fp32.
+__device__ __forceinline__ float rms_inverse(const float* wsum4, int k, float eps) {
+  const float total = (wsum4[0] + wsum4[1]) + (wsum4[2] + wsum4[3]);
+  return (float)(1.0 / sqrt((double)total / (double)k + (double)eps));
+}
+
+// One normalised value: f16(h * r * w), the products in fp32 left to right.
+__device__ __forceinline__ half_t rms_scale(float h, float r, half_t w) {
+#pragma clang fp contract(off)
+  return (half_t)(h * r * (float)w);
+}
+
+// The sums of squares of the M staged rows of a projection that normalises
+// its own input (row m is hrow0 + m * stride), on the threads of each group of
+// 256 (group gr takes rows gr, gr + groups, ...; RPT rows per thread at most,
+// rows of at most 4096 values).  load() issues the loads, finish() sums them
+// in the order of the residual-add kernel and writes each wavefront's sum of
+// row m to wsum[4 m + wavefront % 4].
+template <int RPT>
+struct RmsRows {
+  float4_t v[RPT][4];
+  __device__ __forceinline__ void load(const float* __restrict__ hrow0, int64_t stride, int M, int k) {
+    const int t = threadIdx.x & 255, gr = threadIdx.x >> 8, ngr = blockDim.x >> 8, n4 = k >> 2;
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) {
+      const int m = gr + j * ngr;
+      const float4_t* hr = reinterpret_cast<const float4_t*>(hrow0 + (int64_t)(m < M ? m : 0) * stride);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int c = t + 256 * i;
+        v[j][i] = c < n4 ? hr[c] : float4_t{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+  }
+  __device__ __forceinline__ void finish(int M, int k, float* wsum) const {
+    const int t = threadIdx.x & 255, gr = threadIdx.x >> 8, ngr = blockDim.x >> 8, n4 = k >> 2;
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) {
+      const int m = gr + j * ngr;
+      if (m >= M) continue;  // uniform across the wavefront
+      float ss = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (t + 256 * i < n4) ss += rms_cell_sq(v[j][i]);
+      ss = wave_sum(ss);
+      if ((t & 63) == 0) wsum[4 * m + (t >> 6)] = ss;
+    }
+  }
+};
+
+// Eight normalised activations f16(h * r * w) of one 16-byte cell, from the
+// eight fp32 values h0 | h1 and the eight fp16 norm weights wc.
+__device__ __forceinline__ u32x4 rms_cell(float4_t h0, float4_t h1, u32x4 wc, float r) {
+  const half8_t w8 = __builtin_bit_cast(half8_t, wc);
+  half8_t o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    o[e] = rms_scale(h0[e], r, w8[e]);
+    o[4 + e] = rms_scale(h1[e], r, w8[4 + e]);
+  }
+  return __builtin_bit_cast(u32x4, o);
+}
+
 // Output conversion for y[m][n] in either fp16 or fp32.
 template <bool F16Out>
 __device__ __forceinline__ void store_out(void* y, int64_t idx, float v) {

@@ -33,8 +33,23 @@ hipError_t launch_quantize_int4(const uint16_t* w, int64_t n, int64_t k, uint8_t
 hipError_t launch_quantize_fp8(const uint16_t* w, int64_t n, int64_t k, uint8_t* codes, float* scales,
                                int32_t* flag, hipStream_t stream);
 
+// Input rows of a projection taken as f16(rmsnorm(h row)) with weights w:
+// staged row m is h row m * group + group - 1 ([m * group][k] fp32), normalised
+// inside the projection's activation staging with the arithmetic of
+// launch_add_rmsnorm (the same bits).
+struct NormSrc {
+  const float* h;
+  const uint16_t* w;
+  float eps;
+  int group;
+};
+
+// nrm: activations from normalised rows instead of x (x unused); accum: y is
+// fp32 and the projection is added into it (y += x . W'^T).  Either returns
+// hipErrorNotSupported, enqueuing nothing, for shapes whose kernel lacks it.
 hipError_t launch_gemv_w4(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const uint16_t* scales,
-                          const uint16_t* zeros, int64_t n, void* y, bool f16_out, hipStream_t stream);
+                          const uint16_t* zeros, int64_t n, void* y, bool f16_out, hipStream_t stream,
+                          const NormSrc* nrm = nullptr, bool accum = false);
 hipError_t launch_gemv_w8(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const float* scales,
                           int64_t n, void* y, bool f16_out, hipStream_t stream);
 hipError_t launch_gemm_f16(const uint16_t* x, int m, int64_t k, const uint16_t* w, int64_t n, void* y,
@@ -42,7 +57,7 @@ hipError_t launch_gemm_f16(const uint16_t* x, int m, int64_t k, const uint16_t* 
 // Verification over row blocks on the vector ALUs, 1 <= m <= 8; returns
 // hipErrorNotSupported (nothing enqueued) for shapes it does not take.
 hipError_t launch_gemm_rows_f16(const uint16_t* x, int m, int64_t k, const uint16_t* w, int64_t n, void* y,
-                                bool f16_out, hipStream_t stream);
+                                bool f16_out, hipStream_t stream, const NormSrc* nrm = nullptr, bool accum = false);
 
 // The matrix-core streaming kernels (one implementation for the three weight
 // kinds; m <= 8 for INT4 / FP8, m <= 64 for FP16).

@@ -137,7 +137,7 @@ class SpecDecoder:
 
     def __init__(self, weights: DecoderWeights, batch: int | None = None, k: int | None = None,
                  capacity: int = 1024, temperature: float = 1.0, history: int = 4096, keep_pq: bool = False,
-                 chains: int = 1):
+                 chains: int = 1, fuse: bool = True):
         self.w = weights
         cfg = self.cfg = weights.cfg
         dev = self.device = weights.device
@@ -179,6 +179,7 @@ class SpecDecoder:
             self.q_out = torch.empty((k, R, V), dtype=f32, device=dev)
             self.p_out = torch.empty((R, k + 1, V), dtype=f32, device=dev)
         self.graph = None
+        self.fuse = fuse
 
     # ------------------------------------------------------------- passes
     def _linear(self, draft: bool, key, x, y):
@@ -187,6 +188,28 @@ class SpecDecoder:
             st.draft_gemv(key, x, y)
         else:
             st.verify_gemm(key, x, y)
+
+    def _norm_linear(self, draft: bool, key, h, norm_w, delta, x, y, group: int = 1):
+        """y = f16(rmsnorm(h [+ delta])) . W^T: in one launch where the projection
+        normalises its own input rows (no pending delta), else the residual add
+        + norm into x and the plain projection (the same bits either way)."""
+        if delta is None and self.fuse:
+            st = self.w.stack
+            done = (st.draft_gemv_rmsnorm if draft else st.verify_gemm_rmsnorm)(key, h, norm_w, EPS, group, y)
+            if done:
+                return
+        sq.sq_add_rmsnorm_f16(h, norm_w, EPS, delta=delta, group=group, x=x)
+        self._linear(draft, key, x, y)
+
+    def _residual_linear(self, draft: bool, key, x, h, y):
+        """h += x . W^T where the projection adds into its output (returns None),
+        else y = x . W^T, returned as the delta the next norm adds."""
+        if self.fuse:
+            st = self.w.stack
+            if (st.draft_gemv_acc if draft else st.verify_gemm_acc)(key, x, h):
+                return None
+        self._linear(draft, key, x, y)
+        return y
 
     def forward(self, draft: bool, first, rest, rps: int, offset: int, logits, last_only: bool,
                 len_bound: int | None = None):
@@ -202,10 +225,9 @@ class SpecDecoder:
         lb = self.capacity if len_bound is None else len_bound
         h, x, qkv, q, a, y, gu, t = (b.h[:M], b.x[:M], b.qkv[:M], b.q[:M], b.a[:M], b.y[:M], b.gu[:M], b.t[:M])
         sq.sq_embed_block_f16(w.embed, first, rest, h=h, status=self.status)
-        delta = None
+        delta = None  # a projection output not yet added into h
         for l in range(w.layers):
-            sq.sq_add_rmsnorm_f16(h, w.in_norm[l], EPS, delta=delta, x=x)
-            self._linear(draft, (l, "qkv"), x, qkv)
+            self._norm_linear(draft, (l, "qkv"), h, w.in_norm[l], delta, x, qkv)
             sq.sq_rope_kv_f16(qkv, w.qkv_bias[l], self.pos_base, offset, rps, cfg.q_heads, cache.k[l], cache.v[l],
                               len_bound=lb, theta=THETA, q_out=q, status=self.status)
             if self.attn_hook:
@@ -213,16 +235,13 @@ class SpecDecoder:
             sq.sq_attention_f16(q, cache.k[l], cache.v[l], self.pos_base, offset, rps, len_bound=lb, out=a)
             if self.attn_hook:
                 self.attn_hook(False, rps, offset)
-            self._linear(draft, (l, "o"), a.view(M, cfg.q_dim), y)
-            sq.sq_add_rmsnorm_f16(h, w.post_norm[l], EPS, delta=y, x=x)
-            self._linear(draft, (l, "gate_up"), x, gu)
+            delta = self._residual_linear(draft, (l, "o"), a.view(M, cfg.q_dim), h, y)
+            self._norm_linear(draft, (l, "gate_up"), h, w.post_norm[l], delta, x, gu)
             sq.sq_silu_mul_f16(gu, t)
-            self._linear(draft, (l, "down"), t, y)
-            delta = y
+            delta = self._residual_linear(draft, (l, "down"), t, h, y)
         group = rps if last_only else 1
         xf = b.xf[:M // group]
-        sq.sq_add_rmsnorm_f16(h, w.final_norm, EPS, delta=delta, group=group, x=xf)
-        self._linear(draft, (cfg.layers, "lm_head"), xf, logits)
+        self._norm_linear(draft, (cfg.layers, "lm_head"), h, w.final_norm, delta, xf, logits, group=group)
 
     def prefill(self, prompt: torch.Tensor, chunk: int | None = None, models=(True, False), lengths=None):
         """Feed prompt [B][Lp] (int32) but its last token to both models
@@ -341,8 +360,9 @@ class DirectDecoder(SpecDecoder):
     route of high-complexity prompts, and the plain-decoding baseline."""
 
     def __init__(self, weights: DecoderWeights, batch: int | None = None, capacity: int = 1024,
-                 temperature: float = 1.0, history: int = 4096):
+                 temperature: float = 1.0, history: int = 4096, fuse: bool = True):
         self.w = weights
+        self.fuse = fuse
         cfg = self.cfg = weights.cfg
         dev = self.device = weights.device
         self.B = self.R = B = cfg.batch if batch is None else batch

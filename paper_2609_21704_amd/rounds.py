@@ -79,6 +79,25 @@ class Stack:
     def verify_gemm(self, key, x, y):
         sq.sq_verify_gemm_f16(x, self.w16[key], y=y)
 
+    # The decoder's fused forms (False: the shape's kernel has none, nothing enqueued).
+    def draft_gemv_rmsnorm(self, key, h, norm_w, eps, group, y) -> bool:
+        if self.variant != "int4":
+            return False
+        codes, scales, zeros = self.draft[key]
+        return sq.sq_qgemv_w4a16_rmsnorm(h, norm_w, eps, codes, scales, zeros, group=group, y=y)
+
+    def verify_gemm_rmsnorm(self, key, h, norm_w, eps, group, y) -> bool:
+        return sq.sq_verify_gemm_f16_rmsnorm(h, norm_w, eps, self.w16[key], group=group, y=y)
+
+    def draft_gemv_acc(self, key, x, y) -> bool:
+        if self.variant != "int4":
+            return False
+        codes, scales, zeros = self.draft[key]
+        return sq.sq_qgemv_w4a16_acc(x, codes, scales, zeros, y)
+
+    def verify_gemm_acc(self, key, x, y) -> bool:
+        return sq.sq_verify_gemm_f16_acc(x, self.w16[key], y)
+
 
 @dataclass
 class RoundBuffers:

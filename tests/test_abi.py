@@ -33,11 +33,13 @@ def test_library_exports_every_declared_symbol():
                           "sq_qgemv_w4a16", "sq_qgemv_w8a16", "sq_verify_gemm_f16", "sq_spec_accept",
                           "sq_spec_accept_noalloc", "sq_probe_stream_read", "sq_embed_block_f16",
                           "sq_add_rmsnorm_f16", "sq_rope_kv_f16", "sq_attention_f16", "sq_silu_mul_f16",
-                          "sq_spec_commit", "sq_spec_accept_multi", "sq_kv_adopt_f16", "sq_spec_commit_multi"}
+                          "sq_spec_commit", "sq_spec_accept_multi", "sq_kv_adopt_f16", "sq_spec_commit_multi",
+                          "sq_qgemv_w4a16_rmsnorm", "sq_verify_gemm_f16_rmsnorm", "sq_qgemv_w4a16_acc",
+                          "sq_verify_gemm_f16_acc"}
     assert set(names) == set(sq.EXPORTED)
     for n in names:
         assert hasattr(lib, n), n
-    assert sq.sq_abi_version() == 5
+    assert sq.sq_abi_version() == 6
     for s in range(9):
         assert lib.sq_status_str(s).startswith(b"SQ_")
     assert lib.sq_status_str(9) == b"unknown sq_status"

@@ -1,0 +1,147 @@
+"""GPU checks of the decoder's fused projections: a projection that
+normalises its own input rows (sq_qgemv_w4a16_rmsnorm,
+sq_verify_gemm_f16_rmsnorm) must give the bits of sq_add_rmsnorm_f16
+followed by the plain projection, and a projection added into the residual
+stream (sq_qgemv_w4a16_acc, sq_verify_gemm_f16_acc) the bits of the plain
+projection followed by one fp32 add; shapes without a fused kernel return
+False and leave the output untouched.  Rounds through the decoder with and
+without the fused forms are then equal bit for bit (tokens, positions,
+caches, logits).  The unfused calls are themselves checked against the
+oracle in test_gpu_decoder.py and test_gpu_parity.py."""
+import pytest
+import torch
+
+import paper_2609_21704_amd as sq
+from paper_2609_21704_amd import decoder as dec
+from paper_2609_21704_amd import synth
+from paper_2609_21704_amd.configs import CONFIGS
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+EPS = 1e-6
+
+
+def gen(seed):
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed)
+    return g
+
+
+def bits(t):
+    return t.contiguous().view(torch.int32 if t.dtype == torch.float32 else torch.int16)
+
+
+def int4_weights(n, k, seed):
+    w = (torch.randn((n, k), generator=gen(seed)) * 0.02).half().to(DEV)
+    return sq.sq_quantize_int4_g128(w)
+
+
+def residual(mg, k, seed, scale=3.0):
+    g = gen(seed)
+    h = (torch.randn((mg, k), generator=g) * scale).float().to(DEV)
+    nw = (1.0 + torch.randn((k,), generator=g) * 0.02).half().to(DEV)
+    return h, nw
+
+
+# draft (INT4) shapes: row blocks (q|k|v, o, 1.5B), tasks of rows (gate|up, LM head)
+W4_NORM = [(4608, 3584, 1, 1), (4608, 3584, 2, 1), (37888, 3584, 1, 1), (37888, 3584, 2, 1),
+           (151936, 3584, 1, 2), (151936, 3584, 1, 1), (2048, 1536, 2, 1), (17920, 1536, 1, 1), (4608, 3584, 1, 5)]
+
+
+@pytest.mark.parametrize("n,k,m,group", W4_NORM)
+def test_qgemv_w4a16_rmsnorm_equals_norm_then_gemv(n, k, m, group):
+    codes, scales, zeros = int4_weights(n, k, n + k)
+    h, nw = residual(m * group, k, n + m)
+    h0 = h.clone()
+    y = torch.full((m, n), float("nan"), device=DEV)
+    assert sq.sq_qgemv_w4a16_rmsnorm(h, nw, EPS, codes, scales, zeros, group=group, y=y)
+    x = sq.sq_add_rmsnorm_f16(h.clone(), nw, EPS, group=group)
+    ref = sq.sq_qgemv_w4a16(x, codes, scales, zeros)
+    torch.cuda.synchronize()
+    assert torch.equal(h, h0)
+    assert torch.equal(bits(y), bits(ref))
+
+
+@pytest.mark.parametrize("n,k,m", [(4608, 3584, 5), (3584, 3584, 5), (4864, 896, 5), (2048, 1536, 8),
+                                   (4608, 3584, 1)])
+def test_verify_gemm_f16_rmsnorm_equals_norm_then_gemm(n, k, m):
+    w16 = (torch.randn((n, k), generator=gen(n)) * 0.02).half().to(DEV)
+    h, nw = residual(m, k, n + 7)
+    y = torch.empty((m, n), device=DEV)
+    assert sq.sq_verify_gemm_f16_rmsnorm(h, nw, EPS, w16, y=y)
+    x = sq.sq_add_rmsnorm_f16(h.clone(), nw, EPS)
+    ref = sq.sq_verify_gemm_f16(x, w16)
+    torch.cuda.synchronize()
+    assert torch.equal(bits(y), bits(ref))
+
+
+def test_fused_norm_unsupported_shapes_enqueue_nothing():
+    codes, scales, zeros = int4_weights(4608, 3584, 3)
+    h, nw = residual(3, 3584, 4)
+    y = torch.full((3, 4608), 7.0, device=DEV)
+    assert not sq.sq_qgemv_w4a16_rmsnorm(h, nw, EPS, codes, scales, zeros, y=y)  # m = 3: no fused kernel
+    w16 = (torch.randn((37888, 3584), generator=gen(5)) * 0.02).half().to(DEV)
+    h5, _ = residual(5, 3584, 6)
+    y5 = torch.full((5, 37888), 7.0, device=DEV)
+    assert not sq.sq_verify_gemm_f16_rmsnorm(h5, nw, EPS, w16, y=y5)  # beyond the row-block kernel
+    hk, nwk = residual(1, 5120, 8)
+    c2, s2, z2 = int4_weights(5120, 5120, 9)
+    yk = torch.full((1, 5120), 7.0, device=DEV)
+    assert not sq.sq_qgemv_w4a16_rmsnorm(hk, nwk, EPS, c2, s2, z2, y=yk)  # rows longer than 4096
+    torch.cuda.synchronize()
+    assert (y == 7.0).all() and (y5 == 7.0).all() and (yk == 7.0).all()
+
+
+@pytest.mark.parametrize("n,k,m", [(3584, 3584, 1), (3584, 18944, 1), (3584, 18944, 2), (1536, 8960, 1),
+                                   (37888, 3584, 1), (4608, 3584, 4)])
+def test_qgemv_w4a16_acc_equals_gemv_then_add(n, k, m):
+    codes, scales, zeros = int4_weights(n, k, n * 3 + k)
+    x = torch.randn((m, k), generator=gen(k)).half().to(DEV)
+    y0 = (torch.randn((m, n), generator=gen(n)) * 5).float().to(DEV)
+    y = y0.clone()
+    assert sq.sq_qgemv_w4a16_acc(x, codes, scales, zeros, y)
+    p = sq.sq_qgemv_w4a16(x, codes, scales, zeros)
+    torch.cuda.synchronize()
+    assert torch.equal(bits(y), bits(y0 + p))
+
+
+@pytest.mark.parametrize("n,k,m", [(3584, 3584, 5), (3584, 18944, 5), (1536, 8960, 8), (4608, 3584, 1)])
+def test_verify_gemm_f16_acc_equals_gemm_then_add(n, k, m):
+    w16 = (torch.randn((n, k), generator=gen(n + 1)) * 0.02).half().to(DEV)
+    x = torch.randn((m, k), generator=gen(k + 1)).half().to(DEV)
+    y0 = (torch.randn((m, n), generator=gen(m)) * 5).float().to(DEV)
+    y = y0.clone()
+    assert sq.sq_verify_gemm_f16_acc(x, w16, y)
+    p = sq.sq_verify_gemm_f16(x, w16)
+    # a second call on the same K-slice meeting slots: they were left empty
+    y2 = y0.clone()
+    assert sq.sq_verify_gemm_f16_acc(x, w16, y2)
+    torch.cuda.synchronize()
+    assert torch.equal(bits(y), bits(y0 + p)) and torch.equal(bits(y2), bits(y))
+
+
+@pytest.mark.parametrize("ci,layers,B,k,chains", [(2, 2, 1, 4, 1), (1, 2, 2, 3, 1), (1, 2, 1, 2, 2)])
+def test_fused_rounds_equal_unfused_rounds(ci, layers, B, k, chains):
+    """Decoder rounds with the fused projections reproduce the unfused rounds
+    bit for bit: tokens, positions, both caches and the last logits."""
+    cfg = CONFIGS[ci]
+    w = dec.DecoderWeights(cfg, DEV, layers=layers)
+    cap, R = 256, 3
+    runs = []
+    for fuse in (True, False):
+        sd = dec.SpecDecoder(w, batch=B, k=k, capacity=cap, chains=chains, fuse=fuse)
+        sd.prefill(dec.synthetic_prompt(cfg, B, 40, DEV))
+        ud = synth.uniform_u24((R, k, B * chains), synth.stream_seed(cfg.seed, 97), DEV)
+        ua = synth.uniform_u24((R, B, chains * k + 1), synth.stream_seed(cfg.seed, 98), DEV)
+        for r in range(R):
+            sd.set_uniforms(ud[r], ua[r])
+            sd.run()
+        torch.cuda.synchronize()
+        assert sd.status.item() == 0
+        runs.append((sd.out_tokens[:, :int(sd.out_len.max())].clone(), sd.pos_base.clone(),
+                     sd.target_logits.clone(), sd.draft_logits.clone(), sd.pcache.k_all.clone(),
+                     sd.pcache.v_all.clone(), sd.dcache.k_all.clone(), sd.dcache.v_all.clone()))
+        del sd
+    for a, b, what in zip(runs[0], runs[1], ("tokens", "positions", "target logits", "draft logits", "parent keys",
+                                              "parent values", "draft keys", "draft values")):
+        assert torch.equal(bits(a) if a.is_floating_point() else a, bits(b) if b.is_floating_point() else b), what
