@@ -331,8 +331,8 @@ sq_status sq_qgemv_w4a16_rmsnorm(const float* h, int32_t group, const uint16_t* 
   const Range ins[] = {{h, (size_t)m * group * k * 4}, {norm_w, (size_t)k * 2}, {codes, nk / 2}, {scales, nk / 64},
                        {zeros, nk / 64}};
   if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
-  (void)hipGetLastError();
   if (m > 8) return SQ_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
   const sq::NormSrc nrm{h, norm_w, eps, group};
   return fused_status(sq::launch_gemv_w4(nullptr, (int)m, k, codes, scales, zeros, n, y, y_dtype == SQ_F16, stream,
                                          &nrm, false));
@@ -348,8 +348,8 @@ sq_status sq_qgemv_w4a16_acc(const uint16_t* x, int64_t m, int64_t k, const uint
   const Range outs[] = {{y, (size_t)m * n * 4}};
   const Range ins[] = {{x, (size_t)m * k * 2}, {codes, nk / 2}, {scales, nk / 64}, {zeros, nk / 64}};
   if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
-  (void)hipGetLastError();
   if (m > 8) return SQ_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
   return fused_status(sq::launch_gemv_w4(x, (int)m, k, codes, scales, zeros, n, y, false, stream, nullptr, true));
 }
 
@@ -366,9 +366,9 @@ sq_status sq_verify_gemm_f16_rmsnorm(const float* h, int32_t group, const uint16
   const Range outs[] = {{y, (size_t)m * n * ysz}};
   const Range ins[] = {{h, (size_t)m * group * k * 4}, {norm_w, (size_t)k * 2}, {w16, (size_t)n * k * 2}};
   if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
-  (void)hipGetLastError();
   // the row blocks, where sq_verify_gemm_f16 takes them
   if (!(m <= 8 && n * k * 2 >= kRowsMinBytesF16 && n <= kRowsMaxRowsF16)) return SQ_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
   const sq::NormSrc nrm{h, norm_w, eps, group};
   return fused_status(
       sq::launch_gemm_rows_f16(nullptr, (int)m, k, w16, n, y, y_dtype == SQ_F16, stream, &nrm, false));
@@ -382,8 +382,8 @@ sq_status sq_verify_gemm_f16_acc(const uint16_t* x, int64_t m, int64_t k, const 
   const Range outs[] = {{y, (size_t)m * n * 4}};
   const Range ins[] = {{x, (size_t)m * k * 2}, {w16, (size_t)n * k * 2}};
   if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
-  (void)hipGetLastError();
   if (!(m <= 8 && n * k * 2 >= kRowsMinBytesF16 && n <= kRowsMaxRowsF16)) return SQ_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
   return fused_status(sq::launch_gemm_rows_f16(x, (int)m, k, w16, n, y, false, stream, nullptr, true));
 }
 

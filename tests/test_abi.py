@@ -83,6 +83,40 @@ def test_gemv_gemm_validation():
     assert gm(A, 5, 64, B, 10, B + 100, F32, None) == ALIAS
 
 
+def test_fused_projection_validation():
+    """The decoder's fused projections validate on the host like the plain
+    calls (plus the normalised source); a shape without a fused kernel is
+    SQ_ERR_UNSUPPORTED, still without any HIP call."""
+    lib = sq.load()
+    n4, nf = lib.sq_qgemv_w4a16_rmsnorm, lib.sq_verify_gemm_f16_rmsnorm
+    a4, af = lib.sq_qgemv_w4a16_acc, lib.sq_verify_gemm_f16_acc
+    # (h, group, norm_w, eps, m, k, codes, scales, zeros, n, y, y_dtype, stream)
+    assert n4(None, 1, A, 1e-6, 1, 256, B, C, D, 10, E, F32, None) == NULL
+    assert n4(A, 1, None, 1e-6, 1, 256, B, C, D, 10, E, F32, None) == NULL
+    assert n4(A, 0, C, 1e-6, 1, 256, B, C, D, 10, E, F32, None) == SHAPE
+    assert n4(A, 1, C, float("nan"), 1, 256, B, C, D, 10, E, F32, None) == NONFINITE
+    assert n4(A, 1, C, -1.0, 1, 256, B, C, D, 10, E, F32, None) == SHAPE
+    assert n4(A, 1, C, 1e-6, 1, 32768, B, C, D, 10, E, F32, None) == SHAPE    # rows beyond 16384
+    assert n4(A + 4, 1, C, 1e-6, 1, 256, B, C, D, 10, E, F32, None) == ALIGN
+    assert n4(A, 1, C + 2, 1e-6, 1, 256, B, C + 1024, D, 10, E, F32, None) == ALIGN
+    assert n4(A, 1, C, 1e-6, 1, 256, B, C + 1024, D, 10, A + 64, F32, None) == ALIAS   # y inside h
+    assert n4(A, 1, C, 1e-6, 9, 256, B, C + 1024, D, 10, E, F32, None) == UNSUPPORTED  # m > 8
+    # (h, group, norm_w, eps, m, k, w16, n, y, y_dtype, stream)
+    assert nf(A, 1, C, 1e-6, 0, 64, B, 10, E, F32, None) == SHAPE
+    assert nf(A, 1, C, 1e-6, 5, 64, B + 2, 10, E, F32, None) == ALIGN
+    assert nf(A, 1, C, 1e-6, 5, 64, B, 10, B + 100, F32, None) == ALIAS
+    assert nf(A, 1, C, 1e-6, 5, 64, B, 10, E, F32, None) == UNSUPPORTED  # 1280 bytes of weights: no row blocks
+    # (x, m, k, codes, scales, zeros, n, y, stream) / (x, m, k, w16, n, y, stream)
+    assert a4(A, 1, 256, B, C, D, 10, None, None) == NULL
+    assert a4(A, 1, 256, B, C, D, 10, E + 2, None) == ALIGN
+    assert a4(A, 1, 256, B, C, D, 10, A + 64, None) == ALIAS
+    assert a4(A, 9, 256, B, C, D, 10, E, None) == UNSUPPORTED
+    assert af(A, 5, 12, B, 10, E, None) == SHAPE
+    assert af(A, 5, 64, B, 10, B + 100, None) == ALIAS
+    assert af(A, 65, 64, B, 10, E, None) == SHAPE
+    assert af(A, 5, 64, B, 10, E, None) == UNSUPPORTED
+
+
 def test_accept_validation():
     lib = sq.load()
     acc = lib.sq_spec_accept
