@@ -66,6 +66,25 @@ int main() {
   EXPECT(sq_verify_gemm_f16(at<uint16_t>(A), 65, 64, at<uint16_t>(B), 10, at<void>(E), SQ_F32, s), SQ_ERR_SHAPE);
   EXPECT(sq_verify_gemm_f16(at<uint16_t>(A), 5, 3584, at<uint16_t>(B), 4608, at<void>(E), SQ_F16, s), SQ_OK);
   EXPECT(sq_verify_gemm_f16(at<uint16_t>(A), 36, 3584, at<uint16_t>(B), 151936, at<void>(E), SQ_F32, s), SQ_OK);
+  // the decoder's fused projections
+  EXPECT(sq_qgemv_w4a16_rmsnorm(at<float>(A), 1, at<uint16_t>(C), 1e-6f, 1, 3584, at<uint8_t>(B), at<uint16_t>(D),
+                                at<uint16_t>(D + (1ull << 24)), 4608, at<void>(E), SQ_F32, s),
+         SQ_OK);
+  EXPECT(sq_qgemv_w4a16_rmsnorm(at<float>(A), 2, at<uint16_t>(C), std::nanf(""), 1, 3584, at<uint8_t>(B), at<uint16_t>(D),
+                                at<uint16_t>(D + (1ull << 24)), 4608, at<void>(E), SQ_F32, s),
+         SQ_ERR_NONFINITE);
+  EXPECT(sq_verify_gemm_f16_rmsnorm(at<float>(A), 1, at<uint16_t>(C), 1e-6f, 5, 3584, at<uint16_t>(B), 4608,
+                                    at<void>(E), SQ_F32, s),
+         SQ_OK);
+  EXPECT(sq_verify_gemm_f16_rmsnorm(at<float>(A), 1, at<uint16_t>(C), 1e-6f, 5, 3584, at<uint16_t>(B), 37888,
+                                    at<void>(E), SQ_F32, s),
+         SQ_ERR_UNSUPPORTED);
+  EXPECT(sq_qgemv_w4a16_acc(at<uint16_t>(A), 1, 18944, at<uint8_t>(B), at<uint16_t>(C), at<uint16_t>(D), 3584,
+                            at<float>(E), s),
+         SQ_OK);
+  EXPECT(sq_verify_gemm_f16_acc(at<uint16_t>(A), 5, 18944, at<uint16_t>(B), 3584, at<float>(E), s), SQ_OK);
+  EXPECT(sq_verify_gemm_f16_acc(at<uint16_t>(A), 5, 18944, at<uint16_t>(B), 3584, at<float>(E + 2), s),
+         SQ_ERR_ALIGN);
   // accept, and its allocation-free twin
   float nan = std::nanf("");
   EXPECT(sq_spec_accept(at<float>(A), at<float>(B), at<int32_t>(C), at<uint32_t>(D), 1, 4, 100, nan, at<int32_t>(E),
