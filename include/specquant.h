@@ -27,6 +27,9 @@
  *   sq_qgemv_w4a16_rmsnorm, sq_verify_gemm_f16_rmsnorm
  *                          a projection of RMS-normalised rows of h (the norm
  *                          inside the projection's activation staging)
+ *   sq_qgemv_w4a16_rmsnorm_silu
+ *                          the draft gate|up projection of normalised rows
+ *                          with the SiLU-gated product applied to its outputs
  *   sq_qgemv_w4a16_acc, sq_verify_gemm_f16_acc
  *                          a projection added into the residual stream
  *   sq_spec_commit         emitted tokens and restart position of a round
@@ -322,6 +325,17 @@ sq_status sq_verify_gemm_f16_rmsnorm(const float* h, int32_t group, const uint16
                                      hipStream_t stream);
 sq_status sq_qgemv_w4a16_acc(const uint16_t* x, int64_t m, int64_t k, const uint8_t* codes, const uint16_t* scales,
                              const uint16_t* zeros, int64_t n, float* y, hipStream_t stream);
+
+/* sq_qgemv_w4a16_rmsnorm of the fused gate|up matrix (rows [0, n / 2) the
+ * gate, [n / 2, n) the up projection) followed by sq_silu_mul_f16 of its fp32
+ * outputs, as one call: t[i][c] = f16(g / (1 + exp(-g)) * u) with g, u the
+ * fp32 outputs of rows c and n / 2 + c (the same bits as the two calls).
+ * t [m][n / 2] fp16 out; n even; m <= 2 with two rows per task of the INT4
+ * GEMV (gate|up shapes of at least 2 x 16384 rows, k <= 4096); other shapes
+ * return SQ_ERR_UNSUPPORTED and enqueue nothing. */
+sq_status sq_qgemv_w4a16_rmsnorm_silu(const float* h, int32_t group, const uint16_t* norm_w, float eps, int64_t m,
+                                      int64_t k, const uint8_t* codes, const uint16_t* scales, const uint16_t* zeros,
+                                      int64_t n, uint16_t* t, hipStream_t stream);
 sq_status sq_verify_gemm_f16_acc(const uint16_t* x, int64_t m, int64_t k, const uint16_t* w16, int64_t n, float* y,
                                  hipStream_t stream);
 

@@ -22,6 +22,7 @@ from ._lib import (  # noqa: F401
     sq_qgemv_w4a16,
     sq_qgemv_w4a16_acc,
     sq_qgemv_w4a16_rmsnorm,
+    sq_qgemv_w4a16_rmsnorm_silu,
     sq_qgemv_w8a16,
     sq_quantize_fp8_e4m3,
     sq_quantize_int4_g128,

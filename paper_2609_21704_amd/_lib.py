@@ -62,6 +62,7 @@ def load() -> ctypes.CDLL:
             "sq_qgemv_w4a16_rmsnorm": ([P, I32, P, F, I64, I64, P, P, P, I64, P, S, P], S),
             "sq_verify_gemm_f16_rmsnorm": ([P, I32, P, F, I64, I64, P, I64, P, S, P], S),
             "sq_qgemv_w4a16_acc": ([P, I64, I64, P, P, P, I64, P, P], S),
+            "sq_qgemv_w4a16_rmsnorm_silu": ([P, I32, P, F, I64, I64, P, P, P, I64, P, P], S),
             "sq_verify_gemm_f16_acc": ([P, I64, I64, P, I64, P, P], S),
             "sq_spec_commit": ([P, P, P, I32, I32, P, P, P, P, I64, P, P, P], S),
             "sq_spec_accept_multi": ([P, P, P, P, I32, I32, I32, I32, F, P, P, P, P, P, P], S),
@@ -81,7 +82,7 @@ EXPORTED = ("sq_abi_version", "sq_status_str", "sq_quantize_int4_g128", "sq_quan
             "sq_spec_accept_noalloc", "sq_probe_stream_read", "sq_embed_block_f16", "sq_add_rmsnorm_f16",
             "sq_rope_kv_f16", "sq_attention_f16", "sq_silu_mul_f16", "sq_spec_commit", "sq_spec_accept_multi",
             "sq_kv_adopt_f16", "sq_spec_commit_multi", "sq_qgemv_w4a16_rmsnorm", "sq_verify_gemm_f16_rmsnorm",
-            "sq_qgemv_w4a16_acc", "sq_verify_gemm_f16_acc")
+            "sq_qgemv_w4a16_acc", "sq_verify_gemm_f16_acc", "sq_qgemv_w4a16_rmsnorm_silu")
 
 # device status bits (SQ_DEV_* of include/specquant.h)
 DEV_BAD_TOKEN, DEV_BAD_POS, DEV_OVERFLOW, DEV_NO_DIST = 1, 2, 4, 8
@@ -220,6 +221,23 @@ def sq_qgemv_w4a16_rmsnorm(h, norm_w, eps: float, codes, scales, zeros, group: i
     return _fused(load().sq_qgemv_w4a16_rmsnorm(_ptr(h), int(group), _ptr(norm_w), float(eps), m, k, _ptr(codes),
                                                 _ptr(scales), _ptr(zeros), n, _ptr(y), _dtype_code(y.dtype),
                                                 _stream(h.device)), "sq_qgemv_w4a16_rmsnorm")
+
+
+def sq_qgemv_w4a16_rmsnorm_silu(h, norm_w, eps: float, codes, scales, zeros, t, group: int = 1) -> bool:
+    """t = f16(silu(g) * u) with g | u = x . W4'^T the gate and up halves of the fused gate|up rows and x the
+    rows sq_add_rmsnorm_f16(h, norm_w, eps, group) writes; False (nothing enqueued) where the projection's
+    kernel has no such form."""
+    m, k = _norm_src(h, norm_w, group)
+    n = codes.shape[0]
+    _dev(h, norm_w, codes, scales, zeros, t)
+    _expect(codes, torch.uint8, (n, k // 2), "codes")
+    _expect(scales, torch.float16, (n, k // 128), "scales")
+    _expect(zeros, torch.float16, (n, k // 128), "zeros")
+    if t.dtype != torch.float16 or t.numel() != m * (n // 2):
+        raise ValueError("t must be float16 with m * n / 2 elements")
+    return _fused(load().sq_qgemv_w4a16_rmsnorm_silu(_ptr(h), int(group), _ptr(norm_w), float(eps), m, k,
+                                                     _ptr(codes), _ptr(scales), _ptr(zeros), n, _ptr(t),
+                                                     _stream(h.device)), "sq_qgemv_w4a16_rmsnorm_silu")
 
 
 def sq_verify_gemm_f16_rmsnorm(h, norm_w, eps: float, w16, group: int = 1, y=None) -> bool:

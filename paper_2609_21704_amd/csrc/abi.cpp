@@ -338,6 +338,27 @@ sq_status sq_qgemv_w4a16_rmsnorm(const float* h, int32_t group, const uint16_t* 
                                          &nrm, false));
 }
 
+sq_status sq_qgemv_w4a16_rmsnorm_silu(const float* h, int32_t group, const uint16_t* norm_w, float eps, int64_t m,
+                                      int64_t k, const uint8_t* codes, const uint16_t* scales, const uint16_t* zeros,
+                                      int64_t n, uint16_t* t, hipStream_t stream) {
+  if (!codes || !scales || !zeros || !t) return SQ_ERR_NULL;
+  if (m < 1 || m > 64 || n < 2 || n > kMaxN || n % 2 != 0 || k < 128 || k > kMaxK || k % 128 != 0)
+    return SQ_ERR_SHAPE;
+  const sq_status ns = check_norm_src(h, group, norm_w, eps, m, k);
+  if (ns != SQ_OK) return ns;
+  if (!aligned(codes, 16) || !aligned(scales, 2) || !aligned(zeros, 2) || !aligned(t, 2)) return SQ_ERR_ALIGN;
+  const size_t nk = (size_t)n * (size_t)k;
+  const Range outs[] = {{t, (size_t)m * (n / 2) * 2}};
+  const Range ins[] = {{h, (size_t)m * group * k * 4}, {norm_w, (size_t)k * 2}, {codes, nk / 2}, {scales, nk / 64},
+                       {zeros, nk / 64}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  if (m > 2) return SQ_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
+  const sq::NormSrc nrm{h, norm_w, eps, group};
+  return fused_status(
+      sq::launch_gemv_w4(nullptr, (int)m, k, codes, scales, zeros, n, t, true, stream, &nrm, false, true));
+}
+
 sq_status sq_qgemv_w4a16_acc(const uint16_t* x, int64_t m, int64_t k, const uint8_t* codes, const uint16_t* scales,
                              const uint16_t* zeros, int64_t n, float* y, hipStream_t stream) {
   if (!x || !codes || !scales || !zeros || !y) return SQ_ERR_NULL;

@@ -612,7 +612,7 @@ __global__ __launch_bounds__(256) void silu_mul_kernel(const float* __restrict__
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
     const int64_t row = i / inter, col = i - row * inter;
     const float gv = gu[row * 2 * inter + col], uv = gu[row * 2 * inter + inter + col];
-    t[i] = f32_to_f16_bits(gv / (1.f + expf(-gv)) * uv);
+    t[i] = silu_gate_bits(gv, uv);
   }
 }
 

@@ -79,14 +79,16 @@ struct TaskPtr {
   int last;               // index of the task's last real row (0 .. R-1)
 };
 
-template <bool W8, int R>
+// SILU (R = 2): task t is the gate row t and the up row t + n / 2, at a pitch
+// of n / 2 rows (the caller's row_bytes / groups of load_frag).
+template <bool W8, int R, bool SILU = false>
 __device__ __forceinline__ TaskPtr task_ptr(const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
                                             const uint16_t* __restrict__ zeros, int64_t n, int64_t k, int64_t k0,
                                             int64_t task) {
   TaskPtr t;
-  const int64_t row0 = task * R;
+  const int64_t row0 = SILU ? task : task * R;
   const int64_t left = n - 1 - row0;
-  t.last = left < R - 1 ? (int)left : R - 1;
+  t.last = SILU ? 1 : (left < R - 1 ? (int)left : R - 1);
   t.codes = codes + row0 * (W8 ? k : (k >> 1)) + (W8 ? k0 : (k0 >> 1));
   t.scales = W8 ? nullptr : scales + row0 * (k >> 7) + (k0 >> 7);
   t.zeros = W8 ? nullptr : zeros + row0 * (k >> 7) + (k0 >> 7);
@@ -223,8 +225,9 @@ struct XStage {
   }
 };
 
-// Output modes of the projection kernels: y fp32, y fp16, or y fp32 added to.
-enum : int { kOutF32 = 0, kOutF16 = 1, kOutAcc = 2 };
+// Output modes of the projection kernels: y fp32, y fp16, y fp32 added to, or
+// (SILU, tasks of a gate and an up row) t = f16(silu(gate) * up) [m][n / 2].
+enum : int { kOutF32 = 0, kOutF16 = 1, kOutAcc = 2, kOutSilu = 3 };
 
 __device__ __forceinline__ void store_mode(void* y, int64_t idx, float v, int out_mode) {
   if (out_mode == kOutF16)
@@ -235,7 +238,7 @@ __device__ __forceinline__ void store_mode(void* y, int64_t idx, float v, int ou
     reinterpret_cast<float*>(y)[idx] = v;
 }
 
-template <int M, bool W8, int R, bool MULTI, bool XR, bool NRM>
+template <int M, bool W8, int R, bool MULTI, bool XR, bool NRM, bool SILU>
 __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__ x, int64_t k, int64_t kslice,
                                                        const uint8_t* __restrict__ codes,
                                                        const uint16_t* __restrict__ scales16,
@@ -260,7 +263,7 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
   const int team = wave / nw, wt = wave - team * nw;  // team in the workgroup, wavefront in the team
   const int nteam = (int)(blockDim.x >> 6) / nw;      // teams per workgroup
   const int64_t tstride = (int64_t)gridDim.x * nteam;  // teams in the grid: the task stride
-  const int64_t ntask = (n + R - 1) / R;
+  const int64_t ntask = SILU ? n / 2 : (n + R - 1) / R;
   // multi-wavefront teams meet at barriers, so every team of the grid runs
   // the same number of tasks (ntask_pad / tstride); single-wavefront teams
   // stop at ntask
@@ -270,8 +273,9 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
   half_t* xs = reinterpret_cast<half_t*>(smem);
   float* red = reinterpret_cast<float*>(smem + (size_t)M * kCells * nchunk * 16);  // [teams][nw][R][M]
 
-  const int row_bytes = (int)(W8 ? k : (k >> 1));
-  const int groups = (int)(k >> 7);
+  // distance between the rows of a task: one row, or n / 2 rows (SILU)
+  const int row_bytes = (int)(W8 ? k : (k >> 1)) * (SILU ? (int)(n >> 1) : 1);
+  const int groups = (int)(k >> 7) * (SILU ? (int)(n >> 1) : 1);
 
   // activations first, then the first fragment, so that x is not queued
   // behind the weight stream
@@ -283,7 +287,7 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
   XStage<M, W8, NRM> xst;
   xst.load(x, k, k0, kl, nchunk, 0, nr);
   Frag<R> fa, fb;
-  TaskPtr tp = task_ptr<W8, R>(codes, scales16, zeros16, n, k, k0, task < ntask ? task : ntask - 1);
+  TaskPtr tp = task_ptr<W8, R, SILU>(codes, scales16, zeros16, n, k, k0, task < ntask ? task : ntask - 1);
   fa = load_frag<W8, R>(tp, row_bytes, groups, kl, nchunk, it, lane);
   if constexpr (NRM) {
     float* wsum = reinterpret_cast<float*>(smem + (size_t)M * kCells * nchunk * 16);  // [M][4]
@@ -338,7 +342,7 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
       it_n = wt;
       task_n = task + tstride;
     }
-    const TaskPtr tp_n = task_n == task ? tp : task_ptr<W8, R>(codes, scales16, zeros16, n, k, k0,
+    const TaskPtr tp_n = task_n == task ? tp : task_ptr<W8, R, SILU>(codes, scales16, zeros16, n, k, k0,
                                                              task_n < ntask ? task_n : ntask - 1);
     nxt = load_frag<W8, R>(tp_n, row_bytes, groups, kl, nchunk, it_n, lane);
 
@@ -461,7 +465,13 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
         else
           store_mode(y, (int64_t)m * n + row, val, out_mode);
       };
-      if constexpr (!MULTI) {
+      if constexpr (SILU) {
+        // gate of row m = 0 in lane 0 and (M = 2) of m = 1 in lane 32; its up
+        // value 32 (M = 1) or 16 (M = 2) lanes above: t[m][task] = silu(g) u
+        const float up = __shfl(w[0], lane + (M == 1 ? 32 : 16), kWave);
+        if (lane == 0 || (M == 2 && lane == 32))
+          reinterpret_cast<uint16_t*>(y)[(int64_t)(lane >> 5) * (n >> 1) + task] = silu_gate_bits(w[0], up);
+      } else if constexpr (!MULTI) {
         if (lead) {
 #pragma unroll
           for (int t = 0; t < T; ++t) {
@@ -835,14 +845,14 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   }
 }
 
-template <int M, bool W8, int R, bool MULTI, bool XR, bool NRM>
+template <int M, bool W8, int R, bool MULTI, bool XR, bool NRM, bool SILU = false>
 hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits, const uint8_t* codes,
                        const uint16_t* scales16, const uint16_t* zeros16, const float* scales32, int64_t n, void* y,
                        int out_mode, float* partial, int nw, const NormSrc& nr, hipStream_t stream) {
   constexpr int64_t chunk_k = W8 ? 32 : 64;
   const int64_t kfirst = kslice < k ? kslice : k;
   const int64_t nchunk = (kfirst + chunk_k - 1) / chunk_k;
-  const int64_t ntask = (n + R - 1) / R;
+  const int64_t ntask = SILU ? n / 2 : (n + R - 1) / R;
   const int64_t cus = cu_count();
   // teams: as many as the CUs hold (kWavesPerCu wavefronts each) or
   // as there are tasks; teams per workgroup: enough to cover the CUs once
@@ -860,10 +870,12 @@ hipError_t gemv_launch(const uint16_t* x, int64_t k, int64_t kslice, int splits,
   const int64_t blocks = (teams + T - 1) / T;
   // normalised rows: one K slice staged by 256 threads, 2 M cells each
   if (NRM && (splits != 1 || T * nw != 4 || nchunk > 64)) return hipErrorNotSupported;
+  // SiLU pairs: rows t and t + n / 2 of a task, at a pitch that fits 32 bits
+  if (SILU && (n % 2 != 0 || (n / 2) * (k / 2) >= (int64_t(1) << 31))) return hipErrorNotSupported;
   const size_t lds = (size_t)M * 2 * (size_t)(nchunk * chunk_k) + (MULTI ? (size_t)T * nw * R * M * 4 : 0) +
                      (NRM ? (size_t)M * 4 * sizeof(float) : 0);
   const dim3 grid((unsigned)blocks, (unsigned)splits);
-  hipLaunchKernelGGL((gemv_kernel<M, W8, R, MULTI, XR, NRM>), grid, dim3((unsigned)(T * nw * 64)), lds, stream, x, k,
+  hipLaunchKernelGGL((gemv_kernel<M, W8, R, MULTI, XR, NRM, SILU>), grid, dim3((unsigned)(T * nw * 64)), lds, stream, x, k,
                      kslice, codes, scales16, zeros16, scales32, n, y, out_mode, partial, nw, nr);
   return hipGetLastError();
 }
@@ -978,7 +990,7 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
     // leaves more than a quarter of the lanes idle (measured crossover)
     const int64_t row_chunks = k / 64;
     const bool idle_lanes = 4 * row_chunks < 3 * 64 * ((row_chunks + 63) / 64);
-    if (rows == 1 || idle_lanes) {
+    if ((rows == 1 || idle_lanes) && out_mode != kOutSilu) {
       const hipError_t e =
           nrm ? gemv_rows_m<M, false, true>(x, k, codes, scales16, zeros16, nullptr, n, y, out_mode, nr, stream)
               : gemv_rows_m<M, false, false>(x, k, codes, scales16, zeros16, nullptr, n, y, out_mode, nr, stream);
@@ -992,6 +1004,31 @@ hipError_t gemv_m(const uint16_t* x, int64_t k, const uint8_t* codes, const uint
   }
   // normalised rows and accumulated outputs: one K slice, one wavefront per task
   if ((nrm || out_mode == kOutAcc) && (splits != 1 || (nrm && nw != 1))) return hipErrorNotSupported;
+  if (out_mode == kOutSilu) {  // tasks of the gate and up rows t, t + n / 2: two rows, one wavefront, one slice
+    if constexpr (!W8 && M <= 2) {
+      // only where the plain projection runs this kernel too (the same sums,
+      // so the same bits as the projection followed by the SiLU kernel)
+      const int64_t row_chunks = k / 64;
+      const bool idle_lanes = 4 * row_chunks < 3 * 64 * ((row_chunks + 63) / 64);
+      if (rows != 2 || nw != 1 || splits != 1 || idle_lanes) return hipErrorNotSupported;
+      if constexpr (M == 1) {
+        if (nit == 1)
+          return nrm ? gemv_launch<M, false, 2, false, true, true, true>(x, k, kslice, splits, codes, scales16,
+                                                                          zeros16, nullptr, n, y, out_mode, nullptr,
+                                                                          nw, nr, stream)
+                     : gemv_launch<M, false, 2, false, true, false, true>(x, k, kslice, splits, codes, scales16,
+                                                                           zeros16, nullptr, n, y, out_mode, nullptr,
+                                                                           nw, nr, stream);
+      }
+      return nrm ? gemv_launch<M, false, 2, false, false, true, true>(x, k, kslice, splits, codes, scales16, zeros16,
+                                                                       nullptr, n, y, out_mode, nullptr, nw, nr,
+                                                                       stream)
+                 : gemv_launch<M, false, 2, false, false, false, true>(x, k, kslice, splits, codes, scales16, zeros16,
+                                                                        nullptr, n, y, out_mode, nullptr, nw, nr,
+                                                                        stream);
+    }
+    return hipErrorNotSupported;
+  }
   // split-K partial sums: only the tasks-of-rows kernel needs them
   float* partial = nullptr;
   if (splits > 1) {
@@ -1074,8 +1111,8 @@ hipError_t launch_splitk_reduce(const float* partial, int splits, int64_t mn, vo
 
 hipError_t launch_gemv_w4(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const uint16_t* scales,
                           const uint16_t* zeros, int64_t n, void* y, bool f16_out, hipStream_t stream,
-                          const NormSrc* nrm, bool accum) {
-  const int mode = accum ? kOutAcc : (f16_out ? kOutF16 : kOutF32);
+                          const NormSrc* nrm, bool accum, bool silu) {
+  const int mode = silu ? kOutSilu : (accum ? kOutAcc : (f16_out ? kOutF16 : kOutF32));
   return gemv_dispatch<false>(x, m, k, codes, scales, zeros, nullptr, n, y, mode, nrm, stream);
 }
 

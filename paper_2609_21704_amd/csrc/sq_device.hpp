@@ -139,6 +139,13 @@ __device__ __forceinline__ u32x4 rms_cell(float4_t h0, float4_t h1, u32x4 wc, fl
   return __builtin_bit_cast(u32x4, o);
 }
 
+// The SiLU-gated product f16(g / (1 + e^-g) * u) of a gate and an up value,
+// shared by the SiLU kernel and the gate|up projection that applies it to its
+// own outputs (the same bits).
+__device__ __forceinline__ uint16_t silu_gate_bits(float g, float u) {
+  return f32_to_f16_bits(g / (1.f + expf(-g)) * u);
+}
+
 // Output conversion for y[m][n] in either fp16 or fp32.
 template <bool F16Out>
 __device__ __forceinline__ void store_out(void* y, int64_t idx, float v) {

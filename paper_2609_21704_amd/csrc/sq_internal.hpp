@@ -45,11 +45,13 @@ struct NormSrc {
 };
 
 // nrm: activations from normalised rows instead of x (x unused); accum: y is
-// fp32 and the projection is added into it (y += x . W'^T).  Either returns
-// hipErrorNotSupported, enqueuing nothing, for shapes whose kernel lacks it.
+// fp32 and the projection is added into it (y += x . W'^T); silu: rows
+// [0, n / 2) are gates and [n / 2, n) ups, and y is t [m][n / 2] fp16 =
+// f16(silu(gate) * up).  Each returns hipErrorNotSupported, enqueuing nothing,
+// for shapes whose kernel lacks it.
 hipError_t launch_gemv_w4(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const uint16_t* scales,
                           const uint16_t* zeros, int64_t n, void* y, bool f16_out, hipStream_t stream,
-                          const NormSrc* nrm = nullptr, bool accum = false);
+                          const NormSrc* nrm = nullptr, bool accum = false, bool silu = false);
 hipError_t launch_gemv_w8(const uint16_t* x, int m, int64_t k, const uint8_t* codes, const float* scales,
                           int64_t n, void* y, bool f16_out, hipStream_t stream);
 hipError_t launch_gemm_f16(const uint16_t* x, int m, int64_t k, const uint16_t* w, int64_t n, void* y,

@@ -236,8 +236,10 @@ class SpecDecoder:
             if self.attn_hook:
                 self.attn_hook(False, rps, offset)
             delta = self._residual_linear(draft, (l, "o"), a.view(M, cfg.q_dim), h, y)
-            self._norm_linear(draft, (l, "gate_up"), h, w.post_norm[l], delta, x, gu)
-            sq.sq_silu_mul_f16(gu, t)
+            if not (draft and delta is None and self.fuse and
+                    w.stack.draft_gemv_rmsnorm_silu((l, "gate_up"), h, w.post_norm[l], EPS, t)):
+                self._norm_linear(draft, (l, "gate_up"), h, w.post_norm[l], delta, x, gu)
+                sq.sq_silu_mul_f16(gu, t)
             delta = self._residual_linear(draft, (l, "down"), t, h, y)
         group = rps if last_only else 1
         xf = b.xf[:M // group]

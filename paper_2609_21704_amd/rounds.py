@@ -86,6 +86,12 @@ class Stack:
         codes, scales, zeros = self.draft[key]
         return sq.sq_qgemv_w4a16_rmsnorm(h, norm_w, eps, codes, scales, zeros, group=group, y=y)
 
+    def draft_gemv_rmsnorm_silu(self, key, h, norm_w, eps, t) -> bool:
+        if self.variant != "int4":
+            return False
+        codes, scales, zeros = self.draft[key]
+        return sq.sq_qgemv_w4a16_rmsnorm_silu(h, norm_w, eps, codes, scales, zeros, t)
+
     def verify_gemm_rmsnorm(self, key, h, norm_w, eps, group, y) -> bool:
         return sq.sq_verify_gemm_f16_rmsnorm(h, norm_w, eps, self.w16[key], group=group, y=y)
 

@@ -79,6 +79,15 @@ int main() {
   EXPECT(sq_verify_gemm_f16_rmsnorm(at<float>(A), 1, at<uint16_t>(C), 1e-6f, 5, 3584, at<uint16_t>(B), 37888,
                                     at<void>(E), SQ_F32, s),
          SQ_ERR_UNSUPPORTED);
+  EXPECT(sq_qgemv_w4a16_rmsnorm_silu(at<float>(A), 1, at<uint16_t>(C), 1e-6f, 1, 3584, at<uint8_t>(B),
+                                     at<uint16_t>(D), at<uint16_t>(D + (1ull << 24)), 37888, at<uint16_t>(E), s),
+         SQ_OK);
+  EXPECT(sq_qgemv_w4a16_rmsnorm_silu(at<float>(A), 1, at<uint16_t>(C), 1e-6f, 1, 3584, at<uint8_t>(B),
+                                     at<uint16_t>(D), at<uint16_t>(D + (1ull << 24)), 37887, at<uint16_t>(E), s),
+         SQ_ERR_SHAPE);
+  EXPECT(sq_qgemv_w4a16_rmsnorm_silu(at<float>(A), 1, at<uint16_t>(C), 1e-6f, 3, 3584, at<uint8_t>(B),
+                                     at<uint16_t>(D), at<uint16_t>(D + (1ull << 24)), 37888, at<uint16_t>(E), s),
+         SQ_ERR_UNSUPPORTED);
   EXPECT(sq_qgemv_w4a16_acc(at<uint16_t>(A), 1, 18944, at<uint8_t>(B), at<uint16_t>(C), at<uint16_t>(D), 3584,
                             at<float>(E), s),
          SQ_OK);

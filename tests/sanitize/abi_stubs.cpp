@@ -56,7 +56,7 @@ namespace sq {
 STUB(launch_quantize_int4, const uint16_t*, int64_t, int64_t, uint8_t*, uint16_t*, uint16_t*, int32_t*, hipStream_t)
 STUB(launch_quantize_fp8, const uint16_t*, int64_t, int64_t, uint8_t*, float*, int32_t*, hipStream_t)
 STUB(launch_gemv_w4, const uint16_t*, int, int64_t, const uint8_t*, const uint16_t*, const uint16_t*, int64_t, void*,
-     bool, hipStream_t, const NormSrc*, bool)
+     bool, hipStream_t, const NormSrc*, bool, bool)
 STUB(launch_gemv_w8, const uint16_t*, int, int64_t, const uint8_t*, const float*, int64_t, void*, bool, hipStream_t)
 STUB(launch_gemm_f16, const uint16_t*, int, int64_t, const uint16_t*, int64_t, void*, bool, hipStream_t)
 STUB(launch_gemm_rows_f16, const uint16_t*, int, int64_t, const uint16_t*, int64_t, void*, bool, hipStream_t,

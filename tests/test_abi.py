@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
                           "sq_add_rmsnorm_f16", "sq_rope_kv_f16", "sq_attention_f16", "sq_silu_mul_f16",
                           "sq_spec_commit", "sq_spec_accept_multi", "sq_kv_adopt_f16", "sq_spec_commit_multi",
                           "sq_qgemv_w4a16_rmsnorm", "sq_verify_gemm_f16_rmsnorm", "sq_qgemv_w4a16_acc",
-                          "sq_verify_gemm_f16_acc"}
+                          "sq_verify_gemm_f16_acc", "sq_qgemv_w4a16_rmsnorm_silu"}
     assert set(names) == set(sq.EXPORTED)
     for n in names:
         assert hasattr(lib, n), n

@@ -75,6 +75,37 @@ def test_verify_gemm_f16_rmsnorm_equals_norm_then_gemm(n, k, m):
     assert torch.equal(bits(y), bits(ref))
 
 
+@pytest.mark.parametrize("n,k,m,group", [(37888, 3584, 1, 1), (37888, 3584, 2, 1), (37888, 3584, 1, 3),
+                                         (55296, 3584, 1, 1), (36864, 4096, 2, 1)])
+def test_qgemv_w4a16_rmsnorm_silu_equals_three_calls(n, k, m, group):
+    codes, scales, zeros = int4_weights(n, k, n + 2 * k)
+    h, nw = residual(m * group, k, n + 3)
+    t = torch.full((m, n // 2), float("nan"), dtype=torch.float16, device=DEV)
+    assert sq.sq_qgemv_w4a16_rmsnorm_silu(h, nw, EPS, codes, scales, zeros, t, group=group)
+    x = sq.sq_add_rmsnorm_f16(h.clone(), nw, EPS, group=group)
+    gu = sq.sq_qgemv_w4a16(x, codes, scales, zeros)
+    ref = sq.sq_silu_mul_f16(gu)
+    torch.cuda.synchronize()
+    assert torch.equal(bits(t), bits(ref))
+
+
+def test_silu_fusion_unsupported_shapes_enqueue_nothing():
+    codes, scales, zeros = int4_weights(4096, 3584, 11)  # 2048 gate rows: fewer tasks than wavefronts
+    h, nw = residual(1, 3584, 12)
+    t = torch.full((1, 2048), 7.0, dtype=torch.float16, device=DEV)
+    assert not sq.sq_qgemv_w4a16_rmsnorm_silu(h, nw, EPS, codes, scales, zeros, t)
+    c1, s1, z1 = int4_weights(17920, 1536, 15)  # rows of 1536 k: the plain projection takes the row blocks
+    h1, nw1 = residual(1, 1536, 16)
+    t1 = torch.full((1, 8960), 7.0, dtype=torch.float16, device=DEV)
+    assert not sq.sq_qgemv_w4a16_rmsnorm_silu(h1, nw1, EPS, c1, s1, z1, t1)
+    c2, s2, z2 = int4_weights(37888, 3584, 13)
+    h3, nw3 = residual(3, 3584, 14)
+    t3 = torch.full((3, 18944), 7.0, dtype=torch.float16, device=DEV)
+    assert not sq.sq_qgemv_w4a16_rmsnorm_silu(h3, nw3, EPS, c2, s2, z2, t3)  # m = 3
+    torch.cuda.synchronize()
+    assert (t == 7.0).all() and (t3 == 7.0).all() and (t1 == 7.0).all()
+
+
 def test_fused_norm_unsupported_shapes_enqueue_nothing():
     codes, scales, zeros = int4_weights(4608, 3584, 3)
     h, nw = residual(3, 3584, 4)
