@@ -23,6 +23,8 @@
  *   sq_add_rmsnorm_f16     residual add + RMS normalisation
  *   sq_rope_kv_f16         q|k|v bias + rotary embedding + cache write
  *   sq_attention_f16       causal grouped-query attention over the cache
+ *   sq_rope_attention_f16  the two above in one call (the chunk kernel rotates
+ *                          its own query rows and new cache entries)
  *   sq_silu_mul_f16        SiLU-gated product of the gate|up projection
  *   sq_qgemv_w4a16_rmsnorm, sq_verify_gemm_f16_rmsnorm
  *                          a projection of RMS-normalised rows of h (the norm
@@ -74,7 +76,7 @@
 extern "C" {
 #endif
 
-#define SQ_ABI_VERSION 6
+#define SQ_ABI_VERSION 7
 
 typedef enum sq_status {
   SQ_OK = 0,
@@ -298,6 +300,20 @@ sq_status sq_attention_f16(const uint16_t* q, const uint16_t* k_cache, const uin
                            int32_t rows_per_seq, int32_t hq, int32_t hkv, const int32_t* pos_base,
                            int32_t pos_offset, int64_t len_bound, int64_t capacity, uint16_t* out,
                            hipStream_t stream);
+
+/* sq_rope_kv_f16 followed by sq_attention_f16 of its q_out, in one call: the
+ * same out, the same cache entries and the same status, bit for bit.  The
+ * attention's chunk kernel rotates the block's query rows and new keys from
+ * qkv itself (the arithmetic of sq_rope_kv_f16), uses those new entries
+ * where a chunk holds the block's positions instead of reading them back, and
+ * writes them to the caches; no q_out is written.  Arguments and limits as the two calls;
+ * rows_per_seq <= 16 and rows_per_seq * hq / hkv <= 64 (other blocks return
+ * SQ_ERR_UNSUPPORTED and enqueue nothing).  The caches are read and written;
+ * out must not overlap them. */
+sq_status sq_rope_attention_f16(const float* qkv, const uint16_t* bias, int32_t b, int32_t rows_per_seq, int32_t hq,
+                                int32_t hkv, const int32_t* pos_base, int32_t pos_offset, int64_t len_bound,
+                                int64_t capacity, double theta, uint16_t* k_cache, uint16_t* v_cache, uint16_t* out,
+                                int32_t* status, hipStream_t stream);
 
 /* The projections of a decoder layer with the residual add and the RMS
  * normalisation folded in (one launch instead of two at every norm):

@@ -27,6 +27,7 @@ from ._lib import (  # noqa: F401
     sq_quantize_fp8_e4m3,
     sq_quantize_int4_g128,
     sq_probe_stream_read,
+    sq_rope_attention_f16,
     sq_rope_kv_f16,
     sq_silu_mul_f16,
     sq_spec_accept,

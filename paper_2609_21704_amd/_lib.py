@@ -58,6 +58,8 @@ def load() -> ctypes.CDLL:
             "sq_add_rmsnorm_f16": ([P, P, I64, I64, P, F, I32, P, P], S),
             "sq_rope_kv_f16": ([P, P, I32, I32, I32, I32, P, I32, I64, I64, ctypes.c_double, P, P, P, P, P], S),
             "sq_attention_f16": ([P, P, P, I32, I32, I32, I32, P, I32, I64, I64, P, P], S),
+            "sq_rope_attention_f16": ([P, P, I32, I32, I32, I32, P, I32, I64, I64, ctypes.c_double, P, P, P, P, P],
+                                      S),
             "sq_silu_mul_f16": ([P, I64, I64, P, P], S),
             "sq_qgemv_w4a16_rmsnorm": ([P, I32, P, F, I64, I64, P, P, P, I64, P, S, P], S),
             "sq_verify_gemm_f16_rmsnorm": ([P, I32, P, F, I64, I64, P, I64, P, S, P], S),
@@ -82,7 +84,8 @@ EXPORTED = ("sq_abi_version", "sq_status_str", "sq_quantize_int4_g128", "sq_quan
             "sq_spec_accept_noalloc", "sq_probe_stream_read", "sq_embed_block_f16", "sq_add_rmsnorm_f16",
             "sq_rope_kv_f16", "sq_attention_f16", "sq_silu_mul_f16", "sq_spec_commit", "sq_spec_accept_multi",
             "sq_kv_adopt_f16", "sq_spec_commit_multi", "sq_qgemv_w4a16_rmsnorm", "sq_verify_gemm_f16_rmsnorm",
-            "sq_qgemv_w4a16_acc", "sq_verify_gemm_f16_acc", "sq_qgemv_w4a16_rmsnorm_silu")
+            "sq_qgemv_w4a16_acc", "sq_verify_gemm_f16_acc", "sq_qgemv_w4a16_rmsnorm_silu",
+            "sq_rope_attention_f16")
 
 # device status bits (SQ_DEV_* of include/specquant.h)
 DEV_BAD_TOKEN, DEV_BAD_POS, DEV_OVERFLOW, DEV_NO_DIST = 1, 2, 4, 8
@@ -471,6 +474,28 @@ def sq_attention_f16(q, k_cache, v_cache, pos_base, pos_offset: int, rows_per_se
                                    int(pos_offset), int(len_bound), cap, _ptr(out), _stream(q.device)),
            "sq_attention_f16")
     return out
+
+
+def sq_rope_attention_f16(qkv, bias, pos_base, pos_offset: int, rows_per_seq: int, hq: int, k_cache, v_cache,
+                          out, len_bound: int | None = None, theta: float = 1e6, status=None) -> bool:
+    """sq_rope_kv_f16 then sq_attention_f16 in one call (no q_out), the same bits; False (nothing enqueued)
+    for blocks the fused kernel does not take."""
+    b, hkv, cap = _cache_dims(k_cache, v_cache)
+    m = b * rows_per_seq
+    nh = hq + 2 * hkv
+    len_bound = cap if len_bound is None else len_bound
+    _dev(qkv, bias, pos_base, k_cache, v_cache, out, status)
+    if qkv.dtype != torch.float32 or qkv.numel() != m * nh * HEAD_DIM:
+        raise ValueError("qkv must be float32 [m][(hq + 2 hkv) * 128]")
+    if bias is not None:
+        _expect(bias, torch.float16, (nh * HEAD_DIM,), "bias")
+    _expect(pos_base, torch.int32, (b,), "pos_base")
+    if out.dtype != torch.float16 or out.numel() != m * hq * HEAD_DIM:
+        raise ValueError("out must be float16 [m][hq][128]")
+    return _fused(load().sq_rope_attention_f16(_ptr(qkv), _ptr(bias), b, rows_per_seq, hq, hkv, _ptr(pos_base),
+                                               int(pos_offset), int(len_bound), cap, float(theta), _ptr(k_cache),
+                                               _ptr(v_cache), _ptr(out), _ptr(status), _stream(qkv.device)),
+                  "sq_rope_attention_f16")
 
 
 def sq_silu_mul_f16(gu, t=None):

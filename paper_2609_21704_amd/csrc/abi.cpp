@@ -495,6 +495,29 @@ sq_status sq_attention_f16(const uint16_t* q, const uint16_t* k_cache, const uin
                                             pos_offset, len_bound, out, stream));
 }
 
+sq_status sq_rope_attention_f16(const float* qkv, const uint16_t* bias, int32_t b, int32_t rows_per_seq, int32_t hq,
+                                int32_t hkv, const int32_t* pos_base, int32_t pos_offset, int64_t len_bound,
+                                int64_t capacity, double theta, uint16_t* k_cache, uint16_t* v_cache, uint16_t* out,
+                                int32_t* status, hipStream_t stream) {
+  if (!qkv || !pos_base || !k_cache || !v_cache || !out) return SQ_ERR_NULL;
+  const sq_status bs = check_block(b, rows_per_seq, hq, hkv, len_bound, capacity);
+  if (bs != SQ_OK) return bs;
+  if (!isfinite(theta)) return SQ_ERR_NONFINITE;
+  if (!(theta > 1.0)) return SQ_ERR_SHAPE;
+  if (!aligned(qkv, 16) || !aligned(bias, 16) || !aligned(pos_base, 4) || !aligned(k_cache, 16) ||
+      !aligned(v_cache, 16) || !aligned(out, 16) || !aligned(status, 4))
+    return SQ_ERR_ALIGN;
+  const size_t m = (size_t)b * rows_per_seq, nh = (size_t)hq + 2 * (size_t)hkv;
+  const size_t cache = (size_t)b * hkv * capacity * 128 * 2;
+  const Range outs[] = {{out, m * hq * 128 * 2}, {k_cache, cache}, {v_cache, cache}, {status, 4}};
+  const Range ins[] = {{qkv, m * nh * 128 * 4}, {bias, nh * 128 * 2}, {pos_base, (size_t)b * 4}};
+  if (any_alias(outs, ins)) return SQ_ERR_ALIAS;
+  if (rows_per_seq > 16 || rows_per_seq * (hq / hkv) > 64) return SQ_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
+  return fused_status(sq::launch_rope_attention(qkv, bias, b, rows_per_seq, hq, hkv, capacity, pos_base, pos_offset,
+                                                len_bound, theta, k_cache, v_cache, out, status, stream));
+}
+
 sq_status sq_silu_mul_f16(const float* gu, int64_t m, int64_t inter, uint16_t* t, hipStream_t stream) {
   if (!gu || !t) return SQ_ERR_NULL;
   if (m < 1 || inter < 1 || m > kMaxN || inter > kMaxN || m * inter >= (int64_t(1) << 40)) return SQ_ERR_SHAPE;

@@ -8,6 +8,8 @@
 //   attn_chunk_kernel   causal grouped-query attention over a slot of 64-position
 //                       chunks of the cache on the matrix cores (partial softmax)
 //   attn_merge_kernel   merge of the slots in slot order
+//   attn_chunk_lds_kernel<true>  the chunk kernel that also does rope_kv_kernel's
+//                       work for its block (one launch less per layer)
 //   silu_mul_kernel     t = f16(g / (1 + exp(-g)) * u)
 //   commit_kernel       emitted tokens, next pending token, position
 //   kv_adopt_kernel, commit_multi_kernel  the same with several draft chains per sequence
@@ -126,6 +128,26 @@ __global__ __launch_bounds__(256) void add_rmsnorm_kernel(float* __restrict__ h,
 }
 
 // ------------------------------------------------- bias + RoPE + cache write
+// The rotation shared by rope_kv_kernel and the attention that rotates its own
+// query rows and new cache entries (the same bits): pair (t, t + 64) of a head
+// turns by pos * theta^(-2t/128), the angle and its cosine and sine in fp64,
+// the turn itself in fp32 with every product rounded on its own.
+__device__ __forceinline__ double rope_freq(int t, double theta) {
+  return pow(theta, -2.0 * (double)t / (double)kHd);
+}
+
+__device__ __forceinline__ float2 rope_cos_sin(int64_t pos, double freq) {
+  double sn, cs;
+  sincos((double)pos * freq, &sn, &cs);
+  return make_float2((float)cs, (float)sn);
+}
+
+__device__ __forceinline__ void rope_turn(float a, float e, float2 cs, float& ra, float& re) {
+#pragma clang fp contract(off)
+  ra = a * cs.x - e * cs.y;
+  re = e * cs.x + a * cs.y;
+}
+
 // One wavefront per (row, head); lane t handles the pair (t, t + 64).
 __global__ __launch_bounds__(64) void rope_kv_kernel(const float* __restrict__ qkv, const uint16_t* __restrict__ bias,
                                                      int hq, int hkv, int rps, const int32_t* __restrict__ pos_base,
@@ -147,7 +169,7 @@ __global__ __launch_bounds__(64) void rope_kv_kernel(const float* __restrict__ q
     be = f16_bits_to_f32(bias[hh * kHd + t + 64]);
   }
   const bool rot = hh < hq + hkv;
-  const double freq = rot ? pow(theta, -2.0 * (double)t / (double)kHd) : 0.0;
+  const double freq = rot ? rope_freq(t, theta) : 0.0;
   if (pos < 0 || pos >= len_bound) {
     if (hh < hq) {
       q_out[((int64_t)r * hq + hh) * kHd + t] = kNanF16;
@@ -161,12 +183,8 @@ __global__ __launch_bounds__(64) void rope_kv_kernel(const float* __restrict__ q
     e += be;
   }
   if (rot) {
-    // angle pos * theta^(-2t/128) and its cosine and sine in fp64, the turn in fp32
-    const double ang = (double)pos * freq;
-    double sn, cs;
-    sincos(ang, &sn, &cs);
-    const float c = (float)cs, sv = (float)sn;
-    const float ra = a * c - e * sv, re = e * c + a * sv;
+    float ra, re;
+    rope_turn(a, e, rope_cos_sin(pos, freq), ra, re);
     uint16_t* dst = hh < hq ? q_out + ((int64_t)r * hq + hh) * kHd
                             : kc + (((int64_t)bi * hkv + (hh - hq)) * capacity + pos) * kHd;
     dst[t] = f32_to_f16_bits(ra);
@@ -433,12 +451,44 @@ constexpr int kLdsChunk = 64 * kLdsKeyStride + kHd * kLdsValStride;  // halves p
 constexpr int kLdsThreads = 256;
 constexpr int kLdsCells = 2 * kChunk * kHd * 2 / 16 / kLdsThreads;  // 16-byte cells per thread and chunk: 8
 
+// The attention that also does rope_kv_kernel's work for its block: the
+// sources of the rotation (the q|k|v projection rows) and where the new keys
+// and values go.  At most 64 query rows per (sequence, kv head) and 16 rows
+// per sequence.
+struct RopeSrc {
+  const float* qkv;      // [b rps][(hq + 2 hkv) * 128] fp32
+  const uint16_t* bias;  // [(hq + 2 hkv) * 128] fp16, or null
+  double theta;
+  int64_t len_bound;
+  uint16_t* kc;  // the caches, written at the block's valid positions
+  uint16_t* vc;
+  int32_t* status;
+};
+constexpr int kRopeMaxRows = 16;
+// rotation items (row-head, four pairs) per thread: (64 query rows + 2 * 16) * 16 / 256
+constexpr int kRopeItems = (64 + 2 * kRopeMaxRows) * 16 / kLdsThreads;
+
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+}
+
+// With ROPE, the workgroup first rotates its block's query rows (into LDS
+// buffer 1, which holds no chunk until the second one is staged) and the new
+// keys and values of kv head g (into LDS after the two buffers) with
+// rope_kv_kernel's arithmetic, from q|k|v rows it loads before the positions
+// arrive; the cosines and sines of (row, pair) are computed once, into buffer
+// 1.  The workgroup whose slot holds a valid position of the block writes its
+// new key and value to the caches (once each), and a staged chunk that holds
+// such positions gets their new entries patched over the stale cells it read.
+// Without ROPE, q is read as rope_kv_kernel wrote it.
+template <bool ROPE>
 __global__ __launch_bounds__(kLdsThreads) __attribute__((amdgpu_waves_per_eu(2))) void attn_chunk_lds_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, int hq, int hkv,
     int rps, int64_t capacity, const int32_t* __restrict__ pos_base, int pos_offset, int nslots, int span, int nq_pad,
-    float* __restrict__ part_o, float2* __restrict__ part_ml) {
+    float* __restrict__ part_o, float2* __restrict__ part_ml, RopeSrc rs) {
   extern __shared__ __align__(16) char smem[];
-  half_t* lbuf = reinterpret_cast<half_t*>(smem);  // [2][kLdsChunk]
+  half_t* lbuf = reinterpret_cast<half_t*>(smem);  // [2][kLdsChunk], then (ROPE) new keys and values [2][rps][128]
   const int slot = blockIdx.x;
   const int bg = blockIdx.y;  // bi * hkv + g
   const int bi = bg / hkv, g = bg - bi * hkv;
@@ -463,6 +513,118 @@ __global__ __launch_bounds__(kLdsThreads) __attribute__((amdgpu_waves_per_eu(2))
       }
     }
   };
+
+  load_chunk(slot0);  // before the positions arrive: the slot's first chunk lies in the cache
+  // ROPE: item idx = tid + 256 it is row-head r = idx / 16 (query rows qi < nq
+  // of kv head g, then row j's key, then row j's value) and pairs 4 (idx % 16)
+  // .. +4; its q|k|v sources do not depend on the positions
+  const int nh = hq + 2 * hkv;
+  const int nitems = ROPE ? (a.nq + 2 * rps) * 16 : 0;
+  float4_t ulo[ROPE ? kRopeItems : 1], uhi[ROPE ? kRopeItems : 1];
+  half4_t blo[ROPE ? kRopeItems : 1], bhi[ROPE ? kRopeItems : 1];
+  auto item = [&](int idx, int& j, int& head, int& kind) {  // kind 0 query, 1 key, 2 value
+    const int r = idx >> 4;
+    if (r < a.nq) {
+      j = r / a.G;
+      head = g * a.G + (r - j * a.G);
+      kind = 0;
+    } else if (r < a.nq + rps) {
+      j = r - a.nq;
+      head = hq + g;
+      kind = 1;
+    } else {
+      j = r - a.nq - rps;
+      head = hq + hkv + g;
+      kind = 2;
+    }
+  };
+  if constexpr (ROPE) {
+#pragma unroll
+    for (int it = 0; it < kRopeItems; ++it) {
+      const int idx = tid + kLdsThreads * it;
+      if (idx < nitems) {
+        int j, head, kind;
+        item(idx, j, head, kind);
+        const float* src = rs.qkv + ((int64_t)(bi * rps + j) * nh + head) * kHd + 4 * (idx & 15);
+        ulo[it] = *reinterpret_cast<const float4_t*>(src);
+        uhi[it] = *reinterpret_cast<const float4_t*>(src + 64);
+        if (rs.bias) {
+          const uint16_t* bp = rs.bias + head * kHd + 4 * (idx & 15);
+          blo[it] = *reinterpret_cast<const half4_t*>(bp);
+          bhi[it] = *reinterpret_cast<const half4_t*>(bp + 64);
+        }
+      }
+    }
+  }
+  const int64_t p0 = (int64_t)pos_base[bi] + pos_offset;
+  // the pair of every table entry this thread fills is tid % 64 (256 threads a row step)
+  const double freq = ROPE ? rope_freq(tid & 63, rs.theta) : 0.0;
+  const int64_t pmax = p0 + rps - 1;
+  if constexpr (ROPE) {
+    if (slot == 0 && g == 0 && tid < rps && (p0 + tid < 0 || p0 + tid >= rs.len_bound)) flag(rs.status, kBadPos);
+  }
+  if (slot0 > pmax) return;  // uniform across the workgroup: no row reads this slot
+  const int64_t klast = pmax < capacity - 1 ? pmax : capacity - 1;  // rows past the cache read none of it
+  const int64_t nt64 = (klast - slot0) / kChunk + 1;
+  const int nt = nt64 < span ? (int)nt64 : span;  // chunks of the slot with a key at or before pmax
+  const bool owner = wave < nqt;
+  half8_t qf[4];
+  half_t* newkv = lbuf + 2 * kLdsChunk;  // [2][rps][128]: the block's keys, then its values
+  // a valid position of the block, in this slot: its new entry goes to the caches from here
+  auto store_kv = [&](int64_t pos) {
+    return pos >= 0 && pos < rs.len_bound && pos >= slot0 && pos < slot0 + (int64_t)span * kChunk;
+  };
+  if constexpr (ROPE) {
+    half_t* qb = lbuf + kLdsChunk;                        // [nq][128] rotated query rows
+    float2* tab = reinterpret_cast<float2*>(qb + 64 * kHd);  // [rps][64] cosine, sine of (row, pair)
+    for (int e = tid; e < rps * 64; e += kLdsThreads) tab[e] = rope_cos_sin(p0 + (e >> 6), freq);
+    lds_barrier();
+#pragma unroll
+    for (int it = 0; it < kRopeItems; ++it) {
+      const int idx = tid + kLdsThreads * it;
+      if (idx < nitems) {
+        int j, head, kind;
+        item(idx, j, head, kind);
+        const int t0 = 4 * (idx & 15);
+        half4_t lo, hi;
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          float u = ulo[it][x], v = uhi[it][x];
+          if (rs.bias) {
+            u += (float)blo[it][x];
+            v += (float)bhi[it][x];
+          }
+          if (kind < 2) rope_turn(u, v, tab[j * 64 + t0 + x], u, v);
+          const half_t hu = (half_t)u, hv = (half_t)v;  // scalar copies: vector element lvalues are
+          lo[x] = hu;                                   // misread by bit_cast
+          hi[x] = hv;
+          if (kind == 2 && store_kv(p0 + j)) {
+            uint16_t* vo = rs.vc + ((int64_t)bg * kHd + t0 + x) * capacity + p0 + j;
+            vo[0] = __builtin_bit_cast(uint16_t, hu);
+            vo[(int64_t)64 * capacity] = __builtin_bit_cast(uint16_t, hv);
+          }
+        }
+        half_t* dst = kind == 0 ? qb + (idx >> 4) * kHd : newkv + ((kind - 1) * rps + j) * kHd;
+        *reinterpret_cast<half4_t*>(dst + t0) = lo;
+        *reinterpret_cast<half4_t*>(dst + t0 + 64) = hi;
+        if (kind == 1 && store_kv(p0 + j)) {
+          uint16_t* ko = rs.kc + ((int64_t)bg * capacity + p0 + j) * kHd + t0;
+          *reinterpret_cast<half4_t*>(ko) = lo;
+          *reinterpret_cast<half4_t*>(ko + 64) = hi;
+        }
+      }
+    }
+    lds_barrier();
+    if (owner) {
+      const half8_t zero8 = {0, 0, 0, 0, 0, 0, 0, 0};
+      const int qi = 16 * wave + li;
+#pragma unroll
+      for (int s4 = 0; s4 < 4; ++s4)
+        qf[s4] = qi < a.nq ? *reinterpret_cast<const half8_t*>(qb + qi * kHd + 32 * lg + 8 * s4) : zero8;
+    }
+  } else {
+    if (owner) attn_load_q(q, a, bi, g, wave, li, lg, qf);
+  }
   auto store_chunk = [&](half_t* b) {
 #pragma unroll
     for (int i = 0; i < kLdsCells; ++i) {
@@ -475,18 +637,32 @@ __global__ __launch_bounds__(kLdsThreads) __attribute__((amdgpu_waves_per_eu(2))
       }
     }
   };
-
-  load_chunk(slot0);  // before the positions arrive: the slot's first chunk lies in the cache
-  const int64_t p0 = (int64_t)pos_base[bi] + pos_offset;
-  const int64_t pmax = p0 + rps - 1;
-  if (slot0 > pmax) return;  // uniform across the workgroup: no row reads this slot
-  const int64_t klast = pmax < capacity - 1 ? pmax : capacity - 1;  // rows past the cache read none of it
-  const int64_t nt64 = (klast - slot0) / kChunk + 1;
-  const int nt = nt64 < span ? (int)nt64 : span;  // chunks of the slot with a key at or before pmax
-  const bool owner = wave < nqt;
-  half8_t qf[4];
-  if (owner) attn_load_q(q, a, bi, g, wave, li, lg, qf);
+  // ROPE: a staged chunk that holds valid positions of the block gets their
+  // new entries over the stale ones read from the cache (after a barrier, so
+  // that every plain cell is written first; a short rolled loop, off the
+  // common path)
+  auto patch_chunk = [&](half_t* b, int64_t key0) {
+    if (!(ROPE && key0 + kChunk - 1 >= p0 && key0 <= pmax)) return;  // uniform
+    lds_barrier();
+#pragma unroll 1
+    for (int e = tid; e < rps * (16 + kHd); e += kLdsThreads) {
+      const bool key = e < rps * 16;
+      const int j = key ? e >> 4 : (e - rps * 16) >> 7;
+      const int64_t pos = p0 + j;
+      if (pos < key0 || pos >= key0 + kChunk || pos < 0 || pos >= rs.len_bound) continue;
+      const int r = (int)(pos - key0);
+      if (key) {
+        const int part = e & 15;
+        *reinterpret_cast<u32x4*>(b + r * kLdsKeyStride + part * 8) =
+            *reinterpret_cast<const u32x4*>(newkv + j * kHd + part * 8);
+      } else {
+        const int dv = (e - rps * 16) & (kHd - 1);
+        b[64 * kLdsKeyStride + dv * kLdsValStride + r] = newkv[(rps + j) * kHd + dv];
+      }
+    }
+  };
   store_chunk(lbuf);
+  patch_chunk(lbuf, slot0);
   float m = -__builtin_inff(), l = 0.f;
   float4_t o[8];
 #pragma unroll
@@ -495,8 +671,7 @@ __global__ __launch_bounds__(kLdsThreads) __attribute__((amdgpu_waves_per_eu(2))
     const int64_t key0 = slot0 + (int64_t)t * kChunk;
     if (t + 1 < nt) load_chunk(key0 + kChunk);
     // the LDS writes of buffer t % 2 are done; the next chunk's loads stay in flight
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    __builtin_amdgcn_s_barrier();
+    lds_barrier();
     const half_t* b = lbuf + (t & 1) * kLdsChunk;
     if (owner) {
       const bool tail = key0 + kChunk - 1 > pmax;  // values of keys after pmax are zeroed (stale entries)
@@ -519,7 +694,10 @@ __global__ __launch_bounds__(kLdsThreads) __attribute__((amdgpu_waves_per_eu(2))
       attn_update_src(a, p0, wave, li, lg, qf, kfrag, vfrag, key0, m, l, o);
     }
     // buffer (t + 1) % 2 was last read before this chunk's barrier
-    if (t + 1 < nt) store_chunk(lbuf + ((t + 1) & 1) * kLdsChunk);
+    if (t + 1 < nt) {
+      store_chunk(lbuf + ((t + 1) & 1) * kLdsChunk);
+      patch_chunk(lbuf + ((t + 1) & 1) * kLdsChunk, key0 + kChunk);
+    }
   }
   if (!owner) return;
   float* po = part_o + ((int64_t)bg * nslots + slot) * nq_pad * kHd;
@@ -792,14 +970,37 @@ hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_
   if ((nqt >= 2 && nqt <= 4) || (nqt == 1 && span >= 2)) {
     // chunks through LDS: loaded once for the block's tiles, the next one in flight
     const size_t lds = (size_t)2 * kLdsChunk * sizeof(uint16_t);
-    hipLaunchKernelGGL(attn_chunk_lds_kernel, dim3((unsigned)nslots, (unsigned)(b * hkv)), dim3(kLdsThreads), lds,
-                       stream, q, kc, vc, hq, hkv, rps, capacity, pos_base, pos_offset, nslots, span, nq_pad, part_o,
-                       part_ml);
+    hipLaunchKernelGGL(attn_chunk_lds_kernel<false>, dim3((unsigned)nslots, (unsigned)(b * hkv)), dim3(kLdsThreads),
+                       lds, stream, q, kc, vc, hq, hkv, rps, capacity, pos_base, pos_offset, nslots, span, nq_pad,
+                       part_o, part_ml, RopeSrc{});
   } else {
     const int waves = nqt < 4 ? nqt : 4;  // one query tile per wavefront (16 rows each), at most 4
     hipLaunchKernelGGL(attn_chunk_kernel, dim3((unsigned)nslots, (unsigned)(b * hkv)), dim3(64 * waves), 0, stream, q,
                        kc, vc, hq, hkv, rps, capacity, pos_base, pos_offset, nslots, span, nq_pad, part_o, part_ml);
   }
+  hipLaunchKernelGGL(attn_merge_kernel, dim3((unsigned)(b * rps), (unsigned)hq), dim3(64), 0, stream, part_o,
+                     part_ml, hq, hkv, rps, nslots, span, nq_pad, pos_base, pos_offset, len_bound, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_attention(const float* qkv, const uint16_t* bias, int b, int rps, int hq, int hkv,
+                                 int64_t capacity, const int32_t* pos_base, int pos_offset, int64_t len_bound,
+                                 double theta, uint16_t* kc, uint16_t* vc, uint16_t* out, int32_t* status,
+                                 hipStream_t stream) {
+  if (rps > kRopeMaxRows || rps * (hq / hkv) > 64) return hipErrorNotSupported;
+  const int span = attention_span(b, hq, hkv, rps, len_bound);
+  const int nslots = (int)(((len_bound + kChunk - 1) / kChunk + span - 1) / span);
+  const int nq_pad = (rps * (hq / hkv) + 15) / 16 * 16;
+  void* ws = nullptr;
+  const hipError_t e = workspace(attention_workspace_bytes(b, hq, hkv, rps, len_bound), stream, &ws);
+  if (e != hipSuccess) return e;
+  float* part_o = static_cast<float*>(ws);
+  float2* part_ml = reinterpret_cast<float2*>(part_o + (size_t)b * hkv * nslots * nq_pad * kHd);
+  const size_t lds = ((size_t)2 * kLdsChunk + (size_t)2 * rps * kHd) * sizeof(uint16_t);
+  const RopeSrc rs{qkv, bias, theta, len_bound, kc, vc, status};
+  hipLaunchKernelGGL(attn_chunk_lds_kernel<true>, dim3((unsigned)nslots, (unsigned)(b * hkv)), dim3(kLdsThreads), lds,
+                     stream, nullptr, kc, vc, hq, hkv, rps, capacity, pos_base, pos_offset, nslots, span, nq_pad,
+                     part_o, part_ml, rs);
   hipLaunchKernelGGL(attn_merge_kernel, dim3((unsigned)(b * rps), (unsigned)hq), dim3(64), 0, stream, part_o,
                      part_ml, hq, hkv, rps, nslots, span, nq_pad, pos_base, pos_offset, len_bound, out);
   return hipGetLastError();

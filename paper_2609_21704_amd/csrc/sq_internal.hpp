@@ -109,6 +109,13 @@ size_t attention_workspace_bytes(int b, int hq, int hkv, int rps, int64_t len_bo
 hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, int b, int rps, int hq,
                             int hkv, int64_t capacity, const int32_t* pos_base, int pos_offset, int64_t len_bound,
                             uint16_t* out, hipStream_t stream);
+// launch_rope_kv (without q_out) + launch_attention in one chunk kernel and the
+// merge, the same bits; hipErrorNotSupported (nothing enqueued) for blocks of
+// more than 16 rows per sequence or 64 query rows per kv head.
+hipError_t launch_rope_attention(const float* qkv, const uint16_t* bias, int b, int rps, int hq, int hkv,
+                                 int64_t capacity, const int32_t* pos_base, int pos_offset, int64_t len_bound,
+                                 double theta, uint16_t* kc, uint16_t* vc, uint16_t* out, int32_t* status,
+                                 hipStream_t stream);
 hipError_t launch_silu_mul(const float* gu, int64_t m, int64_t inter, uint16_t* t, hipStream_t stream);
 hipError_t launch_spec_commit(const int32_t* n_accepted, const int32_t* next_token, const int32_t* drafts, int b,
                               int kd, int32_t* pending, int32_t* prev, int32_t* pos_base, int32_t* out_tokens,

@@ -228,13 +228,17 @@ class SpecDecoder:
         delta = None  # a projection output not yet added into h
         for l in range(w.layers):
             self._norm_linear(draft, (l, "qkv"), h, w.in_norm[l], delta, x, qkv)
-            sq.sq_rope_kv_f16(qkv, w.qkv_bias[l], self.pos_base, offset, rps, cfg.q_heads, cache.k[l], cache.v[l],
-                              len_bound=lb, theta=THETA, q_out=q, status=self.status)
-            if self.attn_hook:
-                self.attn_hook(True, rps, offset)
-            sq.sq_attention_f16(q, cache.k[l], cache.v[l], self.pos_base, offset, rps, len_bound=lb, out=a)
-            if self.attn_hook:
-                self.attn_hook(False, rps, offset)
+            if not (self.fuse and self.attn_hook is None and
+                    sq.sq_rope_attention_f16(qkv, w.qkv_bias[l], self.pos_base, offset, rps, cfg.q_heads,
+                                             cache.k[l], cache.v[l], a, len_bound=lb, theta=THETA,
+                                             status=self.status)):
+                sq.sq_rope_kv_f16(qkv, w.qkv_bias[l], self.pos_base, offset, rps, cfg.q_heads, cache.k[l],
+                                  cache.v[l], len_bound=lb, theta=THETA, q_out=q, status=self.status)
+                if self.attn_hook:
+                    self.attn_hook(True, rps, offset)
+                sq.sq_attention_f16(q, cache.k[l], cache.v[l], self.pos_base, offset, rps, len_bound=lb, out=a)
+                if self.attn_hook:
+                    self.attn_hook(False, rps, offset)
             delta = self._residual_linear(draft, (l, "o"), a.view(M, cfg.q_dim), h, y)
             if not (draft and delta is None and self.fuse and
                     w.stack.draft_gemv_rmsnorm_silu((l, "gate_up"), h, w.post_norm[l], EPS, t)):

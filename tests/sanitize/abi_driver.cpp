@@ -94,6 +94,16 @@ int main() {
   EXPECT(sq_verify_gemm_f16_acc(at<uint16_t>(A), 5, 18944, at<uint16_t>(B), 3584, at<float>(E), s), SQ_OK);
   EXPECT(sq_verify_gemm_f16_acc(at<uint16_t>(A), 5, 18944, at<uint16_t>(B), 3584, at<float>(E + 2), s),
          SQ_ERR_ALIGN);
+  // bias + rotation + attention in one call
+  EXPECT(sq_rope_attention_f16(at<float>(A), at<uint16_t>(B), 1, 5, 28, 4, at<int32_t>(C), 0, 2048, 2048, 1e6,
+                               at<uint16_t>(D), at<uint16_t>(D + (1ull << 24)), at<uint16_t>(E), nullptr, s),
+         SQ_OK);
+  EXPECT(sq_rope_attention_f16(at<float>(A), at<uint16_t>(B), 1, 10, 28, 4, at<int32_t>(C), 0, 2048, 2048, 1e6,
+                               at<uint16_t>(D), at<uint16_t>(D + (1ull << 24)), at<uint16_t>(E), nullptr, s),
+         SQ_ERR_UNSUPPORTED);
+  EXPECT(sq_rope_attention_f16(at<float>(A), at<uint16_t>(B), 1, 5, 28, 4, at<int32_t>(C), 0, 2048, 2048, 1e6,
+                               at<uint16_t>(D), at<uint16_t>(D + 4096), at<uint16_t>(E), nullptr, s),
+         SQ_ERR_ALIAS);
   // accept, and its allocation-free twin
   float nan = std::nanf("");
   EXPECT(sq_spec_accept(at<float>(A), at<float>(B), at<int32_t>(C), at<uint32_t>(D), 1, 4, 100, nan, at<int32_t>(E),

@@ -78,6 +78,8 @@ STUB(launch_rope_kv, const float*, const uint16_t*, int, int, int, int, const in
      uint16_t*, uint16_t*, uint16_t*, int32_t*, hipStream_t)
 STUB(launch_attention, const uint16_t*, const uint16_t*, const uint16_t*, int, int, int, int, int64_t, const int32_t*,
      int, int64_t, uint16_t*, hipStream_t)
+STUB(launch_rope_attention, const float*, const uint16_t*, int, int, int, int, int64_t, const int32_t*, int, int64_t,
+     double, uint16_t*, uint16_t*, uint16_t*, int32_t*, hipStream_t)
 STUB(launch_silu_mul, const float*, int64_t, int64_t, uint16_t*, hipStream_t)
 STUB(launch_spec_commit, const int32_t*, const int32_t*, const int32_t*, int, int, int32_t*, int32_t*, int32_t*,
      int32_t*, int64_t, int32_t*, int32_t*, hipStream_t)

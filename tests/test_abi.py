@@ -35,11 +35,11 @@ def test_library_exports_every_declared_symbol():
                           "sq_add_rmsnorm_f16", "sq_rope_kv_f16", "sq_attention_f16", "sq_silu_mul_f16",
                           "sq_spec_commit", "sq_spec_accept_multi", "sq_kv_adopt_f16", "sq_spec_commit_multi",
                           "sq_qgemv_w4a16_rmsnorm", "sq_verify_gemm_f16_rmsnorm", "sq_qgemv_w4a16_acc",
-                          "sq_verify_gemm_f16_acc", "sq_qgemv_w4a16_rmsnorm_silu"}
+                          "sq_verify_gemm_f16_acc", "sq_qgemv_w4a16_rmsnorm_silu", "sq_rope_attention_f16"}
     assert set(names) == set(sq.EXPORTED)
     for n in names:
         assert hasattr(lib, n), n
-    assert sq.sq_abi_version() == 6
+    assert sq.sq_abi_version() == 7
     for s in range(9):
         assert lib.sq_status_str(s).startswith(b"SQ_")
     assert lib.sq_status_str(9) == b"unknown sq_status"
@@ -217,6 +217,20 @@ def test_decoder_layer_validation():
     assert call(pos=B + 2) == ALIGN
     assert call(q=D + 4096) == ALIAS                   # q_out inside the key cache
     assert call(vc=D + 64) == ALIAS                    # the two caches overlap
+    ra = lib.sq_rope_attention_f16
+
+    def fused(**kw):
+        a = dict(args, **kw)
+        return ra(a["qkv"], a["bias"], a["b"], a["rps"], a["hq"], a["hkv"], a["pos"], a["off"], a["lb"], a["cap"],
+                  a["theta"], a["kc"], a["vc"], a["q"], a["st"], None)
+    assert fused(q=None) == NULL                       # out
+    assert fused(cap=1000, lb=1000) == SHAPE
+    assert fused(theta=float("nan")) == NONFINITE
+    assert fused(q=C + 2) == ALIGN
+    assert fused(q=D + 4096) == ALIAS                  # out inside the key cache
+    assert fused(qkv=E + 64) == ALIAS                  # the projection rows inside the value cache
+    assert fused(rps=17, hq=8, hkv=8) == UNSUPPORTED   # more than 16 rows per sequence
+    assert fused(rps=10) == UNSUPPORTED                # 70 query rows per kv head
     att = lib.sq_attention_f16
     assert att(A, None, E, 1, 5, 28, 4, B, 0, 1024, 1024, C, None) == NULL
     assert att(A, D, E, 1, 5, 28, 4, B, 0, 1024, 1000, C, None) == SHAPE

@@ -3,8 +3,11 @@ normalises its own input rows (sq_qgemv_w4a16_rmsnorm,
 sq_verify_gemm_f16_rmsnorm) must give the bits of sq_add_rmsnorm_f16
 followed by the plain projection, and a projection added into the residual
 stream (sq_qgemv_w4a16_acc, sq_verify_gemm_f16_acc) the bits of the plain
-projection followed by one fp32 add; shapes without a fused kernel return
-False and leave the output untouched.  Rounds through the decoder with and
+projection followed by one fp32 add, the gate|up projection with the SiLU
+product in its epilogue the bits of the three calls, and the attention that
+rotates its own rows (sq_rope_attention_f16) the bits of sq_rope_kv_f16 +
+sq_attention_f16 (output, both caches, status); shapes without a fused
+kernel return False and leave the output untouched.  Rounds through the decoder with and
 without the fused forms are then equal bit for bit (tokens, positions,
 caches, logits).  The unfused calls are themselves checked against the
 oracle in test_gpu_decoder.py and test_gpu_parity.py."""
@@ -176,3 +179,56 @@ def test_fused_rounds_equal_unfused_rounds(ci, layers, B, k, chains):
     for a, b, what in zip(runs[0], runs[1], ("tokens", "positions", "target logits", "draft logits", "parent keys",
                                               "parent values", "draft keys", "draft values")):
         assert torch.equal(bits(a) if a.is_floating_point() else a, bits(b) if b.is_floating_point() else b), what
+
+
+def rope_block(b, rps, hq, hkv, cap, pb, seed, with_bias=True):
+    """Projection rows, bias and caches full of finite stale entries."""
+    g = gen(seed)
+    nh = hq + 2 * hkv
+    qkv = (torch.randn((b * rps, nh * 128), generator=g) * 2).float().to(DEV)
+    bias = (torch.randn((nh * 128,), generator=g) * 0.5).half().to(DEV) if with_bias else None
+    kc = (torch.randn((b, hkv, cap, 128), generator=g)).half().to(DEV)
+    vc = (torch.randn((b, hkv, 128, cap), generator=g)).half().to(DEV)
+    return qkv, bias, kc, vc, torch.tensor(pb, dtype=torch.int32, device=DEV)
+
+
+# (b, rps, hq, hkv, capacity, len_bound, pos_base, offset, bias): the 7B draft
+# step and verification block (a block across a chunk boundary), four
+# sequences of 9 rows (four query tiles), a long cache (slots of several
+# chunks), the 1.5B heads without bias, one query head per kv head with 16
+# rows from position 0, and rows before 0 and past len_bound
+ROPE_ATT = [(1, 1, 28, 4, 2048, 2048, [1100], 0, True),
+            (1, 5, 28, 4, 2048, 2048, [1020], 2, True),
+            (4, 9, 28, 4, 4096, 4096, [100, 1000, 2040, 4000], 0, True),
+            (4, 9, 28, 4, 8192, 8192, [8000, 7000, 64, 8180], 1, True),
+            (2, 5, 12, 2, 1024, 1024, [511, 0], 0, False),
+            (1, 16, 8, 8, 512, 512, [0], 0, True),
+            (3, 5, 28, 4, 1024, 900, [-3, 897, 60], 0, True)]
+
+
+@pytest.mark.parametrize("b,rps,hq,hkv,cap,lb,pb,off,with_bias", ROPE_ATT)
+def test_rope_attention_equals_rope_then_attention(b, rps, hq, hkv, cap, lb, pb, off, with_bias):
+    qkv, bias, kc, vc, pbt = rope_block(b, rps, hq, hkv, cap, pb, 500 + rps + cap, with_bias)
+    k1, v1, k2, v2 = kc.clone(), vc.clone(), kc.clone(), vc.clone()
+    s1 = torch.zeros(1, dtype=torch.int32, device=DEV)
+    s2 = torch.zeros(1, dtype=torch.int32, device=DEV)
+    q = sq.sq_rope_kv_f16(qkv, bias, pbt, off, rps, hq, k1, v1, len_bound=lb, theta=1e6, status=s1)
+    out1 = sq.sq_attention_f16(q, k1, v1, pbt, off, rps, len_bound=lb)
+    out2 = torch.full_like(out1, 7.0)
+    assert sq.sq_rope_attention_f16(qkv, bias, pbt, off, rps, hq, k2, v2, out2, len_bound=lb, theta=1e6, status=s2)
+    torch.cuda.synchronize()
+    assert torch.equal(bits(out1), bits(out2))
+    assert torch.equal(bits(k1), bits(k2)) and torch.equal(bits(v1), bits(v2))
+    assert int(s1.item()) == int(s2.item())
+    bad = any(p + off + j < 0 or p + off + j >= lb for p in pb for j in range(rps))
+    assert (int(s2.item()) != 0) == bad
+
+
+def test_rope_attention_unsupported_blocks_enqueue_nothing():
+    for b, rps, hq, hkv in ((1, 17, 8, 8), (1, 10, 28, 4)):
+        qkv, bias, kc, vc, pbt = rope_block(b, rps, hq, hkv, 1024, [100] * b, 77)
+        k0, v0 = kc.clone(), vc.clone()
+        out = torch.full((b * rps, hq, 128), 3.0, dtype=torch.float16, device=DEV)
+        assert not sq.sq_rope_attention_f16(qkv, bias, pbt, 0, rps, hq, kc, vc, out)
+        torch.cuda.synchronize()
+        assert torch.equal(kc, k0) and torch.equal(vc, v0) and bool((out == 3.0).all())
