@@ -688,8 +688,8 @@ def measure_attention_long(dev, context: int = 8192, batch: int = 4, rows: int =
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20, help="timed rounds")
-    ap.add_argument("--warmup", type=int, default=3, help="untimed rounds")
+    ap.add_argument("--steps", type=int, default=200, help="timed rounds")
+    ap.add_argument("--warmup", type=int, default=20, help="untimed rounds")
     ap.add_argument("--config", type=int, default=2, help="workload index (2 = Qwen2.5-7B-shaped, INT4, k=4)")
     ap.add_argument("--temperature", type=float, default=1.0)
     ap.add_argument("--gemv-steps", type=int, default=2, help="draft passes timed per launch for the roofline")
