@@ -241,7 +241,7 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(const float* __restric
   int invalid = 0;
   for (int rr = threadIdx.x; rr < 2 * kd + 1; rr += kThreads) invalid |= isnan(sS[rr]) ? 1 : 0;
   invalid = __syncthreads_or(invalid);
-  if (threadIdx.x < kd && !invalid) {
+  if ((int)threadIdx.x < kd && !invalid) {
     const int i = threadIdx.x;
     const int32_t xt = tokens[(int64_t)i * b + s];
     int acc = 0;

@@ -1,7 +1,6 @@
 """CPU-only checks of the C ABI: the built library loads, exports every symbol
 the header declares, and rejects invalid arguments on the host before any HIP
 call (fake, never dereferenced device addresses are passed)."""
-import ctypes
 import os
 import re
 

@@ -4,7 +4,6 @@ sq_spec_accept: two calls in a row, the second smaller, in every mode
 results bit for bit equal, and checked against the oracle on the kernel's own
 distributions.  Then the call captured in a HIP graph: every replay, with
 eager work and synchronisations in between, gives the eager results."""
-import numpy as np
 import pytest
 import torch
 
