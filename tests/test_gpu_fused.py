@@ -196,14 +196,18 @@ def rope_block(b, rps, hq, hkv, cap, pb, seed, with_bias=True):
 # step and verification block (a block across a chunk boundary), four
 # sequences of 9 rows (four query tiles), a long cache (slots of several
 # chunks), the 1.5B heads without bias, one query head per kv head with 16
-# rows from position 0, and rows before 0 and past len_bound
+# rows from position 0, rows before 0 and past len_bound (a sequence with
+# every row before 0 among them), and one query tile over 64 slots
 ROPE_ATT = [(1, 1, 28, 4, 2048, 2048, [1100], 0, True),
             (1, 5, 28, 4, 2048, 2048, [1020], 2, True),
             (4, 9, 28, 4, 4096, 4096, [100, 1000, 2040, 4000], 0, True),
             (4, 9, 28, 4, 8192, 8192, [8000, 7000, 64, 8180], 1, True),
             (2, 5, 12, 2, 1024, 1024, [511, 0], 0, False),
             (1, 16, 8, 8, 512, 512, [0], 0, True),
-            (3, 5, 28, 4, 1024, 900, [-3, 897, 60], 0, True)]
+            (3, 5, 28, 4, 1024, 900, [-3, 897, 60], 0, True),
+            (2, 1, 28, 4, 1024, 900, [-5, 100], 0, True),
+            (1, 2, 14, 2, 1024, 512, [511], 0, True),
+            (1, 1, 28, 4, 4096, 4096, [3000], 0, True)]
 
 
 @pytest.mark.parametrize("b,rps,hq,hkv,cap,lb,pb,off,with_bias", ROPE_ATT)
