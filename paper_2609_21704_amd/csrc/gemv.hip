@@ -95,6 +95,16 @@ __device__ __forceinline__ TaskPtr task_ptr(const uint8_t* __restrict__ codes, c
   return t;
 }
 
+// A row base the wavefront holds in common, as a global-memory pointer: a
+// load then adds only a zero-extended 32-bit lane offset to the scalar base
+// (no 64-bit address arithmetic per lane).  The cast keeps all 64 bits.
+template <class T>
+using gptr = __attribute__((address_space(1))) const T*;
+template <class T>
+__device__ __forceinline__ gptr<T> uniform_ptr(const T* p) {
+  return (gptr<T>)p;
+}
+
 // Codes of a task's rows for the lane's chunk of step `it`.  The loads are
 // unconditional: a lane past the end of the slice reads the slice's last chunk
 // again (its contribution is dropped in the compute), and an FP8 slice that
@@ -107,16 +117,18 @@ __device__ __forceinline__ Frag<R> load_frag(const TaskPtr& t, int row_bytes, in
   int chunk = it * kWave + lane;
   chunk = chunk < nchunk ? chunk : nchunk - 1;
   const bool hi = W8 ? (chunk * 32 + 16 < kl) : true;
+  // a uniform row base plus a zero-extended 32-bit lane offset: the loads take
+  // the scalar-base form, with no 64-bit address arithmetic per lane
+  const uint32_t coff = (uint32_t)chunk * (uint32_t)kLaneBytes, goff = (uint32_t)chunk >> 1;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int rr = r < t.last ? r : t.last;
-    const u32x4* p = reinterpret_cast<const u32x4*>(t.codes + rr * row_bytes + chunk * kLaneBytes);
+    const gptr<u32x4> p = (gptr<u32x4>)(uniform_ptr(t.codes + (int64_t)rr * row_bytes) + coff);
     f.c[r][0] = p[0];
     f.c[r][1] = p[hi ? 1 : 0];
     if constexpr (!W8) {
-      const int gi = rr * groups + (chunk >> 1);
-      f.s[r] = t.scales[gi];
-      f.z[r] = t.zeros[gi];
+      f.s[r] = uniform_ptr(t.scales + (int64_t)rr * groups)[goff];
+      f.z[r] = uniform_ptr(t.zeros + (int64_t)rr * groups)[goff];
     } else {
       f.s[r] = 0u;
       f.z[r] = 0u;
@@ -584,12 +596,13 @@ __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restr
     int p = ps + 64 * s + lane;
     p = p < pe ? p : pe - 1;
     p = p > 0 ? p : 0;  // a run without pieces reads piece 0
-    const u32x4* cp = reinterpret_cast<const u32x4*>(bcodes + (int64_t)p * 32);
+    // a zero-extended 32-bit offset from the block base (p < 2^27): scalar-base loads
+    const u32x4* cp = reinterpret_cast<const u32x4*>(bcodes + (uint32_t)p * 32u);
     f.c[0] = cp[0];
     f.c[1] = cp[1];
     if constexpr (!W8) {
-      f.s = bscales[p >> 1];
-      f.z = bzeros[p >> 1];
+      f.s = bscales[(uint32_t)p >> 1];
+      f.z = bzeros[(uint32_t)p >> 1];
     } else {
       f.s = f.z = 0u;
     }
