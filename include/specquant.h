@@ -189,7 +189,7 @@ sq_status sq_verify_gemm_f16(const uint16_t* x, int64_t m, int64_t k, const uint
  * q_out [kd][b][v] f32, p_out [b][kd+1][v] f32: optional (nullable) copies of
  *   the distributions, T > 0 only.
  * Limits: 1 <= b < 2^24, 0 <= kd <= 64, 1 <= v <= 2^26,
- *   b * (2 kd + 1) * ceil(v / 4096) < 2^24; T finite and >= 0. */
+ *   b * (2 kd + 1) * ceil(v / 1024) < 2^24; T finite and >= 0. */
 sq_status sq_spec_accept(const float* draft_logits, const float* target_logits,
                          const int32_t* draft_tokens, const uint32_t* u24, int32_t b, int32_t kd,
                          int32_t v, float temperature, int32_t* n_accepted, int32_t* next_token,
@@ -202,11 +202,11 @@ sq_status sq_spec_accept(const float* draft_logits, const float* target_logits,
  * per-sequence state) is a static device array of SQ_NOALLOC_SCRATCH_BYTES
  * per GPU, held by the library until the process ends.  A call needs
  *   T > 0: 16 * (b * (2 kd + 1) * C) + 16 * (b * C) + 40 * b bytes,
- *   T = 0: 8 * (b * (kd + 1) * C) bytes, C = ceil(v / 4096),
+ *   T = 0: 8 * (b * (kd + 1) * C) bytes, C = ceil(v / 1024),
  * each term rounded up to a multiple of 256 (the 40 b term excepted); a call
  * that needs more than SQ_NOALLOC_SCRATCH_BYTES returns SQ_ERR_SHAPE and
- * enqueues nothing (e.g. 4 sequences, kd = 8, v = 151936 need 44 KB; 256
- * sequences at kd = 8 need 2.8 MB).  Every call on a GPU shares that GPU's
+ * enqueues nothing (e.g. 4 sequences, kd = 8, v = 151936 need 168 KB; 64
+ * sequences at kd = 8 need 2.7 MB).  Every call on a GPU shares that GPU's
  * array, and nothing in it needs to start at zero; calls that overlap on one
  * GPU (concurrently running streams) race on it, so order them on one
  * stream. */
@@ -416,7 +416,7 @@ sq_status sq_spec_commit(const int32_t* n_accepted, const int32_t* next_token, c
  *   (T > 0: any of its rows; T = 0: any target row) gets -1 in all three.
  * q_out [kd][b][c][v], p_out [b][c][kd+1][v]: optional fp32 copies, T > 0 only.
  * Limits: 1 <= b <= 65535, 1 <= c <= 64, 0 <= kd <= 64, 1 <= v <= 2^26,
- *   b c (2 kd + 1) ceil(v / 4096) < 2^24; T finite and >= 0.  Uses the library
+ *   b c (2 kd + 1) ceil(v / 1024) < 2^24; T finite and >= 0.  Uses the library
  *   workspace (row statistics, the fp32 rows unless q_out / p_out are given,
  *   and one int64 row per sequence). */
 sq_status sq_spec_accept_multi(const float* draft_logits, const float* target_logits, const int32_t* draft_tokens,

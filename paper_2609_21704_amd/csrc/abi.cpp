@@ -562,7 +562,7 @@ sq_status sq_spec_accept_multi(const float* draft_logits, const float* target_lo
   if (!target_logits || !n_accepted || !next_token || !chain) return SQ_ERR_NULL;
   if (kd > 0 && (!draft_logits || !draft_tokens)) return SQ_ERR_NULL;
   if (b < 1 || b > 65535 || c < 1 || c > 64 || kd < 0 || kd > 64 || v < 1 || v > (1 << 26)) return SQ_ERR_SHAPE;
-  const int64_t nchunk = (v + 4095) / 4096;
+  const int64_t nchunk = (v + sq::kAcceptChunk - 1) / sq::kAcceptChunk;
   if ((int64_t)b * c * (2 * kd + 1) * nchunk >= (int64_t(1) << 24)) return SQ_ERR_SHAPE;
   if (!isfinite(temperature)) return SQ_ERR_NONFINITE;
   if (temperature < 0.0f) return SQ_ERR_UNSUPPORTED;
@@ -643,7 +643,7 @@ sq_status validate_accept(const float* draft_logits, const float* target_logits,
   if (!target_logits || !n_accepted || !next_token) return SQ_ERR_NULL;
   if (kd > 0 && (!draft_logits || !draft_tokens)) return SQ_ERR_NULL;
   if (b < 1 || b >= (1 << 24) || kd < 0 || kd > 64 || v < 1 || v > (1 << 26)) return SQ_ERR_SHAPE;
-  const int64_t nchunk = (v + 4095) / 4096;
+  const int64_t nchunk = (v + sq::kAcceptChunk - 1) / sq::kAcceptChunk;
   // every kernel grid stays below 2^24 workgroups of 256 threads (2^32 work-items)
   if ((int64_t)b * (2 * kd + 1) * nchunk >= (int64_t(1) << 24)) return SQ_ERR_SHAPE;
   if (!isfinite(temperature)) return SQ_ERR_NONFINITE;

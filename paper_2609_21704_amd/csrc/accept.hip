@@ -34,7 +34,7 @@ namespace sq {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kChunk = 4096;
+constexpr int kChunk = kAcceptChunk;  // 1024: a 152k-token row spreads over 149 workgroups
 constexpr int kPer = kChunk / kThreads;  // logits per thread and chunk
 
 struct SeqInfo {
@@ -319,7 +319,7 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(const float* __restric
 
 // 3. per sequence: the draw.  The chunk holding t is found with a block scan
 // over the chunk totals (256 chunks at a time), then the chunk is scanned
-// with 16 consecutive logits per thread, so that the block's exclusive scan
+// with kPer consecutive logits per thread, so that the block's exclusive scan
 // of the thread sums orders them.  All sums are int64, so exact.
 __global__ __launch_bounds__(kThreads) void draw_kernel(const float* __restrict__ draft,
                                                         const float* __restrict__ target,

@@ -82,6 +82,10 @@ hipError_t launch_spec_accept(const float* draft, const float* target, const int
                               int b, int kd, int v, float temperature, int32_t* n_accepted, int32_t* next_token,
                               float* q_out, float* p_out, hipStream_t stream);
 
+// Logits per chunk of a vocabulary row in the accept kernels (the chunk
+// partials of the softmax statistics and of the draw weights).
+constexpr int kAcceptChunk = 1024;
+
 // Bytes of scratch one accept call needs (workspace or static array).
 size_t spec_accept_scratch_bytes(int b, int kd, int v, float temperature);
 

@@ -119,7 +119,7 @@ int main() {
                         at<int32_t>(FE), at<int32_t>(FE + 64), at<float>(FE + (1ull << 40)),
                         at<float>(FE + (2ull << 40)), s),
          SQ_OK);
-  EXPECT(sq_spec_accept_noalloc(at<float>(A), at<float>(B), at<int32_t>(C), at<uint32_t>(D), 400, 8, 151936, 1.0f,
+  EXPECT(sq_spec_accept_noalloc(at<float>(A), at<float>(B), at<int32_t>(C), at<uint32_t>(D), 100, 8, 151936, 1.0f,
                                 at<int32_t>(E), at<int32_t>(E + 4096), nullptr, nullptr, s),
          SQ_ERR_SHAPE);
   EXPECT(sq_spec_accept_noalloc(at<float>(A), at<float>(B), at<int32_t>(C), at<uint32_t>(D), 4, 8, 151936, 1.0f,

@@ -90,7 +90,7 @@ STUB(launch_kv_adopt, uint16_t*, uint16_t*, int, int, int, int, int64_t, const i
 STUB(launch_spec_commit_multi, const int32_t*, const int32_t*, const int32_t*, const int32_t*, int, int, int, int32_t*,
      int32_t*, int32_t*, int32_t*, int64_t, int32_t*, int32_t*, hipStream_t)
 size_t spec_accept_scratch_bytes(int b, int kd, int v, float) {
-  const size_t c = (size_t)(v + 4095) / 4096;
+  const size_t c = (size_t)(v + kAcceptChunk - 1) / kAcceptChunk;
   return 16 * (size_t)b * (2 * kd + 1) * c + 16 * (size_t)b * c + 40 * (size_t)b;
 }
 }  // namespace sq

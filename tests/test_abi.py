@@ -153,9 +153,9 @@ def test_accept_noalloc_validation():
              (A, B, C, D, 1, 4, 100, 1.0, E, E, None, None, None)]
     for c in cases:
         assert na(*c) == acc(*c) != OK
-    # 256 sequences at kd = 8 over 151936 logits need 2.8 MB: within the 4 MiB array (not launched here);
-    # 400 need 4.4 MB: rejected before any HIP call
-    assert na(A, B, C, D, 400, 8, 151936, 1.0, E, E + 4096, None, None, None) == SHAPE
+    # 64 sequences at kd = 8 over 151936 logits need 2.7 MB: within the 4 MiB array (not launched here);
+    # 100 need 4.3 MB: rejected before any HIP call
+    assert na(A, B, C, D, 100, 8, 151936, 1.0, E, E + 4096, None, None, None) == SHAPE
     assert na(None, B, None, D, 300000, 0, 1, 1.0, E, E + (1 << 21), None, None, None) == SHAPE   # 16.8 MB
 
 

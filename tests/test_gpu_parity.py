@@ -349,7 +349,7 @@ def test_spec_accept_zero_residual_falls_back_to_p_n():
 
 
 def test_spec_accept_masked_chunks():
-    """-inf logits over whole 4096-logit chunks and scattered tokens: masked
+    """-inf logits over whole chunks (1024 logits each) and scattered tokens: masked
     tokens get probability 0 and are never emitted; rows of masked chunks
     merge like the oracle's softmax."""
     b, kd, v = 6, 3, 20000

@@ -58,7 +58,7 @@ def test_noalloc_matches_spec_accept_two_calls_second_smaller(temp):
 
 def test_noalloc_plain_sampler_and_largest_within_the_array():
     _both(3, 0, 151936, 1.0, 13)                 # kd = 0: a draft-token draw
-    _both(256, 8, 151936, 1.0, 14)               # 2.8 MB of the 4 MiB array
+    _both(96, 8, 151936, 1.0, 14)                # 4.1 MB of the 4 MiB array (97 sequences at most)
     _both(1, 1, 5, 1.0, 15)
 
 
