@@ -116,18 +116,42 @@ __device__ int64_t block_exclusive_scan_i64(int64_t v, int64_t* sh, int64_t& tot
 }
 
 // One wavefront merges a row's chunk partials: L = max over chunks, S = the
-// sum of S_c exp(L_c - L), each lane taking every 64th chunk and the lanes
-// combined in a fixed shuffle tree.  A fully masked chunk (S_c = 0) adds
-// nothing; a chunk marked invalid (S_c NaN), or a row without any mass, gives
-// L = S = NaN.  Every lane returns the values.
-__device__ void wave_merge(const double2* st, int nchunk, double& L, double& S) {
+// sum of S_c exp(L_c - L), each lane taking every 64th chunk in increasing
+// order and the lanes combined in a fixed shuffle tree.  A fully masked chunk
+// (S_c = 0) adds nothing; a chunk marked invalid (S_c NaN), or a row without
+// any mass, gives L = S = NaN.  Every lane returns the values.
+//
+// The first kCells chunks of each lane are loaded ahead (load_cells: lane l
+// chunks l, l + 64, ..., a chunk past the row's end replaced by the row's
+// last one and ignored), so that a kernel can issue them beside its other
+// independent loads.  Rows of more than 64 kCells chunks take the rest from
+// memory (kWide); without kWide the code holds no loop over memory, so that
+// the compiler's load counters wait for exactly the loads a value needs.
+constexpr int kCells = 4;
+
+__device__ __forceinline__ void load_cells(const double2* st, int nchunk, double2 (&e)[kCells]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int i = 0; i < kCells; ++i) e[i] = st[min(lane + 64 * i, nchunk - 1)];
+}
+
+template <bool kWide>
+__device__ void merge_cells(const double2* st, int nchunk, const double2 (&e)[kCells], double& L, double& S) {
   const int lane = threadIdx.x & 63;
   double mx = -INFINITY;
   int bad = 0;
-  for (int c = lane; c < nchunk; c += 64) {
-    const double2 e = st[c];
-    bad |= isnan(e.y) ? 1 : 0;
-    if (e.y > 0.0) mx = fmax(mx, e.x);
+#pragma unroll
+  for (int i = 0; i < kCells; ++i) {
+    const bool in = lane + 64 * i < nchunk;
+    bad |= in && isnan(e[i].y) ? 1 : 0;
+    if (in && e[i].y > 0.0) mx = fmax(mx, e[i].x);
+  }
+  if constexpr (kWide) {
+    for (int c = lane + 64 * kCells; c < nchunk; c += 64) {
+      const double2 f = st[c];
+      bad |= isnan(f.y) ? 1 : 0;
+      if (f.y > 0.0) mx = fmax(mx, f.x);
+    }
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
@@ -135,9 +159,14 @@ __device__ void wave_merge(const double2* st, int nchunk, double& L, double& S) 
     bad |= __shfl_xor(bad, off, 64);
   }
   double s = 0.0;
-  for (int c = lane; c < nchunk; c += 64) {
-    const double2 e = st[c];
-    if (e.y > 0.0) s += e.y * exp(e.x - mx);
+#pragma unroll
+  for (int i = 0; i < kCells; ++i)
+    if (lane + 64 * i < nchunk && e[i].y > 0.0) s += e[i].y * exp(e[i].x - mx);
+  if constexpr (kWide) {
+    for (int c = lane + 64 * kCells; c < nchunk; c += 64) {
+      const double2 f = st[c];
+      if (f.y > 0.0) s += f.y * exp(f.x - mx);
+    }
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
@@ -147,6 +176,12 @@ __device__ void wave_merge(const double2* st, int nchunk, double& L, double& S) 
   }
   L = mx;
   S = s;
+}
+
+__device__ void wave_merge(const double2* st, int nchunk, double& L, double& S) {
+  double2 e[kCells];
+  load_cells(st, nchunk, e);
+  merge_cells<true>(st, nchunk, e, L, S);
 }
 
 // 1. per (row, chunk): (max z, sum exp(z - max z)).  blockIdx.x = row * nchunk + chunk.
@@ -214,42 +249,94 @@ __global__ __launch_bounds__(kThreads) void probs_kernel(const float* __restrict
 // p_n (the fallback when the residual mass is zero).  A sequence with a row
 // without a distribution gets n = -1 and zero weights.
 // blockIdx.x = s * nchunk + c.
+// Loads that wait for nothing computed here go out together, so that their
+// round trips overlap: the draft tokens and their uniforms, the first rows of
+// chunk partials, the logits at the tokens, and this chunk of p_0 and q_0
+// (the draw rows when the first draft token is rejected, or when kd = 0).
+// Every one of them is unconditional (indices clamped, the value ignored
+// where it does not apply).
+template <bool kWide>
 __global__ __launch_bounds__(kThreads) void decide_kernel(const float* __restrict__ draft,
                                                           const float* __restrict__ target,
                                                           const int32_t* __restrict__ tokens,
                                                           const uint32_t* __restrict__ u24, int b, int kd, int v,
                                                           float temp, int nchunk, const double2* __restrict__ stats,
                                                           int64_t* __restrict__ zs, SeqInfo* __restrict__ info) {
+  constexpr int kBatch = 3;  // rows of partials a wavefront holds at once
   __shared__ double sL[129], sS[129];
   __shared__ int sAcc[64];
   __shared__ int sN;
   __shared__ int64_t shi[4];
   const int s = blockIdx.x / nchunk;
   const int c = blockIdx.x % nchunk;
+  const int w = threadIdx.x >> 6;
+  const int nrows = 2 * kd + 1;
   const int64_t rows_t = (int64_t)b * (kd + 1);
-  // the 2kd + 1 rows' statistics, one wavefront per row
-  for (int rr = threadIdx.x >> 6; rr < 2 * kd + 1; rr += kThreads / 64) {
-    const int64_t row = rr <= kd ? (int64_t)s * (kd + 1) + rr : rows_t + (int64_t)(rr - kd - 1) * b + s;
-    double L, S;
-    wave_merge(stats + row * nchunk, nchunk, L, S);
-    if ((threadIdx.x & 63) == 0) {
-      sL[rr] = L;
-      sS[rr] = S;
+  const float* trow = target + (int64_t)s * (kd + 1) * v;  // p_0 of the sequence
+  // row rr of the sequence: target rows 0..kd, then draft rows 0..kd-1
+  auto row_of = [&](int rr) -> int64_t {
+    return rr <= kd ? (int64_t)s * (kd + 1) + rr : rows_t + (int64_t)(rr - kd - 1) * b + s;
+  };
+  // thread i < kd: draft position i; the other threads read position 0 (or,
+  // with kd = 0, the sequence's uniform) and ignore it
+  const bool dlane = (int)threadIdx.x < kd;
+  const int di = dlane ? (int)threadIdx.x : 0;
+  const int32_t* tp = kd > 0 ? tokens + (int64_t)di * b + s : (const int32_t*)(u24 + (int64_t)s * (kd + 1));
+  const int32_t xraw = *tp;
+  const uint32_t ut = u24[(int64_t)s * (kd + 1) + di];
+  // the 2kd + 1 rows' statistics, one wavefront per row, kBatch rows in flight
+  double2 e[kBatch][kCells];
+  auto load_batch = [&](int r0) {
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j)
+      load_cells(stats + row_of(min(r0 + 4 * j, nrows - 1)) * nchunk, nchunk, e[j]);
+  };
+  load_batch(w);
+  // this chunk of p_0 and q_0 (of p_0 twice when kd = 0), thread t holding
+  // logits t, t + 256, ...
+  float pv[kPer], qv[kPer];
+  const float* q0 = kd > 0 ? draft + (int64_t)s * v : trow;
+  auto load_chunk = [&](const float* row, float (&dst)[kPer]) {
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) dst[k] = row[min(c * kChunk + k * kThreads + (int)threadIdx.x, v - 1)];
+  };
+  load_chunk(trow, pv);
+  load_chunk(q0, qv);
+  const bool tok_ok = dlane && xraw >= 0 && xraw < v;
+  const int xi = tok_ok ? xraw : 0;
+  const float lpt = trow[(int64_t)di * v + xi];
+  const float lqt = kd > 0 ? draft[((int64_t)di * b + s) * v + xi] : trow[xi];
+  auto merge_batch = [&](int r0) {
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int rr = r0 + 4 * j;
+      if (rr < nrows) {
+        double L, S;
+        merge_cells<kWide>(stats + row_of(rr) * nchunk, nchunk, e[j], L, S);
+        if ((threadIdx.x & 63) == 0) {
+          sL[rr] = L;
+          sS[rr] = S;
+        }
+      }
     }
+  };
+  merge_batch(w);
+  for (int r0 = w + 4 * kBatch; r0 < nrows; r0 += 4 * kBatch) {  // kd >= 6
+    load_batch(r0);
+    merge_batch(r0);
   }
   __syncthreads();
   int invalid = 0;
-  for (int rr = threadIdx.x; rr < 2 * kd + 1; rr += kThreads) invalid |= isnan(sS[rr]) ? 1 : 0;
+  for (int rr = threadIdx.x; rr < nrows; rr += kThreads) invalid |= isnan(sS[rr]) ? 1 : 0;
   invalid = __syncthreads_or(invalid);
-  if ((int)threadIdx.x < kd && !invalid) {
+  if (dlane && !invalid) {
     const int i = threadIdx.x;
-    const int32_t xt = tokens[(int64_t)i * b + s];
     int acc = 0;
-    if (xt >= 0 && xt < v) {
+    if (tok_ok) {
       // fp32 probabilities; u (24 bits) times q (24 bits) is exact in fp64
-      const float p = prob32(target[((int64_t)s * (kd + 1) + i) * v + xt], temp, sL[i], sS[i]);
-      const float q = prob32(draft[((int64_t)i * b + s) * v + xt], temp, sL[kd + 1 + i], sS[kd + 1 + i]);
-      const double u = ldexp((double)(u24[(int64_t)s * (kd + 1) + i] & 0xFFFFFFu), -24);
+      const float p = prob32(lpt, temp, sL[i], sS[i]);
+      const float q = prob32(lqt, temp, sL[kd + 1 + i], sS[kd + 1 + i]);
+      const double u = ldexp((double)(ut & 0xFFFFFFu), -24);
       acc = (u * (double)q < (double)p) ? 1 : 0;
     }
     sAcc[i] = acc;
@@ -280,18 +367,21 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(const float* __restric
     }
     return;
   }
-  const float* lp = target + ((int64_t)s * (kd + 1) + n) * v;
   const double Lp = sL[n], Sp = sS[n];
   const bool resid = n < kd;
-  const float* lq = resid ? draft + ((int64_t)n * b + s) * v : nullptr;
   const double Lq = resid ? sL[kd + 1 + n] : 0.0, Sq = resid ? sS[kd + 1 + n] : 1.0;
+  if (n > 0) {  // uniform across the block; n = 0 uses the rows loaded ahead
+    load_chunk(trow + (int64_t)n * v, pv);
+    if (resid) load_chunk(draft + ((int64_t)n * b + s) * v, qv);
+  }
   int64_t z0 = 0, z1 = 0;
-  for (int e = 0; e < kPer; ++e) {
-    const int j = c * kChunk + e * kThreads + threadIdx.x;
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int j = c * kChunk + k * kThreads + threadIdx.x;
     if (j >= v) break;
-    const float p = prob32(lp[j], temp, Lp, Sp);
+    const float p = prob32(pv[k], temp, Lp, Sp);
     if (resid) {
-      const float q = prob32(lq[j], temp, Lq, Sq);
+      const float q = prob32(qv[k], temp, Lq, Sq);
       const double r = (double)p - (double)q;
       z0 += grid_weight(r > 0.0 ? r : 0.0);
       z1 += grid_weight((double)p);
@@ -320,7 +410,9 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(const float* __restric
 // 3. per sequence: the draw.  The chunk holding t is found with a block scan
 // over the chunk totals (256 chunks at a time), then the chunk is scanned
 // with kPer consecutive logits per thread, so that the block's exclusive scan
-// of the thread sums orders them.  All sums are int64, so exact.
+// of the thread sums orders them.  All sums are int64, so exact.  The
+// sequence's record, its uniform and the first 256 chunk totals are loaded
+// together at the start (none waits for another).
 __global__ __launch_bounds__(kThreads) void draw_kernel(const float* __restrict__ draft,
                                                         const float* __restrict__ target,
                                                         const uint32_t* __restrict__ u24, int b, int kd, int v,
@@ -332,26 +424,33 @@ __global__ __launch_bounds__(kThreads) void draw_kernel(const float* __restrict_
   __shared__ int sChunk;
   __shared__ int64_t shi[4];
   const int s = blockIdx.x;
+  const int64_t* z = zs + (int64_t)s * nchunk * 2;
   const SeqInfo si = info[s];
+  const uint32_t us = u24[(int64_t)s * (kd + 1) + kd];
+  // thread t holds chunk t's totals (a thread past the last chunk reads the
+  // last one and takes 0)
+  const int tc = min((int)threadIdx.x, nchunk - 1);
+  const int64_t ra = z[2 * tc], rb = z[2 * tc + 1];
+  const bool first = (int)threadIdx.x < nchunk;
+  const int64_t za = first ? ra : 0, zb = first ? rb : 0;
+
+  // the total mass Z of the draw row (the residual's, else p_n's when that is zero on the grid)
+  int64_t part = za;
+  for (int c = threadIdx.x + kThreads; c < nchunk; c += kThreads) part += z[2 * c];
+  int64_t Z = block_sum_i64(part, shi);
   const int n = si.n;
-  if (n < 0) {  // a row without a distribution
+  if (n < 0) {  // a row without a distribution (uniform across the block)
     if (threadIdx.x == 0) {
       n_accepted[s] = -1;
       next_token[s] = -1;
     }
     return;
   }
-  const int64_t* z = zs + (int64_t)s * nchunk * 2;
-
-  // the total mass Z of the draw row (the residual's, else p_n's when that is zero on the grid)
-  int64_t part = 0;
-  for (int c = threadIdx.x; c < nchunk; c += kThreads) part += z[2 * c];
-  int64_t Z = block_sum_i64(part, shi);
   int which = 0;
   if (Z == 0 && n < kd) {  // uniform across the block
     which = 1;
-    part = 0;
-    for (int c = threadIdx.x; c < nchunk; c += kThreads) part += z[2 * c + 1];
+    part = zb;
+    for (int c = threadIdx.x + kThreads; c < nchunk; c += kThreads) part += z[2 * c + 1];
     Z = block_sum_i64(part, shi);
   }
   if (Z == 0) {  // no mass on the fixed-point grid
@@ -361,7 +460,7 @@ __global__ __launch_bounds__(kThreads) void draw_kernel(const float* __restrict_
     }
     return;
   }
-  const uint64_t uu = u24[(int64_t)s * (kd + 1) + kd] & 0xFFFFFFu;
+  const uint64_t uu = us & 0xFFFFFFu;
   const uint64_t lo = uu * (uint64_t)Z;
   const uint64_t hi = __umul64hi(uu, (uint64_t)Z);
   const int64_t t = (int64_t)((hi << 40) | (lo >> 24));  // floor(u * Z / 2^24) < Z
@@ -371,7 +470,7 @@ __global__ __launch_bounds__(kThreads) void draw_kernel(const float* __restrict_
   int64_t run = 0;
   for (int c0 = 0; c0 < nchunk; c0 += kThreads) {
     const int c = c0 + (int)threadIdx.x;
-    const int64_t zc = c < nchunk ? z[2 * c + which] : 0;
+    const int64_t zc = c0 == 0 ? (which ? zb : za) : c < nchunk ? z[2 * c + which] : 0;
     int64_t tile;
     const int64_t pre = run + block_exclusive_scan_i64(zc, shi, tile);
     if (zc > 0 && pre <= t && t < pre + zc) {
@@ -397,14 +496,21 @@ __global__ __launch_bounds__(kThreads) void draw_kernel(const float* __restrict_
   int64_t R[kPer];
   int64_t local = 0;
   const int beg = chunk * kChunk + threadIdx.x * kPer;
+  float pv[kPer], qv[kPer];  // every load of the chunk in flight at once
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) {
+    const int j = beg + e;
+    pv[e] = j < v ? lp[j] : 0.0f;
+    qv[e] = resid && j < v ? lq[j] : 0.0f;
+  }
 #pragma unroll
   for (int e = 0; e < kPer; ++e) {
     const int j = beg + e;
     int64_t w = 0;
     if (j < v) {
-      const float p = prob32(lp[j], temp, si.lp, si.sp);
+      const float p = prob32(pv[e], temp, si.lp, si.sp);
       if (resid) {
-        const float q = prob32(lq[j], temp, si.lq, si.sq);
+        const float q = prob32(qv[e], temp, si.lq, si.sq);
         const double r = (double)p - (double)q;
         w = grid_weight(r > 0.0 ? r : 0.0);
       } else {
@@ -868,8 +974,12 @@ hipError_t enqueue_accept(const float* draft, const float* target, const int32_t
   if (p_out || q_out)
     hipLaunchKernelGGL(probs_kernel, dim3((unsigned)(rows * nchunk)), dim3(kThreads), 0, stream, draft, target, rows_t,
                        v, temperature, nchunk, stats, q_out, p_out);
-  hipLaunchKernelGGL(decide_kernel, dim3((unsigned)((int64_t)b * nchunk)), dim3(kThreads), 0, stream, draft, target,
-                     tokens, u24, b, kd, v, temperature, nchunk, stats, zs, info);
+  if (nchunk > 64 * kCells)
+    hipLaunchKernelGGL(decide_kernel<true>, dim3((unsigned)((int64_t)b * nchunk)), dim3(kThreads), 0, stream, draft,
+                       target, tokens, u24, b, kd, v, temperature, nchunk, stats, zs, info);
+  else
+    hipLaunchKernelGGL(decide_kernel<false>, dim3((unsigned)((int64_t)b * nchunk)), dim3(kThreads), 0, stream, draft,
+                       target, tokens, u24, b, kd, v, temperature, nchunk, stats, zs, info);
   hipLaunchKernelGGL(draw_kernel, dim3((unsigned)b), dim3(kThreads), 0, stream, draft, target, u24, b, kd, v,
                      temperature, nchunk, zs, info, n_accepted, next_token);
   return hipGetLastError();
