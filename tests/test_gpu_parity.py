@@ -302,6 +302,8 @@ def _run_accept(draft, target, tok, u24, temp, want_pq=False):
 ACCEPT_CASES = [
     (1, 4, 4096, 1.0), (1, 4, 151936, 1.0), (4, 8, 151936, 1.0), (3, 0, 1000, 1.0), (7, 3, 8, 0.7),
     (2, 64, 300, 1.0), (64, 2, 5000, 1.3), (16, 6, 152064, 1.0), (5, 1, 4097, 0.5),
+    # 256 chunk partials per row held in registers, then one more read from memory
+    (2, 3, 262144, 1.0), (2, 3, 262145, 1.0),
 ]
 
 
