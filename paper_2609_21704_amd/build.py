@@ -20,6 +20,8 @@ FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
     # never let the compiler form packed fp32 arithmetic
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # the first 14 kernel-argument dwords arrive in scalar registers at dispatch
+    "-mllvm", "-amdgpu-kernarg-preload-count=14",
     "-I", INCLUDE, "-I", CSRC,
 ]
 

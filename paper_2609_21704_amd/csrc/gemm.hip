@@ -166,12 +166,13 @@ enum : int { kOutF32 = 0, kOutF16 = 1, kOutAcc = 2 };
 
 template <int M, int NA, int NWV, int XB, int D, int KS, bool NRM>
 __global__ __launch_bounds__(1024) void gemm_rows_kernel(const uint16_t* __restrict__ x, int64_t k,
-                                                        const uint16_t* __restrict__ w, int64_t n,
-                                                        void* __restrict__ y, int out_mode, int64_t rows_q,
-                                                        int rows_rem, unsigned long long* __restrict__ slots,
+                                                        const uint16_t* __restrict__ w, int64_t rows_q,
+                                                        int rows_rem, int64_t n, void* __restrict__ y,
+                                                        int out_mode, unsigned long long* __restrict__ slots,
                                                         NormSrc nr) {
-  // every argument in one batch of scalar loads, before the first address needs one
-  asm volatile("" ::"s"(x), "s"(k), "s"(w), "s"(n), "s"(y), "s"(out_mode), "s"(rows_q), "s"(rows_rem), "s"(slots));
+  // The arguments the first loads need come first: the library is built with
+  // the first 14 argument dwords preloaded into scalar registers at dispatch.
+  asm volatile("" ::"s"(x), "s"(k), "s"(w), "s"(rows_q), "s"(rows_rem), "s"(n));
   extern __shared__ __align__(16) char smem[];
   constexpr int nwave = NWV, nthr = 64 * NWV;
   const int b = blockIdx.x;
@@ -496,14 +497,14 @@ hipError_t gemm_rows_m(const uint16_t* x, int64_t k, const uint16_t* w, int64_t 
     if constexpr (KS == 1 && XB <= 4) {
       if (nrm) {
         hipLaunchKernelGGL((gemm_rows_kernel<M, NA, nwave, XB, verify_rows_depth<KS>(), KS, true>),
-                           dim3((unsigned)blocks, (unsigned)KS), dim3(nthr), lds_launch, stream, x, k, w, n, y,
-                           out_mode, q, rem, slots, nr);
+                           dim3((unsigned)blocks, (unsigned)KS), dim3(nthr), lds_launch, stream, x, k, w, q, rem,
+                           n, y, out_mode, slots, nr);
         return;
       }
     }
     hipLaunchKernelGGL((gemm_rows_kernel<M, NA, nwave, XB, verify_rows_depth<KS>(), KS, false>),
-                       dim3((unsigned)blocks, (unsigned)KS), dim3(nthr), lds_launch, stream, x, k, w, n, y, out_mode,
-                       q, rem, slots, nr);
+                       dim3((unsigned)blocks, (unsigned)KS), dim3(nthr), lds_launch, stream, x, k, w, q, rem, n, y,
+                       out_mode, slots, nr);
   };
   using C1 = RowsIntC<1>;
   using C2 = RowsIntC<2>;

@@ -553,14 +553,16 @@ template <int M, bool W8, int D, int XB, int NA, int NWV, bool NRM>
 __global__ __launch_bounds__(1024) void gemv_rows_kernel(const uint16_t* __restrict__ x, int64_t k,
                                                         const uint8_t* __restrict__ codes,
                                                         const uint16_t* __restrict__ scales16,
-                                                        const uint16_t* __restrict__ zeros16,
-                                                        const float* __restrict__ scales32, int64_t n,
-                                                        void* __restrict__ y, int out_mode, int64_t rows_q,
-                                                        int rows_rem, NormSrc nr) {
+                                                        const uint16_t* __restrict__ zeros16, int64_t rows_q,
+                                                        int rows_rem, const float* __restrict__ scales32,
+                                                        int64_t n, void* __restrict__ y, int out_mode,
+                                                        NormSrc nr) {
   extern __shared__ __align__(16) char smem[];
-  // every argument in one batch of scalar loads, before the first address needs one
-  asm volatile("" ::"s"(x), "s"(k), "s"(codes), "s"(scales16), "s"(zeros16), "s"(scales32), "s"(n), "s"(y),
-               "s"(out_mode), "s"(rows_q), "s"(rows_rem));
+  // The arguments the first loads need come first: the library is built with
+  // the first 14 argument dwords preloaded into scalar registers at dispatch,
+  // so the activation and code loads issue without waiting for a kernel-
+  // argument load.
+  asm volatile("" ::"s"(x), "s"(k), "s"(codes), "s"(scales16), "s"(zeros16), "s"(rows_q), "s"(rows_rem));
   constexpr int kCPC = W8 ? 4 : 8;  // activation cells (8 halves) per chunk of a piece
   constexpr int kPad = kCPC + 1;    // LDS cells per chunk: the cells and one pad
   constexpr int nwave = NWV;        // wavefronts per workgroup, a power of two
@@ -931,7 +933,7 @@ hipError_t gemv_rows_m(const uint16_t* x, int64_t k, const uint8_t* codes, const
   auto go = [&](auto xb_tag, auto na_tag, auto nw_tag) {
     constexpr int XB = decltype(xb_tag)::value, NA = decltype(na_tag)::value, NWV = decltype(nw_tag)::value;
     hipLaunchKernelGGL((gemv_rows_kernel<M, W8, D, XB, NA, NWV, NRM>), dim3((unsigned)blocks), dim3(nthr),
-                       lds_launch, stream, x, k, codes, scales16, zeros16, scales32, n, y, out_mode, q, rem, nr);
+                       lds_launch, stream, x, k, codes, scales16, zeros16, q, rem, scales32, n, y, out_mode, nr);
   };
   // the fewest activation cells per thread that cover the activations: the
   // loads past the end are redundant and delay the code loads behind them
